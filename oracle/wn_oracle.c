@@ -1,0 +1,265 @@
+/*
+ * CPU oracle for autoregressive WaveNet sample generation (Deep Voice,
+ * arXiv 1702.07825).  TEST INFRASTRUCTURE ONLY: the GPU library never links,
+ * loads or calls this file; only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg do.
+ *
+ * Plain, slow, sequential C in double precision.  It follows the equations of
+ * the paper's Appendix A.1 ("Auto-regressive WaveNet") for one timestep, in the
+ * per-layer order the paper's CPU-implementation section lists (sample
+ * embedding, then per layer the two halves of the dilated convolution, the gated
+ * activation, the residual 1x1 and the skip accumulation, then the two output
+ * 1x1 convolutions and the softmax), and it keeps one history buffer per layer
+ * so that nothing is recomputed (Section 5, "Optimizing Inference").
+ *
+ * Readings of the paper taken here (each one is listed in the design doc):
+ *  - residual: x^(j) = x^(j-1) + W_res h^(j) + B_res (appendix equation; the CPU
+ *    section's x^(j) = W_res h^(j) + B_res is read as shorthand);
+ *  - input embedding: one table, x^(0)_t = E[y_{t-1}] + B_embed;
+ *  - every layer's history is zero before the first step (zero left padding);
+ *    y_{-1} = initial_sample;
+ *  - gate split: rows 0..r-1 of W_prev, W_cur, B and L feed tanh, rows r..2r-1
+ *    feed the sigmoid;
+ *  - skip: q^(0) = B_skip, q^(j) = q^(j-1) + W_skip^(j) h^(j), z_s = relu(q^(l));
+ *  - direct sampling: y = min{k : u < C_k} with C_k = p_0 + ... + p_k and
+ *    C_{a-1} taken as 1, i.e. y = #{k <= a-2 : C_k <= u}.  The decision is
+ *    taken in fp32 (the precision of the paper's inference kernels): C_k is
+ *    computed in double, rounded to float, and compared with the fp32 uniform.
+ *    The margin min_k |u - C_k| (double, k <= a-2) is reported so that callers
+ *    can tell which draws no rounding difference of a float implementation can
+ *    change.
+ *  - bf16 weight storage: every matrix (W_prev, W_cur, W_res, W_skip, W_relu,
+ *    W_out and the embedding table) is rounded to bfloat16 with round-to-
+ *    nearest-even and used as the exact value of that bfloat16; biases stay fp32.
+ *
+ * Layouts: every matrix is row-major [out][in]; conditioning is [T][l][2r].
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+typedef struct {
+    int n_layers, r, s, a;
+    const int *dilations;     /* [n_layers], each >= 1 */
+    int initial_sample;       /* y_{-1} */
+    int bf16_weights;         /* 0: use the fp32 weights; 1: round matrices to bf16 first */
+    const float *embed;       /* [a][r] */
+    const float *b_embed;     /* [r] */
+    const float *w_prev;      /* [l][2r][r] */
+    const float *w_cur;       /* [l][2r][r] */
+    const float *b_gate;      /* [l][2r] */
+    const float *w_res;       /* [l][r][r] */
+    const float *b_res;       /* [l][r] */
+    const float *w_skip;      /* [l][s][r] */
+    const float *b_skip;      /* [s] */
+    const float *w_relu;      /* [a][s] */
+    const float *b_relu;      /* [a] */
+    const float *w_out;       /* [a][a] */
+    const float *b_out;       /* [a] */
+} oracle_model;
+
+/* Generator state of one stream: per-layer histories and the last sample. */
+typedef struct {
+    long long t;              /* steps already taken */
+    int last_sample;          /* y_{t-1} */
+    double *hist;             /* sum(d) * r doubles, layer j at offset r * sum_{i<j} d_i */
+} oracle_state;
+
+/* Round an fp32 value to bfloat16 (round to nearest, ties to even) and return it as float. */
+static float round_bf16(float f) {
+    uint32_t u;
+    memcpy(&u, &f, 4);
+    if ((u & 0x7f800000u) == 0x7f800000u) { /* inf or nan: truncate, keep nan quiet */
+        if (u & 0x007fffffu) u |= 0x00400000u;
+        u &= 0xffff0000u;
+    } else {
+        uint32_t lsb = (u >> 16) & 1u;
+        u = (u + 0x7fffu + lsb) & 0xffff0000u;
+    }
+    float g;
+    memcpy(&g, &u, 4);
+    return g;
+}
+
+float oracle_round_bf16(float f) { return round_bf16(f); }
+
+static double wv(const oracle_model *m, const float *p, long idx) {
+    float f = p[idx];
+    if (m->bf16_weights) f = round_bf16(f);
+    return (double)f;
+}
+
+static double sigmoid(double v) { return 1.0 / (1.0 + exp(-v)); }
+
+long long oracle_history_len(const oracle_model *m) {
+    long long n = 0;
+    for (int j = 0; j < m->n_layers; ++j) n += m->dilations[j];
+    return n * m->r;
+}
+
+void oracle_reset(const oracle_model *m, oracle_state *st) {
+    st->t = 0;
+    st->last_sample = m->initial_sample;
+    memset(st->hist, 0, sizeof(double) * (size_t)oracle_history_len(m));
+}
+
+/*
+ * One timestep t of one stream: consumes y_{t-1} = st->last_sample and the
+ * conditioning of step t ([l][2r]), writes the a = 256 logits of step t and
+ * advances the histories.  Returns 0 or -1 on allocation failure.
+ */
+static int oracle_step(const oracle_model *m, oracle_state *st, const float *cond_t, double *logits) {
+    const int L = m->n_layers, r = m->r, s = m->s, a = m->a;
+    double *x = malloc(sizeof(double) * r), *xn = malloc(sizeof(double) * r);
+    double *act = malloc(sizeof(double) * 2 * r), *h = malloc(sizeof(double) * r);
+    double *q = malloc(sizeof(double) * s), *za = malloc(sizeof(double) * a);
+    if (!x || !xn || !act || !h || !q || !za) {
+        free(x); free(xn); free(act); free(h); free(q); free(za);
+        return -1;
+    }
+    /* Sample embedding: x^(0) = E[y_{t-1}] + B_embed. */
+    for (int c = 0; c < r; ++c)
+        x[c] = wv(m, m->embed, (long)st->last_sample * r + c) + (double)m->b_embed[c];
+    /* q^(0) = B_skip. */
+    for (int k = 0; k < s; ++k) q[k] = (double)m->b_skip[k];
+
+    long long hoff = 0;
+    for (int j = 0; j < L; ++j) {
+        const int d = m->dilations[j];
+        double *slot = st->hist + hoff + (st->t % d) * r;   /* holds x^(j-1)_{t-d} */
+        /* a = W_prev x_{t-d} + W_cur x_t + B + L  (the two halves of the width-2 dilated conv) */
+        for (int o = 0; o < 2 * r; ++o) {
+            double ap = 0.0, ac = 0.0;
+            for (int c = 0; c < r; ++c) {
+                ap += wv(m, m->w_prev, ((long)j * 2 * r + o) * r + c) * slot[c];
+                ac += wv(m, m->w_cur, ((long)j * 2 * r + o) * r + c) * x[c];
+            }
+            act[o] = ap + ac + (double)m->b_gate[(long)j * 2 * r + o] + (double)cond_t[(long)j * 2 * r + o];
+        }
+        /* gated activation: h = tanh(a[0:r]) * sigmoid(a[r:2r]) */
+        for (int c = 0; c < r; ++c) h[c] = tanh(act[c]) * sigmoid(act[r + c]);
+        /* history: x^(j-1)_t replaces x^(j-1)_{t-d} (it is read again at t+d) */
+        for (int c = 0; c < r; ++c) slot[c] = x[c];
+        /* skip contribution: q += W_skip^(j) h */
+        for (int k = 0; k < s; ++k) {
+            double acc = 0.0;
+            for (int c = 0; c < r; ++c) acc += wv(m, m->w_skip, ((long)j * s + k) * r + c) * h[c];
+            q[k] += acc;
+        }
+        /* residual: x^(j) = x^(j-1) + W_res h + B_res */
+        for (int o = 0; o < r; ++o) {
+            double acc = 0.0;
+            for (int c = 0; c < r; ++c) acc += wv(m, m->w_res, ((long)j * r + o) * r + c) * h[c];
+            xn[o] = x[o] + acc + (double)m->b_res[(long)j * r + o];
+        }
+        memcpy(x, xn, sizeof(double) * r);
+        hoff += (long long)d * r;
+    }
+    /* output: z_s = relu(q); z_a = relu(W_relu z_s + B_relu); logits = W_out z_a + B_out */
+    for (int k = 0; k < s; ++k) q[k] = q[k] > 0.0 ? q[k] : 0.0;
+    for (int i = 0; i < a; ++i) {
+        double acc = 0.0;
+        for (int k = 0; k < s; ++k) acc += wv(m, m->w_relu, (long)i * s + k) * q[k];
+        acc += (double)m->b_relu[i];
+        za[i] = acc > 0.0 ? acc : 0.0;
+    }
+    for (int i = 0; i < a; ++i) {
+        double acc = 0.0;
+        for (int k = 0; k < a; ++k) acc += wv(m, m->w_out, (long)i * a + k) * za[k];
+        logits[i] = acc + (double)m->b_out[i];
+    }
+    free(x); free(xn); free(act); free(h); free(q); free(za);
+    st->t += 1;
+    return 0;
+}
+
+/*
+ * Direct sampling from softmax(logits) with the uniform u (Appendix A,
+ * "Sampling from Output Distribution": direct sampling; the softmax is the
+ * max-subtracted form of the performance-model appendix).  Writes the
+ * probabilities if prob != NULL and the margin if margin != NULL.
+ */
+int oracle_draw(int a, const double *logits, float u, double *prob, double *margin) {
+    double mx = logits[0];
+    for (int i = 1; i < a; ++i) if (logits[i] > mx) mx = logits[i];
+    double z = 0.0;
+    for (int i = 0; i < a; ++i) z += exp(logits[i] - mx);
+    double cdf = 0.0, best = 1e300;
+    int y = 0;
+    for (int k = 0; k < a; ++k) {
+        double p = exp(logits[k] - mx) / z;
+        if (prob) prob[k] = p;
+        cdf += p;
+        if (k <= a - 2) {
+            if ((float)cdf <= u) y += 1;
+            double gap = fabs((double)u - cdf);
+            if (gap < best) best = gap;
+        }
+    }
+    if (margin) *margin = best;
+    return y;
+}
+
+/*
+ * Run T steps of one stream.
+ *   mode 0 (generate): y_{t} is drawn from step t's distribution with u[t] and
+ *                      fed back; samples_out[t] receives it.
+ *   mode 1 (teacher forcing): step t consumes y_in[t-1] (y_in[-1] is the state's
+ *                      last sample); samples_out, if given, receives the draw that
+ *                      u[t] would make from step t's distribution.
+ * logits_out [T][a] (double), margin_out [T] may be NULL.  u may be NULL in mode 1.
+ * If st is NULL a fresh zero state is used.  Returns 0, -1 (bad arguments) or
+ * -2 (allocation failure).
+ */
+int oracle_run(const oracle_model *m, oracle_state *st, int mode, long long T,
+               const float *cond, const float *u, const int *y_in,
+               int *samples_out, double *logits_out, double *margin_out) {
+    if (!m || T < 0 || (mode != 0 && mode != 1)) return -1;
+    if (mode == 0 && !u) return -1;
+    if (mode == 1 && !y_in) return -1;
+    oracle_state local;
+    double *own = NULL;
+    if (!st) {
+        own = malloc(sizeof(double) * (size_t)(oracle_history_len(m) > 0 ? oracle_history_len(m) : 1));
+        if (!own) return -2;
+        local.hist = own;
+        oracle_reset(m, &local);
+        st = &local;
+    }
+    double *lg = malloc(sizeof(double) * m->a);
+    if (!lg) { free(own); return -2; }
+    const long long per_step = (long long)m->n_layers * 2 * m->r;
+    for (long long t = 0; t < T; ++t) {
+        if (oracle_step(m, st, cond + t * per_step, lg) != 0) { free(lg); free(own); return -2; }
+        if (logits_out) memcpy(logits_out + t * m->a, lg, sizeof(double) * m->a);
+        int y = 0;
+        double mg = 0.0;
+        if (u) y = oracle_draw(m->a, lg, u[t], NULL, &mg);
+        if (margin_out) margin_out[t] = u ? mg : 0.0;
+        if (samples_out) samples_out[t] = y;
+        st->last_sample = (mode == 0) ? y : y_in[t];
+    }
+    free(lg);
+    free(own);
+    return 0;
+}
+
+/* Number of parameters of the layout above (the paper's model-size estimate). */
+long long oracle_param_count(int n_layers, int r, int s, int a) {
+    long long L = n_layers;
+    long long per_layer = 2LL * (2 * r) * r + 2 * r + (long long)r * r + r + (long long)s * r;
+    return (long long)a * r + r + L * per_layer + s + (long long)a * s + a + (long long)a * a + a;
+}
+
+/* FLOPs per generated sample, the performance-model appendix's final equation. */
+double oracle_flops_per_sample(int n_layers, int r, int s, int a, double f_div, double f_exp) {
+    double L = n_layers, R = r, S = s, A = a;
+    return L * (10.0 * R * R + 11.0 * R + 2.0 * R * (f_div + f_exp)) + S * (2.0 * R * L + 2.0) +
+           A * (2.0 * S + 2.0 * A + 3.0) + A * (3.0 + f_div + f_exp);
+}
+
+/* Vector form of the bf16 rounding above. */
+void oracle_round_bf16_array(const float *in, float *out, long long n) {
+    for (long long i = 0; i < n; ++i) out[i] = round_bf16(in[i]);
+}

@@ -1,0 +1,260 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Every test here runs on the CPU.  Each one checks the oracle against an
+independent computation or an exact property, so that a plausible mistake in it
+(a dropped bias, a wrong sign, a history slot off by one, swapped gate halves,
+a transposed matrix) fails at least one of them.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests import brute_force
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _model(L, r, s, dil, a=256, seed=0, bias=0.5, wscale=1.0, init=128, bf16=False):
+    w = synth.make_weights(L, r, s, a, seed=seed, bias_scale=bias, weight_scale=wscale)
+    return w, oracle.Model(w, dil, initial_sample=init, bf16_weights=bf16)
+
+
+def _cond(L, r, T, seed):
+    return synth.make_cond(L, r, 1, T, seed=seed)[0].numpy()
+
+
+CASES = [
+    # (L, r, s, a, dilations, T)
+    (4, 16, 32, 256, (1, 2, 4, 8), 70),
+    (3, 8, 12, 7, (3, 1, 2), 40),
+    (5, 4, 6, 256, (2, 2, 1, 5, 3), 50),
+    (1, 2, 3, 5, (1,), 12),
+]
+
+
+@pytest.mark.parametrize("L,r,s,a,dil,T", CASES)
+def test_incremental_equals_whole_sequence_conv(L, r, s, a, dil, T):
+    """History-buffer generation == the full causal dilated convolution (appendix A.1 equations)."""
+    w, m = _model(L, r, s, dil, a=a, seed=L * 7 + r, bias=0.5, init=a // 2)
+    cond = _cond(L, r, T, seed=11)
+    y = synth.make_samples(1, T, a=a, seed=5)[0]
+    _, lg, _ = oracle.run(m, cond, y_in=y)
+    ref = brute_force.logits(w, dil, cond, y, initial_sample=a // 2)
+    np.testing.assert_allclose(lg, ref, rtol=0, atol=1e-10)
+    assert np.abs(lg).max() > 1e-2  # not a degenerate all-zero case
+
+
+def test_no_recurrence_special_case_is_a_dense_mlp():
+    """With W_prev = W_cur = 0 each step's logits are a pure function of that step's conditioning."""
+    L, r, s, a, dil, T = 3, 8, 16, 256, (1, 2, 4), 30
+    w = synth.make_weights(L, r, s, a, seed=3, bias_scale=0.7)
+    w["w_prev"][:] = 0
+    w["w_cur"][:] = 0
+    m = oracle.Model(w, dil)
+    cond = _cond(L, r, T, seed=4).astype(np.float64)
+    y = synth.make_samples(1, T, seed=9)[0]
+    _, lg, _ = oracle.run(m, cond.astype(np.float32), y_in=y)
+    pre = cond + w["b_gate"][None].astype(np.float64)               # [T, L, 2r]
+    hid = np.tanh(pre[:, :, :r]) / (1.0 + np.exp(-pre[:, :, r:]))     # [T, L, r]
+    q = hid.reshape(T, L * r) @ np.concatenate(list(w["w_skip"]), axis=1).T.astype(np.float64) + w["b_skip"]
+    za = np.maximum(np.maximum(q, 0) @ w["w_relu"].T.astype(np.float64) + w["b_relu"], 0)
+    ref = za @ w["w_out"].T.astype(np.float64) + w["b_out"]
+    np.testing.assert_allclose(lg, ref, rtol=0, atol=1e-11)
+
+
+def test_head_and_sampler_special_case():
+    """W_out = 0, B_out = log(q): p equals q and the draw is the textbook inverse CDF (searchsorted)."""
+    rng = np.random.default_rng(0)
+    L, r, s, a, dil, T = 2, 4, 8, 256, (1, 2), 400
+    w = synth.make_weights(L, r, s, a, seed=1, bias_scale=0.3)
+    qv = rng.dirichlet(np.full(a, 0.7))
+    qv = np.maximum(qv, 1e-12)
+    qv /= qv.sum()
+    w["w_out"][:] = 0
+    w["b_out"] = np.log(qv).astype(np.float32)
+    m = oracle.Model(w, dil)
+    cond = _cond(L, r, T, seed=2)
+    u = synth.make_uniforms(1, T, seed=3)[0]
+    ys, lg, mg = oracle.run(m, cond, u=u)
+    np.testing.assert_array_equal(lg, np.repeat(w["b_out"][None].astype(np.float64), T, 0))
+    pf = np.exp(w["b_out"].astype(np.float64))
+    pf /= pf.sum()
+    _, p, _ = oracle.draw(lg[0], 0.5)
+    np.testing.assert_allclose(p, pf, rtol=1e-12, atol=0)
+    cdf = np.cumsum(pf)
+    ref = np.minimum(np.searchsorted(cdf.astype(np.float32), u, side="right"), a - 1)
+    np.testing.assert_array_equal(ys, ref)
+    ref_margin = np.abs(u[:, None].astype(np.float64) - cdf[None, : a - 1]).min(axis=1)
+    np.testing.assert_allclose(mg, ref_margin, rtol=0, atol=1e-15)
+
+
+def test_draw_edge_cases():
+    a = 256
+    lg = np.zeros(a)
+    assert oracle.draw(lg, 0.0)[0] == 0
+    assert oracle.draw(lg, np.nextafter(np.float32(1), np.float32(0)))[0] == a - 1
+    # uniform p: C_k = (k+1)/256 exactly; u = C_k goes up (strict <): y = k + 1
+    assert oracle.draw(lg, 10 / 256)[0] == 10
+    assert oracle.draw(lg, np.nextafter(np.float32(10 / 256), np.float32(0)))[0] == 9
+    # all mass on one class
+    spike = np.full(a, -1e4)
+    spike[77] = 0
+    for u in (0.0, 0.3, 0.999):
+        assert oracle.draw(spike, u)[0] == 77
+    # monotone in u
+    rng = np.random.default_rng(1)
+    lg = rng.standard_normal(a)
+    ys = [oracle.draw(lg, u)[0] for u in np.linspace(0, 0.9999, 500)]
+    assert all(b >= a_ for a_, b in zip(ys, ys[1:]))
+
+
+def _changed_steps(ref, lg):
+    return set(np.nonzero(np.any(ref != lg, axis=1))[0].tolist())
+
+
+def _subset_sums(ds):
+    sums = {0}
+    for d in ds:
+        sums |= {x + d for x in sums}
+    return sums
+
+
+@pytest.mark.parametrize("dil", [(1, 2, 4, 8), (3, 1, 2), (2, 5)])
+def test_receptive_field_and_causality(dil):
+    """Step t sees exactly y_{t-1-o}, o in the subset sums of the dilations (so R = 1 + sum d for 1,2,4,...)."""
+    L, r, s = len(dil), 6, 8
+    T = 3 * (1 + sum(dil)) + 10
+    w, m = _model(L, r, s, dil, seed=21, bias=0.4)
+    cond = _cond(L, r, T, seed=22)
+    y = synth.make_samples(1, T, seed=23)[0]
+    _, ref, _ = oracle.run(m, cond, y_in=y)
+    k = T // 3
+    y2 = y.copy()
+    y2[k] = (y2[k] + 101) % 256
+    _, lg, _ = oracle.run(m, cond, y_in=y2)
+    expect = {k + 1 + o for o in _subset_sums(dil)} & set(range(T))
+    assert _changed_steps(ref, lg) == expect
+    if dil == (1, 2, 4, 8):
+        assert max(expect) - k == oracle.receptive_field(dil) == 16
+        assert expect == set(range(k + 1, k + 17))
+    # conditioning of layer j at step k reaches steps k + (subset sums of the later dilations)
+    for j in range(L):
+        c2 = cond.copy()
+        c2[k, j, :] += 0.5
+        _, lg, _ = oracle.run(m, c2, y_in=y)
+        assert _changed_steps(ref, lg) == {k + o for o in _subset_sums(dil[j + 1:])}
+
+
+def test_receptive_field_paper_figures():
+    g = json.load(open(os.path.join(GOLDEN, "paper_figures.json")))
+    r40 = oracle.receptive_field(synth.dilation_cycle(40))
+    r20 = oracle.receptive_field(synth.dilation_cycle(20))
+    assert (r40, r20) == (4093, 2047)
+    assert abs(r20 / r40 - g["receptive_field_ratio_20_vs_40_layers"]["value"]) < 1e-3
+    # 40 layers at 48 kHz: the paper says 83 ms; the 2^(i mod 10) schedule gives 85.3 ms
+    assert abs(r40 / 48000 - g["receptive_field_40_layers_at_48khz_s"]["value"]) / 0.083 < 0.03
+
+
+def test_chunked_equals_one_shot():
+    L, r, s, dil, T = 4, 16, 32, (1, 2, 4, 8), 200
+    w, m = _model(L, r, s, dil, seed=31, bias=0.2)
+    cond = _cond(L, r, T, seed=32)
+    u = synth.make_uniforms(1, T, seed=33)[0]
+    y1, lg1, _ = oracle.run(m, cond, u=u)
+    st = oracle.State(m)
+    parts = []
+    for a_, b_ in [(0, 1), (1, 17), (17, 17), (17, 100), (100, 200)]:
+        ys, lg, _ = oracle.run(m, cond[a_:b_], u=u[a_:b_], state=st)
+        parts.append((ys, lg))
+    assert st.t == T and st.last_sample == y1[-1]
+    np.testing.assert_array_equal(np.concatenate([p[0] for p in parts]), y1)
+    np.testing.assert_array_equal(np.concatenate([p[1] for p in parts]), lg1)
+
+
+def test_generate_equals_teacher_forcing_on_its_own_samples():
+    L, r, s, dil, T = 4, 16, 32, (1, 2, 4, 8), 150
+    w, m = _model(L, r, s, dil, seed=41)
+    cond = _cond(L, r, T, seed=42)
+    u = synth.make_uniforms(1, T, seed=43)[0]
+    y, lg, mg = oracle.run(m, cond, u=u)
+    y2, lg2, mg2 = oracle.run(m, cond, u=u, y_in=y)
+    np.testing.assert_array_equal(lg, lg2)
+    np.testing.assert_array_equal(y, y2)
+    np.testing.assert_array_equal(mg, mg2)
+
+
+def test_bf16_weights_round_to_nearest_even():
+    """The oracle's bf16 storage mode == the fp32 oracle on weights rounded by torch's bfloat16 cast."""
+    L, r, s, dil, T = 3, 16, 32, (1, 2, 4), 40
+    w = synth.make_weights(L, r, s, seed=51, bias_scale=0.3)
+    mats = ("embed", "w_prev", "w_cur", "w_res", "w_skip", "w_relu", "w_out")
+    wr = {k: (torch.tensor(v).to(torch.bfloat16).to(torch.float32).numpy() if k in mats else v)
+          for k, v in w.items()}
+    for k in mats:
+        np.testing.assert_array_equal(oracle.round_bf16(w[k]), wr[k])
+    edge = np.array([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -(1.0 + 2 ** -8), 3.0e38, np.inf, -0.0], np.float32)
+    np.testing.assert_array_equal(oracle.round_bf16(edge),
+                                  torch.tensor(edge).to(torch.bfloat16).to(torch.float32).numpy())
+    cond = _cond(L, r, T, seed=52)
+    y = synth.make_samples(1, T, seed=53)[0]
+    _, lg_b, _ = oracle.run(oracle.Model(w, dil, bf16_weights=True), cond, y_in=y)
+    _, lg_r, _ = oracle.run(oracle.Model(wr, dil), cond, y_in=y)
+    np.testing.assert_array_equal(lg_b, lg_r)
+    _, lg_f, _ = oracle.run(oracle.Model(w, dil), cond, y_in=y)
+    assert 1e-5 < np.abs(lg_b - lg_f).max() < 5e-2
+
+
+def test_model_size_and_flops_match_the_paper():
+    g = json.load(open(os.path.join(GOLDEN, "paper_figures.json")))
+    n = oracle.param_count(40, 64, 256)
+    shapes = synth.weight_shapes(40, 64, 256, 256)
+    assert n == sum(int(np.prod(s)) for s in shapes.values()) == 1630528
+    assert abs(n - g["parameters"]["value"]) / g["parameters"]["value"] < 0.05
+    assert abs(4 * n - g["parameters"]["bytes_fp32"]) / g["parameters"]["bytes_fp32"] < 0.05
+    bw = 4 * n * g["weight_bandwidth_per_second"]["rate_hz"]
+    assert abs(bw - g["weight_bandwidth_per_second"]["value"]) / g["weight_bandwidth_per_second"]["value"] < 0.10
+    f = oracle.flops_per_sample(40, 64, 256, 256, 10, 10) * 16384
+    assert abs(f - g["flops_per_audio_second"]["value"]) / g["flops_per_audio_second"]["value"] < 0.01
+    # per layer: 10 r^2 + 11 r (the r-only terms of the layer cost)
+    per_layer = oracle.flops_per_sample(2, 64, 0, 0, 0, 0) - oracle.flops_per_sample(1, 64, 0, 0, 0, 0)
+    assert per_layer == 10 * 64 ** 2 + 11 * 64
+    assert abs(per_layer - g["flops_per_layer"]["value"]) / g["flops_per_layer"]["value"] < 0.02
+    # 60 us per sample at 16 kHz and 1.5 us per layer for 40 layers
+    assert abs(1e6 / 16384 - g["per_sample_budget_us_16khz"]["value"]) < 2
+    assert abs(1e6 / 16384 / 40 - g["per_layer_budget_us_40_layers"]["value"]) < 0.1
+
+
+def test_mulaw_round_trip_and_closed_form():
+    mu = oracle.mulaw
+    codes = np.arange(256)
+    np.testing.assert_array_equal(mu.encode(mu.decode(codes)), codes)
+    assert mu.encode(0.0) == 128 and mu.encode(1.0) == 255 and mu.encode(-1.0) == 0
+    np.testing.assert_allclose(mu.decode(255 - codes), -mu.decode(codes), atol=1e-15)
+    x = np.linspace(-1, 1, 20001)
+    np.testing.assert_allclose(mu.expand(mu.compress(x)), x, atol=1e-12)
+    e = mu.encode(x)
+    assert np.all(np.diff(e) >= 0)
+    # companding: steps near 0 are about (1 + mu) / ln(1 + mu) * ... finer than near full scale
+    dec = mu.decode(codes)
+    step0, step1 = dec[129] - dec[128], dec[255] - dec[254]
+    assert step1 / step0 > 100
+    # the transform's endpoints and odd symmetry
+    assert mu.compress(1.0) == pytest.approx(1.0, abs=1e-15)
+    np.testing.assert_allclose(mu.compress(-x), -mu.compress(x), atol=1e-15)
+
+
+def test_history_is_zero_padded_before_the_first_step():
+    """At t = 0 every layer's past input is zero: the W_prev halves contribute nothing."""
+    L, r, s, dil = 3, 8, 16, (1, 2, 4)
+    w, m = _model(L, r, s, dil, seed=61, bias=0.3)
+    cond = _cond(L, r, 1, seed=62)
+    _, lg, _ = oracle.run(m, cond, y_in=np.array([5], np.int32))
+    w2 = {k: v.copy() for k, v in w.items()}
+    w2["w_prev"][:] = 123.0
+    _, lg2, _ = oracle.run(oracle.Model(w2, dil), cond, y_in=np.array([5], np.int32))
+    np.testing.assert_array_equal(lg, lg2)
