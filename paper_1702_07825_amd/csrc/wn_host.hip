@@ -1,0 +1,293 @@
+// Host side of the libwn C ABI: argument checks, weight packing, workspace
+// layout and kernel selection.  Declarations and contracts are in include/wn.h.
+#include "wn.h"
+#include "wn_internal.h"
+
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+struct wn_handle {
+  int device = 0;
+  int L = 0, R = 0, S = 0, A = 0;
+  int init_sample = 128;
+  int dtype = WN_F32;
+  std::vector<int> dil;
+  void* dmem = nullptr;
+  WnDims dims{};
+  WnDevWeights w{};
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  g_err = std::string(what) + ": " + hipGetErrorString(e);
+  return WN_EHIP;
+}
+
+// Round fp32 to bfloat16, nearest even (NaN stays NaN).
+uint16_t to_bf16(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  if ((u & 0x7f800000u) == 0x7f800000u) {
+    if (u & 0x007fffffu) u |= 0x00400000u;
+    return (uint16_t)(u >> 16);
+  }
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+class DeviceScope {
+ public:
+  explicit DeviceScope(int dev) {
+    ok_ = hipGetDevice(&prev_) == hipSuccess;
+    if (ok_ && prev_ != dev) ok_ = hipSetDevice(dev) == hipSuccess;
+  }
+  ~DeviceScope() {
+    int cur = -1;
+    if (hipGetDevice(&cur) == hipSuccess && cur != prev_) (void)hipSetDevice(prev_);
+  }
+  bool ok() const { return ok_; }
+
+ private:
+  int prev_ = 0;
+  bool ok_ = false;
+};
+
+struct WsLayout {
+  size_t status_off, state_off, hist_off, total;
+};
+
+WsLayout ws_layout(const wn_handle* h, int B) {
+  WsLayout l;
+  l.status_off = 0;
+  l.state_off = 256;
+  l.hist_off = align_up(l.state_off + (size_t)B * 2 * sizeof(int64_t), 256);
+  l.total = align_up(l.hist_off + (size_t)B * h->dims.hist_len * sizeof(float), 256);
+  return l;
+}
+
+int check_call(wn_handle* h, int B, int T, const void* cond, const void* a1, const void* a2, void* ws,
+               size_t ws_bytes, int reset) {
+  if (!h) return fail(WN_EINVAL, "null handle");
+  if (B < 1) return fail(WN_EINVAL, "B must be >= 1");
+  if (T < 0) return fail(WN_EINVAL, "T must be >= 0");
+  if (reset != 0 && reset != 1) return fail(WN_EINVAL, "reset must be 0 or 1");
+  if (T == 0) return WN_OK;
+  if (!cond || !a1 || !a2) return fail(WN_EINVAL, "null input or output pointer");
+  if (!ws) return fail(WN_EINVAL, "null workspace");
+  if (reinterpret_cast<uintptr_t>(ws) % 256 != 0) return fail(WN_EINVAL, "workspace must be 256-byte aligned");
+  if (ws_bytes < ws_layout(h, B).total) return fail(WN_EINVAL, "workspace too small");
+  if ((size_t)B * (size_t)T > (size_t)1 << 40) return fail(WN_EINVAL, "B*T too large");
+  return WN_OK;
+}
+
+int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const int32_t* y_in, int32_t* y_out,
+           float* logits, void* ws, int reset, void* stream, bool teacher) {
+  DeviceScope scope(h->device);
+  if (!scope.ok()) return fail(WN_EHIP, "cannot select the handle's device");
+  const WsLayout l = ws_layout(h, B);
+  char* base = static_cast<char*>(ws);
+  WnStreamArgs args{};
+  args.d = h->dims;
+  args.w = h->w;
+  args.io.cond = cond;
+  args.io.u = u;
+  args.io.y_in = y_in;
+  args.io.y_out = y_out;
+  args.io.logits = logits;
+  args.io.B = B;
+  args.io.T = T;
+  args.io.reset = reset;
+  args.io.init_sample = h->init_sample;
+  args.ws.status = reinterpret_cast<int32_t*>(base + l.status_off);
+  args.ws.state = reinterpret_cast<int64_t*>(base + l.state_off);
+  args.ws.hist = reinterpret_cast<float*>(base + l.hist_off);
+  const hipError_t e = wn_stream_launch(args, teacher, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  return WN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
+  g_err.clear();
+  if (!c || !w || !out) return fail(WN_EINVAL, "null argument");
+  if (c->n_layers < 1 || c->n_layers > WN_MAX_LAYERS) return fail(WN_EINVAL, "n_layers must be 1..64");
+  if (!c->dilations) return fail(WN_EINVAL, "null dilations");
+  if (c->r < 1 || c->s < 1 || c->a < 1) return fail(WN_EINVAL, "r, s, a must be >= 1");
+  if (c->weight_dtype != WN_F32 && c->weight_dtype != WN_BF16) return fail(WN_EINVAL, "unknown weight_dtype");
+  if (c->initial_sample < 0 || c->initial_sample >= c->a) return fail(WN_EINVAL, "initial_sample out of range");
+  if (c->embed_taps < 1 || c->embed_taps > 2) return fail(WN_EINVAL, "embed_taps must be 1 or 2");
+  long long hist_steps = 0;
+  for (int j = 0; j < c->n_layers; ++j) {
+    if (c->dilations[j] < 1 || c->dilations[j] > 65536) return fail(WN_EINVAL, "dilations must be 1..65536");
+    hist_steps += c->dilations[j];
+  }
+  const void* need[] = {w->embed, w->b_embed, w->w_prev, w->w_cur, w->b_gate, w->w_res, w->b_res,
+                        w->w_skip, w->b_skip, w->w_relu, w->b_relu, w->w_out, w->b_out};
+  for (const void* p : need)
+    if (!p) return fail(WN_EINVAL, "null weight array");
+  if (c->a != WN_A) return fail(WN_EUNSUPPORTED, "a must be 256");
+  if (c->embed_taps != 1) return fail(WN_EUNSUPPORTED, "only embed_taps = 1 is implemented");
+  if (!wn_stream_supported(c->r, c->s)) return fail(WN_EUNSUPPORTED, "unsupported (r, s) pair");
+
+  wn_handle* h = new (std::nothrow) wn_handle();
+  if (!h) return fail(WN_ENOMEM, "host allocation");
+  h->L = c->n_layers;
+  h->R = c->r;
+  h->S = c->s;
+  h->A = c->a;
+  h->init_sample = c->initial_sample;
+  h->dtype = c->weight_dtype;
+  h->dil.assign(c->dilations, c->dilations + c->n_layers);
+  if (hipGetDevice(&h->device) != hipSuccess) {
+    delete h;
+    return fail(WN_EHIP, "hipGetDevice failed");
+  }
+  const int L = h->L, R = h->R, S = h->S, A = h->A;
+  h->dims.L = L;
+  h->dims.R = R;
+  h->dims.S = S;
+  h->dims.hist_len = (int)(hist_steps * R);
+  {
+    int off = 0;
+    for (int j = 0; j < L; ++j) {
+      h->dims.dil[j] = h->dil[j];
+      h->dims.hoff[j] = off;
+      off += h->dil[j] * R;
+    }
+  }
+
+  // Pack every array into one device allocation, each 256-byte aligned.
+  const bool bf = (h->dtype == WN_BF16);
+  const size_t we = bf ? 2 : 4;
+  struct Arr { const float* src; size_t n; bool matrix; size_t off; };
+  Arr arrs[] = {
+      {w->embed, (size_t)A * R, true, 0},          {w->w_prev, (size_t)L * 2 * R * R, true, 0},
+      {w->w_cur, (size_t)L * 2 * R * R, true, 0},  {w->w_res, (size_t)L * R * R, true, 0},
+      {w->w_skip, (size_t)L * S * R, true, 0},     {w->w_relu, (size_t)A * S, true, 0},
+      {w->w_out, (size_t)A * A, true, 0},          {w->b_embed, (size_t)R, false, 0},
+      {w->b_gate, (size_t)L * 2 * R, false, 0},    {w->b_res, (size_t)L * R, false, 0},
+      {w->b_skip, (size_t)S, false, 0},            {w->b_relu, (size_t)A, false, 0},
+      {w->b_out, (size_t)A, false, 0},
+  };
+  size_t total = 0;
+  for (Arr& a : arrs) {
+    a.off = total;
+    total = align_up(total + a.n * (a.matrix ? we : 4), 256);
+  }
+  std::vector<unsigned char> host(total, 0);
+  for (const Arr& a : arrs) {
+    if (a.matrix && bf) {
+      uint16_t* d = reinterpret_cast<uint16_t*>(host.data() + a.off);
+      for (size_t i = 0; i < a.n; ++i) d[i] = to_bf16(a.src[i]);
+    } else {
+      std::memcpy(host.data() + a.off, a.src, a.n * 4);
+    }
+  }
+  hipError_t e = hipMalloc(&h->dmem, total);
+  if (e != hipSuccess) {
+    delete h;
+    return e == hipErrorOutOfMemory ? fail(WN_ENOMEM, "hipMalloc of weights") : hip_fail(e, "hipMalloc");
+  }
+  e = hipMemcpy(h->dmem, host.data(), total, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(h->dmem);
+    delete h;
+    return hip_fail(e, "hipMemcpy of weights");
+  }
+  char* d = static_cast<char*>(h->dmem);
+  h->w.embed = d + arrs[0].off;
+  h->w.w_prev = d + arrs[1].off;
+  h->w.w_cur = d + arrs[2].off;
+  h->w.w_res = d + arrs[3].off;
+  h->w.w_skip = d + arrs[4].off;
+  h->w.w_relu = d + arrs[5].off;
+  h->w.w_out = d + arrs[6].off;
+  h->w.b_embed = reinterpret_cast<const float*>(d + arrs[7].off);
+  h->w.b_gate = reinterpret_cast<const float*>(d + arrs[8].off);
+  h->w.b_res = reinterpret_cast<const float*>(d + arrs[9].off);
+  h->w.b_skip = reinterpret_cast<const float*>(d + arrs[10].off);
+  h->w.b_relu = reinterpret_cast<const float*>(d + arrs[11].off);
+  h->w.b_out = reinterpret_cast<const float*>(d + arrs[12].off);
+  h->w.bf16 = bf ? 1 : 0;
+  *out = h;
+  return WN_OK;
+}
+
+size_t wn_workspace_bytes(const wn_handle* h, int32_t B) {
+  if (!h || B < 1) return 0;
+  return ws_layout(h, B).total;
+}
+
+int wn_generate(wn_handle* h, int32_t B, int32_t T, const float* cond, const float* uniforms, int32_t* samples,
+                void* workspace, size_t ws_bytes, int32_t reset, void* stream) {
+  g_err.clear();
+  int rc = check_call(h, B, T, cond, uniforms, samples, workspace, ws_bytes, reset);
+  if (rc != WN_OK || T == 0) return rc;
+  return launch(h, B, T, cond, uniforms, nullptr, samples, nullptr, workspace, reset, stream, false);
+}
+
+int wn_teacher_force(wn_handle* h, int32_t B, int32_t T, const float* cond, const int32_t* y, float* logits,
+                     void* workspace, size_t ws_bytes, int32_t reset, void* stream) {
+  g_err.clear();
+  int rc = check_call(h, B, T, cond, y, logits, workspace, ws_bytes, reset);
+  if (rc != WN_OK || T == 0) return rc;
+  return launch(h, B, T, cond, nullptr, y, nullptr, logits, workspace, reset, stream, true);
+}
+
+int wn_status(wn_handle* h, const void* workspace, void* stream) {
+  g_err.clear();
+  if (!h || !workspace) return fail(WN_EINVAL, "null argument");
+  DeviceScope scope(h->device);
+  if (!scope.ok()) return fail(WN_EHIP, "cannot select the handle's device");
+  int32_t st = 0;
+  hipError_t e = hipMemcpyAsync(&st, workspace, sizeof(st), hipMemcpyDeviceToHost, static_cast<hipStream_t>(stream));
+  if (e == hipSuccess) e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "reading the status word");
+  return st;
+}
+
+const char* wn_kernel_variant(const wn_handle* h, int32_t B) {
+  if (!h || B < 1) return "";
+  return "stream_l2";
+}
+
+void wn_destroy(wn_handle* h) {
+  if (!h) return;
+  {
+    DeviceScope scope(h->device);
+    if (h->dmem) (void)hipFree(h->dmem);
+  }
+  delete h;
+}
+
+const char* wn_error_string(int code) {
+  switch (code) {
+    case WN_OK: return "success";
+    case WN_EINVAL: return "invalid argument";
+    case WN_EUNSUPPORTED: return "model not supported by any kernel";
+    case WN_ENOMEM: return "out of memory";
+    case WN_EHIP: return "HIP runtime error";
+    case WN_ETIMEOUT: return "kernel wait timed out";
+    case WN_EABORTED: return "kernel aborted";
+    default: return "unknown error";
+  }
+}
+
+const char* wn_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,64 @@
+// Internal interface between the libwn host code and its HIP kernels (gfx950).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+#define WN_MAX_LAYERS 64
+#define WN_A 256
+
+// Model sizes and the per-stream history layout: layer j keeps d_j slots of r
+// floats starting at hoff[j] (in floats) inside a stream's history block of
+// hist_len floats.
+struct WnDims {
+  int L, R, S;
+  int hist_len;
+  int dil[WN_MAX_LAYERS];
+  int hoff[WN_MAX_LAYERS];
+};
+
+// Device copies of the weights.  Matrices are row-major [out][in] and either
+// fp32 or bf16 (uint16 bit patterns); biases are fp32.
+struct WnDevWeights {
+  const void* embed;   // [A][R]
+  const void* w_prev;  // [L][2R][R]
+  const void* w_cur;   // [L][2R][R]
+  const void* w_res;   // [L][R][R]
+  const void* w_skip;  // [L][S][R]
+  const void* w_relu;  // [A][S]
+  const void* w_out;   // [A][A]
+  const float* b_embed;
+  const float* b_gate;
+  const float* b_res;
+  const float* b_skip;
+  const float* b_relu;
+  const float* b_out;
+  int bf16;
+};
+
+// One call's inputs and outputs (device pointers, caller-owned).
+struct WnIO {
+  const float* cond;    // [B][T][L][2R]
+  const float* u;       // [B][T]            (generation)
+  const int32_t* y_in;  // [B][T]            (teacher forcing)
+  int32_t* y_out;       // [B][T]            (generation)
+  float* logits;        // [B][T][A]         (teacher forcing)
+  int B, T, reset, init_sample;
+};
+
+// Caller-owned workspace, carved by the host code.
+struct WnWorkspace {
+  int32_t* status;      // one word
+  int64_t* state;       // [B][2]: steps taken, last sample
+  float* hist;          // [B][hist_len]
+};
+
+struct WnStreamArgs {
+  WnDims d;
+  WnDevWeights w;
+  WnIO io;
+  WnWorkspace ws;
+};
+
+// Kernel families.  Each returns hipSuccess or the launch error.
+bool wn_stream_supported(int R, int S);
+hipError_t wn_stream_launch(const WnStreamArgs& args, bool teacher, hipStream_t stream);

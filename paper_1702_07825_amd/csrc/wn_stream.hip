@@ -1,0 +1,320 @@
+// Persistent per-stream generation kernel for gfx950.
+//
+// One 1024-thread workgroup (16 wave64s) owns one stream for the whole call and
+// loops over its T steps.  Each step evaluates the autoregressive WaveNet of
+// Deep Voice (arXiv 1702.07825), Appendix A.1, in the order of the paper's
+// CPU-inference section (Section 5.1): sample embedding, then per layer the two
+// halves of the width-2 dilated convolution (W_prev on the history slot, W_cur
+// on the current input), the gated activation, the residual and skip 1x1
+// projections, then the relu head, the softmax and the draw.
+//
+// Data placement:
+//  - weights stay in HBM and are re-read every step through the L2 (each row is
+//    read by LPR adjacent lanes with 16-byte loads, so a wave instruction covers
+//    contiguous row segments);
+//  - activations (x, h, q, z_a, logits) and the step's conditioning and history
+//    reads live in LDS;
+//  - each layer's dilation history is a ring of d_j slots of r floats in the
+//    workspace: slot (tg mod d_j) holds x_{j-1}[tg - d_j] when step tg starts and
+//    receives x_{j-1}[tg] during it.
+// Matrix-vector products reduce across the LPR lanes of a row with cross-lane
+// shuffles.  The draw is a single-wave max / exp / inclusive scan / count.
+#include "wn_internal.h"
+
+namespace {
+
+constexpr int NT = 1024;
+constexpr int A = WN_A;
+
+__device__ __forceinline__ float ex2(float v) { return __builtin_amdgcn_exp2f(v); }
+__device__ __forceinline__ float rcp(float v) { return __builtin_amdgcn_rcpf(v); }
+__device__ __forceinline__ float expf_fast(float v) { return ex2(v * 1.4426950408889634f); }
+// tanh(v) = 1 - 2 / (1 + e^{2v}); saturates correctly at both ends.
+__device__ __forceinline__ float tanh_f(float v) { return 1.0f - 2.0f * rcp(1.0f + expf_fast(2.0f * v)); }
+__device__ __forceinline__ float sigmoid_f(float v) { return rcp(1.0f + expf_fast(-v)); }
+
+__device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ float4 ld4(const uint16_t* p) {
+  const uint2 v = *reinterpret_cast<const uint2*>(p);
+  return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
+                     __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u));
+}
+__device__ __forceinline__ float dot4(float4 w, float4 x, float acc) {
+  acc = fmaf(w.x, x.x, acc);
+  acc = fmaf(w.y, x.y, acc);
+  acc = fmaf(w.z, x.z, acc);
+  return fmaf(w.w, x.w, acc);
+}
+
+// Dot products of K-long rows: LPR adjacent lanes share a row, each handling NV
+// float4 chunks (chunk index lane + i*LPR), then reduce across the LPR lanes.
+template <int K>
+struct RowDot {
+  static constexpr int LPR = (K / 4 < 16) ? K / 4 : 16;
+  static constexpr int NV = K / 4 / LPR;
+  static constexpr int G = NT / LPR;  // rows per pass over the workgroup
+  template <typename WT>
+  __device__ static float partial(const WT* row, const float4 (&x4)[NV], int li) {
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) s = dot4(ld4(row + 4 * (li + i * LPR)), x4[i], s);
+    return s;
+  }
+  __device__ static void load_x(const float* x, float4 (&x4)[NV], int li) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) x4[i] = reinterpret_cast<const float4*>(x)[li + i * LPR];
+  }
+  __device__ static float reduce(float v) {
+#pragma unroll
+    for (int o = LPR / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+  }
+};
+
+template <int R, int S, typename WT, bool TF>
+__global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) {
+  const WnDims& D = args.d;
+  const int L = D.L;
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int T = args.io.T;
+
+  extern __shared__ float dyn[];
+  float* xr = dyn;              // [L][R] history reads of this step
+  float* cs = dyn + L * R;      // [L][2R] conditioning of this step
+  __shared__ float xs[R];       // x_{j-1}, updated in place to x_j
+  __shared__ float hs[R];
+  __shared__ float qs[S];
+  __shared__ float zas[A];
+  __shared__ float lgs[A];
+  __shared__ int yprev_s;
+
+  const WT* embed = static_cast<const WT*>(args.w.embed);
+  const WT* w_prev = static_cast<const WT*>(args.w.w_prev);
+  const WT* w_cur = static_cast<const WT*>(args.w.w_cur);
+  const WT* w_res = static_cast<const WT*>(args.w.w_res);
+  const WT* w_skip = static_cast<const WT*>(args.w.w_skip);
+  const WT* w_relu = static_cast<const WT*>(args.w.w_relu);
+  const WT* w_out = static_cast<const WT*>(args.w.w_out);
+
+  float* hist = args.ws.hist + (size_t)b * D.hist_len;
+  int64_t* state = args.ws.state + 2 * (size_t)b;
+
+  int64_t tg0;
+  if (args.io.reset) {
+    for (int i = tid; i < D.hist_len / 4; i += NT) reinterpret_cast<float4*>(hist)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    tg0 = 0;
+    if (tid == 0) yprev_s = args.io.init_sample;
+    if (b == 0 && tid == 0) *args.ws.status = 0;
+  } else {
+    tg0 = state[0];
+    if (tid == 0) yprev_s = (int)state[1];
+  }
+  __syncthreads();
+
+  for (int t = 0; t < T; ++t) {
+    const int64_t tg = tg0 + t;
+    const size_t bt = (size_t)b * T + t;
+    // ---- step inputs: history slots, conditioning, embedding, q = B_skip ----
+    {
+      const float* cond_t = args.io.cond + bt * (size_t)(L * 2 * R);
+      for (int i = tid; i < L * 2 * R / 4; i += NT)
+        reinterpret_cast<float4*>(cs)[i] = reinterpret_cast<const float4*>(cond_t)[i];
+      for (int i = tid; i < L * R / 4; i += NT) {
+        const int j = i / (R / 4), c4 = i % (R / 4);
+        const int slot = (int)(tg % D.dil[j]);
+        reinterpret_cast<float4*>(xr)[i] = reinterpret_cast<const float4*>(hist + D.hoff[j] + slot * R)[c4];
+      }
+      const int yp = yprev_s;
+      if (tid < R) {
+        const WT* e = embed + (size_t)yp * R;
+        float ev;
+        if constexpr (sizeof(WT) == 2) ev = __uint_as_float((uint32_t)e[tid] << 16);
+        else ev = e[tid];
+        xs[tid] = ev + args.w.b_embed[tid];
+      }
+      for (int m = tid; m < S; m += NT) qs[m] = args.w.b_skip[m];
+    }
+    __syncthreads();
+
+    for (int j = 0; j < L; ++j) {
+      // ---- a = W_prev x[t-d] + W_cur x[t] + B + L ; h = tanh(a[:R]) * sigmoid(a[R:]) ----
+      {
+        using RD = RowDot<R>;
+        const int li = tid % RD::LPR, grp = tid / RD::LPR;
+        float4 xp4[RD::NV], xc4[RD::NV];
+        RD::load_x(xr + j * R, xp4, li);
+        RD::load_x(xs, xc4, li);
+        const WT* wp = w_prev + (size_t)j * 2 * R * R;
+        const WT* wc = w_cur + (size_t)j * 2 * R * R;
+        constexpr int P = (R + RD::G - 1) / RD::G;
+#pragma unroll
+        for (int p = 0; p < P; ++p) {
+          const int c = p * RD::G + grp;
+          if (c < R) {
+            float s0 = RD::partial(wp + (size_t)c * R, xp4, li) + RD::partial(wc + (size_t)c * R, xc4, li);
+            float s1 = RD::partial(wp + (size_t)(c + R) * R, xp4, li) + RD::partial(wc + (size_t)(c + R) * R, xc4, li);
+            s0 = RD::reduce(s0);
+            s1 = RD::reduce(s1);
+            if (li == 0) {
+              const float* bg = args.w.b_gate + j * 2 * R;
+              const float a0 = s0 + bg[c] + cs[j * 2 * R + c];
+              const float a1 = s1 + bg[c + R] + cs[j * 2 * R + c + R];
+              hs[c] = tanh_f(a0) * sigmoid_f(a1);
+            }
+          }
+        }
+        // x_{j-1}[tg] goes into the slot whose old value (x_{j-1}[tg - d]) was read above
+        if (tid < R) hist[D.hoff[j] + (int)(tg % D.dil[j]) * R + tid] = xs[tid];
+      }
+      __syncthreads();
+      // ---- x += W_res h + B_res (rows 0..R-1) ; q += W_skip h (rows R..R+S-1) ----
+      {
+        using RD = RowDot<R>;
+        const int li = tid % RD::LPR, grp = tid / RD::LPR;
+        float4 h4[RD::NV];
+        RD::load_x(hs, h4, li);
+        const bool last = (j == L - 1);  // x_L feeds nothing
+        const WT* wr = w_res + (size_t)j * R * R;
+        const WT* wk = w_skip + (size_t)j * S * R;
+        constexpr int P = (R + S + RD::G - 1) / RD::G;
+#pragma unroll
+        for (int p = 0; p < P; ++p) {
+          const int row = p * RD::G + grp;
+          if (row < R) {
+            if (!last) {
+              const float v = RD::reduce(RD::partial(wr + (size_t)row * R, h4, li));
+              if (li == 0) xs[row] += v + args.w.b_res[j * R + row];
+            }
+          } else if (row < R + S) {
+            const int m = row - R;
+            const float v = RD::reduce(RD::partial(wk + (size_t)m * R, h4, li));
+            if (li == 0) qs[m] += v;
+          }
+        }
+      }
+      __syncthreads();
+    }
+
+    // ---- z_a = relu(W_relu relu(q) + B_relu) ----
+    {
+      using RD = RowDot<S>;
+      const int li = tid % RD::LPR, grp = tid / RD::LPR;
+      float4 z4[RD::NV];
+      RD::load_x(qs, z4, li);
+#pragma unroll
+      for (int i = 0; i < RD::NV; ++i) {
+        z4[i].x = fmaxf(z4[i].x, 0.f); z4[i].y = fmaxf(z4[i].y, 0.f);
+        z4[i].z = fmaxf(z4[i].z, 0.f); z4[i].w = fmaxf(z4[i].w, 0.f);
+      }
+      constexpr int P = A / RD::G;
+#pragma unroll
+      for (int p = 0; p < P; ++p) {
+        const int i = p * RD::G + grp;
+        const float v = RD::reduce(RD::partial(w_relu + (size_t)i * S, z4, li));
+        if (li == 0) zas[i] = fmaxf(v + args.w.b_relu[i], 0.f);
+      }
+    }
+    __syncthreads();
+    // ---- logits = W_out z_a + B_out ----
+    {
+      using RD = RowDot<A>;
+      const int li = tid % RD::LPR, grp = tid / RD::LPR;
+      float4 z4[RD::NV];
+      RD::load_x(zas, z4, li);
+      constexpr int P = A / RD::G;
+#pragma unroll
+      for (int p = 0; p < P; ++p) {
+        const int i = p * RD::G + grp;
+        const float v = RD::reduce(RD::partial(w_out + (size_t)i * A, z4, li));
+        if (li == 0) {
+          const float lg = v + args.w.b_out[i];
+          if constexpr (TF) args.io.logits[bt * A + i] = lg;
+          else lgs[i] = lg;
+        }
+      }
+    }
+    if constexpr (TF) {
+      if (tid == 0) {
+        int y = args.io.y_in[bt];
+        yprev_s = y < 0 ? 0 : (y > A - 1 ? A - 1 : y);
+      }
+    } else {
+      __syncthreads();
+      // ---- p = softmax(logits); y = #{k <= A-2 : C_k <= u} (one wave) ----
+      if (tid < 64) {
+        const int lane = tid;
+        float l0 = lgs[4 * lane], l1 = lgs[4 * lane + 1], l2 = lgs[4 * lane + 2], l3 = lgs[4 * lane + 3];
+        float m = fmaxf(fmaxf(l0, l1), fmaxf(l2, l3));
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+        const float e0 = expf_fast(l0 - m), e1 = expf_fast(l1 - m), e2 = expf_fast(l2 - m), e3 = expf_fast(l3 - m);
+        const float s0 = e0, s1 = s0 + e1, s2 = s1 + e2, s3 = s2 + e3;
+        float incl = s3;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const float v = __shfl_up(incl, o, 64);
+          if (lane >= o) incl += v;
+        }
+        float excl = __shfl_up(incl, 1, 64);
+        if (lane == 0) excl = 0.f;
+        const float Z = __shfl(incl, 63, 64);
+        const float u = args.io.u[bt];
+        int cnt = 0;
+        cnt += ((excl + s0) / Z <= u);
+        cnt += ((excl + s1) / Z <= u);
+        cnt += ((excl + s2) / Z <= u);
+        if (lane != 63) cnt += ((excl + s3) / Z <= u);  // k = 255 is never counted
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
+        if (lane == 0) {
+          args.io.y_out[bt] = cnt;
+          yprev_s = cnt;
+        }
+      }
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    state[0] = tg0 + T;
+    state[1] = yprev_s;
+  }
+}
+
+template <int R, int S>
+hipError_t launch_rs(const WnStreamArgs& args, bool teacher, hipStream_t stream) {
+  const size_t dyn = (size_t)args.d.L * 3 * R * sizeof(float);
+  const dim3 grid(args.io.B), block(NT);
+  hipError_t e;
+#define WN_LAUNCH(WT, TF)                                                                            \
+  do {                                                                                               \
+    auto k = wn_stream_kernel<R, S, WT, TF>;                                                         \
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(k), hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn); \
+    if (e != hipSuccess) return e;                                                                   \
+    hipLaunchKernelGGL(k, grid, block, dyn, stream, args);                                           \
+  } while (0)
+  if (args.w.bf16) {
+    if (teacher) WN_LAUNCH(uint16_t, true); else WN_LAUNCH(uint16_t, false);
+  } else {
+    if (teacher) WN_LAUNCH(float, true); else WN_LAUNCH(float, false);
+  }
+#undef WN_LAUNCH
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool wn_stream_supported(int R, int S) {
+  return (R == 16 && S == 32) || (R == 32 && S == 128) || (R == 64 && S == 128) || (R == 64 && S == 256) ||
+         (R == 128 && S == 256);
+}
+
+hipError_t wn_stream_launch(const WnStreamArgs& args, bool teacher, hipStream_t stream) {
+  const int R = args.d.R, S = args.d.S;
+  if (R == 16 && S == 32) return launch_rs<16, 32>(args, teacher, stream);
+  if (R == 32 && S == 128) return launch_rs<32, 128>(args, teacher, stream);
+  if (R == 64 && S == 128) return launch_rs<64, 128>(args, teacher, stream);
+  if (R == 64 && S == 256) return launch_rs<64, 256>(args, teacher, stream);
+  if (R == 128 && S == 256) return launch_rs<128, 256>(args, teacher, stream);
+  return hipErrorInvalidValue;
+}

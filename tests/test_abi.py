@@ -1,0 +1,103 @@
+"""C ABI checks that need no GPU: the library loads, exports every function that
+include/wn.h declares, and rejects bad arguments before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "wn.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(wn_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_1702_07825_amd as wn
+    if not os.path.exists(wn.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    return wn.load_library()
+
+
+def test_exports_every_declared_function(lib):
+    import paper_1702_07825_amd as wn
+    names = _declared()
+    assert set(names) == set(wn.EXPORTED)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_error_strings(lib):
+    for code in (0, -1, -2, -3, -4, -5, -6):
+        assert lib.wn_error_string(code).decode()
+    assert lib.wn_error_string(99).decode() == "unknown error"
+
+
+def _cfg(wn, **kw):
+    import numpy as np
+    d = np.array(kw.pop("dil", [1, 2, 4, 8]), np.int32)
+    c = wn.Config(kw.get("L", 4), kw.get("r", 16), kw.get("s", 32), kw.get("a", 256),
+                  d.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), kw.get("taps", 1), kw.get("init", 128),
+                  kw.get("dtype", 0))
+    return c, d
+
+
+def _weights(wn):
+    import numpy as np
+    import synth
+    w = synth.make_weights(4, 16, 32)
+    keep = {k: np.ascontiguousarray(w[k]) for k in wn.WEIGHT_FIELDS}
+    return wn.Weights(*[keep[k].ctypes.data_as(ctypes.POINTER(ctypes.c_float)) for k in wn.WEIGHT_FIELDS]), keep
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(L=0), -1), (dict(L=65), -1), (dict(init=256), -1), (dict(init=-1), -1), (dict(dtype=7), -1),
+    (dict(dil=[1, 0, 4, 8]), -1), (dict(taps=3), -1), (dict(r=0), -1),
+    (dict(a=255), -2), (dict(taps=2), -2), (dict(r=48, s=32), -2), (dict(r=16, s=64), -2),
+])
+def test_create_rejects_before_any_device_call(lib, kw, code):
+    import paper_1702_07825_amd as wn
+    c, _d = _cfg(wn, **kw)
+    w, _keep = _weights(wn)
+    h = ctypes.c_void_p()
+    assert lib.wn_create(ctypes.byref(c), ctypes.byref(w), ctypes.byref(h)) == code
+    assert h.value is None
+    assert lib.wn_last_error().decode()
+
+
+def test_null_arguments(lib):
+    import paper_1702_07825_amd as wn
+    c, _d = _cfg(wn)
+    h = ctypes.c_void_p()
+    assert lib.wn_create(None, None, ctypes.byref(h)) == -1
+    assert lib.wn_create(ctypes.byref(c), None, ctypes.byref(h)) == -1
+    w, _keep = _weights(wn)
+    w.w_out = None
+    assert lib.wn_create(ctypes.byref(c), ctypes.byref(w), ctypes.byref(h)) == -1
+    assert lib.wn_workspace_bytes(None, 1) == 0
+    assert lib.wn_generate(None, 1, 1, None, None, None, None, 0, 1, None) == -1
+    assert lib.wn_teacher_force(None, 1, 1, None, None, None, None, 0, 1, None) == -1
+    assert lib.wn_status(None, None, None) == -1
+    assert lib.wn_kernel_variant(None, 1) == b""
+    lib.wn_destroy(None)
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    import paper_1702_07825_amd as wn
+    with pytest.raises(RuntimeError):
+        wn.load_library.__wrapped__(str(tmp_path / "missing.so")) if hasattr(wn.load_library, "__wrapped__") \
+            else _load_missing(wn, str(tmp_path / "missing.so"))
+
+
+def _load_missing(wn, path):
+    saved = wn._lib
+    wn._lib = None
+    try:
+        wn.load_library(path)
+    finally:
+        wn._lib = saved

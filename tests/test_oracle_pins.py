@@ -258,3 +258,27 @@ def test_history_is_zero_padded_before_the_first_step():
     w2["w_prev"][:] = 123.0
     _, lg2, _ = oracle.run(oracle.Model(w2, dil), cond, y_in=np.array([5], np.int32))
     np.testing.assert_array_equal(lg, lg2)
+
+
+def test_window_of_receptive_field_reproduces_full_run():
+    """Step t's logits depend only on steps [t - sum(d), t]: a teacher-forced run over that window,
+    started from zero histories with y_{t0-1} as its initial sample, gives them bit for bit."""
+    L, r, s, dil = 4, 16, 32, (1, 2, 4, 8)
+    T = 120
+    w, m = _model(L, r, s, dil, seed=71, bias=0.3)
+    cond = _cond(L, r, T, seed=72)
+    u = synth.make_uniforms(1, T, seed=73)[0]
+    y, lg, mg = oracle.run(m, cond, u=u)
+    sd = sum(dil)
+    for t in (sd, sd + 1, 57, T - 1):
+        t0 = t - sd
+        mw = oracle.Model(w, dil, initial_sample=int(y[t0 - 1]) if t0 > 0 else 128)
+        yw, lw, mw_ = oracle.run(mw, cond[t0:t + 1], u=u[t0:t + 1], y_in=y[t0:t + 1])
+        np.testing.assert_array_equal(lw[-1], lg[t])
+        assert yw[-1] == y[t] and mw_[-1] == mg[t]
+    # one step shorter is not enough (the oldest input is reached through every layer)
+    t = T - 1
+    t0 = t - sd + 1
+    mw = oracle.Model(w, dil, initial_sample=int(y[t0 - 1]))
+    _, lw, _ = oracle.run(mw, cond[t0:t + 1], y_in=y[t0:t + 1])
+    assert np.any(lw[-1] != lg[t])
