@@ -1,0 +1,174 @@
+"""Benchmark: autoregressive WaveNet generation on one MI355X.
+
+A "step" is one wn_generate call over the whole workload (every stream, every
+sample) from a reset state, with conditioning and uniforms already resident in
+HBM.  Prints ONE JSON line on stdout:
+  value      generated samples/s (all streams) over the timed steps
+  roofline   the generation kernel's algorithmic FLOP rate (2 x multiply-adds
+             per sample of the model) over its average launch duration, from HIP
+             events on the stream the kernel runs on, against the chip's peak
+  cpu_baseline  the CPU oracle timed on this host on a bounded sample
+Default workload: l=20, r=64, s=256, B=1, T=16000 (1 s of 16 kHz audio), fp32.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAKS = {  # MI355X published dense peaks
+    "f32_vector_tflops": 157.3,
+    "f32_mfma_tflops": 157.3,
+    "bf16_mfma_tflops": 2500.0,
+    "hbm_gbs": 8000.0,
+}
+RATE_HZ = 16000
+PAPER_RATE_HZ = 16384
+
+
+def macs_per_sample(L, r, s, a=256, last_res=False):
+    """Multiply-adds one generated sample needs: per layer W_prev and W_cur (2r x r each), W_res
+    (r x r, not for the last layer, whose x feeds nothing) and W_skip (s x r); head W_relu (a x s)
+    and W_out (a x a)."""
+    per_layer = 2 * (2 * r * r) + r * r + s * r
+    return L * per_layer - (0 if last_res else r * r) + a * s + a * a
+
+
+def kernel_source_digest():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_1702_07825_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".h")):
+            h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profiles(workload, variant):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if taken on the current kernels."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        rec = json.load(open(path))[workload]
+    except Exception:
+        return None
+    if rec.get("source_digest") != kernel_source_digest() or rec.get("variant") != variant:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(wl, w, cond_dev, u_np, steps):
+    import numpy as np
+    import oracle
+    m = oracle.Model(w, wl.dilations, bf16_weights=(wl.weight_dtype == "bf16"))
+    cond = cond_dev[0, :steps].cpu().numpy()
+    t0 = time.perf_counter()
+    oracle.run(m, cond, u=u_np[0, :steps], want_logits=False)
+    dt = time.perf_counter() - t0
+    return {"value": steps / dt, "unit": "samples/s", "cores": 1, "kind": "oracle",
+            "sample": "stream 0, first %d of %d steps, generation, single thread (fp64 C oracle)" % (steps, wl.T),
+            "seconds": round(dt, 2)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="l20_r64_b1")
+    ap.add_argument("--cpu-steps", type=int, default=8000, help="oracle sample size (0 = skip)")
+    ap.add_argument("--seed", type=int, default=0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU only (streams are independent; see DESIGN.md for how "
+              "the batched workloads would shard); --gpus %d is not supported" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_1702_07825_amd as wn
+
+    wl = synth.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = synth.make_weights(wl.n_layers, wl.r, wl.s, seed=args.seed)
+    net = wn.WaveNet(w, wl.dilations, weight_dtype=wl.weight_dtype)
+    cond = synth.make_cond(wl.n_layers, wl.r, wl.B, wl.T, seed=args.seed, device="cuda:0")
+    u_np = synth.make_uniforms(wl.B, wl.T, seed=args.seed)
+    u = torch.tensor(u_np, device=dev)
+    samples = torch.empty((wl.B, wl.T), dtype=torch.int32, device=dev)
+    ws = net.new_workspace(wl.B, dev)
+    variant = net.kernel_variant(wl.B)
+    print("bench: %s, kernel %s, %d warmup + %d timed steps" % (wl.description, variant, args.warmup, args.steps),
+          file=sys.stderr, flush=True)
+
+    for _ in range(args.warmup):
+        net.generate(cond, u, samples=samples, workspace=ws, reset=True)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        net.generate(cond, u, samples=samples, workspace=ws, reset=True)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    assert net.status(ws) == 0
+    launch_ms = [a.elapsed_time(b) for a, b in ev]
+    avg_launch_s = sum(launch_ms) / len(launch_ms) / 1e3
+
+    n = wl.B * wl.T
+    value = n * args.steps / elapsed
+    flop_per_launch = 2.0 * macs_per_sample(wl.n_layers, wl.r, wl.s) * n
+    peak = PEAKS["f32_vector_tflops"]
+    achieved = flop_per_launch / avg_launch_s / 1e12
+    per_stream_rate = wl.T / avg_launch_s
+    y = samples.cpu().numpy()
+    out = {
+        "metric": "generated samples/s (16 kHz mu-law audio, all streams)",
+        "value": round(value, 1),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if wl.weight_dtype == "f32" else "bf16-weights/f32",
+        "data": "synthetic (seeded N(0,1/fan_in) weights, N(0,1) conditioning, U[0,1) uniforms)",
+        "config": {"workload": wl.description, "B": wl.B, "T": wl.T, "n_layers": wl.n_layers, "r": wl.r,
+                   "s": wl.s, "a": wl.a, "kernel": variant},
+        "real_time_factor_16khz": round(per_stream_rate / RATE_HZ, 3),
+        "real_time_factor_16384hz": round(per_stream_rate / PAPER_RATE_HZ, 3),
+        "us_per_sample_step": round(avg_launch_s / wl.T * 1e6, 3),
+        "roofline": {
+            "bound": "alu",
+            "achieved": round(achieved, 4),
+            "peak": peak,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 6),
+            "traffic": traffic_from_profiles(args.workload, variant),
+            "algorithmic_flop_per_launch": flop_per_launch,
+            "avg_launch_ms": round(avg_launch_s * 1e3, 4),
+        },
+        "sample_histogram_entropy_bits": round(float(-(lambda p: (p[p > 0] * np.log2(p[p > 0])).sum())(
+            np.bincount(y.ravel(), minlength=256) / y.size)), 3),
+    }
+    if args.cpu_steps > 0:
+        out["cpu_baseline"] = cpu_baseline(wl, w, cond, u_np, min(args.cpu_steps, wl.T))
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+    net.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -4,9 +4,12 @@
 #include "wn_internal.h"
 
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
+
+enum WnVariant { WN_VARIANT_STREAM = 0, WN_VARIANT_CHAIN = 1 };
 
 struct wn_handle {
   int device = 0;
@@ -17,6 +20,9 @@ struct wn_handle {
   void* dmem = nullptr;
   WnDims dims{};
   WnDevWeights w{};
+  bool chain_ok = false;  // the multi-CU kernel can serve B = 1
+  int nch = 0;            // its chain CUs
+  int layer_begin[WN_MAX_CHAIN + 1] = {};
 };
 
 namespace {
@@ -64,8 +70,12 @@ class DeviceScope {
   bool ok_ = false;
 };
 
+int variant_for(const wn_handle* h, int B) { return (B == 1 && h->chain_ok) ? WN_VARIANT_CHAIN : WN_VARIANT_STREAM; }
+
+// Workspace: status word, per-stream state, then either fp32 histories (stream kernel) or
+// tagged 64-bit histories followed by the inter-CU mailboxes (multi-CU kernel).
 struct WsLayout {
-  size_t status_off, state_off, hist_off, total;
+  size_t status_off, state_off, hist_off, mb_off, mb_words, total;
 };
 
 WsLayout ws_layout(const wn_handle* h, int B) {
@@ -73,7 +83,15 @@ WsLayout ws_layout(const wn_handle* h, int B) {
   l.status_off = 0;
   l.state_off = 256;
   l.hist_off = align_up(l.state_off + (size_t)B * 2 * sizeof(int64_t), 256);
-  l.total = align_up(l.hist_off + (size_t)B * h->dims.hist_len * sizeof(float), 256);
+  if (variant_for(h, B) == WN_VARIANT_CHAIN) {
+    l.mb_off = align_up(l.hist_off + (size_t)h->dims.hist_len * 8, 256);
+    l.mb_words = wn_chain_mailbox_words(h->L, h->R, h->S);
+    l.total = align_up(l.mb_off + l.mb_words * 8, 256);
+  } else {
+    l.mb_off = 0;
+    l.mb_words = 0;
+    l.total = align_up(l.hist_off + (size_t)B * h->dims.hist_len * sizeof(float), 256);
+  }
   return l;
 }
 
@@ -98,6 +116,43 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
   if (!scope.ok()) return fail(WN_EHIP, "cannot select the handle's device");
   const WsLayout l = ws_layout(h, B);
   char* base = static_cast<char*>(ws);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (variant_for(h, B) == WN_VARIANT_CHAIN) {
+    WnChainArgs g{};
+    g.d = h->dims;
+    g.w = h->w;
+    g.io.cond = cond;
+    g.io.u = u;
+    g.io.y_in = y_in;
+    g.io.y_out = y_out;
+    g.io.logits = logits;
+    g.io.B = B;
+    g.io.T = T;
+    g.io.reset = reset;
+    g.io.init_sample = h->init_sample;
+    g.status = reinterpret_cast<int32_t*>(base + l.status_off);
+    g.state = reinterpret_cast<int64_t*>(base + l.state_off);
+    g.ring = reinterpret_cast<unsigned long long*>(base + l.hist_off);
+    unsigned long long* mb = reinterpret_cast<unsigned long long*>(base + l.mb_off);
+    const int L = h->L, R = h->R, S = h->S;
+    g.mb_pre = mb;
+    g.mb_h = g.mb_pre + (size_t)L * 2 * 2 * R;
+    g.mb_q = g.mb_h + (size_t)L * 2 * R;
+    g.mb_x = g.mb_q + (size_t)L * 2 * S;
+    g.mb_logit = g.mb_x + (size_t)h->nch * 2 * R;
+    g.mb_qtail = g.mb_logit + (size_t)4 * 2 * WN_A;
+    g.nch = h->nch;
+    for (int c = 0; c <= h->nch; ++c) g.layer_begin[c] = h->layer_begin[c];
+    g.spin_limit = 1 << 22;
+    if (reset) {
+      const size_t words = (l.mb_off - l.hist_off) / 8 + l.mb_words;
+      const hipError_t e = wn_chain_reset(g.ring, words, g.status, st);
+      if (e != hipSuccess) return hip_fail(e, "reset kernel launch");
+    }
+    const hipError_t e = wn_chain_launch(g, teacher, st);
+    if (e != hipSuccess) return hip_fail(e, "multi-CU kernel launch");
+    return WN_OK;
+  }
   WnStreamArgs args{};
   args.d = h->dims;
   args.w = h->w;
@@ -113,7 +168,7 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
   args.ws.status = reinterpret_cast<int32_t*>(base + l.status_off);
   args.ws.state = reinterpret_cast<int64_t*>(base + l.state_off);
   args.ws.hist = reinterpret_cast<float*>(base + l.hist_off);
-  const hipError_t e = wn_stream_launch(args, teacher, static_cast<hipStream_t>(stream));
+  const hipError_t e = wn_stream_launch(args, teacher, st);
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return WN_OK;
 }
@@ -224,6 +279,21 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
   h->w.b_relu = reinterpret_cast<const float*>(d + arrs[11].off);
   h->w.b_out = reinterpret_cast<const float*>(d + arrs[12].off);
   h->w.bf16 = bf ? 1 : 0;
+
+  // The multi-CU kernel needs fp32 weights, a supported shape and one CU per block of its grid.
+  const char* force = std::getenv("WN_KERNEL");
+  const bool want_chain = !(force && std::strcmp(force, "stream") == 0);
+  int cus = 0, coop = 0;
+  (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device);
+  (void)hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, h->device);
+  if (want_chain && !bf && wn_chain_supported(R, S, L) && cus >= WN_CHAIN_GRID && coop) {
+    const int nlc = wn_chain_layers_per_cu(R);
+    h->nch = (L + nlc - 1) / nlc;
+    const int base = L / h->nch, extra = L % h->nch;
+    h->layer_begin[0] = 0;
+    for (int c = 0; c < h->nch; ++c) h->layer_begin[c + 1] = h->layer_begin[c] + base + (c < extra ? 1 : 0);
+    h->chain_ok = true;
+  }
   *out = h;
   return WN_OK;
 }
@@ -263,7 +333,7 @@ int wn_status(wn_handle* h, const void* workspace, void* stream) {
 
 const char* wn_kernel_variant(const wn_handle* h, int32_t B) {
   if (!h || B < 1) return "";
-  return "stream_l2";
+  return variant_for(h, B) == WN_VARIANT_CHAIN ? "multi_cu_chain" : "stream_l2";
 }
 
 void wn_destroy(wn_handle* h) {

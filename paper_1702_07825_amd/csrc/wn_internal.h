@@ -59,6 +59,35 @@ struct WnStreamArgs {
   WnWorkspace ws;
 };
 
+#define WN_MAX_CHAIN 16   // chain CUs of the multi-CU kernel
+#define WN_CHAIN_GRID 256 // blocks of the multi-CU kernel (one per CU)
+
+// Multi-CU kernel for one stream: tagged 64-bit words (value | step + 1 << 32).
+struct WnChainArgs {
+  WnDims d;
+  WnDevWeights w;
+  WnIO io;
+  int32_t* status;
+  int64_t* state;                // [2]: steps taken, last sample
+  unsigned long long* ring;      // [hist_len] tagged dilation histories
+  unsigned long long* mb_pre;    // [L][2][2R] pre-activations (aux -> chain)
+  unsigned long long* mb_h;      // [L][2][R] hidden states (chain -> aux)
+  unsigned long long* mb_q;      // [L][2][S] skip partials (aux -> head)
+  unsigned long long* mb_x;      // [nch][2][R] layer-run outputs (chain -> next chain)
+  unsigned long long* mb_logit;  // [4][2][A] partial logits (head -> chain CU 0)
+  unsigned long long* mb_qtail;  // [2][S] last layer's skip projection (last chain CU -> head)
+  int nch;                       // chain CUs
+  int layer_begin[WN_MAX_CHAIN + 1];
+  int spin_limit;                // polls before a wait gives up with WN_ETIMEOUT
+};
+
 // Kernel families.  Each returns hipSuccess or the launch error.
 bool wn_stream_supported(int R, int S);
 hipError_t wn_stream_launch(const WnStreamArgs& args, bool teacher, hipStream_t stream);
+
+bool wn_chain_supported(int R, int S, int L);
+int wn_chain_layers_per_cu(int R);
+int wn_chain_num_cus(int L, int R);
+size_t wn_chain_mailbox_words(int L, int R, int S);
+hipError_t wn_chain_reset(unsigned long long* words, size_t n, int* status, hipStream_t stream);
+hipError_t wn_chain_launch(const WnChainArgs& g, bool teacher, hipStream_t stream);

@@ -208,3 +208,63 @@ def test_full_size_sampled(name):
     assert worst <= LOGIT_TOL[wl.weight_dtype]
     assert mism == 0
     net.close()
+
+
+# ---------------------------------------------------------------------------------------------
+# The multi-CU kernel that serves single-stream fp32 models (l=20/40, r=64, s=256).
+# ---------------------------------------------------------------------------------------------
+
+def _force_stream(monkeypatch):
+    monkeypatch.setenv("WN_KERNEL", "stream")
+
+
+def test_multi_cu_kernel_is_used_for_one_stream():
+    wn = _wn()
+    w = synth.make_weights(20, 64, 256, seed=1)
+    net = wn.WaveNet(w, synth.dilation_cycle(20))
+    assert net.kernel_variant(1) == "multi_cu_chain"
+    assert net.kernel_variant(2) == "stream_l2"
+    net.close()
+
+
+@pytest.mark.parametrize("L,S", [(20, 256), (9, 128), (40, 256), (3, 256), (7, 128)])
+def test_multi_cu_kernel_parity_and_state(L, S, monkeypatch):
+    """Chain kernel vs oracle (logits, confident indices), chunked == one-shot, run twice == once."""
+    r, T = 64, 400
+    dil = tuple(synth.dilation_cycle(L))
+    _log("multi-CU L=%d r=%d s=%d T=%d" % (L, r, S, T))
+    w, net, cond, u, model = _setup(L, r, S, dil, 1, T, seed=L + S, bias=0.3)
+    assert net.kernel_variant(1) == "multi_cu_chain"
+    y = net.generate(cond, u)
+    y2 = net.generate(cond, u)
+    lg = net.teacher_force(cond, y)
+    ws = net.new_workspace(1)
+    parts, a = [], 0
+    for b_ in (1, 2, 150, 151, T):
+        parts.append(net.generate(cond[:, a:b_].contiguous(), u[:, a:b_].contiguous(), workspace=ws, reset=(a == 0)))
+        a = b_
+    ws2 = net.new_workspace(1)
+    lgp = [net.teacher_force(cond[:, :77].contiguous(), y[:, :77].contiguous(), workspace=ws2, reset=True),
+           net.teacher_force(cond[:, 77:].contiguous(), y[:, 77:].contiguous(), workspace=ws2, reset=False)]
+    torch.cuda.synchronize()
+    assert net.status(ws) == 0 and net.status(ws2) == 0
+    assert torch.equal(y, y2)
+    assert torch.equal(torch.cat(parts, 1), y)
+    assert torch.equal(torch.cat(lgp, 1), lg)
+    y_np = y.cpu().numpy()
+    ys, lo, mg = oracle.run(model, cond.cpu().numpy()[0], u=u.cpu().numpy()[0], y_in=y_np[0])
+    err = np.abs(lg.cpu().numpy()[0] - lo).max()
+    ok = mg > MARGIN
+    mism = int(np.sum(ys[ok] != y_np[0][ok]))
+    _log("  max|dlogit|=%.3g confident=%d mismatches=%d" % (err, int(ok.sum()), mism))
+    assert err <= 1e-3 and mism == 0
+    # the generic kernel agrees on the same inputs
+    _force_stream(monkeypatch)
+    wn = _wn()
+    ref = wn.WaveNet(w, dil, weight_dtype="f32")
+    assert ref.kernel_variant(1) == "stream_l2"
+    lg_ref = ref.teacher_force(cond, y)
+    torch.cuda.synchronize()
+    assert float((lg_ref - lg).abs().max()) <= 1e-4
+    ref.close()
+    net.close()
