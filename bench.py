@@ -81,7 +81,18 @@ def main():
     ap.add_argument("--workload", default="l20_r64_b1")
     ap.add_argument("--cpu-steps", type=int, default=8000, help="oracle sample size (0 = skip)")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run one device-to-device copy of BYTES (calibrates HBM byte counters) and exit")
     args = ap.parse_args()
+    if args.copy_probe:
+        import torch
+        src = torch.ones(args.copy_probe // 4, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": args.copy_probe}))
+        return
     if args.gpus != 1:
         print("bench.py: this build runs on one GPU only (streams are independent; see DESIGN.md for how "
               "the batched workloads would shard); --gpus %d is not supported" % args.gpus, file=sys.stderr)

@@ -6,7 +6,7 @@
  * Appendix A.1: an input embedding of the previous mu-law sample, l gated layers
  * of width-2 dilated causal convolutions with residual and skip 1x1
  * projections, a relu -> 1x1 -> relu -> 1x1 head over a = 256 classes, a softmax
- * and a draw from it ("direct sampling", Appendix A, "Sampling from Output
+ * and a draw from it ("direct sampling", Appendix A.4, "Sampling from Output
  * Distribution").  Generation runs one sample per step; the per-layer
  * conditioning is an input computed beforehand, as in the paper's inference
  * benchmark (Section 5), which excludes the conditioning network.

@@ -175,7 +175,7 @@ static int oracle_step(const oracle_model *m, oracle_state *st, const float *con
 }
 
 /*
- * Direct sampling from softmax(logits) with the uniform u (Appendix A,
+ * Direct sampling from softmax(logits) with the uniform u (Appendix A.4,
  * "Sampling from Output Distribution": direct sampling; the softmax is the
  * max-subtracted form of the performance-model appendix).  Writes the
  * probabilities if prob != NULL and the margin if margin != NULL.

@@ -5,7 +5,7 @@
 // the draw that feeds the next step (Deep Voice, arXiv 1702.07825, Appendix A.1;
 // Section 5 explains why inference must go one timestep and one layer at a time).
 // The paper's GPU design keeps the weights in the register files of many SMs and
-// passes control round-robin between them through L2 (Appendix C).  This kernel
+// passes control round-robin between them through L2 (Appendix D).  This kernel
 // keeps that idea -- weights resident in VGPRs, nothing re-read from memory -- but
 // takes the off-chain work off the critical path, as the paper's CPU design does
 // with its auxiliary threads (Section 5.1):
