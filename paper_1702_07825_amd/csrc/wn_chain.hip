@@ -84,15 +84,6 @@ __device__ __forceinline__ float gsum(float v) {
   else if constexpr (N == 8) return gsum8(v);
   else return gsum16(v);
 }
-// Value held by the partner group of N lanes inside an aligned group of 2N lanes
-// (valid after a gsum<N>, when every lane of a group holds the same value).
-template <int N>
-__device__ __forceinline__ float partner(float v) {
-  if constexpr (N == 4) return dpp<0x141>(v);   // lane i <- 7 - i within 8
-  else if constexpr (N == 8) return dpp<0x140>(v);  // lane i <- 15 - i within 16
-  else return __shfl_xor(v, N, 64);
-}
-
 // Inclusive prefix sum over the 64 lanes of a wave: row scans by row_shr, then row broadcasts.
 __device__ __forceinline__ float wave_incl_scan(float v) {
   v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x111, 0xf, 0xf, true));
@@ -204,17 +195,30 @@ __device__ void poll2(const WnChainArgs& g, const Items a, const Items b, float*
 
 template <int R>
 struct ChainMap {
-  static constexpr int LPR1 = NT / (2 * R);  // lanes per W_cur / W_prev row
+  static constexpr int LPR1 = NT / (2 * R);  // lanes per W_prev row (aux CUs)
   static constexpr int KC1 = R / LPR1;       // weights per lane per row
+  static constexpr int LPRG = NT / R;        // lanes per gate pair (rows c and c + R of W_cur)
+  static constexpr int KCG = R / LPRG;       // inputs per lane for each of the two rows
   static constexpr int LPR2 = NT / R;        // lanes per W_res row
   static constexpr int KC2 = R / LPR2;
-  static_assert(LPR1 >= 1 && KC1 % 2 == 0 && KC2 >= 2, "unsupported R");
+  static_assert(LPR1 >= 1 && KC1 % 2 == 0 && KC2 >= 2 && KCG >= 2, "unsupported R");
 };
 
 template <int K>
 __device__ __forceinline__ float dot_lds(const float (&w)[K], const float* x) {
   float s0 = 0.f, s1 = 0.f;
-  if constexpr (K % 4 == 0) {
+  if constexpr (K % 8 == 0) {
+    float s2 = 0.f, s3 = 0.f;
+#pragma unroll
+    for (int i = 0; i < K; i += 4) {
+      const float4 v = *reinterpret_cast<const float4*>(x + i);
+      s0 = fmaf(w[i], v.x, s0);
+      s1 = fmaf(w[i + 1], v.y, s1);
+      s2 = fmaf(w[i + 2], v.z, s2);
+      s3 = fmaf(w[i + 3], v.w, s3);
+    }
+    return (s0 + s1) + (s2 + s3);
+  } else if constexpr (K % 4 == 0) {
 #pragma unroll
     for (int i = 0; i < K; i += 4) {
       const float4 v = *reinterpret_cast<const float4*>(x + i);
@@ -250,8 +254,7 @@ __device__ void chain_role(const WnChainArgs& g, const int c, float* dyn, Sync s
   float* hs = xs + R;                 // R
   float* pre = hs + R;                // NLC*2R pre-activations of this step
   float* lgp = pre + NLC * 2 * R;     // NHEAD*A partial logits (chain CU 0)
-  float* lg = lgp + NHEAD * A;        // A
-  float* ubuf = lg + A;               // UB uniforms (generation) / samples in (teacher forcing)
+  float* ubuf = lgp + NHEAD * A;      // UB uniforms (generation) / samples in (teacher forcing)
   int* ybuf = reinterpret_cast<int*>(ubuf + UB);  // UB drawn samples
   float* xbuf = reinterpret_cast<float*>(ybuf + UB);  // NLC*R x_{j-1} of this step (history writes)
   float* emb = xbuf + NLC * R;                         // A*R embedding table (chain CU 0)
@@ -261,28 +264,32 @@ __device__ void chain_role(const WnChainArgs& g, const int c, float* dyn, Sync s
   const bool lastc = (c + 1 == g.nch);
 
   // resident weights
-  const int g1 = tid / (2 * M::LPR1), half = (tid / M::LPR1) & 1, kq = tid % M::LPR1;
-  const int row1 = g1 + half * R;
+  // W_cur: lane group c (LPRG lanes) holds rows c and c + R, lane kq of it inputs kq*KCG .. +KCG
+  const int g1 = tid / M::LPRG, kq = tid % M::LPRG;
   const int row2 = tid / M::LPR2, kk = tid % M::LPR2;
-  float wc[NLC][M::KC1], wr[NLC][M::KC2];
+  float wc[NLC][2 * M::KCG], wr[NLC][M::KC2];
   const float* Wc = static_cast<const float*>(g.w.w_cur);
   const float* Wr = static_cast<const float*>(g.w.w_res);
 #pragma unroll
   for (int l = 0; l < NLC; ++l) {
     const int j = j0 + (l < nl ? l : 0);
 #pragma unroll
-    for (int i = 0; i < M::KC1; ++i) wc[l][i] = Wc[((size_t)j * 2 * R + row1) * R + kq * M::KC1 + i];
+    for (int i = 0; i < M::KCG; ++i) {
+      wc[l][i] = Wc[((size_t)j * 2 * R + g1) * R + kq * M::KCG + i];
+      wc[l][M::KCG + i] = Wc[((size_t)j * 2 * R + g1 + R) * R + kq * M::KCG + i];
+    }
 #pragma unroll
     for (int i = 0; i < M::KC2; ++i) wr[l][i] = Wr[((size_t)j * R + row2) * R + kk * M::KC2 + i];
   }
   for (int i = tid; i < nl * R; i += NT) bres[i] = g.w.b_res[(size_t)j0 * R + i];
-  float bemb = 0.f, bout = 0.f;
+  float bemb = 0.f;
+  float4 bout4 = make_float4(0.f, 0.f, 0.f, 0.f);  // B_out of the 4 logits lane l of wave 0 draws from
   if (lastc) {
     const float* Wk = static_cast<const float*>(g.w.w_skip) + (size_t)(L - 1) * S * R;
     for (int i = tid; i < S * R; i += NT) wsk[i] = Wk[i];
   }
   if (first) {
-    if (tid < A) bout = g.w.b_out[tid];
+    if (wave == 0) bout4 = *reinterpret_cast<const float4*>(g.w.b_out + 4 * lane);
     const float* E = static_cast<const float*>(g.w.embed);
     for (int i = tid; i < A * R; i += NT) emb[i] = E[i];
     if (tid < R) bemb = g.w.b_embed[tid];
@@ -300,15 +307,27 @@ __device__ void chain_role(const WnChainArgs& g, const int c, float* dyn, Sync s
   }
   lds_barrier();
 
-  // Draw (generation) or read (teacher forcing) the sample of global step ts from lg[]; one wave.
+  // One wave sums the head's partial logits of global step ts (lane l owns logits 4l..4l+3),
+  // writes them out when teacher forcing, and draws (generation) or reads (teacher forcing)
+  // the sample.
   auto sample_step = [&](int64_t ts) {
     if (wave == 0) {
+      float4 lv = bout4;
+#pragma unroll
+      for (int h = 0; h < NHEAD; ++h) {
+        const float4 p = *reinterpret_cast<const float4*>(lgp + h * A + 4 * lane);
+        lv.x += p.x;
+        lv.y += p.y;
+        lv.z += p.z;
+        lv.w += p.w;
+      }
       int y;
       if constexpr (TF) {
+        *reinterpret_cast<float4*>(g.io.logits + (size_t)(ts - tg0) * A + 4 * lane) = lv;
         y = reinterpret_cast<const int*>(ubuf)[ts - ub0];
         y = y < 0 ? 0 : (y > A - 1 ? A - 1 : y);
       } else {
-        const float l0 = lg[4 * lane], l1 = lg[4 * lane + 1], l2 = lg[4 * lane + 2], l3 = lg[4 * lane + 3];
+        const float l0 = lv.x, l1 = lv.y, l2 = lv.z, l3 = lv.w;
         const float m = wave_max(fmaxf(fmaxf(l0, l1), fmaxf(l2, l3)));
         const float e0 = expf_fast(l0 - m), e1 = expf_fast(l1 - m), e2 = expf_fast(l2 - m), e3 = expf_fast(l3 - m);
         const float s0 = e0, s1 = s0 + e1, s2 = s1 + e2, s3 = s2 + e3;
@@ -330,17 +349,6 @@ __device__ void chain_role(const WnChainArgs& g, const int c, float* dyn, Sync s
   // The head's partial logits of step ts (tag ts + 1).
   auto logit_items = [&](int64_t ts) {
     return Items{g.mb_logit + (size_t)(ts & 1) * A, A, 2 * A, NHEAD * A, lgp, (unsigned)(ts + 1)};
-  };
-  // Sum the polled partial logits of step ts into lg[]; write them out when teacher forcing.
-  auto sum_logits = [&](int64_t ts) {
-    if (tid < A) {
-      float v = bout;
-#pragma unroll
-      for (int h = 0; h < NHEAD; ++h) v += lgp[h * A + tid];
-      lg[tid] = v;
-      if constexpr (TF) g.io.logits[(size_t)(ts - tg0) * A + tid] = v;
-    }
-    lds_barrier();
   };
   // Move staged samples to the output and stage the next block of inputs.
   auto roll_buffers = [&](int64_t next0) {
@@ -373,7 +381,6 @@ __device__ void chain_role(const WnChainArgs& g, const int c, float* dyn, Sync s
         poll2(g, logit_items(t - 1), pre_items, dyn, sy);
         lds_barrier();
         if (sy.failed()) return;
-        sum_logits(t - 1);
         if (t - 1 - ub0 >= UB) roll_buffers(t - 1);
         sample_step(t - 1);
       } else {
@@ -399,13 +406,45 @@ __device__ void chain_role(const WnChainArgs& g, const int c, float* dyn, Sync s
     for (int l = 0; l < NLC; ++l) {
       if (l < nl) {
         const int j = j0 + l;
-        // a = W_cur x + pre ; h = tanh(a[0:R]) * sigmoid(a[R:2R])
-        float s = gsum<M::LPR1>(dot_lds<M::KC1>(wc[l], xs + kq * M::KC1));
-        const float o = partner<M::LPR1>(s);
-        const float ah = (half ? o : s) + pre[l * 2 * R + g1];
-        const float ag = (half ? s : o) + pre[l * 2 * R + g1 + R];
+        // a = W_cur x + pre ; h = tanh(a[0:R]) * sigmoid(a[R:2R]).  Each lane has both rows of its
+        // pair; lane 0 of the group starts its partial sums from pre, so pre joins the reduction.
+        float ah, ag;
+        {
+          float sh0 = 0.f, sh1 = 0.f, sg0 = 0.f, sg1 = 0.f;
+          if (kq == 0) {
+            sh0 = pre[l * 2 * R + g1];
+            sg0 = pre[l * 2 * R + g1 + R];
+          }
+          const float* xk = xs + kq * M::KCG;
+          if constexpr (M::KCG % 4 == 0) {
+#pragma unroll
+            for (int i = 0; i < M::KCG; i += 4) {
+              const float4 v = *reinterpret_cast<const float4*>(xk + i);
+              sh0 = fmaf(wc[l][i], v.x, sh0);
+              sh1 = fmaf(wc[l][i + 1], v.y, sh1);
+              sh0 = fmaf(wc[l][i + 2], v.z, sh0);
+              sh1 = fmaf(wc[l][i + 3], v.w, sh1);
+              sg0 = fmaf(wc[l][M::KCG + i], v.x, sg0);
+              sg1 = fmaf(wc[l][M::KCG + i + 1], v.y, sg1);
+              sg0 = fmaf(wc[l][M::KCG + i + 2], v.z, sg0);
+              sg1 = fmaf(wc[l][M::KCG + i + 3], v.w, sg1);
+            }
+          } else {
+            static_assert(M::KCG % 2 == 0, "inputs per lane must be even");
+#pragma unroll
+            for (int i = 0; i < M::KCG; i += 2) {
+              const float2 v = *reinterpret_cast<const float2*>(xk + i);
+              sh0 = fmaf(wc[l][i], v.x, sh0);
+              sh1 = fmaf(wc[l][i + 1], v.y, sh1);
+              sg0 = fmaf(wc[l][M::KCG + i], v.x, sg0);
+              sg1 = fmaf(wc[l][M::KCG + i + 1], v.y, sg1);
+            }
+          }
+          ah = gsum<M::LPRG>(sh0 + sh1);
+          ag = gsum<M::LPRG>(sg0 + sg1);
+        }
         const float h = tanh_f(ah) * sigmoid_f(ag);
-        if (tid % (2 * M::LPR1) == 0) {
+        if (kq == 0) {
           hs[g1] = h;
         }
         lds_barrier();
@@ -420,11 +459,11 @@ __device__ void chain_role(const WnChainArgs& g, const int c, float* dyn, Sync s
         }
         // x_j = x_{j-1} + W_res h + B_res (x_l feeds nothing); x_{j-1} is kept for the history
         if (j < L - 1) {
+          const float xo = xs[row2], bo = bres[l * R + row2];
           const float r = gsum<M::LPR2>(dot_lds<M::KC2>(wr[l], hs + kk * M::KC2));
           if (kk == 0) {
-            const float xo = xs[row2];
             xbuf[l * R + row2] = xo;
-            xs[row2] = xo + r + bres[l * R + row2];
+            xs[row2] = xo + r + bo;
           }
         } else if (tid < R) {
           xbuf[l * R + tid] = xs[tid];
@@ -475,7 +514,6 @@ __device__ void chain_role(const WnChainArgs& g, const int c, float* dyn, Sync s
       poll2(g, logit_items(tl), no_items(), dyn, sy);
       lds_barrier();
       if (sy.failed()) return;
-      sum_logits(tl);
       if (tl - ub0 >= UB) roll_buffers(tl);
       sample_step(tl);
       lds_barrier();
@@ -634,7 +672,7 @@ template <int R, int S>
 hipError_t launch_chain_rs(const WnChainArgs& g, bool teacher, hipStream_t stream) {
   constexpr int NLC = chain_nlc<R>();
   const size_t chain_lds =
-      ((size_t)2 * R + NLC * 2 * R + NHEAD * A + A + 2 * UB + 2 * NLC * R + (size_t)A * R + (size_t)S * R) *
+      ((size_t)2 * R + NLC * 2 * R + NHEAD * A + 2 * UB + 2 * NLC * R + (size_t)A * R + (size_t)S * R) *
       sizeof(float);
   const size_t head_lds = ((size_t)g.d.L * S + S + HR) * sizeof(float);
   const size_t aux_lds = (size_t)4 * R * sizeof(float);
