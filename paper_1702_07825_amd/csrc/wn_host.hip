@@ -9,7 +9,7 @@
 #include <string>
 #include <vector>
 
-enum WnVariant { WN_VARIANT_STREAM = 0, WN_VARIANT_CHAIN = 1 };
+enum WnVariant { WN_VARIANT_STREAM = 0, WN_VARIANT_CHAIN = 1, WN_VARIANT_GROUP = 2 };
 
 struct wn_handle {
   int device = 0;
@@ -23,7 +23,21 @@ struct wn_handle {
   bool chain_ok = false;  // the multi-CU kernel can serve B = 1
   int nch = 0;            // its chain CUs
   int layer_begin[WN_MAX_CHAIN + 1] = {};
+  bool group_ok = false;  // the batched MFMA kernel serves every B
+  void* dpack = nullptr;  // its packed bf16 weight tiles
 };
+
+// Round fp32 to bfloat16, nearest even (NaN stays NaN).
+uint16_t wn_to_bf16(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  if ((u & 0x7f800000u) == 0x7f800000u) {
+    if (u & 0x007fffffu) u |= 0x00400000u;
+    return (uint16_t)(u >> 16);
+  }
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
 
 namespace {
 
@@ -37,18 +51,6 @@ int fail(int code, const std::string& msg) {
 int hip_fail(hipError_t e, const char* what) {
   g_err = std::string(what) + ": " + hipGetErrorString(e);
   return WN_EHIP;
-}
-
-// Round fp32 to bfloat16, nearest even (NaN stays NaN).
-uint16_t to_bf16(float f) {
-  uint32_t u;
-  std::memcpy(&u, &f, 4);
-  if ((u & 0x7f800000u) == 0x7f800000u) {
-    if (u & 0x007fffffu) u |= 0x00400000u;
-    return (uint16_t)(u >> 16);
-  }
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
 }
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -70,10 +72,13 @@ class DeviceScope {
   bool ok_ = false;
 };
 
-int variant_for(const wn_handle* h, int B) { return (B == 1 && h->chain_ok) ? WN_VARIANT_CHAIN : WN_VARIANT_STREAM; }
+int variant_for(const wn_handle* h, int B) {
+  if (B == 1 && h->chain_ok) return WN_VARIANT_CHAIN;
+  return h->group_ok ? WN_VARIANT_GROUP : WN_VARIANT_STREAM;
+}
 
-// Workspace: status word, per-stream state, then either fp32 histories (stream kernel) or
-// tagged 64-bit histories followed by the inter-CU mailboxes (multi-CU kernel).
+// Workspace: status word, per-stream state, then either fp32 histories (per-stream and batched
+// kernels) or tagged 64-bit histories followed by the inter-CU mailboxes (multi-CU kernel).
 struct WsLayout {
   size_t status_off, state_off, hist_off, mb_off, mb_words, total;
 };
@@ -151,6 +156,27 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
     }
     const hipError_t e = wn_chain_launch(g, teacher, st);
     if (e != hipSuccess) return hip_fail(e, "multi-CU kernel launch");
+    return WN_OK;
+  }
+  if (variant_for(h, B) == WN_VARIANT_GROUP) {
+    WnGroupArgs g{};
+    g.d = h->dims;
+    g.w = h->w;
+    g.packed = h->dpack;
+    g.io.cond = cond;
+    g.io.u = u;
+    g.io.y_in = y_in;
+    g.io.y_out = y_out;
+    g.io.logits = logits;
+    g.io.B = B;
+    g.io.T = T;
+    g.io.reset = reset;
+    g.io.init_sample = h->init_sample;
+    g.ws.status = reinterpret_cast<int32_t*>(base + l.status_off);
+    g.ws.state = reinterpret_cast<int64_t*>(base + l.state_off);
+    g.ws.hist = reinterpret_cast<float*>(base + l.hist_off);
+    const hipError_t e = wn_group_launch(g, teacher, st);
+    if (e != hipSuccess) return hip_fail(e, "batched kernel launch");
     return WN_OK;
   }
   WnStreamArgs args{};
@@ -248,7 +274,7 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
   for (const Arr& a : arrs) {
     if (a.matrix && bf) {
       uint16_t* d = reinterpret_cast<uint16_t*>(host.data() + a.off);
-      for (size_t i = 0; i < a.n; ++i) d[i] = to_bf16(a.src[i]);
+      for (size_t i = 0; i < a.n; ++i) d[i] = wn_to_bf16(a.src[i]);
     } else {
       std::memcpy(host.data() + a.off, a.src, a.n * 4);
     }
@@ -294,6 +320,23 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
     for (int c = 0; c < h->nch; ++c) h->layer_begin[c + 1] = h->layer_begin[c] + base + (c < extra ? 1 : 0);
     h->chain_ok = true;
   }
+  // The batched MFMA kernel needs bf16 weights, r = 64 and its LDS footprint on one CU.
+  int lds_max = 0;
+  (void)hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device);
+  if (want_chain && bf && wn_group_supported(R, S, L) && wn_group_lds_bytes(L, S) + 256 <= (size_t)lds_max) {
+    const std::vector<uint16_t> tiles =
+        wn_group_pack(L, R, S, w->w_prev, w->w_cur, w->w_res, w->w_skip, w->w_relu, w->w_out);
+    e = hipMalloc(&h->dpack, tiles.size() * sizeof(uint16_t));
+    if (e == hipSuccess) e = hipMemcpy(h->dpack, tiles.data(), tiles.size() * sizeof(uint16_t), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      if (h->dpack) (void)hipFree(h->dpack);
+      (void)hipFree(h->dmem);
+      delete h;
+      return e == hipErrorOutOfMemory ? fail(WN_ENOMEM, "hipMalloc of packed weights")
+                                      : hip_fail(e, "packed weights upload");
+    }
+    h->group_ok = true;
+  }
   *out = h;
   return WN_OK;
 }
@@ -333,7 +376,11 @@ int wn_status(wn_handle* h, const void* workspace, void* stream) {
 
 const char* wn_kernel_variant(const wn_handle* h, int32_t B) {
   if (!h || B < 1) return "";
-  return variant_for(h, B) == WN_VARIANT_CHAIN ? "multi_cu_chain" : "stream_l2";
+  switch (variant_for(h, B)) {
+    case WN_VARIANT_CHAIN: return "multi_cu_chain";
+    case WN_VARIANT_GROUP: return "mfma_group";
+    default: return "stream_l2";
+  }
 }
 
 void wn_destroy(wn_handle* h) {
@@ -341,6 +388,7 @@ void wn_destroy(wn_handle* h) {
   {
     DeviceScope scope(h->device);
     if (h->dmem) (void)hipFree(h->dmem);
+    if (h->dpack) (void)hipFree(h->dpack);
   }
   delete h;
 }

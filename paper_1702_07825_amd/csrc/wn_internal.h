@@ -2,6 +2,7 @@
 #pragma once
 #include <hip/hip_runtime.h>
 #include <cstdint>
+#include <vector>
 
 #define WN_MAX_LAYERS 64
 #define WN_A 256
@@ -91,3 +92,25 @@ int wn_chain_num_cus(int L, int R);
 size_t wn_chain_mailbox_words(int L, int R, int S);
 hipError_t wn_chain_reset(unsigned long long* words, size_t n, int* status, hipStream_t stream);
 hipError_t wn_chain_launch(const WnChainArgs& g, bool teacher, hipStream_t stream);
+
+// Batched kernel for bf16 weights: one workgroup per group of 16 streams, MFMA for every
+// product, weights pre-packed into MFMA operand tiles (wn_group_pack) and streamed from L2.
+struct WnGroupArgs {
+  WnDims d;
+  WnDevWeights w;     // biases and the embedding (bf16) are read from here
+  const void* packed; // tiles from wn_group_pack, device copy
+  WnIO io;
+  WnWorkspace ws;     // same layout as the per-stream kernel's
+};
+#define WN_GROUP_MAX_LAYERS 40
+bool wn_group_supported(int R, int S, int L);
+size_t wn_group_lds_bytes(int L, int S);
+// Packs W_prev/W_cur/W_res/W_skip of every layer and the two head matrices (fp32 host arrays
+// in the wn_weights layout) into bf16 tiles, the order the kernel streams them in.
+std::vector<uint16_t> wn_group_pack(int L, int R, int S, const float* w_prev, const float* w_cur,
+                                    const float* w_res, const float* w_skip, const float* w_relu,
+                                    const float* w_out);
+hipError_t wn_group_launch(const WnGroupArgs& g, bool teacher, hipStream_t stream);
+
+// fp32 -> bf16 bit pattern, round to nearest even (NaN stays NaN).
+uint16_t wn_to_bf16(float f);
