@@ -7,21 +7,26 @@
 //
 //   phase A  waves 0-3: gate.  Wave g computes the tanh rows 16g..16g+15 of a and the matching
 //            sigmoid rows r+16g.., so h = tanh * sigmoid needs no exchange between waves.
-//            wave 7: writes x_{j-1}[t] to the dilation history, moves the history and
-//            conditioning rows of the next layer (loaded a layer earlier) into LDS and issues
-//            the loads for the layer after that.  Only this wave touches HBM, so the in-order
-//            completion counters of the weight-loading waves never wait on an HBM access.
-//   phase B  waves 0-3: x += W_res h + B_res.   waves 4-6: q += W_skip h (q in MFMA accumulators).
+//            wave 7: moves the history and conditioning rows of the next layer (loaded a layer
+//            earlier) into LDS, writes x_{j-1}[t] to the dilation history and issues the loads
+//            for the layer after that.  Only this wave touches HBM, and it alone stores to
+//            global memory, so the weight-loading waves never wait on an HBM access or a store.
+//   phase B  waves 0-3: x += W_res h + B_res (each lane keeps its four rows of x in registers).
+//            waves 4-6: q += W_skip h (q in MFMA accumulators).
 //
 // After the last layer: z_s = relu(q + B_skip), z_a = relu(W_relu z_s + B_relu), logits =
-// W_out z_a + B_out (all 8 waves), then the softmax and draw (two streams per wave), which also
-// lays out the next step's x0 = E[y] + B_embed.
+// W_out z_a + B_out (all 8 waves; the head's tiles are loaded during the last layer), then the
+// softmax and draw (two streams per wave), which also lays out the next step's x0 = E[y] +
+// B_embed.
 //
 // Weights are packed on the host into MFMA A-operand tiles (16 rows x 32 inputs of bf16, 1 KB,
 // one 16-byte load per lane) and streamed from L2 every step; each wave issues the loads of the
-// next layer's tiles before it waits for the current ones.  Activations stay fp32 in LDS; a B
-// operand is split into bf16 hi + lo and both parts are multiplied, so a product keeps about 16
-// bits of the activation (the weights are exactly bf16).  Accumulation is fp32.
+// next layer's tiles before it waits for the current ones.  An activation that feeds a product
+// is kept as a pair of bf16 values, hi = bf16(v) and lo = bf16(v - hi), and both parts are
+// multiplied, so a product sees about 16 bits of the activation (the weights are exactly bf16);
+// accumulation, the gate, the residual sum and the softmax are fp32.  Activation rows in LDS
+// and the dilation histories in the workspace hold the pairs: a row of K values is K hi parts
+// followed by K lo parts.
 #include "wn_internal.h"
 #include "wn_wave.h"
 
@@ -33,43 +38,59 @@ namespace {
 using namespace wnk;
 
 constexpr int NT = 512;
-constexpr int G = 16;      // streams per workgroup (the MFMA N dimension)
-constexpr int R = 64;      // residual channels
+constexpr int G = 16;  // streams per workgroup (the MFMA N dimension)
+constexpr int R = 64;  // residual channels
 constexpr int A = WN_A;
-constexpr int PX = R + 4;  // padded LDS rows
-constexpr int PC = 2 * R + 4;
+constexpr int PC = 2 * R + 4;  // fp32 row pitches in LDS
 constexpr int PA = A + 4;
-constexpr int PF = 12;     // 16-byte values each lane prefetches per layer
+constexpr int SR = 2 * R + 8;  // split-row pitch of an r-vector, in 16-bit units
+constexpr int SA = 2 * A + 8;
 
+typedef unsigned short u16;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ unsigned short bf16_bits(float v) {  // nearest even; activations are finite
-  unsigned u = __float_as_uint(v);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (unsigned short)(u >> 16);
+// bf16 of a and b (nearest even; v_cvt_pk_bf16_f32), a in the low half
+__device__ __forceinline__ unsigned pack_bf16(float a, float b) {
+  const bf16x2 h = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(unsigned, h);
 }
-__device__ __forceinline__ float bf16_val(unsigned short b) { return __uint_as_float((unsigned)b << 16); }
-
-// B operand of a 16x16x32 MFMA for one stream: 8 consecutive fp32 activations as hi = bf16(v)
-// and lo = bf16(v - hi).
-__device__ __forceinline__ void split8(const float* p, bf16x8& hi, bf16x8& lo) {
-  const float4 a = *reinterpret_cast<const float4*>(p);
-  const float4 b = *reinterpret_cast<const float4*>(p + 4);
-  const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const unsigned short h = bf16_bits(v[e]);
-    hi[e] = __builtin_bit_cast(__bf16, h);
-    lo[e] = __builtin_bit_cast(__bf16, bf16_bits(v[e] - bf16_val(h)));
-  }
+__device__ __forceinline__ float low_bf16(unsigned p) { return __uint_as_float(p << 16); }
+__device__ __forceinline__ float high_bf16(unsigned p) { return __uint_as_float(p & 0xffff0000u); }
+__device__ __forceinline__ float bf16_val(u16 b) { return __uint_as_float((unsigned)b << 16); }
+// hi / lo parts of four consecutive values
+__device__ __forceinline__ void split4(float4 v, uint2& hi, uint2& lo) {
+  const unsigned h01 = pack_bf16(v.x, v.y), h23 = pack_bf16(v.z, v.w);
+  hi = make_uint2(h01, h23);
+  lo = make_uint2(pack_bf16(v.x - low_bf16(h01), v.y - high_bf16(h01)),
+                  pack_bf16(v.z - low_bf16(h23), v.w - high_bf16(h23)));
 }
-__device__ __forceinline__ f32x4 mfma2(uint4 w, const bf16x8& hi, const bf16x8& lo, f32x4 acc) {
+// hi / lo parts of one value, as 16-bit patterns
+__device__ __forceinline__ void split1(float v, u16& hi, u16& lo) {
+  const unsigned p = pack_bf16(v, 0.f);
+  hi = (u16)p;
+  lo = (u16)pack_bf16(v - low_bf16(p), 0.f);
+}
+// hi / lo parts of four rows m0..m0+3 into a split row of K values
+template <int K>
+__device__ __forceinline__ void store_split4(u16* row, int m0, float4 v) {
+  uint2 hi, lo;
+  split4(v, hi, lo);
+  *reinterpret_cast<uint2*>(row + m0) = hi;
+  *reinterpret_cast<uint2*>(row + K + m0) = lo;
+}
+// Product of a weight tile with the B operand taken from a split row: inputs k0 .. k0 + 7 of
+// this lane's stream, hi and lo parts.
+template <int K>
+__device__ __forceinline__ f32x4 mfma_row(u32x4 w, const u16* row, int k0, f32x4 acc) {
   const bf16x8 a = __builtin_bit_cast(bf16x8, w);
+  const bf16x8 hi = *reinterpret_cast<const bf16x8*>(row + k0);
+  const bf16x8 lo = *reinterpret_cast<const bf16x8*>(row + K + k0);
   acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, hi, acc, 0, 0, 0);
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, lo, acc, 0, 0, 0);
 }
-__device__ __forceinline__ float4 as_f4(uint4 v) { return __builtin_bit_cast(float4, v); }
 
 // Tile order of the packed weights, in 1 KB blocks (64 lanes x 16 bytes).
 template <int S>
@@ -78,25 +99,25 @@ struct Pack {
   static constexpr int KTR = R / 32;
   static constexpr int KTH = S / 32;
   static constexpr int KTO = A / 32;
-  static constexpr int GATE = 0;                              // [2R x 2R]: block mt * KTG + kt
-  static constexpr int RES = GATE + (2 * R / 16) * KTG;       // [R x R]
-  static constexpr int SKIP = RES + (R / 16) * KTR;           // [S x R]
-  static constexpr int LAYER = SKIP + (S / 16) * KTR;         // blocks per layer
-  static constexpr int NSKT = S / 16;                         // skip row tiles
-  static constexpr int SKW = (NSKT + 2) / 3;                  // skip row tiles per skip wave
-  static_assert(2 * KTG + KTR <= PF && SKW * KTR <= PF, "prefetch buffer too small");
+  static constexpr int GATE = 0;                         // [2R x 2R]: block mt * KTG + kt
+  static constexpr int RES = GATE + (2 * R / 16) * KTG;  // [R x R]
+  static constexpr int SKIP = RES + (R / 16) * KTR;      // [S x R]
+  static constexpr int LAYER = SKIP + (S / 16) * KTR;    // blocks per layer
+  static constexpr int NSKT = S / 16;                    // skip row tiles
+  static constexpr int SKW = (NSKT + 2) / 3;             // skip row tiles per skip wave
+  static constexpr int SS = 2 * S + 8;                   // split-row pitch of an s-vector
 };
 
 template <int S>
-constexpr size_t lds_floats(int L) {
-  return (size_t)G * PX * 4 + (size_t)2 * G * PC + (size_t)G * (S + 4) + (size_t)2 * G * PA +
-         (size_t)L * 3 * R + R + S + 2 * A + (size_t)A * R / 2;
+constexpr size_t lds_bytes(int L) {
+  return 4 * ((size_t)2 * G * PC + (size_t)G * PA + (size_t)L * 3 * R + R + S + 2 * A) +
+         2 * ((size_t)4 * G * SR + (size_t)G * Pack<S>::SS + (size_t)G * SA + (size_t)A * R);
 }
 
 template <int S, bool TF>
 __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
   using P = Pack<S>;
-  constexpr int PS = S + 4;
+  constexpr int SS = P::SS;
   const WnDims& D = g.d;
   const int L = D.L;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -106,25 +127,36 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
   const int n = lane & 15, quad = lane >> 4;  // MFMA column (stream) and row quad of this lane
 
   extern __shared__ __align__(16) float sm[];
-  float* X = sm;                  // [G][PX]  x_{j-1}, updated in place
-  float* H = X + G * PX;          // [G][PX]  h_j
-  float* XP = H + G * PX;         // [2][G][PX] history rows x_{j-1}[t - d_j] (position parity)
-  float* CD = XP + 2 * G * PX;    // [2][G][PC] conditioning rows
-  float* ZS = CD + 2 * G * PC;    // [G][PS]  relu(q + B_skip)
-  float* ZA = ZS + G * PS;        // [G][PA]
-  float* LG = ZA + G * PA;        // [G][PA]  logits
-  float* BG = LG + G * PA;        // [L][2R]
-  float* BR = BG + L * 2 * R;     // [L][R]
-  float* BE = BR + L * R;         // [R]
-  float* BS = BE + R;             // [S]
-  float* BRL = BS + S;            // [A]
-  float* BO = BRL + A;            // [A]
-  unsigned short* EMB = reinterpret_cast<unsigned short*>(BO + A);  // [A][R] bf16
+  float* CD = sm;                // [2][G][PC] conditioning rows (layer parity)
+  float* LG = CD + 2 * G * PC;   // [G][PA]    logits
+  float* BG = LG + G * PA;       // [L][2R]
+  float* BR = BG + L * 2 * R;    // [L][R]
+  float* BE = BR + L * R;        // [R]
+  float* BS = BE + R;            // [S]
+  float* BRL = BS + S;           // [A]
+  float* BO = BRL + A;           // [A]
+  u16* XS = reinterpret_cast<u16*>(BO + A);  // [G][SR]    x_{j-1}, split
+  u16* HS = XS + G * SR;                      // [G][SR]    h_j, split
+  u16* XP = HS + G * SR;                      // [2][G][SR] history rows x_{j-1}[t - d_j] (layer parity)
+  u16* ZS = XP + 2 * G * SR;                  // [G][SS]    relu(q + B_skip), split
+  u16* ZA = ZS + G * SS;                      // [G][SA]    z_a, split
+  u16* EMB = ZA + G * SA;                     // [A][R]     embedding (bf16)
   __shared__ int s_y[G];
   __shared__ float s_u[G];
   __shared__ int s_yin[G];
+  __shared__ int s_slot[WN_GROUP_MAX_LAYERS];  // history slot (t mod d_j) of the next write of layer j
 
-  const uint4* pk = static_cast<const uint4*>(g.packed);
+  const u32x4* pk = static_cast<const u32x4*>(g.packed);
+  const unsigned loff = (unsigned)lane * 16u;  // this lane's bytes within a 1 KB tile
+  // Opaque copies of the tile base and the lane offset keep the compiler from hoisting the
+  // addresses of loop-invariant tiles (head, first layer) out of the loops, where they would
+  // hold registers for the whole call; the load takes the base in SGPRs and the lane offset.
+  auto tile = [&](size_t blk) __attribute__((always_inline)) {
+    const char* b = reinterpret_cast<const char*>(pk + blk * 64);
+    unsigned o = loff;
+    asm volatile("" : "+s"(b), "+v"(o));
+    return *reinterpret_cast<const u32x4*>(b + o);
+  };
   int64_t tg0 = 0;
   {
     // every stream of a call has taken the same number of steps
@@ -136,6 +168,7 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
       s_y[tid] = y < 0 ? 0 : (y > A - 1 ? A - 1 : y);
     }
   }
+  if (tid < L) s_slot[tid] = (int)(tg0 % D.dil[tid]);
   for (int i = tid; i < L * 2 * R; i += NT) BG[i] = g.w.b_gate[i];
   for (int i = tid; i < L * R; i += NT) BR[i] = g.w.b_res[i];
   for (int i = tid; i < R; i += NT) BE[i] = g.w.b_embed[i];
@@ -143,7 +176,7 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
   for (int i = tid; i < A; i += NT) BRL[i] = g.w.b_relu[i];
   for (int i = tid; i < A; i += NT) BO[i] = g.w.b_out[i];
   {
-    const unsigned short* E = static_cast<const unsigned short*>(g.w.embed);
+    const u16* E = static_cast<const u16*>(g.w.embed);
     for (int i = tid; i < A * R; i += NT) EMB[i] = E[i];
   }
   if (g.io.reset) {
@@ -156,7 +189,7 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
   __syncthreads();  // also orders the history zeroing before the loader's reads
   for (int i = tid; i < G * R; i += NT) {
     const int nn = i / R, c = i % R;
-    X[nn * PX + c] = bf16_val(EMB[s_y[nn] * R + c]) + BE[c];
+    split1(bf16_val(EMB[s_y[nn] * R + c]) + BE[c], XS[nn * SR + c], XS[nn * SR + R + c]);
   }
 
   const int64_t nq = (int64_t)T * L;  // positions (step, layer) of this call
@@ -177,56 +210,60 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
     }
   };
 
-  // After the last layer of step tl: the head (every wave: row tiles 2w and 2w + 1 of W_relu,
-  // then of W_out), the draw (streams 2w and 2w + 1) and the next step's x0.  Three barriers.
-  // Results stay in LDS (logits in LG, samples in s_y); the loader wave writes them out.
-  auto head_and_draw = [&](int64_t tl) __attribute__((always_inline)) {
+  // Head tiles of this wave: row tiles 2w and 2w + 1 of W_relu (issued during the last layer)
+  // and of W_out (issued after the W_relu products).
+  constexpr size_t HEAD1 = 0, HEAD2 = (size_t)(A / 16) * P::KTH;
+  const size_t hbase = (size_t)L * P::LAYER;
+  auto issue_head1 = [&](u32x4 (&w)[2 * P::KTH]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int k = 0; k < 2; ++k)
+#pragma unroll
+      for (int kt = 0; kt < P::KTH; ++kt) w[k * P::KTH + kt] = tile(hbase + HEAD1 + (2 * wave + k) * P::KTH + kt);
+  };
+  // After the last layer of step tl: the head, the draw (streams 2w and 2w + 1) and the next
+  // step's x0.  Three barriers.  Results stay in LDS (logits in LG, samples in s_y); the loader
+  // wave writes them out.
+  auto head_and_draw = [&](int64_t tl, const u32x4 (&w1)[2 * P::KTH]) __attribute__((always_inline)) {
+    u32x4 w2[2 * P::KTO];
     {
-      const uint4* hw = pk + (size_t)L * P::LAYER * 64 + lane;
-      uint4 w[2 * P::KTH];
+      f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+      const u16* row = ZS + n * SS;
+#pragma unroll
+      for (int kt = 0; kt < P::KTH; ++kt) {
+        acc[0] = mfma_row<S>(w1[kt], row, kt * 32 + quad * 8, acc[0]);
+        acc[1] = mfma_row<S>(w1[P::KTH + kt], row, kt * 32 + quad * 8, acc[1]);
+      }
+      // W_out tiles: issued once the W_relu tiles are consumed (the empty asm keeps the loads
+      // behind the products), so the two sets never hold registers at the same time
+      asm volatile("" : "+v"(acc[0]), "+v"(acc[1])::"memory");
 #pragma unroll
       for (int k = 0; k < 2; ++k)
 #pragma unroll
-        for (int kt = 0; kt < P::KTH; ++kt) w[k * P::KTH + kt] = hw[((2 * wave + k) * P::KTH + kt) * 64];
-      f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-#pragma unroll
-      for (int kt = 0; kt < P::KTH; ++kt) {
-        bf16x8 hi, lo;
-        split8(ZS + n * PS + kt * 32 + quad * 8, hi, lo);
-        acc[0] = mfma2(w[kt], hi, lo, acc[0]);
-        acc[1] = mfma2(w[P::KTH + kt], hi, lo, acc[1]);
-      }
+        for (int kt = 0; kt < P::KTO; ++kt) w2[k * P::KTO + kt] = tile(hbase + HEAD2 + (2 * wave + k) * P::KTO + kt);
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
         const int m0 = (2 * wave + k) * 16 + quad * 4;
         const float4 b = *reinterpret_cast<const float4*>(BRL + m0);
-        *reinterpret_cast<float4*>(ZA + n * PA + m0) =
-            make_float4(fmaxf(acc[k][0] + b.x, 0.f), fmaxf(acc[k][1] + b.y, 0.f), fmaxf(acc[k][2] + b.z, 0.f),
-                        fmaxf(acc[k][3] + b.w, 0.f));
+        store_split4<A>(ZA + n * SA, m0,
+                        make_float4(fmaxf(acc[k][0] + b.x, 0.f), fmaxf(acc[k][1] + b.y, 0.f),
+                                    fmaxf(acc[k][2] + b.z, 0.f), fmaxf(acc[k][3] + b.w, 0.f)));
       }
     }
     lds_barrier();
     {
-      const uint4* ow = pk + ((size_t)L * P::LAYER + (A / 16) * P::KTH) * 64 + lane;
-      uint4 w[2 * P::KTO];
-#pragma unroll
-      for (int k = 0; k < 2; ++k)
-#pragma unroll
-        for (int kt = 0; kt < P::KTO; ++kt) w[k * P::KTO + kt] = ow[((2 * wave + k) * P::KTO + kt) * 64];
       f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+      const u16* row = ZA + n * SA;
 #pragma unroll
       for (int kt = 0; kt < P::KTO; ++kt) {
-        bf16x8 hi, lo;
-        split8(ZA + n * PA + kt * 32 + quad * 8, hi, lo);
-        acc[0] = mfma2(w[kt], hi, lo, acc[0]);
-        acc[1] = mfma2(w[P::KTO + kt], hi, lo, acc[1]);
+        acc[0] = mfma_row<A>(w2[kt], row, kt * 32 + quad * 8, acc[0]);
+        acc[1] = mfma_row<A>(w2[P::KTO + kt], row, kt * 32 + quad * 8, acc[1]);
       }
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
         const int m0 = (2 * wave + k) * 16 + quad * 4;
         const float4 b = *reinterpret_cast<const float4*>(BO + m0);
-        const float4 lv = make_float4(acc[k][0] + b.x, acc[k][1] + b.y, acc[k][2] + b.z, acc[k][3] + b.w);
-        *reinterpret_cast<float4*>(LG + n * PA + m0) = lv;
+        *reinterpret_cast<float4*>(LG + n * PA + m0) =
+            make_float4(acc[k][0] + b.x, acc[k][1] + b.y, acc[k][2] + b.z, acc[k][3] + b.w);
       }
     }
     lds_barrier();
@@ -252,7 +289,7 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
         y = wave_sum_int(cnt);
       }
       if (lane == 0) s_y[nn] = y;
-      X[nn * PX + lane] = bf16_val(EMB[y * R + lane]) + BE[lane];
+      split1(bf16_val(EMB[y * R + lane]) + BE[lane], XS[nn * SR + lane], XS[nn * SR + R + lane]);
     }
     lds_barrier();
   };
@@ -263,40 +300,45 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
     // ---------------- gate and residual: row tile gi of W_res, gi and gi + 4 of [W_prev | W_cur] ----------------
     constexpr int NB = 2 * P::KTG + P::KTR;
     const int gi = wave;
-    auto issue = [&](uint4 (&buf)[NB], int j) __attribute__((always_inline)) {
-      const uint4* lw = pk + (size_t)j * P::LAYER * 64 + lane;
+    const int m0 = gi * 16 + quad * 4;  // this lane's rows of x, h and the tanh half of a
+    auto issue = [&](u32x4 (&buf)[NB], int j) __attribute__((always_inline)) {
+      const size_t lb = (size_t)j * P::LAYER;
 #pragma unroll
       for (int kt = 0; kt < P::KTG; ++kt) {
-        buf[kt] = lw[(P::GATE + gi * P::KTG + kt) * 64];
-        buf[P::KTG + kt] = lw[(P::GATE + (gi + R / 16) * P::KTG + kt) * 64];
+        buf[kt] = tile(lb + P::GATE + gi * P::KTG + kt);
+        buf[P::KTG + kt] = tile(lb + P::GATE + (gi + R / 16) * P::KTG + kt);
       }
       if (j != L - 1) {  // the last layer's x feeds nothing
 #pragma unroll
-        for (int kt = 0; kt < P::KTR; ++kt) buf[2 * P::KTG + kt] = lw[(P::RES + gi * P::KTR + kt) * 64];
+        for (int kt = 0; kt < P::KTR; ++kt) buf[2 * P::KTG + kt] = tile(lb + P::RES + gi * P::KTR + kt);
       }
     };
-    uint4 bufA[NB], bufB[NB];
+    u32x4 bufA[NB], bufB[NB];
+    float4 xr = make_float4(0.f, 0.f, 0.f, 0.f);  // x_{j-1}[t], rows m0 .. m0 + 3 of stream n, fp32
     issue(bufA, 0);
     __syncthreads();
     run([&](auto parity, int64_t q, int64_t tl, int j) __attribute__((always_inline)) {
-      uint4(&cur)[NB] = decltype(parity)::value == 0 ? bufA : bufB;
-      uint4(&nxt)[NB] = decltype(parity)::value == 0 ? bufB : bufA;
+      u32x4(&cur)[NB] = decltype(parity)::value == 0 ? bufA : bufB;
+      u32x4(&nxt)[NB] = decltype(parity)::value == 0 ? bufB : bufA;
       const int slot = (int)(q & 1);
       issue(nxt, j + 1 == L ? 0 : j + 1);
+      if (j == 0) {  // x0 = E[y_{t-1}] + B_embed
+        const u16* e = EMB + s_y[n] * R + m0;
+        xr = make_float4(bf16_val(e[0]) + BE[m0], bf16_val(e[1]) + BE[m0 + 1], bf16_val(e[2]) + BE[m0 + 2],
+                         bf16_val(e[3]) + BE[m0 + 3]);
+      }
       f32x4 at = {0.f, 0.f, 0.f, 0.f}, as = {0.f, 0.f, 0.f, 0.f};
-      const float* xp = XP + slot * G * PX + n * PX;
-      const float* xc = X + n * PX;
+      const u16* xp = XP + (slot * G + n) * SR;
+      const u16* xc = XS + n * SR;
 #pragma unroll
       for (int kt = 0; kt < P::KTG; ++kt) {
         // inputs 0..R-1: the history row x_{j-1}[t - d_j]; R..2R-1: the current x_{j-1}[t]
-        const float* src = (kt < R / 32) ? xp + kt * 32 + quad * 8 : xc + (kt - R / 32) * 32 + quad * 8;
-        bf16x8 hi, lo;
-        split8(src, hi, lo);
-        at = mfma2(cur[kt], hi, lo, at);
-        as = mfma2(cur[P::KTG + kt], hi, lo, as);
+        const u16* row = kt < R / 32 ? xp : xc;
+        const int k0 = (kt % (R / 32)) * 32 + quad * 8;
+        at = mfma_row<R>(cur[kt], row, k0, at);
+        as = mfma_row<R>(cur[P::KTG + kt], row, k0, as);
       }
-      const float* cd = CD + slot * G * PC + n * PC;
-      const int m0 = gi * 16 + quad * 4;
+      const float* cd = CD + (slot * G + n) * PC;
       const float4 ch = *reinterpret_cast<const float4*>(cd + m0);
       const float4 cg = *reinterpret_cast<const float4*>(cd + R + m0);
       const float4 bh = *reinterpret_cast<const float4*>(BG + j * 2 * R + m0);
@@ -306,78 +348,83 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
       hv.y = tanh_f(at[1] + bh.y + ch.y) * sigmoid_f(as[1] + bg.y + cg.y);
       hv.z = tanh_f(at[2] + bh.z + ch.z) * sigmoid_f(as[2] + bg.z + cg.z);
       hv.w = tanh_f(at[3] + bh.w + ch.w) * sigmoid_f(as[3] + bg.w + cg.w);
-      *reinterpret_cast<float4*>(H + n * PX + m0) = hv;
+      store_split4<R>(HS + n * SR, m0, hv);
       lds_barrier();
       if (j < L - 1) {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kt = 0; kt < P::KTR; ++kt) {
-          bf16x8 hi, lo;
-          split8(H + n * PX + kt * 32 + quad * 8, hi, lo);
-          acc = mfma2(cur[2 * P::KTG + kt], hi, lo, acc);
-        }
-        float4 xv = *reinterpret_cast<const float4*>(X + n * PX + m0);
+        for (int kt = 0; kt < P::KTR; ++kt) acc = mfma_row<R>(cur[2 * P::KTG + kt], HS + n * SR, kt * 32 + quad * 8, acc);
         const float4 br = *reinterpret_cast<const float4*>(BR + j * R + m0);
-        xv.x += acc[0] + br.x;
-        xv.y += acc[1] + br.y;
-        xv.z += acc[2] + br.z;
-        xv.w += acc[3] + br.w;
-        *reinterpret_cast<float4*>(X + n * PX + m0) = xv;
+        xr.x += acc[0] + br.x;
+        xr.y += acc[1] + br.y;
+        xr.z += acc[2] + br.z;
+        xr.w += acc[3] + br.w;
+        store_split4<R>(XS + n * SR, m0, xr);
+        lds_barrier();
+      } else {
+        u32x4 w1[2 * P::KTH];
+        issue_head1(w1);
+        lds_barrier();
+        head_and_draw(tl, w1);
       }
-      lds_barrier();
-      if (j == L - 1) head_and_draw(tl);
     });
   } else if (wave < 7) {
     // ---------------- skip: row tiles sk0 .. sk0 + nsk - 1 of W_skip ----------------
     constexpr int NB = P::SKW * P::KTR;
     const int sk0 = (wave - 4) * P::SKW;
     const int nsk = min(P::SKW, P::NSKT - sk0);
-    auto issue = [&](uint4 (&buf)[NB], int j) __attribute__((always_inline)) {
-      const uint4* lw = pk + (size_t)j * P::LAYER * 64 + lane;
+    auto issue = [&](u32x4 (&buf)[NB], int j) __attribute__((always_inline)) {
+      const size_t lb = (size_t)j * P::LAYER;
 #pragma unroll
       for (int k = 0; k < P::SKW; ++k)
         if (k < nsk) {
 #pragma unroll
-          for (int kt = 0; kt < P::KTR; ++kt) buf[k * P::KTR + kt] = lw[(P::SKIP + (sk0 + k) * P::KTR + kt) * 64];
+          for (int kt = 0; kt < P::KTR; ++kt) buf[k * P::KTR + kt] = tile(lb + P::SKIP + (sk0 + k) * P::KTR + kt);
         }
     };
-    uint4 bufA[NB], bufB[NB];
+    u32x4 bufA[NB], bufB[NB];
     f32x4 qacc[P::SKW];
     issue(bufA, 0);
     __syncthreads();
     run([&](auto parity, int64_t q, int64_t tl, int j) __attribute__((always_inline)) {
-      uint4(&cur)[NB] = decltype(parity)::value == 0 ? bufA : bufB;
-      uint4(&nxt)[NB] = decltype(parity)::value == 0 ? bufB : bufA;
+      u32x4(&cur)[NB] = decltype(parity)::value == 0 ? bufA : bufB;
+      u32x4(&nxt)[NB] = decltype(parity)::value == 0 ? bufB : bufA;
       issue(nxt, j + 1 == L ? 0 : j + 1);
       lds_barrier();
-      bf16x8 hi[P::KTR], lo[P::KTR];
+      // q += W_skip h_j; the first layer starts the sum, so q holds nothing between the head and
+      // the next step
+      auto skip = [&](bool first) __attribute__((always_inline)) {
 #pragma unroll
-      for (int kt = 0; kt < P::KTR; ++kt) split8(H + n * PX + kt * 32 + quad * 8, hi[kt], lo[kt]);
-      // the first layer starts the sum, so q holds nothing between the head and the next step
-      const bool first = j == 0;
+        for (int k = 0; k < P::SKW; ++k) {
+          if (k < nsk) {
+            f32x4 acc = first ? f32x4{0.f, 0.f, 0.f, 0.f} : qacc[k];
 #pragma unroll
-      for (int k = 0; k < P::SKW; ++k) {
-        if (k < nsk) {
-          f32x4 acc = first ? f32x4{0.f, 0.f, 0.f, 0.f} : qacc[k];
-#pragma unroll
-          for (int kt = 0; kt < P::KTR; ++kt) acc = mfma2(cur[k * P::KTR + kt], hi[kt], lo[kt], acc);
-          qacc[k] = acc;
+            for (int kt = 0; kt < P::KTR; ++kt)
+              acc = mfma_row<R>(cur[k * P::KTR + kt], HS + n * SR, kt * 32 + quad * 8, acc);
+            qacc[k] = acc;
+          }
         }
-      }
-      if (j == L - 1) {
+      };
+      if (j < L - 1) {
+        skip(j == 0);
+        lds_barrier();
+      } else {
+        skip(false);
 #pragma unroll
         for (int k = 0; k < P::SKW; ++k) {
           if (k < nsk) {
             const int m0 = (sk0 + k) * 16 + quad * 4;
             const float4 bs = *reinterpret_cast<const float4*>(BS + m0);
-            const float4 z = make_float4(fmaxf(qacc[k][0] + bs.x, 0.f), fmaxf(qacc[k][1] + bs.y, 0.f),
-                                         fmaxf(qacc[k][2] + bs.z, 0.f), fmaxf(qacc[k][3] + bs.w, 0.f));
-            *reinterpret_cast<float4*>(ZS + n * PS + m0) = z;
+            store_split4<S>(ZS + n * SS, m0,
+                            make_float4(fmaxf(qacc[k][0] + bs.x, 0.f), fmaxf(qacc[k][1] + bs.y, 0.f),
+                                        fmaxf(qacc[k][2] + bs.z, 0.f), fmaxf(qacc[k][3] + bs.w, 0.f)));
           }
         }
+        u32x4 w1[2 * P::KTH];  // after the skip products, whose tiles no longer hold registers
+        issue_head1(w1);
+        lds_barrier();
+        head_and_draw(tl, w1);
       }
-      lds_barrier();
-      if (j == L - 1) head_and_draw(tl);
     });
   } else {
     // ---------------- loader: lane = stream ldn, quarter ldq of a row ----------------
@@ -385,29 +432,26 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
     const int ldn = lane >> 2, ldq = lane & 3;
     const int ldb = min(b0 + ldn, B - 1);  // reads of a partial group are clamped
     const int lub = min(b0 + lane, B - 1);
-    // history row x_{j-1}[ts - d_j] and conditioning row of position q for stream ldn
-    auto issue = [&](uint4 (&buf)[NB], int64_t q) __attribute__((always_inline)) {
-      if (q >= nq) return;
-      const int64_t tl = q / L;
-      const int j = (int)(q - tl * L);
-      const int64_t ts = tg0 + tl;
-      const int d = D.dil[j];
-      const uint4* hist = reinterpret_cast<const uint4*>(g.ws.hist + (size_t)ldb * D.hist_len + D.hoff[j] +
-                                                         (size_t)(ts % d) * R + ldq * 16);
+    const char* hrd = reinterpret_cast<const char*>(g.ws.hist + (size_t)ldb * D.hist_len) + ldq * 64;
+    const float* crd = g.io.cond + (size_t)ldb * T * L * 2 * R + ldq * 32;
+    // history row x_{j-1}[ts - d_j] (slot s_slot[j], see below) and conditioning row of (tl, j)
+    auto issue = [&](u32x4 (&buf)[NB], int64_t tl, int j) __attribute__((always_inline)) {
+      if (tl >= T) return;
+      const int slot = __builtin_amdgcn_readfirstlane(s_slot[j]);
+      const u32x4* h = reinterpret_cast<const u32x4*>(hrd + ((size_t)D.hoff[j] + (size_t)slot * R) * 4);
 #pragma unroll
-      for (int k = 0; k < 4; ++k) buf[k] = hist[k];
-      const uint4* c =
-          reinterpret_cast<const uint4*>(g.io.cond + (((size_t)ldb * T + tl) * L + j) * 2 * R + ldq * 32);
+      for (int k = 0; k < 4; ++k) buf[k] = h[k];
+      const u32x4* c = reinterpret_cast<const u32x4*>(crd + ((size_t)tl * L + j) * 2 * R);
 #pragma unroll
       for (int k = 0; k < 8; ++k) buf[4 + k] = c[k];
     };
-    auto store = [&](int slot, const uint4 (&buf)[NB]) __attribute__((always_inline)) {
-      float* xp = XP + slot * G * PX + ldn * PX + ldq * 16;
+    auto store = [&](int slot, const u32x4 (&buf)[NB]) __attribute__((always_inline)) {
+      u32x4* xp = reinterpret_cast<u32x4*>(XP + (slot * G + ldn) * SR) + ldq * 4;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) reinterpret_cast<float4*>(xp)[k] = as_f4(buf[k]);
-      float* cd = CD + slot * G * PC + ldn * PC + ldq * 32;
+      for (int k = 0; k < 4; ++k) xp[k] = buf[k];
+      float* cd = CD + (slot * G + ldn) * PC + ldq * 32;
 #pragma unroll
-      for (int k = 0; k < 8; ++k) reinterpret_cast<float4*>(cd)[k] = as_f4(buf[4 + k]);
+      for (int k = 0; k < 8; ++k) reinterpret_cast<u32x4*>(cd)[k] = buf[4 + k];
     };
     // Samples (generation) or logits (teacher forcing) of step tl, from s_y / LG, for the 16 streams.
     auto write_outputs = [&](int64_t tl) __attribute__((always_inline)) {
@@ -426,17 +470,19 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
         if (lane < G && b0 + lane < B) g.io.y_out[(size_t)(b0 + lane) * T + tl] = s_y[lane];
       }
     };
-    uint4 bufA[NB], bufB[NB];
+    u32x4 bufA[NB], bufB[NB];
     float pre_u = 0.f;
     int pre_y = 0;
-    issue(bufB, 0);
+    // rows of positions 0 and 1 (both in the first step: the kernel takes l >= 2)
+    issue(bufB, 0, 0);
     store(0, bufB);
-    issue(bufA, 1);
+    issue(bufA, 0, 1);
+    int64_t tl2 = 2 / L;  // position q + 2 of the loop below
+    int j2 = 2 % L;
     __syncthreads();
     run([&](auto parity, int64_t q, int64_t tl, int j) __attribute__((always_inline)) {
-      uint4(&cur)[NB] = decltype(parity)::value == 0 ? bufA : bufB;
-      uint4(&nxt)[NB] = decltype(parity)::value == 0 ? bufB : bufA;
-      const int64_t t = tg0 + tl;
+      u32x4(&cur)[NB] = decltype(parity)::value == 0 ? bufA : bufB;
+      u32x4(&nxt)[NB] = decltype(parity)::value == 0 ? bufB : bufA;
       // On gfx950 a wait for a load while stores are outstanding also waits for the stores, so
       // this wave first consumes what it loaded a layer ago, then stores, then issues its loads:
       // the next layer's wait then covers only stores that were issued before the loads it needs.
@@ -446,25 +492,27 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
         if constexpr (TF) s_yin[lane] = pre_y < 0 ? 0 : (pre_y > A - 1 ? A - 1 : pre_y);
         else s_u[lane] = pre_u;
       }
-      // x_{j-1}[t] into slot t mod d_j of layer j's history; it is read again at step t + d_j
-      // (by a load issued below when d_j l = 2).  All four values are read before the first
-      // store so that each store has registers of its own.
+      // x_{j-1}[t] (split) into slot t mod d_j of layer j's history, read again at step t + d_j.
+      // The slot counter of layer j then moves on to step t + 1, so a read issued from here on
+      // for layer j (step t + 1) or for a layer after j (step t) finds its slot in s_slot.
       {
-        const size_t so = D.hoff[j] + (size_t)(t % D.dil[j]) * R;
-        static_assert(G * R / 4 / 64 == 4, "four history values per loader lane");
+        const int slot = __builtin_amdgcn_readfirstlane(s_slot[j]);
+        char* hw = reinterpret_cast<char*>(g.ws.hist) + ((size_t)D.hoff[j] + (size_t)slot * R) * 4;
+        static_assert(G * 2 * R * 2 / 16 / 64 == 4, "four 16-byte pieces of x per loader lane");
         f32x4 v[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-          const int i = lane + 64 * k;
-          v[k] = *reinterpret_cast<const f32x4*>(X + (i / (R / 4)) * PX + (i % (R / 4)) * 4);
+          const int i = lane + 64 * k;  // stream i / 16, piece i % 16 of its 256-byte row
+          v[k] = *reinterpret_cast<const f32x4*>(XS + (i >> 4) * SR + (i & 15) * 8);
         }
         asm volatile("" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]));
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-          const int i = lane + 64 * k;
-          const int nn = i / (R / 4), c4 = i % (R / 4);
-          if (b0 + nn < B) reinterpret_cast<f32x4*>(g.ws.hist + (size_t)(b0 + nn) * D.hist_len + so)[c4] = v[k];
+          const int i = lane + 64 * k, nn = i >> 4;
+          if (b0 + nn < B)
+            *reinterpret_cast<f32x4*>(hw + (size_t)(b0 + nn) * D.hist_len * 4 + (i & 15) * 16) = v[k];
         }
+        if (lane == 0) s_slot[j] = slot + 1 == D.dil[j] ? 0 : slot + 1;
       }
       // outputs of the previous step, left in LDS by its head and draw
       if (j == 0 && tl > 0) write_outputs(tl - 1);
@@ -472,10 +520,17 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
         if constexpr (TF) pre_y = g.io.y_in[(size_t)lub * T + tl];
         else pre_u = g.io.u[(size_t)lub * T + tl];
       }
-      issue(nxt, q + 2);
+      issue(nxt, tl2, j2);
+      if (++j2 == L) j2 = 0, ++tl2;
       lds_barrier();
-      lds_barrier();
-      if (j == L - 1) head_and_draw(tl);
+      if (j < L - 1) {
+        lds_barrier();
+      } else {
+        u32x4 w1[2 * P::KTH];
+        issue_head1(w1);
+        lds_barrier();
+        head_and_draw(tl, w1);
+      }
     });
     write_outputs(T - 1);  // the last step's, after its draw
   }
@@ -489,7 +544,7 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
 
 template <int S>
 hipError_t launch_group_s(const WnGroupArgs& g, bool teacher, hipStream_t stream) {
-  const size_t dyn = lds_floats<S>(g.d.L) * sizeof(float);
+  const size_t dyn = lds_bytes<S>(g.d.L);
   const dim3 grid((g.io.B + G - 1) / G), block(NT);
   const void* k = teacher ? reinterpret_cast<const void*>(wn_group_kernel<S, true>)
                           : reinterpret_cast<const void*>(wn_group_kernel<S, false>);
@@ -517,7 +572,7 @@ bool wn_group_supported(int R_, int S_, int L) {
 }
 
 size_t wn_group_lds_bytes(int L, int S_) {
-  return (S_ == 256 ? lds_floats<256>(L) : lds_floats<128>(L)) * sizeof(float);
+  return S_ == 256 ? lds_bytes<256>(L) : lds_bytes<128>(L);
 }
 
 std::vector<uint16_t> wn_group_pack(int L, int R_, int S_, const float* w_prev, const float* w_cur,
