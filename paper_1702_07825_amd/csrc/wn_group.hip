@@ -45,6 +45,7 @@ constexpr int PC = 2 * R + 4;  // fp32 row pitches in LDS
 constexpr int PA = A + 4;
 constexpr int SR = 2 * R + 8;  // split-row pitch of an r-vector, in 16-bit units
 constexpr int SA = 2 * A + 8;
+constexpr int WB = 3;  // weight-tile buffers per wave: tiles are issued two layers ahead
 
 typedef unsigned short u16;
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -111,7 +112,7 @@ struct Pack {
 template <int S>
 constexpr size_t lds_bytes(int L) {
   return 4 * ((size_t)2 * G * PC + (size_t)G * PA + (size_t)L * 3 * R + R + S + 2 * A) +
-         2 * ((size_t)4 * G * SR + (size_t)G * Pack<S>::SS + (size_t)G * SA + (size_t)A * R);
+         2 * ((size_t)5 * G * SR + (size_t)G * Pack<S>::SS + (size_t)G * SA + (size_t)A * R);
 }
 
 template <int S, bool TF>
@@ -135,8 +136,8 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
   float* BS = BE + R;            // [S]
   float* BRL = BS + S;           // [A]
   float* BO = BRL + A;           // [A]
-  u16* XS = reinterpret_cast<u16*>(BO + A);  // [G][SR]    x_{j-1}, split
-  u16* HS = XS + G * SR;                      // [G][SR]    h_j, split
+  u16* XS = reinterpret_cast<u16*>(BO + A);  // [2][G][SR] x_{j-1}, split, in buffer j mod 2
+  u16* HS = XS + 2 * G * SR;                  // [G][SR]    h_j, split
   u16* XP = HS + G * SR;                      // [2][G][SR] history rows x_{j-1}[t - d_j] (layer parity)
   u16* ZS = XP + 2 * G * SR;                  // [G][SS]    relu(q + B_skip), split
   u16* ZA = ZS + G * SS;                      // [G][SA]    z_a, split
@@ -145,6 +146,9 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
   __shared__ float s_u[G];
   __shared__ int s_yin[G];
   __shared__ int s_slot[WN_GROUP_MAX_LAYERS];  // history slot (t mod d_j) of the next write of layer j
+  // layer j's history offset and dilation: read from LDS in the loop (a dynamically indexed
+  // kernel argument would be a scalar memory load each time)
+  __shared__ int s_hoff[WN_GROUP_MAX_LAYERS], s_dil[WN_GROUP_MAX_LAYERS];
 
   const u32x4* pk = static_cast<const u32x4*>(g.packed);
   const unsigned loff = (unsigned)lane * 16u;  // this lane's bytes within a 1 KB tile
@@ -168,7 +172,11 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
       s_y[tid] = y < 0 ? 0 : (y > A - 1 ? A - 1 : y);
     }
   }
-  if (tid < L) s_slot[tid] = (int)(tg0 % D.dil[tid]);
+  if (tid < L) {
+    s_slot[tid] = (int)(tg0 % D.dil[tid]);
+    s_hoff[tid] = D.hoff[tid];
+    s_dil[tid] = D.dil[tid];
+  }
   for (int i = tid; i < L * 2 * R; i += NT) BG[i] = g.w.b_gate[i];
   for (int i = tid; i < L * R; i += NT) BR[i] = g.w.b_res[i];
   for (int i = tid; i < R; i += NT) BE[i] = g.w.b_embed[i];
@@ -194,19 +202,26 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
 
   const int64_t nq = (int64_t)T * L;  // positions (step, layer) of this call
 
-  // Runs every position (step, layer) of the call; positions alternate between two prefetch
-  // buffers, passed to the body as a compile-time parity.  The loop leaves right after the
-  // position that used a buffer or goes on to the one that refills it.
-  auto run = [&](auto&& body) __attribute__((always_inline)) {
+  // Runs every position (step, layer) of the call.  Positions rotate through NBUF prefetch
+  // buffers; the body gets the buffer index as a compile-time constant.  The loop leaves right
+  // after the position that used a buffer or goes on to the one that refills it.
+  auto run = [&](auto nbuf, auto&& body) __attribute__((always_inline)) {
+    constexpr int NBUF = decltype(nbuf)::value;
+    static_assert(NBUF == 2 || NBUF == 3, "two or three prefetch buffers");
     int64_t tl = 0;
     int j = 0;
-    for (int64_t q = 0;;) {
-      body(std::integral_constant<int, 0>{}, q, tl, j);
+    int64_t q = 0;
+    auto step = [&](auto kc) __attribute__((always_inline)) {
+      body(kc, q, tl, j);
       if (++j == L) j = 0, ++tl;
-      if (++q == nq) break;
-      body(std::integral_constant<int, 1>{}, q, tl, j);
-      if (++j == L) j = 0, ++tl;
-      if (++q == nq) break;
+      return ++q == nq;
+    };
+    for (;;) {
+      if (step(std::integral_constant<int, 0>{})) break;
+      if (step(std::integral_constant<int, 1>{})) break;
+      if constexpr (NBUF == 3) {
+        if (step(std::integral_constant<int, 2>{})) break;
+      }
     }
   };
 
@@ -313,15 +328,14 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
         for (int kt = 0; kt < P::KTR; ++kt) buf[2 * P::KTG + kt] = tile(lb + P::RES + gi * P::KTR + kt);
       }
     };
-    u32x4 bufA[NB], bufB[NB];
+    u32x4 buf[WB][NB];  // tiles of layers j, j + 1, j + 2
     float4 xr = make_float4(0.f, 0.f, 0.f, 0.f);  // x_{j-1}[t], rows m0 .. m0 + 3 of stream n, fp32
-    issue(bufA, 0);
+    for (int k = 0; k + 1 < WB; ++k) issue(buf[k], k % L);
     __syncthreads();
-    run([&](auto parity, int64_t q, int64_t tl, int j) __attribute__((always_inline)) {
-      u32x4(&cur)[NB] = decltype(parity)::value == 0 ? bufA : bufB;
-      u32x4(&nxt)[NB] = decltype(parity)::value == 0 ? bufB : bufA;
+    run(std::integral_constant<int, WB>{}, [&](auto kc, int64_t q, int64_t tl, int j) __attribute__((always_inline)) {
+      constexpr int k = decltype(kc)::value;
+      u32x4(&cur)[NB] = buf[k];
       const int slot = (int)(q & 1);
-      issue(nxt, j + 1 == L ? 0 : j + 1);
       if (j == 0) {  // x0 = E[y_{t-1}] + B_embed
         const u16* e = EMB + s_y[n] * R + m0;
         xr = make_float4(bf16_val(e[0]) + BE[m0], bf16_val(e[1]) + BE[m0 + 1], bf16_val(e[2]) + BE[m0 + 2],
@@ -329,7 +343,7 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
       }
       f32x4 at = {0.f, 0.f, 0.f, 0.f}, as = {0.f, 0.f, 0.f, 0.f};
       const u16* xp = XP + (slot * G + n) * SR;
-      const u16* xc = XS + n * SR;
+      const u16* xc = XS + ((j & 1) * G + n) * SR;
 #pragma unroll
       for (int kt = 0; kt < P::KTG; ++kt) {
         // inputs 0..R-1: the history row x_{j-1}[t - d_j]; R..2R-1: the current x_{j-1}[t]
@@ -338,6 +352,8 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
         at = mfma_row<R>(cur[kt], row, k0, at);
         as = mfma_row<R>(cur[P::KTG + kt], row, k0, as);
       }
+      // the next tiles, issued once this layer's products are under way
+      issue(buf[(k + WB - 1) % WB], (j + WB - 1) % L);
       const float* cd = CD + (slot * G + n) * PC;
       const float4 ch = *reinterpret_cast<const float4*>(cd + m0);
       const float4 cg = *reinterpret_cast<const float4*>(cd + R + m0);
@@ -359,7 +375,7 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
         xr.y += acc[1] + br.y;
         xr.z += acc[2] + br.z;
         xr.w += acc[3] + br.w;
-        store_split4<R>(XS + n * SR, m0, xr);
+        store_split4<R>(XS + (((j + 1) & 1) * G + n) * SR, m0, xr);
         lds_barrier();
       } else {
         u32x4 w1[2 * P::KTH];
@@ -382,14 +398,15 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
           for (int kt = 0; kt < P::KTR; ++kt) buf[k * P::KTR + kt] = tile(lb + P::SKIP + (sk0 + k) * P::KTR + kt);
         }
     };
-    u32x4 bufA[NB], bufB[NB];
+    constexpr int SB = 2;  // tiles of layers j and j + 1 (three sets would not fit in registers)
+    u32x4 buf[SB][NB];
     f32x4 qacc[P::SKW];
-    issue(bufA, 0);
+    for (int k = 0; k + 1 < SB; ++k) issue(buf[k], k % L);
     __syncthreads();
-    run([&](auto parity, int64_t q, int64_t tl, int j) __attribute__((always_inline)) {
-      u32x4(&cur)[NB] = decltype(parity)::value == 0 ? bufA : bufB;
-      u32x4(&nxt)[NB] = decltype(parity)::value == 0 ? bufB : bufA;
-      issue(nxt, j + 1 == L ? 0 : j + 1);
+    run(std::integral_constant<int, SB>{}, [&](auto kc, int64_t q, int64_t tl, int j) __attribute__((always_inline)) {
+      constexpr int k = decltype(kc)::value;
+      u32x4(&cur)[NB] = buf[k];
+      issue(buf[(k + SB - 1) % SB], (j + SB - 1) % L);
       lds_barrier();
       // q += W_skip h_j; the first layer starts the sum, so q holds nothing between the head and
       // the next step
@@ -437,8 +454,8 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
     // history row x_{j-1}[ts - d_j] (slot s_slot[j], see below) and conditioning row of (tl, j)
     auto issue = [&](u32x4 (&buf)[NB], int64_t tl, int j) __attribute__((always_inline)) {
       if (tl >= T) return;
-      const int slot = __builtin_amdgcn_readfirstlane(s_slot[j]);
-      const u32x4* h = reinterpret_cast<const u32x4*>(hrd + ((size_t)D.hoff[j] + (size_t)slot * R) * 4);
+      const int hoff = __builtin_amdgcn_readfirstlane(s_hoff[j] + s_slot[j] * R);
+      const u32x4* h = reinterpret_cast<const u32x4*>(hrd + (size_t)hoff * 4);
 #pragma unroll
       for (int k = 0; k < 4; ++k) buf[k] = h[k];
       const u32x4* c = reinterpret_cast<const u32x4*>(crd + ((size_t)tl * L + j) * 2 * R);
@@ -480,12 +497,13 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
     int64_t tl2 = 2 / L;  // position q + 2 of the loop below
     int j2 = 2 % L;
     __syncthreads();
-    run([&](auto parity, int64_t q, int64_t tl, int j) __attribute__((always_inline)) {
+    run(std::integral_constant<int, 2>{}, [&](auto parity, int64_t q, int64_t tl, int j) __attribute__((always_inline)) {
       u32x4(&cur)[NB] = decltype(parity)::value == 0 ? bufA : bufB;
       u32x4(&nxt)[NB] = decltype(parity)::value == 0 ? bufB : bufA;
       // On gfx950 a wait for a load while stores are outstanding also waits for the stores, so
       // this wave first consumes what it loaded a layer ago, then stores, then issues its loads:
       // the next layer's wait then covers only stores that were issued before the loads it needs.
+      // (Moving this work to phase B, when the weight waves issue nothing, measured slower.)
       if (q + 1 < nq) store((int)((q + 1) & 1), cur);
       // this step's uniform (or teacher sample): read at the first layer, staged at the second
       if (j == 1 && lane < G) {
@@ -497,13 +515,13 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
       // for layer j (step t + 1) or for a layer after j (step t) finds its slot in s_slot.
       {
         const int slot = __builtin_amdgcn_readfirstlane(s_slot[j]);
-        char* hw = reinterpret_cast<char*>(g.ws.hist) + ((size_t)D.hoff[j] + (size_t)slot * R) * 4;
+        char* hw = reinterpret_cast<char*>(g.ws.hist) + ((size_t)s_hoff[j] + (size_t)slot * R) * 4;
         static_assert(G * 2 * R * 2 / 16 / 64 == 4, "four 16-byte pieces of x per loader lane");
         f32x4 v[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
           const int i = lane + 64 * k;  // stream i / 16, piece i % 16 of its 256-byte row
-          v[k] = *reinterpret_cast<const f32x4*>(XS + (i >> 4) * SR + (i & 15) * 8);
+          v[k] = *reinterpret_cast<const f32x4*>(XS + ((j & 1) * G + (i >> 4)) * SR + (i & 15) * 8);
         }
         asm volatile("" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]));
 #pragma unroll
@@ -512,7 +530,7 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
           if (b0 + nn < B)
             *reinterpret_cast<f32x4*>(hw + (size_t)(b0 + nn) * D.hist_len * 4 + (i & 15) * 16) = v[k];
         }
-        if (lane == 0) s_slot[j] = slot + 1 == D.dil[j] ? 0 : slot + 1;
+        if (lane == 0) s_slot[j] = slot + 1 == s_dil[j] ? 0 : slot + 1;
       }
       // outputs of the previous step, left in LDS by its head and draw
       if (j == 0 && tl > 0) write_outputs(tl - 1);
