@@ -39,12 +39,19 @@ def macs_per_sample(L, r, s, a=256, last_res=False):
     return L * per_layer - (0 if last_res else r * r) + a * s + a * a
 
 
-def kernel_source_digest():
+# Source files each kernel family is built from (the digest of a committed counter run must match).
+KERNEL_SOURCES = {
+    "multi_cu_chain": ["wn_chain.hip", "wn_wave.h", "wn_internal.h"],
+    "mfma_group": ["wn_group.hip", "wn_wave.h", "wn_internal.h"],
+    "stream_l2": ["wn_stream.hip", "wn_internal.h"],
+}
+
+
+def kernel_source_digest(variant):
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_1702_07825_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
-        if f.endswith((".hip", ".h")):
-            h.update(open(os.path.join(csrc, f), "rb").read())
+    for f in KERNEL_SOURCES[variant]:
+        h.update(open(os.path.join(csrc, f), "rb").read())
     return h.hexdigest()[:16]
 
 
@@ -55,7 +62,7 @@ def traffic_from_profiles(workload, variant):
         rec = json.load(open(path))[workload]
     except Exception:
         return None
-    if rec.get("source_digest") != kernel_source_digest() or rec.get("variant") != variant:
+    if rec.get("variant") != variant or rec.get("source_digest") != kernel_source_digest(variant):
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -138,7 +145,8 @@ def main():
     n = wl.B * wl.T
     value = n * args.steps / elapsed
     flop_per_launch = 2.0 * macs_per_sample(wl.n_layers, wl.r, wl.s) * n
-    peak = PEAKS["f32_vector_tflops"]
+    # The batched kernel computes its products on bf16 MFMA; the others on the fp32 vector ALUs.
+    bound, peak = ("mfma", PEAKS["bf16_mfma_tflops"]) if variant == "mfma_group" else ("alu", PEAKS["f32_vector_tflops"])
     achieved = flop_per_launch / avg_launch_s / 1e12
     per_stream_rate = wl.T / avg_launch_s
     y = samples.cpu().numpy()
@@ -156,12 +164,12 @@ def main():
         "dtype": "f32" if wl.weight_dtype == "f32" else "bf16-weights/f32",
         "data": "synthetic (seeded N(0,1/fan_in) weights, N(0,1) conditioning, U[0,1) uniforms)",
         "config": {"workload": wl.description, "B": wl.B, "T": wl.T, "n_layers": wl.n_layers, "r": wl.r,
-                   "s": wl.s, "a": wl.a, "kernel": variant},
+                   "s": wl.s, "a": wl.a, "kernel": variant, "source_digest": kernel_source_digest(variant)},
         "real_time_factor_16khz": round(per_stream_rate / RATE_HZ, 3),
         "real_time_factor_16384hz": round(per_stream_rate / PAPER_RATE_HZ, 3),
         "us_per_sample_step": round(avg_launch_s / wl.T * 1e6, 3),
         "roofline": {
-            "bound": "alu",
+            "bound": bound,
             "achieved": round(achieved, 4),
             "peak": peak,
             "unit": "TFLOP/s",
