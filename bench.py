@@ -80,38 +80,20 @@ def cpu_baseline(wl, w, cond_dev, u_np, steps):
             "seconds": round(dt, 2)}
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="l20_r64_b1")
-    ap.add_argument("--cpu-steps", type=int, default=8000, help="oracle sample size (0 = skip)")
-    ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
-                    help="only run one device-to-device copy of BYTES (calibrates HBM byte counters) and exit")
-    args = ap.parse_args()
-    if args.copy_probe:
-        import torch
-        src = torch.ones(args.copy_probe // 4, dtype=torch.float32, device="cuda:0")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        print(json.dumps({"copy_probe_bytes": args.copy_probe}))
-        return
-    if args.gpus != 1:
-        print("bench.py: this build runs on one GPU only (streams are independent; see DESIGN.md for how "
-              "the batched workloads would shard); --gpus %d is not supported" % args.gpus, file=sys.stderr)
-        sys.exit(2)
+def algorithmic_hbm_bytes_per_sample(wl):
+    """HBM bytes one generated sample needs at least: its conditioning (l x 2r fp32), uniform and
+    sample, and the history of every layer read and written once (2 x l x r x 4 B)."""
+    return wl.n_layers * 2 * wl.r * 4 + 4 + 4 + 2 * wl.n_layers * wl.r * 4
 
+
+def run_workload(name, args):
     import numpy as np
     import torch
 
     import synth
     import paper_1702_07825_amd as wn
 
-    wl = synth.WORKLOADS[args.workload]
+    wl = synth.WORKLOADS[name]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     w = synth.make_weights(wl.n_layers, wl.r, wl.s, seed=args.seed)
@@ -149,6 +131,7 @@ def main():
     bound, peak = ("mfma", PEAKS["bf16_mfma_tflops"]) if variant == "mfma_group" else ("alu", PEAKS["f32_vector_tflops"])
     achieved = flop_per_launch / avg_launch_s / 1e12
     per_stream_rate = wl.T / avg_launch_s
+    hbm_alg = algorithmic_hbm_bytes_per_sample(wl) * n
     y = samples.cpu().numpy()
     out = {
         "metric": "generated samples/s (16 kHz mu-law audio, all streams)",
@@ -174,8 +157,12 @@ def main():
             "peak": peak,
             "unit": "TFLOP/s",
             "frac": round(achieved / peak, 6),
-            "traffic": traffic_from_profiles(args.workload, variant),
+            "traffic": traffic_from_profiles(name, variant),
             "algorithmic_flop_per_launch": flop_per_launch,
+            "hbm": {"algorithmic_bytes_per_launch": hbm_alg,
+                    "achieved_gbs": round(hbm_alg / avg_launch_s / 1e9, 2),
+                    "peak_gbs": PEAKS["hbm_gbs"],
+                    "frac": round(hbm_alg / avg_launch_s / 1e9 / PEAKS["hbm_gbs"], 6)},
             "avg_launch_ms": round(avg_launch_s * 1e3, 4),
         },
         "sample_histogram_entropy_bits": round(float(-(lambda p: (p[p > 0] * np.log2(p[p > 0])).sum())(
@@ -187,6 +174,38 @@ def main():
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)
     net.close()
+    del cond, u, samples, ws
+    torch.cuda.empty_cache()
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="l20_r64_b1", help="a workload name, or 'all' (one JSON line each)")
+    ap.add_argument("--cpu-steps", type=int, default=8000, help="oracle sample size (0 = skip)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run one device-to-device copy of BYTES (calibrates HBM byte counters) and exit")
+    args = ap.parse_args()
+    if args.copy_probe:
+        import torch
+        src = torch.ones(args.copy_probe // 4, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": args.copy_probe}))
+        return
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU only (streams are independent; see DESIGN.md for how "
+              "the batched workloads would shard); --gpus %d is not supported" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import synth
+    names = list(synth.WORKLOADS) if args.workload == "all" else [args.workload]
+    for name in names:
+        run_workload(name, args)
 
 
 if __name__ == "__main__":
