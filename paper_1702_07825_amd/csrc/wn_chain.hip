@@ -1,4 +1,4 @@
-// Multi-CU persistent generation kernel for one stream (B = 1), fp32, gfx950.
+// Multi-CU persistent generation kernel, fp32 weights, gfx950.
 //
 // One generated sample is a strictly serial chain: the previous sample's
 // embedding, then l gated layers, then the skip sum and the two-layer head, then
@@ -30,12 +30,20 @@
 // its consumer.  The dilation histories are rings of tagged words in the
 // workspace: slot (t mod d) of layer j holds x_{j-1}[t] tagged t + 1.
 //
+// Several streams: the roles above form one replica.  Up to 256 / (roles per replica) replicas
+// run side by side, each serving G streams, and every role of a replica takes its streams in
+// turn within each step (stream i of step t after stream i - 1).  All messages are per stream,
+// so the per-stream protocol is unchanged; while chain CU c works on stream i, chain CU c + 1
+// works on stream i - 1, so the interleaved streams fill the chain's idle time.  Every role
+// takes the (step, stream) pairs in the same order, and each input of a pair is produced at an
+// earlier pair by its producer, so no role can wait on a role that waits on it.
+//
 // Every wait is bounded.  A block that times out stores WN_ETIMEOUT in the
 // workspace status word; every waiting block polls that word and leaves, so the
-// grid always drains.  Block b takes role (b mod 8) * 32 + b / 8, which puts
-// roles 0..31 (the chain and head CUs and the first aux CUs) on one XCD when
-// blocks are dealt round-robin over the eight XCDs; the protocol does not depend
-// on that placement, only the hop latency does.
+// grid always drains.  The host gives each block its role: when blocks are dealt
+// round-robin over the eight XCDs (block b on XCD b mod 8), a replica's chain and
+// head CUs and as many of its aux CUs as fit (the last layers first) share one XCD.
+// The protocol does not depend on that placement, only the hop latency does.
 #include "wn_internal.h"
 #include "wn_wave.h"
 
@@ -87,19 +95,21 @@ struct Items {
 __device__ __forceinline__ Items no_items() { return Items{nullptr, 1, 0, 0, nullptr, 0u}; }
 
 // Wait until every item of `a` and `b` owned by this thread (item i belongs to thread i mod NT)
-// carries its descriptor's tag, writing the values to LDS (dst pointers lie in `lds`).  All owned
-// loads are in flight together.  A thread that times out, or sees a nonzero status word, sets the
+// carries its descriptor's tag, writing the values to LDS (dst pointers lie in `lds`).  Up to K
+// owned loads are in flight together.  A thread that times out, or sees a nonzero status word, sets the
 // block's abort flag and stops waiting.  Every polled word lies in the workspace's tagged region,
 // which starts at g.ring; items are tracked as 32-bit word offsets from there.
+template <int K = 4>
 __device__ void poll2(const WnChainArgs& g, const Items a, const Items b, float* lds, Sync s) {
   const int n = a.n + b.n;
   const u64* wbase = g.ring;
-  for (int base = threadIdx.x; base < n; base += 4 * NT) {
-    u64 w[4];
-    unsigned so[4], dofs[4];
+  for (int base = threadIdx.x; base < n; base += K * NT) {
+    u64 w[K];
+    unsigned so[K], dofs[K];
     unsigned pend = 0, useb = 0;  // bit k: item base + k * NT pending / belongs to descriptor b
+    static_assert(K <= 32, "pending bits");
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
+    for (int k = 0; k < K; ++k) {
       const int i = base + k * NT;
       if (i < n) {
         const bool inb = (i >= a.n);
@@ -115,7 +125,7 @@ __device__ void poll2(const WnChainArgs& g, const Items a, const Items b, float*
     int spins = 0;
     while (true) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
+      for (int k = 0; k < K; ++k) {
         if (pend & (1u << k)) {
           if (wtag(w[k]) == ((useb & (1u << k)) ? b.tag : a.tag)) {
             pend &= ~(1u << k);
@@ -130,7 +140,7 @@ __device__ void poll2(const WnChainArgs& g, const Items a, const Items b, float*
         return;
       }
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
+      for (int k = 0; k < K; ++k)
         if (pend & (1u << k)) w[k] = ldw(wbase + so[k]);
     }
   }
@@ -145,7 +155,30 @@ struct ChainMap {
   static constexpr int LPR2 = NT / R;        // lanes per W_res row
   static constexpr int KC2 = R / LPR2;
   static_assert(LPR1 >= 1 && KC1 % 2 == 0 && KC2 >= 2 && KCG >= 2, "unsupported R");
+  // r = 128 keeps W_res of one layer in VGPRs; a CU with two layers keeps both W_res in LDS
+  static constexpr int WRV = (R == 128) ? 1 : 1 << 30;
 };
+
+// Row stride (floats) of a matrix kept in LDS and read as float4 chunks by `lanes` lanes per row,
+// lane k taking chunks k, k + lanes, ...: consecutive rows start 4 * lanes banks apart, so the 16
+// lanes of a 64-bank access phase hit distinct banks.
+constexpr int lds_row_stride(int K, int lanes) { return K + ((4 * lanes - K % 64) % 64 + 64) % 64; }
+
+// Dot product of K-long LDS rows read as interleaved float4 chunks (stride 4 * STEP floats).
+template <int K, int STEP>
+__device__ __forceinline__ float dot_lds_il(const float* w, const float* x) {
+  float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+  for (int i = 0; i < K / 4; ++i) {
+    const float4 a = *reinterpret_cast<const float4*>(w + 4 * STEP * i);
+    const float4 v = *reinterpret_cast<const float4*>(x + 4 * STEP * i);
+    s0 = fmaf(a.x, v.x, s0);
+    s1 = fmaf(a.y, v.y, s1);
+    s0 = fmaf(a.z, v.z, s0);
+    s1 = fmaf(a.w, v.w, s1);
+  }
+  return s0 + s1;
+}
 
 template <int K>
 __device__ __forceinline__ float dot_lds(const float (&w)[K], const float* x) {
@@ -184,33 +217,51 @@ __device__ __forceinline__ float dot_lds(const float (&w)[K], const float* x) {
 // ------------------------------------------------------------------------------------------
 // chain CU
 // ------------------------------------------------------------------------------------------
-template <int R, int S, int NLC, bool TF>
-__device__ void chain_role(const WnChainArgs& g, const int c, float* dyn, Sync sy, const int64_t tg0, const int yprev0) {
+template <int R, int S, int NLC, bool TF, bool MS>
+__device__ void chain_role(const WnChainArgs& g, const int c, const int b0, const int ns, float* dyn, Sync sy,
+                           const int64_t tg0) {
   using M = ChainMap<R>;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int L = g.d.L;
   const int j0 = g.layer_begin[c], nl = g.layer_begin[c + 1] - j0;
   const bool first = (c == 0);
-  const int T = g.io.T;
-
-  float* xs = dyn;                    // R      x_{j-1}, updated in place
-  float* hs = xs + R;                 // R
-  float* pre = hs + R;                // NLC*2R pre-activations of this step
-  float* lgp = pre + NLC * 2 * R;     // NHEAD*A partial logits (chain CU 0)
-  float* ubuf = lgp + NHEAD * A;      // UB uniforms (generation) / samples in (teacher forcing)
-  int* ybuf = reinterpret_cast<int*>(ubuf + UB);  // UB drawn samples
-  float* xbuf = reinterpret_cast<float*>(ybuf + UB);  // NLC*R x_{j-1} of this step (history writes)
-  float* emb = xbuf + NLC * R;                         // A*R embedding table (chain CU 0)
-  float* wsk = emb + A * R;                            // S*R W_skip of layer l-1 (last chain CU)
-  float* bres = wsk + S * R;                           // NLC*R B_res of my layers
-  __shared__ int s_y;
   const bool lastc = (c + 1 == g.nch);
+  const bool tail = lastc && g.tail_on_chain;
+  const int T = g.io.T;
+  // streams per replica and staged steps per stream (a power of two); constants for one stream
+  const int G = MS ? g.G : 1;
+  const int ub = MS ? g.ub : 512, ubs = MS ? __builtin_ctz(g.ub) : 9;
+
+  constexpr int NLCP = (NLC + 3) & ~3;
+  constexpr int LPRS = NT / S, KCS = R / LPRS;    // tail skip projection: lanes per row, inputs per lane
+  constexpr int WSK = lds_row_stride(R, LPRS);    // W_skip row stride in LDS
+  constexpr int WRS = lds_row_stride(R, M::LPR2); // W_res row stride in LDS
+  // LDS: the part every chain CU uses, then a part that depends on the CU's place in the chain
+  float* xs = dyn;                                  // R      x_{j-1}, updated in place
+  float* hs = xs + R;                               // R
+  float* pre = hs + R;                              // NLC*2R pre-activations of this step
+  float* xbuf = pre + NLC * 2 * R;                  // NLC*R  x_{j-1} of this step (history writes)
+  float* bres = xbuf + NLC * R;                     // NLC*R  B_res of my layers
+  int* slotv = reinterpret_cast<int*>(bres + NLC * R);  // 2*NLCP history slot (t mod d) of each layer, by step parity
+  float* var = reinterpret_cast<float*>(slotv + 2 * NLCP);
+  // chain CU 0: partial logits, staged inputs and samples, last samples, the embedding table
+  float* lgp = var;                                 // NHEAD*A
+  float* ubuf = lgp + NHEAD * A;                    // G*ub   uniforms / samples in, per stream
+  int* ybuf = reinterpret_cast<int*>(ubuf + G * ub);  // G*ub drawn samples
+  int* syv = ybuf + G * ub;                         // G      last sample of each stream
+  float* emb = reinterpret_cast<float*>(syv + ((G + 3) & ~3));  // A*R
+  // last chain CU: W_skip of layer l-1, S rows of stride WSK (after the table if it is also CU 0)
+  float* wsk = first ? emb + A * R : var;
+  // a middle r = 128 CU with two layers: their W_res, R rows of stride WRS each
+  float* wres = var;
+  const bool wres_lds = nl > M::WRV;
 
   // resident weights
   // W_cur: lane group c (LPRG lanes) holds rows c and c + R, lane kq of it inputs kq*KCG .. +KCG
   const int g1 = tid / M::LPRG, kq = tid % M::LPRG;
   const int row2 = tid / M::LPR2, kk = tid % M::LPR2;
-  float wc[NLC][2 * M::KCG], wr[NLC][M::KC2];
+  constexpr int NWR = NLC < M::WRV ? NLC : M::WRV;
+  float wc[NLC][2 * M::KCG], wr[NWR][M::KC2];
   const float* Wc = static_cast<const float*>(g.w.w_cur);
   const float* Wr = static_cast<const float*>(g.w.w_res);
 #pragma unroll
@@ -221,39 +272,58 @@ __device__ void chain_role(const WnChainArgs& g, const int c, float* dyn, Sync s
       wc[l][i] = Wc[((size_t)j * 2 * R + g1) * R + kq * M::KCG + i];
       wc[l][M::KCG + i] = Wc[((size_t)j * 2 * R + g1 + R) * R + kq * M::KCG + i];
     }
+  }
+  if (wres_lds) {
+    for (int i = tid; i < nl * R * R; i += NT) {
+      const int l = i / (R * R), rr = (i / R) % R, k = i % R;
+      wres[(l * R + rr) * WRS + k] = Wr[(size_t)j0 * R * R + i];
+    }
+  } else {
 #pragma unroll
-    for (int i = 0; i < M::KC2; ++i) wr[l][i] = Wr[((size_t)j * R + row2) * R + kk * M::KC2 + i];
+    for (int l = 0; l < NWR; ++l) {
+      const int j = j0 + (l < nl ? l : 0);
+#pragma unroll
+      for (int i = 0; i < M::KC2; ++i) wr[l][i] = Wr[((size_t)j * R + row2) * R + kk * M::KC2 + i];
+    }
   }
   for (int i = tid; i < nl * R; i += NT) bres[i] = g.w.b_res[(size_t)j0 * R + i];
+  if (tid < nl) slotv[(tg0 & 1) * NLCP + tid] = (int)(tg0 % g.d.dil[j0 + tid]);
   float bemb = 0.f;
   float4 bout4 = make_float4(0.f, 0.f, 0.f, 0.f);  // B_out of the 4 logits lane l of wave 0 draws from
-  if (lastc) {
+  if (tail) {
     const float* Wk = static_cast<const float*>(g.w.w_skip) + (size_t)(L - 1) * S * R;
-    for (int i = tid; i < S * R; i += NT) wsk[i] = Wk[i];
+    for (int i = tid; i < S * R; i += NT) wsk[(i / R) * WSK + i % R] = Wk[i];
   }
+  int64_t ub0 = tg0;  // first global step held in ubuf / ybuf
+  // Stage steps ub0 .. ub0 + ub - 1 of every stream's uniforms (or teacher-forced samples).
+  auto stage_inputs = [&]() {
+    for (int idx = tid; idx < ns * ub; idx += NT) {
+      const int i = idx >> ubs, k = idx & (ub - 1);
+      const int64_t t = ub0 + k;
+      if (t < tg0 + T) {
+        const size_t at = (size_t)(b0 + i) * T + (size_t)(t - tg0);
+        if constexpr (TF) reinterpret_cast<int*>(ubuf)[idx] = g.io.y_in[at];
+        else ubuf[idx] = g.io.u[at];
+      }
+    }
+  };
   if (first) {
     if (wave == 0) bout4 = *reinterpret_cast<const float4*>(g.w.b_out + 4 * lane);
     const float* E = static_cast<const float*>(g.w.embed);
     for (int i = tid; i < A * R; i += NT) emb[i] = E[i];
     if (tid < R) bemb = g.w.b_embed[tid];
-    if (tid == 0) s_y = yprev0;
-  }
-  int64_t ub0 = tg0;  // first global step held in ubuf / ybuf
-  if (first) {
-    for (int i = tid; i < UB; i += NT) {
-      const int64_t t = tg0 + i;
-      if (t < tg0 + T) {
-        if constexpr (TF) reinterpret_cast<int*>(ubuf)[i] = g.io.y_in[t - tg0];
-        else ubuf[i] = g.io.u[t - tg0];
-      }
+    for (int i = tid; i < ns; i += NT) {
+      int y = g.io.reset ? g.io.init_sample : (int)g.state[2 * (size_t)(b0 + i) + 1];
+      syv[i] = y < 0 ? 0 : (y > A - 1 ? A - 1 : y);
     }
+    stage_inputs();
   }
   lds_barrier();
 
-  // One wave sums the head's partial logits of global step ts (lane l owns logits 4l..4l+3),
-  // writes them out when teacher forcing, and draws (generation) or reads (teacher forcing)
-  // the sample.
-  auto sample_step = [&](int64_t ts) {
+  // One wave sums the head's partial logits of global step ts of local stream i (lane l owns
+  // logits 4l..4l+3), writes them out when teacher forcing, and draws (generation) or reads
+  // (teacher forcing) the sample.
+  auto sample_step = [&](int64_t ts, int i) {
     if (wave == 0) {
       float4 lv = bout4;
 #pragma unroll
@@ -264,10 +334,11 @@ __device__ void chain_role(const WnChainArgs& g, const int c, float* dyn, Sync s
         lv.z += p.z;
         lv.w += p.w;
       }
+      const int at = (i << ubs) + (int)(ts - ub0);
       int y;
       if constexpr (TF) {
-        *reinterpret_cast<float4*>(g.io.logits + (size_t)(ts - tg0) * A + 4 * lane) = lv;
-        y = reinterpret_cast<const int*>(ubuf)[ts - ub0];
+        *reinterpret_cast<float4*>(g.io.logits + ((size_t)(b0 + i) * T + (size_t)(ts - tg0)) * A + 4 * lane) = lv;
+        y = reinterpret_cast<const int*>(ubuf)[at];
         y = y < 0 ? 0 : (y > A - 1 ? A - 1 : y);
       } else {
         const float l0 = lv.x, l1 = lv.y, l2 = lv.z, l3 = lv.w;
@@ -278,193 +349,196 @@ __device__ void chain_role(const WnChainArgs& g, const int c, float* dyn, Sync s
         const float excl = wave_shr1(incl);
         const float Z = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, incl), 63));
         const float iz = 1.0f / Z;
-        const float u = ubuf[ts - ub0];
+        const float u = ubuf[at];
         int cnt = ((excl + s0) * iz <= u) + ((excl + s1) * iz <= u) + ((excl + s2) * iz <= u);
         if (lane != 63) cnt += ((excl + s3) * iz <= u);
         y = wave_sum_int(cnt);
       }
       if (lane == 0) {
-        s_y = y;
-        ybuf[ts - ub0] = y;
+        syv[i] = y;
+        ybuf[at] = y;
       }
     }
   };
-  // The head's partial logits of step ts (tag ts + 1).
-  auto logit_items = [&](int64_t ts) {
-    return Items{g.mb_logit + (size_t)(ts & 1) * A, A, 2 * A, NHEAD * A, lgp, (unsigned)(ts + 1)};
+  // The head's partial logits of step ts of stream b (tag ts + 1).
+  auto logit_items = [&](int64_t ts, int b) {
+    return Items{g.mb + (size_t)b * g.mb_words + g.off_logit + (size_t)(ts & 1) * A, A, 2 * A, NHEAD * A, lgp,
+                 (unsigned)(ts + 1)};
   };
-  // Move staged samples to the output and stage the next block of inputs.
+  // Move staged samples (steps before next0) to the output and stage the next block of inputs.
   auto roll_buffers = [&](int64_t next0) {
     if constexpr (!TF) {
-      for (int i = tid; i < UB; i += NT) {
-        const int64_t t = ub0 + i;
-        if (t < next0 && t < tg0 + T) g.io.y_out[t - tg0] = ybuf[i];
+      for (int idx = tid; idx < ns * ub; idx += NT) {
+        const int i = idx >> ubs, k = idx & (ub - 1);
+        const int64_t t = ub0 + k;
+        if (t < next0 && t < tg0 + T) g.io.y_out[(size_t)(b0 + i) * T + (size_t)(t - tg0)] = ybuf[idx];
       }
     }
     lds_barrier();
     ub0 = next0;
-    for (int i = tid; i < UB; i += NT) {
-      const int64_t t = ub0 + i;
-      if (t < tg0 + T) {
-        if constexpr (TF) reinterpret_cast<int*>(ubuf)[i] = g.io.y_in[t - tg0];
-        else ubuf[i] = g.io.u[t - tg0];
-      }
-    }
+    stage_inputs();
     lds_barrier();
   };
 
   for (int64_t t = tg0; t < tg0 + T; ++t) {
     const unsigned tag = (unsigned)(t + 1);
     const int par = (int)(t & 1);
-    // ---- inputs of this step, all waited for together: the pre-activations of my layers, and
-    //      either x from the previous chain CU or (chain CU 0) the previous step's partial logits ----
-    const Items pre_items{g.mb_pre + ((size_t)j0 * 2 + par) * 2 * R, 2 * R, 2 * 2 * R, nl * 2 * R, pre, tag};
-    if (first) {
-      if (t > tg0) {
-        poll2(g, logit_items(t - 1), pre_items, dyn, sy);
+    for (int i = 0; i < ns; ++i) {
+      const int b = b0 + i;
+      u64* const mbs = g.mb + (size_t)b * g.mb_words;
+      u64* const rings = g.ring + (size_t)b * g.d.hist_len;
+      // ---- inputs of this step, all waited for together: the pre-activations of my layers, and
+      //      either x from the previous chain CU or (chain CU 0) the previous step's partial logits ----
+      const Items pre_items{mbs + ((size_t)j0 * 2 + par) * 2 * R, 2 * R, 2 * 2 * R, nl * 2 * R, pre, tag};
+      if (first) {
+        if (t > tg0) {
+          poll2(g, logit_items(t - 1, b), pre_items, dyn, sy);
+          lds_barrier();
+          if (sy.failed()) return;
+          if (i == 0 && t - 1 - ub0 >= ub) roll_buffers(t - 1);
+          sample_step(t - 1, i);
+        } else {
+          poll2(g, pre_items, no_items(), dyn, sy);
+        }
         lds_barrier();
         if (sy.failed()) return;
-        if (t - 1 - ub0 >= UB) roll_buffers(t - 1);
-        sample_step(t - 1);
+        if (tid < R) xs[tid] = emb[syv[i] * R + tid] + bemb;
       } else {
-        poll2(g, pre_items, no_items(), dyn, sy);
+        poll2(g, pre_items, Items{mbs + g.off_x + ((size_t)c * 2 + par) * R, R, R, R, xs, tag}, dyn, sy);
       }
       lds_barrier();
       if (sy.failed()) return;
-      if (tid < R) xs[tid] = emb[s_y * R + tid] + bemb;
-    } else {
-      poll2(g, pre_items, Items{g.mb_x + ((size_t)c * 2 + par) * R, R, R, R, xs, tag}, dyn, sy);
-    }
-    lds_barrier();
-    if (sy.failed()) return;
+      // history slots of step t + 1 (step t's stay readable until then: the slots of the other
+      // parity were last read during step t - 1, which every thread has left)
+      if (i == 0 && tid < nl) {
+        const int sl = slotv[par * NLCP + tid] + 1;
+        slotv[(par ^ 1) * NLCP + tid] = (sl == g.d.dil[j0 + tid]) ? 0 : sl;
+      }
 
-    // Store data of the per-layer h posts, rotating over HPOST register pairs: a pair is written
-    // again HPOST layers after its store was issued, by when that store has completed, so the
-    // wait the compiler places before the overwrite costs nothing inside the layer loop.
-    constexpr int HPOST = 3;
-    u64 hpost[HPOST];
+      // Store data of the per-layer h posts, rotating over HPOST register pairs: a pair is written
+      // again HPOST layers after its store was issued, by when that store has completed, so the
+      // wait the compiler places before the overwrite costs nothing inside the layer loop.
+      constexpr int HPOST = 3;
+      constexpr int HPW = R < 64 ? 64 : R;  // the last HPW threads post h
+      u64 hpost[HPOST];
 #pragma unroll
-    for (int l = 0; l < HPOST; ++l) hpost[l] = 0;
+      for (int l = 0; l < HPOST; ++l) hpost[l] = 0;
 #pragma unroll
-    for (int l = 0; l < NLC; ++l) {
-      if (l < nl) {
-        const int j = j0 + l;
-        // a = W_cur x + pre ; h = tanh(a[0:R]) * sigmoid(a[R:2R]).  Each lane has both rows of its
-        // pair; lane 0 of the group starts its partial sums from pre, so pre joins the reduction.
-        float ah, ag;
-        {
-          float sh0 = 0.f, sh1 = 0.f, sg0 = 0.f, sg1 = 0.f;
+      for (int l = 0; l < NLC; ++l) {
+        if (l < nl) {
+          const int j = j0 + l;
+          // a = W_cur x + pre ; h = tanh(a[0:R]) * sigmoid(a[R:2R]).  Each lane has both rows of its
+          // pair; lane 0 of the group starts its partial sums from pre, so pre joins the reduction.
+          float ah, ag;
+          {
+            float sh0 = 0.f, sh1 = 0.f, sg0 = 0.f, sg1 = 0.f;
+            if (kq == 0) {
+              sh0 = pre[l * 2 * R + g1];
+              sg0 = pre[l * 2 * R + g1 + R];
+            }
+            const float* xk = xs + kq * M::KCG;
+            if constexpr (M::KCG % 4 == 0) {
+#pragma unroll
+              for (int i2 = 0; i2 < M::KCG; i2 += 4) {
+                const float4 v = *reinterpret_cast<const float4*>(xk + i2);
+                sh0 = fmaf(wc[l][i2], v.x, sh0);
+                sh1 = fmaf(wc[l][i2 + 1], v.y, sh1);
+                sh0 = fmaf(wc[l][i2 + 2], v.z, sh0);
+                sh1 = fmaf(wc[l][i2 + 3], v.w, sh1);
+                sg0 = fmaf(wc[l][M::KCG + i2], v.x, sg0);
+                sg1 = fmaf(wc[l][M::KCG + i2 + 1], v.y, sg1);
+                sg0 = fmaf(wc[l][M::KCG + i2 + 2], v.z, sg0);
+                sg1 = fmaf(wc[l][M::KCG + i2 + 3], v.w, sg1);
+              }
+            } else {
+              static_assert(M::KCG % 2 == 0, "inputs per lane must be even");
+#pragma unroll
+              for (int i2 = 0; i2 < M::KCG; i2 += 2) {
+                const float2 v = *reinterpret_cast<const float2*>(xk + i2);
+                sh0 = fmaf(wc[l][i2], v.x, sh0);
+                sh1 = fmaf(wc[l][i2 + 1], v.y, sh1);
+                sg0 = fmaf(wc[l][M::KCG + i2], v.x, sg0);
+                sg1 = fmaf(wc[l][M::KCG + i2 + 1], v.y, sg1);
+              }
+            }
+            ah = gsum<M::LPRG>(sh0 + sh1);
+            ag = gsum<M::LPRG>(sg0 + sg1);
+          }
+          const float h = tanh_f(ah) * sigmoid_f(ag);
           if (kq == 0) {
-            sh0 = pre[l * 2 * R + g1];
-            sg0 = pre[l * 2 * R + g1 + R];
+            hs[g1] = h;
           }
-          const float* xk = xs + kq * M::KCG;
-          if constexpr (M::KCG % 4 == 0) {
-#pragma unroll
-            for (int i = 0; i < M::KCG; i += 4) {
-              const float4 v = *reinterpret_cast<const float4*>(xk + i);
-              sh0 = fmaf(wc[l][i], v.x, sh0);
-              sh1 = fmaf(wc[l][i + 1], v.y, sh1);
-              sh0 = fmaf(wc[l][i + 2], v.z, sh0);
-              sh1 = fmaf(wc[l][i + 3], v.w, sh1);
-              sg0 = fmaf(wc[l][M::KCG + i], v.x, sg0);
-              sg1 = fmaf(wc[l][M::KCG + i + 1], v.y, sg1);
-              sg0 = fmaf(wc[l][M::KCG + i + 2], v.z, sg0);
-              sg1 = fmaf(wc[l][M::KCG + i + 3], v.w, sg1);
+          lds_barrier();
+          // h_j[t] -> layer j's aux CU (skip projection)
+          {
+            // an opaque index keeps the compiler from hoisting one 64-bit address per layer
+            // out of the step loop (they would not fit in registers)
+            int ln = tid - (NT - HPW);
+            asm volatile("" : "+v"(ln));
+            if (ln >= 0 && ln < R) {
+              hpost[l % HPOST] = pack(hs[ln], tag);
+              stw(mbs + g.off_h + ((size_t)j * 2 + par) * R + ln, hpost[l % HPOST]);
             }
+          }
+          // x_j = x_{j-1} + W_res h + B_res (x_l feeds nothing); x_{j-1} is kept for the history
+          if (j < L - 1) {
+            const float xo = xs[row2], bo = bres[l * R + row2];
+            const float r =
+                wres_lds ? gsum<M::LPR2>(dot_lds_il<M::KC2, M::LPR2>(wres + (l * R + row2) * WRS + 4 * kk, hs + 4 * kk))
+                         : gsum<M::LPR2>(dot_lds<M::KC2>(wr[l < NWR ? l : 0], hs + kk * M::KC2));
+            if (kk == 0) {
+              xbuf[l * R + row2] = xo;
+              xs[row2] = xo + r + bo;
+            }
+          } else if (tid < R) {
+            xbuf[l * R + tid] = xs[tid];
+          }
+          lds_barrier();
+        }
+      }
+      // The last chain CU adds the skip projection of the last layer itself (its W_skip is in
+      // LDS), which saves the hop through that layer's aux CU on the way to the head.
+      if (tail) {
+        const int m = tid / LPRS, ks = tid % LPRS;
+        const float q = gsum<LPRS>(dot_lds_il<KCS, LPRS>(wsk + m * WSK + 4 * ks, hs + 4 * ks));
+        if (ks == 0) stw(mbs + g.off_qtail + (size_t)par * S + m, pack(q, tag));
+      }
+      // Then, one or two words per lane: x for the next chain CU, and x_{j-1} into the history
+      // slot (t mod d_j) that layer j's aux CU reads again at t + d_j.
+      {
+        const int nx = (c + 1 < g.nch) ? R : 0;
+        for (int k0 = tid; k0 < nx + nl * R; k0 += NT) {
+          if (k0 < nx) {
+            stw(mbs + g.off_x + ((size_t)(c + 1) * 2 + par) * R + k0, pack(xs[k0], tag));
           } else {
-            static_assert(M::KCG % 2 == 0, "inputs per lane must be even");
-#pragma unroll
-            for (int i = 0; i < M::KCG; i += 2) {
-              const float2 v = *reinterpret_cast<const float2*>(xk + i);
-              sh0 = fmaf(wc[l][i], v.x, sh0);
-              sh1 = fmaf(wc[l][i + 1], v.y, sh1);
-              sg0 = fmaf(wc[l][M::KCG + i], v.x, sg0);
-              sg1 = fmaf(wc[l][M::KCG + i + 1], v.y, sg1);
-            }
+            const int k = k0 - nx, l = k / R, e = k % R, j = j0 + l;
+            const int slot = slotv[par * NLCP + l];
+            stw(rings + g.d.hoff[j] + (size_t)slot * R + e, pack(xbuf[l * R + e], tag));
           }
-          ah = gsum<M::LPRG>(sh0 + sh1);
-          ag = gsum<M::LPRG>(sg0 + sg1);
         }
-        const float h = tanh_f(ah) * sigmoid_f(ag);
-        if (kq == 0) {
-          hs[g1] = h;
-        }
-        lds_barrier();
-        // h_j[t] -> layer j's aux CU (skip projection)
-        if (wave == NT / 64 - 1 && lane < R) {
-          // an opaque lane index keeps the compiler from hoisting one 64-bit address per layer
-          // out of the step loop (they would not fit in registers)
-          int ln = lane;
-          asm volatile("" : "+v"(ln));
-          hpost[l % HPOST] = pack(hs[ln], tag);
-          stw(g.mb_h + ((size_t)j * 2 + par) * R + ln, hpost[l % HPOST]);
-        }
-        // x_j = x_{j-1} + W_res h + B_res (x_l feeds nothing); x_{j-1} is kept for the history
-        if (j < L - 1) {
-          const float xo = xs[row2], bo = bres[l * R + row2];
-          const float r = gsum<M::LPR2>(dot_lds<M::KC2>(wr[l], hs + kk * M::KC2));
-          if (kk == 0) {
-            xbuf[l * R + row2] = xo;
-            xs[row2] = xo + r + bo;
-          }
-        } else if (tid < R) {
-          xbuf[l * R + tid] = xs[tid];
-        }
-        lds_barrier();
       }
-    }
-    // The last chain CU adds the skip projection of the last layer itself (its W_skip is in LDS),
-    // which saves the hop through that layer's aux CU on the way to the head.
-    if (lastc) {
-      constexpr int LPRS = NT / S, KCS = R / LPRS;
-      const int m = tid / LPRS, ks = tid % LPRS;
-      float acc0 = 0.f, acc1 = 0.f;
-      const float* wrow = wsk + m * R + ks * KCS;
-      const float* hk = hs + ks * KCS;
 #pragma unroll
-      for (int i = 0; i < KCS; i += 4) {
-        const float4 w4 = *reinterpret_cast<const float4*>(wrow + i);
-        const float4 h4 = *reinterpret_cast<const float4*>(hk + i);
-        acc0 = fmaf(w4.x, h4.x, acc0);
-        acc1 = fmaf(w4.y, h4.y, acc1);
-        acc0 = fmaf(w4.z, h4.z, acc0);
-        acc1 = fmaf(w4.w, h4.w, acc1);
-      }
-      const float q = gsum<LPRS>(acc0 + acc1);
-      if (ks == 0) stw(g.mb_qtail + (size_t)par * S + m, pack(q, tag));
+      for (int l = 0; l < HPOST; ++l) asm volatile("" ::"v"(hpost[l]));
     }
-    // Then, one or two words per lane: x for the next chain CU, and x_{j-1} into the history
-    // slot (t mod d_j) that layer j's aux CU reads again at t + d_j.
-    {
-      const int nx = (c + 1 < g.nch) ? R : 0;
-      for (int i = tid; i < nx + nl * R; i += NT) {
-        if (i < nx) {
-          stw(g.mb_x + ((size_t)(c + 1) * 2 + par) * R + i, pack(xs[i], tag));
-        } else {
-          const int k = i - nx, l = k / R, e = k % R, j = j0 + l;
-          const int slot = (int)(t % g.d.dil[j]);
-          stw(g.ring + g.d.hoff[j] + (size_t)slot * R + e, pack(xbuf[l * R + e], tag));
-        }
-      }
-    }
-#pragma unroll
-    for (int l = 0; l < HPOST; ++l) asm volatile("" ::"v"(hpost[l]));
   }
   if (first) {
     if (T > 0) {
       const int64_t tl = tg0 + T - 1;
-      poll2(g, logit_items(tl), no_items(), dyn, sy);
-      lds_barrier();
-      if (sy.failed()) return;
-      if (tl - ub0 >= UB) roll_buffers(tl);
-      sample_step(tl);
-      lds_barrier();
+      for (int i = 0; i < ns; ++i) {
+        poll2(g, logit_items(tl, b0 + i), no_items(), dyn, sy);
+        lds_barrier();
+        if (sy.failed()) return;
+        if (i == 0 && tl - ub0 >= ub) roll_buffers(tl);
+        sample_step(tl, i);
+        lds_barrier();
+      }
       roll_buffers(tg0 + T);
     }
-    if (tid == 0 && !sy.failed()) {
-      g.state[0] = tg0 + T;
-      g.state[1] = s_y;
+    if (!sy.failed()) {
+      for (int i = tid; i < ns; i += NT) {
+        g.state[2 * (size_t)(b0 + i)] = tg0 + T;
+        g.state[2 * (size_t)(b0 + i) + 1] = syv[i];
+      }
     }
   }
 }
@@ -472,16 +546,19 @@ __device__ void chain_role(const WnChainArgs& g, const int c, float* dyn, Sync s
 // ------------------------------------------------------------------------------------------
 // aux CU (one per layer): pre-activations of the next step and the skip partial
 // ------------------------------------------------------------------------------------------
-template <int R, int S, bool TF>
-__device__ void aux_role(const WnChainArgs& g, const int j, float* dyn, Sync sy, const int64_t tg0) {
+template <int R, int S, bool TF, bool MS>
+__device__ void aux_role(const WnChainArgs& g, const int j, const int b0, const int ns, float* dyn, Sync sy,
+                         const int64_t tg0) {
   using M = ChainMap<R>;
   constexpr int LPRS = NT / S, KCS = R / LPRS;
+  constexpr int CQ = (WN_CHAIN_MAX_G * 2 * R / 4 + NT - 1) / NT;  // conditioning float4s per thread
   const int tid = threadIdx.x;
   const int L = g.d.L, d = g.d.dil[j];
   const int T = g.io.T;
-  float* xp = dyn;        // R   history read
-  float* hs = xp + R;     // R
-  float* cl = hs + R;     // 2R  conditioning of the target step
+  const int G = MS ? g.G : 1;
+  float* hs = dyn;            // R     h_j of the current stream
+  float* xpg = hs + R;        // G*R   history reads x_{j-1}[ts - d] of every stream
+  float* clg = xpg + G * R;   // G*2R  conditioning rows L[b, ts, j] of every stream
 
   const int rowp = tid / M::LPR1, kq = tid % M::LPR1;
   const int rows = tid / LPRS, ks = tid % LPRS;
@@ -494,50 +571,95 @@ __device__ void aux_role(const WnChainArgs& g, const int j, float* dyn, Sync sy,
   for (int i = 0; i < KCS; ++i) wk[i] = Wk[((size_t)j * S + rows) * R + ks * KCS + i];
   const float bg = g.w.b_gate[j * 2 * R + rowp];
 
-  // pre_j[ts] = W_prev x_{j-1}[ts - d] + B + L[ts], posted with tag ts + 1
-  auto make_pre = [&](int64_t ts) {
-    const int slot = (int)(ts % d);
+  // The history slot that pre_j[ts] reads, for every stream of the replica (consecutive streams'
+  // histories are hist_len words apart).
+  auto hist_items = [&](int64_t ts) {
+    const int slot = (d == 1) ? 0 : (int)(ts % d);
     const unsigned etag = (ts - d >= 0) ? (unsigned)(ts - d + 1) : 0u;
-    poll2(g, Items{g.ring + g.d.hoff[j] + (size_t)slot * R, R, R, R, xp, etag}, no_items(), dyn, sy);
-    if (tid >= 64 && tid < 64 + 2 * R)
-      cl[tid - 64] = g.io.cond[((size_t)(ts - tg0) * L + j) * 2 * R + (tid - 64)];
-    lds_barrier();
-    if (sy.failed()) return;
-    const float a = gsum<M::LPR1>(dot_lds<M::KC1>(wp, xp + kq * M::KC1));
-    if (kq == 0)
-      stw(g.mb_pre + ((size_t)j * 2 + (ts & 1)) * 2 * R + rowp, pack(a + bg + cl[rowp], (unsigned)(ts + 1)));
-    lds_barrier();
+    return Items{g.ring + (size_t)b0 * g.d.hist_len + g.d.hoff[j] + (size_t)slot * R, R, g.d.hist_len, ns * R, xpg,
+                 etag};
   };
-
-  make_pre(tg0);
-  const bool skip_here = (j < L - 1);  // the last layer's skip projection runs on the last chain CU
-  for (int64_t t = tg0; t < tg0 + T; ++t) {
-    if (sy.failed()) return;
-    // Waiting for h_j[t] also paces this CU: once it has arrived the chain has consumed pre_j[t],
-    // so posting pre_j[t + 1] below cannot overwrite a slot the chain has yet to read.
-    poll2(g, Items{g.mb_h + ((size_t)j * 2 + (t & 1)) * R, R, R, R, hs, (unsigned)(t + 1)}, no_items(), dyn, sy);
-    lds_barrier();
-    if (sy.failed()) return;
-    if (skip_here) {
-      const float q = gsum<LPRS>(dot_lds<KCS>(wk, hs + ks * KCS));
-      if (ks == 0) stw(g.mb_q + ((size_t)j * 2 + (t & 1)) * S + rows, pack(q, (unsigned)(t + 1)));
+  // Stage the inputs of pre_j[ts] for every stream at once: the conditioning rows (one HBM round
+  // trip for all streams) and, when `hist`, the history reads.  The history of ts - d is final
+  // once step ts - d is over, so it is staged here when d >= 2 or at the call's first step; with
+  // d = 1 it is read per stream, together with h_j (both come from the same chain CU).
+  auto stage = [&](int64_t ts, bool hist) {
+    float4 cq[CQ];
+    const float* crow = g.io.cond + ((size_t)b0 * T + (size_t)(ts - tg0)) * L * 2 * R + (size_t)j * 2 * R;
+#pragma unroll
+    for (int k = 0; k < CQ; ++k) {
+      const int q = tid + k * NT;
+      if (q < ns * (2 * R / 4)) {
+        const int i = q / (2 * R / 4), e = q % (2 * R / 4);
+        cq[k] = *reinterpret_cast<const float4*>(crow + (size_t)i * T * L * 2 * R + 4 * e);
+      }
+    }
+    if (hist) poll2(g, hist_items(ts), no_items(), dyn, sy);
+#pragma unroll
+    for (int k = 0; k < CQ; ++k) {
+      const int q = tid + k * NT;
+      if (q < ns * (2 * R / 4)) reinterpret_cast<float4*>(clg)[q] = cq[k];
     }
     lds_barrier();
-    if (t + 1 < tg0 + T) make_pre(t + 1);
+  };
+  // pre_j[ts] of local stream i = W_prev x_{j-1}[ts - d] + B + L[b, ts], posted with tag ts + 1
+  auto post_pre = [&](int64_t ts, int i) {
+    const float a = gsum<M::LPR1>(dot_lds<M::KC1>(wp, xpg + i * R + kq * M::KC1));
+    if (kq == 0)
+      stw(g.mb + (size_t)(b0 + i) * g.mb_words + ((size_t)j * 2 + (ts & 1)) * 2 * R + rowp,
+          pack(a + bg + clg[i * 2 * R + rowp], (unsigned)(ts + 1)));
+  };
+
+  stage(tg0, true);
+  if (sy.failed()) return;
+  for (int i = 0; i < ns; ++i) post_pre(tg0, i);
+  // the last layer's skip projection runs on the last chain CU when it has room for W_skip
+  const bool skip_here = (j < L - 1) || !g.tail_on_chain;
+  for (int64_t t = tg0; t < tg0 + T; ++t) {
+    const bool more = (t + 1 < tg0 + T);
+    lds_barrier();
+    if (more) stage(t + 1, d >= 2);
+    if (sy.failed()) return;
+    for (int i = 0; i < ns; ++i) {
+      const int b = b0 + i;
+      u64* const mbs = g.mb + (size_t)b * g.mb_words;
+      // Waiting for h_j[t] also paces this CU: once it has arrived the chain has consumed
+      // pre_j[t], so posting pre_j[t + 1] below cannot overwrite a slot the chain has yet to read.
+      const Items hi{mbs + g.off_h + ((size_t)j * 2 + (t & 1)) * R, R, R, R, hs, (unsigned)(t + 1)};
+      if (more && d == 1) {
+        Items xi = hist_items(t + 1);
+        xi.base += (size_t)i * g.d.hist_len;
+        xi.n = R;
+        xi.dst = xpg + i * R;
+        poll2(g, hi, xi, dyn, sy);
+      } else {
+        poll2(g, hi, no_items(), dyn, sy);
+      }
+      lds_barrier();
+      if (sy.failed()) return;
+      if (skip_here) {
+        const float q = gsum<LPRS>(dot_lds<KCS>(wk, hs + ks * KCS));
+        if (ks == 0) stw(mbs + g.off_q + ((size_t)j * 2 + (t & 1)) * S + rows, pack(q, (unsigned)(t + 1)));
+      }
+      if (more) post_pre(t + 1, i);
+      lds_barrier();
+    }
   }
 }
 
 // ------------------------------------------------------------------------------------------
 // head CU: rows [64 h, 64 h + 64) of z_a and their share of the logits
 // ------------------------------------------------------------------------------------------
-template <int R, int S, bool TF>
-__device__ void head_role(const WnChainArgs& g, const int hh, float* dyn, Sync sy, const int64_t tg0) {
+template <int R, int S, bool TF, bool MS>
+__device__ void head_role(const WnChainArgs& g, const int hh, const int b0, const int ns, float* dyn, Sync sy,
+                          const int64_t tg0) {
   constexpr int LPRH = NT / HR, KCH = S / LPRH;   // W_relu: 8 lanes per row
   constexpr int LPRO = NT / A, KCO = HR / LPRO;   // W_out: 2 lanes per output
   const int tid = threadIdx.x;
   const int L = g.d.L;
   const int T = g.io.T;
-  float* qall = dyn;           // L*S skip partials of one step: layers 0..L-2, then the tail
+  const int nq = g.tail_on_chain ? L - 1 : L;  // skip partials that come from aux CUs
+  float* qall = dyn;           // L*S skip partials of one step: layers 0..nq-1, then the tail
   float* zs = qall + L * S;    // S
   float* za = zs + S;          // HR
 
@@ -556,49 +678,56 @@ __device__ void head_role(const WnChainArgs& g, const int hh, float* dyn, Sync s
   for (int64_t t = tg0; t < tg0 + T; ++t) {
     const unsigned tag = (unsigned)(t + 1);
     const int par = (int)(t & 1);
-    // all skip partials of this step: W_skip_j h_j from the aux CUs (j < l-1) and the last
-    // layer's from the last chain CU
-    poll2(g, Items{g.mb_q + (size_t)par * S, S, 2 * S, (L - 1) * S, qall, tag},
-          Items{g.mb_qtail + (size_t)par * S, S, S, S, qall + (L - 1) * S, tag}, dyn, sy);
-    lds_barrier();
-    if (sy.failed()) return;
-    // z_s = relu(B_skip + sum_j q_j), summed in layer order
-    if (tid < S) {
-      float q = bsk;
-      for (int j = 0; j < L; ++j) q += qall[j * S + tid];
-      zs[tid] = fmaxf(q, 0.f);
+    for (int i = 0; i < ns; ++i) {
+      u64* const mbs = g.mb + (size_t)(b0 + i) * g.mb_words;
+      // all skip partials of this step: W_skip_j h_j from the aux CUs and (when the last chain
+      // CU computes it) the last layer's
+      poll2<12>(g, Items{mbs + g.off_q + (size_t)par * S, S, 2 * S, nq * S, qall, tag},
+            nq < L ? Items{mbs + g.off_qtail + (size_t)par * S, S, S, S, qall + (L - 1) * S, tag} : no_items(), dyn,
+            sy);
+      lds_barrier();
+      if (sy.failed()) return;
+      // z_s = relu(B_skip + sum_j q_j), summed in layer order
+      if (tid < S) {
+        float q = bsk;
+        for (int j = 0; j < L; ++j) q += qall[j * S + tid];
+        zs[tid] = fmaxf(q, 0.f);
+      }
+      lds_barrier();
+      {
+        const float v = gsum<LPRH>(dot_lds<KCH>(wl, zs + kr * KCH));
+        if (kr == 0) za[rl] = fmaxf(v + bl, 0.f);
+      }
+      lds_barrier();
+      {
+        const float v = gsum<LPRO>(dot_lds<KCO>(wo, za + ko * KCO));
+        if (ko == 0) stw(mbs + g.off_logit + ((size_t)hh * 2 + par) * A + oo, pack(v, tag));
+      }
+      lds_barrier();
     }
-    lds_barrier();
-    {
-      const float v = gsum<LPRH>(dot_lds<KCH>(wl, zs + kr * KCH));
-      if (kr == 0) za[rl] = fmaxf(v + bl, 0.f);
-    }
-    lds_barrier();
-    {
-      const float v = gsum<LPRO>(dot_lds<KCO>(wo, za + ko * KCO));
-      if (ko == 0) stw(g.mb_logit + ((size_t)hh * 2 + par) * A + oo, pack(v, tag));
-    }
-    lds_barrier();
   }
 }
 
-template <int R, int S, int NLC, bool TF>
+template <int R, int S, int NLC, bool TF, bool MS>
 __global__ __launch_bounds__(NT) void wn_chain_kernel(const WnChainArgs g) {
   extern __shared__ __align__(16) float dyn[];
   __shared__ int s_abort;
-  const int b = blockIdx.x;
-  const int role = (b % 8) * 32 + b / 8;
-  if (role >= g.nch + NHEAD + g.d.L) return;
+  const int rb = g.role_of_block[blockIdx.x];
+  if (rb == 0xffff) return;
+  const int per = g.nch + NHEAD + g.d.L;
+  const int k = MS ? rb / per : 0, role = rb - k * per;
+  const int b0 = MS ? k * g.G : 0;
+  const int ns = MS ? min(g.G, g.io.B - b0) : 1;  // streams of this replica
+  if (ns <= 0) return;
   if (threadIdx.x == 0) s_abort = 0;
-  // where this call starts: from zero, or where the previous call on this workspace stopped
-  const int64_t tg0 = g.io.reset ? 0 : g.state[0];
-  int yprev0 = g.io.reset ? g.io.init_sample : (int)g.state[1];
-  yprev0 = yprev0 < 0 ? 0 : (yprev0 > A - 1 ? A - 1 : yprev0);
+  // where this call starts: from zero, or where the previous call on this workspace stopped (the
+  // replica's chain CU 0 rewrites its streams' state only after every role of it has started)
+  const int64_t tg0 = g.io.reset ? 0 : g.state[2 * (size_t)b0];
   __syncthreads();
   Sync sy{&s_abort};
-  if (role < g.nch) chain_role<R, S, NLC, TF>(g, role, dyn, sy, tg0, yprev0);
-  else if (role < g.nch + NHEAD) head_role<R, S, TF>(g, role - g.nch, dyn, sy, tg0);
-  else aux_role<R, S, TF>(g, role - g.nch - NHEAD, dyn, sy, tg0);
+  if (role < g.nch) chain_role<R, S, NLC, TF, MS>(g, role, b0, ns, dyn, sy, tg0);
+  else if (role < g.nch + NHEAD) head_role<R, S, TF, MS>(g, role - g.nch, b0, ns, dyn, sy, tg0);
+  else aux_role<R, S, TF, MS>(g, role - g.nch - NHEAD, b0, ns, dyn, sy, tg0);
 }
 
 // Clears the tagged histories and mailboxes and the status word before a run from zero.
@@ -609,20 +738,64 @@ __global__ void wn_chain_reset_kernel(u64* words, size_t n, int* status) {
 }
 
 template <int R>
-constexpr int chain_nlc() { return R == 64 ? 7 : 16; }
+constexpr int chain_nlc() { return R == 128 ? 2 : (R == 64 ? 7 : 16); }
+
+int nlc_for(int R) { return R == 128 ? chain_nlc<128>() : (R == 64 ? chain_nlc<64>() : chain_nlc<32>()); }
+
+// Layers of each chain CU: runs of at most nlc layers, as even as possible.  With r = 128 the
+// first CU (which also holds the embedding table) and the last (which holds the last layer's
+// W_skip) take one layer each, since two layers' W_res only fit in the LDS of the CUs between.
+int chain_split(int L, int R, int* layer_begin) {
+  const int nlc = nlc_for(R);
+  int first = 0, last = 0, mid = L;
+  if (R == 128 && L >= 2) {
+    first = 1;
+    last = 1;
+    mid = L - 2;
+  }
+  const int nmid = (mid + nlc - 1) / nlc;
+  const int nch = (first ? 1 : 0) + nmid + (last ? 1 : 0);
+  if (nch > WN_MAX_CHAIN) return nch;
+  int c = 0;
+  layer_begin[0] = 0;
+  if (first) {
+    layer_begin[1] = 1;
+    c = 1;
+  }
+  const int base = nmid ? mid / nmid : 0, extra = nmid ? mid % nmid : 0;
+  for (int k = 0; k < nmid; ++k, ++c) layer_begin[c + 1] = layer_begin[c] + base + (k < extra ? 1 : 0);
+  if (last) layer_begin[c + 1] = layer_begin[c] + 1;
+  return nch;
+}
+
+// Dynamic LDS floats of each role (the launch takes the largest); mirrors the carving in the roles.
+size_t chain_lds_floats(int R, int S, int nlc, int G, int ub, int nch, int tail) {
+  const int nlcp = (nlc + 3) & ~3;
+  const size_t common = (size_t)2 * R + (size_t)nlc * 2 * R + (size_t)2 * nlc * R + 2 * nlcp;
+  const size_t wsk = (size_t)S * lds_row_stride(R, NT / S);
+  size_t cu0 = (size_t)NHEAD * A + (size_t)2 * G * ub + ((G + 3) & ~3) + (size_t)A * R;
+  if (nch == 1 && tail) cu0 += wsk;
+  size_t var = cu0;
+  if (tail) var = std::max(var, wsk);
+  if (R == 128) var = std::max(var, (size_t)2 * R * lds_row_stride(R, NT / R));
+  return common + var;
+}
+size_t head_lds_floats(int L, int S) { return (size_t)L * S + S + HR; }
+size_t aux_lds_floats(int R, int G) { return (size_t)R + (size_t)3 * R * G; }
+constexpr size_t kMaxLds = 160 * 1024;
 
 template <int R, int S>
 hipError_t launch_chain_rs(const WnChainArgs& g, bool teacher, hipStream_t stream) {
   constexpr int NLC = chain_nlc<R>();
-  const size_t chain_lds =
-      ((size_t)2 * R + NLC * 2 * R + NHEAD * A + 2 * UB + 2 * NLC * R + (size_t)A * R + (size_t)S * R) *
-      sizeof(float);
-  const size_t head_lds = ((size_t)g.d.L * S + S + HR) * sizeof(float);
-  const size_t aux_lds = (size_t)4 * R * sizeof(float);
-  const size_t dyn = std::max(chain_lds, std::max(head_lds, aux_lds));
+  const size_t dyn = sizeof(float) * std::max(chain_lds_floats(R, S, NLC, g.G, g.ub, g.nch, g.tail_on_chain),
+                                              std::max(head_lds_floats(g.d.L, S), aux_lds_floats(R, g.G)));
   void* args[] = {const_cast<WnChainArgs*>(&g)};
-  const void* k = teacher ? reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, true>)
-                          : reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, false>);
+  // one stream (no replicas) gets a build with the stream loops folded away
+  const bool ms = g.io.B > 1;
+  const void* k = teacher ? (ms ? reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, true, true>)
+                                : reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, true, false>))
+                          : (ms ? reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, false, true>)
+                                : reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, false, false>));
   hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
   if (e != hipSuccess) return e;
   return hipLaunchCooperativeKernel(k, dim3(WN_CHAIN_GRID), dim3(NT), args, (unsigned)dyn, stream);
@@ -630,25 +803,60 @@ hipError_t launch_chain_rs(const WnChainArgs& g, bool teacher, hipStream_t strea
 
 }  // namespace
 
-int wn_chain_layers_per_cu(int R) { return R == 64 ? chain_nlc<64>() : (R == 32 ? chain_nlc<32>() : 0); }
-
 bool wn_chain_supported(int R, int S, int L) {
-  if (!((R == 64 && (S == 256 || S == 128)) || (R == 32 && S == 128))) return false;
-  const int nlc = wn_chain_layers_per_cu(R);
-  const int nch = (L + nlc - 1) / nlc;
-  return L >= 1 && L <= WN_MAX_LAYERS && nch <= WN_MAX_CHAIN && nch + NHEAD + L <= WN_CHAIN_GRID;
+  if (!((R == 128 && S == 256) || (R == 64 && (S == 256 || S == 128)) || (R == 32 && S == 128))) return false;
+  if (L < 1 || L > WN_MAX_LAYERS) return false;
+  int lb[WN_MAX_LAYERS + 2];
+  const int nch = chain_split(L, R, lb);
+  return L >= 1 && L <= WN_MAX_LAYERS && nch <= WN_MAX_CHAIN && nch + NHEAD + L <= WN_CHAIN_GRID &&
+         head_lds_floats(L, S) * sizeof(float) <= kMaxLds;
 }
 
-int wn_chain_num_cus(int L, int R) {
-  const int nlc = wn_chain_layers_per_cu(R);
-  return (L + nlc - 1) / nlc + NHEAD + L;
-}
-
-size_t wn_chain_mailbox_words(int L, int R, int S) {
-  const int nlc = wn_chain_layers_per_cu(R);
-  const int nch = (L + nlc - 1) / nlc;
-  return (size_t)L * 2 * 2 * R + (size_t)L * 2 * R + (size_t)L * 2 * S + (size_t)nch * 2 * R + (size_t)NHEAD * 2 * A +
-         (size_t)2 * S;
+bool wn_chain_plan(int L, int R, int S, int B, WnChainPlan* p) {
+  if (!p || B < 1 || !wn_chain_supported(R, S, L)) return false;
+  WnChainPlan q{};
+  const int nlc = nlc_for(R);
+  q.nch = chain_split(L, R, q.layer_begin);
+  // as many replicas as the grid holds, the streams spread evenly over them
+  const int per = q.nch + NHEAD + L;
+  const int max_rep = WN_CHAIN_GRID / per;
+  q.G = (B + std::min(B, max_rep) - 1) / std::min(B, max_rep);
+  q.nrep = (B + q.G - 1) / q.G;
+  if (q.G > WN_CHAIN_MAX_G) return false;
+  int gp = 1;
+  while (gp < q.G) gp *= 2;
+  q.ub = std::max(16, 512 / gp);
+  q.tail_on_chain = 1;
+  if (chain_lds_floats(R, S, nlc, q.G, q.ub, q.nch, 1) * sizeof(float) > kMaxLds) q.tail_on_chain = 0;
+  if (chain_lds_floats(R, S, nlc, q.G, q.ub, q.nch, q.tail_on_chain) * sizeof(float) > kMaxLds) return false;
+  // mailboxes of one stream: pre, h, q, x, logits, tail (see WnChainArgs)
+  const long long pre_w = (long long)L * 2 * 2 * R;
+  q.off_h = (int)pre_w;
+  q.off_q = q.off_h + L * 2 * R;
+  q.off_x = q.off_q + L * 2 * S;
+  q.off_logit = q.off_x + q.nch * 2 * R;
+  q.off_qtail = q.off_logit + NHEAD * 2 * A;
+  q.mb_words = ((long long)q.off_qtail + 2 * S + 31) / 32 * 32;
+  // Placement: slot i of XCD x is block 8 i + x.  Each replica's chain and head CUs go to its home
+  // XCD first, then its aux CUs, last layers first, overflowing to the XCD with the most room.
+  int used[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  constexpr int per_xcd = WN_CHAIN_GRID / 8;
+  for (int b = 0; b < WN_CHAIN_GRID; ++b) q.role_of_block[b] = 0xffff;
+  auto place = [&](int role, int home) {
+    int x = home;
+    if (used[x] >= per_xcd) {
+      for (int y = 0; y < 8; ++y)
+        if (used[y] < used[x]) x = y;
+    }
+    q.role_of_block[8 * used[x] + x] = (uint16_t)role;
+    ++used[x];
+  };
+  for (int k = 0; k < q.nrep; ++k)
+    for (int r = 0; r < q.nch + NHEAD; ++r) place(k * per + r, k % 8);
+  for (int k = 0; k < q.nrep; ++k)
+    for (int j = L - 1; j >= 0; --j) place(k * per + q.nch + NHEAD + j, k % 8);
+  *p = q;
+  return true;
 }
 
 hipError_t wn_chain_reset(unsigned long long* words, size_t n, int* status, hipStream_t stream) {
@@ -658,6 +866,7 @@ hipError_t wn_chain_reset(unsigned long long* words, size_t n, int* status, hipS
 
 hipError_t wn_chain_launch(const WnChainArgs& g, bool teacher, hipStream_t stream) {
   const int R = g.d.R, S = g.d.S;
+  if (R == 128 && S == 256) return launch_chain_rs<128, 256>(g, teacher, stream);
   if (R == 64 && S == 256) return launch_chain_rs<64, 256>(g, teacher, stream);
   if (R == 64 && S == 128) return launch_chain_rs<64, 128>(g, teacher, stream);
   if (R == 32 && S == 128) return launch_chain_rs<32, 128>(g, teacher, stream);

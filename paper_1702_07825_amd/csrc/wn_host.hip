@@ -20,9 +20,7 @@ struct wn_handle {
   void* dmem = nullptr;
   WnDims dims{};
   WnDevWeights w{};
-  bool chain_ok = false;  // the multi-CU kernel can serve B = 1
-  int nch = 0;            // its chain CUs
-  int layer_begin[WN_MAX_CHAIN + 1] = {};
+  bool chain_ok = false;  // the multi-CU kernel can serve this model (fp32, supported shape)
   bool group_ok = false;  // the batched MFMA kernel serves every B
   void* dpack = nullptr;  // its packed bf16 weight tiles
 };
@@ -72,8 +70,17 @@ class DeviceScope {
   bool ok_ = false;
 };
 
+// The multi-CU kernel's layout of B streams, if it serves them: every tagged word it polls
+// (histories, then mailboxes) must lie within 2^32 words of the first.
+bool chain_plan_for(const wn_handle* h, int B, WnChainPlan* p) {
+  if (!h->chain_ok || !wn_chain_plan(h->L, h->R, h->S, B, p)) return false;
+  return (unsigned long long)B * ((unsigned long long)h->dims.hist_len + (unsigned long long)p->mb_words) + 64 <
+         (1ull << 32);
+}
+
 int variant_for(const wn_handle* h, int B) {
-  if (B == 1 && h->chain_ok) return WN_VARIANT_CHAIN;
+  WnChainPlan p;
+  if (chain_plan_for(h, B, &p)) return WN_VARIANT_CHAIN;
   return h->group_ok ? WN_VARIANT_GROUP : WN_VARIANT_STREAM;
 }
 
@@ -88,9 +95,10 @@ WsLayout ws_layout(const wn_handle* h, int B) {
   l.status_off = 0;
   l.state_off = 256;
   l.hist_off = align_up(l.state_off + (size_t)B * 2 * sizeof(int64_t), 256);
-  if (variant_for(h, B) == WN_VARIANT_CHAIN) {
-    l.mb_off = align_up(l.hist_off + (size_t)h->dims.hist_len * 8, 256);
-    l.mb_words = wn_chain_mailbox_words(h->L, h->R, h->S);
+  WnChainPlan p;
+  if (chain_plan_for(h, B, &p)) {
+    l.mb_off = align_up(l.hist_off + (size_t)B * h->dims.hist_len * 8, 256);
+    l.mb_words = (size_t)B * p.mb_words;
     l.total = align_up(l.mb_off + l.mb_words * 8, 256);
   } else {
     l.mb_off = 0;
@@ -122,7 +130,8 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
   const WsLayout l = ws_layout(h, B);
   char* base = static_cast<char*>(ws);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (variant_for(h, B) == WN_VARIANT_CHAIN) {
+  WnChainPlan plan;
+  if (chain_plan_for(h, B, &plan)) {
     WnChainArgs g{};
     g.d = h->dims;
     g.w = h->w;
@@ -138,17 +147,21 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
     g.status = reinterpret_cast<int32_t*>(base + l.status_off);
     g.state = reinterpret_cast<int64_t*>(base + l.state_off);
     g.ring = reinterpret_cast<unsigned long long*>(base + l.hist_off);
-    unsigned long long* mb = reinterpret_cast<unsigned long long*>(base + l.mb_off);
-    const int L = h->L, R = h->R, S = h->S;
-    g.mb_pre = mb;
-    g.mb_h = g.mb_pre + (size_t)L * 2 * 2 * R;
-    g.mb_q = g.mb_h + (size_t)L * 2 * R;
-    g.mb_x = g.mb_q + (size_t)L * 2 * S;
-    g.mb_logit = g.mb_x + (size_t)h->nch * 2 * R;
-    g.mb_qtail = g.mb_logit + (size_t)4 * 2 * WN_A;
-    g.nch = h->nch;
-    for (int c = 0; c <= h->nch; ++c) g.layer_begin[c] = h->layer_begin[c];
+    g.mb = reinterpret_cast<unsigned long long*>(base + l.mb_off);
+    g.mb_words = plan.mb_words;
+    g.off_h = plan.off_h;
+    g.off_q = plan.off_q;
+    g.off_x = plan.off_x;
+    g.off_logit = plan.off_logit;
+    g.off_qtail = plan.off_qtail;
+    g.nch = plan.nch;
+    for (int c = 0; c <= plan.nch; ++c) g.layer_begin[c] = plan.layer_begin[c];
     g.spin_limit = 1 << 22;
+    g.nrep = plan.nrep;
+    g.G = plan.G;
+    g.ub = plan.ub;
+    g.tail_on_chain = plan.tail_on_chain;
+    std::memcpy(g.role_of_block, plan.role_of_block, sizeof(g.role_of_block));
     if (reset) {
       const size_t words = (l.mb_off - l.hist_off) / 8 + l.mb_words;
       const hipError_t e = wn_chain_reset(g.ring, words, g.status, st);
@@ -312,14 +325,7 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
   int cus = 0, coop = 0;
   (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device);
   (void)hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, h->device);
-  if (want_chain && !bf && wn_chain_supported(R, S, L) && cus >= WN_CHAIN_GRID && coop) {
-    const int nlc = wn_chain_layers_per_cu(R);
-    h->nch = (L + nlc - 1) / nlc;
-    const int base = L / h->nch, extra = L % h->nch;
-    h->layer_begin[0] = 0;
-    for (int c = 0; c < h->nch; ++c) h->layer_begin[c + 1] = h->layer_begin[c] + base + (c < extra ? 1 : 0);
-    h->chain_ok = true;
-  }
+  if (want_chain && !bf && wn_chain_supported(R, S, L) && cus >= WN_CHAIN_GRID && coop) h->chain_ok = true;
   // The batched MFMA kernel needs bf16 weights, r = 64 and its LDS footprint on one CU.
   int lds_max = 0;
   (void)hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device);

@@ -60,26 +60,43 @@ struct WnStreamArgs {
   WnWorkspace ws;
 };
 
-#define WN_MAX_CHAIN 16   // chain CUs of the multi-CU kernel
+#define WN_MAX_CHAIN 32   // chain CUs of one replica of the multi-CU kernel
 #define WN_CHAIN_GRID 256 // blocks of the multi-CU kernel (one per CU)
+#define WN_CHAIN_MAX_G 16 // streams one replica interleaves
 
-// Multi-CU kernel for one stream: tagged 64-bit words (value | step + 1 << 32).
+// Multi-CU kernel: tagged 64-bit words (value | step + 1 << 32).  The roles (chain, head and aux
+// CUs) form a replica; nrep replicas run side by side, replica k serving streams
+// [k G, min(B, (k + 1) G)), each interleaving its streams step by step.
 struct WnChainArgs {
   WnDims d;
   WnDevWeights w;
   WnIO io;
   int32_t* status;
-  int64_t* state;                // [2]: steps taken, last sample
-  unsigned long long* ring;      // [hist_len] tagged dilation histories
-  unsigned long long* mb_pre;    // [L][2][2R] pre-activations (aux -> chain)
-  unsigned long long* mb_h;      // [L][2][R] hidden states (chain -> aux)
-  unsigned long long* mb_q;      // [L][2][S] skip partials (aux -> head)
-  unsigned long long* mb_x;      // [nch][2][R] layer-run outputs (chain -> next chain)
-  unsigned long long* mb_logit;  // [4][2][A] partial logits (head -> chain CU 0)
-  unsigned long long* mb_qtail;  // [2][S] last layer's skip projection (last chain CU -> head)
-  int nch;                       // chain CUs
+  int64_t* state;                // [B][2]: steps taken, last sample
+  unsigned long long* ring;      // [B][hist_len] tagged dilation histories
+  unsigned long long* mb;        // [B][mb_words] mailboxes, placed after the histories
+  long long mb_words;            // words of one stream's mailbox block
+  // word offsets inside a stream's block: pre-activations [L][2][2R] (aux -> chain) at 0,
+  // hidden states [L][2][R] (chain -> aux), skip partials [L][2][S] (aux -> head),
+  // layer-run outputs [nch][2][R] (chain -> next chain), partial logits [4][2][A]
+  // (head -> chain CU 0), last layer's skip projection [2][S] (last chain CU -> head)
+  int off_h, off_q, off_x, off_logit, off_qtail;
+  int nch;                       // chain CUs per replica
   int layer_begin[WN_MAX_CHAIN + 1];
   int spin_limit;                // polls before a wait gives up with WN_ETIMEOUT
+  int nrep, G;                   // replicas, streams per replica
+  int ub;                        // steps of uniforms / samples staged in LDS per stream
+  int tail_on_chain;             // 1: the last chain CU computes the last layer's skip projection
+  uint16_t role_of_block[WN_CHAIN_GRID];  // replica * per_replica + role; 0xffff = idle block
+};
+
+// How the multi-CU kernel lays out a model and a batch over the chip.
+struct WnChainPlan {
+  int nch, nrep, G, ub, tail_on_chain;
+  int layer_begin[WN_MAX_CHAIN + 1];
+  uint16_t role_of_block[WN_CHAIN_GRID];
+  long long mb_words;
+  int off_h, off_q, off_x, off_logit, off_qtail;
 };
 
 // Kernel families.  Each returns hipSuccess or the launch error.
@@ -87,9 +104,9 @@ bool wn_stream_supported(int R, int S);
 hipError_t wn_stream_launch(const WnStreamArgs& args, bool teacher, hipStream_t stream);
 
 bool wn_chain_supported(int R, int S, int L);
-int wn_chain_layers_per_cu(int R);
-int wn_chain_num_cus(int L, int R);
-size_t wn_chain_mailbox_words(int L, int R, int S);
+// Fills *p for B streams; false if the kernel cannot serve them (too many streams per replica,
+// or a layout that does not fit).
+bool wn_chain_plan(int L, int R, int S, int B, WnChainPlan* p);
 hipError_t wn_chain_reset(unsigned long long* words, size_t n, int* status, hipStream_t stream);
 hipError_t wn_chain_launch(const WnChainArgs& g, bool teacher, hipStream_t stream);
 

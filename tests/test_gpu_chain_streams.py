@@ -1,0 +1,114 @@
+"""GPU parity of the multi-CU kernel serving several streams (fp32 weights).
+
+Replicas of the chain / head / aux roles run side by side and each interleaves
+its streams step by step; these cases cover several streams per replica, an
+uneven last replica, more steps than the kernel stages per stream, r = 128 with
+one layer per chain CU, and a single chain CU whose last-layer skip projection
+goes through the aux CU.  Bars as in test_gpu_parity: teacher-forced logits
+within 1e-3 of the oracle, indices bit-exact at every step whose oracle CDF
+margin exceeds 1e-4 (the oracle replays the GPU's own samples).
+"""
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+MARGIN = 1e-4
+
+
+def _setup(L, r, s, dil, B, T, seed, bias=0.0):
+    import paper_1702_07825_amd as wn
+    w = synth.make_weights(L, r, s, seed=seed, bias_scale=bias)
+    net = wn.WaveNet(w, dil)
+    cond = synth.make_cond(L, r, B, T, seed=seed, device="cuda")
+    u = torch.tensor(synth.make_uniforms(B, T, seed=seed), device="cuda")
+    return w, net, cond, u, oracle.Model(w, dil)
+
+
+CASES = [
+    # name, L, r, s, dilations, B, T, bias  (replicas x streams per replica in the comment)
+    ("l20_r128_b11", 20, 128, 256, tuple(synth.dilation_cycle(20)), 11, 300, 0.2),  # 4 x 3 (last 2)
+    ("l20_r64_b12", 20, 64, 256, tuple(synth.dilation_cycle(20)), 12, 300, 0.0),    # 6 x 2
+    ("l3_r128_b5", 3, 128, 256, (1, 3, 2), 5, 200, 0.3),                             # 5 x 1
+    ("l1_r128_b2", 1, 128, 256, (1,), 2, 150, 0.4),                                  # one chain CU, skip on aux
+    ("l5_r128_b3", 5, 128, 256, (2, 1, 4, 1, 3), 3, 200, 0.3),                      # chain CUs of 1, 2, 1, 1 layers
+    ("l9_r32_b40", 9, 32, 128, (1, 2, 4, 8, 16, 32, 64, 128, 256), 40, 200, 0.2),    # 14 x 3 (last 1)
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_multi_stream_chain_parity(case):
+    name, L, r, s, dil, B, T, bias = case
+    print("case %s: L=%d r=%d s=%d B=%d T=%d" % (name, L, r, s, B, T), flush=True)
+    w, net, cond, u, model = _setup(L, r, s, dil, B, T, seed=zlib.crc32(name.encode()) % 1000, bias=bias)
+    assert net.kernel_variant(B) == "multi_cu_chain"
+    ws = net.new_workspace(B)
+    y = net.generate(cond, u, workspace=ws)
+    lg = net.teacher_force(cond, y)
+    torch.cuda.synchronize()
+    assert net.status(ws) == 0
+    y_np, lg_np = y.cpu().numpy(), lg.cpu().numpy()
+    assert y_np.min() >= 0 and y_np.max() <= 255
+    ys, lo, mg = oracle.run_streams(model, cond.cpu().numpy(), u=u.cpu().numpy(), y_in=y_np, threads=8)
+    err = float(np.abs(lg_np - lo).max())
+    ok = mg > MARGIN
+    mism = int(np.sum(ys[ok] != y_np[ok]))
+    print("  max|dlogit|=%.3g confident=%d/%d mismatches=%d" % (err, int(ok.sum()), ok.size, mism), flush=True)
+    assert err <= 1e-3
+    assert mism == 0
+    net.close()
+
+
+def test_multi_stream_chain_state_and_placement():
+    """Chunked calls continue exactly; results do not depend on which replica or slot serves a stream."""
+    L, r, s, B, T = 20, 128, 256, 11, 260
+    dil = tuple(synth.dilation_cycle(L))
+    w, net, cond, u, _ = _setup(L, r, s, dil, B, T, seed=21, bias=0.1)
+    y = net.generate(cond, u)
+    y2 = net.generate(cond, u)
+    lg = net.teacher_force(cond, y)
+    ws = net.new_workspace(B)
+    parts, a = [], 0
+    for b_ in (1, 2, 129, 130, T):
+        parts.append(net.generate(cond[:, a:b_].contiguous(), u[:, a:b_].contiguous(), workspace=ws, reset=(a == 0)))
+        a = b_
+    ws2 = net.new_workspace(B)
+    lgp = [net.teacher_force(cond[:, :77].contiguous(), y[:, :77].contiguous(), workspace=ws2, reset=True),
+           net.teacher_force(cond[:, 77:].contiguous(), y[:, 77:].contiguous(), workspace=ws2, reset=False)]
+    perm = torch.tensor([10, 3, 7, 0, 9, 1, 5, 8, 2, 6, 4], device="cuda")
+    yp = net.generate(cond[perm].contiguous(), u[perm].contiguous())
+    # fewer streams: a different plan (one stream per replica) for the same first streams
+    y5 = net.generate(cond[:5].contiguous(), u[:5].contiguous())
+    torch.cuda.synchronize()
+    assert net.status(ws) == 0 and net.status(ws2) == 0
+    assert torch.equal(y, y2)
+    assert torch.equal(torch.cat(parts, 1), y)
+    assert torch.equal(torch.cat(lgp, 1), lg)
+    assert torch.equal(yp, y[perm])
+    assert torch.equal(y5, y[:5])
+    net.close()
+
+
+def test_multi_stream_chain_matches_per_stream_kernel(monkeypatch):
+    L, r, s, B, T = 20, 128, 256, 7, 120
+    dil = tuple(synth.dilation_cycle(L))
+    w, net, cond, u, _ = _setup(L, r, s, dil, B, T, seed=22, bias=0.2)
+    y = net.generate(cond, u)
+    lg = net.teacher_force(cond, y)
+    monkeypatch.setenv("WN_KERNEL", "stream")
+    import paper_1702_07825_amd as wn
+    ref = wn.WaveNet(w, dil)
+    assert ref.kernel_variant(B) == "stream_l2"
+    lg_ref = ref.teacher_force(cond, y)
+    torch.cuda.synchronize()
+    d = float((lg_ref - lg).abs().max())
+    print("  max|dlogit| chain vs per-stream kernel %.3g" % d, flush=True)
+    assert d <= 1e-4
+    ref.close()
+    net.close()
