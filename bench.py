@@ -67,17 +67,25 @@ def traffic_from_profiles(workload, variant):
     return rec.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(wl, w, cond_dev, u_np, steps):
-    import numpy as np
+def cpu_baseline(wl, w, cond_dev, u_np, min_seconds):
+    """The CPU oracle on whole streams of the workload (stream 0, 1, ...; stream 0 again when the
+    workload has one), one thread, until at least `min_seconds` of oracle time have passed."""
     import oracle
     m = oracle.Model(w, wl.dilations, bf16_weights=(wl.weight_dtype == "bf16"))
-    cond = cond_dev[0, :steps].cpu().numpy()
-    t0 = time.perf_counter()
-    oracle.run(m, cond, u=u_np[0, :steps], want_logits=False)
-    dt = time.perf_counter() - t0
-    return {"value": steps / dt, "unit": "samples/s", "cores": 1, "kind": "oracle",
-            "sample": "stream 0, first %d of %d steps, generation, single thread (fp64 C oracle)" % (steps, wl.T),
-            "seconds": round(dt, 2)}
+    steps, secs, runs = 0, 0.0, []
+    while secs < min_seconds:
+        b = len(runs) % wl.B
+        cond = cond_dev[b].cpu().numpy()
+        t0 = time.perf_counter()
+        oracle.run(m, cond, u=u_np[b], want_logits=False)
+        secs += time.perf_counter() - t0
+        steps += wl.T
+        runs.append(b)
+    which = ("stream 0, %d runs" % len(runs)) if wl.B == 1 else \
+            ("streams 0..%d" % (len(runs) - 1) if len(runs) <= wl.B else "streams 0..%d, %d runs" % (wl.B - 1, len(runs)))
+    return {"value": steps / secs, "unit": "samples/s", "cores": 1, "kind": "oracle",
+            "sample": "whole streams of %d steps (%s), generation, one thread, fp64 C oracle" % (wl.T, which),
+            "seconds": round(secs, 2)}
 
 
 def algorithmic_hbm_bytes_per_sample(wl):
@@ -168,8 +176,8 @@ def run_workload(name, args):
         "sample_histogram_entropy_bits": round(float(-(lambda p: (p[p > 0] * np.log2(p[p > 0])).sum())(
             np.bincount(y.ravel(), minlength=256) / y.size)), 3),
     }
-    if args.cpu_steps > 0:
-        out["cpu_baseline"] = cpu_baseline(wl, w, cond, u_np, min(args.cpu_steps, wl.T))
+    if args.cpu_seconds > 0:
+        out["cpu_baseline"] = cpu_baseline(wl, w, cond, u_np, args.cpu_seconds)
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)
@@ -184,11 +192,15 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="l20_r64_b1", help="a workload name, or 'all' (one JSON line each)")
-    ap.add_argument("--cpu-steps", type=int, default=8000, help="oracle sample size (0 = skip)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="least oracle time for the CPU baseline, in whole streams (0 = skip)")
+    ap.add_argument("--cpu-steps", type=int, default=None, choices=[0], help="0: skip the CPU baseline")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run one device-to-device copy of BYTES (calibrates HBM byte counters) and exit")
     args = ap.parse_args()
+    if args.cpu_steps == 0:
+        args.cpu_seconds = 0.0
     if args.copy_probe:
         import torch
         src = torch.ones(args.copy_probe // 4, dtype=torch.float32, device="cuda:0")

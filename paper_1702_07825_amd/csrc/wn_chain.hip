@@ -157,28 +157,21 @@ struct ChainMap {
   static_assert(LPR1 >= 1 && KC1 % 2 == 0 && KC2 >= 2 && KCG >= 2, "unsupported R");
   // r = 128 keeps W_res of one layer in VGPRs; a CU with two layers keeps both W_res in LDS
   static constexpr int WRV = (R == 128) ? 1 : 1 << 30;
+  // r = 128 uses 8-lane groups instead: group q holds gate pairs 2q, 2q + 1 (W_cur) and rows
+  // 2q, 2q + 1 (W_res); lane i of a group takes the inputs 4 (i + 8 m) .. + 3, m < R / 32.
+  static constexpr bool G8 = (R == 128);
+  static constexpr int CPL = R / 32;  // float4 input chunks per lane in the 8-lane layout
 };
 
-// Row stride (floats) of a matrix kept in LDS and read as float4 chunks by `lanes` lanes per row,
-// lane k taking chunks k, k + lanes, ...: consecutive rows start 4 * lanes banks apart, so the 16
-// lanes of a 64-bank access phase hit distinct banks.
-constexpr int lds_row_stride(int K, int lanes) { return K + ((4 * lanes - K % 64) % 64 + 64) % 64; }
-
-// Dot product of K-long LDS rows read as interleaved float4 chunks (stride 4 * STEP floats).
-template <int K, int STEP>
-__device__ __forceinline__ float dot_lds_il(const float* w, const float* x) {
-  float s0 = 0.f, s1 = 0.f;
-#pragma unroll
-  for (int i = 0; i < K / 4; ++i) {
-    const float4 a = *reinterpret_cast<const float4*>(w + 4 * STEP * i);
-    const float4 v = *reinterpret_cast<const float4*>(x + 4 * STEP * i);
-    s0 = fmaf(a.x, v.x, s0);
-    s1 = fmaf(a.y, v.y, s1);
-    s0 = fmaf(a.z, v.z, s0);
-    s1 = fmaf(a.w, v.w, s1);
-  }
-  return s0 + s1;
+// Row stride (floats) of a matrix kept in LDS and read by 8-lane groups, lane i of a group taking
+// the float4 chunks i, i + 8, ... of a row and group g + 1 reading the row `rows` after group g's:
+// the two groups of a 16-lane access phase then hit the two halves of the 64 banks.
+constexpr int lds_row_stride(int K, int rows) {
+  int w = K;
+  while ((rows * w) % 64 != 32) ++w;
+  return w;
 }
+
 
 template <int K>
 __device__ __forceinline__ float dot_lds(const float (&w)[K], const float* x) {
@@ -233,9 +226,11 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
   const int ub = MS ? g.ub : 512, ubs = MS ? __builtin_ctz(g.ub) : 9;
 
   constexpr int NLCP = (NLC + 3) & ~3;
-  constexpr int LPRS = NT / S, KCS = R / LPRS;    // tail skip projection: lanes per row, inputs per lane
-  constexpr int WSK = lds_row_stride(R, LPRS);    // W_skip row stride in LDS
-  constexpr int WRS = lds_row_stride(R, M::LPR2); // W_res row stride in LDS
+  constexpr int RPG = S / 64;                     // tail skip projection: rows per 8-lane group
+  constexpr int WSK = lds_row_stride(R, RPG);     // W_skip row stride in LDS
+  constexpr int WRS = lds_row_stride(R, 2);       // W_res row stride in LDS (r = 128)
+  const int gq = tid >> 3, li = tid & 7;          // 8-lane group and lane in it
+  const bool upper = (li & 4) != 0;
   // LDS: the part every chain CU uses, then a part that depends on the CU's place in the chain
   float* xs = dyn;                                  // R      x_{j-1}, updated in place
   float* hs = xs + R;                               // R
@@ -243,7 +238,11 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
   float* xbuf = pre + NLC * 2 * R;                  // NLC*R  x_{j-1} of this step (history writes)
   float* bres = xbuf + NLC * R;                     // NLC*R  B_res of my layers
   int* slotv = reinterpret_cast<int*>(bres + NLC * R);  // 2*NLCP history slot (t mod d) of each layer, by step parity
-  float* var = reinterpret_cast<float*>(slotv + 2 * NLCP);
+  // dilation and history offset of each of my layers (a kernel-argument array indexed at run time
+  // would be read from memory, and the wait for that read also waits for this wave's stores)
+  int* ldil = slotv + 2 * NLCP;                     // NLCP
+  int* lhoff = ldil + NLCP;                         // NLCP
+  float* var = reinterpret_cast<float*>(lhoff + NLCP);
   // chain CU 0: partial logits, staged inputs and samples, last samples, the embedding table
   float* lgp = var;                                 // NHEAD*A
   float* ubuf = lgp + NHEAD * A;                    // G*ub   uniforms / samples in, per stream
@@ -267,10 +266,23 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
 #pragma unroll
   for (int l = 0; l < NLC; ++l) {
     const int j = j0 + (l < nl ? l : 0);
+    if constexpr (M::G8) {
+      // rows tanh 2q, sigmoid 2q, tanh 2q + 1, sigmoid 2q + 1; chunk m of each
 #pragma unroll
-    for (int i = 0; i < M::KCG; ++i) {
-      wc[l][i] = Wc[((size_t)j * 2 * R + g1) * R + kq * M::KCG + i];
-      wc[l][M::KCG + i] = Wc[((size_t)j * 2 * R + g1 + R) * R + kq * M::KCG + i];
+      for (int rr = 0; rr < 4; ++rr) {
+        const int row = 2 * gq + (rr >> 1) + (rr & 1) * R;
+#pragma unroll
+        for (int m = 0; m < M::CPL; ++m)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            wc[l][(rr * M::CPL + m) * 4 + e] = Wc[((size_t)j * 2 * R + row) * R + 4 * (li + 8 * m) + e];
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < M::KCG; ++i) {
+        wc[l][i] = Wc[((size_t)j * 2 * R + g1) * R + kq * M::KCG + i];
+        wc[l][M::KCG + i] = Wc[((size_t)j * 2 * R + g1 + R) * R + kq * M::KCG + i];
+      }
     }
   }
   if (wres_lds) {
@@ -282,12 +294,26 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
 #pragma unroll
     for (int l = 0; l < NWR; ++l) {
       const int j = j0 + (l < nl ? l : 0);
+      if constexpr (M::G8) {
 #pragma unroll
-      for (int i = 0; i < M::KC2; ++i) wr[l][i] = Wr[((size_t)j * R + row2) * R + kk * M::KC2 + i];
+        for (int rr = 0; rr < 2; ++rr)
+#pragma unroll
+          for (int m = 0; m < M::CPL; ++m)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              wr[l][(rr * M::CPL + m) * 4 + e] = Wr[((size_t)j * R + 2 * gq + rr) * R + 4 * (li + 8 * m) + e];
+      } else {
+#pragma unroll
+        for (int i = 0; i < M::KC2; ++i) wr[l][i] = Wr[((size_t)j * R + row2) * R + kk * M::KC2 + i];
+      }
     }
   }
   for (int i = tid; i < nl * R; i += NT) bres[i] = g.w.b_res[(size_t)j0 * R + i];
-  if (tid < nl) slotv[(tg0 & 1) * NLCP + tid] = (int)(tg0 % g.d.dil[j0 + tid]);
+  if (tid < nl) {
+    slotv[(tg0 & 1) * NLCP + tid] = (int)(tg0 % g.d.dil[j0 + tid]);
+    ldil[tid] = g.d.dil[j0 + tid];
+    lhoff[tid] = g.d.hoff[j0 + tid];
+  }
   float bemb = 0.f;
   float4 bout4 = make_float4(0.f, 0.f, 0.f, 0.f);  // B_out of the 4 logits lane l of wave 0 draws from
   if (tail) {
@@ -412,7 +438,7 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
       // parity were last read during step t - 1, which every thread has left)
       if (i == 0 && tid < nl) {
         const int sl = slotv[par * NLCP + tid] + 1;
-        slotv[(par ^ 1) * NLCP + tid] = (sl == g.d.dil[j0 + tid]) ? 0 : sl;
+        slotv[(par ^ 1) * NLCP + tid] = (sl == ldil[tid]) ? 0 : sl;
       }
 
       // Store data of the per-layer h posts, rotating over HPOST register pairs: a pair is written
@@ -427,10 +453,37 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
       for (int l = 0; l < NLC; ++l) {
         if (l < nl) {
           const int j = j0 + l;
-          // a = W_cur x + pre ; h = tanh(a[0:R]) * sigmoid(a[R:2R]).  Each lane has both rows of its
-          // pair; lane 0 of the group starts its partial sums from pre, so pre joins the reduction.
-          float ah, ag;
-          {
+          // a = W_cur x + pre ; h = tanh(a[0:R]) * sigmoid(a[R:2R]).  Each lane ends with both rows
+          // of a pair; the first lane of a group starts its partial sums from pre, so pre joins
+          // the reduction.
+          if constexpr (M::G8) {
+            float p[4][2];
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) p[rr][0] = p[rr][1] = 0.f;
+            if (li == 0) {
+#pragma unroll
+              for (int rr = 0; rr < 4; ++rr) p[rr][0] = pre[l * 2 * R + 2 * gq + (rr >> 1) + (rr & 1) * R];
+            }
+#pragma unroll
+            for (int m = 0; m < M::CPL; ++m) {
+              const float4 v = *reinterpret_cast<const float4*>(xs + 4 * (li + 8 * m));
+#pragma unroll
+              for (int rr = 0; rr < 4; ++rr) {
+                const float* w = &wc[l][(rr * M::CPL + m) * 4];
+                p[rr][0] = fmaf(w[0], v.x, p[rr][0]);
+                p[rr][1] = fmaf(w[1], v.y, p[rr][1]);
+                p[rr][0] = fmaf(w[2], v.z, p[rr][0]);
+                p[rr][1] = fmaf(w[3], v.w, p[rr][1]);
+              }
+            }
+            // lower four lanes: pair 2q, upper four: pair 2q + 1
+            float ah, ag;
+            xsplit8_2(p[0][0] + p[0][1], p[1][0] + p[1][1], p[2][0] + p[2][1], p[3][0] + p[3][1], upper, ah, ag);
+            ah = gsum4(ah);
+            ag = gsum4(ag);
+            const float h = tanh_f(ah) * sigmoid_f(ag);
+            if ((li & 3) == 0) hs[2 * gq + (upper ? 1 : 0)] = h;
+          } else {
             float sh0 = 0.f, sh1 = 0.f, sg0 = 0.f, sg1 = 0.f;
             if (kq == 0) {
               sh0 = pre[l * 2 * R + g1];
@@ -461,15 +514,59 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
                 sg1 = fmaf(wc[l][M::KCG + i2 + 1], v.y, sg1);
               }
             }
-            ah = gsum<M::LPRG>(sh0 + sh1);
-            ag = gsum<M::LPRG>(sg0 + sg1);
-          }
-          const float h = tanh_f(ah) * sigmoid_f(ag);
-          if (kq == 0) {
-            hs[g1] = h;
+            const float ah = gsum<M::LPRG>(sh0 + sh1);
+            const float ag = gsum<M::LPRG>(sg0 + sg1);
+            const float h = tanh_f(ah) * sigmoid_f(ag);
+            if (kq == 0) hs[g1] = h;
           }
           lds_barrier();
-          // h_j[t] -> layer j's aux CU (skip projection)
+          // x_j = x_{j-1} + W_res h + B_res (x_l feeds nothing); x_{j-1} is kept for the history
+          if (j < L - 1) {
+            if constexpr (M::G8) {
+              // lower four lanes: row 2q, upper four: row 2q + 1
+              float r0 = 0.f, r1 = 0.f;
+              if (wres_lds) {
+                const float* w0 = wres + (l * R + 2 * gq) * WRS;
+#pragma unroll
+                for (int m = 0; m < M::CPL; ++m) {
+                  const int k = 4 * (li + 8 * m);
+                  const float4 v = *reinterpret_cast<const float4*>(hs + k);
+                  const float4 a = *reinterpret_cast<const float4*>(w0 + k);
+                  const float4 b = *reinterpret_cast<const float4*>(w0 + WRS + k);
+                  r0 = fmaf(a.x, v.x, fmaf(a.y, v.y, fmaf(a.z, v.z, fmaf(a.w, v.w, r0))));
+                  r1 = fmaf(b.x, v.x, fmaf(b.y, v.y, fmaf(b.z, v.z, fmaf(b.w, v.w, r1))));
+                }
+              } else {
+                const float* w = wr[l < NWR ? l : 0];
+#pragma unroll
+                for (int m = 0; m < M::CPL; ++m) {
+                  const float4 v = *reinterpret_cast<const float4*>(hs + 4 * (li + 8 * m));
+                  const float* a = w + m * 4;
+                  const float* b = w + (M::CPL + m) * 4;
+                  r0 = fmaf(a[0], v.x, fmaf(a[1], v.y, fmaf(a[2], v.z, fmaf(a[3], v.w, r0))));
+                  r1 = fmaf(b[0], v.x, fmaf(b[1], v.y, fmaf(b[2], v.z, fmaf(b[3], v.w, r1))));
+                }
+              }
+              const float r = gsum4(xsplit8_1(r0, r1, upper));
+              const int row = 2 * gq + (upper ? 1 : 0);
+              if ((li & 3) == 0) {
+                const float xo = xs[row];
+                xbuf[l * R + row] = xo;
+                xs[row] = xo + r + bres[l * R + row];
+              }
+            } else {
+              const float xo = xs[row2], bo = bres[l * R + row2];
+              const float r = gsum<M::LPR2>(dot_lds<M::KC2>(wr[l < NWR ? l : 0], hs + kk * M::KC2));
+              if (kk == 0) {
+                xbuf[l * R + row2] = xo;
+                xs[row2] = xo + r + bo;
+              }
+            }
+          } else if (tid < R) {
+            xbuf[l * R + tid] = xs[tid];
+          }
+          // h_j[t] -> layer j's aux CU (skip projection), after this wave's share of the residual
+          // product so that its LDS read does not hold up the barrier below
           {
             // an opaque index keeps the compiler from hoisting one 64-bit address per layer
             // out of the step loop (they would not fit in registers)
@@ -480,27 +577,29 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
               stw(mbs + g.off_h + ((size_t)j * 2 + par) * R + ln, hpost[l % HPOST]);
             }
           }
-          // x_j = x_{j-1} + W_res h + B_res (x_l feeds nothing); x_{j-1} is kept for the history
-          if (j < L - 1) {
-            const float xo = xs[row2], bo = bres[l * R + row2];
-            const float r =
-                wres_lds ? gsum<M::LPR2>(dot_lds_il<M::KC2, M::LPR2>(wres + (l * R + row2) * WRS + 4 * kk, hs + 4 * kk))
-                         : gsum<M::LPR2>(dot_lds<M::KC2>(wr[l < NWR ? l : 0], hs + kk * M::KC2));
-            if (kk == 0) {
-              xbuf[l * R + row2] = xo;
-              xs[row2] = xo + r + bo;
-            }
-          } else if (tid < R) {
-            xbuf[l * R + tid] = xs[tid];
-          }
           lds_barrier();
         }
       }
       // The last chain CU adds the skip projection of the last layer itself (its W_skip is in
       // LDS), which saves the hop through that layer's aux CU on the way to the head.
       if (tail) {
-        const int m = tid / LPRS, ks = tid % LPRS;
-        const float q = gsum<LPRS>(dot_lds_il<KCS, LPRS>(wsk + m * WSK + 4 * ks, hs + 4 * ks));
+        // group q: rows RPG q .. RPG q + RPG - 1; lane i: chunks i, i + 8, ... of each row
+        float p[RPG];
+#pragma unroll
+        for (int rr = 0; rr < RPG; ++rr) p[rr] = 0.f;
+#pragma unroll
+        for (int m = 0; m < R / 32; ++m) {
+          const int k = 4 * (li + 8 * m);
+          const float4 v = *reinterpret_cast<const float4*>(hs + k);
+#pragma unroll
+          for (int rr = 0; rr < RPG; ++rr) {
+            const float4 a = *reinterpret_cast<const float4*>(wsk + (RPG * gq + rr) * WSK + k);
+            p[rr] = fmaf(a.x, v.x, fmaf(a.y, v.y, fmaf(a.z, v.z, fmaf(a.w, v.w, p[rr]))));
+          }
+        }
+        const float q = xreduce8<RPG>(p, li);
+        const int m = RPG * gq + (upper ? RPG / 2 : 0) + (RPG == 4 && (li & 2) ? 1 : 0);
+        const int ks = (RPG == 4) ? (li & 1) : (li & 3);  // lanes holding the same row: post once
         if (ks == 0) stw(mbs + g.off_qtail + (size_t)par * S + m, pack(q, tag));
       }
       // Then, one or two words per lane: x for the next chain CU, and x_{j-1} into the history
@@ -511,9 +610,9 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
           if (k0 < nx) {
             stw(mbs + g.off_x + ((size_t)(c + 1) * 2 + par) * R + k0, pack(xs[k0], tag));
           } else {
-            const int k = k0 - nx, l = k / R, e = k % R, j = j0 + l;
+            const int k = k0 - nx, l = k / R, e = k % R;
             const int slot = slotv[par * NLCP + l];
-            stw(rings + g.d.hoff[j] + (size_t)slot * R + e, pack(xbuf[l * R + e], tag));
+            stw(rings + lhoff[l] + (size_t)slot * R + e, pack(xbuf[l * R + e], tag));
           }
         }
       }
@@ -771,13 +870,13 @@ int chain_split(int L, int R, int* layer_begin) {
 // Dynamic LDS floats of each role (the launch takes the largest); mirrors the carving in the roles.
 size_t chain_lds_floats(int R, int S, int nlc, int G, int ub, int nch, int tail) {
   const int nlcp = (nlc + 3) & ~3;
-  const size_t common = (size_t)2 * R + (size_t)nlc * 2 * R + (size_t)2 * nlc * R + 2 * nlcp;
-  const size_t wsk = (size_t)S * lds_row_stride(R, NT / S);
+  const size_t common = (size_t)2 * R + (size_t)nlc * 2 * R + (size_t)2 * nlc * R + 4 * nlcp;
+  const size_t wsk = (size_t)S * lds_row_stride(R, S / 64);
   size_t cu0 = (size_t)NHEAD * A + (size_t)2 * G * ub + ((G + 3) & ~3) + (size_t)A * R;
   if (nch == 1 && tail) cu0 += wsk;
   size_t var = cu0;
   if (tail) var = std::max(var, wsk);
-  if (R == 128) var = std::max(var, (size_t)2 * R * lds_row_stride(R, NT / R));
+  if (R == 128) var = std::max(var, (size_t)2 * R * lds_row_stride(R, 2));
   return common + var;
 }
 size_t head_lds_floats(int L, int S) { return (size_t)L * S + S + HR; }

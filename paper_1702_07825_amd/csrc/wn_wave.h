@@ -22,6 +22,38 @@ __device__ __forceinline__ float gsum(float v) {
   else if constexpr (N == 8) return gsum8(v);
   else return gsum16(v);
 }
+// Transposed reductions over aligned 8-lane groups.  Each lane holds partial sums of several rows;
+// a step pairs lane i with lane 7 - i (row_half_mirror) and each lane keeps half of the rows, adding
+// its partner's partial of the rows it keeps, so the rows spread over the lanes instead of every
+// lane summing every row.  `upper` is bit 2 of the lane index.
+// Rows (a0, a1) and (b0, b1): the lower four lanes end with the sums of a0, a1 over their mirror
+// pair, the upper four with b0, b1.
+__device__ __forceinline__ void xsplit8_2(float a0, float a1, float b0, float b1, bool upper, float& k0, float& k1) {
+  k0 = (upper ? b0 : a0) + dpp<0x141>(upper ? a0 : b0);
+  k1 = (upper ? b1 : a1) + dpp<0x141>(upper ? a1 : b1);
+}
+// Rows a, b: the lower four lanes end with a, the upper four with b (over the mirror pair).
+__device__ __forceinline__ float xsplit8_1(float a, float b, bool upper) {
+  return (upper ? b : a) + dpp<0x141>(upper ? a : b);
+}
+// Full sums over the 8 lanes of N rows v[0..N-1] (N = 2 or 4): lane i ends with row
+// (i >> 2 & 1) * N / 2 + (N == 4 ? (i >> 1 & 1) : 0); lanes differing only in the lowest bit
+// (and, for N = 2, bit 1) hold the same row.
+template <int N>
+__device__ __forceinline__ float xreduce8(const float (&v)[N], int li) {
+  const bool up = (li & 4) != 0;
+  if constexpr (N == 2) {
+    return gsum4(xsplit8_1(v[0], v[1], up));
+  } else {
+    static_assert(N == 4, "two or four rows");
+    float k0, k1;
+    xsplit8_2(v[0], v[1], v[2], v[3], up, k0, k1);
+    const bool up2 = (li & 2) != 0;
+    const float k = (up2 ? k1 : k0) + dpp<0x4E>(up2 ? k0 : k1);  // quad_perm 2,3,0,1
+    return gsum2(k);
+  }
+}
+
 // Inclusive prefix sum over the 64 lanes of a wave: row scans by row_shr, then row broadcasts.
 __device__ __forceinline__ float wave_incl_scan(float v) {
   v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x111, 0xf, 0xf, true));
