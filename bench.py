@@ -211,8 +211,8 @@ def main():
         print(json.dumps({"copy_probe_bytes": args.copy_probe}))
         return
     if args.gpus != 1:
-        print("bench.py: this build runs on one GPU only (streams are independent; see DESIGN.md for how "
-              "the batched workloads would shard); --gpus %d is not supported" % args.gpus, file=sys.stderr)
+        print("bench.py: runs on one GPU only; --gpus %d is not supported (streams are independent, so a "
+              "batch would shard by stream, each GPU holding a weight replica)" % args.gpus, file=sys.stderr)
         sys.exit(2)
     import synth
     names = list(synth.WORKLOADS) if args.workload == "all" else [args.workload]

@@ -12,7 +12,7 @@
  * 1x1 convolutions and the softmax), and it keeps one history buffer per layer
  * so that nothing is recomputed (Section 5, "Optimizing Inference").
  *
- * Readings of the paper taken here (each one is listed in the design doc):
+ * Readings of the paper taken here:
  *  - residual: x^(j) = x^(j-1) + W_res h^(j) + B_res (appendix equation; the CPU
  *    section's x^(j) = W_res h^(j) + B_res is read as shorthand);
  *  - input embedding: one table, x^(0)_t = E[y_{t-1}] + B_embed;
