@@ -67,6 +67,11 @@ def lib():
             L.oracle_run.argtypes = [ctypes.POINTER(_Model), ctypes.POINTER(_State), ctypes.c_int, ctypes.c_longlong,
                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                      ctypes.c_void_p, ctypes.c_void_p]
+            L.oracle_run_sampled.restype = ctypes.c_int
+            L.oracle_run_sampled.argtypes = L.oracle_run.argtypes + [ctypes.c_int, ctypes.c_double, ctypes.c_int]
+            L.oracle_sample.restype = ctypes.c_int
+            L.oracle_sample.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_float, ctypes.c_int, ctypes.c_double,
+                                        ctypes.c_int, ctypes.c_void_p]
             L.oracle_draw.restype = ctypes.c_int
             L.oracle_draw.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
             L.oracle_history_len.restype = ctypes.c_longlong
@@ -136,11 +141,18 @@ class State:
         return int(self._s.last_sample)
 
 
+# Ways of using the output distribution (Appendix "Sampling from Output Distribution"):
+# (mode, temperature, top_k) with mode 0 direct, 1 temperature, 2 top k, 3 mode (argmax), 4 mean.
+DIRECT = (0, 1.0, 256)
+SAMPLE_MODES = {"direct": 0, "temperature": 1, "top_k": 2, "mode": 3, "mean": 4}
+
+
 def run(model: Model, cond: np.ndarray, u: Optional[np.ndarray] = None, y_in: Optional[np.ndarray] = None,
-        state: Optional[State] = None, want_logits: bool = True):
+        state: Optional[State] = None, want_logits: bool = True, sampler=DIRECT):
     """Run one stream for T = cond.shape[0] steps.
 
-    Generation if ``y_in`` is None (needs ``u``), else teacher forcing on ``y_in``.
+    Generation if ``y_in`` is None (needs ``u``), else teacher forcing on ``y_in``.  Draws use
+    ``sampler`` = (mode, temperature, top_k).
     Returns (samples int32 [T] or None, logits float64 [T, a] or None, margins float64 [T] or None).
     """
     cond = np.ascontiguousarray(cond, dtype=np.float32)
@@ -157,21 +169,23 @@ def run(model: Model, cond: np.ndarray, u: Optional[np.ndarray] = None, y_in: Op
     samples = np.zeros(T, np.int32) if (mode == 0 or u is not None) else None
     logits = np.zeros((T, model.a), np.float64) if want_logits else None
     margins = np.zeros(T, np.float64) if u is not None else None
-    rc = lib().oracle_run(ctypes.byref(model._m), None if state is None else ctypes.byref(state._s), mode, T,
-                          _ptr(cond), _ptr(u), _ptr(y_in), _ptr(samples), _ptr(logits), _ptr(margins))
+    smode, temp, top_k = sampler
+    rc = lib().oracle_run_sampled(ctypes.byref(model._m), None if state is None else ctypes.byref(state._s), mode, T,
+                                  _ptr(cond), _ptr(u), _ptr(y_in), _ptr(samples), _ptr(logits), _ptr(margins),
+                                  int(smode), float(temp), int(top_k))
     if rc != 0:
         raise RuntimeError("oracle_run failed with %d" % rc)
     return samples, logits, margins
 
 
 def run_streams(model: Model, cond: np.ndarray, u: Optional[np.ndarray] = None, y_in: Optional[np.ndarray] = None,
-                want_logits: bool = True, threads: int = 1):
+                want_logits: bool = True, threads: int = 1, sampler=DIRECT):
     """``run`` over the leading stream axis of cond [B, T, l, 2r]; streams go to ``threads`` host threads."""
     B = cond.shape[0]
 
     def one(b):
         return run(model, cond[b], None if u is None else u[b], None if y_in is None else y_in[b],
-                   want_logits=want_logits)
+                   want_logits=want_logits, sampler=sampler)
 
     if threads <= 1:
         res = [one(b) for b in range(B)]
@@ -192,6 +206,18 @@ def draw(logits: np.ndarray, u: float):
     mg = ctypes.c_double(0.0)
     y = lib().oracle_draw(lg.shape[0], _ptr(lg), ctypes.c_float(float(u)), _ptr(p), ctypes.byref(mg))
     return int(y), p, float(mg.value)
+
+
+def sample(logits: np.ndarray, u: float, sampler=DIRECT):
+    """One step's result under ``sampler`` = (mode, temperature, top_k): returns (index, margin)."""
+    lg = np.ascontiguousarray(logits, dtype=np.float64)
+    mg = ctypes.c_double(0.0)
+    smode, temp, top_k = sampler
+    y = lib().oracle_sample(lg.shape[0], _ptr(lg), ctypes.c_float(float(u)), int(smode), float(temp), int(top_k),
+                            ctypes.byref(mg))
+    if y < 0:
+        raise ValueError("invalid sampler %r" % (sampler,))
+    return int(y), float(mg.value)
 
 
 def round_bf16(x: np.ndarray) -> np.ndarray:

@@ -202,19 +202,107 @@ int oracle_draw(int a, const double *logits, float u, double *prob, double *marg
 }
 
 /*
+ * The other ways of using the output distribution that the paper lists beside
+ * direct sampling (Appendix A.4, "Sampling from Output Distribution"), each
+ * taken from its definition there:
+ *   mode 0  direct:       draw from P                      (oracle_draw above)
+ *   mode 1  temperature:  draw from P^(1/t) / Z, i.e. from softmax(logits / t)
+ *   mode 2  top k:        draw from P restricted to the classes whose P is at
+ *                         least the k-th largest P (ties at the k-th are kept),
+ *                         renormalised; P is ordered as the logits are
+ *   mode 3  mode:         argmax P (the smallest index among equal maxima)
+ *   mode 4  mean:         E_P[y] = sum_k k P(k), taken to the nearest class
+ *                         index (halves go up); the paper gives no rounding
+ * A draw is an inverse CDF as in oracle_draw: y = #{k <= a-2 : C_k <= u} with
+ * the CDF rounded to float, where C_k sums the distribution actually sampled.
+ * *margin receives how far the result is from changing: the distance of u from
+ * the nearest C_k (modes 0-2), also the gap between the k-th and (k+1)-th
+ * largest logits (mode 2, k < a), the gap between the two largest logits
+ * (mode 3), or the distance of the mean from the nearest half-integer (mode 4).
+ * Returns the index, or -1 for an invalid mode, temperature or k.
+ */
+int oracle_sample(int a, const double *logits, float u, int mode, double temperature, int top_k, double *margin) {
+    if (mode == 0) return oracle_draw(a, logits, u, NULL, margin);
+    if (mode < 0 || mode > 4 || (mode == 1 && !(temperature > 0.0)) || (mode == 2 && (top_k < 1 || top_k > a)))
+        return -1;
+    double *w = malloc(sizeof(double) * (size_t)a);
+    if (!w) return -1;
+    int y = 0;
+    double best = 1e300;
+    if (mode == 3) {
+        for (int k = 1; k < a; ++k) if (logits[k] > logits[y]) y = k;
+        for (int k = 0; k < a; ++k) {
+            double gap = logits[y] - logits[k];
+            if (k != y && gap < best) best = gap;
+        }
+    } else {
+        /* weights proportional to the distribution sampled */
+        double mx = -1e300;
+        for (int k = 0; k < a; ++k) {
+            double v = (mode == 1) ? logits[k] / temperature : logits[k];
+            if (v > mx) mx = v;
+        }
+        for (int k = 0; k < a; ++k) w[k] = exp(((mode == 1) ? logits[k] / temperature : logits[k]) - mx);
+        int last_kept = a - 1;
+        if (mode == 2) {
+            /* the k-th largest logit, by selection over a sorted copy */
+            double *srt = malloc(sizeof(double) * (size_t)a);
+            if (!srt) { free(w); return -1; }
+            memcpy(srt, logits, sizeof(double) * (size_t)a);
+            for (int i = 1; i < a; ++i) {  /* insertion sort, descending */
+                double v = srt[i];
+                int j = i - 1;
+                while (j >= 0 && srt[j] < v) { srt[j + 1] = srt[j]; --j; }
+                srt[j + 1] = v;
+            }
+            const double kth = srt[top_k - 1];
+            if (top_k < a) best = kth - srt[top_k];
+            free(srt);
+            for (int k = 0; k < a; ++k) if (logits[k] < kth) w[k] = 0.0;
+            while (last_kept > 0 && w[last_kept] == 0.0) --last_kept;
+        }
+        double z = 0.0;
+        for (int k = 0; k < a; ++k) z += w[k];
+        if (mode == 4) {
+            double mean = 0.0;
+            for (int k = 0; k < a; ++k) mean += (double)k * (w[k] / z);
+            y = (int)floor(mean + 0.5);
+            if (y > a - 1) y = a - 1;
+            best = fabs(mean - (floor(mean) + 0.5));
+        } else {
+            double cdf = 0.0;
+            for (int k = 0; k < a; ++k) {
+                cdf += w[k] / z;
+                if (k <= a - 2) {
+                    if ((float)cdf <= u) y += 1;
+                    double gap = fabs((double)u - cdf);
+                    if (gap < best) best = gap;
+                }
+            }
+            if (y > last_kept) y = last_kept;  /* only by rounding: C at the last kept class is 1 */
+        }
+    }
+    free(w);
+    if (margin) *margin = best;
+    return y;
+}
+
+/*
  * Run T steps of one stream.
  *   mode 0 (generate): y_{t} is drawn from step t's distribution with u[t] and
  *                      fed back; samples_out[t] receives it.
  *   mode 1 (teacher forcing): step t consumes y_in[t-1] (y_in[-1] is the state's
  *                      last sample); samples_out, if given, receives the draw that
  *                      u[t] would make from step t's distribution.
- * logits_out [T][a] (double), margin_out [T] may be NULL.  u may be NULL in mode 1.
- * If st is NULL a fresh zero state is used.  Returns 0, -1 (bad arguments) or
- * -2 (allocation failure).
+ * Draws follow oracle_sample's rule (sample_mode, temperature, top_k); margin_out
+ * receives its margins.  logits_out [T][a] (double), margin_out [T] may be NULL.
+ * u may be NULL in mode 1.  If st is NULL a fresh zero state is used.  Returns
+ * 0, -1 (bad arguments) or -2 (allocation failure).
  */
-int oracle_run(const oracle_model *m, oracle_state *st, int mode, long long T,
-               const float *cond, const float *u, const int *y_in,
-               int *samples_out, double *logits_out, double *margin_out) {
+int oracle_run_sampled(const oracle_model *m, oracle_state *st, int mode, long long T,
+                       const float *cond, const float *u, const int *y_in,
+                       int *samples_out, double *logits_out, double *margin_out,
+                       int sample_mode, double temperature, int top_k) {
     if (!m || T < 0 || (mode != 0 && mode != 1)) return -1;
     if (mode == 0 && !u) return -1;
     if (mode == 1 && !y_in) return -1;
@@ -235,7 +323,8 @@ int oracle_run(const oracle_model *m, oracle_state *st, int mode, long long T,
         if (logits_out) memcpy(logits_out + t * m->a, lg, sizeof(double) * m->a);
         int y = 0;
         double mg = 0.0;
-        if (u) y = oracle_draw(m->a, lg, u[t], NULL, &mg);
+        if (u) y = oracle_sample(m->a, lg, u[t], sample_mode, temperature, top_k, &mg);
+        if (y < 0) { free(lg); free(own); return -1; }
         if (margin_out) margin_out[t] = u ? mg : 0.0;
         if (samples_out) samples_out[t] = y;
         st->last_sample = (mode == 0) ? y : y_in[t];
@@ -243,6 +332,13 @@ int oracle_run(const oracle_model *m, oracle_state *st, int mode, long long T,
     free(lg);
     free(own);
     return 0;
+}
+
+/* oracle_run_sampled with direct sampling. */
+int oracle_run(const oracle_model *m, oracle_state *st, int mode, long long T,
+               const float *cond, const float *u, const int *y_in,
+               int *samples_out, double *logits_out, double *margin_out) {
+    return oracle_run_sampled(m, st, mode, T, cond, u, y_in, samples_out, logits_out, margin_out, 0, 1.0, m ? m->a : 0);
 }
 
 /* Number of parameters of the layout above (the paper's model-size estimate). */

@@ -28,6 +28,7 @@ CASES = [
     # name, L, s, dilations, B, T, bias
     ("l2_d1_b1", 2, 128, (1, 1), 1, 300, 0.3),
     ("l3_b16", 3, 256, (1, 2, 4), 16, 200, 0.0),
+    ("l3_d1_b5", 3, 256, (1, 1, 1), 5, 200, 0.2),
     ("l5_s128_b17", 5, 128, (1, 3, 9, 2, 4), 17, 150, 0.4),
     ("l20_b33", 20, 256, tuple(synth.dilation_cycle(20)), 33, 120, 0.1),
     ("l40_b20", 40, 256, tuple(synth.dilation_cycle(40)), 20, 60, 0.0),

@@ -282,3 +282,95 @@ def test_window_of_receptive_field_reproduces_full_run():
     mw = oracle.Model(w, dil, initial_sample=int(y[t0 - 1]))
     _, lw, _ = oracle.run(mw, cond[t0:t + 1], y_in=y[t0:t + 1])
     assert np.any(lw[-1] != lg[t])
+
+
+def _known_distribution_run(seed, T=400):
+    """A model whose every step has the same known distribution: W_out = 0, B_out = log q."""
+    rng = np.random.default_rng(seed)
+    L, r, s, a, dil = 2, 4, 8, 256, (1, 2)
+    w = synth.make_weights(L, r, s, a, seed=seed, bias_scale=0.3)
+    qv = np.maximum(rng.dirichlet(np.full(a, 0.5)), 1e-12)
+    w["w_out"][:] = 0
+    w["b_out"] = np.log(qv / qv.sum()).astype(np.float32)
+    m = oracle.Model(w, dil)
+    cond = _cond(L, r, T, seed=seed + 1)
+    u = synth.make_uniforms(1, T, seed=seed + 2)[0]
+    pf = np.exp(w["b_out"].astype(np.float64))
+    return m, cond, u, pf / pf.sum(), a
+
+
+@pytest.mark.parametrize("sampler", [(1, 0.5, 256), (1, 2.0, 256), (2, 1.0, 1), (2, 1.0, 3), (2, 1.0, 17),
+                                     (2, 1.0, 256), (3, 1.0, 256), (4, 1.0, 256)])
+def test_sampling_variants_on_a_known_distribution(sampler):
+    """Each rule of the paper's sampling appendix against its textbook form on a known P:
+    temperature draws from P^(1/t)/Z, top k from P kept at or above its k-th largest value and
+    renormalised, mode is argmax P, mean is E_P[y] to the nearest index; draws are inverse CDFs
+    (numpy searchsorted on the float32-rounded CDF)."""
+    mode, t, k = sampler
+    m, cond, u, p, a = _known_distribution_run(seed=40 + mode * 7 + k % 5)
+    ys, lg, mg = oracle.run(m, cond, u=u, sampler=sampler)
+    if mode == 3:
+        ref = np.full(len(u), int(np.argmax(p)))
+    elif mode == 4:
+        ref = np.full(len(u), int(np.floor((np.arange(a) * p).sum() + 0.5)))
+    else:
+        q = p ** (1.0 / t) if mode == 1 else p.copy()
+        last = a - 1
+        if mode == 2:
+            kth = np.sort(p)[::-1][k - 1]
+            q[p < kth] = 0.0
+            last = int(np.nonzero(q)[0].max())
+        q /= q.sum()
+        cdf = np.cumsum(q)
+        ref = np.minimum(np.searchsorted(cdf.astype(np.float32)[:a - 1], u, side="right"), last)
+    ok = mg > 1e-9
+    assert ok.sum() > 0.9 * len(u)
+    np.testing.assert_array_equal(ys[ok], ref[ok])
+    if mode == 2:
+        assert set(np.unique(ys)) <= set(np.nonzero(p >= np.sort(p)[::-1][k - 1])[0])
+
+
+def test_sampling_variant_identities_on_a_model():
+    """On a random model's own generation: t = 1 and k = a are direct sampling, k = 1 is the
+    mode, and a temperature near 0 draws the mode wherever the top two logits are apart."""
+    L, r, s, dil, T = 4, 16, 32, (1, 2, 4, 8), 300
+    w = synth.make_weights(L, r, s, seed=5, bias_scale=0.5)
+    w["w_out"] *= 4.0  # sharper distributions, so that the mode and the draws differ visibly
+    m = oracle.Model(w, dil)
+    cond = _cond(L, r, T, seed=6)
+    u = synth.make_uniforms(1, T, seed=7)[0]
+    y0, _, _ = oracle.run(m, cond, u=u)
+    for smp in [(1, 1.0, 256), (2, 1.0, 256)]:
+        np.testing.assert_array_equal(oracle.run(m, cond, u=u, sampler=smp)[0], y0)
+    ym, lg, _ = oracle.run(m, cond, u=u, sampler=(3, 1.0, 256))
+    np.testing.assert_array_equal(oracle.run(m, cond, u=u, sampler=(2, 1.0, 1))[0], ym)
+    np.testing.assert_array_equal(ym, np.argmax(lg, axis=1))
+    assert not np.array_equal(ym, y0)
+    yc, lgc, _ = oracle.run(m, cond, u=u, sampler=(1, 1e-4, 256))
+    top2 = np.sort(lgc, axis=1)[:, -2:]
+    apart = (top2[:, 1] - top2[:, 0]) > 1e-2
+    np.testing.assert_array_equal(yc[apart], np.argmax(lgc, axis=1)[apart])
+    # teacher forcing on the mode's own samples reproduces its logits
+    _, lgt, _ = oracle.run(m, cond, y_in=ym)
+    np.testing.assert_array_equal(lgt, lg)
+
+
+def test_sampler_rejects_invalid_rules():
+    lg = np.zeros(256)
+    for bad in [(1, 0.0, 256), (1, -1.0, 256), (2, 1.0, 0), (2, 1.0, 257), (5, 1.0, 256)]:
+        with pytest.raises(ValueError):
+            oracle.sample(lg, 0.5, bad)
+
+
+@pytest.mark.parametrize("lo,hi,w_hi", [(100, 101, 0.7), (100, 101, 0.3), (0, 255, 0.5004), (3, 9, 0.3)])
+def test_sampling_mean_rounds_to_the_nearest_index(lo, hi, w_hi):
+    """E_P[y] of a distribution on two classes (plus a negligible floor elsewhere) is
+    lo + w_hi (hi - lo) up to that floor; the mean rule takes the nearest index."""
+    a = 256
+    p = np.full(a, 1e-30)
+    p[lo], p[hi] = 1.0 - w_hi, w_hi
+    lg = np.log(p)
+    y, mg = oracle.sample(lg, 0.5, (4, 1.0, a))
+    mean = lo + w_hi * (hi - lo)
+    assert mg > 1e-6
+    assert y == int(np.floor(mean + 0.5))
