@@ -59,6 +59,32 @@ typedef enum {
 
 typedef enum { WN_F32 = 0, WN_BF16 = 1 } wn_dtype_t;
 
+/*
+ * How a step's output distribution P = softmax(logits) becomes its sample: the ways the paper
+ * lists (Appendix A.4, "Sampling from Output Distribution").  C_k is the CDF of the distribution
+ * sampled and u the step's uniform.
+ *   WN_SAMPLE_DIRECT       y = #{k <= a-2 : C_k <= u} on P (what wn_generate does)
+ *   WN_SAMPLE_TEMPERATURE  the same on P^(1/t) / Z = softmax(logits / t), t = temperature > 0
+ *   WN_SAMPLE_TOPK         the same on P kept where its logit is at least the top_k-th largest
+ *                          logit (ties at the top_k-th are kept) and renormalised, 1 <= top_k <= a
+ *   WN_SAMPLE_MODE         argmax P, the smallest index among equal maxima (u unused)
+ *   WN_SAMPLE_MEAN         E_P[y] = sum_k k P(k) to the nearest index, halves up (u unused; the
+ *                          paper does not say how the mean becomes an index)
+ */
+typedef enum {
+  WN_SAMPLE_DIRECT = 0,
+  WN_SAMPLE_TEMPERATURE = 1,
+  WN_SAMPLE_TOPK = 2,
+  WN_SAMPLE_MODE = 3,
+  WN_SAMPLE_MEAN = 4
+} wn_sample_mode_t;
+
+typedef struct {
+  int32_t mode;       /* wn_sample_mode_t */
+  float temperature;  /* WN_SAMPLE_TEMPERATURE: t > 0 (finite); ignored otherwise */
+  int32_t top_k;      /* WN_SAMPLE_TOPK: 1 .. a; ignored otherwise */
+} wn_sampler;
+
 typedef struct {
   int32_t n_layers;          /* l, 1 .. 64 */
   int32_t r;                 /* residual channels: 16, 32, 64 or 128 */
@@ -123,6 +149,16 @@ size_t wn_workspace_bytes(const wn_handle* h, int32_t B);
  */
 int wn_generate(wn_handle* h, int32_t B, int32_t T, const float* cond, const float* uniforms,
                 int32_t* samples, void* workspace, size_t ws_bytes, int32_t reset, void* stream);
+
+/*
+ * wn_generate with another way of turning each step's distribution into its sample (see
+ * wn_sampler; Appendix A.4).  sampler = NULL is direct sampling.  uniforms are required for
+ * every mode (MODE and MEAN read none of them).  Errors: those of wn_generate, and WN_EINVAL for
+ * an unknown mode, a temperature that is not finite and > 0, or top_k outside 1 .. a.
+ */
+int wn_generate_sampled(wn_handle* h, int32_t B, int32_t T, const float* cond, const float* uniforms,
+                        int32_t* samples, void* workspace, size_t ws_bytes, int32_t reset,
+                        const wn_sampler* sampler, void* stream);
 
 /*
  * Teacher forcing: step t consumes y[b][t-1] (for t = 0: y_{-1} = initial_sample

@@ -21,8 +21,10 @@ LIB_PATH = os.path.join(_HERE, "libwn.so")
 WN_OK, WN_EINVAL, WN_EUNSUPPORTED, WN_ENOMEM, WN_EHIP, WN_ETIMEOUT, WN_EABORTED = 0, -1, -2, -3, -4, -5, -6
 WN_F32, WN_BF16 = 0, 1
 A_CLASSES = 256
-EXPORTED = ("wn_create", "wn_workspace_bytes", "wn_generate", "wn_teacher_force", "wn_status",
+EXPORTED = ("wn_create", "wn_workspace_bytes", "wn_generate", "wn_generate_sampled", "wn_teacher_force", "wn_status",
             "wn_kernel_variant", "wn_destroy", "wn_error_string", "wn_last_error")
+# wn_sample_mode_t: how a step's distribution becomes its sample
+SAMPLE_DIRECT, SAMPLE_TEMPERATURE, SAMPLE_TOPK, SAMPLE_MODE, SAMPLE_MEAN = 0, 1, 2, 3, 4
 
 _lib = None
 _lock = threading.Lock()
@@ -38,6 +40,10 @@ class Config(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("r", ctypes.c_int32), ("s", ctypes.c_int32), ("a", ctypes.c_int32),
                 ("dilations", ctypes.POINTER(ctypes.c_int32)), ("embed_taps", ctypes.c_int32),
                 ("initial_sample", ctypes.c_int32), ("weight_dtype", ctypes.c_int32)]
+
+
+class Sampler(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_int32), ("temperature", ctypes.c_float), ("top_k", ctypes.c_int32)]
 
 
 WEIGHT_FIELDS = ("embed", "b_embed", "w_prev", "w_cur", "b_gate", "w_res", "b_res", "w_skip", "b_skip",
@@ -64,6 +70,8 @@ def load_library(path: str = LIB_PATH):
         L.wn_workspace_bytes.argtypes = [vp, i32]
         L.wn_generate.restype = ctypes.c_int
         L.wn_generate.argtypes = [vp, i32, i32, vp, vp, vp, vp, sz, i32, vp]
+        L.wn_generate_sampled.restype = ctypes.c_int
+        L.wn_generate_sampled.argtypes = [vp, i32, i32, vp, vp, vp, vp, sz, i32, ctypes.POINTER(Sampler), vp]
         L.wn_teacher_force.restype = ctypes.c_int
         L.wn_teacher_force.argtypes = [vp, i32, i32, vp, vp, vp, vp, sz, i32, vp]
         L.wn_status.restype = ctypes.c_int
@@ -155,8 +163,11 @@ class WaveNet:
     def kernel_variant(self, B: int) -> str:
         return self._lib.wn_kernel_variant(self._h, int(B)).decode()
 
-    def generate(self, cond, uniforms, samples=None, workspace=None, reset: bool = True, stream=None):
-        """cond fp32 [B,T,l,2r], uniforms fp32 [B,T] (device) -> samples int32 [B,T]."""
+    def generate(self, cond, uniforms, samples=None, workspace=None, reset: bool = True, stream=None, sampler=None):
+        """cond fp32 [B,T,l,2r], uniforms fp32 [B,T] (device) -> samples int32 [B,T].
+
+        ``sampler``: None (direct sampling) or (mode, temperature, top_k) with mode one of the
+        SAMPLE_* values (include/wn.h, wn_sampler)."""
         import torch
         B, T = int(cond.shape[0]), int(cond.shape[1])
         cp = _dev_ptr(cond, torch.float32, (B, T, self.n_layers, 2 * self.r), "cond")
@@ -166,8 +177,14 @@ class WaveNet:
         sp = _dev_ptr(samples, torch.int32, (B, T), "samples")
         if workspace is None:
             workspace = self.new_workspace(B, cond.device)
-        _check(self._lib.wn_generate(self._h, B, T, cp, up, sp, workspace.data_ptr(), workspace.numel(),
-                                     1 if reset else 0, _stream_handle(stream)), "wn_generate")
+        if sampler is None:
+            _check(self._lib.wn_generate(self._h, B, T, cp, up, sp, workspace.data_ptr(), workspace.numel(),
+                                         1 if reset else 0, _stream_handle(stream)), "wn_generate")
+        else:
+            smp = Sampler(int(sampler[0]), float(sampler[1]), int(sampler[2]))
+            _check(self._lib.wn_generate_sampled(self._h, B, T, cp, up, sp, workspace.data_ptr(), workspace.numel(),
+                                                 1 if reset else 0, ctypes.byref(smp), _stream_handle(stream)),
+                   "wn_generate_sampled")
         return samples
 
     def teacher_force(self, cond, y, logits=None, workspace=None, reset: bool = True, stream=None):

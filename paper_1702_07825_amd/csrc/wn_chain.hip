@@ -367,18 +367,7 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
         y = reinterpret_cast<const int*>(ubuf)[at];
         y = y < 0 ? 0 : (y > A - 1 ? A - 1 : y);
       } else {
-        const float l0 = lv.x, l1 = lv.y, l2 = lv.z, l3 = lv.w;
-        const float m = wave_max(fmaxf(fmaxf(l0, l1), fmaxf(l2, l3)));
-        const float e0 = expf_fast(l0 - m), e1 = expf_fast(l1 - m), e2 = expf_fast(l2 - m), e3 = expf_fast(l3 - m);
-        const float s0 = e0, s1 = s0 + e1, s2 = s1 + e2, s3 = s2 + e3;
-        const float incl = wave_incl_scan(s3);
-        const float excl = wave_shr1(incl);
-        const float Z = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, incl), 63));
-        const float iz = 1.0f / Z;
-        const float u = ubuf[at];
-        int cnt = ((excl + s0) * iz <= u) + ((excl + s1) * iz <= u) + ((excl + s2) * iz <= u);
-        if (lane != 63) cnt += ((excl + s3) * iz <= u);
-        y = wave_sum_int(cnt);
+        y = wave_draw(lv, ubuf[at], g.io.smode, g.io.inv_t, g.io.top_k, lane);
       }
       if (lane == 0) {
         syv[i] = y;

@@ -290,18 +290,7 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
         y = s_yin[nn];
       } else {
         const float4 lv = *reinterpret_cast<const float4*>(LG + nn * PA + 4 * lane);
-        const float m = wave_max(fmaxf(fmaxf(lv.x, lv.y), fmaxf(lv.z, lv.w)));
-        const float e0 = expf_fast(lv.x - m), e1 = expf_fast(lv.y - m), e2 = expf_fast(lv.z - m),
-                    e3 = expf_fast(lv.w - m);
-        const float s0 = e0, s1 = s0 + e1, s2 = s1 + e2, s3 = s2 + e3;
-        const float incl = wave_incl_scan(s3);
-        const float excl = wave_shr1(incl);
-        const float Z = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, incl), 63));
-        const float iz = 1.0f / Z;
-        const float u = s_u[nn];
-        int cnt = ((excl + s0) * iz <= u) + ((excl + s1) * iz <= u) + ((excl + s2) * iz <= u);
-        if (lane != 63) cnt += ((excl + s3) * iz <= u);
-        y = wave_sum_int(cnt);
+        y = wave_draw(lv, s_u[nn], g.io.smode, g.io.inv_t, g.io.top_k, lane);
       }
       if (lane == 0) s_y[nn] = y;
       split1(bf16_val(EMB[y * R + lane]) + BE[lane], XS[nn * SR + lane], XS[nn * SR + R + lane]);

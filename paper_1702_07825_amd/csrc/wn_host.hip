@@ -3,6 +3,7 @@
 #include "wn.h"
 #include "wn_internal.h"
 
+#include <cmath>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -108,6 +109,24 @@ WsLayout ws_layout(const wn_handle* h, int B) {
   return l;
 }
 
+const wn_sampler kDirect = {WN_SAMPLE_DIRECT, 1.0f, WN_A};
+
+void set_sampler(WnIO& io, const wn_sampler& sp) {
+  io.smode = sp.mode;
+  io.inv_t = sp.mode == WN_SAMPLE_TEMPERATURE ? 1.0f / sp.temperature : 1.0f;
+  io.top_k = sp.mode == WN_SAMPLE_TOPK ? sp.top_k : WN_A;
+}
+
+int check_sampler(const wn_sampler& sp) {
+  if (sp.mode < WN_SAMPLE_DIRECT || sp.mode > WN_SAMPLE_MEAN) return fail(WN_EINVAL, "unknown sampling mode");
+  if (sp.mode == WN_SAMPLE_TEMPERATURE && !(std::isfinite(sp.temperature) && sp.temperature > 0.0f))
+    return fail(WN_EINVAL, "temperature must be finite and > 0");
+  if (sp.mode == WN_SAMPLE_TEMPERATURE && !std::isfinite(1.0f / sp.temperature))
+    return fail(WN_EINVAL, "temperature too small");
+  if (sp.mode == WN_SAMPLE_TOPK && (sp.top_k < 1 || sp.top_k > WN_A)) return fail(WN_EINVAL, "top_k must be 1..a");
+  return WN_OK;
+}
+
 int check_call(wn_handle* h, int B, int T, const void* cond, const void* a1, const void* a2, void* ws,
                size_t ws_bytes, int reset) {
   if (!h) return fail(WN_EINVAL, "null handle");
@@ -124,7 +143,7 @@ int check_call(wn_handle* h, int B, int T, const void* cond, const void* a1, con
 }
 
 int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const int32_t* y_in, int32_t* y_out,
-           float* logits, void* ws, int reset, void* stream, bool teacher) {
+           float* logits, void* ws, int reset, void* stream, bool teacher, const wn_sampler& sp) {
   DeviceScope scope(h->device);
   if (!scope.ok()) return fail(WN_EHIP, "cannot select the handle's device");
   const WsLayout l = ws_layout(h, B);
@@ -144,6 +163,7 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
     g.io.T = T;
     g.io.reset = reset;
     g.io.init_sample = h->init_sample;
+    set_sampler(g.io, sp);
     g.status = reinterpret_cast<int32_t*>(base + l.status_off);
     g.state = reinterpret_cast<int64_t*>(base + l.state_off);
     g.ring = reinterpret_cast<unsigned long long*>(base + l.hist_off);
@@ -185,6 +205,7 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
     g.io.T = T;
     g.io.reset = reset;
     g.io.init_sample = h->init_sample;
+    set_sampler(g.io, sp);
     g.ws.status = reinterpret_cast<int32_t*>(base + l.status_off);
     g.ws.state = reinterpret_cast<int64_t*>(base + l.state_off);
     g.ws.hist = reinterpret_cast<float*>(base + l.hist_off);
@@ -204,6 +225,7 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
   args.io.T = T;
   args.io.reset = reset;
   args.io.init_sample = h->init_sample;
+  set_sampler(args.io, sp);
   args.ws.status = reinterpret_cast<int32_t*>(base + l.status_off);
   args.ws.state = reinterpret_cast<int64_t*>(base + l.state_off);
   args.ws.hist = reinterpret_cast<float*>(base + l.hist_off);
@@ -357,7 +379,19 @@ int wn_generate(wn_handle* h, int32_t B, int32_t T, const float* cond, const flo
   g_err.clear();
   int rc = check_call(h, B, T, cond, uniforms, samples, workspace, ws_bytes, reset);
   if (rc != WN_OK || T == 0) return rc;
-  return launch(h, B, T, cond, uniforms, nullptr, samples, nullptr, workspace, reset, stream, false);
+  return launch(h, B, T, cond, uniforms, nullptr, samples, nullptr, workspace, reset, stream, false, kDirect);
+}
+
+int wn_generate_sampled(wn_handle* h, int32_t B, int32_t T, const float* cond, const float* uniforms,
+                        int32_t* samples, void* workspace, size_t ws_bytes, int32_t reset,
+                        const wn_sampler* sampler, void* stream) {
+  g_err.clear();
+  const wn_sampler sp = sampler ? *sampler : kDirect;
+  int rc = check_sampler(sp);
+  if (rc != WN_OK) return rc;
+  rc = check_call(h, B, T, cond, uniforms, samples, workspace, ws_bytes, reset);
+  if (rc != WN_OK || T == 0) return rc;
+  return launch(h, B, T, cond, uniforms, nullptr, samples, nullptr, workspace, reset, stream, false, sp);
 }
 
 int wn_teacher_force(wn_handle* h, int32_t B, int32_t T, const float* cond, const int32_t* y, float* logits,
@@ -365,7 +399,7 @@ int wn_teacher_force(wn_handle* h, int32_t B, int32_t T, const float* cond, cons
   g_err.clear();
   int rc = check_call(h, B, T, cond, y, logits, workspace, ws_bytes, reset);
   if (rc != WN_OK || T == 0) return rc;
-  return launch(h, B, T, cond, nullptr, y, nullptr, logits, workspace, reset, stream, true);
+  return launch(h, B, T, cond, nullptr, y, nullptr, logits, workspace, reset, stream, true, kDirect);
 }
 
 int wn_status(wn_handle* h, const void* workspace, void* stream) {

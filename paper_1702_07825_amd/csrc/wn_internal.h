@@ -44,6 +44,11 @@ struct WnIO {
   int32_t* y_out;       // [B][T]            (generation)
   float* logits;        // [B][T][A]         (teacher forcing)
   int B, T, reset, init_sample;
+  // how a step's distribution becomes its sample (generation): wn_sample_mode_t, 1 / temperature,
+  // k of top-k sampling
+  int smode;
+  float inv_t;
+  int top_k;
 };
 
 // Caller-owned workspace, carved by the host code.

@@ -20,6 +20,7 @@
 // Matrix-vector products reduce across the LPR lanes of a row with cross-lane
 // shuffles.  The draw is a single-wave max / exp / inclusive scan / count.
 #include "wn_internal.h"
+#include "wn_wave.h"
 
 namespace {
 
@@ -86,7 +87,7 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
   __shared__ float hs[R];
   __shared__ float qs[S];
   __shared__ float zas[A];
-  __shared__ float lgs[A];
+  __shared__ __align__(16) float lgs[A];
   __shared__ int yprev_s;
 
   const WT* embed = static_cast<const WT*>(args.w.embed);
@@ -241,35 +242,14 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
       }
     } else {
       __syncthreads();
-      // ---- p = softmax(logits); y = #{k <= A-2 : C_k <= u} (one wave) ----
+      // ---- the draw from p = softmax(logits) (one wave) ----
       if (tid < 64) {
         const int lane = tid;
-        float l0 = lgs[4 * lane], l1 = lgs[4 * lane + 1], l2 = lgs[4 * lane + 2], l3 = lgs[4 * lane + 3];
-        float m = fmaxf(fmaxf(l0, l1), fmaxf(l2, l3));
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
-        const float e0 = expf_fast(l0 - m), e1 = expf_fast(l1 - m), e2 = expf_fast(l2 - m), e3 = expf_fast(l3 - m);
-        const float s0 = e0, s1 = s0 + e1, s2 = s1 + e2, s3 = s2 + e3;
-        float incl = s3;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const float v = __shfl_up(incl, o, 64);
-          if (lane >= o) incl += v;
-        }
-        float excl = __shfl_up(incl, 1, 64);
-        if (lane == 0) excl = 0.f;
-        const float Z = __shfl(incl, 63, 64);
-        const float u = args.io.u[bt];
-        int cnt = 0;
-        cnt += ((excl + s0) / Z <= u);
-        cnt += ((excl + s1) / Z <= u);
-        cnt += ((excl + s2) / Z <= u);
-        if (lane != 63) cnt += ((excl + s3) / Z <= u);  // k = 255 is never counted
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
+        const float4 lv = *reinterpret_cast<const float4*>(lgs + 4 * lane);
+        const int y = wnk::wave_draw(lv, args.io.u[bt], args.io.smode, args.io.inv_t, args.io.top_k, lane);
         if (lane == 0) {
-          args.io.y_out[bt] = cnt;
-          yprev_s = cnt;
+          args.io.y_out[bt] = y;
+          yprev_s = y;
         }
       }
     }

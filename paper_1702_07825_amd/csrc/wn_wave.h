@@ -94,6 +94,95 @@ __device__ __forceinline__ float expf_fast(float v) { return __builtin_amdgcn_ex
 __device__ __forceinline__ float tanh_f(float v) { return 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + expf_fast(2.0f * v)); }
 __device__ __forceinline__ float sigmoid_f(float v) { return __builtin_amdgcn_rcpf(1.0f + expf_fast(-v)); }
 
+// Sum over the 64 lanes of a wave (every lane gets it).
+__device__ __forceinline__ float wave_sum(float v) {
+  v = gsum16(v);
+  const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+  const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+  const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+  const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+  return (r0 + r1) + (r2 + r3);
+}
+
+// Order-preserving map of a (non-NaN) float to an unsigned key.
+__device__ __forceinline__ unsigned float_key(float f) {
+  const unsigned b = __float_as_uint(f);
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+// Rules for turning a step's output distribution P into a sample (Deep Voice, Appendix A.4,
+// "Sampling from Output Distribution"); the values are those of wn_sample_mode_t.
+enum { WN_DRAW_DIRECT = 0, WN_DRAW_TEMPERATURE = 1, WN_DRAW_TOPK = 2, WN_DRAW_MODE = 3, WN_DRAW_MEAN = 4 };
+
+// One step's sample from the a = 256 logits held by one wave, lane l holding logits 4l .. 4l+3;
+// every lane returns it.  P = softmax(logits).  Rules (mode is wave-uniform):
+//   direct       y = #{k <= 254 : C_k <= u}, C_k = (p_0 + .. + p_k), the inverse CDF at u
+//   temperature  the same on softmax(logits * inv_t), i.e. P^(1/t) / Z
+//   top k        the same on P kept where its logit is at least the k-th largest logit (ties
+//                kept) and renormalised; a result past the last kept class (only possible by
+//                rounding) becomes that class
+//   mode         the smallest index of the largest logit
+//   mean         floor(sum_k k p_k + 1/2)
+__device__ __forceinline__ int wave_draw(float4 lv, float u, int mode, float inv_t, int top_k, int lane) {
+  float l[4] = {lv.x, lv.y, lv.z, lv.w};
+  if (mode == WN_DRAW_MODE) {
+    const float m = wave_max(fmaxf(fmaxf(l[0], l[1]), fmaxf(l[2], l[3])));
+    int best = 256;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const unsigned long long mk = __ballot(l[i] == m);
+      if (mk) best = min(best, 4 * (__ffsll((long long)mk) - 1) + i);
+    }
+    return best;
+  }
+  if (mode == WN_DRAW_TEMPERATURE) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) l[i] *= inv_t;
+  }
+  const float m = wave_max(fmaxf(fmaxf(l[0], l[1]), fmaxf(l[2], l[3])));
+  float e[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) e[i] = expf_fast(l[i] - m);
+  int last = 255;
+  if (mode == WN_DRAW_TOPK) {
+    // the k-th largest key, built bit by bit: the largest t with #{key >= t} >= k
+    unsigned key[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) key[i] = float_key(l[i]);
+    unsigned thr = 0;
+    for (int bit = 31; bit >= 0; --bit) {
+      const unsigned cand = thr | (1u << bit);
+      int cnt = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) cnt += __popcll(__ballot(key[i] >= cand));
+      if (cnt >= top_k) thr = cand;
+    }
+    last = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const bool keep = key[i] >= thr;
+      e[i] = keep ? e[i] : 0.f;
+      const unsigned long long mk = __ballot(keep);
+      if (mk) last = max(last, 4 * (63 - __clzll((long long)mk)) + i);
+    }
+  }
+  const float s0 = e[0], s1 = s0 + e[1], s2 = s1 + e[2], s3 = s2 + e[3];
+  const float incl = wave_incl_scan(s3);
+  const float excl = wave_shr1(incl);
+  const float Z = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, incl), 63));
+  const float iz = 1.0f / Z;
+  if (mode == WN_DRAW_MEAN) {
+    const float k0 = (float)(4 * lane);
+    const float part = k0 * e[0] + (k0 + 1.f) * e[1] + (k0 + 2.f) * e[2] + (k0 + 3.f) * e[3];
+    const int y = (int)floorf(wave_sum(part) * iz + 0.5f);
+    return y < 0 ? 0 : (y > 255 ? 255 : y);
+  }
+  int cnt = ((excl + s0) * iz <= u) + ((excl + s1) * iz <= u) + ((excl + s2) * iz <= u);
+  if (lane != 63) cnt += ((excl + s3) * iz <= u);  // k = 255 is never counted
+  const int y = wave_sum_int(cnt);
+  return y > last ? last : y;
+}
+
 // LDS-only barrier: waits for this wave's LDS traffic, not for its global stores.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
