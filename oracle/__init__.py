@@ -12,7 +12,9 @@ Pins of this oracle (tests/test_oracle_pins.py): a whole-sequence dilated
 causal convolution written with torch's conv1d, the no-recurrence special case
 as numpy matmuls, the head-and-sampler special case against numpy's
 searchsorted, receptive field and causality, chunked == one-shot, the skip
-concatenation identity, and the paper's model-size and FLOP figures.
+concatenation identity, the paper's model-size and FLOP figures, and the other
+sampling rules (temperature, top k, mode, mean) on a known distribution and
+through their identities with direct sampling and the argmax.
 """
 from __future__ import annotations
 

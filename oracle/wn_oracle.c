@@ -28,6 +28,9 @@
  *    The margin min_k |u - C_k| (double, k <= a-2) is reported so that callers
  *    can tell which draws no rounding difference of a float implementation can
  *    change.
+ *  - the other sampling rules (oracle_sample): top k keeps every class whose P
+ *    is at least the k-th largest P (ties kept); the mean E_P[y] is taken to the
+ *    nearest class index, halves up.
  *  - bf16 weight storage: every matrix (W_prev, W_cur, W_res, W_skip, W_relu,
  *    W_out and the embedding table) is rounded to bfloat16 with round-to-
  *    nearest-even and used as the exact value of that bfloat16; biases stay fp32.
