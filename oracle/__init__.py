@@ -74,6 +74,9 @@ def lib():
             L.oracle_sample.restype = ctypes.c_int
             L.oracle_sample.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_float, ctypes.c_int, ctypes.c_double,
                                         ctypes.c_int, ctypes.c_void_p]
+            L.oracle_condition.restype = ctypes.c_int
+            L.oracle_condition.argtypes = [ctypes.POINTER(_CondModel), ctypes.c_longlong, ctypes.c_void_p,
+                                           ctypes.c_longlong, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
             L.oracle_draw.restype = ctypes.c_int
             L.oracle_draw.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
             L.oracle_history_len.restype = ctypes.c_longlong
@@ -88,6 +91,12 @@ def lib():
             L.oracle_round_bf16_array.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_longlong]
             _lib = L
     return _lib
+
+
+class _CondModel(ctypes.Structure):
+    _fields_ = [("n_features", ctypes.c_int), ("h1", ctypes.c_int), ("h2", ctypes.c_int),
+                ("w1", ctypes.POINTER(ctypes.c_float)), ("b1", ctypes.POINTER(ctypes.c_float)),
+                ("w2", ctypes.POINTER(ctypes.c_float)), ("b2", ctypes.POINTER(ctypes.c_float))]
 
 
 def _ptr(a: Optional[np.ndarray]):
@@ -220,6 +229,24 @@ def sample(logits: np.ndarray, u: float, sampler=DIRECT):
     if y < 0:
         raise ValueError("invalid sampler %r" % (sampler,))
     return int(y), float(mg.value)
+
+
+def condition(weights: Dict[str, np.ndarray], features: np.ndarray, n_audio: int, frame_rate: int,
+              audio_rate: int) -> np.ndarray:
+    """Conditioning network (Appendix A.2): features [Tf, F] -> cond [n_audio, 2 h2] (float64).
+
+    ``weights``: w1 [2, 3 h1, 2, F], b1 [2, 3 h1], w2 [2, 3 h2, 2, 2 h1], b2 [2, 3 h2] (fp32)."""
+    w = {k: np.ascontiguousarray(weights[k], dtype=np.float32) for k in ("w1", "b1", "w2", "b2")}
+    x = np.ascontiguousarray(features, dtype=np.float32)
+    Tf, F = x.shape
+    h1, h2 = w["b1"].shape[1] // 3, w["b2"].shape[1] // 3
+    assert w["w1"].shape == (2, 3 * h1, 2, F) and w["w2"].shape == (2, 3 * h2, 2, 2 * h1)
+    m = _CondModel(F, h1, h2, *[w[k].ctypes.data_as(ctypes.POINTER(ctypes.c_float)) for k in ("w1", "b1", "w2", "b2")])
+    out = np.zeros((n_audio, 2 * h2), np.float64)
+    rc = lib().oracle_condition(ctypes.byref(m), Tf, _ptr(x), n_audio, int(frame_rate), int(audio_rate), _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle_condition failed with %d" % rc)
+    return out
 
 
 def round_bf16(x: np.ndarray) -> np.ndarray:

@@ -362,3 +362,87 @@ double oracle_flops_per_sample(int n_layers, int r, int s, int a, double f_div, 
 void oracle_round_bf16_array(const float *in, float *out, long long n) {
     for (long long i = 0; i < n; ++i) out[i] = round_bf16(in[i]);
 }
+
+/*
+ * Conditioning network (Appendix A.2, "Conditioning Network"): the per-layer
+ * conditioning L of every audio step from linguistic features at the frame
+ * rate.  Two bidirectional QRNN layers with fo-pooling and width-2
+ * convolutions, then the channels of the two directions interleaved, then
+ * upsampling to the audio rate by repetition.  A unidirectional layer computes,
+ * over the frames in its own order,
+ *     h~_t = tanh(W_h * x + B_h), o_t = sigma(W_o * x + B_o), f_t = sigma(W_f * x + B_f)
+ *     h_t  = f_t h_{t-1} + (1 - f_t) h~_t   (h before the first frame is 0)
+ *     z_t  = o_t h_t
+ * where W * x is the width-2 convolution over [x_{t'}, x_t], t' the frame before
+ * t in that order (zero before the first).  The backward layer runs on the
+ * reversed frames, so its previous frame is t + 1.  Readings taken here: the
+ * convolution is causal in each direction's own order; the bidirectional output
+ * stacks forward then backward channels; after the second layer output channel
+ * 2k + d is channel k of direction d, and the 2 h2 = l * 2r channels of an audio
+ * step are layer j's L in block j; audio step tau repeats frame
+ * floor(tau * frame_rate / audio_rate).
+ */
+typedef struct {
+    int n_features;     /* F */
+    int h1, h2;         /* channels per direction of layer 1 and layer 2 */
+    const float *w1;    /* [2][3 h1][2][F]: direction, gate row (blocks h~, o, f), tap (0: previous frame, 1: current), input */
+    const float *b1;    /* [2][3 h1] */
+    const float *w2;    /* [2][3 h2][2][2 h1] */
+    const float *b2;    /* [2][3 h2] */
+} oracle_cond_model;
+
+/* One bidirectional QRNN layer over T frames of `in` channels: out [T][2h], forward channels first. */
+static void oracle_qrnn_layer(long long T, int in, int h, const double *x, const float *w, const float *b,
+                              double *out) {
+    for (int dir = 0; dir < 2; ++dir) {
+        const float *wd = w + (size_t)dir * 3 * h * 2 * in;
+        const float *bd = b + (size_t)dir * 3 * h;
+        for (int k = 0; k < h; ++k) {
+            double hprev = 0.0;
+            for (long long s = 0; s < T; ++s) {
+                const long long t = dir == 0 ? s : T - 1 - s;
+                const long long tp = dir == 0 ? t - 1 : t + 1;
+                double a[3];
+                for (int gt = 0; gt < 3; ++gt) {
+                    const float *row = wd + (size_t)(gt * h + k) * 2 * in;
+                    double acc = bd[gt * h + k];
+                    if (tp >= 0 && tp < T)
+                        for (int i = 0; i < in; ++i) acc += (double)row[i] * x[(size_t)tp * in + i];
+                    for (int i = 0; i < in; ++i) acc += (double)row[in + i] * x[(size_t)t * in + i];
+                    a[gt] = acc;
+                }
+                const double ht = tanh(a[0]), o = sigmoid(a[1]), f = sigmoid(a[2]);
+                const double hc = f * hprev + (1.0 - f) * ht;
+                out[(size_t)t * 2 * h + (size_t)dir * h + k] = o * hc;
+                hprev = hc;
+            }
+        }
+    }
+}
+
+/*
+ * cond [Ta][2 h2] (double) from features [Tf][F].  Returns 0, -1 (bad
+ * arguments, or an audio step past the last frame) or -2 (allocation failure).
+ */
+int oracle_condition(const oracle_cond_model *m, long long Tf, const float *features, long long Ta,
+                     int frame_rate, int audio_rate, double *cond) {
+    if (!m || Tf < 1 || Ta < 0 || frame_rate < 1 || audio_rate < 1 || m->n_features < 1 || m->h1 < 1 || m->h2 < 1)
+        return -1;
+    if (Ta > 0 && (Ta - 1) * (long long)frame_rate / audio_rate >= Tf) return -1;
+    const int F = m->n_features, h1 = m->h1, h2 = m->h2;
+    double *x = malloc(sizeof(double) * (size_t)Tf * F);
+    double *z1 = malloc(sizeof(double) * (size_t)Tf * 2 * h1);
+    double *z2 = malloc(sizeof(double) * (size_t)Tf * 2 * h2);
+    if (!x || !z1 || !z2) { free(x); free(z1); free(z2); return -2; }
+    for (long long i = 0; i < Tf * F; ++i) x[i] = features[i];
+    oracle_qrnn_layer(Tf, F, h1, x, m->w1, m->b1, z1);
+    oracle_qrnn_layer(Tf, 2 * h1, h2, z1, m->w2, m->b2, z2);
+    for (long long tau = 0; tau < Ta; ++tau) {
+        const long long t = tau * (long long)frame_rate / audio_rate;
+        for (int k = 0; k < h2; ++k)
+            for (int dir = 0; dir < 2; ++dir)
+                cond[(size_t)tau * 2 * h2 + 2 * k + dir] = z2[(size_t)t * 2 * h2 + (size_t)dir * h2 + k];
+    }
+    free(x); free(z1); free(z2);
+    return 0;
+}

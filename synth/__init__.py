@@ -151,3 +151,53 @@ def make_samples(B: int, T: int, a: int = A_CLASSES, seed: int = 0) -> np.ndarra
     """int32 sample indices in [0, a) for teacher-forced runs (any sequence is valid input)."""
     rng = np.random.Generator(np.random.PCG64(_stream_seed(seed, 3, 0)))
     return rng.integers(0, a, size=(B, T), dtype=np.int32)
+
+
+# ---------------------------------------------------------------------------------------------
+# Conditioning network inputs (Appendix A.2 "Conditioning Network" and "Input Featurization")
+# ---------------------------------------------------------------------------------------------
+N_PHONEMES = 40      # 39 ARPABET phonemes + silence
+N_STRESS = 5         # no, primary, secondary, tertiary, quaternary stress
+N_FEATURES = 5 * (N_PHONEMES + N_STRESS) + 2  # 227: five phonemes in context, voiced flag, log F0
+FRAME_RATE_HZ = 256
+COND_H1 = 256        # channels per direction of the first QRNN layer (the paper gives no size)
+
+
+def make_features(B: int, n_frames: int, seed: int, min_dur: int = 8, max_dur: int = 40) -> np.ndarray:
+    """Seeded features [B, n_frames, 227] with the paper's layout: for the current phoneme, the two
+    before it and the two after it, a 40-way identity one-hot and a 5-way stress one-hot (the last
+    two stress levels never occur, as in datasets without them), then a voiced flag and a
+    normalised log F0 in [-1, 1] (0 when unvoiced).  Phonemes last min_dur..max_dur frames."""
+    out = np.zeros((B, n_frames, N_FEATURES), np.float32)
+    for b in range(B):
+        rng = np.random.default_rng((seed, b))
+        ids, stress, voiced, durs = [], [], [], []
+        while sum(durs) < n_frames + 2 * max_dur:
+            ids.append(int(rng.integers(N_PHONEMES)))
+            stress.append(int(rng.integers(3)))
+            voiced.append(bool(rng.random() < 0.6))
+            durs.append(int(rng.integers(min_dur, max_dur + 1)))
+        starts = np.cumsum([0] + durs)
+        f0 = np.clip(np.cumsum(rng.normal(0.0, 0.05, n_frames)) * 0.5 + rng.uniform(-0.5, 0.5), -1.0, 1.0)
+        for t in range(n_frames):
+            p = int(np.searchsorted(starts, t, side="right")) - 1
+            for c, q in enumerate(range(p - 2, p + 3)):
+                if 0 <= q < len(ids):
+                    out[b, t, c * N_PHONEMES + ids[q]] = 1.0
+                    out[b, t, 5 * N_PHONEMES + c * N_STRESS + stress[q]] = 1.0
+            if voiced[p]:
+                out[b, t, N_FEATURES - 2] = 1.0
+                out[b, t, N_FEATURES - 1] = f0[t]
+    return out
+
+
+def make_cond_weights(n_features: int, h1: int, h2: int, seed: int, bias_scale: float = 0.0) -> Dict[str, np.ndarray]:
+    """Seeded conditioning-network weights: w1 [2, 3 h1, 2, F], b1 [2, 3 h1], w2 [2, 3 h2, 2, 2 h1],
+    b2 [2, 3 h2] (direction, gate rows h~ / o / f, convolution tap, input); matrices N(0, 1/fan_in)
+    with fan_in = 2 x inputs (the width-2 convolution), biases 0 unless bias_scale > 0."""
+    rng = np.random.default_rng((seed, 77))
+    w = {}
+    for name, h, cin in (("1", h1, n_features), ("2", h2, 2 * h1)):
+        w["w" + name] = (rng.standard_normal((2, 3 * h, 2, cin)) / np.sqrt(2 * cin)).astype(np.float32)
+        w["b" + name] = (rng.standard_normal((2, 3 * h)) * bias_scale).astype(np.float32)
+    return w

@@ -374,3 +374,94 @@ def test_sampling_mean_rounds_to_the_nearest_index(lo, hi, w_hi):
     mean = lo + w_hi * (hi - lo)
     assert mg > 1e-6
     assert y == int(np.floor(mean + 0.5))
+
+
+# ---------------------------------------------------------------------------------------------
+# Conditioning network (Appendix A.2)
+# ---------------------------------------------------------------------------------------------
+
+def _small_cond(seed, F=7, h1=5, h2=6, Tf=11, bias=0.3):
+    w = synth.make_cond_weights(F, h1, h2, seed=seed, bias_scale=bias)
+    x = np.random.default_rng(seed).normal(size=(Tf, F)).astype(np.float32)
+    return w, x
+
+
+@pytest.mark.parametrize("frame_rate,audio_rate", [(4, 16), (3, 8), (1, 1), (256, 16000)])
+def test_conditioning_equals_whole_sequence_form(frame_rate, audio_rate):
+    """Oracle (per-frame recurrences) == torch conv1d gates + closed-form fo-pool + flipped
+    backward direction + gather upsampling, including non-integer rate ratios."""
+    w, x = _small_cond(seed=frame_rate + audio_rate)
+    Tf = x.shape[0]
+    Ta = (Tf * audio_rate + frame_rate - 1) // frame_rate
+    c = oracle.condition(w, x, Ta, frame_rate, audio_rate)
+    ref = brute_force.condition(w, x, Ta, frame_rate, audio_rate)
+    np.testing.assert_allclose(c, ref, rtol=0, atol=1e-12)
+    assert np.abs(c).max() > 1e-2
+
+
+def test_conditioning_with_forget_gate_zero_is_feedforward():
+    """f = 0 and o = 1 in both layers: h = h~, so the network is tanh(conv(tanh(conv(x)))), written
+    here with numpy matmuls frame by frame."""
+    w, x = _small_cond(seed=3)
+    for k in ("1", "2"):
+        h = w["b" + k].shape[1] // 3
+        w["w" + k][:, h:] = 0.0                    # o and f rows see no input
+        w["b" + k][:, h:2 * h] = 1e4               # o = 1
+        w["b" + k][:, 2 * h:] = -1e4               # f = 0
+    Tf = x.shape[0]
+    z = x.astype(np.float64)
+    for k in ("1", "2"):
+        wk, bk = w["w" + k].astype(np.float64), w["b" + k].astype(np.float64)
+        h = bk.shape[1] // 3
+        prev_f = np.vstack([np.zeros((1, z.shape[1])), z[:-1]])   # forward direction: frame t - 1
+        prev_b = np.vstack([z[1:], np.zeros((1, z.shape[1]))])    # backward direction: frame t + 1
+        fwd = np.tanh(prev_f @ wk[0, :h, 0].T + z @ wk[0, :h, 1].T + bk[0, :h])
+        bwd = np.tanh(prev_b @ wk[1, :h, 0].T + z @ wk[1, :h, 1].T + bk[1, :h])
+        z = np.hstack([fwd, bwd])
+    h2 = z.shape[1] // 2
+    ref = np.stack([z[:, :h2], z[:, h2:]], 2).reshape(Tf, 2 * h2)
+    np.testing.assert_allclose(oracle.condition(w, x, Tf, 1, 1), ref, rtol=0, atol=1e-12)
+
+
+def test_conditioning_forget_gate_one_holds_zero_and_interleave():
+    """f = 1 holds h at its initial 0 (all outputs 0); o = 0 in the backward direction of the
+    second layer zeroes exactly the odd (backward) channels of the interleaved output."""
+    w, x = _small_cond(seed=4)
+    h2 = w["b2"].shape[1] // 3
+    w1 = {k: v.copy() for k, v in w.items()}
+    w1["w2"][:, 2 * h2:] = 0.0
+    w1["b2"][:, 2 * h2:] = 1e4
+    assert np.all(oracle.condition(w1, x, 11, 1, 1) == 0.0)
+    wb = {k: v.copy() for k, v in w.items()}
+    wb["w2"][1, h2:2 * h2] = 0.0
+    wb["b2"][1, h2:2 * h2] = -1e4
+    c = oracle.condition(wb, x, 11, 1, 1)
+    assert np.all(c[:, 1::2] == 0.0) and np.abs(c[:, 0::2]).min() > 0.0
+    np.testing.assert_array_equal(c[:, 0::2], oracle.condition(w, x, 11, 1, 1)[:, 0::2])
+
+
+def test_conditioning_time_reversal():
+    """Reversing the frames and swapping the two directions' weights (and, in layer 2, the halves
+    of its input, since layer 1's output then comes backward half first) reverses the output in
+    time and swaps each interleaved channel pair."""
+    w, x = _small_cond(seed=5)
+    sw = {k: v[::-1].copy() for k, v in w.items()}
+    h1 = w["b1"].shape[1] // 3
+    sw["w2"] = np.concatenate([sw["w2"][..., h1:], sw["w2"][..., :h1]], axis=-1).copy()
+    c = oracle.condition(w, x, x.shape[0], 1, 1)
+    cr = oracle.condition(sw, x[::-1].copy(), x.shape[0], 1, 1)
+    swapped = cr.reshape(cr.shape[0], -1, 2)[:, :, ::-1].reshape(cr.shape)
+    np.testing.assert_allclose(swapped[::-1], c, rtol=0, atol=1e-12)
+
+
+def test_conditioning_upsampling_by_repetition():
+    """256 Hz frames at 16384 Hz repeat 64 times each; at 16000 Hz the runs are 62 or 63 long."""
+    w, x = _small_cond(seed=6, Tf=20)
+    for audio_rate, runs in ((16384, {64}), (16000, {62, 63})):
+        Ta = 19 * audio_rate // 256
+        c = oracle.condition(w, x, Ta, 256, audio_rate)
+        change = np.nonzero(np.any(c[1:] != c[:-1], axis=1))[0] + 1
+        lengths = np.diff(np.concatenate([[0], change]))
+        assert set(lengths.tolist()) <= runs and len(lengths) == 18
+    with pytest.raises(ValueError):
+        oracle.condition(w, x, 20 * 64 + 1, 256, 16384)  # past the last frame
