@@ -188,12 +188,85 @@ def run_workload(name, args):
     torch.cuda.empty_cache()
 
 
+def cond_flops(wl):
+    """Multiply-adds x 2 of the two layers' gate contractions (both directions): per frame
+    2 directions x 3h x 2 inputs-per-tap x cin for each layer."""
+    h2 = wl.n_layers * wl.r
+    per_frame = 2 * 3 * wl.h1 * 2 * wl.n_features + 2 * 3 * h2 * 2 * (2 * wl.h1)
+    return 2.0 * per_frame * wl.B * wl.n_frames
+
+
+def run_cond_workload(name, args):
+    """The conditioning network (Appendix A.2) over a batch of utterances: one wn_condition call
+    per step, features already in HBM; value = audio steps of conditioning produced per second."""
+    import torch
+    import synth
+    import paper_1702_07825_amd as wn
+
+    wl = synth.COND_WORKLOADS[name]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = synth.make_cond_weights(wl.n_features, wl.h1, wl.n_layers * wl.r, seed=args.seed)
+    net = wn.Conditioner(w, wl.n_layers, wl.r, wl.frame_rate, wl.audio_rate)
+    x = torch.tensor(synth.make_features(wl.B, wl.n_frames, seed=args.seed), device=dev)
+    cond = torch.empty((wl.B, wl.T, wl.n_layers, 2 * wl.r), dtype=torch.float32, device=dev)
+    ws = torch.empty(net.workspace_bytes(wl.B, wl.n_frames), dtype=torch.uint8, device=dev)
+    print("bench: %s, %d warmup + %d timed steps" % (wl.description, args.warmup, args.steps), file=sys.stderr,
+          flush=True)
+    for _ in range(args.warmup):
+        net(x, wl.T, cond=cond, workspace=ws)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        net(x, wl.T, cond=cond, workspace=ws)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    avg_s = sum(a.elapsed_time(b) for a, b in ev) / args.steps / 1e3
+    flop = cond_flops(wl)
+    out_bytes = wl.B * wl.T * 2 * wl.n_layers * wl.r * 4
+    out = {
+        "metric": "conditioned audio steps/s (conditioning network, all streams)",
+        "value": round(wl.B * wl.T * args.steps / elapsed, 1),
+        "unit": "samples/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded 227-dim phoneme/stress/F0 features, N(0,1/fan_in) weights)",
+        "config": {"workload": wl.description, "B": wl.B, "n_frames": wl.n_frames, "T": wl.T, "h1": wl.h1,
+                   "h2": wl.n_layers * wl.r},
+        "real_time_factor_16khz": round(wl.T / avg_s / RATE_HZ, 1),
+        "roofline": {
+            "bound": "mfma",
+            "achieved": round(flop / avg_s / 1e12, 4),
+            "peak": PEAKS["f32_mfma_tflops"],
+            "unit": "TFLOP/s",
+            "frac": round(flop / avg_s / 1e12 / PEAKS["f32_mfma_tflops"], 6),
+            "traffic": None,
+            "note": "whole wn_condition call (gate contractions, pools, upsampling) against the fp32 MFMA peak",
+            "algorithmic_flop_per_launch": flop,
+            "hbm": {"output_bytes_per_launch": out_bytes, "achieved_gbs": round(out_bytes / avg_s / 1e9, 2),
+                    "peak_gbs": PEAKS["hbm_gbs"], "frac": round(out_bytes / avg_s / 1e9 / PEAKS["hbm_gbs"], 6)},
+            "avg_launch_ms": round(avg_s * 1e3, 4),
+        },
+        "cpu_baseline": None,
+    }
+    print(json.dumps(out), flush=True)
+    net.close()
+    del x, cond, ws
+    torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="l20_r64_b1", help="a workload name, or 'all' (one JSON line each)")
+    ap.add_argument("--workload", default="l20_r64_b1",
+                    help="a generation or conditioning-network workload name, or 'all' (one JSON line each)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="least oracle time for the CPU baseline, in whole streams (0 = skip)")
     ap.add_argument("--cpu-steps", type=int, default=None, choices=[0], help="0: skip the CPU baseline")
@@ -217,9 +290,12 @@ def main():
               "batch would shard by stream, each GPU holding a weight replica)" % args.gpus, file=sys.stderr)
         sys.exit(2)
     import synth
-    names = list(synth.WORKLOADS) if args.workload == "all" else [args.workload]
+    names = list(synth.WORKLOADS) + list(synth.COND_WORKLOADS) if args.workload == "all" else [args.workload]
     for name in names:
-        run_workload(name, args)
+        if name in synth.COND_WORKLOADS:
+            run_cond_workload(name, args)
+        else:
+            run_workload(name, args)
 
 
 if __name__ == "__main__":

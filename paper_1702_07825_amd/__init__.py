@@ -22,7 +22,8 @@ WN_OK, WN_EINVAL, WN_EUNSUPPORTED, WN_ENOMEM, WN_EHIP, WN_ETIMEOUT, WN_EABORTED 
 WN_F32, WN_BF16 = 0, 1
 A_CLASSES = 256
 EXPORTED = ("wn_create", "wn_workspace_bytes", "wn_generate", "wn_generate_sampled", "wn_teacher_force", "wn_status",
-            "wn_kernel_variant", "wn_destroy", "wn_error_string", "wn_last_error")
+            "wn_kernel_variant", "wn_destroy", "wn_error_string", "wn_last_error",
+            "wn_cond_create", "wn_cond_workspace_bytes", "wn_condition", "wn_cond_destroy")
 # wn_sample_mode_t: how a step's distribution becomes its sample
 SAMPLE_DIRECT, SAMPLE_TEMPERATURE, SAMPLE_TOPK, SAMPLE_MODE, SAMPLE_MEAN = 0, 1, 2, 3, 4
 
@@ -44,6 +45,15 @@ class Config(ctypes.Structure):
 
 class Sampler(ctypes.Structure):
     _fields_ = [("mode", ctypes.c_int32), ("temperature", ctypes.c_float), ("top_k", ctypes.c_int32)]
+
+
+class CondConfig(ctypes.Structure):
+    _fields_ = [("n_features", ctypes.c_int32), ("h1", ctypes.c_int32), ("n_layers", ctypes.c_int32),
+                ("r", ctypes.c_int32), ("frame_rate", ctypes.c_int32), ("audio_rate", ctypes.c_int32)]
+
+
+class CondWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.POINTER(ctypes.c_float)) for n in ("w1", "b1", "w2", "b2")]
 
 
 WEIGHT_FIELDS = ("embed", "b_embed", "w_prev", "w_cur", "b_gate", "w_res", "b_res", "w_skip", "b_skip",
@@ -72,6 +82,14 @@ def load_library(path: str = LIB_PATH):
         L.wn_generate.argtypes = [vp, i32, i32, vp, vp, vp, vp, sz, i32, vp]
         L.wn_generate_sampled.restype = ctypes.c_int
         L.wn_generate_sampled.argtypes = [vp, i32, i32, vp, vp, vp, vp, sz, i32, ctypes.POINTER(Sampler), vp]
+        L.wn_cond_create.restype = ctypes.c_int
+        L.wn_cond_create.argtypes = [ctypes.POINTER(CondConfig), ctypes.POINTER(CondWeights), ctypes.POINTER(vp)]
+        L.wn_cond_workspace_bytes.restype = sz
+        L.wn_cond_workspace_bytes.argtypes = [vp, i32, i32]
+        L.wn_condition.restype = ctypes.c_int
+        L.wn_condition.argtypes = [vp, i32, i32, vp, i32, vp, vp, sz, vp]
+        L.wn_cond_destroy.restype = None
+        L.wn_cond_destroy.argtypes = [vp]
         L.wn_teacher_force.restype = ctypes.c_int
         L.wn_teacher_force.argtypes = [vp, i32, i32, vp, vp, vp, vp, sz, i32, vp]
         L.wn_status.restype = ctypes.c_int
@@ -205,3 +223,52 @@ class WaveNet:
     def status(self, workspace, stream=None) -> int:
         """Synchronise the stream and return the kernel status word (0 = ok)."""
         return int(self._lib.wn_status(self._h, workspace.data_ptr(), _stream_handle(stream)))
+
+
+class Conditioner:
+    """The conditioning network on one GPU (wraps wn_cond_create / wn_cond_destroy, include/wn_cond.h).
+
+    ``weights``: fp32 host arrays w1 [2, 3 h1, 2, F], b1 [2, 3 h1], w2 [2, 3 h2, 2, 2 h1], b2 [2, 3 h2]
+    with h2 = n_layers * r.
+    """
+
+    def __init__(self, weights: Dict[str, np.ndarray], n_layers: int, r: int, frame_rate: int, audio_rate: int):
+        self._lib = load_library()
+        self._h = None
+        w = {k: np.ascontiguousarray(weights[k], dtype=np.float32) for k in ("w1", "b1", "w2", "b2")}
+        _, three_h1, _, F = w["w1"].shape
+        self.n_features, self.h1 = int(F), int(three_h1 // 3)
+        self.n_layers, self.r = int(n_layers), int(r)
+        cfg = CondConfig(self.n_features, self.h1, self.n_layers, self.r, int(frame_rate), int(audio_rate))
+        ws = CondWeights(*[w[k].ctypes.data_as(ctypes.POINTER(ctypes.c_float)) for k in ("w1", "b1", "w2", "b2")])
+        h = ctypes.c_void_p()
+        _check(self._lib.wn_cond_create(ctypes.byref(cfg), ctypes.byref(ws), ctypes.byref(h)), "wn_cond_create")
+        self._h = h
+
+    def close(self):
+        if self._h is not None:
+            self._lib.wn_cond_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def workspace_bytes(self, B: int, n_frames: int) -> int:
+        return int(self._lib.wn_cond_workspace_bytes(self._h, int(B), int(n_frames)))
+
+    def __call__(self, features, T: int, cond=None, workspace=None, stream=None):
+        """features fp32 [B, n_frames, F] (device) -> cond fp32 [B, T, n_layers, 2r]."""
+        import torch
+        B, Tf = int(features.shape[0]), int(features.shape[1])
+        fp = _dev_ptr(features, torch.float32, (B, Tf, self.n_features), "features")
+        if cond is None:
+            cond = torch.empty((B, T, self.n_layers, 2 * self.r), dtype=torch.float32, device=features.device)
+        cp = _dev_ptr(cond, torch.float32, (B, T, self.n_layers, 2 * self.r), "cond")
+        if workspace is None:
+            workspace = torch.empty(max(self.workspace_bytes(B, Tf), 1), dtype=torch.uint8, device=features.device)
+        _check(self._lib.wn_condition(self._h, B, Tf, fp, int(T), cp, workspace.data_ptr(), workspace.numel(),
+                                      _stream_handle(stream)), "wn_condition")
+        return cond

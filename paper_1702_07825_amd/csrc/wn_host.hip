@@ -26,6 +26,16 @@ struct wn_handle {
   void* dpack = nullptr;  // its packed bf16 weight tiles
 };
 
+namespace {
+thread_local std::string g_err;
+}  // namespace
+
+int wn_set_last_error(int code, const char* msg) {
+  g_err = msg;
+  return code;
+}
+void wn_clear_last_error() { g_err.clear(); }
+
 // Round fp32 to bfloat16, nearest even (NaN stays NaN).
 uint16_t wn_to_bf16(float f) {
   uint32_t u;
@@ -39,8 +49,6 @@ uint16_t wn_to_bf16(float f) {
 }
 
 namespace {
-
-thread_local std::string g_err;
 
 int fail(int code, const std::string& msg) {
   g_err = msg;

@@ -134,5 +134,9 @@ std::vector<uint16_t> wn_group_pack(int L, int R, int S, const float* w_prev, co
                                     const float* w_out);
 hipError_t wn_group_launch(const WnGroupArgs& g, bool teacher, hipStream_t stream);
 
+// The calling thread's last-error detail (wn_last_error): set it and return `code`, or clear it.
+int wn_set_last_error(int code, const char* msg);
+void wn_clear_last_error();
+
 // fp32 -> bf16 bit pattern, round to nearest even (NaN stays NaN).
 uint16_t wn_to_bf16(float f);

@@ -201,3 +201,34 @@ def make_cond_weights(n_features: int, h1: int, h2: int, seed: int, bias_scale: 
         w["w" + name] = (rng.standard_normal((2, 3 * h, 2, cin)) / np.sqrt(2 * cin)).astype(np.float32)
         w["b" + name] = (rng.standard_normal((2, 3 * h)) * bias_scale).astype(np.float32)
     return w
+
+
+@dataclasses.dataclass(frozen=True)
+class CondWorkload:
+    name: str
+    n_features: int
+    h1: int
+    n_layers: int
+    r: int
+    B: int
+    n_frames: int
+    frame_rate: int
+    audio_rate: int
+    description: str
+
+    @property
+    def T(self) -> int:
+        return self.n_frames * self.audio_rate // self.frame_rate
+
+
+def _cond_wl(name, n_layers, r, B, seconds):
+    fr, ar = FRAME_RATE_HZ, SAMPLE_RATE_HZ
+    return CondWorkload(name, N_FEATURES, COND_H1, n_layers, r, B, seconds * fr, fr, ar,
+                        "conditioning network: %d features at %d Hz -> l=%d x 2r=%d at %d Hz, h1=%d, B=%d, %d s"
+                        % (N_FEATURES, fr, n_layers, 2 * r, ar, COND_H1, B, seconds))
+
+
+COND_WORKLOADS = {
+    "cond_l20_r64_b1": _cond_wl("cond_l20_r64_b1", 20, 64, 1, 1),
+    "cond_l20_r64_b256": _cond_wl("cond_l20_r64_b256", 20, 64, 256, 2),
+}

@@ -1,5 +1,5 @@
 """C ABI checks that need no GPU: the library loads, exports every function that
-include/wn.h declares, and rejects bad arguments before touching the device."""
+include/*.h declares, and rejects bad arguments before touching the device."""
 import ctypes
 import os
 import re
@@ -10,9 +10,13 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 def _declared():
-    src = open(os.path.join(ROOT, "include", "wn.h")).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(wn_[a-z_]+)\s*\(", src)))
+    names = set()
+    for h in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        if h.endswith(".h"):
+            src = open(os.path.join(ROOT, "include", h)).read()
+            src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+            names |= set(re.findall(r"\b(wn_[a-z_]+)\s*\(", src))
+    return sorted(names)
 
 
 @pytest.fixture(scope="module")
@@ -101,3 +105,19 @@ def _load_missing(wn, path):
         wn.load_library(path)
     finally:
         wn._lib = saved
+
+
+def test_conditioning_network_rejects_before_any_device_call(lib):
+    import paper_1702_07825_amd as wn
+    vp = ctypes.c_void_p
+    out = vp()
+    w = wn.CondWeights(*([ctypes.cast(ctypes.create_string_buffer(4), ctypes.POINTER(ctypes.c_float))] * 4))
+    for cfg in [wn.CondConfig(0, 8, 2, 4, 256, 16000), wn.CondConfig(227, 0, 2, 4, 256, 16000),
+                wn.CondConfig(227, 8, 0, 4, 256, 16000), wn.CondConfig(227, 8, 2, 4, 0, 16000),
+                wn.CondConfig(227, 8, 4096, 4, 256, 16000)]:
+        assert lib.wn_cond_create(ctypes.byref(cfg), ctypes.byref(w), ctypes.byref(out)) == wn.WN_EINVAL
+        assert lib.wn_last_error().decode()
+    assert lib.wn_cond_create(None, None, None) == wn.WN_EINVAL
+    assert lib.wn_cond_workspace_bytes(None, 1, 1) == 0
+    assert lib.wn_condition(None, 1, 1, None, 1, None, None, 0, None) == wn.WN_EINVAL
+    lib.wn_cond_destroy(None)

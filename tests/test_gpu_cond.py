@@ -1,0 +1,129 @@
+"""GPU parity of the conditioning network (Appendix A.2) through the C ABI (include/wn_cond.h).
+
+The GPU output is compared element by element with the oracle (fp64, per-frame recurrences) on
+the same seeded features and weights: max-abs 1e-4.  That bound is fp32 arithmetic over
+contractions of up to 2 x 2 h1 terms, then a recurrence over the frames whose forget gate keeps
+the error from growing.  Cases span several 64 x 64 GEMM tiles with ragged edges, a channel
+count not a multiple of 4, the paper's sizes (227 features, 20 x 64 channels per direction at
+256 Hz) and an end-to-end run: features -> conditioning -> generation.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+
+def _wn():
+    import paper_1702_07825_amd as wn
+    return wn
+
+
+CASES = [
+    # name, F, h1, n_layers, r, B, n_frames, frame_rate, audio_rate
+    ("ragged_tiles", 227, 40, 3, 16, 2, 70, 256, 16000),
+    ("odd_channels", 19, 7, 3, 3, 3, 33, 3, 8),
+    ("one_frame", 5, 4, 1, 4, 1, 1, 1, 16),
+    ("frame_rate_output", 227, 256, 4, 64, 2, 90, 1, 1),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_conditioning_matches_oracle(case):
+    name, F, h1, L, r, B, Tf, fr, ar = case
+    print("cond case %s" % name, flush=True)
+    wn = _wn()
+    w = synth.make_cond_weights(F, h1, L * r, seed=len(name), bias_scale=0.2)
+    x = synth.make_features(B, Tf, seed=3)[:, :, :F] if F <= synth.N_FEATURES else None
+    x = np.ascontiguousarray(x + np.random.default_rng(1).normal(0, 0.1, x.shape).astype(np.float32))
+    T = (Tf * ar) // fr
+    net = wn.Conditioner(w, L, r, fr, ar)
+    cond = net(torch.tensor(x, device="cuda"), T)
+    torch.cuda.synchronize()
+    got = cond.cpu().numpy().reshape(B, T, 2 * L * r)
+    worst = 0.0
+    for b in range(B):
+        ref = oracle.condition(w, x[b], T, fr, ar)
+        worst = max(worst, float(np.abs(got[b] - ref).max()))
+    print("  max|dcond| = %.3g" % worst, flush=True)
+    assert worst <= TOL
+    net.close()
+
+
+def test_paper_sizes_and_upsampling():
+    """227 features, h1 = 256, l = 20, r = 64 (h2 = 1280 per direction), 256 frames (1 s) at 256 Hz:
+    frame-level values against the oracle, and the 16 kHz output equal to the frames gathered."""
+    wn = _wn()
+    F, h1, L, r, B, Tf = synth.N_FEATURES, synth.COND_H1, 20, 64, 2, 256
+    w = synth.make_cond_weights(F, h1, L * r, seed=11)
+    x = synth.make_features(B, Tf, seed=12)
+    xd = torch.tensor(x, device="cuda")
+    frame = wn.Conditioner(w, L, r, 1, 1)
+    audio = wn.Conditioner(w, L, r, synth.FRAME_RATE_HZ, synth.SAMPLE_RATE_HZ)
+    T = Tf * synth.SAMPLE_RATE_HZ // synth.FRAME_RATE_HZ
+    cf = frame(xd, Tf)
+    ca = audio(xd, T)
+    torch.cuda.synchronize()
+    idx = torch.arange(T, device="cuda") * synth.FRAME_RATE_HZ // synth.SAMPLE_RATE_HZ
+    assert torch.equal(ca, cf[:, idx])
+    ref = oracle.condition(w, x[1], Tf, 1, 1)
+    err = float(np.abs(cf[1].cpu().numpy().reshape(Tf, -1) - ref).max())
+    print("  paper sizes: max|dcond| = %.3g, |cond| max %.3g" % (err, float(np.abs(ref).max())), flush=True)
+    assert err <= TOL
+    frame.close()
+    audio.close()
+
+
+def test_end_to_end_features_to_samples():
+    """features -> wn_condition -> wn_generate, against the oracle's conditioning fed to the
+    oracle's generation (teacher-forced on the GPU's samples): logits within 1e-3, indices
+    bit-exact at confident steps."""
+    wn = _wn()
+    L, r, s, B, Tf = 20, 64, 256, 2, 6
+    fr, ar = synth.FRAME_RATE_HZ, synth.SAMPLE_RATE_HZ
+    T = Tf * ar // fr
+    dil = tuple(synth.dilation_cycle(L))
+    cw = synth.make_cond_weights(synth.N_FEATURES, 64, L * r, seed=21, bias_scale=0.1)
+    x = synth.make_features(B, Tf, seed=22)
+    cnet = wn.Conditioner(cw, L, r, fr, ar)
+    cond = cnet(torch.tensor(x, device="cuda"), T)
+    ww = synth.make_weights(L, r, s, seed=23)
+    gnet = wn.WaveNet(ww, dil)
+    u = torch.tensor(synth.make_uniforms(B, T, seed=24), device="cuda")
+    y = gnet.generate(cond, u)
+    lg = gnet.teacher_force(cond, y)
+    torch.cuda.synchronize()
+    y_np, lg_np, u_np = y.cpu().numpy(), lg.cpu().numpy(), u.cpu().numpy()
+    model = oracle.Model(ww, dil)
+    for b in range(B):
+        oc = oracle.condition(cw, x[b], T, fr, ar).astype(np.float32).reshape(T, L, 2 * r)
+        ys, lo, mg = oracle.run(model, oc, u=u_np[b], y_in=y_np[b])
+        ok = mg > 1e-4
+        err = float(np.abs(lg_np[b] - lo).max())
+        print("  stream %d: max|dlogit| %.3g, confident %d/%d, mismatches %d" %
+              (b, err, int(ok.sum()), T, int((ys[ok] != y_np[b][ok]).sum())), flush=True)
+        assert err <= 1e-3
+        assert np.array_equal(ys[ok], y_np[b][ok])
+    cnet.close()
+    gnet.close()
+
+
+def test_conditioning_argument_checks():
+    wn = _wn()
+    w = synth.make_cond_weights(8, 4, 8, seed=1)
+    net = wn.Conditioner(w, 2, 4, 256, 16000)
+    x = torch.zeros((1, 4, 8), device="cuda")
+    with pytest.raises(wn.WnError) as e:
+        net(x, 4 * 16000 // 256 + 1)  # past the last frame
+    assert e.value.code == wn.WN_EINVAL
+    out = net(x, 0)
+    assert out.shape == (1, 0, 2, 8)
+    small = torch.empty(16, dtype=torch.uint8, device="cuda")
+    with pytest.raises(wn.WnError):
+        net(x, 10, workspace=small)
+    net.close()
