@@ -4,9 +4,10 @@
 // in include/wn_cond.h.
 //
 // Each layer is two kernels.  The gate pre-activations of all frames at once are a dense
-// contraction, [B*Tf x 2 cin] . [2 cin x 3h] per direction (the width-2 convolution: inputs
-// 0..cin-1 are the direction's previous frame, cin..2cin-1 the current one), run on fp32 MFMA
-// (v_mfma_f32_16x16x4_f32) in 64 x 64 tiles staged through LDS.  The fo-pool is a linear
+// contraction, [3h x 2 cin] . [2 cin x B*Tf] per direction (the width-2 convolution: tap 0 is the
+// direction's previous frame, tap 1 the current one), run on fp32 MFMA (v_mfma_f32_16x16x4f32) in
+// 128 x 128 tiles staged through double-buffered LDS; the weights are stored with each tap padded
+// to a multiple of 32 inputs so that K chunks never straddle the taps.  The fo-pool is a linear
 // recurrence along the frames, independent per (stream, direction, channel): one thread each,
 // with the gate pre-activations of 16 frames loaded ahead of the dependent chain.  The second
 // layer's pool writes its output interleaved, and a last kernel repeats every frame over its
@@ -23,6 +24,7 @@
 struct wn_cond {
   int device = 0;
   int F = 0, h1 = 0, h2 = 0, fr = 1, ar = 1;
+  int cinp1 = 0, cinp2 = 0;  // per-tap input widths of the two layers rounded up to 32
   void* dmem = nullptr;
   const float *w1 = nullptr, *b1 = nullptr, *w2 = nullptr, *b2 = nullptr;
 };
@@ -31,79 +33,136 @@ namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int TM = 64, TN = 64, TK = 16;  // output tile (frames x gate rows) and K chunk
-constexpr int NTG = 256;                  // four waves, each a 32 x 32 sub-tile
-
 struct GateArgs {
   const float* x;  // [B][Tf][cin]
-  const float* w;  // [2][N][2 cin]
+  const float* w;  // [2][N][2 cinp]: tap 0 (previous frame) inputs 0..cin-1, tap 1 at cinp.., zeros past cin
   const float* b;  // [2][N]
   float* p;        // [B][Tf][2][N]
-  int B, Tf, cin, N;
+  int B, Tf, cin, cinp, N;
 };
 
-// Gate pre-activations p[b][t][dir][n] = b[dir][n] + sum_k w[dir][n][k] x2[b][t][k], where
-// x2[b][t] = [x[b][t'], x[b][t]] with t' = t - 1 (forward) or t + 1 (backward), zero outside.
-__global__ __launch_bounds__(NTG) void qrnn_gate_gemm(const GateArgs a) {
+// Gate pre-activations of every frame of a layer, both directions (grid.z):
+//   p[b][t][dir][n] = b[dir][n] + sum_k w[dir][n][0][k] x[b][t'][k] + w[dir][n][1][k] x[b][t][k]
+// with t' = t - 1 (forward) or t + 1 (backward) and x = 0 outside the frames: the width-2
+// convolution as one dense contraction [N x 2 cinp] . [2 cinp x B Tf] on fp32 MFMA
+// (v_mfma_f32_16x16x4f32).  128 x 128 output tiles (gate rows x frames) per 256 threads, each wave
+// a 64 x 64 quarter; K in chunks of 32 that never straddle the two taps (cinp is a multiple of
+// 32).  LDS is double-buffered, one barrier per chunk, with the next chunk's global loads in
+// flight during the current chunk's products.  The MFMA A operand is the weight rows and B the
+// frames, so each lane ends with four consecutive gate rows of one frame.  Within a chunk the k
+// index is permuted (lane group q of MFMA step e takes k = 4q + e of each 16), identically for
+// both operands, so one b128 LDS read feeds four MFMA steps.  VX: the input rows are float4
+// aligned (cin % 4 == 0), else they are read one float at a time.
+constexpr int NTG = 256;
+constexpr int VM = 128, VN = 128, VK = 32, VLD = VK + 4;  // tile, K chunk, LDS row (floats)
+
+template <bool VX>
+__global__ __launch_bounds__(NTG, 2) void qrnn_gate_gemm(const GateArgs a) {
   const int dir = blockIdx.z;
-  const int m0 = blockIdx.x * TM, n0 = blockIdx.y * TN;
-  const int M = a.B * a.Tf, K = 2 * a.cin;
-  __shared__ float As[TM][TK + 1];
-  __shared__ float Bs[TN][TK + 1];
+  const int m0 = blockIdx.x * VM, n0 = blockIdx.y * VN;
+  const int M = a.B * a.Tf, K = 2 * a.cinp, N = a.N;
+  __shared__ __align__(16) float Ws[2][VN][VLD];
+  __shared__ __align__(16) float Xs[2][VM][VLD];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int wm = (wave >> 1) * 32, wn = (wave & 1) * 32;
-  const int row = lane & 15, kq = lane >> 4;  // MFMA operand: row / column of the 16, k of the 4
-  f32x4 acc[2][2];
+  const int wn = (wave >> 1) * 64, wm = (wave & 1) * 64;
+  const int r16 = lane & 15, q = lane >> 4;
+  // global -> LDS assignment: rows tid/8 + 32 i, float4 column tid % 8 of the chunk
+  const int lr = tid >> 3, lc = (tid & 7) * 4;
+  const float* wd = a.w + (size_t)dir * N * K;
+  const float* xcur[4];
+  const float* xprev[4];
+  const float* wrow[4];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + lr + 32 * i;
+    xcur[i] = xprev[i] = nullptr;
+    if (m < M) {
+      const int bb = m / a.Tf, t = m - bb * a.Tf;
+      const int tp = dir == 0 ? t - 1 : t + 1;
+      xcur[i] = a.x + ((size_t)bb * a.Tf + t) * a.cin;
+      if (tp >= 0 && tp < a.Tf) xprev[i] = a.x + ((size_t)bb * a.Tf + tp) * a.cin;
+    }
+    const int n = n0 + lr + 32 * i;
+    wrow[i] = n < N ? wd + (size_t)n * K + lc : nullptr;
+  }
+  f32x4 gx[4], gw[4];
+  auto load = [&](int k0) {
+    const bool prev = k0 < a.cinp;
+    const int kk = (prev ? k0 : k0 - a.cinp) + lc;  // input index of this thread's first float
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const float* wd = a.w + (size_t)dir * a.N * K;
-  for (int k0 = 0; k0 < K; k0 += TK) {
-    for (int i = tid; i < TM * TK; i += NTG) {
-      const int r = i / TK, kk = i % TK;
-      const int m = m0 + r, k = k0 + kk;
-      float v = 0.f;
-      if (m < M && k < K) {
-        const int bb = m / a.Tf, t = m % a.Tf;
-        const bool prev = k < a.cin;
-        const int tt = prev ? (dir == 0 ? t - 1 : t + 1) : t;
-        if (tt >= 0 && tt < a.Tf) v = a.x[((size_t)bb * a.Tf + tt) * a.cin + (prev ? k : k - a.cin)];
+    for (int i = 0; i < 4; ++i) {
+      const float* xp = prev ? xprev[i] : xcur[i];
+      if (VX) {
+        gx[i] = xp && kk < a.cin ? *reinterpret_cast<const f32x4*>(xp + kk) : f32x4{0.f, 0.f, 0.f, 0.f};
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) gx[i][e] = xp && kk + e < a.cin ? xp[kk + e] : 0.f;
       }
-      As[r][kk] = v;
+      gw[i] = wrow[i] ? *reinterpret_cast<const f32x4*>(wrow[i] + k0) : f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    for (int i = tid; i < TN * TK; i += NTG) {
-      const int r = i / TK, kk = i % TK;
-      const int n = n0 + r, k = k0 + kk;
-      Bs[r][kk] = (n < a.N && k < K) ? wd[(size_t)n * K + k] : 0.f;
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      *reinterpret_cast<f32x4*>(&Xs[buf][lr + 32 * i][lc]) = gx[i];
+      *reinterpret_cast<f32x4*>(&Ws[buf][lr + 32 * i][lc]) = gw[i];
     }
-    __syncthreads();
+  };
+  f32x4 acc[4][4];
 #pragma unroll
-    for (int ks = 0; ks < TK; ks += 4) {
-      float av[2], bv[2];
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int i = 0; i < 2; ++i) av[i] = As[wm + i * 16 + row][ks + kq];
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  load(0);
+  stash(0);
+  __syncthreads();
+  const int nk = K / VK;
+  for (int c = 0; c < nk; ++c) {
+    const int buf = c & 1;
+    if (c + 1 < nk) load((c + 1) * VK);
 #pragma unroll
-      for (int j = 0; j < 2; ++j) bv[j] = Bs[wn + j * 16 + row][ks + kq];
+    for (int h = 0; h < VK; h += 16) {
+      f32x4 wa[4], xb[4];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < 4; ++i) wa[i] = *reinterpret_cast<const f32x4*>(&Ws[buf][wn + 16 * i + r16][h + 4 * q]);
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], bv[j], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < 4; ++j) xb[j] = *reinterpret_cast<const f32x4*>(&Xs[buf][wm + 16 * j + r16][h + 4 * q]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(wa[i][e], xb[j][e], acc[i][j], 0, 0, 0);
     }
+    if (c + 1 < nk) stash(buf ^ 1);
     __syncthreads();
   }
-  // result (i, j): lane holds rows 4 kq .. 4 kq + 3 of column `row`
+  // acc[i][j]: lane holds gate rows wn + 16 i + 4 q .. +3 of frame wm + 16 j + r16
+  const float* bd = a.b + (size_t)dir * N;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 4; ++i) {
+    const int n = n0 + wn + 16 * i + 4 * q;
+    if (n >= N) continue;
+    const bool whole = (N & 3) == 0;  // then n + 3 < N and the row offsets are float4 aligned
+    f32x4 bias;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int n = n0 + wn + j * 16 + row;
+    for (int v = 0; v < 4; ++v) bias[v] = n + v < N ? bd[n + v] : 0.f;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int m = m0 + wm + i * 16 + 4 * kq + v;
-        if (m < M && n < a.N) a.p[((size_t)m * 2 + dir) * a.N + n] = acc[i][j][v] + a.b[(size_t)dir * a.N + n];
+    for (int j = 0; j < 4; ++j) {
+      const int m = m0 + wm + 16 * j + r16;
+      if (m >= M) continue;
+      float* dst = a.p + ((size_t)m * 2 + dir) * N + n;
+      const f32x4 v4 = acc[i][j] + bias;
+      if (whole) {
+        *reinterpret_cast<f32x4*>(dst) = v4;
+      } else {
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          if (n + v < N) dst[v] = v4[v];
       }
     }
+  }
 }
 
 struct PoolArgs {
@@ -149,23 +208,32 @@ __global__ __launch_bounds__(256) void qrnn_pool(const PoolArgs a) {
   }
 }
 
-// cond[b][tau][c] = src[b][floor(tau * fr / ar)][c] for c < C (C % 4 == 0: float4 copies).
-__global__ __launch_bounds__(256) void cond_upsample4(const float4* src, float4* cond, int Tf, long long T, int C4,
-                                                      long long n4, int fr, int ar) {
-  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (long long)gridDim.x * blockDim.x) {
-    const long long row = i / C4, c = i - row * C4;
-    const long long b = row / T, tau = row - b * T;
-    const long long t = tau * fr / ar;
-    cond[i] = src[((size_t)b * Tf + t) * C4 + c];
+// Upsampling by repetition: cond[b][tau][:] = src[b][floor(tau fr / ar)][:].  One block per source
+// frame (b, t); the frame covers the audio steps ceil(t ar / fr) <= tau < ceil((t + 1) ar / fr)
+// (clipped to T), so its row is read once and stored to each of them (plain stores: nontemporal
+// ones measured 4% slower here).
+__global__ __launch_bounds__(256) void cond_repeat4(const f32x4* src, f32x4* cond, int Tf, long long T, int C4,
+                                                    int fr, int ar) {
+  const long long b = blockIdx.x / Tf, t = blockIdx.x - b * Tf;
+  const long long tau0 = (t * ar + fr - 1) / fr;
+  const long long tau1 = std::min<long long>(T, ((t + 1) * ar + fr - 1) / fr);
+  const f32x4* s = src + (size_t)blockIdx.x * C4;
+  f32x4* o = cond + (size_t)b * T * C4;
+  for (int c = threadIdx.x; c < C4; c += 256) {
+    const f32x4 v = s[c];
+    for (long long tau = tau0; tau < tau1; ++tau) o[tau * C4 + c] = v;
   }
 }
-__global__ __launch_bounds__(256) void cond_upsample1(const float* src, float* cond, int Tf, long long T, int C,
-                                                      long long n, int fr, int ar) {
-  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long long)gridDim.x * blockDim.x) {
-    const long long row = i / C, c = i - row * C;
-    const long long b = row / T, tau = row - b * T;
-    const long long t = tau * fr / ar;
-    cond[i] = src[((size_t)b * Tf + t) * C + c];
+__global__ __launch_bounds__(256) void cond_repeat1(const float* src, float* cond, int Tf, long long T, int C, int fr,
+                                                    int ar) {
+  const long long b = blockIdx.x / Tf, t = blockIdx.x - b * Tf;
+  const long long tau0 = (t * ar + fr - 1) / fr;
+  const long long tau1 = std::min<long long>(T, ((t + 1) * ar + fr - 1) / fr);
+  const float* s = src + (size_t)blockIdx.x * C;
+  float* o = cond + (size_t)b * T * C;
+  for (int c = threadIdx.x; c < C; c += 256) {
+    const float v = s[c];
+    for (long long tau = tau0; tau < tau1; ++tau) o[tau * C + c] = v;
   }
 }
 
@@ -201,16 +269,27 @@ class DeviceScope {
   bool ok_ = false;
 };
 
-hipError_t run_layer(const float* x, int B, int Tf, int cin, int H, const float* w, const float* b, float* p,
-                     float* out, int interleave, hipStream_t st) {
-  GateArgs g{x, w, b, p, B, Tf, cin, 3 * H};
-  const dim3 grid((unsigned)((B * Tf + TM - 1) / TM), (unsigned)((3 * H + TN - 1) / TN), 2);
-  hipLaunchKernelGGL(qrnn_gate_gemm, grid, dim3(NTG), 0, st, g);
+hipError_t run_layer(const float* x, int B, int Tf, int cin, int cinp, int H, const float* w, const float* b,
+                     float* p, float* out, int interleave, hipStream_t st) {
+  GateArgs g{x, w, b, p, B, Tf, cin, cinp, 3 * H};
+  const dim3 grid((unsigned)((B * Tf + VM - 1) / VM), (unsigned)((3 * H + VN - 1) / VN), 2);
+  if (cin % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0)
+    hipLaunchKernelGGL(qrnn_gate_gemm<true>, grid, dim3(NTG), 0, st, g);
+  else
+    hipLaunchKernelGGL(qrnn_gate_gemm<false>, grid, dim3(NTG), 0, st, g);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   PoolArgs pa{p, out, B, Tf, H, interleave};
   hipLaunchKernelGGL(qrnn_pool, dim3((unsigned)((H + 255) / 256), (unsigned)(2 * B)), dim3(256), 0, st, pa);
   return hipGetLastError();
+}
+
+// [2][n][2][cin] -> [2][n][2][cinp], zeros in inputs cin..cinp-1 of each tap.
+std::vector<float> pad_taps(const float* w, int n, int cin, int cinp) {
+  std::vector<float> out((size_t)2 * n * 2 * cinp, 0.f);
+  for (size_t row = 0; row < (size_t)2 * n * 2; ++row)
+    std::memcpy(out.data() + row * cinp, w + row * cin, (size_t)cin * sizeof(float));
+  return out;
 }
 
 }  // namespace
@@ -236,10 +315,19 @@ int wn_cond_create(const wn_cond_config* cfg, const wn_cond_weights* w, wn_cond*
     delete c;
     return wn_set_last_error(WN_EHIP, "hipGetDevice failed");
   }
-  const size_t n_w1 = (size_t)2 * 3 * c->h1 * 2 * c->F, n_b1 = (size_t)2 * 3 * c->h1;
-  const size_t n_w2 = (size_t)2 * 3 * c->h2 * 2 * 2 * c->h1, n_b2 = (size_t)2 * 3 * c->h2;
-  const size_t o_b1 = align_up(n_w1 * 4, 256), o_w2 = align_up(o_b1 + n_b1 * 4, 256);
-  const size_t o_b2 = align_up(o_w2 + n_w2 * 4, 256), total = align_up(o_b2 + n_b2 * 4, 256);
+  c->cinp1 = (c->F + 31) / 32 * 32;
+  c->cinp2 = (2 * c->h1 + 31) / 32 * 32;
+  std::vector<float> w1p, w2p;
+  try {
+    w1p = pad_taps(w->w1, 3 * c->h1, c->F, c->cinp1);
+    w2p = pad_taps(w->w2, 3 * c->h2, 2 * c->h1, c->cinp2);
+  } catch (const std::bad_alloc&) {
+    delete c;
+    return wn_set_last_error(WN_ENOMEM, "host allocation");
+  }
+  const size_t n_b1 = (size_t)2 * 3 * c->h1, n_b2 = (size_t)2 * 3 * c->h2;
+  const size_t o_b1 = align_up(w1p.size() * 4, 256), o_w2 = align_up(o_b1 + n_b1 * 4, 256);
+  const size_t o_b2 = align_up(o_w2 + w2p.size() * 4, 256), total = align_up(o_b2 + n_b2 * 4, 256);
   hipError_t e = hipMalloc(&c->dmem, total);
   if (e != hipSuccess) {
     delete c;
@@ -248,7 +336,7 @@ int wn_cond_create(const wn_cond_config* cfg, const wn_cond_weights* w, wn_cond*
   }
   char* d = static_cast<char*>(c->dmem);
   const struct { const float* src; size_t n, off; } parts[] = {
-      {w->w1, n_w1, 0}, {w->b1, n_b1, o_b1}, {w->w2, n_w2, o_w2}, {w->b2, n_b2, o_b2}};
+      {w1p.data(), w1p.size(), 0}, {w->b1, n_b1, o_b1}, {w2p.data(), w2p.size(), o_w2}, {w->b2, n_b2, o_b2}};
   for (const auto& pt : parts) {
     if (e == hipSuccess) e = hipMemcpy(d + pt.off, pt.src, pt.n * 4, hipMemcpyHostToDevice);
   }
@@ -291,21 +379,17 @@ int wn_condition(wn_cond* c, int32_t B, int32_t n_frames, const float* features,
   float* p = reinterpret_cast<float*>(ws + l.p_off);
   float* z1 = reinterpret_cast<float*>(ws + l.z1_off);
   float* cf = reinterpret_cast<float*>(ws + l.c_off);
-  hipError_t e = run_layer(features, B, n_frames, c->F, c->h1, c->w1, c->b1, p, z1, 0, st);
-  if (e == hipSuccess) e = run_layer(z1, B, n_frames, 2 * c->h1, c->h2, c->w2, c->b2, p, cf, 1, st);
+  hipError_t e = run_layer(features, B, n_frames, c->F, c->cinp1, c->h1, c->w1, c->b1, p, z1, 0, st);
+  if (e == hipSuccess) e = run_layer(z1, B, n_frames, 2 * c->h1, c->cinp2, c->h2, c->w2, c->b2, p, cf, 1, st);
   if (e == hipSuccess) {
     const int C = 2 * c->h2;
-    const long long n = (long long)B * T * C;
-    if (C % 4 == 0) {
-      const long long n4 = n / 4;
-      const unsigned blocks = (unsigned)std::min<long long>((n4 + 255) / 256, 65536);
-      hipLaunchKernelGGL(cond_upsample4, dim3(blocks), dim3(256), 0, st, reinterpret_cast<const float4*>(cf),
-                         reinterpret_cast<float4*>(cond), n_frames, (long long)T, C / 4, n4, c->fr, c->ar);
-    } else {
-      const unsigned blocks = (unsigned)std::min<long long>((n + 255) / 256, 65536);
-      hipLaunchKernelGGL(cond_upsample1, dim3(blocks), dim3(256), 0, st, cf, cond, n_frames, (long long)T, C, n,
-                         c->fr, c->ar);
-    }
+    const unsigned blocks = (unsigned)((long long)B * n_frames);
+    if (C % 4 == 0 && reinterpret_cast<uintptr_t>(cond) % 16 == 0)
+      hipLaunchKernelGGL(cond_repeat4, dim3(blocks), dim3(256), 0, st, reinterpret_cast<const f32x4*>(cf),
+                         reinterpret_cast<f32x4*>(cond), n_frames, (long long)T, C / 4, c->fr, c->ar);
+    else
+      hipLaunchKernelGGL(cond_repeat1, dim3(blocks), dim3(256), 0, st, cf, cond, n_frames, (long long)T, C, c->fr,
+                         c->ar);
     e = hipGetLastError();
   }
   if (e != hipSuccess) return wn_set_last_error(WN_EHIP, hipGetErrorString(e));

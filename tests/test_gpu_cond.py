@@ -3,9 +3,11 @@
 The GPU output is compared element by element with the oracle (fp64, per-frame recurrences) on
 the same seeded features and weights: max-abs 1e-4.  That bound is fp32 arithmetic over
 contractions of up to 2 x 2 h1 terms, then a recurrence over the frames whose forget gate keeps
-the error from growing.  Cases span several 64 x 64 GEMM tiles with ragged edges, a channel
-count not a multiple of 4, the paper's sizes (227 features, 20 x 64 channels per direction at
-256 Hz) and an end-to-end run: features -> conditioning -> generation.
+the error from growing.  Cases span several tiles of both contraction kernels (64 x 64 for any
+input width, 128 x 128 for widths that are multiples of 32) with ragged edges, a channel count
+not a multiple of 4, an output that ends inside a frame's run of audio steps, the paper's sizes
+(227 features, 20 x 64 channels per direction at 256 Hz) and an end-to-end run: features ->
+conditioning -> generation.
 """
 import numpy as np
 import pytest
@@ -25,23 +27,28 @@ def _wn():
 
 
 CASES = [
-    # name, F, h1, n_layers, r, B, n_frames, frame_rate, audio_rate
-    ("ragged_tiles", 227, 40, 3, 16, 2, 70, 256, 16000),
-    ("odd_channels", 19, 7, 3, 3, 3, 33, 3, 8),
-    ("one_frame", 5, 4, 1, 4, 1, 1, 1, 16),
-    ("frame_rate_output", 227, 256, 4, 64, 2, 90, 1, 1),
+    # name, F, h1, n_layers, r, B, n_frames, frame_rate, audio_rate, T (None: every frame's steps)
+    ("ragged_tiles", 227, 40, 3, 16, 2, 70, 256, 16000, None),
+    ("odd_channels", 19, 7, 3, 3, 3, 33, 3, 8, None),
+    ("one_frame", 5, 4, 1, 4, 1, 1, 1, 16, None),
+    ("frame_rate_output", 227, 256, 4, 64, 2, 90, 1, 1, None),
+    # input widths that are multiples of 32 (the float4 contraction) with ragged 128-row and
+    # 128-frame tiles, and T ending inside a frame's run of audio steps
+    ("wide_ragged", 227, 48, 3, 12, 3, 77, 256, 16000, 4801),
+    ("wide_both_layers", 64, 16, 2, 8, 2, 50, 1, 1, None),
+    ("short_T", 19, 7, 3, 3, 2, 33, 3, 8, 50),
 ]
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_conditioning_matches_oracle(case):
-    name, F, h1, L, r, B, Tf, fr, ar = case
+    name, F, h1, L, r, B, Tf, fr, ar, T = case
     print("cond case %s" % name, flush=True)
     wn = _wn()
     w = synth.make_cond_weights(F, h1, L * r, seed=len(name), bias_scale=0.2)
     x = synth.make_features(B, Tf, seed=3)[:, :, :F] if F <= synth.N_FEATURES else None
     x = np.ascontiguousarray(x + np.random.default_rng(1).normal(0, 0.1, x.shape).astype(np.float32))
-    T = (Tf * ar) // fr
+    T = (Tf * ar) // fr if T is None else T
     net = wn.Conditioner(w, L, r, fr, ar)
     cond = net(torch.tensor(x, device="cuda"), T)
     torch.cuda.synchronize()
