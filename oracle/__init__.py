@@ -48,14 +48,15 @@ def build(force: bool = True) -> str:
 class _Model(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int), ("r", ctypes.c_int), ("s", ctypes.c_int), ("a", ctypes.c_int),
                 ("dilations", ctypes.POINTER(ctypes.c_int)), ("initial_sample", ctypes.c_int),
-                ("bf16_weights", ctypes.c_int)] + [
+                ("bf16_weights", ctypes.c_int), ("embed_taps", ctypes.c_int)] + [
         (n, ctypes.POINTER(ctypes.c_float)) for n in
         ("embed", "b_embed", "w_prev", "w_cur", "b_gate", "w_res", "b_res", "w_skip", "b_skip",
          "w_relu", "b_relu", "w_out", "b_out")]
 
 
 class _State(ctypes.Structure):
-    _fields_ = [("t", ctypes.c_longlong), ("last_sample", ctypes.c_int), ("hist", ctypes.POINTER(ctypes.c_double))]
+    _fields_ = [("t", ctypes.c_longlong), ("last_sample", ctypes.c_int), ("prev_sample", ctypes.c_int),
+                ("hist", ctypes.POINTER(ctypes.c_double))]
 
 
 def lib():
@@ -104,7 +105,10 @@ def _ptr(a: Optional[np.ndarray]):
 
 
 class Model:
-    """A WaveNet parameter set as the oracle sees it (fp32 arrays, row-major [out][in])."""
+    """A WaveNet parameter set as the oracle sees it (fp32 arrays, row-major [out][in]).
+
+    ``embed`` is [a, r] (one tap: x0 = E[y_{t-1}] + B_embed) or [2, a, r] (two taps: tap 0
+    embeds y_{t-2}, tap 1 y_{t-1})."""
 
     def __init__(self, weights: Dict[str, np.ndarray], dilations: Sequence[int], initial_sample: int = 128,
                  bf16_weights: bool = False):
@@ -117,11 +121,15 @@ class Model:
         self.dilations = np.ascontiguousarray(dilations, dtype=np.int32)
         self.initial_sample = int(initial_sample)
         self.bf16 = bool(bf16_weights)
+        e = self.w["embed"]
+        assert e.shape[-2:] == (a, r) and (e.ndim == 2 or (e.ndim == 3 and e.shape[0] == 2)), e.shape
+        self.embed_taps = 1 if e.ndim == 2 else 2
         m = _Model()
         m.n_layers, m.r, m.s, m.a = L, r, s, a
         m.dilations = self.dilations.ctypes.data_as(ctypes.POINTER(ctypes.c_int))
         m.initial_sample = self.initial_sample
         m.bf16_weights = int(self.bf16)
+        m.embed_taps = self.embed_taps
         for name in ("embed", "b_embed", "w_prev", "w_cur", "b_gate", "w_res", "b_res", "w_skip", "b_skip",
                      "w_relu", "b_relu", "w_out", "b_out"):
             setattr(m, name, self.w[name].ctypes.data_as(ctypes.POINTER(ctypes.c_float)))
@@ -129,7 +137,7 @@ class Model:
 
     @property
     def receptive_field(self) -> int:
-        return receptive_field(self.dilations)
+        return receptive_field(self.dilations, self.embed_taps)
 
 
 class State:
@@ -150,6 +158,10 @@ class State:
     @property
     def last_sample(self) -> int:
         return int(self._s.last_sample)
+
+    @property
+    def prev_sample(self) -> int:
+        return int(self._s.prev_sample)
 
 
 # Ways of using the output distribution (Appendix "Sampling from Output Distribution"):
@@ -256,9 +268,9 @@ def round_bf16(x: np.ndarray) -> np.ndarray:
     return out
 
 
-def receptive_field(dilations: Sequence[int]) -> int:
-    """R = 1 + sum of dilations: samples y_{t-1-k}, k = 0..sum(d), reach step t's distribution."""
-    return 1 + int(sum(int(d) for d in dilations))
+def receptive_field(dilations: Sequence[int], embed_taps: int = 1) -> int:
+    """R = taps + sum of dilations: samples y_{t-1-k}, k = 0..taps-1+sum(d), reach step t's distribution."""
+    return int(embed_taps) + int(sum(int(d) for d in dilations))
 
 
 def param_count(n_layers: int, r: int, s: int, a: int = 256) -> int:

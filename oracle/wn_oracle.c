@@ -15,7 +15,11 @@
  * Readings of the paper taken here:
  *  - residual: x^(j) = x^(j-1) + W_res h^(j) + B_res (appendix equation; the CPU
  *    section's x^(j) = W_res h^(j) + B_res is read as shorthand);
- *  - input embedding: one table, x^(0)_t = E[y_{t-1}] + B_embed;
+ *  - input embedding, one tap: x^(0)_t = E[y_{t-1}] + B_embed; two taps (the
+ *    sample embedding of Section 5.1, the appendix's initial 2x1 convolution over
+ *    the one-hot input): x^(0)_t = E_prev[y_{t-2}] + E_cur[y_{t-1}] + B_embed,
+ *    where y_{t-2} at t = 0 lies before the input and contributes nothing (zero
+ *    left padding, as for every layer's history);
  *  - every layer's history is zero before the first step (zero left padding);
  *    y_{-1} = initial_sample;
  *  - gate split: rows 0..r-1 of W_prev, W_cur, B and L feed tanh, rows r..2r-1
@@ -47,7 +51,8 @@ typedef struct {
     const int *dilations;     /* [n_layers], each >= 1 */
     int initial_sample;       /* y_{-1} */
     int bf16_weights;         /* 0: use the fp32 weights; 1: round matrices to bf16 first */
-    const float *embed;       /* [a][r] */
+    int embed_taps;           /* 1 or 2 */
+    const float *embed;       /* [taps][a][r]: the last tap embeds y_{t-1}, tap 0 of two y_{t-2} */
     const float *b_embed;     /* [r] */
     const float *w_prev;      /* [l][2r][r] */
     const float *w_cur;       /* [l][2r][r] */
@@ -66,6 +71,7 @@ typedef struct {
 typedef struct {
     long long t;              /* steps already taken */
     int last_sample;          /* y_{t-1} */
+    int prev_sample;          /* y_{t-2}, or -1 at t = 0 (no input before the first) */
     double *hist;             /* sum(d) * r doubles, layer j at offset r * sum_{i<j} d_i */
 } oracle_state;
 
@@ -104,13 +110,15 @@ long long oracle_history_len(const oracle_model *m) {
 void oracle_reset(const oracle_model *m, oracle_state *st) {
     st->t = 0;
     st->last_sample = m->initial_sample;
+    st->prev_sample = -1;
     memset(st->hist, 0, sizeof(double) * (size_t)oracle_history_len(m));
 }
 
 /*
- * One timestep t of one stream: consumes y_{t-1} = st->last_sample and the
- * conditioning of step t ([l][2r]), writes the a = 256 logits of step t and
- * advances the histories.  Returns 0 or -1 on allocation failure.
+ * One timestep t of one stream: consumes y_{t-1} = st->last_sample (and, with two
+ * embedding taps, y_{t-2} = st->prev_sample) and the conditioning of step t
+ * ([l][2r]), writes the a = 256 logits of step t and advances the histories.
+ * Returns 0 or -1 on allocation failure.
  */
 static int oracle_step(const oracle_model *m, oracle_state *st, const float *cond_t, double *logits) {
     const int L = m->n_layers, r = m->r, s = m->s, a = m->a;
@@ -121,9 +129,12 @@ static int oracle_step(const oracle_model *m, oracle_state *st, const float *con
         free(x); free(xn); free(act); free(h); free(q); free(za);
         return -1;
     }
-    /* Sample embedding: x^(0) = E[y_{t-1}] + B_embed. */
-    for (int c = 0; c < r; ++c)
-        x[c] = wv(m, m->embed, (long)st->last_sample * r + c) + (double)m->b_embed[c];
+    /* Sample embedding: x^(0) = E_cur[y_{t-1}] (+ E_prev[y_{t-2}]) + B_embed. */
+    const long cur = (long)(m->embed_taps - 1) * a;  /* first row of the current tap's table */
+    for (int c = 0; c < r; ++c) {
+        x[c] = wv(m, m->embed, (cur + st->last_sample) * r + c) + (double)m->b_embed[c];
+        if (m->embed_taps == 2 && st->prev_sample >= 0) x[c] += wv(m, m->embed, (long)st->prev_sample * r + c);
+    }
     /* q^(0) = B_skip. */
     for (int k = 0; k < s; ++k) q[k] = (double)m->b_skip[k];
 
@@ -306,7 +317,7 @@ int oracle_run_sampled(const oracle_model *m, oracle_state *st, int mode, long l
                        const float *cond, const float *u, const int *y_in,
                        int *samples_out, double *logits_out, double *margin_out,
                        int sample_mode, double temperature, int top_k) {
-    if (!m || T < 0 || (mode != 0 && mode != 1)) return -1;
+    if (!m || T < 0 || (mode != 0 && mode != 1) || m->embed_taps < 1 || m->embed_taps > 2) return -1;
     if (mode == 0 && !u) return -1;
     if (mode == 1 && !y_in) return -1;
     oracle_state local;
@@ -330,6 +341,7 @@ int oracle_run_sampled(const oracle_model *m, oracle_state *st, int mode, long l
         if (y < 0) { free(lg); free(own); return -1; }
         if (margin_out) margin_out[t] = u ? mg : 0.0;
         if (samples_out) samples_out[t] = y;
+        st->prev_sample = st->last_sample;
         st->last_sample = (mode == 0) ? y : y_in[t];
     }
     free(lg);

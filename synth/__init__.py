@@ -78,11 +78,12 @@ WEIGHT_NAMES = ("embed", "b_embed", "w_prev", "w_cur", "b_gate", "w_res", "b_res
                 "w_skip", "b_skip", "w_relu", "b_relu", "w_out", "b_out")
 
 
-def weight_shapes(n_layers: int, r: int, s: int, a: int) -> Dict[str, tuple]:
-    """Row-major [out][in] shapes of every parameter array."""
+def weight_shapes(n_layers: int, r: int, s: int, a: int, embed_taps: int = 1) -> Dict[str, tuple]:
+    """Row-major [out][in] shapes of every parameter array (a two-tap embedding is [2, a, r]:
+    tap 0 embeds y_{t-2}, tap 1 y_{t-1})."""
     L = n_layers
     return {
-        "embed": (a, r), "b_embed": (r,),
+        "embed": (a, r) if embed_taps == 1 else (embed_taps, a, r), "b_embed": (r,),
         "w_prev": (L, 2 * r, r), "w_cur": (L, 2 * r, r), "b_gate": (L, 2 * r),
         "w_res": (L, r, r), "b_res": (L, r),
         "w_skip": (L, s, r), "b_skip": (s,),
@@ -91,18 +92,18 @@ def weight_shapes(n_layers: int, r: int, s: int, a: int) -> Dict[str, tuple]:
     }
 
 
-def fan_in(name: str, n_layers: int, r: int, s: int, a: int) -> Optional[int]:
-    return {"embed": 1, "w_prev": 2 * r, "w_cur": 2 * r, "w_res": r,
+def fan_in(name: str, n_layers: int, r: int, s: int, a: int, embed_taps: int = 1) -> Optional[int]:
+    return {"embed": embed_taps, "w_prev": 2 * r, "w_cur": 2 * r, "w_res": r,
             "w_skip": n_layers * r, "w_relu": s, "w_out": a}.get(name)
 
 
 def make_weights(n_layers: int, r: int, s: int, a: int = A_CLASSES, seed: int = 0,
-                 bias_scale: float = 0.0, weight_scale: float = 1.0) -> Dict[str, np.ndarray]:
+                 bias_scale: float = 0.0, weight_scale: float = 1.0, embed_taps: int = 1) -> Dict[str, np.ndarray]:
     """fp32 host weights; matrices N(0, weight_scale^2/fan_in), biases N(0, bias_scale^2) (zero by default)."""
     rng = np.random.Generator(np.random.PCG64(seed))
     out = {}
-    for name, shape in weight_shapes(n_layers, r, s, a).items():
-        fi = fan_in(name, n_layers, r, s, a)
+    for name, shape in weight_shapes(n_layers, r, s, a, embed_taps).items():
+        fi = fan_in(name, n_layers, r, s, a, embed_taps)
         if fi is None:
             if bias_scale > 0:
                 out[name] = (rng.standard_normal(shape) * bias_scale).astype(np.float32)

@@ -18,9 +18,16 @@ def logits(w, dilations, cond, y_in, initial_sample=128):
     cond = torch.tensor(np.asarray(cond), dtype=torch.float64)
     T = cond.shape[0]
     y_prev = torch.tensor(np.concatenate([[initial_sample], np.asarray(y_in)[:-1]]).astype(np.int64))
-    onehot = F.one_hot(y_prev, a).to(torch.float64)               # [T, a]
-    # the input convolution over a one-hot signal: one row of the embedding per step
-    X = (onehot @ t64["embed"] + t64["b_embed"]).T                 # [r, T]
+    onehot = F.one_hot(y_prev, a).to(torch.float64)               # [T, a]: step t's input y_{t-1}
+    E = t64["embed"]
+    if E.dim() == 2:
+        # the input convolution over a one-hot signal: one row of the embedding per step
+        X = (onehot @ E + t64["b_embed"]).T                        # [r, T]
+    else:
+        # width-2 causal convolution over the one-hot inputs, zero before the first: tap 0 sees
+        # step t's previous input y_{t-2}, tap 1 its input y_{t-1}
+        kernel = torch.stack([E[0].T, E[1].T], dim=-1)             # [r, a, 2]
+        X = F.conv1d(F.pad(onehot.T[None], (1, 0)), kernel, bias=t64["b_embed"])[0]
     hidden = []
     for j, d in enumerate(dilations):
         kernel = torch.stack([t64["w_prev"][j], t64["w_cur"][j]], dim=-1)   # [2r, r, 2]: tap 0 sees t-d

@@ -19,8 +19,8 @@ from tests import brute_force
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
-def _model(L, r, s, dil, a=256, seed=0, bias=0.5, wscale=1.0, init=128, bf16=False):
-    w = synth.make_weights(L, r, s, a, seed=seed, bias_scale=bias, weight_scale=wscale)
+def _model(L, r, s, dil, a=256, seed=0, bias=0.5, wscale=1.0, init=128, bf16=False, taps=1):
+    w = synth.make_weights(L, r, s, a, seed=seed, bias_scale=bias, weight_scale=wscale, embed_taps=taps)
     return w, oracle.Model(w, dil, initial_sample=init, bf16_weights=bf16)
 
 
@@ -37,10 +37,12 @@ CASES = [
 ]
 
 
+@pytest.mark.parametrize("taps", [1, 2])
 @pytest.mark.parametrize("L,r,s,a,dil,T", CASES)
-def test_incremental_equals_whole_sequence_conv(L, r, s, a, dil, T):
-    """History-buffer generation == the full causal dilated convolution (appendix A.1 equations)."""
-    w, m = _model(L, r, s, dil, a=a, seed=L * 7 + r, bias=0.5, init=a // 2)
+def test_incremental_equals_whole_sequence_conv(L, r, s, a, dil, T, taps):
+    """History-buffer generation == the full causal dilated convolution (appendix A.1 equations),
+    with the one-table embedding and with the width-2 input convolution (Section 5.1)."""
+    w, m = _model(L, r, s, dil, a=a, seed=L * 7 + r, bias=0.5, init=a // 2, taps=taps)
     cond = _cond(L, r, T, seed=11)
     y = synth.make_samples(1, T, a=a, seed=5)[0]
     _, lg, _ = oracle.run(m, cond, y_in=y)
@@ -150,6 +152,64 @@ def test_receptive_field_and_causality(dil):
         assert _changed_steps(ref, lg) == {k + o for o in _subset_sums(dil[j + 1:])}
 
 
+@pytest.mark.parametrize("dil", [(1, 2, 4, 8), (3, 1, 2)])
+def test_two_tap_receptive_field_and_causality(dil):
+    """With two embedding taps y_k reaches steps k + 1 + e + o, e in {0, 1}, o in the subset sums
+    of the dilations: R = 2 + sum d (17 for 1,2,4,8)."""
+    L, r, s = len(dil), 6, 8
+    T = 3 * (2 + sum(dil)) + 10
+    w, m = _model(L, r, s, dil, seed=24, bias=0.4, taps=2)
+    cond = _cond(L, r, T, seed=25)
+    y = synth.make_samples(1, T, seed=26)[0]
+    _, ref, _ = oracle.run(m, cond, y_in=y)
+    k = T // 3
+    y2 = y.copy()
+    y2[k] = (y2[k] + 101) % 256
+    _, lg, _ = oracle.run(m, cond, y_in=y2)
+    expect = {k + 1 + e + o for e in (0, 1) for o in _subset_sums(dil)} & set(range(T))
+    assert _changed_steps(ref, lg) == expect
+    assert max(expect) - k == m.receptive_field == 2 + sum(dil)
+    if dil == (1, 2, 4, 8):
+        assert expect == set(range(k + 1, k + 18))
+
+
+def test_two_tap_embedding_special_cases():
+    """E_prev = 0 reproduces the one-table model with E = E_cur exactly; E_cur = 0 makes step t's
+    input depend on y_{t-2} alone, and step 0's on nothing but B_embed (zero left padding)."""
+    L, r, s, dil, T = 3, 8, 16, (1, 2, 4), 60
+    w = synth.make_weights(L, r, s, seed=41, bias_scale=0.4, embed_taps=2)
+    cond = _cond(L, r, T, seed=42)
+    y = synth.make_samples(1, T, seed=43)[0]
+    w0 = dict(w)
+    w0["embed"] = w["embed"].copy()
+    w0["embed"][0] = 0.0
+    w1 = dict(w)
+    w1["embed"] = w["embed"][1].copy()
+    _, lg0, _ = oracle.run(oracle.Model(w0, dil), cond, y_in=y)
+    _, lg1, _ = oracle.run(oracle.Model(w1, dil), cond, y_in=y)
+    np.testing.assert_array_equal(lg0, lg1)
+    wp = dict(w)
+    wp["embed"] = w["embed"].copy()
+    wp["embed"][1] = 0.0
+    mp = oracle.Model(wp, dil)
+    _, ref, _ = oracle.run(mp, cond, y_in=y)
+    # changing only the initial sample (step 0's y_{t-1}, step 1's y_{t-2}) changes nothing at step 0
+    _, lg, _ = oracle.run(oracle.Model(wp, dil, initial_sample=3), cond, y_in=y)
+    assert np.array_equal(lg[0], ref[0]) and not np.array_equal(lg[1], ref[1])
+    # with E_prev the only table and no recurrence (W_prev = 0, W_cur = 0 past layer 1), y_k
+    # reaches step k + 2 only
+    wz = dict(wp)
+    wz["w_prev"] = np.zeros_like(w["w_prev"])
+    wz["w_cur"] = w["w_cur"].copy()
+    wz["w_cur"][1:] = 0.0
+    y2 = y.copy()
+    y2[20] = (y2[20] + 77) % 256
+    mz = oracle.Model(wz, dil)
+    _, a_, _ = oracle.run(mz, cond, y_in=y)
+    _, b_, _ = oracle.run(mz, cond, y_in=y2)
+    assert _changed_steps(a_, b_) == {22}
+
+
 def test_receptive_field_paper_figures():
     g = json.load(open(os.path.join(GOLDEN, "paper_figures.json")))
     r40 = oracle.receptive_field(synth.dilation_cycle(40))
@@ -173,6 +233,23 @@ def test_chunked_equals_one_shot():
         parts.append((ys, lg))
     assert st.t == T and st.last_sample == y1[-1]
     np.testing.assert_array_equal(np.concatenate([p[0] for p in parts]), y1)
+
+
+def test_two_tap_chunked_equals_one_shot():
+    """The state carries y_{t-2} across calls: chunk boundaries change nothing with two taps."""
+    L, r, s, dil, T = 4, 16, 32, (1, 2, 4, 8), 120
+    w, m = _model(L, r, s, dil, seed=34, bias=0.2, taps=2)
+    cond = _cond(L, r, T, seed=35)
+    u = synth.make_uniforms(1, T, seed=36)[0]
+    y1, lg1, _ = oracle.run(m, cond, u=u)
+    st = oracle.State(m)
+    assert st.prev_sample == -1
+    parts = []
+    for a_, b_ in [(0, 1), (1, 2), (2, 50), (50, 120)]:
+        parts.append(oracle.run(m, cond[a_:b_], u=u[a_:b_], state=st)[:2])
+    assert st.t == T and st.last_sample == y1[-1] and st.prev_sample == y1[-2]
+    np.testing.assert_array_equal(np.concatenate([p[0] for p in parts]), y1)
+    np.testing.assert_array_equal(np.concatenate([p[1] for p in parts]), lg1)
     np.testing.assert_array_equal(np.concatenate([p[1] for p in parts]), lg1)
 
 
