@@ -12,14 +12,15 @@
  * benchmark (Section 5), which excludes the conditioning network.
  *
  * Per stream b and step t (t = 0 .. T-1 within a call, tg = global step):
- *   x0      = E[y_{tg-1}] + B_embed
+ *   x0      = E[y_{tg-1}] + B_embed        (two taps: + E_prev[y_{tg-2}], Section 5.1)
  *   a_j     = W_prev_j x_{j-1}[tg - d_j] + W_cur_j x_{j-1}[tg] + B_j + L[b,t,j,:]
  *   h_j     = tanh(a_j[0:r]) * sigmoid(a_j[r:2r])
  *   x_j     = x_{j-1} + W_res_j h_j + B_res_j
  *   q       = B_skip + sum_j W_skip_j h_j
  *   logits  = W_out relu(W_relu relu(q) + B_relu) + B_out
  *   y_tg    = #{k <= a-2 : C_k <= u[b,t]},  C_k = p_0 + .. + p_k,  p = softmax(logits)
- * Layer histories are zero before the first step and y_{-1} = initial_sample.
+ * Layer histories are zero before the first step, y_{-1} = initial_sample, and
+ * y_{-2} contributes nothing.
  *
  * Conventions:
  *  - Every matrix is row-major [out][in], fp32 on the host.  wn_create copies
@@ -91,14 +92,18 @@ typedef struct {
   int32_t s;                 /* skip channels: 32, 64, 128 or 256 */
   int32_t a;                 /* output classes: must be 256 (8-bit mu-law) */
   const int32_t* dilations;  /* host [n_layers], each 1 .. 65536; copied by wn_create */
-  int32_t embed_taps;        /* 1: x0 = E[y_{t-1}] + B_embed (only value implemented) */
+  int32_t embed_taps;        /* 1: x0 = E[y_{t-1}] + B_embed;
+                                2: x0 = E_prev[y_{t-2}] + E_cur[y_{t-1}] + B_embed, the width-2
+                                input convolution of Section 5.1 (y_{t-2} before the first step
+                                contributes nothing) */
   int32_t initial_sample;    /* y_{-1}, 0 .. a-1; 128 is the mu-law code of silence */
   int32_t weight_dtype;      /* wn_dtype_t: storage of the matrices and the embedding;
                                 biases, activations and accumulation are always fp32 */
 } wn_config;
 
 typedef struct {             /* host fp32, row-major, shapes below */
-  const float* embed;        /* [a][r]       embedding of the previous sample      */
+  const float* embed;        /* [taps][a][r] embedding tables: the last embeds y_{t-1},
+                                            with two taps the first embeds y_{t-2}      */
   const float* b_embed;      /* [r]                                                 */
   const float* w_prev;       /* [l][2r][r]   conv tap on x_{t-d} (rows 0..r-1 tanh)  */
   const float* w_cur;        /* [l][2r][r]   conv tap on x_t                         */
@@ -120,7 +125,7 @@ typedef struct wn_handle wn_handle;
  * Model: Appendix A.1 (layer equations) and Section 5 (the W_prev/W_cur split
  * of each dilated convolution into two matrix-vector products per step).
  * Errors: WN_EINVAL for null pointers or values out of the ranges above;
- * WN_EUNSUPPORTED for a != 256, embed_taps != 1, or an (r, s) pair outside
+ * WN_EUNSUPPORTED for a != 256, or an (r, s) pair outside
  * {(16,32), (32,128), (64,128), (64,256), (128,256)}; WN_ENOMEM; WN_EHIP.
  * *out is set only on success.
  */
@@ -129,7 +134,7 @@ int wn_create(const wn_config* config, const wn_weights* weights, wn_handle** ou
 /*
  * Bytes of device workspace one call with B streams needs: the generator state
  * of every stream (each layer's dilation history of r fp32 values per step of
- * its dilation, the step counter and the last sample) plus a status word.
+ * its dilation, the step counter and the last two samples) plus a status word.
  * The layout is private.  Returns 0 for a null handle or B < 1.
  */
 size_t wn_workspace_bytes(const wn_handle* h, int32_t B);

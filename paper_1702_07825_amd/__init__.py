@@ -139,14 +139,20 @@ def _dev_ptr(t, dtype, shape, name):
 class WaveNet:
     """A WaveNet model resident on one GPU (wraps wn_create / wn_destroy).
 
-    ``weights``: dict of fp32 host arrays with the row-major shapes of include/wn.h.
+    ``weights``: dict of fp32 host arrays with the row-major shapes of include/wn.h; ``embed`` is
+    [a, r] (one tap) or [2, a, r] (two taps: tap 0 embeds y_{t-2}, tap 1 y_{t-1}).
     """
 
     def __init__(self, weights: Dict[str, np.ndarray], dilations: Sequence[int], initial_sample: int = 128,
-                 weight_dtype: str = "f32", embed_taps: int = 1):
+                 weight_dtype: str = "f32", embed_taps: Optional[int] = None):
         self._lib = load_library()
         self._h = None
         w = {k: np.ascontiguousarray(weights[k], dtype=np.float32) for k in WEIGHT_FIELDS}
+        taps = 1 if w["embed"].ndim == 2 else int(w["embed"].shape[0])
+        if embed_taps is not None and int(embed_taps) != taps:
+            raise ValueError("embed_taps=%d but the embedding has %d tables" % (embed_taps, taps))
+        self.embed_taps = taps
+        embed_taps = taps
         L, two_r, r = w["w_prev"].shape
         self.n_layers, self.r, self.s, self.a = int(L), int(r), int(w["w_skip"].shape[1]), int(w["w_out"].shape[0])
         self.dilations = np.ascontiguousarray(dilations, dtype=np.int32)

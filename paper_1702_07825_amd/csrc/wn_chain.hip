@@ -50,6 +50,7 @@
 #include "wn.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace {
 
@@ -210,7 +211,7 @@ __device__ __forceinline__ float dot_lds(const float (&w)[K], const float* x) {
 // ------------------------------------------------------------------------------------------
 // chain CU
 // ------------------------------------------------------------------------------------------
-template <int R, int S, int NLC, bool TF, bool MS>
+template <int R, int S, int NLC, bool TF, bool MS, bool E2>
 __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, const int ns, float* dyn, Sync sy,
                            const int64_t tg0) {
   using M = ChainMap<R>;
@@ -247,8 +248,9 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
   float* lgp = var;                                 // NHEAD*A
   float* ubuf = lgp + NHEAD * A;                    // G*ub   uniforms / samples in, per stream
   int* ybuf = reinterpret_cast<int*>(ubuf + G * ub);  // G*ub drawn samples
-  int* syv = ybuf + G * ub;                         // G      last sample of each stream
-  float* emb = reinterpret_cast<float*>(syv + ((G + 3) & ~3));  // A*R
+  int* syv = ybuf + G * ub;                         // G      y_{t-1} of each stream
+  int* syv2 = syv + ((G + 3) & ~3);                 // G      y_{t-2} (-1 before the first input)
+  float* emb = reinterpret_cast<float*>(syv2 + ((G + 3) & ~3));  // A*R
   // last chain CU: W_skip of layer l-1, S rows of stride WSK (after the table if it is also CU 0)
   float* wsk = first ? emb + A * R : var;
   // a middle r = 128 CU with two layers: their W_res, R rows of stride WRS each
@@ -315,6 +317,8 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
     lhoff[tid] = g.d.hoff[j0 + tid];
   }
   float bemb = 0.f;
+  // two-tap input convolution (E2): the table of y_{t-2}
+  const float* const Eprev = E2 ? static_cast<const float*>(g.w.embed_prev) : nullptr;
   float4 bout4 = make_float4(0.f, 0.f, 0.f, 0.f);  // B_out of the 4 logits lane l of wave 0 draws from
   if (tail) {
     const float* Wk = static_cast<const float*>(g.w.w_skip) + (size_t)(L - 1) * S * R;
@@ -339,8 +343,11 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
     for (int i = tid; i < A * R; i += NT) emb[i] = E[i];
     if (tid < R) bemb = g.w.b_embed[tid];
     for (int i = tid; i < ns; i += NT) {
-      int y = g.io.reset ? g.io.init_sample : (int)g.state[2 * (size_t)(b0 + i) + 1];
+      const int64_t* st = g.state + WN_STATE_WORDS * (size_t)(b0 + i);
+      int y = g.io.reset ? g.io.init_sample : (int)st[1];
       syv[i] = y < 0 ? 0 : (y > A - 1 ? A - 1 : y);
+      int y2 = g.io.reset ? -1 : (int)st[2];
+      syv2[i] = y2 < 0 ? -1 : (y2 > A - 1 ? A - 1 : y2);
     }
     stage_inputs();
   }
@@ -370,6 +377,7 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
         y = wave_draw(lv, ubuf[at], g.io.smode, g.io.inv_t, g.io.top_k, lane);
       }
       if (lane == 0) {
+        if constexpr (E2) syv2[i] = syv[i];
         syv[i] = y;
         ybuf[at] = y;
       }
@@ -406,6 +414,13 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
       //      either x from the previous chain CU or (chain CU 0) the previous step's partial logits ----
       const Items pre_items{mbs + ((size_t)j0 * 2 + par) * 2 * R, 2 * R, 2 * 2 * R, nl * 2 * R, pre, tag};
       if (first) {
+        // two-tap embedding: the row of y_{t-2} (known since the previous step) is loaded before
+        // the wait for the previous step's logits, which hides its latency
+        float ep = 0.f;
+        if constexpr (E2) {
+          const int y2 = t > tg0 ? syv[i] : syv2[i];
+          if (tid < R && y2 >= 0) ep = Eprev[(size_t)y2 * R + tid];
+        }
         if (t > tg0) {
           poll2(g, logit_items(t - 1, b), pre_items, dyn, sy);
           lds_barrier();
@@ -417,7 +432,10 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
         }
         lds_barrier();
         if (sy.failed()) return;
-        if (tid < R) xs[tid] = emb[syv[i] * R + tid] + bemb;
+        if (tid < R) {
+          if constexpr (E2) xs[tid] = emb[syv[i] * R + tid] + bemb + ep;
+          else xs[tid] = emb[syv[i] * R + tid] + bemb;
+        }
       } else {
         poll2(g, pre_items, Items{mbs + g.off_x + ((size_t)c * 2 + par) * R, R, R, R, xs, tag}, dyn, sy);
       }
@@ -624,8 +642,10 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
     }
     if (!sy.failed()) {
       for (int i = tid; i < ns; i += NT) {
-        g.state[2 * (size_t)(b0 + i)] = tg0 + T;
-        g.state[2 * (size_t)(b0 + i) + 1] = syv[i];
+        int64_t* st = g.state + WN_STATE_WORDS * (size_t)(b0 + i);
+        st[0] = tg0 + T;
+        st[1] = syv[i];
+        st[2] = syv2[i];
       }
     }
   }
@@ -796,7 +816,7 @@ __device__ void head_role(const WnChainArgs& g, const int hh, const int b0, cons
   }
 }
 
-template <int R, int S, int NLC, bool TF, bool MS>
+template <int R, int S, int NLC, bool TF, bool MS, bool E2>
 __global__ __launch_bounds__(NT) void wn_chain_kernel(const WnChainArgs g) {
   extern __shared__ __align__(16) float dyn[];
   __shared__ int s_abort;
@@ -810,10 +830,10 @@ __global__ __launch_bounds__(NT) void wn_chain_kernel(const WnChainArgs g) {
   if (threadIdx.x == 0) s_abort = 0;
   // where this call starts: from zero, or where the previous call on this workspace stopped (the
   // replica's chain CU 0 rewrites its streams' state only after every role of it has started)
-  const int64_t tg0 = g.io.reset ? 0 : g.state[2 * (size_t)b0];
+  const int64_t tg0 = g.io.reset ? 0 : g.state[WN_STATE_WORDS * (size_t)b0];
   __syncthreads();
   Sync sy{&s_abort};
-  if (role < g.nch) chain_role<R, S, NLC, TF, MS>(g, role, b0, ns, dyn, sy, tg0);
+  if (role < g.nch) chain_role<R, S, NLC, TF, MS, E2>(g, role, b0, ns, dyn, sy, tg0);
   else if (role < g.nch + NHEAD) head_role<R, S, TF, MS>(g, role - g.nch, b0, ns, dyn, sy, tg0);
   else aux_role<R, S, TF, MS>(g, role - g.nch - NHEAD, b0, ns, dyn, sy, tg0);
 }
@@ -861,7 +881,7 @@ size_t chain_lds_floats(int R, int S, int nlc, int G, int ub, int nch, int tail)
   const int nlcp = (nlc + 3) & ~3;
   const size_t common = (size_t)2 * R + (size_t)nlc * 2 * R + (size_t)2 * nlc * R + 4 * nlcp;
   const size_t wsk = (size_t)S * lds_row_stride(R, S / 64);
-  size_t cu0 = (size_t)NHEAD * A + (size_t)2 * G * ub + ((G + 3) & ~3) + (size_t)A * R;
+  size_t cu0 = (size_t)NHEAD * A + (size_t)2 * G * ub + 2 * ((G + 3) & ~3) + (size_t)A * R;
   if (nch == 1 && tail) cu0 += wsk;
   size_t var = cu0;
   if (tail) var = std::max(var, wsk);
@@ -878,12 +898,17 @@ hipError_t launch_chain_rs(const WnChainArgs& g, bool teacher, hipStream_t strea
   const size_t dyn = sizeof(float) * std::max(chain_lds_floats(R, S, NLC, g.G, g.ub, g.nch, g.tail_on_chain),
                                               std::max(head_lds_floats(g.d.L, S), aux_lds_floats(R, g.G)));
   void* args[] = {const_cast<WnChainArgs*>(&g)};
-  // one stream (no replicas) gets a build with the stream loops folded away
-  const bool ms = g.io.B > 1;
-  const void* k = teacher ? (ms ? reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, true, true>)
-                                : reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, true, false>))
-                          : (ms ? reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, false, true>)
-                                : reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, false, false>));
+  // one stream (no replicas) gets a build with the stream loops folded away, a one-table
+  // embedding one without the second table's load
+  const bool ms = g.io.B > 1, e2 = g.w.embed_prev != nullptr;
+  auto pick = [&](auto tf, auto msc) -> const void* {
+    constexpr bool TF = decltype(tf)::value, MS = decltype(msc)::value;
+    return e2 ? reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, TF, MS, true>)
+              : reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, TF, MS, false>);
+  };
+  using t_ = std::true_type;
+  using f_ = std::false_type;
+  const void* k = teacher ? (ms ? pick(t_{}, t_{}) : pick(t_{}, f_{})) : (ms ? pick(f_{}, t_{}) : pick(f_{}, f_{}));
   hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
   if (e != hipSuccess) return e;
   return hipLaunchCooperativeKernel(k, dim3(WN_CHAIN_GRID), dim3(NT), args, (unsigned)dyn, stream);

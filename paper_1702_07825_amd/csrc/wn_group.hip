@@ -17,7 +17,8 @@
 // After the last layer: z_s = relu(q + B_skip), z_a = relu(W_relu z_s + B_relu), logits =
 // W_out z_a + B_out (all 8 waves; the head's tiles are loaded during the last layer), then the
 // softmax and draw (two streams per wave), which also lays out the next step's x0 = E[y] +
-// B_embed.
+// B_embed (+ E_prev[y_{t-1}] with the two-tap input convolution of Section 5.1: the loader reads
+// that row during the step, since the sample it embeds is known a step ahead).
 //
 // Weights are packed on the host into MFMA A-operand tiles (16 rows x 32 inputs of bf16, 1 KB,
 // one 16-byte load per lane) and streamed from L2 every step; each wave issues the loads of the
@@ -112,7 +113,7 @@ struct Pack {
 template <int S>
 constexpr size_t lds_bytes(int L) {
   return 4 * ((size_t)2 * G * PC + (size_t)G * PA + (size_t)L * 3 * R + R + S + 2 * A) +
-         2 * ((size_t)5 * G * SR + (size_t)G * Pack<S>::SS + (size_t)G * SA + (size_t)A * R);
+         2 * ((size_t)5 * G * SR + (size_t)G * Pack<S>::SS + (size_t)G * SA + (size_t)A * R + (size_t)G * R);
 }
 
 template <int S, bool TF>
@@ -141,8 +142,10 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
   u16* XP = HS + G * SR;                      // [2][G][SR] history rows x_{j-1}[t - d_j] (layer parity)
   u16* ZS = XP + 2 * G * SR;                  // [G][SS]    relu(q + B_skip), split
   u16* ZA = ZS + G * SS;                      // [G][SA]    z_a, split
-  u16* EMB = ZA + G * SA;                     // [A][R]     embedding (bf16)
-  __shared__ int s_y[G];
+  u16* EMB = ZA + G * SA;                     // [A][R]     embedding of y_{t-1} (bf16)
+  u16* EPB = EMB + A * R;                     // [G][R]     embedding row of y_{t-2} (two taps; else 0)
+  __shared__ int s_y[G];   // y_{t-1}
+  __shared__ int s_y2[G];  // y_{t-2}, -1 before the first input
   __shared__ float s_u[G];
   __shared__ int s_yin[G];
   __shared__ int s_slot[WN_GROUP_MAX_LAYERS];  // history slot (t mod d_j) of the next write of layer j
@@ -165,11 +168,15 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
   {
     // every stream of a call has taken the same number of steps
     const int64_t* st = g.ws.state;
-    if (!g.io.reset) tg0 = st[2 * (size_t)b0];
+    if (!g.io.reset) tg0 = st[WN_STATE_WORDS * (size_t)b0];
     if (tid < G) {
-      int y = g.io.init_sample;
-      if (!g.io.reset && b0 + tid < B) y = (int)st[2 * (size_t)(b0 + tid) + 1];
+      int y = g.io.init_sample, y2 = -1;
+      if (!g.io.reset && b0 + tid < B) {
+        y = (int)st[WN_STATE_WORDS * (size_t)(b0 + tid) + 1];
+        y2 = (int)st[WN_STATE_WORDS * (size_t)(b0 + tid) + 2];
+      }
       s_y[tid] = y < 0 ? 0 : (y > A - 1 ? A - 1 : y);
+      s_y2[tid] = y2 < 0 ? -1 : (y2 > A - 1 ? A - 1 : y2);
     }
   }
   if (tid < L) {
@@ -195,9 +202,14 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
     if (blockIdx.x == 0 && tid == 0) *g.ws.status = 0;
   }
   __syncthreads();  // also orders the history zeroing before the loader's reads
+  // x0 of the first step; EPB holds E_prev[y_{t-2}] of the step whose x0 is formed next (the
+  // loader refreshes it a step ahead)
+  const u16* Eprev = static_cast<const u16*>(g.w.embed_prev);  // null with one tap
   for (int i = tid; i < G * R; i += NT) {
     const int nn = i / R, c = i % R;
-    split1(bf16_val(EMB[s_y[nn] * R + c]) + BE[c], XS[nn * SR + c], XS[nn * SR + R + c]);
+    const u16 ep = (Eprev && s_y2[nn] >= 0) ? Eprev[(size_t)s_y2[nn] * R + c] : (u16)0;
+    EPB[i] = ep;
+    split1(bf16_val(EMB[s_y[nn] * R + c]) + BE[c] + bf16_val(ep), XS[nn * SR + c], XS[nn * SR + R + c]);
   }
 
   const int64_t nq = (int64_t)T * L;  // positions (step, layer) of this call
@@ -292,8 +304,12 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
         const float4 lv = *reinterpret_cast<const float4*>(LG + nn * PA + 4 * lane);
         y = wave_draw(lv, s_u[nn], g.io.smode, g.io.inv_t, g.io.top_k, lane);
       }
-      if (lane == 0) s_y[nn] = y;
-      split1(bf16_val(EMB[y * R + lane]) + BE[lane], XS[nn * SR + lane], XS[nn * SR + R + lane]);
+      if (lane == 0) {
+        s_y2[nn] = s_y[nn];
+        s_y[nn] = y;
+      }
+      split1(bf16_val(EMB[y * R + lane]) + BE[lane] + bf16_val(EPB[nn * R + lane]), XS[nn * SR + lane],
+             XS[nn * SR + R + lane]);
     }
     lds_barrier();
   };
@@ -325,10 +341,11 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
       constexpr int k = decltype(kc)::value;
       u32x4(&cur)[NB] = buf[k];
       const int slot = (int)(q & 1);
-      if (j == 0) {  // x0 = E[y_{t-1}] + B_embed
+      if (j == 0) {  // x0 = E[y_{t-1}] + B_embed (+ E_prev[y_{t-2}])
         const u16* e = EMB + s_y[n] * R + m0;
-        xr = make_float4(bf16_val(e[0]) + BE[m0], bf16_val(e[1]) + BE[m0 + 1], bf16_val(e[2]) + BE[m0 + 2],
-                         bf16_val(e[3]) + BE[m0 + 3]);
+        const u16* ep = EPB + n * R + m0;
+        xr = make_float4(bf16_val(e[0]) + BE[m0] + bf16_val(ep[0]), bf16_val(e[1]) + BE[m0 + 1] + bf16_val(ep[1]),
+                         bf16_val(e[2]) + BE[m0 + 2] + bf16_val(ep[2]), bf16_val(e[3]) + BE[m0 + 3] + bf16_val(ep[3]));
       }
       f32x4 at = {0.f, 0.f, 0.f, 0.f}, as = {0.f, 0.f, 0.f, 0.f};
       const u16* xp = XP + (slot * G + n) * SR;
@@ -479,6 +496,7 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
     u32x4 bufA[NB], bufB[NB];
     float pre_u = 0.f;
     int pre_y = 0;
+    u32x4 pre_e[2];  // two taps: quarter ldq of E_prev[y_{t-1}] of stream ldn, for the next step
     // rows of positions 0 and 1 (both in the first step: the kernel takes l >= 2)
     issue(bufB, 0, 0);
     store(0, bufB);
@@ -498,6 +516,13 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
       if (j == 1 && lane < G) {
         if constexpr (TF) s_yin[lane] = pre_y < 0 ? 0 : (pre_y > A - 1 ? A - 1 : pre_y);
         else s_u[lane] = pre_u;
+      }
+      // two taps: E_prev[y_{t-1}], read at the first layer, replaces E_prev[y_{t-2}] once the first
+      // layer has used it; the draw at the end of this step forms the next x0 from it
+      if (j == 1 && Eprev) {
+        u32x4* d = reinterpret_cast<u32x4*>(EPB + ldn * R + ldq * 16);
+        d[0] = pre_e[0];
+        d[1] = pre_e[1];
       }
       // x_{j-1}[t] (split) into slot t mod d_j of layer j's history, read again at step t + d_j.
       // The slot counter of layer j then moves on to step t + 1, so a read issued from here on
@@ -527,6 +552,11 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
         if constexpr (TF) pre_y = g.io.y_in[(size_t)lub * T + tl];
         else pre_u = g.io.u[(size_t)lub * T + tl];
       }
+      if (j == 0 && Eprev) {
+        const u32x4* e = reinterpret_cast<const u32x4*>(Eprev + (size_t)s_y[ldn] * R + ldq * 16);
+        pre_e[0] = e[0];
+        pre_e[1] = e[1];
+      }
       issue(nxt, tl2, j2);
       if (++j2 == L) j2 = 0, ++tl2;
       lds_barrier();
@@ -543,9 +573,10 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
   }
   __syncthreads();
   if (tid < G && b0 + tid < B) {
-    int64_t* st = g.ws.state + 2 * (size_t)(b0 + tid);
+    int64_t* st = g.ws.state + WN_STATE_WORDS * (size_t)(b0 + tid);
     st[0] = tg0 + T;
     st[1] = s_y[tid];
+    st[2] = s_y2[tid];
   }
 }
 
@@ -578,7 +609,7 @@ bool wn_group_supported(int R_, int S_, int L) {
   return R_ == R && (S_ == 256 || S_ == 128) && L >= 2 && L <= WN_GROUP_MAX_LAYERS;
 }
 
-size_t wn_group_lds_bytes(int L, int S_) {
+size_t wn_group_lds_bytes(int L, int S_, bool) {
   return S_ == 256 ? lds_bytes<256>(L) : lds_bytes<128>(L);
 }
 

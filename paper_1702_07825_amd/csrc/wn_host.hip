@@ -103,7 +103,7 @@ WsLayout ws_layout(const wn_handle* h, int B) {
   WsLayout l;
   l.status_off = 0;
   l.state_off = 256;
-  l.hist_off = align_up(l.state_off + (size_t)B * 2 * sizeof(int64_t), 256);
+  l.hist_off = align_up(l.state_off + (size_t)B * WN_STATE_WORDS * sizeof(int64_t), 256);
   WnChainPlan p;
   if (chain_plan_for(h, B, &p)) {
     l.mb_off = align_up(l.hist_off + (size_t)B * h->dims.hist_len * 8, 256);
@@ -265,7 +265,6 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
   for (const void* p : need)
     if (!p) return fail(WN_EINVAL, "null weight array");
   if (c->a != WN_A) return fail(WN_EUNSUPPORTED, "a must be 256");
-  if (c->embed_taps != 1) return fail(WN_EUNSUPPORTED, "only embed_taps = 1 is implemented");
   if (!wn_stream_supported(c->r, c->s)) return fail(WN_EUNSUPPORTED, "unsupported (r, s) pair");
 
   wn_handle* h = new (std::nothrow) wn_handle();
@@ -300,7 +299,7 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
   const size_t we = bf ? 2 : 4;
   struct Arr { const float* src; size_t n; bool matrix; size_t off; };
   Arr arrs[] = {
-      {w->embed, (size_t)A * R, true, 0},          {w->w_prev, (size_t)L * 2 * R * R, true, 0},
+      {w->embed, (size_t)c->embed_taps * A * R, true, 0}, {w->w_prev, (size_t)L * 2 * R * R, true, 0},
       {w->w_cur, (size_t)L * 2 * R * R, true, 0},  {w->w_res, (size_t)L * R * R, true, 0},
       {w->w_skip, (size_t)L * S * R, true, 0},     {w->w_relu, (size_t)A * S, true, 0},
       {w->w_out, (size_t)A * A, true, 0},          {w->b_embed, (size_t)R, false, 0},
@@ -334,7 +333,9 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
     return hip_fail(e, "hipMemcpy of weights");
   }
   char* d = static_cast<char*>(h->dmem);
-  h->w.embed = d + arrs[0].off;
+  // [taps][A][R]: the last table embeds y_{t-1}, the first of two y_{t-2}
+  h->w.embed = d + arrs[0].off + (size_t)(c->embed_taps - 1) * A * R * we;
+  h->w.embed_prev = c->embed_taps == 2 ? d + arrs[0].off : nullptr;
   h->w.w_prev = d + arrs[1].off;
   h->w.w_cur = d + arrs[2].off;
   h->w.w_res = d + arrs[3].off;
@@ -359,7 +360,7 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
   // The batched MFMA kernel needs bf16 weights, r = 64 and its LDS footprint on one CU.
   int lds_max = 0;
   (void)hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device);
-  if (want_chain && bf && wn_group_supported(R, S, L) && wn_group_lds_bytes(L, S) + 256 <= (size_t)lds_max) {
+  if (want_chain && bf && wn_group_supported(R, S, L) && wn_group_lds_bytes(L, S, c->embed_taps == 2) + 256 <= (size_t)lds_max) {
     const std::vector<uint16_t> tiles =
         wn_group_pack(L, R, S, w->w_prev, w->w_cur, w->w_res, w->w_skip, w->w_relu, w->w_out);
     e = hipMalloc(&h->dpack, tiles.size() * sizeof(uint16_t));

@@ -6,6 +6,9 @@
 
 #define WN_MAX_LAYERS 64
 #define WN_A 256
+// Per-stream generator state in the workspace, int64 words: steps taken, y_{t-1}, y_{t-2}
+// (-1 before the first input), one spare.
+#define WN_STATE_WORDS 4
 
 // Model sizes and the per-stream history layout: layer j keeps d_j slots of r
 // floats starting at hoff[j] (in floats) inside a stream's history block of
@@ -20,7 +23,8 @@ struct WnDims {
 // Device copies of the weights.  Matrices are row-major [out][in] and either
 // fp32 or bf16 (uint16 bit patterns); biases are fp32.
 struct WnDevWeights {
-  const void* embed;   // [A][R]
+  const void* embed;       // [A][R] embedding of y_{t-1}
+  const void* embed_prev;  // [A][R] embedding of y_{t-2} (two-tap input convolution), or null
   const void* w_prev;  // [L][2R][R]
   const void* w_cur;   // [L][2R][R]
   const void* w_res;   // [L][R][R]
@@ -54,7 +58,7 @@ struct WnIO {
 // Caller-owned workspace, carved by the host code.
 struct WnWorkspace {
   int32_t* status;      // one word
-  int64_t* state;       // [B][2]: steps taken, last sample
+  int64_t* state;       // [B][WN_STATE_WORDS]
   float* hist;          // [B][hist_len]
 };
 
@@ -77,7 +81,7 @@ struct WnChainArgs {
   WnDevWeights w;
   WnIO io;
   int32_t* status;
-  int64_t* state;                // [B][2]: steps taken, last sample
+  int64_t* state;                // [B][WN_STATE_WORDS]
   unsigned long long* ring;      // [B][hist_len] tagged dilation histories
   unsigned long long* mb;        // [B][mb_words] mailboxes, placed after the histories
   long long mb_words;            // words of one stream's mailbox block
@@ -126,7 +130,7 @@ struct WnGroupArgs {
 };
 #define WN_GROUP_MAX_LAYERS 40
 bool wn_group_supported(int R, int S, int L);
-size_t wn_group_lds_bytes(int L, int S);
+size_t wn_group_lds_bytes(int L, int S, bool two_taps);
 // Packs W_prev/W_cur/W_res/W_skip of every layer and the two head matrices (fp32 host arrays
 // in the wn_weights layout) into bf16 tiles, the order the kernel streams them in.
 std::vector<uint16_t> wn_group_pack(int L, int R, int S, const float* w_prev, const float* w_cur,

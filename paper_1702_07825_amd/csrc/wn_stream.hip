@@ -88,9 +88,11 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
   __shared__ float qs[S];
   __shared__ float zas[A];
   __shared__ __align__(16) float lgs[A];
-  __shared__ int yprev_s;
+  __shared__ int yprev_s;   // y_{t-1}
+  __shared__ int yprev2_s;  // y_{t-2}, -1 before the first input
 
   const WT* embed = static_cast<const WT*>(args.w.embed);
+  const WT* embed_prev = static_cast<const WT*>(args.w.embed_prev);  // null with one tap
   const WT* w_prev = static_cast<const WT*>(args.w.w_prev);
   const WT* w_cur = static_cast<const WT*>(args.w.w_cur);
   const WT* w_res = static_cast<const WT*>(args.w.w_res);
@@ -99,17 +101,23 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
   const WT* w_out = static_cast<const WT*>(args.w.w_out);
 
   float* hist = args.ws.hist + (size_t)b * D.hist_len;
-  int64_t* state = args.ws.state + 2 * (size_t)b;
+  int64_t* state = args.ws.state + WN_STATE_WORDS * (size_t)b;
 
   int64_t tg0;
   if (args.io.reset) {
     for (int i = tid; i < D.hist_len / 4; i += NT) reinterpret_cast<float4*>(hist)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     tg0 = 0;
-    if (tid == 0) yprev_s = args.io.init_sample;
+    if (tid == 0) {
+      yprev_s = args.io.init_sample;
+      yprev2_s = -1;
+    }
     if (b == 0 && tid == 0) *args.ws.status = 0;
   } else {
     tg0 = state[0];
-    if (tid == 0) yprev_s = (int)state[1];
+    if (tid == 0) {
+      yprev_s = (int)state[1];
+      yprev2_s = (int)state[2];
+    }
   }
   __syncthreads();
 
@@ -126,13 +134,15 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
         const int slot = (int)(tg % D.dil[j]);
         reinterpret_cast<float4*>(xr)[i] = reinterpret_cast<const float4*>(hist + D.hoff[j] + slot * R)[c4];
       }
-      const int yp = yprev_s;
+      const int yp = yprev_s, yp2 = yprev2_s;
       if (tid < R) {
-        const WT* e = embed + (size_t)yp * R;
-        float ev;
-        if constexpr (sizeof(WT) == 2) ev = __uint_as_float((uint32_t)e[tid] << 16);
-        else ev = e[tid];
-        xs[tid] = ev + args.w.b_embed[tid];
+        auto ld = [&](const WT* e) {
+          if constexpr (sizeof(WT) == 2) return __uint_as_float((uint32_t)e[tid] << 16);
+          else return (float)e[tid];
+        };
+        float ev = ld(embed + (size_t)yp * R) + args.w.b_embed[tid];
+        if (embed_prev && yp2 >= 0) ev += ld(embed_prev + (size_t)yp2 * R);
+        xs[tid] = ev;
       }
       for (int m = tid; m < S; m += NT) qs[m] = args.w.b_skip[m];
     }
@@ -238,6 +248,7 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
     if constexpr (TF) {
       if (tid == 0) {
         int y = args.io.y_in[bt];
+        yprev2_s = yprev_s;
         yprev_s = y < 0 ? 0 : (y > A - 1 ? A - 1 : y);
       }
     } else {
@@ -249,6 +260,7 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
         const int y = wnk::wave_draw(lv, args.io.u[bt], args.io.smode, args.io.inv_t, args.io.top_k, lane);
         if (lane == 0) {
           args.io.y_out[bt] = y;
+          yprev2_s = yprev_s;
           yprev_s = y;
         }
       }
@@ -258,6 +270,7 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
   if (tid == 0) {
     state[0] = tg0 + T;
     state[1] = yprev_s;
+    state[2] = yprev2_s;
   }
 }
 

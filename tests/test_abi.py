@@ -62,7 +62,7 @@ def _weights(wn):
 @pytest.mark.parametrize("kw,code", [
     (dict(L=0), -1), (dict(L=65), -1), (dict(init=256), -1), (dict(init=-1), -1), (dict(dtype=7), -1),
     (dict(dil=[1, 0, 4, 8]), -1), (dict(taps=3), -1), (dict(r=0), -1),
-    (dict(a=255), -2), (dict(taps=2), -2), (dict(r=48, s=32), -2), (dict(r=16, s=64), -2),
+    (dict(a=255), -2), (dict(r=48, s=32), -2), (dict(r=16, s=64), -2),
 ])
 def test_create_rejects_before_any_device_call(lib, kw, code):
     import paper_1702_07825_amd as wn
