@@ -105,7 +105,7 @@ def run_workload(name, args):
     wl = synth.WORKLOADS[name]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    w = synth.make_weights(wl.n_layers, wl.r, wl.s, seed=args.seed)
+    w = synth.make_weights(wl.n_layers, wl.r, wl.s, seed=args.seed, embed_taps=wl.embed_taps)
     net = wn.WaveNet(w, wl.dilations, weight_dtype=wl.weight_dtype)
     cond = synth.make_cond(wl.n_layers, wl.r, wl.B, wl.T, seed=args.seed, device="cuda:0")
     u_np = synth.make_uniforms(wl.B, wl.T, seed=args.seed)
@@ -160,6 +160,7 @@ def run_workload(name, args):
         "real_time_factor_16khz": round(per_stream_rate / RATE_HZ, 3),
         "real_time_factor_16384hz": round(per_stream_rate / PAPER_RATE_HZ, 3),
         "real_time_factor_48khz": round(per_stream_rate / HI_RATE_HZ, 3),
+        "real_time_factor_at_workload_rate": round(per_stream_rate / wl.sample_rate, 3),
         "us_per_sample_step": round(avg_launch_s / wl.T * 1e6, 3),
         "roofline": {
             "bound": bound,

@@ -211,9 +211,13 @@ __device__ __forceinline__ float dot_lds(const float (&w)[K], const float* x) {
 // ------------------------------------------------------------------------------------------
 // chain CU
 // ------------------------------------------------------------------------------------------
+// Two embedding tables fit chain CU 0's LDS beside its other buffers up to r = 64.
+constexpr bool e2_in_lds(int R) { return R <= 64; }
+
 template <int R, int S, int NLC, bool TF, bool MS, bool E2>
 __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, const int ns, float* dyn, Sync sy,
                            const int64_t tg0) {
+  constexpr bool E2L = E2 && e2_in_lds(R);
   using M = ChainMap<R>;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int L = g.d.L;
@@ -251,8 +255,11 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
   int* syv = ybuf + G * ub;                         // G      y_{t-1} of each stream
   int* syv2 = syv + ((G + 3) & ~3);                 // G      y_{t-2} (-1 before the first input)
   float* emb = reinterpret_cast<float*>(syv2 + ((G + 3) & ~3));  // A*R
-  // last chain CU: W_skip of layer l-1, S rows of stride WSK (after the table if it is also CU 0)
-  float* wsk = first ? emb + A * R : var;
+  // the table of y_{t-2} (two taps, r <= 64; a global load instead at r = 128, where two tables
+  // do not fit)
+  float* emb2 = emb + A * R;                        // A*R when E2L
+  // last chain CU: W_skip of layer l-1, S rows of stride WSK (after the tables if it is also CU 0)
+  float* wsk = first ? emb2 + (E2L ? A * R : 0) : var;
   // a middle r = 128 CU with two layers: their W_res, R rows of stride WRS each
   float* wres = var;
   const bool wres_lds = nl > M::WRV;
@@ -317,7 +324,7 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
     lhoff[tid] = g.d.hoff[j0 + tid];
   }
   float bemb = 0.f;
-  // two-tap input convolution (E2): the table of y_{t-2}
+  // two-tap input convolution (E2): the table of y_{t-2}, copied to LDS when it fits (E2L)
   const float* const Eprev = E2 ? static_cast<const float*>(g.w.embed_prev) : nullptr;
   float4 bout4 = make_float4(0.f, 0.f, 0.f, 0.f);  // B_out of the 4 logits lane l of wave 0 draws from
   if (tail) {
@@ -341,6 +348,8 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
     if (wave == 0) bout4 = *reinterpret_cast<const float4*>(g.w.b_out + 4 * lane);
     const float* E = static_cast<const float*>(g.w.embed);
     for (int i = tid; i < A * R; i += NT) emb[i] = E[i];
+    if constexpr (E2L)
+      for (int i = tid; i < A * R; i += NT) emb2[i] = Eprev[i];
     if (tid < R) bemb = g.w.b_embed[tid];
     for (int i = tid; i < ns; i += NT) {
       const int64_t* st = g.state + WN_STATE_WORDS * (size_t)(b0 + i);
@@ -414,12 +423,19 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
       //      either x from the previous chain CU or (chain CU 0) the previous step's partial logits ----
       const Items pre_items{mbs + ((size_t)j0 * 2 + par) * 2 * R, 2 * R, 2 * 2 * R, nl * 2 * R, pre, tag};
       if (first) {
-        // two-tap embedding: the row of y_{t-2} (known since the previous step) is loaded before
-        // the wait for the previous step's logits, which hides its latency
+        // two-tap embedding: the row of y_{t-2}, known since the previous step, from LDS; at
+        // r = 128 from global memory before the wait for the previous step's logits (the empty
+        // asm keeps the compiler from sinking the load to its use after that wait).  A global
+        // load here measured ~0.4 us of step time even when it hits in cache; the LDS read none.
         float ep = 0.f;
         if constexpr (E2) {
           const int y2 = t > tg0 ? syv[i] : syv2[i];
-          if (tid < R && y2 >= 0) ep = Eprev[(size_t)y2 * R + tid];
+          if constexpr (E2L) {
+            if (tid < R && y2 >= 0) ep = emb2[y2 * R + tid];
+          } else {
+            if (tid < R && y2 >= 0) ep = Eprev[(size_t)y2 * R + tid];
+            asm volatile("" : "+v"(ep));
+          }
         }
         if (t > tg0) {
           poll2(g, logit_items(t - 1, b), pre_items, dyn, sy);
@@ -877,11 +893,12 @@ int chain_split(int L, int R, int* layer_begin) {
 }
 
 // Dynamic LDS floats of each role (the launch takes the largest); mirrors the carving in the roles.
-size_t chain_lds_floats(int R, int S, int nlc, int G, int ub, int nch, int tail) {
+size_t chain_lds_floats(int R, int S, int nlc, int G, int ub, int nch, int tail, bool e2) {
   const int nlcp = (nlc + 3) & ~3;
   const size_t common = (size_t)2 * R + (size_t)nlc * 2 * R + (size_t)2 * nlc * R + 4 * nlcp;
   const size_t wsk = (size_t)S * lds_row_stride(R, S / 64);
   size_t cu0 = (size_t)NHEAD * A + (size_t)2 * G * ub + 2 * ((G + 3) & ~3) + (size_t)A * R;
+  if (e2 && e2_in_lds(R)) cu0 += (size_t)A * R;
   if (nch == 1 && tail) cu0 += wsk;
   size_t var = cu0;
   if (tail) var = std::max(var, wsk);
@@ -895,7 +912,8 @@ constexpr size_t kMaxLds = 160 * 1024;
 template <int R, int S>
 hipError_t launch_chain_rs(const WnChainArgs& g, bool teacher, hipStream_t stream) {
   constexpr int NLC = chain_nlc<R>();
-  const size_t dyn = sizeof(float) * std::max(chain_lds_floats(R, S, NLC, g.G, g.ub, g.nch, g.tail_on_chain),
+  const size_t dyn = sizeof(float) * std::max(chain_lds_floats(R, S, NLC, g.G, g.ub, g.nch, g.tail_on_chain,
+                                                                g.w.embed_prev != nullptr),
                                               std::max(head_lds_floats(g.d.L, S), aux_lds_floats(R, g.G)));
   void* args[] = {const_cast<WnChainArgs*>(&g)};
   // one stream (no replicas) gets a build with the stream loops folded away, a one-table
@@ -925,7 +943,7 @@ bool wn_chain_supported(int R, int S, int L) {
          head_lds_floats(L, S) * sizeof(float) <= kMaxLds;
 }
 
-bool wn_chain_plan(int L, int R, int S, int B, WnChainPlan* p) {
+bool wn_chain_plan(int L, int R, int S, int B, bool two_taps, WnChainPlan* p) {
   if (!p || B < 1 || !wn_chain_supported(R, S, L)) return false;
   WnChainPlan q{};
   const int nlc = nlc_for(R);
@@ -940,8 +958,9 @@ bool wn_chain_plan(int L, int R, int S, int B, WnChainPlan* p) {
   while (gp < q.G) gp *= 2;
   q.ub = std::max(16, 512 / gp);
   q.tail_on_chain = 1;
-  if (chain_lds_floats(R, S, nlc, q.G, q.ub, q.nch, 1) * sizeof(float) > kMaxLds) q.tail_on_chain = 0;
-  if (chain_lds_floats(R, S, nlc, q.G, q.ub, q.nch, q.tail_on_chain) * sizeof(float) > kMaxLds) return false;
+  if (chain_lds_floats(R, S, nlc, q.G, q.ub, q.nch, 1, two_taps) * sizeof(float) > kMaxLds) q.tail_on_chain = 0;
+  if (chain_lds_floats(R, S, nlc, q.G, q.ub, q.nch, q.tail_on_chain, two_taps) * sizeof(float) > kMaxLds)
+    return false;
   // mailboxes of one stream: pre, h, q, x, logits, tail (see WnChainArgs)
   const long long pre_w = (long long)L * 2 * 2 * R;
   q.off_h = (int)pre_w;

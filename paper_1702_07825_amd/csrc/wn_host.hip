@@ -82,7 +82,7 @@ class DeviceScope {
 // The multi-CU kernel's layout of B streams, if it serves them: every tagged word it polls
 // (histories, then mailboxes) must lie within 2^32 words of the first.
 bool chain_plan_for(const wn_handle* h, int B, WnChainPlan* p) {
-  if (!h->chain_ok || !wn_chain_plan(h->L, h->R, h->S, B, p)) return false;
+  if (!h->chain_ok || !wn_chain_plan(h->L, h->R, h->S, B, h->w.embed_prev != nullptr, p)) return false;
   return (unsigned long long)B * ((unsigned long long)h->dims.hist_len + (unsigned long long)p->mb_words) + 64 <
          (1ull << 32);
 }

@@ -115,7 +115,7 @@ hipError_t wn_stream_launch(const WnStreamArgs& args, bool teacher, hipStream_t 
 bool wn_chain_supported(int R, int S, int L);
 // Fills *p for B streams; false if the kernel cannot serve them (too many streams per replica,
 // or a layout that does not fit).
-bool wn_chain_plan(int L, int R, int S, int B, WnChainPlan* p);
+bool wn_chain_plan(int L, int R, int S, int B, bool two_taps, WnChainPlan* p);
 hipError_t wn_chain_reset(unsigned long long* words, size_t n, int* status, hipStream_t stream);
 hipError_t wn_chain_launch(const WnChainArgs& g, bool teacher, hipStream_t stream);
 

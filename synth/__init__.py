@@ -53,10 +53,12 @@ class Workload:
     T: int
     weight_dtype: str  # "f32" or "bf16" (storage); arithmetic is fp32 on the GPU
     description: str
+    embed_taps: int = 1          # 2: the width-2 input convolution of Section 5.1
+    sample_rate: int = 16000     # Hz of the audio the workload stands for
 
     @property
     def receptive_field(self) -> int:
-        return 1 + sum(self.dilations)
+        return self.embed_taps + sum(self.dilations)
 
 
 WORKLOADS: Dict[str, Workload] = {
@@ -72,6 +74,10 @@ WORKLOADS: Dict[str, Workload] = {
                                   "bf16",
                                   "l=20 (d=2^(i mod 10)), r=64, s=256, a=256, B=256, T=32000, "
                                   "bf16 weights, fp32 accumulate and activations"),
+    "l20_r64_b1_2tap_48k": Workload("l20_r64_b1_2tap_48k", 20, 64, 256, A_CLASSES, tuple(dilation_cycle(20)), 1,
+                                    48000, "f32",
+                                    "l=20 (d=2^(i mod 10)), r=64, s=256, a=256, two-tap input embedding, B=1, "
+                                    "T=48000 (1 s at 48 kHz), fp32", embed_taps=2, sample_rate=48000),
 }
 
 WEIGHT_NAMES = ("embed", "b_embed", "w_prev", "w_cur", "b_gate", "w_res", "b_res",

@@ -37,6 +37,8 @@ CASES = [
     ("wide_ragged", 227, 48, 3, 12, 3, 77, 256, 16000, 4801),
     ("wide_both_layers", 64, 16, 2, 8, 2, 50, 1, 1, None),
     ("short_T", 19, 7, 3, 3, 2, 33, 3, 8, 50),
+    # 256 Hz frames at 48 kHz: runs of 187 or 188 audio steps per frame
+    ("rate_48k", 227, 32, 2, 16, 1, 40, 256, 48000, None),
 ]
 
 
