@@ -48,7 +48,7 @@ def build(force: bool = True) -> str:
 class _Model(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int), ("r", ctypes.c_int), ("s", ctypes.c_int), ("a", ctypes.c_int),
                 ("dilations", ctypes.POINTER(ctypes.c_int)), ("initial_sample", ctypes.c_int),
-                ("bf16_weights", ctypes.c_int), ("embed_taps", ctypes.c_int)] + [
+                ("bf16_weights", ctypes.c_int), ("embed_taps", ctypes.c_int), ("approx_nonlin", ctypes.c_int)] + [
         (n, ctypes.POINTER(ctypes.c_float)) for n in
         ("embed", "b_embed", "w_prev", "w_cur", "b_gate", "w_res", "b_res", "w_skip", "b_skip",
          "w_relu", "b_relu", "w_out", "b_out")]
@@ -72,12 +72,20 @@ def lib():
                                      ctypes.c_void_p, ctypes.c_void_p]
             L.oracle_run_sampled.restype = ctypes.c_int
             L.oracle_run_sampled.argtypes = L.oracle_run.argtypes + [ctypes.c_int, ctypes.c_double, ctypes.c_int]
+            L.oracle_approx_nonlin.restype = None
+            L.oracle_approx_nonlin.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_longlong]
+            L.oracle_sample_nl.restype = ctypes.c_int
+            L.oracle_sample_nl.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_float, ctypes.c_int,
+                                           ctypes.c_double, ctypes.c_int, ctypes.c_void_p]
             L.oracle_sample.restype = ctypes.c_int
             L.oracle_sample.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_float, ctypes.c_int, ctypes.c_double,
                                         ctypes.c_int, ctypes.c_void_p]
             L.oracle_condition.restype = ctypes.c_int
             L.oracle_condition.argtypes = [ctypes.POINTER(_CondModel), ctypes.c_longlong, ctypes.c_void_p,
                                            ctypes.c_longlong, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+            L.oracle_draw_nl.restype = ctypes.c_int
+            L.oracle_draw_nl.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_float, ctypes.c_void_p,
+                                         ctypes.c_void_p]
             L.oracle_draw.restype = ctypes.c_int
             L.oracle_draw.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
             L.oracle_history_len.restype = ctypes.c_longlong
@@ -111,7 +119,7 @@ class Model:
     embeds y_{t-2}, tap 1 y_{t-1})."""
 
     def __init__(self, weights: Dict[str, np.ndarray], dilations: Sequence[int], initial_sample: int = 128,
-                 bf16_weights: bool = False):
+                 bf16_weights: bool = False, approx_nonlin: bool = False):
         self.w = {k: np.ascontiguousarray(v, dtype=np.float32) for k, v in weights.items()}
         L, two_r, r = self.w["w_prev"].shape
         s = self.w["w_skip"].shape[1]
@@ -130,6 +138,8 @@ class Model:
         m.initial_sample = self.initial_sample
         m.bf16_weights = int(self.bf16)
         m.embed_taps = self.embed_taps
+        self.approx_nonlin = bool(approx_nonlin)
+        m.approx_nonlin = int(self.approx_nonlin)
         for name in ("embed", "b_embed", "w_prev", "w_cur", "b_gate", "w_res", "b_res", "w_skip", "b_skip",
                      "w_relu", "b_relu", "w_out", "b_out"):
             setattr(m, name, self.w[name].ctypes.data_as(ctypes.POINTER(ctypes.c_float)))
@@ -222,22 +232,23 @@ def run_streams(model: Model, cond: np.ndarray, u: Optional[np.ndarray] = None, 
     return stack(0), stack(1), stack(2)
 
 
-def draw(logits: np.ndarray, u: float):
+def draw(logits: np.ndarray, u: float, approx_nonlin: bool = False):
     """Direct sampling of one step: returns (index, probabilities, margin)."""
     lg = np.ascontiguousarray(logits, dtype=np.float64)
     p = np.zeros_like(lg)
     mg = ctypes.c_double(0.0)
-    y = lib().oracle_draw(lg.shape[0], _ptr(lg), ctypes.c_float(float(u)), _ptr(p), ctypes.byref(mg))
+    y = lib().oracle_draw_nl(int(bool(approx_nonlin)), lg.shape[0], _ptr(lg), ctypes.c_float(float(u)), _ptr(p),
+                             ctypes.byref(mg))
     return int(y), p, float(mg.value)
 
 
-def sample(logits: np.ndarray, u: float, sampler=DIRECT):
+def sample(logits: np.ndarray, u: float, sampler=DIRECT, approx_nonlin: bool = False):
     """One step's result under ``sampler`` = (mode, temperature, top_k): returns (index, margin)."""
     lg = np.ascontiguousarray(logits, dtype=np.float64)
     mg = ctypes.c_double(0.0)
     smode, temp, top_k = sampler
-    y = lib().oracle_sample(lg.shape[0], _ptr(lg), ctypes.c_float(float(u)), int(smode), float(temp), int(top_k),
-                            ctypes.byref(mg))
+    y = lib().oracle_sample_nl(int(bool(approx_nonlin)), lg.shape[0], _ptr(lg), ctypes.c_float(float(u)), int(smode),
+                               float(temp), int(top_k), ctypes.byref(mg))
     if y < 0:
         raise ValueError("invalid sampler %r" % (sampler,))
     return int(y), float(mg.value)
@@ -265,6 +276,17 @@ def round_bf16(x: np.ndarray) -> np.ndarray:
     x = np.ascontiguousarray(x, dtype=np.float32)
     out = np.empty_like(x)
     lib().oracle_round_bf16_array(_ptr(x), _ptr(out), x.size)
+    return out
+
+
+APPROX = {"tanh": 0, "sigmoid": 1, "exp": 2}
+
+
+def approx_nonlin(which: str, x: np.ndarray) -> np.ndarray:
+    """The approximate tanh, sigmoid or exp of Appendix C at every element of x (float64)."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    out = np.empty_like(x)
+    lib().oracle_approx_nonlin(APPROX[which], _ptr(x), _ptr(out), x.size)
     return out
 
 

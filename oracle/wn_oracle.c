@@ -35,6 +35,13 @@
  *  - the other sampling rules (oracle_sample): top k keeps every class whose P
  *    is at least the k-th largest P (ties kept); the mean E_P[y] is taken to the
  *    nearest class index, halves up.
+ *  - approximate nonlinearities (approx_nonlin = 1; Appendix C): the gate's tanh
+ *    and sigmoid through e~(x) = 1 + |x| + 0.5658 x^2 + 0.143 x^4 as
+ *    sign(x) (e~ - 1/e~) / (e~ + 1/e~) and e~ / (1 + e~) (x >= 0) or 1 / (1 + e~)
+ *    (x < 0), and every e^x of the softmax and the sampling rules through the
+ *    2^x bit pattern: y = x / ln 2, z = y - floor(y), the float whose bits are the
+ *    integer part of (y + 126 + g(z)) 2^23 with g the appendix's rational fit of
+ *    2^z - z; 0 where y <= -126 (the pattern has no exponent left);
  *  - bf16 weight storage: every matrix (W_prev, W_cur, W_res, W_skip, W_relu,
  *    W_out and the embedding table) is rounded to bfloat16 with round-to-
  *    nearest-even and used as the exact value of that bfloat16; biases stay fp32.
@@ -52,6 +59,7 @@ typedef struct {
     int initial_sample;       /* y_{-1} */
     int bf16_weights;         /* 0: use the fp32 weights; 1: round matrices to bf16 first */
     int embed_taps;           /* 1 or 2 */
+    int approx_nonlin;        /* 0: exact tanh, sigmoid, exp; 1: the approximations of Appendix C */
     const float *embed;       /* [taps][a][r]: the last tap embeds y_{t-1}, tap 0 of two y_{t-2} */
     const float *b_embed;     /* [r] */
     const float *w_prev;      /* [l][2r][r] */
@@ -100,6 +108,43 @@ static double wv(const oracle_model *m, const float *p, long idx) {
 }
 
 static double sigmoid(double v) { return 1.0 / (1.0 + exp(-v)); }
+
+/* Appendix C: e~(x), a stand-in for e^|x| that gives good tanh and sigmoid values. */
+static double e_tilde(double x) {
+    const double a = fabs(x);
+    return 1.0 + a + 0.5658 * x * x + 0.143 * x * x * x * x;
+}
+static double tanh_approx(double x) {
+    const double e = e_tilde(x);
+    const double t = (e - 1.0 / e) / (e + 1.0 / e);
+    return x < 0.0 ? -t : (x > 0.0 ? t : 0.0);
+}
+static double sigmoid_approx(double x) {
+    const double e = e_tilde(x);
+    return x >= 0.0 ? e / (1.0 + e) : 1.0 / (1.0 + e);
+}
+/* Appendix C: e^x through the fp32 bit pattern of 2^(x / ln 2). */
+static double exp_approx(double x) {
+    const double y = x / log(2.0);
+    if (y <= -126.0) return 0.0;
+    const double z = y - floor(y);
+    const double g = -4.7259162 + 27.7280233 / (4.84252568 - z) - 1.49012907 * z;
+    const double v = (y + 126.0 + g) * 8388608.0;
+    if (v >= 4294967295.0) return INFINITY;
+    const uint32_t bits = (uint32_t)v;  /* integer part */
+    float f;
+    memcpy(&f, &bits, 4);
+    return (double)f;
+}
+static double tanh_nl(int ax, double x) { return ax ? tanh_approx(x) : tanh(x); }
+static double sigmoid_nl(int ax, double x) { return ax ? sigmoid_approx(x) : sigmoid(x); }
+static double exp_nl(int ax, double x) { return ax ? exp_approx(x) : exp(x); }
+
+/* Array forms of the three approximations, for the tests that pin them. */
+void oracle_approx_nonlin(int which, const double *x, double *out, long long n) {
+    for (long long i = 0; i < n; ++i)
+        out[i] = which == 0 ? tanh_approx(x[i]) : (which == 1 ? sigmoid_approx(x[i]) : exp_approx(x[i]));
+}
 
 long long oracle_history_len(const oracle_model *m) {
     long long n = 0;
@@ -152,7 +197,7 @@ static int oracle_step(const oracle_model *m, oracle_state *st, const float *con
             act[o] = ap + ac + (double)m->b_gate[(long)j * 2 * r + o] + (double)cond_t[(long)j * 2 * r + o];
         }
         /* gated activation: h = tanh(a[0:r]) * sigmoid(a[r:2r]) */
-        for (int c = 0; c < r; ++c) h[c] = tanh(act[c]) * sigmoid(act[r + c]);
+        for (int c = 0; c < r; ++c) h[c] = tanh_nl(m->approx_nonlin, act[c]) * sigmoid_nl(m->approx_nonlin, act[r + c]);
         /* history: x^(j-1)_t replaces x^(j-1)_{t-d} (it is read again at t+d) */
         for (int c = 0; c < r; ++c) slot[c] = x[c];
         /* skip contribution: q += W_skip^(j) h */
@@ -194,15 +239,15 @@ static int oracle_step(const oracle_model *m, oracle_state *st, const float *con
  * max-subtracted form of the performance-model appendix).  Writes the
  * probabilities if prob != NULL and the margin if margin != NULL.
  */
-int oracle_draw(int a, const double *logits, float u, double *prob, double *margin) {
+static int draw_nl(int ax, int a, const double *logits, float u, double *prob, double *margin) {
     double mx = logits[0];
     for (int i = 1; i < a; ++i) if (logits[i] > mx) mx = logits[i];
     double z = 0.0;
-    for (int i = 0; i < a; ++i) z += exp(logits[i] - mx);
+    for (int i = 0; i < a; ++i) z += exp_nl(ax, logits[i] - mx);
     double cdf = 0.0, best = 1e300;
     int y = 0;
     for (int k = 0; k < a; ++k) {
-        double p = exp(logits[k] - mx) / z;
+        double p = exp_nl(ax, logits[k] - mx) / z;
         if (prob) prob[k] = p;
         cdf += p;
         if (k <= a - 2) {
@@ -213,6 +258,15 @@ int oracle_draw(int a, const double *logits, float u, double *prob, double *marg
     }
     if (margin) *margin = best;
     return y;
+}
+
+int oracle_draw(int a, const double *logits, float u, double *prob, double *margin) {
+    return draw_nl(0, a, logits, u, prob, margin);
+}
+
+/* oracle_draw with the approximate exp of Appendix C when ax = 1. */
+int oracle_draw_nl(int ax, int a, const double *logits, float u, double *prob, double *margin) {
+    return draw_nl(ax, a, logits, u, prob, margin);
 }
 
 /*
@@ -235,8 +289,9 @@ int oracle_draw(int a, const double *logits, float u, double *prob, double *marg
  * (mode 3), or the distance of the mean from the nearest half-integer (mode 4).
  * Returns the index, or -1 for an invalid mode, temperature or k.
  */
-int oracle_sample(int a, const double *logits, float u, int mode, double temperature, int top_k, double *margin) {
-    if (mode == 0) return oracle_draw(a, logits, u, NULL, margin);
+static int sample_nl(int ax, int a, const double *logits, float u, int mode, double temperature, int top_k,
+                     double *margin) {
+    if (mode == 0) return draw_nl(ax, a, logits, u, NULL, margin);
     if (mode < 0 || mode > 4 || (mode == 1 && !(temperature > 0.0)) || (mode == 2 && (top_k < 1 || top_k > a)))
         return -1;
     double *w = malloc(sizeof(double) * (size_t)a);
@@ -256,7 +311,7 @@ int oracle_sample(int a, const double *logits, float u, int mode, double tempera
             double v = (mode == 1) ? logits[k] / temperature : logits[k];
             if (v > mx) mx = v;
         }
-        for (int k = 0; k < a; ++k) w[k] = exp(((mode == 1) ? logits[k] / temperature : logits[k]) - mx);
+        for (int k = 0; k < a; ++k) w[k] = exp_nl(ax, ((mode == 1) ? logits[k] / temperature : logits[k]) - mx);
         int last_kept = a - 1;
         if (mode == 2) {
             /* the k-th largest logit, by selection over a sorted copy */
@@ -301,6 +356,16 @@ int oracle_sample(int a, const double *logits, float u, int mode, double tempera
     return y;
 }
 
+int oracle_sample(int a, const double *logits, float u, int mode, double temperature, int top_k, double *margin) {
+    return sample_nl(0, a, logits, u, mode, temperature, top_k, margin);
+}
+
+/* oracle_sample with the approximate exp of Appendix C when ax = 1. */
+int oracle_sample_nl(int ax, int a, const double *logits, float u, int mode, double temperature, int top_k,
+                     double *margin) {
+    return sample_nl(ax, a, logits, u, mode, temperature, top_k, margin);
+}
+
 /*
  * Run T steps of one stream.
  *   mode 0 (generate): y_{t} is drawn from step t's distribution with u[t] and
@@ -317,7 +382,9 @@ int oracle_run_sampled(const oracle_model *m, oracle_state *st, int mode, long l
                        const float *cond, const float *u, const int *y_in,
                        int *samples_out, double *logits_out, double *margin_out,
                        int sample_mode, double temperature, int top_k) {
-    if (!m || T < 0 || (mode != 0 && mode != 1) || m->embed_taps < 1 || m->embed_taps > 2) return -1;
+    if (!m || T < 0 || (mode != 0 && mode != 1) || m->embed_taps < 1 || m->embed_taps > 2 ||
+        (m->approx_nonlin != 0 && m->approx_nonlin != 1))
+        return -1;
     if (mode == 0 && !u) return -1;
     if (mode == 1 && !y_in) return -1;
     oracle_state local;
@@ -337,7 +404,7 @@ int oracle_run_sampled(const oracle_model *m, oracle_state *st, int mode, long l
         if (logits_out) memcpy(logits_out + t * m->a, lg, sizeof(double) * m->a);
         int y = 0;
         double mg = 0.0;
-        if (u) y = oracle_sample(m->a, lg, u[t], sample_mode, temperature, top_k, &mg);
+        if (u) y = sample_nl(m->approx_nonlin, m->a, lg, u[t], sample_mode, temperature, top_k, &mg);
         if (y < 0) { free(lg); free(own); return -1; }
         if (margin_out) margin_out[t] = u ? mg : 0.0;
         if (samples_out) samples_out[t] = y;

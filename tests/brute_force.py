@@ -10,8 +10,9 @@ import torch
 import torch.nn.functional as F
 
 
-def logits(w, dilations, cond, y_in, initial_sample=128):
-    """w: dict of fp32 arrays; cond [T, l, 2r]; y_in [T] (step t consumes y_in[t-1]). Returns [T, a] float64."""
+def logits(w, dilations, cond, y_in, initial_sample=128, tanh=torch.tanh, sigmoid=torch.sigmoid):
+    """w: dict of fp32 arrays; cond [T, l, 2r]; y_in [T] (step t consumes y_in[t-1]). Returns [T, a] float64.
+    ``tanh`` and ``sigmoid`` are the gate's nonlinearities (float64 tensor -> tensor)."""
     t64 = {k: torch.tensor(np.asarray(v), dtype=torch.float64) for k, v in w.items()}
     L, two_r, r = t64["w_prev"].shape
     a = t64["w_out"].shape[0]
@@ -33,7 +34,7 @@ def logits(w, dilations, cond, y_in, initial_sample=128):
         kernel = torch.stack([t64["w_prev"][j], t64["w_cur"][j]], dim=-1)   # [2r, r, 2]: tap 0 sees t-d
         Xp = F.pad(X[None], (int(d), 0))
         A = F.conv1d(Xp, kernel, bias=t64["b_gate"][j], dilation=int(d))[0] + cond[:, j, :].T
-        H = torch.tanh(A[:r]) * torch.sigmoid(A[r:])
+        H = tanh(A[:r]) * sigmoid(A[r:])
         hidden.append(H)
         X = X + F.conv1d(H[None], t64["w_res"][j][:, :, None], bias=t64["b_res"][j])[0]
     Hcat = torch.cat(hidden, dim=0)                                       # [l r, T]

@@ -542,3 +542,98 @@ def test_conditioning_upsampling_by_repetition():
         assert set(lengths.tolist()) <= runs and len(lengths) == 18
     with pytest.raises(ValueError):
         oracle.condition(w, x, 20 * 64 + 1, 256, 16384)  # past the last frame
+
+
+# ---------------------------------------------------------------------------------------------
+# Approximate nonlinearities (Appendix C; error figures in Section 5.1)
+# ---------------------------------------------------------------------------------------------
+
+def test_approximate_nonlinearities_meet_the_papers_error_figures():
+    """Against numpy's tanh, logistic and exp on dense grids: the largest errors are the paper's
+    figures to the digits it prints (tanh 1.5e-3; sigmoid 2.5e-3 printed, 2.59e-3 measured; exp
+    2.4e-5 printed: the fit's relative error at the top of its interval), and close to them, so
+    that a changed coefficient moves them out of the window."""
+    x = np.linspace(-30.0, 30.0, 1200001)
+    et = np.abs(oracle.approx_nonlin("tanh", x) - np.tanh(x)).max()
+    es = np.abs(oracle.approx_nonlin("sigmoid", x) - 1.0 / (1.0 + np.exp(-x))).max()
+    assert 1.50e-3 <= et <= 1.52e-3, et
+    assert 2.55e-3 <= es <= 2.60e-3, es
+    v = np.linspace(-85.0, 0.0, 4000001)
+    ev = oracle.approx_nonlin("exp", v)
+    rel = np.abs(ev - np.exp(v)) / np.exp(v)
+    # the fit's own relative error (2^z at z = 0 is 1 + 2.62e-5) everywhere but in narrow windows
+    # just below each power of two, where the fit's excess carries the fraction into the exponent
+    # and the error doubles to the fit's error at z = 1 (4.79e-5)
+    carry = ev >= 2.0 ** np.ceil(v / np.log(2.0))
+    assert 0 < carry.mean() < 1e-4
+    assert 2.55e-5 <= rel[~carry].max() <= 2.65e-5, rel[~carry].max()
+    assert 4.7e-5 <= rel.max() <= 4.8e-5, rel.max()
+    assert np.abs(ev - np.exp(v)).max() <= 4.8e-5
+
+
+def test_approximate_nonlinearities_identities():
+    x = np.linspace(-12.0, 12.0, 24001)
+    t, sg = oracle.approx_nonlin("tanh", x), oracle.approx_nonlin("sigmoid", x)
+    np.testing.assert_array_equal(t, -oracle.approx_nonlin("tanh", -x))          # odd
+    np.testing.assert_allclose(sg + oracle.approx_nonlin("sigmoid", -x), 1.0, rtol=0, atol=4.5e-16)
+    assert oracle.approx_nonlin("tanh", np.array([0.0]))[0] == 0.0
+    assert oracle.approx_nonlin("sigmoid", np.array([0.0]))[0] == 0.5
+    assert np.all(np.diff(t) >= 0) and np.all(np.diff(sg) >= 0)                   # monotone
+    assert np.all(np.abs(t) < 1) and np.all((sg > 0) & (sg < 1))
+    v = np.linspace(-100.0, 0.0, 200001)
+    ev = oracle.approx_nonlin("exp", v)
+    assert np.all(np.diff(ev) >= 0)
+    # powers of two: y = k ln 2 / ln 2 is k or a rounding below it, so the value is 2^k times
+    # g(0) = 1 + 2.62e-5, or the carried fit at z = 1 (1 + 4.79e-5)
+    k = np.arange(-120, 1)
+    np.testing.assert_allclose(oracle.approx_nonlin("exp", k * np.log(2.0)), 2.0 ** k, rtol=4.8e-5, atol=0)
+    assert np.all(oracle.approx_nonlin("exp", k * np.log(2.0)) > 2.0 ** k)
+    # no exponent left below 2^-126: zero
+    assert np.all(oracle.approx_nonlin("exp", np.array([-88.0, -100.0, -1e4])) == 0.0)
+
+
+def test_approximate_nonlinearities_in_the_model():
+    """With approx_nonlin the gate uses the approximate tanh and sigmoid (whole-sequence form with
+    those two functions: 1e-10) and the draw the approximate exp (known-distribution special case:
+    numpy searchsorted on the normalised approximate exps)."""
+    L, r, s, a, dil, T = 4, 16, 32, 256, (1, 2, 4, 8), 60
+    w = synth.make_weights(L, r, s, a, seed=51, bias_scale=0.5)
+    m = oracle.Model(w, dil, approx_nonlin=True)
+    cond = _cond(L, r, T, seed=52)
+    y = synth.make_samples(1, T, seed=53)[0]
+    _, lg, _ = oracle.run(m, cond, y_in=y)
+
+    def ta(t):
+        return torch.tensor(oracle.approx_nonlin("tanh", t.numpy()), dtype=torch.float64)
+
+    def sa(t):
+        return torch.tensor(oracle.approx_nonlin("sigmoid", t.numpy()), dtype=torch.float64)
+
+    ref = brute_force.logits(w, dil, cond, y, tanh=ta, sigmoid=sa)
+    np.testing.assert_allclose(lg, ref, rtol=0, atol=1e-10)
+    _, lg_exact, _ = oracle.run(oracle.Model(w, dil), cond, y_in=y)
+    assert 1e-4 < np.abs(lg - lg_exact).max() < 5e-2
+
+    rng = np.random.default_rng(5)
+    qv = rng.dirichlet(np.full(a, 0.7))
+    w2 = synth.make_weights(2, 4, 8, a, seed=1, bias_scale=0.3)
+    w2["w_out"][:] = 0
+    w2["b_out"] = np.log(np.maximum(qv, 1e-12)).astype(np.float32)
+    m2 = oracle.Model(w2, (1, 2), approx_nonlin=True)
+    u = synth.make_uniforms(1, 400, seed=6)[0]
+    ys, _, mg = oracle.run(m2, _cond(2, 4, 400, seed=7), u=u)
+    b = w2["b_out"].astype(np.float64)
+    pa = oracle.approx_nonlin("exp", b - b.max())
+    cdf = np.cumsum(pa / pa.sum())
+    ref = np.minimum(np.searchsorted(cdf.astype(np.float32), u, side="right"), a - 1)
+    np.testing.assert_array_equal(ys, ref)
+    np.testing.assert_allclose(mg, np.abs(u[:, None].astype(np.float64) - cdf[None, : a - 1]).min(axis=1),
+                               rtol=0, atol=1e-14)
+    _, p_ax, _ = oracle.draw(b, 0.5, approx_nonlin=True)
+    _, p_ex, _ = oracle.draw(b, 0.5)
+    np.testing.assert_allclose(p_ax, pa / pa.sum(), rtol=1e-13, atol=0)
+    assert np.abs(p_ax / p_ex - 1).max() > 1e-5
+    for sm in [(1, 0.7, a), (2, 1.0, 12), (4, 1.0, a)]:   # temperature, top k, mean take it too
+        y_ax = oracle.sample(b, 0.37, sm, approx_nonlin=True)[0]
+        y_ex = oracle.sample(b, 0.37, sm)[0]
+        assert abs(y_ax - y_ex) <= 1
