@@ -86,6 +86,13 @@ typedef struct {
   int32_t top_k;      /* WN_SAMPLE_TOPK: 1 .. a; ignored otherwise */
 } wn_sampler;
 
+/* Nonlinearities: exact (hardware exp2 and reciprocal, the default), or the approximations of
+ * Appendix C ("Nonlinearity Approximation Details"): tanh and sigmoid through
+ * e~(x) = 1 + |x| + 0.5658 x^2 + 0.143 x^4, e^x through the fp32 bit pattern of 2^(x / ln 2) with
+ * the appendix's rational fit of 2^z - z.  Their largest errors against the exact functions are
+ * 1.5e-3 (tanh), 2.6e-3 (sigmoid) and 4.8e-5 (e^x on x <= 0). */
+typedef enum { WN_NONLIN_EXACT = 0, WN_NONLIN_PAPER = 1 } wn_nonlin_t;
+
 typedef struct {
   int32_t n_layers;          /* l, 1 .. 64 */
   int32_t r;                 /* residual channels: 16, 32, 64 or 128 */
@@ -99,6 +106,7 @@ typedef struct {
   int32_t initial_sample;    /* y_{-1}, 0 .. a-1; 128 is the mu-law code of silence */
   int32_t weight_dtype;      /* wn_dtype_t: storage of the matrices and the embedding;
                                 biases, activations and accumulation are always fp32 */
+  int32_t nonlinearity;      /* wn_nonlin_t: the gate's tanh and sigmoid and the softmax's exp */
 } wn_config;
 
 typedef struct {             /* host fp32, row-major, shapes below */

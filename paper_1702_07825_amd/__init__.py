@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libwn.so")
 
 WN_OK, WN_EINVAL, WN_EUNSUPPORTED, WN_ENOMEM, WN_EHIP, WN_ETIMEOUT, WN_EABORTED = 0, -1, -2, -3, -4, -5, -6
 WN_F32, WN_BF16 = 0, 1
+WN_NONLIN_EXACT, WN_NONLIN_PAPER = 0, 1
 A_CLASSES = 256
 EXPORTED = ("wn_create", "wn_workspace_bytes", "wn_generate", "wn_generate_sampled", "wn_teacher_force", "wn_status",
             "wn_kernel_variant", "wn_destroy", "wn_error_string", "wn_last_error",
@@ -40,7 +41,7 @@ class WnError(RuntimeError):
 class Config(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("r", ctypes.c_int32), ("s", ctypes.c_int32), ("a", ctypes.c_int32),
                 ("dilations", ctypes.POINTER(ctypes.c_int32)), ("embed_taps", ctypes.c_int32),
-                ("initial_sample", ctypes.c_int32), ("weight_dtype", ctypes.c_int32)]
+                ("initial_sample", ctypes.c_int32), ("weight_dtype", ctypes.c_int32), ("nonlinearity", ctypes.c_int32)]
 
 
 class Sampler(ctypes.Structure):
@@ -144,7 +145,7 @@ class WaveNet:
     """
 
     def __init__(self, weights: Dict[str, np.ndarray], dilations: Sequence[int], initial_sample: int = 128,
-                 weight_dtype: str = "f32", embed_taps: Optional[int] = None):
+                 weight_dtype: str = "f32", embed_taps: Optional[int] = None, approx_nonlin: bool = False):
         self._lib = load_library()
         self._h = None
         w = {k: np.ascontiguousarray(weights[k], dtype=np.float32) for k in WEIGHT_FIELDS}
@@ -160,7 +161,9 @@ class WaveNet:
         self.weight_dtype = weight_dtype
         cfg = Config(self.n_layers, self.r, self.s, self.a,
                      self.dilations.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), int(embed_taps),
-                     self.initial_sample, {"f32": WN_F32, "bf16": WN_BF16}[weight_dtype])
+                     self.initial_sample, {"f32": WN_F32, "bf16": WN_BF16}[weight_dtype],
+                     WN_NONLIN_PAPER if approx_nonlin else WN_NONLIN_EXACT)
+        self.approx_nonlin = bool(approx_nonlin)
         ws = Weights(*[w[k].ctypes.data_as(ctypes.POINTER(ctypes.c_float)) for k in WEIGHT_FIELDS])
         h = ctypes.c_void_p()
         _check(self._lib.wn_create(ctypes.byref(cfg), ctypes.byref(ws), ctypes.byref(h)), "wn_create")

@@ -214,7 +214,7 @@ __device__ __forceinline__ float dot_lds(const float (&w)[K], const float* x) {
 // Two embedding tables fit chain CU 0's LDS beside its other buffers up to r = 64.
 constexpr bool e2_in_lds(int R) { return R <= 64; }
 
-template <int R, int S, int NLC, bool TF, bool MS, bool E2>
+template <int R, int S, int NLC, bool TF, bool MS, bool E2, bool AX>
 __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, const int ns, float* dyn, Sync sy,
                            const int64_t tg0) {
   constexpr bool E2L = E2 && e2_in_lds(R);
@@ -383,7 +383,7 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
         y = reinterpret_cast<const int*>(ubuf)[at];
         y = y < 0 ? 0 : (y > A - 1 ? A - 1 : y);
       } else {
-        y = wave_draw(lv, ubuf[at], g.io.smode, g.io.inv_t, g.io.top_k, lane);
+        y = wave_draw<AX>(lv, ubuf[at], g.io.smode, g.io.inv_t, g.io.top_k, lane);
       }
       if (lane == 0) {
         if constexpr (E2) syv2[i] = syv[i];
@@ -504,7 +504,7 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
             xsplit8_2(p[0][0] + p[0][1], p[1][0] + p[1][1], p[2][0] + p[2][1], p[3][0] + p[3][1], upper, ah, ag);
             ah = gsum4(ah);
             ag = gsum4(ag);
-            const float h = tanh_f(ah) * sigmoid_f(ag);
+            const float h = tanh_nl<AX>(ah) * sigmoid_nl<AX>(ag);
             if ((li & 3) == 0) hs[2 * gq + (upper ? 1 : 0)] = h;
           } else {
             float sh0 = 0.f, sh1 = 0.f, sg0 = 0.f, sg1 = 0.f;
@@ -539,7 +539,7 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
             }
             const float ah = gsum<M::LPRG>(sh0 + sh1);
             const float ag = gsum<M::LPRG>(sg0 + sg1);
-            const float h = tanh_f(ah) * sigmoid_f(ag);
+            const float h = tanh_nl<AX>(ah) * sigmoid_nl<AX>(ag);
             if (kq == 0) hs[g1] = h;
           }
           lds_barrier();
@@ -832,7 +832,7 @@ __device__ void head_role(const WnChainArgs& g, const int hh, const int b0, cons
   }
 }
 
-template <int R, int S, int NLC, bool TF, bool MS, bool E2>
+template <int R, int S, int NLC, bool TF, bool MS, bool E2, bool AX>
 __global__ __launch_bounds__(NT) void wn_chain_kernel(const WnChainArgs g) {
   extern __shared__ __align__(16) float dyn[];
   __shared__ int s_abort;
@@ -849,7 +849,7 @@ __global__ __launch_bounds__(NT) void wn_chain_kernel(const WnChainArgs g) {
   const int64_t tg0 = g.io.reset ? 0 : g.state[WN_STATE_WORDS * (size_t)b0];
   __syncthreads();
   Sync sy{&s_abort};
-  if (role < g.nch) chain_role<R, S, NLC, TF, MS, E2>(g, role, b0, ns, dyn, sy, tg0);
+  if (role < g.nch) chain_role<R, S, NLC, TF, MS, E2, AX>(g, role, b0, ns, dyn, sy, tg0);
   else if (role < g.nch + NHEAD) head_role<R, S, TF, MS>(g, role - g.nch, b0, ns, dyn, sy, tg0);
   else aux_role<R, S, TF, MS>(g, role - g.nch - NHEAD, b0, ns, dyn, sy, tg0);
 }
@@ -917,12 +917,18 @@ hipError_t launch_chain_rs(const WnChainArgs& g, bool teacher, hipStream_t strea
                                               std::max(head_lds_floats(g.d.L, S), aux_lds_floats(R, g.G)));
   void* args[] = {const_cast<WnChainArgs*>(&g)};
   // one stream (no replicas) gets a build with the stream loops folded away, a one-table
-  // embedding one without the second table's load
-  const bool ms = g.io.B > 1, e2 = g.w.embed_prev != nullptr;
+  // embedding one without the second table's load; the approximate nonlinearities are built
+  // only with the stream loops (they serve one stream too)
+  const bool ax = g.w.approx_nl != 0, ms = g.io.B > 1 || ax, e2 = g.w.embed_prev != nullptr;
   auto pick = [&](auto tf, auto msc) -> const void* {
     constexpr bool TF = decltype(tf)::value, MS = decltype(msc)::value;
-    return e2 ? reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, TF, MS, true>)
-              : reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, TF, MS, false>);
+    if constexpr (MS) {
+      if (ax)
+        return e2 ? reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, TF, true, true, true>)
+                  : reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, TF, true, false, true>);
+    }
+    return e2 ? reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, TF, MS, true, false>)
+              : reinterpret_cast<const void*>(wn_chain_kernel<R, S, NLC, TF, MS, false, false>);
   };
   using t_ = std::true_type;
   using f_ = std::false_type;

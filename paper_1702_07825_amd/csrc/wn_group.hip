@@ -116,7 +116,7 @@ constexpr size_t lds_bytes(int L) {
          2 * ((size_t)5 * G * SR + (size_t)G * Pack<S>::SS + (size_t)G * SA + (size_t)A * R + (size_t)G * R);
 }
 
-template <int S, bool TF>
+template <int S, bool TF, bool AX>
 __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
   using P = Pack<S>;
   constexpr int SS = P::SS;
@@ -302,7 +302,7 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
         y = s_yin[nn];
       } else {
         const float4 lv = *reinterpret_cast<const float4*>(LG + nn * PA + 4 * lane);
-        y = wave_draw(lv, s_u[nn], g.io.smode, g.io.inv_t, g.io.top_k, lane);
+        y = wave_draw<AX>(lv, s_u[nn], g.io.smode, g.io.inv_t, g.io.top_k, lane);
       }
       if (lane == 0) {
         s_y2[nn] = s_y[nn];
@@ -366,10 +366,10 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
       const float4 bh = *reinterpret_cast<const float4*>(BG + j * 2 * R + m0);
       const float4 bg = *reinterpret_cast<const float4*>(BG + j * 2 * R + R + m0);
       float4 hv;
-      hv.x = tanh_f(at[0] + bh.x + ch.x) * sigmoid_f(as[0] + bg.x + cg.x);
-      hv.y = tanh_f(at[1] + bh.y + ch.y) * sigmoid_f(as[1] + bg.y + cg.y);
-      hv.z = tanh_f(at[2] + bh.z + ch.z) * sigmoid_f(as[2] + bg.z + cg.z);
-      hv.w = tanh_f(at[3] + bh.w + ch.w) * sigmoid_f(as[3] + bg.w + cg.w);
+      hv.x = tanh_nl<AX>(at[0] + bh.x + ch.x) * sigmoid_nl<AX>(as[0] + bg.x + cg.x);
+      hv.y = tanh_nl<AX>(at[1] + bh.y + ch.y) * sigmoid_nl<AX>(as[1] + bg.y + cg.y);
+      hv.z = tanh_nl<AX>(at[2] + bh.z + ch.z) * sigmoid_nl<AX>(as[2] + bg.z + cg.z);
+      hv.w = tanh_nl<AX>(at[3] + bh.w + ch.w) * sigmoid_nl<AX>(as[3] + bg.w + cg.w);
       store_split4<R>(HS + n * SR, m0, hv);
       lds_barrier();
       if (j < L - 1) {
@@ -584,12 +584,20 @@ template <int S>
 hipError_t launch_group_s(const WnGroupArgs& g, bool teacher, hipStream_t stream) {
   const size_t dyn = lds_bytes<S>(g.d.L);
   const dim3 grid((g.io.B + G - 1) / G), block(NT);
-  const void* k = teacher ? reinterpret_cast<const void*>(wn_group_kernel<S, true>)
-                          : reinterpret_cast<const void*>(wn_group_kernel<S, false>);
+  const bool ax = g.w.approx_nl != 0;
+  const void* k = teacher ? (ax ? reinterpret_cast<const void*>(wn_group_kernel<S, true, true>)
+                                : reinterpret_cast<const void*>(wn_group_kernel<S, true, false>))
+                          : (ax ? reinterpret_cast<const void*>(wn_group_kernel<S, false, true>)
+                                : reinterpret_cast<const void*>(wn_group_kernel<S, false, false>));
   hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
   if (e != hipSuccess) return e;
-  if (teacher) hipLaunchKernelGGL((wn_group_kernel<S, true>), grid, block, dyn, stream, g);
-  else hipLaunchKernelGGL((wn_group_kernel<S, false>), grid, block, dyn, stream, g);
+  if (teacher) {
+    if (ax) hipLaunchKernelGGL((wn_group_kernel<S, true, true>), grid, block, dyn, stream, g);
+    else hipLaunchKernelGGL((wn_group_kernel<S, true, false>), grid, block, dyn, stream, g);
+  } else {
+    if (ax) hipLaunchKernelGGL((wn_group_kernel<S, false, true>), grid, block, dyn, stream, g);
+    else hipLaunchKernelGGL((wn_group_kernel<S, false, false>), grid, block, dyn, stream, g);
+  }
   return hipGetLastError();
 }
 

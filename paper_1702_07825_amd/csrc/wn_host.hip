@@ -255,6 +255,8 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
   if (c->weight_dtype != WN_F32 && c->weight_dtype != WN_BF16) return fail(WN_EINVAL, "unknown weight_dtype");
   if (c->initial_sample < 0 || c->initial_sample >= c->a) return fail(WN_EINVAL, "initial_sample out of range");
   if (c->embed_taps < 1 || c->embed_taps > 2) return fail(WN_EINVAL, "embed_taps must be 1 or 2");
+  if (c->nonlinearity != WN_NONLIN_EXACT && c->nonlinearity != WN_NONLIN_PAPER)
+    return fail(WN_EINVAL, "unknown nonlinearity");
   long long hist_steps = 0;
   for (int j = 0; j < c->n_layers; ++j) {
     if (c->dilations[j] < 1 || c->dilations[j] > 65536) return fail(WN_EINVAL, "dilations must be 1..65536");
@@ -349,6 +351,7 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
   h->w.b_relu = reinterpret_cast<const float*>(d + arrs[11].off);
   h->w.b_out = reinterpret_cast<const float*>(d + arrs[12].off);
   h->w.bf16 = bf ? 1 : 0;
+  h->w.approx_nl = c->nonlinearity == WN_NONLIN_PAPER ? 1 : 0;
 
   // The multi-CU kernel needs fp32 weights, a supported shape and one CU per block of its grid.
   const char* force = std::getenv("WN_KERNEL");

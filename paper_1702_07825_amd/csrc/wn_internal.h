@@ -38,6 +38,7 @@ struct WnDevWeights {
   const float* b_relu;
   const float* b_out;
   int bf16;
+  int approx_nl;  // 1: the approximate tanh, sigmoid and softmax exp of the paper's Appendix C
 };
 
 // One call's inputs and outputs (device pointers, caller-owned).

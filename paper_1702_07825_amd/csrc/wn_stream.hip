@@ -171,7 +171,7 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
               const float* bg = args.w.b_gate + j * 2 * R;
               const float a0 = s0 + bg[c] + cs[j * 2 * R + c];
               const float a1 = s1 + bg[c + R] + cs[j * 2 * R + c + R];
-              hs[c] = tanh_f(a0) * sigmoid_f(a1);
+              hs[c] = args.w.approx_nl ? wnk::tanh_paper(a0) * wnk::sigmoid_paper(a1) : tanh_f(a0) * sigmoid_f(a1);
             }
           }
         }
@@ -257,7 +257,9 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
       if (tid < 64) {
         const int lane = tid;
         const float4 lv = *reinterpret_cast<const float4*>(lgs + 4 * lane);
-        const int y = wnk::wave_draw(lv, args.io.u[bt], args.io.smode, args.io.inv_t, args.io.top_k, lane);
+        const int y = args.w.approx_nl
+                          ? wnk::wave_draw<true>(lv, args.io.u[bt], args.io.smode, args.io.inv_t, args.io.top_k, lane)
+                          : wnk::wave_draw<false>(lv, args.io.u[bt], args.io.smode, args.io.inv_t, args.io.top_k, lane);
         if (lane == 0) {
           args.io.y_out[bt] = y;
           yprev2_s = yprev_s;

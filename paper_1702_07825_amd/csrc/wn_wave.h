@@ -94,6 +94,39 @@ __device__ __forceinline__ float expf_fast(float v) { return __builtin_amdgcn_ex
 __device__ __forceinline__ float tanh_f(float v) { return 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + expf_fast(2.0f * v)); }
 __device__ __forceinline__ float sigmoid_f(float v) { return __builtin_amdgcn_rcpf(1.0f + expf_fast(-v)); }
 
+// The approximate nonlinearities of the paper's Appendix C.  e~(x) = 1 + |x| + 0.5658 x^2 +
+// 0.143 x^4 stands in for e^|x| in tanh(x) ~ sign(x) (e~ - 1/e~) / (e~ + 1/e~) and sigmoid(x) ~
+// e~ / (1 + e~) (x >= 0) or 1 / (1 + e~) (x < 0); |x| is clamped to 1e9 so that e~ stays finite
+// (the results there are +-1, 1 or 0 to fp32 either way).
+__device__ __forceinline__ float e_tilde(float x) {
+  const float c = fminf(fmaxf(x, -1e9f), 1e9f), a = fabsf(c), x2 = c * c;
+  return 1.0f + a + x2 * (0.5658f + 0.143f * x2);
+}
+__device__ __forceinline__ float tanh_paper(float x) {
+  const float e = e_tilde(x), r = __builtin_amdgcn_rcpf(e);
+  return copysignf((e - r) * __builtin_amdgcn_rcpf(e + r), x);
+}
+__device__ __forceinline__ float sigmoid_paper(float x) {
+  const float e = e_tilde(x), r = __builtin_amdgcn_rcpf(1.0f + e);
+  return x >= 0.0f ? e * r : r;
+}
+// e^x for x <= 0 (the softmax's arguments) through the fp32 bit pattern of 2^y, y = x / ln 2:
+// with z = y - floor(y) the pattern is (floor(y) + 126) 2^23 + (z + g(z)) 2^23, g the rational
+// fit of 2^z - z, truncated to an integer (the integer part of the first term is exact, so fp32
+// rounds only z + g); 0 where y <= -126.
+__device__ __forceinline__ float exp_paper(float x) {
+  const float y = x * 1.4426950408889634f;
+  if (!(y > -126.0f)) return 0.0f;
+  const float fl = floorf(y), z = y - fl;
+  const float g = -4.7259162f + 27.7280233f * __builtin_amdgcn_rcpf(4.84252568f - z) - 1.49012907f * z;
+  const unsigned bits = ((unsigned)((int)fl + 126) << 23) + (unsigned)((z + g) * 8388608.0f);
+  return __uint_as_float(bits);
+}
+// Exact (AX = false) or approximate (AX = true) nonlinearities.
+template <bool AX> __device__ __forceinline__ float tanh_nl(float v) { return AX ? tanh_paper(v) : tanh_f(v); }
+template <bool AX> __device__ __forceinline__ float sigmoid_nl(float v) { return AX ? sigmoid_paper(v) : sigmoid_f(v); }
+template <bool AX> __device__ __forceinline__ float exp_nl(float v) { return AX ? exp_paper(v) : expf_fast(v); }
+
 // Sum over the 64 lanes of a wave (every lane gets it).
 __device__ __forceinline__ float wave_sum(float v) {
   v = gsum16(v);
@@ -123,6 +156,8 @@ enum { WN_DRAW_DIRECT = 0, WN_DRAW_TEMPERATURE = 1, WN_DRAW_TOPK = 2, WN_DRAW_MO
 //                rounding) becomes that class
 //   mode         the smallest index of the largest logit
 //   mean         floor(sum_k k p_k + 1/2)
+// AX: e^x of the softmax by the approximation of Appendix C.
+template <bool AX = false>
 __device__ __forceinline__ int wave_draw(float4 lv, float u, int mode, float inv_t, int top_k, int lane) {
   float l[4] = {lv.x, lv.y, lv.z, lv.w};
   if (mode == WN_DRAW_MODE) {
@@ -142,7 +177,7 @@ __device__ __forceinline__ int wave_draw(float4 lv, float u, int mode, float inv
   const float m = wave_max(fmaxf(fmaxf(l[0], l[1]), fmaxf(l[2], l[3])));
   float e[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) e[i] = expf_fast(l[i] - m);
+  for (int i = 0; i < 4; ++i) e[i] = exp_nl<AX>(l[i] - m);
   int last = 255;
   if (mode == WN_DRAW_TOPK) {
     // the k-th largest key, built bit by bit: the largest t with #{key >= t} >= k

@@ -47,7 +47,7 @@ def _cfg(wn, **kw):
     d = np.array(kw.pop("dil", [1, 2, 4, 8]), np.int32)
     c = wn.Config(kw.get("L", 4), kw.get("r", 16), kw.get("s", 32), kw.get("a", 256),
                   d.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), kw.get("taps", 1), kw.get("init", 128),
-                  kw.get("dtype", 0))
+                  kw.get("dtype", 0), kw.get("nl", 0))
     return c, d
 
 
@@ -61,7 +61,7 @@ def _weights(wn):
 
 @pytest.mark.parametrize("kw,code", [
     (dict(L=0), -1), (dict(L=65), -1), (dict(init=256), -1), (dict(init=-1), -1), (dict(dtype=7), -1),
-    (dict(dil=[1, 0, 4, 8]), -1), (dict(taps=3), -1), (dict(r=0), -1),
+    (dict(dil=[1, 0, 4, 8]), -1), (dict(taps=3), -1), (dict(r=0), -1), (dict(nl=2), -1), (dict(nl=-1), -1),
     (dict(a=255), -2), (dict(r=48, s=32), -2), (dict(r=16, s=64), -2),
 ])
 def test_create_rejects_before_any_device_call(lib, kw, code):
