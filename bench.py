@@ -44,7 +44,8 @@ def macs_per_sample(L, r, s, a=256, last_res=False):
 KERNEL_SOURCES = {
     "multi_cu_chain": ["wn_chain.hip", "wn_wave.h", "wn_internal.h"],
     "mfma_group": ["wn_group.hip", "wn_wave.h", "wn_internal.h"],
-    "stream_l2": ["wn_stream.hip", "wn_internal.h"],
+    "stream_l2": ["wn_stream.hip", "wn_wave.h", "wn_internal.h"],
+    "conditioning": ["wn_cond.hip", "wn_wave.h", "wn_internal.h"],
 }
 
 
@@ -197,6 +198,23 @@ def cond_flops(wl):
     return 2.0 * per_frame * wl.B * wl.n_frames
 
 
+def cond_cpu_baseline(wl, w, x_dev, min_seconds):
+    """The CPU oracle's conditioning network on whole utterances of the workload (stream 0, 1, ...),
+    one thread, until at least `min_seconds` of oracle time have passed."""
+    import oracle
+    steps, secs, runs = 0, 0.0, 0
+    while secs < min_seconds:
+        xb = x_dev[runs % wl.B].cpu().numpy()
+        t0 = time.perf_counter()
+        oracle.condition(w, xb, wl.T, wl.frame_rate, wl.audio_rate)
+        secs += time.perf_counter() - t0
+        steps += wl.T
+        runs += 1
+    return {"value": steps / secs, "unit": "samples/s", "cores": 1, "kind": "oracle",
+            "sample": "%d whole utterance(s) of %d frames -> %d audio steps, one thread, fp64 C oracle" %
+                      (runs, wl.n_frames, wl.T), "seconds": round(secs, 2)}
+
+
 def run_cond_workload(name, args):
     """The conditioning network (Appendix A.2) over a batch of utterances: one wn_condition call
     per step, features already in HBM; value = audio steps of conditioning produced per second."""
@@ -246,7 +264,7 @@ def run_cond_workload(name, args):
             "peak": PEAKS["f32_mfma_tflops"],
             "unit": "TFLOP/s",
             "frac": round(flop / avg_s / 1e12 / PEAKS["f32_mfma_tflops"], 6),
-            "traffic": None,
+            "traffic": traffic_from_profiles(name, "conditioning"),
             "note": "whole wn_condition call (gate contractions, pools, upsampling) against the fp32 MFMA peak",
             "algorithmic_flop_per_launch": flop,
             "hbm": {"output_bytes_per_launch": out_bytes, "achieved_gbs": round(out_bytes / avg_s / 1e9, 2),
@@ -255,6 +273,8 @@ def run_cond_workload(name, args):
         },
         "cpu_baseline": None,
     }
+    if args.cpu_seconds > 0:
+        out["cpu_baseline"] = cond_cpu_baseline(wl, w, x, args.cpu_seconds)
     print(json.dumps(out), flush=True)
     net.close()
     del x, cond, ws

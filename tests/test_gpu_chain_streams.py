@@ -39,6 +39,10 @@ CASES = [
     ("l1_r128_b2", 1, 128, 256, (1,), 2, 150, 0.4),                                  # one chain CU, skip on aux
     ("l5_r128_b3", 5, 128, 256, (2, 1, 4, 1, 3), 3, 200, 0.3),                      # chain CUs of 1, 2, 1, 1 layers
     ("l9_r32_b40", 9, 32, 128, (1, 2, 4, 8, 16, 32, 64, 128, 256), 40, 200, 0.2),    # 14 x 3 (last 1)
+    # the largest batch one launch serves at l = 20, r = 64: 9 replicas of 27 CUs, 16 streams each
+    ("l20_r64_b144", 20, 64, 256, tuple(synth.dilation_cycle(20)), 144, 40, 0.1),
+    # the most layers the library takes
+    ("l64_r64_b1", 64, 64, 256, tuple(synth.dilation_cycle(64)), 1, 120, 0.1),
 ]
 
 

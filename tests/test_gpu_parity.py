@@ -163,22 +163,24 @@ def test_initial_sample_and_bias_paths():
 # ---------------------------------------------------------------------------------------------
 
 def _window(w, dil, dtype, cond_b, u_b, y_b, t):
-    """Oracle logits, draw and margin of step t from a teacher-forced run over [t - sum(d), t]."""
-    t0 = max(0, t - int(sum(dil)))
+    """Oracle logits, draw and margin of step t from a teacher-forced run over
+    [t - (taps - 1) - sum(d), t], the window step t depends on (taps = embedding taps)."""
+    taps = 1 if np.asarray(w["embed"]).ndim == 2 else 2
+    t0 = max(0, t - (taps - 1) - int(sum(dil)))
     init = 128 if t0 == 0 else int(y_b[t0 - 1])
     m = oracle.Model(w, dil, initial_sample=init, bf16_weights=(dtype == "bf16"))
     ys, lo, mg = oracle.run(m, cond_b[t0:t + 1], u=u_b[t0:t + 1], y_in=y_b[t0:t + 1])
     return lo[-1], int(ys[-1]), float(mg[-1])
 
 
-FULL = ["l20_r64_b1", "l40_r64_b1", "tiny", "l20_r128_b32", "l20_r64_b256_bf16"]
+FULL = ["l20_r64_b1", "l40_r64_b1", "tiny", "l20_r128_b32", "l20_r64_b256_bf16", "l20_r64_b1_2tap_48k"]
 
 
 @pytest.mark.parametrize("name", FULL)
 def test_full_size_sampled(name):
     wl = synth.WORKLOADS[name]
     _log("full-size %s: %s" % (name, wl.description))
-    w = synth.make_weights(wl.n_layers, wl.r, wl.s, seed=0)
+    w = synth.make_weights(wl.n_layers, wl.r, wl.s, seed=0, embed_taps=wl.embed_taps)
     wn = _wn()
     net = wn.WaveNet(w, wl.dilations, weight_dtype=wl.weight_dtype)
     cond = synth.make_cond(wl.n_layers, wl.r, wl.B, wl.T, seed=0, device="cuda")
