@@ -175,8 +175,8 @@ constexpr int lds_row_stride(int K, int rows) {
 
 
 template <int K>
-__device__ __forceinline__ float dot_lds(const float (&w)[K], const float* x) {
-  float s0 = 0.f, s1 = 0.f;
+__device__ __forceinline__ float dot_lds(const float (&w)[K], const float* x, float init = 0.f) {
+  float s0 = init, s1 = 0.f;
   if constexpr (K % 8 == 0) {
     float s2 = 0.f, s3 = 0.f;
 #pragma unroll
@@ -464,18 +464,31 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
         slotv[(par ^ 1) * NLCP + tid] = (sl == ldil[tid]) ? 0 : sl;
       }
 
-      // Store data of the per-layer h posts, rotating over HPOST register pairs: a pair is written
-      // again HPOST layers after its store was issued, by when that store has completed, so the
-      // wait the compiler places before the overwrite costs nothing inside the layer loop.
+      // h_j[t] -> layer j's aux CU (skip projection), posted by the lanes that computed it.  The
+      // store data rotate over HPOST register pairs: a pair is written again HPOST layers after
+      // its store was issued, by when that store has completed, so the wait the compiler places
+      // before the overwrite costs nothing inside the layer loop.
       constexpr int HPOST = 3;
-      constexpr int HPW = R < 64 ? 64 : R;  // the last HPW threads post h
       u64 hpost[HPOST];
 #pragma unroll
       for (int l = 0; l < HPOST; ++l) hpost[l] = 0;
+      auto post_h = [&](int l, int j, int row, float h) __attribute__((always_inline)) {
+        // an opaque row index keeps the compiler from hoisting one 64-bit address per layer out
+        // of the step loop (they would not fit in registers)
+        asm volatile("" : "+v"(row));
+        hpost[l % HPOST] = pack(h, tag);
+        stw(mbs + g.off_h + ((size_t)j * 2 + par) * R + row, hpost[l % HPOST]);
+      };
+      // x of this CU's last layer -> the next chain CU, posted by the lanes that computed it
+      const bool handoff = c + 1 < g.nch;
+      auto post_x = [&](int row, float v) __attribute__((always_inline)) {
+        if (handoff) stw(mbs + g.off_x + ((size_t)(c + 1) * 2 + par) * R + row, pack(v, tag));
+      };
 #pragma unroll
       for (int l = 0; l < NLC; ++l) {
         if (l < nl) {
           const int j = j0 + l;
+          if (j == L - 1 && tid < R) xbuf[l * R + tid] = xs[tid];
           // a = W_cur x + pre ; h = tanh(a[0:R]) * sigmoid(a[R:2R]).  Each lane ends with both rows
           // of a pair; the first lane of a group starts its partial sums from pre, so pre joins
           // the reduction.
@@ -505,7 +518,11 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
             ah = gsum4(ah);
             ag = gsum4(ag);
             const float h = tanh_nl<AX>(ah) * sigmoid_nl<AX>(ag);
-            if ((li & 3) == 0) hs[2 * gq + (upper ? 1 : 0)] = h;
+            if ((li & 3) == 0) {
+              int hr = 2 * gq + (upper ? 1 : 0);
+              hs[hr] = h;
+              post_h(l, j, hr, h);
+            }
           } else {
             float sh0 = 0.f, sh1 = 0.f, sg0 = 0.f, sg1 = 0.f;
             if (kq == 0) {
@@ -540,14 +557,22 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
             const float ah = gsum<M::LPRG>(sh0 + sh1);
             const float ag = gsum<M::LPRG>(sg0 + sg1);
             const float h = tanh_nl<AX>(ah) * sigmoid_nl<AX>(ag);
-            if (kq == 0) hs[g1] = h;
+            if (kq == 0) {
+              hs[g1] = h;
+              post_h(l, j, g1, h);
+            }
           }
           lds_barrier();
           // x_j = x_{j-1} + W_res h + B_res (x_l feeds nothing); x_{j-1} is kept for the history
           if (j < L - 1) {
             if constexpr (M::G8) {
-              // lower four lanes: row 2q, upper four: row 2q + 1
-              float r0 = 0.f, r1 = 0.f;
+              // lower four lanes: row 2q, upper four: row 2q + 1.  x_{j-1} + B_res of the row joins
+              // the reduction through lane 0 (row 2q) and lane 4 (row 2q + 1); every lane reads
+              // it, so the read is issued with those of h rather than after the reduction
+              const int row = 2 * gq + (upper ? 1 : 0);
+              const float xo = xs[row];
+              const float c0 = (li & 3) == 0 ? xo + bres[l * R + row] : 0.f;
+              float r0 = upper ? 0.f : c0, r1 = upper ? c0 : 0.f;
               if (wres_lds) {
                 const float* w0 = wres + (l * R + 2 * gq) * WRS;
 #pragma unroll
@@ -571,36 +596,27 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
                 }
               }
               const float r = gsum4(xsplit8_1(r0, r1, upper));
-              const int row = 2 * gq + (upper ? 1 : 0);
               if ((li & 3) == 0) {
-                const float xo = xs[row];
                 xbuf[l * R + row] = xo;
-                xs[row] = xo + r + bres[l * R + row];
+                xs[row] = r;
+                if (l == nl - 1) post_x(row, r);
               }
             } else {
-              const float xo = xs[row2], bo = bres[l * R + row2];
-              const float r = gsum<M::LPR2>(dot_lds<M::KC2>(wr[l < NWR ? l : 0], hs + kk * M::KC2));
+              // x_{j-1} + B_res joins the reduction through lane kk = 0 (read by every lane, so
+              // it is issued with the reads of h)
+              const float xo = xs[row2];
+              const float c0 = kk == 0 ? xo + bres[l * R + row2] : 0.f;
+              const float r = gsum<M::LPR2>(dot_lds<M::KC2>(wr[l < NWR ? l : 0], hs + kk * M::KC2, c0));
               if (kk == 0) {
                 xbuf[l * R + row2] = xo;
-                xs[row2] = xo + r + bo;
+                xs[row2] = r;
+                if (l == nl - 1) post_x(row2, r);
               }
             }
-          } else if (tid < R) {
-            xbuf[l * R + tid] = xs[tid];
+            lds_barrier();
           }
-          // h_j[t] -> layer j's aux CU (skip projection), after this wave's share of the residual
-          // product so that its LDS read does not hold up the barrier below
-          {
-            // an opaque index keeps the compiler from hoisting one 64-bit address per layer
-            // out of the step loop (they would not fit in registers)
-            int ln = tid - (NT - HPW);
-            asm volatile("" : "+v"(ln));
-            if (ln >= 0 && ln < R) {
-              hpost[l % HPOST] = pack(hs[ln], tag);
-              stw(mbs + g.off_h + ((size_t)j * 2 + par) * R + ln, hpost[l % HPOST]);
-            }
-          }
-          lds_barrier();
+          // the network's last layer has no residual (x_l feeds nothing): its x_{j-1} went to
+          // xbuf before the first barrier, and the skip projection below reads h
         }
       }
       // The last chain CU adds the skip projection of the last layer itself (its W_skip is in
@@ -625,19 +641,12 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
         const int ks = (RPG == 4) ? (li & 1) : (li & 3);  // lanes holding the same row: post once
         if (ks == 0) stw(mbs + g.off_qtail + (size_t)par * S + m, pack(q, tag));
       }
-      // Then, one or two words per lane: x for the next chain CU, and x_{j-1} into the history
-      // slot (t mod d_j) that layer j's aux CU reads again at t + d_j.
-      {
-        const int nx = (c + 1 < g.nch) ? R : 0;
-        for (int k0 = tid; k0 < nx + nl * R; k0 += NT) {
-          if (k0 < nx) {
-            stw(mbs + g.off_x + ((size_t)(c + 1) * 2 + par) * R + k0, pack(xs[k0], tag));
-          } else {
-            const int k = k0 - nx, l = k / R, e = k % R;
-            const int slot = slotv[par * NLCP + l];
-            stw(rings + lhoff[l] + (size_t)slot * R + e, pack(xbuf[l * R + e], tag));
-          }
-        }
+      // Then x_{j-1} of each layer into the history slot (t mod d_j) that layer j's aux CU reads
+      // again at t + d_j (the next chain CU's x went out in the last layer).
+      for (int k = tid; k < nl * R; k += NT) {
+        const int l = k / R, e = k % R;
+        const int slot = slotv[par * NLCP + l];
+        stw(rings + lhoff[l] + (size_t)slot * R + e, pack(xbuf[l * R + e], tag));
       }
 #pragma unroll
       for (int l = 0; l < HPOST; ++l) asm volatile("" ::"v"(hpost[l]));
