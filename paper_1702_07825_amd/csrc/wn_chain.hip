@@ -60,7 +60,6 @@ constexpr int NT = 512;
 constexpr int A = WN_A;
 constexpr int NHEAD = 4;
 constexpr int HR = A / NHEAD;  // z_a rows per head CU
-constexpr int UB = 512;        // per-step host inputs / outputs staged in LDS
 
 typedef unsigned long long u64;
 
@@ -365,7 +364,10 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
   // One wave sums the head's partial logits of global step ts of local stream i (lane l owns
   // logits 4l..4l+3), writes them out when teacher forcing, and draws (generation) or reads
   // (teacher forcing) the sample.
-  auto sample_step = [&](int64_t ts, int i) {
+  // With r <= 64 (and the second embedding table, if any, in LDS) the drawing wave also forms the
+  // next step's x0 = E[y] + B_embed (+ ep = E_prev[y_{t-2}]) from the sample in its registers.
+  constexpr bool X0W = R <= 64 && (!E2 || E2L);
+  auto sample_step = [&](int64_t ts, int i, float ep) {
     if (wave == 0) {
       float4 lv = bout4;
 #pragma unroll
@@ -389,6 +391,12 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
         if constexpr (E2) syv2[i] = syv[i];
         syv[i] = y;
         ybuf[at] = y;
+      }
+      if constexpr (X0W) {
+        if (lane < R) {
+          if constexpr (E2) xs[lane] = emb[y * R + lane] + bemb + ep;
+          else xs[lane] = emb[y * R + lane] + bemb;
+        }
       }
     }
   };
@@ -437,20 +445,24 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
             asm volatile("" : "+v"(ep));
           }
         }
+        bool x0_done = false;
         if (t > tg0) {
           poll2(g, logit_items(t - 1, b), pre_items, dyn, sy);
           lds_barrier();
           if (sy.failed()) return;
           if (i == 0 && t - 1 - ub0 >= ub) roll_buffers(t - 1);
-          sample_step(t - 1, i);
+          sample_step(t - 1, i, ep);
+          x0_done = X0W;
         } else {
           poll2(g, pre_items, no_items(), dyn, sy);
         }
-        lds_barrier();
-        if (sy.failed()) return;
-        if (tid < R) {
-          if constexpr (E2) xs[tid] = emb[syv[i] * R + tid] + bemb + ep;
-          else xs[tid] = emb[syv[i] * R + tid] + bemb;
+        if (!x0_done) {
+          lds_barrier();
+          if (sy.failed()) return;
+          if (tid < R) {
+            if constexpr (E2) xs[tid] = emb[syv[i] * R + tid] + bemb + ep;
+            else xs[tid] = emb[syv[i] * R + tid] + bemb;
+          }
         }
       } else {
         poll2(g, pre_items, Items{mbs + g.off_x + ((size_t)c * 2 + par) * R, R, R, R, xs, tag}, dyn, sy);
@@ -660,7 +672,7 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
         lds_barrier();
         if (sy.failed()) return;
         if (i == 0 && tl - ub0 >= ub) roll_buffers(tl);
-        sample_step(tl, i);
+        sample_step(tl, i, 0.f);
         lds_barrier();
       }
       roll_buffers(tg0 + T);
