@@ -529,7 +529,7 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
             xsplit8_2(p[0][0] + p[0][1], p[1][0] + p[1][1], p[2][0] + p[2][1], p[3][0] + p[3][1], upper, ah, ag);
             ah = gsum4(ah);
             ag = gsum4(ag);
-            const float h = tanh_nl<AX>(ah) * sigmoid_nl<AX>(ag);
+            const float h = gate_nl<AX>(ah, ag, lane);  // lane pairs share (ah, ag)
             if ((li & 3) == 0) {
               int hr = 2 * gq + (upper ? 1 : 0);
               hs[hr] = h;
@@ -568,7 +568,7 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
             }
             const float ah = gsum<M::LPRG>(sh0 + sh1);
             const float ag = gsum<M::LPRG>(sg0 + sg1);
-            const float h = tanh_nl<AX>(ah) * sigmoid_nl<AX>(ag);
+            const float h = gate_nl<AX>(ah, ag, lane);  // lane pairs share (ah, ag)
             if (kq == 0) {
               hs[g1] = h;
               post_h(l, j, g1, h);

@@ -122,10 +122,26 @@ __device__ __forceinline__ float exp_paper(float x) {
   const unsigned bits = ((unsigned)((int)fl + 126) << 23) + (unsigned)((z + g) * 8388608.0f);
   return __uint_as_float(bits);
 }
+// h = tanh(ah) * sigmoid(ag) for a pair of lanes (2k, 2k + 1) that hold the same ah and ag: the
+// even lane evaluates the tanh and the odd one the sigmoid, one exp2 and one reciprocal each (so a
+// wave issues two quarter-rate transcendental instructions rather than four), and the two meet
+// through a DPP swap; both lanes return h.  The formulas are tanh_f's and sigmoid_f's and the
+// product is the same, so the result is bit for bit that of tanh_f(ah) * sigmoid_f(ag).
+__device__ __forceinline__ float gate_pair(float ah, float ag, int lane) {
+  const bool even = (lane & 1) == 0;
+  const float r = __builtin_amdgcn_rcpf(1.0f + expf_fast(even ? 2.0f * ah : -ag));
+  const float v = even ? 1.0f - 2.0f * r : r;
+  const float o = dpp<0xB1>(v);
+  return even ? v * o : o * v;
+}
 // Exact (AX = false) or approximate (AX = true) nonlinearities.
 template <bool AX> __device__ __forceinline__ float tanh_nl(float v) { return AX ? tanh_paper(v) : tanh_f(v); }
 template <bool AX> __device__ __forceinline__ float sigmoid_nl(float v) { return AX ? sigmoid_paper(v) : sigmoid_f(v); }
 template <bool AX> __device__ __forceinline__ float exp_nl(float v) { return AX ? exp_paper(v) : expf_fast(v); }
+template <bool AX> __device__ __forceinline__ float gate_nl(float ah, float ag, int lane) {
+  if constexpr (AX) return tanh_paper(ah) * sigmoid_paper(ag);
+  else return gate_pair(ah, ag, lane);
+}
 
 // Sum over the 64 lanes of a wave (every lane gets it).
 __device__ __forceinline__ float wave_sum(float v) {
