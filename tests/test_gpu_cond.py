@@ -136,3 +136,29 @@ def test_conditioning_argument_checks():
     with pytest.raises(wn.WnError):
         net(x, 10, workspace=small)
     net.close()
+
+
+def test_full_size_sampled():
+    """The benchmark's batch (256 utterances of 512 frames -> 32000 audio steps each, 84 GB of
+    output) in the launch the benchmark times; sampled streams and steps against the oracle."""
+    wn = _wn()
+    wl = synth.COND_WORKLOADS["cond_l20_r64_b256"]
+    w = synth.make_cond_weights(wl.n_features, wl.h1, wl.n_layers * wl.r, seed=0)
+    x = synth.make_features(wl.B, wl.n_frames, seed=0)
+    net = wn.Conditioner(w, wl.n_layers, wl.r, wl.frame_rate, wl.audio_rate)
+    xd = torch.tensor(x, device="cuda")
+    cond = net(xd, wl.T)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(0)
+    streams = [0, wl.B // 2, wl.B - 1]
+    steps = np.unique(np.concatenate([[0, wl.T - 1], rng.integers(0, wl.T, 30)]))
+    got = {b: cond[b, torch.tensor(steps, device="cuda")].cpu().numpy().reshape(len(steps), -1) for b in streams}
+    del cond
+    torch.cuda.empty_cache()
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(max_workers=3) as ex:
+        refs = list(ex.map(lambda b: oracle.condition(w, x[b], wl.T, wl.frame_rate, wl.audio_rate)[steps], streams))
+    worst = max(float(np.abs(got[b] - ref).max()) for b, ref in zip(streams, refs))
+    print("  full size: %d streams x %d steps, max|dcond| = %.3g" % (len(streams), len(steps), worst), flush=True)
+    assert worst <= TOL
+    net.close()
