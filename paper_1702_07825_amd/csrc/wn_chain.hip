@@ -99,8 +99,10 @@ __device__ __forceinline__ Items no_items() { return Items{nullptr, 1, 0, 0, nul
 // owned loads are in flight together.  A thread that times out, or sees a nonzero status word, sets the
 // block's abort flag and stops waiting.  Every polled word lies in the workspace's tagged region,
 // which starts at g.ring; items are tracked as 32-bit word offsets from there.
+// With acc != nullptr the thread also adds the values of its items to *acc, in item order.
 template <int K = 4>
-__device__ void poll2(const WnChainArgs& g, const Items a, const Items b, float* lds, Sync s) {
+__device__ void poll2(const WnChainArgs& g, const Items a, const Items b, float* lds, Sync s,
+                      float* acc = nullptr) {
   const int n = a.n + b.n;
   const u64* wbase = g.ring;
   for (int base = threadIdx.x; base < n; base += K * NT) {
@@ -133,7 +135,14 @@ __device__ void poll2(const WnChainArgs& g, const Items a, const Items b, float*
           }
         }
       }
-      if (!pend) break;
+      if (!pend) {
+        if (acc) {
+#pragma unroll
+          for (int k = 0; k < K; ++k)
+            if (base + k * NT < n) *acc += wval(w[k]);
+        }
+        break;
+      }
       if (++spins > g.spin_limit || ((spins & 63) == 0 && ld_status(g.status) != 0)) {
         if (ld_status(g.status) == 0) atomicCAS(g.status, 0, (int)WN_ETIMEOUT);
         *s.flag = 1;
@@ -807,6 +816,8 @@ __device__ void head_role(const WnChainArgs& g, const int hh, const int b0, cons
   float* qall = dyn;           // L*S skip partials of one step: layers 0..nq-1, then the tail
   float* zs = qall + L * S;    // S
   float* za = zs + S;          // HR
+  float* qpart = za + HR;      // NT per-thread partial sums
+  static_assert(NT % S == 0, "a thread's skip items share one channel");
 
   const int rl = tid / LPRH, kr = tid % LPRH;
   const int oo = tid / LPRO, ko = tid % LPRO;
@@ -826,16 +837,22 @@ __device__ void head_role(const WnChainArgs& g, const int hh, const int b0, cons
     for (int i = 0; i < ns; ++i) {
       u64* const mbs = g.mb + (size_t)(b0 + i) * g.mb_words;
       // all skip partials of this step: W_skip_j h_j from the aux CUs and (when the last chain
-      // CU computes it) the last layer's
+      // CU computes it) the last layer's.  Item i is channel i mod S of layer i / S and the
+      // thread of item i is i mod NT, so thread tid polls channel tid mod S of every (NT / S)-th
+      // layer and sums those as they arrive; the NT / S partial sums of a channel then meet in
+      // LDS, in a fixed order.
+      float part = 0.f;
       poll2<12>(g, Items{mbs + g.off_q + (size_t)par * S, S, 2 * S, nq * S, qall, tag},
-            nq < L ? Items{mbs + g.off_qtail + (size_t)par * S, S, S, S, qall + (L - 1) * S, tag} : no_items(), dyn,
-            sy);
+                nq < L ? Items{mbs + g.off_qtail + (size_t)par * S, S, S, S, qall + (L - 1) * S, tag} : no_items(),
+                dyn, sy, &part);
+      qpart[tid] = part;
       lds_barrier();
       if (sy.failed()) return;
-      // z_s = relu(B_skip + sum_j q_j), summed in layer order
+      // z_s = relu(B_skip + sum_j q_j)
       if (tid < S) {
         float q = bsk;
-        for (int j = 0; j < L; ++j) q += qall[j * S + tid];
+#pragma unroll
+        for (int p = 0; p < NT / S; ++p) q += qpart[p * S + tid];
         zs[tid] = fmaxf(q, 0.f);
       }
       lds_barrier();
@@ -926,7 +943,7 @@ size_t chain_lds_floats(int R, int S, int nlc, int G, int ub, int nch, int tail,
   if (R == 128) var = std::max(var, (size_t)2 * R * lds_row_stride(R, 2));
   return common + var;
 }
-size_t head_lds_floats(int L, int S) { return (size_t)L * S + S + HR; }
+size_t head_lds_floats(int L, int S) { return (size_t)L * S + S + HR + NT; }
 size_t aux_lds_floats(int R, int G) { return (size_t)R + (size_t)3 * R * G; }
 constexpr size_t kMaxLds = 160 * 1024;
 
