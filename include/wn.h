@@ -187,7 +187,11 @@ int wn_teacher_force(wn_handle* h, int32_t B, int32_t T, const float* cond, cons
 /*
  * Wait for `stream` and return the status word the kernels left in `workspace`:
  * WN_OK, WN_ETIMEOUT or WN_EABORTED; WN_EINVAL for null arguments; WN_EHIP if
- * the stream reports an error.  Blocks the calling thread.
+ * the stream reports an error.  Blocks the calling thread.  The multi-CU kernel's
+ * waits for other CUs give up after a bounded number of polls (a few seconds);
+ * the environment variable WN_SPIN_LIMIT, read at each call, sets that number
+ * (tests force the timeout path with it).  After WN_ETIMEOUT the workspace state
+ * is stale: the next call must pass reset = 1.
  */
 int wn_status(wn_handle* h, const void* workspace, void* stream);
 

@@ -184,7 +184,13 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
     g.off_qtail = plan.off_qtail;
     g.nch = plan.nch;
     for (int c = 0; c <= plan.nch; ++c) g.layer_begin[c] = plan.layer_begin[c];
+    // polls before a wait gives up (seconds of spinning); WN_SPIN_LIMIT overrides it so that tests
+    // can force the timeout path from the host
     g.spin_limit = 1 << 22;
+    if (const char* sl = std::getenv("WN_SPIN_LIMIT")) {
+      const long v = std::strtol(sl, nullptr, 10);
+      if (v > 0 && v < (1L << 30)) g.spin_limit = (int)v;
+    }
     g.nrep = plan.nrep;
     g.G = plan.G;
     g.ub = plan.ub;

@@ -116,3 +116,28 @@ def test_multi_stream_chain_matches_per_stream_kernel(monkeypatch):
     assert d <= 1e-4
     ref.close()
     net.close()
+
+
+def test_timeout_path_drains_and_recovers(monkeypatch):
+    """Every wait of the multi-CU kernel is bounded.  With the host's spin limit forced to one
+    poll, a launch must end with WN_ETIMEOUT in the status word (every block leaves, so the call
+    returns), and the next call that starts from zero on the same workspace must run cleanly."""
+    import paper_1702_07825_amd as wn
+    L, r, s, dil, B, T = 20, 64, 256, tuple(synth.dilation_cycle(20)), 2, 50
+    w, net, cond, u, model = _setup(L, r, s, dil, B, T, seed=77, bias=0.1)
+    assert net.kernel_variant(B) == "multi_cu_chain"
+    ws = net.new_workspace(B)
+    monkeypatch.setenv("WN_SPIN_LIMIT", "1")
+    print("forced timeout run", flush=True)
+    net.generate(cond, u, workspace=ws)
+    assert net.status(ws) == wn.WN_ETIMEOUT
+    monkeypatch.delenv("WN_SPIN_LIMIT")
+    y = net.generate(cond, u, workspace=ws, reset=True)
+    assert net.status(ws) == 0
+    lg = net.teacher_force(cond, y)
+    torch.cuda.synchronize()
+    ys, lo, mg = oracle.run_streams(model, cond.cpu().numpy(), u=u.cpu().numpy(), y_in=y.cpu().numpy(), threads=8)
+    assert float(np.abs(lg.cpu().numpy() - lo).max()) <= 1e-3
+    ok = mg > MARGIN
+    assert np.array_equal(ys[ok], y.cpu().numpy()[ok])
+    net.close()
