@@ -27,6 +27,10 @@ PEAKS = {  # MI355X published dense peaks
     "bf16_mfma_tflops": 2500.0,
     "hbm_gbs": 8000.0,
 }
+# Measured on one MI355X with a b128 LDS read loop over all 256 CUs: 53.0 TB/s at a shader clock of
+# 2.394 GHz, i.e. 86.4 bytes per clock per CU.
+LDS_BYTES_PER_CLK_PER_CU = 86.4
+SHADER_CLOCK_GHZ = 2.394
 RATE_HZ = 16000
 PAPER_RATE_HZ = 16384
 HI_RATE_HZ = 48000  # the paper's 48 kHz case: a 20 us per-sample budget (Section 5)
@@ -142,6 +146,18 @@ def run_workload(name, args):
     achieved = flop_per_launch / avg_launch_s / 1e12
     per_stream_rate = wl.T / avg_launch_s
     hbm_alg = algorithmic_hbm_bytes_per_sample(wl) * n
+    onchip = None
+    if variant == "multi_cu_chain":
+        # Every weight of a replica is read once per step from the LDS/VGPRs of the CUs holding it;
+        # the floor is those bytes at the measured LDS rate of the CUs the launch occupies.
+        wgs, reps = net.launch_info(wl.B)
+        wbytes = 4.0 * macs_per_sample(wl.n_layers, wl.r, wl.s) * reps * wl.T
+        lds_gbs = wgs * LDS_BYTES_PER_CLK_PER_CU * SHADER_CLOCK_GHZ
+        onchip = {"bound": "lds", "weight_bytes_per_launch": wbytes, "workgroups": wgs, "replicas": reps,
+                  "achieved_gbs": round(wbytes / avg_launch_s / 1e9, 2), "peak_gbs": round(lds_gbs, 1),
+                  "peak_basis": "%.1f B/clk/CU measured x %.3f GHz x workgroups" % (LDS_BYTES_PER_CLK_PER_CU,
+                                                                                   SHADER_CLOCK_GHZ),
+                  "frac": round(wbytes / avg_launch_s / 1e9 / lds_gbs, 6)}
     y = samples.cpu().numpy()
     out = {
         "metric": "generated samples/s (16 kHz mu-law audio, all streams)",
@@ -175,6 +191,7 @@ def run_workload(name, args):
                     "achieved_gbs": round(hbm_alg / avg_launch_s / 1e9, 2),
                     "peak_gbs": PEAKS["hbm_gbs"],
                     "frac": round(hbm_alg / avg_launch_s / 1e9 / PEAKS["hbm_gbs"], 6)},
+            "onchip": onchip,
             "avg_launch_ms": round(avg_launch_s * 1e3, 4),
         },
         "sample_histogram_entropy_bits": round(float(-(lambda p: (p[p > 0] * np.log2(p[p > 0])).sum())(

@@ -198,6 +198,11 @@ int wn_status(wn_handle* h, const void* workspace, void* stream);
 /* Name of the kernel family that calls with B streams use (for reports). */
 const char* wn_kernel_variant(const wn_handle* h, int32_t B);
 
+/* For reports: the workgroups (one per CU) a call with B streams launches, and how many
+ * independent copies of the model they form (multi-CU kernel: replicas; the others: one per
+ * workgroup).  WN_EINVAL for a null handle or pointer or B < 1. */
+int wn_launch_info(const wn_handle* h, int32_t B, int32_t* workgroups, int32_t* replicas);
+
 /* Free the handle's device weights.  Null is allowed.  No call may be in flight. */
 void wn_destroy(wn_handle* h);
 

@@ -23,7 +23,7 @@ WN_F32, WN_BF16 = 0, 1
 WN_NONLIN_EXACT, WN_NONLIN_PAPER = 0, 1
 A_CLASSES = 256
 EXPORTED = ("wn_create", "wn_workspace_bytes", "wn_generate", "wn_generate_sampled", "wn_teacher_force", "wn_status",
-            "wn_kernel_variant", "wn_destroy", "wn_error_string", "wn_last_error",
+            "wn_kernel_variant", "wn_launch_info", "wn_destroy", "wn_error_string", "wn_last_error",
             "wn_cond_create", "wn_cond_workspace_bytes", "wn_condition", "wn_cond_destroy")
 # wn_sample_mode_t: how a step's distribution becomes its sample
 SAMPLE_DIRECT, SAMPLE_TEMPERATURE, SAMPLE_TOPK, SAMPLE_MODE, SAMPLE_MEAN = 0, 1, 2, 3, 4
@@ -97,6 +97,8 @@ def load_library(path: str = LIB_PATH):
         L.wn_status.argtypes = [vp, vp, vp]
         L.wn_kernel_variant.restype = ctypes.c_char_p
         L.wn_kernel_variant.argtypes = [vp, i32]
+        L.wn_launch_info.restype = ctypes.c_int
+        L.wn_launch_info.argtypes = [vp, i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
         L.wn_destroy.restype = None
         L.wn_destroy.argtypes = [vp]
         L.wn_error_string.restype = ctypes.c_char_p
@@ -189,6 +191,12 @@ class WaveNet:
 
     def kernel_variant(self, B: int) -> str:
         return self._lib.wn_kernel_variant(self._h, int(B)).decode()
+
+    def launch_info(self, B: int):
+        """(workgroups, replicas) a call with B streams launches (see wn_launch_info)."""
+        wg, rep = ctypes.c_int32(0), ctypes.c_int32(0)
+        _check(self._lib.wn_launch_info(self._h, int(B), ctypes.byref(wg), ctypes.byref(rep)), "wn_launch_info")
+        return int(wg.value), int(rep.value)
 
     def generate(self, cond, uniforms, samples=None, workspace=None, reset: bool = True, stream=None, sampler=None):
         """cond fp32 [B,T,l,2r], uniforms fp32 [B,T] (device) -> samples int32 [B,T].

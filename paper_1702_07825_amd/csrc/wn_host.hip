@@ -441,6 +441,24 @@ const char* wn_kernel_variant(const wn_handle* h, int32_t B) {
   }
 }
 
+int wn_launch_info(const wn_handle* h, int32_t B, int32_t* workgroups, int32_t* replicas) {
+  if (!h || B < 1 || !workgroups || !replicas) return WN_EINVAL;
+  WnChainPlan p;
+  if (chain_plan_for(h, B, &p)) {
+    int used = 0;
+    for (int b = 0; b < WN_CHAIN_GRID; ++b) used += p.role_of_block[b] != 0xffff;
+    *workgroups = used;
+    *replicas = p.nrep;
+  } else if (h->group_ok) {
+    *workgroups = (B + 15) / 16;
+    *replicas = *workgroups;
+  } else {
+    *workgroups = B;
+    *replicas = B;
+  }
+  return WN_OK;
+}
+
 void wn_destroy(wn_handle* h) {
   if (!h) return;
   {

@@ -88,6 +88,9 @@ def test_null_arguments(lib):
     assert lib.wn_teacher_force(None, 1, 1, None, None, None, None, 0, 1, None) == -1
     assert lib.wn_status(None, None, None) == -1
     assert lib.wn_kernel_variant(None, 1) == b""
+    wg, rep = ctypes.c_int32(7), ctypes.c_int32(7)
+    assert lib.wn_launch_info(None, 1, ctypes.byref(wg), ctypes.byref(rep)) == -1
+    assert (wg.value, rep.value) == (7, 7)
     lib.wn_destroy(None)
 
 

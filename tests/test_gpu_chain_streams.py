@@ -46,12 +46,22 @@ CASES = [
 ]
 
 
+# (workgroups, replicas) wn_launch_info reports where the layout is stated above
+LAUNCH = {"l20_r128_b11": (None, 4), "l20_r64_b12": (None, 6), "l3_r128_b5": (None, 5), "l9_r32_b40": (None, 14),
+          "l20_r64_b144": (243, 9), "l64_r64_b1": (None, 1)}
+
+
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_multi_stream_chain_parity(case):
     name, L, r, s, dil, B, T, bias = case
     print("case %s: L=%d r=%d s=%d B=%d T=%d" % (name, L, r, s, B, T), flush=True)
     w, net, cond, u, model = _setup(L, r, s, dil, B, T, seed=zlib.crc32(name.encode()) % 1000, bias=bias)
     assert net.kernel_variant(B) == "multi_cu_chain"
+    wgs, reps = net.launch_info(B)
+    assert 1 <= reps <= wgs <= 256 and -(-B // reps) <= 16
+    want_wgs, want_reps = LAUNCH.get(name, (None, None))
+    assert want_reps is None or reps == want_reps
+    assert want_wgs is None or wgs == want_wgs
     ws = net.new_workspace(B)
     y = net.generate(cond, u, workspace=ws)
     lg = net.teacher_force(cond, y)
