@@ -32,23 +32,24 @@ def _setup(L, r, s, dil, B, T, seed, bias=0.0):
 
 
 CASES = [
-    # name, L, r, s, dilations, B, T, bias  (replicas x streams per replica in the comment)
-    ("l20_r128_b11", 20, 128, 256, tuple(synth.dilation_cycle(20)), 11, 300, 0.2),  # 4 x 3 (last 2)
-    ("l20_r64_b12", 20, 64, 256, tuple(synth.dilation_cycle(20)), 12, 300, 0.0),    # 6 x 2
-    ("l3_r128_b5", 3, 128, 256, (1, 3, 2), 5, 200, 0.3),                             # 5 x 1
+    # name, L, r, s, dilations, B, T, bias
+    # (replicas x streams per replica; a replica is nch chain + 4 head + L aux CUs)
+    ("l20_r128_b11", 20, 128, 256, tuple(synth.dilation_cycle(20)), 11, 300, 0.2),  # 6 x 2 (last 1), 35 CUs each
+    ("l20_r64_b12", 20, 64, 256, tuple(synth.dilation_cycle(20)), 12, 300, 0.0),    # 6 x 2, 27 CUs each
+    ("l3_r128_b5", 3, 128, 256, (1, 3, 2), 5, 200, 0.3),                             # 5 x 1, 10 CUs each
     ("l1_r128_b2", 1, 128, 256, (1,), 2, 150, 0.4),                                  # one chain CU, skip on aux
     ("l5_r128_b3", 5, 128, 256, (2, 1, 4, 1, 3), 3, 200, 0.3),                      # chain CUs of 1, 2, 1, 1 layers
-    ("l9_r32_b40", 9, 32, 128, (1, 2, 4, 8, 16, 32, 64, 128, 256), 40, 200, 0.2),    # 14 x 3 (last 1)
+    ("l9_r32_b40", 9, 32, 128, (1, 2, 4, 8, 16, 32, 64, 128, 256), 40, 200, 0.2),    # 14 x 3 (last 1), 14 CUs each
     # the largest batch one launch serves at l = 20, r = 64: 9 replicas of 27 CUs, 16 streams each
     ("l20_r64_b144", 20, 64, 256, tuple(synth.dilation_cycle(20)), 144, 40, 0.1),
-    # the most layers the library takes
+    # the most layers the library takes: 10 chain CUs of up to 7 layers
     ("l64_r64_b1", 64, 64, 256, tuple(synth.dilation_cycle(64)), 1, 120, 0.1),
 ]
 
 
-# (workgroups, replicas) wn_launch_info reports where the layout is stated above
-LAUNCH = {"l20_r128_b11": (None, 4), "l20_r64_b12": (None, 6), "l3_r128_b5": (None, 5), "l9_r32_b40": (None, 14),
-          "l20_r64_b144": (243, 9), "l64_r64_b1": (None, 1)}
+# (workgroups, replicas) wn_launch_info reports for the layouts stated above
+LAUNCH = {"l20_r128_b11": (210, 6), "l20_r64_b12": (162, 6), "l3_r128_b5": (50, 5), "l1_r128_b2": (12, 2),
+          "l5_r128_b3": (39, 3), "l9_r32_b40": (196, 14), "l20_r64_b144": (243, 9), "l64_r64_b1": (78, 1)}
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
@@ -59,9 +60,7 @@ def test_multi_stream_chain_parity(case):
     assert net.kernel_variant(B) == "multi_cu_chain"
     wgs, reps = net.launch_info(B)
     assert 1 <= reps <= wgs <= 256 and -(-B // reps) <= 16
-    want_wgs, want_reps = LAUNCH.get(name, (None, None))
-    assert want_reps is None or reps == want_reps
-    assert want_wgs is None or wgs == want_wgs
+    assert (wgs, reps) == LAUNCH[name]
     ws = net.new_workspace(B)
     y = net.generate(cond, u, workspace=ws)
     lg = net.teacher_force(cond, y)
