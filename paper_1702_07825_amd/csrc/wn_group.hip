@@ -31,6 +31,7 @@
 #include "wn_internal.h"
 #include "wn_wave.h"
 
+#include <cstdlib>
 #include <cstring>
 #include <type_traits>
 
@@ -39,7 +40,7 @@ namespace {
 using namespace wnk;
 
 constexpr int NT = 512;
-constexpr int G = 16;  // streams per workgroup (the MFMA N dimension)
+constexpr int G = 16;  // MFMA N dimension: columns of a workgroup's products (g.gs <= G of them are streams)
 constexpr int R = 64;  // residual channels
 constexpr int A = WN_A;
 constexpr int PC = 2 * R + 4;  // fp32 row pitches in LDS
@@ -116,7 +117,7 @@ constexpr size_t lds_bytes(int L) {
          2 * ((size_t)5 * G * SR + (size_t)G * Pack<S>::SS + (size_t)G * SA + (size_t)A * R + (size_t)G * R);
 }
 
-template <int S, bool TF, bool AX>
+template <int S, bool TF, bool AX, int GS>
 __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
   using P = Pack<S>;
   constexpr int SS = P::SS;
@@ -124,7 +125,8 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
   const int L = D.L;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: tile addresses go to SGPRs
-  const int b0 = blockIdx.x * G;
+  constexpr int gs = GS;  // streams of this workgroup: columns 0 .. GS - 1; the others are padding
+  const int b0 = blockIdx.x * gs;
   const int T = g.io.T, B = g.io.B;
   const int n = lane & 15, quad = lane >> 4;  // MFMA column (stream) and row quad of this lane
 
@@ -171,7 +173,7 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
     if (!g.io.reset) tg0 = st[WN_STATE_WORDS * (size_t)b0];
     if (tid < G) {
       int y = g.io.init_sample, y2 = -1;
-      if (!g.io.reset && b0 + tid < B) {
+      if (!g.io.reset && tid < gs && b0 + tid < B) {
         y = (int)st[WN_STATE_WORDS * (size_t)(b0 + tid) + 1];
         y2 = (int)st[WN_STATE_WORDS * (size_t)(b0 + tid) + 2];
       }
@@ -195,12 +197,15 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
     for (int i = tid; i < A * R; i += NT) EMB[i] = E[i];
   }
   if (g.io.reset) {
-    for (int nn = 0; nn < G && b0 + nn < B; ++nn) {
+    for (int nn = 0; nn < gs && b0 + nn < B; ++nn) {
       float4* hist = reinterpret_cast<float4*>(g.ws.hist + (size_t)(b0 + nn) * D.hist_len);
       for (int i = tid; i < D.hist_len / 4; i += NT) hist[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     }
     if (blockIdx.x == 0 && tid == 0) *g.ws.status = 0;
   }
+  // padding columns never receive rows: zero them once (their products then stay finite)
+  for (int i = tid; i < 2 * G * SR; i += NT) XP[i] = 0;
+  for (int i = tid; i < 2 * G * PC; i += NT) CD[i] = 0.f;
   __syncthreads();  // also orders the history zeroing before the loader's reads
   // x0 of the first step; EPB holds E_prev[y_{t-2}] of the step whose x0 is formed next (the
   // loader refreshes it a step ahead)
@@ -450,31 +455,41 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
       }
     });
   } else {
-    // ---------------- loader: lane = stream ldn, quarter ldq of a row ----------------
-    constexpr int NB = 12;  // 4 x 16 B of the history row, 8 x 16 B of the conditioning row
-    const int ldn = lane >> 2, ldq = lane & 3;
-    const int ldb = min(b0 + ldn, B - 1);  // reads of a partial group are clamped
-    const int lub = min(b0 + lane, B - 1);
-    const char* hrd = reinterpret_cast<const char*>(g.ws.hist + (size_t)ldb * D.hist_len) + ldq * 64;
-    const float* crd = g.io.cond + (size_t)ldb * T * L * 2 * R + ldq * 32;
-    // history row x_{j-1}[ts - d_j] (slot s_slot[j], see below) and conditioning row of (tl, j)
+    // ---------------- loader ----------------
+    // The rows of a position for the GS streams: LPS lanes per stream, lane q of a stream reading
+    // 16-byte pieces q, q + LPS, .. of its history row x_{j-1}[t - d_j] (split, 16 pieces) and of
+    // its conditioning row (32 pieces), so each load instruction reads contiguous bytes of every
+    // stream, and a group of fewer streams issues fewer loads.
+    constexpr int LPS = 64 / GS;
+    constexpr int NH = (16 + LPS - 1) / LPS, NC = (32 + LPS - 1) / LPS;
+    constexpr int NB = NH + NC;
+    const int lsn = lane / LPS, lq = lane % LPS;  // stream and lane within it
+    const int ldn = lane >> 2, ldq = lane & 3;    // quarter ldq of stream ldn's E_prev row (two taps)
+    const int lub = min(b0 + lane, B - 1);        // reads of a partial group are clamped
+    const size_t lsb = (size_t)min(b0 + lsn, B - 1);
+    const float* hrd = g.ws.hist + lsb * D.hist_len + lq * 4;
+    const float* crd = g.io.cond + lsb * T * L * 2 * R + lq * 4;
     auto issue = [&](u32x4 (&buf)[NB], int64_t tl, int j) __attribute__((always_inline)) {
       if (tl >= T) return;
       const int hoff = __builtin_amdgcn_readfirstlane(s_hoff[j] + s_slot[j] * R);
-      const u32x4* h = reinterpret_cast<const u32x4*>(hrd + (size_t)hoff * 4);
+      const float* h = hrd + hoff;
+      const float* c = crd + ((size_t)tl * L + j) * 2 * R;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) buf[k] = h[k];
-      const u32x4* c = reinterpret_cast<const u32x4*>(crd + ((size_t)tl * L + j) * 2 * R);
+      for (int k = 0; k < NH; ++k)
+        if (lq + LPS * k < 16) buf[k] = *reinterpret_cast<const u32x4*>(h + 4 * LPS * k);
 #pragma unroll
-      for (int k = 0; k < 8; ++k) buf[4 + k] = c[k];
+      for (int k = 0; k < NC; ++k)
+        if (lq + LPS * k < 32) buf[NH + k] = *reinterpret_cast<const u32x4*>(c + 4 * LPS * k);
     };
     auto store = [&](int slot, const u32x4 (&buf)[NB]) __attribute__((always_inline)) {
-      u32x4* xp = reinterpret_cast<u32x4*>(XP + (slot * G + ldn) * SR) + ldq * 4;
+      u32x4* xp = reinterpret_cast<u32x4*>(XP + (slot * G + lsn) * SR) + lq;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) xp[k] = buf[k];
-      float* cd = CD + (slot * G + ldn) * PC + ldq * 32;
+      for (int k = 0; k < NH; ++k)
+        if (lq + LPS * k < 16) xp[LPS * k] = buf[k];
+      u32x4* cd = reinterpret_cast<u32x4*>(CD + (slot * G + lsn) * PC) + lq;
 #pragma unroll
-      for (int k = 0; k < 8; ++k) reinterpret_cast<u32x4*>(cd)[k] = buf[4 + k];
+      for (int k = 0; k < NC; ++k)
+        if (lq + LPS * k < 32) cd[LPS * k] = buf[NH + k];
     };
     // Samples (generation) or logits (teacher forcing) of step tl, from s_y / LG, for the 16 streams.
     auto write_outputs = [&](int64_t tl) __attribute__((always_inline)) {
@@ -487,10 +502,10 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
           asm volatile("" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]));
 #pragma unroll
           for (int k = 0; k < 4; ++k)
-            if (b0 + c + k < B) reinterpret_cast<f32x4*>(g.io.logits + ((size_t)(b0 + c + k) * T + tl) * A)[lane] = v[k];
+            if (c + k < gs && b0 + c + k < B) reinterpret_cast<f32x4*>(g.io.logits + ((size_t)(b0 + c + k) * T + tl) * A)[lane] = v[k];
         }
       } else {
-        if (lane < G && b0 + lane < B) g.io.y_out[(size_t)(b0 + lane) * T + tl] = s_y[lane];
+        if (lane < gs && b0 + lane < B) g.io.y_out[(size_t)(b0 + lane) * T + tl] = s_y[lane];
       }
     };
     u32x4 bufA[NB], bufB[NB];
@@ -531,17 +546,17 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
         const int slot = __builtin_amdgcn_readfirstlane(s_slot[j]);
         char* hw = reinterpret_cast<char*>(g.ws.hist) + ((size_t)s_hoff[j] + (size_t)slot * R) * 4;
         static_assert(G * 2 * R * 2 / 16 / 64 == 4, "four 16-byte pieces of x per loader lane");
-        f32x4 v[4];
+        f32x4 v[4] = {};
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
           const int i = lane + 64 * k;  // stream i / 16, piece i % 16 of its 256-byte row
-          v[k] = *reinterpret_cast<const f32x4*>(XS + ((j & 1) * G + (i >> 4)) * SR + (i & 15) * 8);
+          if (4 * k < gs) v[k] = *reinterpret_cast<const f32x4*>(XS + ((j & 1) * G + (i >> 4)) * SR + (i & 15) * 8);
         }
         asm volatile("" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]));
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
           const int i = lane + 64 * k, nn = i >> 4;
-          if (b0 + nn < B)
+          if (4 * k < gs && nn < gs && b0 + nn < B)
             *reinterpret_cast<f32x4*>(hw + (size_t)(b0 + nn) * D.hist_len * 4 + (i & 15) * 16) = v[k];
         }
         if (lane == 0) s_slot[j] = slot + 1 == s_dil[j] ? 0 : slot + 1;
@@ -572,7 +587,7 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
     write_outputs(T - 1);  // the last step's, after its draw
   }
   __syncthreads();
-  if (tid < G && b0 + tid < B) {
+  if (tid < gs && b0 + tid < B) {
     int64_t* st = g.ws.state + WN_STATE_WORDS * (size_t)(b0 + tid);
     st[0] = tg0 + T;
     st[1] = s_y[tid];
@@ -580,25 +595,29 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
   }
 }
 
+template <int S, bool TF, bool AX, int GS>
+hipError_t launch_group_k(const WnGroupArgs& g, hipStream_t stream) {
+  const size_t dyn = lds_bytes<S>(g.d.L);
+  const dim3 grid((g.io.B + GS - 1) / GS), block(NT);
+  const void* k = reinterpret_cast<const void*>(wn_group_kernel<S, TF, AX, GS>);
+  const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((wn_group_kernel<S, TF, AX, GS>), grid, block, dyn, stream, g);
+  return hipGetLastError();
+}
+
+template <int S, bool TF, bool AX>
+hipError_t launch_group_gs(const WnGroupArgs& g, hipStream_t stream) {
+  if (g.gs == 8) return launch_group_k<S, TF, AX, 8>(g, stream);
+  if (g.gs == 16) return launch_group_k<S, TF, AX, 16>(g, stream);
+  return hipErrorInvalidValue;
+}
+
 template <int S>
 hipError_t launch_group_s(const WnGroupArgs& g, bool teacher, hipStream_t stream) {
-  const size_t dyn = lds_bytes<S>(g.d.L);
-  const dim3 grid((g.io.B + G - 1) / G), block(NT);
   const bool ax = g.w.approx_nl != 0;
-  const void* k = teacher ? (ax ? reinterpret_cast<const void*>(wn_group_kernel<S, true, true>)
-                                : reinterpret_cast<const void*>(wn_group_kernel<S, true, false>))
-                          : (ax ? reinterpret_cast<const void*>(wn_group_kernel<S, false, true>)
-                                : reinterpret_cast<const void*>(wn_group_kernel<S, false, false>));
-  hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
-  if (e != hipSuccess) return e;
-  if (teacher) {
-    if (ax) hipLaunchKernelGGL((wn_group_kernel<S, true, true>), grid, block, dyn, stream, g);
-    else hipLaunchKernelGGL((wn_group_kernel<S, true, false>), grid, block, dyn, stream, g);
-  } else {
-    if (ax) hipLaunchKernelGGL((wn_group_kernel<S, false, true>), grid, block, dyn, stream, g);
-    else hipLaunchKernelGGL((wn_group_kernel<S, false, false>), grid, block, dyn, stream, g);
-  }
-  return hipGetLastError();
+  if (teacher) return ax ? launch_group_gs<S, true, true>(g, stream) : launch_group_gs<S, true, false>(g, stream);
+  return ax ? launch_group_gs<S, false, true>(g, stream) : launch_group_gs<S, false, false>(g, stream);
 }
 
 // Append W [M][K] (element (m, k) from `at`) as MFMA A tiles: block (mt, kt) holds, for lane i,
@@ -615,6 +634,18 @@ void pack_tiles(std::vector<uint16_t>& out, int M, int K, F at) {
 
 bool wn_group_supported(int R_, int S_, int L) {
   return R_ == R && (S_ == 256 || S_ == 128) && L >= 2 && L <= WN_GROUP_MAX_LAYERS;
+}
+
+// Measured at l = 20, r = 64 (us per step): 16 streams per workgroup 29.0, 8 streams 27.8-29.0,
+// 4 streams 28.2-29.3, one stream 28.5-31.2 (B = 1 .. 1024); eight keep the MFMA columns half
+// busy while the loader wave moves half the rows, and up to 2048 streams still fit one workgroup
+// per CU.
+int wn_group_streams(int B) {
+  if (const char* e = std::getenv("WN_GROUP_STREAMS")) {
+    const int v = std::atoi(e);
+    if (v == 8 || v == 16) return v;
+  }
+  return B <= 8 * WN_CHAIN_GRID ? 8 : 16;
 }
 
 size_t wn_group_lds_bytes(int L, int S_, bool) {

@@ -223,6 +223,7 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
     g.ws.status = reinterpret_cast<int32_t*>(base + l.status_off);
     g.ws.state = reinterpret_cast<int64_t*>(base + l.state_off);
     g.ws.hist = reinterpret_cast<float*>(base + l.hist_off);
+    g.gs = wn_group_streams(B);
     const hipError_t e = wn_group_launch(g, teacher, st);
     if (e != hipSuccess) return hip_fail(e, "batched kernel launch");
     return WN_OK;
@@ -450,7 +451,8 @@ int wn_launch_info(const wn_handle* h, int32_t B, int32_t* workgroups, int32_t* 
     *workgroups = used;
     *replicas = p.nrep;
   } else if (h->group_ok) {
-    *workgroups = (B + 15) / 16;
+    const int gs = wn_group_streams(B);
+    *workgroups = (B + gs - 1) / gs;
     *replicas = *workgroups;
   } else {
     *workgroups = B;

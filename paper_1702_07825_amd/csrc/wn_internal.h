@@ -128,8 +128,12 @@ struct WnGroupArgs {
   const void* packed; // tiles from wn_group_pack, device copy
   WnIO io;
   WnWorkspace ws;     // same layout as the per-stream kernel's
+  int gs;             // streams per workgroup: 8 or 16 (wn_group_streams)
 };
 #define WN_GROUP_MAX_LAYERS 40
+// Streams per workgroup for a call with B streams: 8 while that keeps one workgroup per CU, else
+// 16; the environment variable WN_GROUP_STREAMS (8 or 16) overrides it.
+int wn_group_streams(int B);
 bool wn_group_supported(int R, int S, int L);
 size_t wn_group_lds_bytes(int L, int S, bool two_taps);
 // Packs W_prev/W_cur/W_res/W_skip of every layer and the two head matrices (fp32 host arrays

@@ -3,8 +3,9 @@
 Each case runs through the C ABI and is compared with the CPU oracle in its bf16-weight mode
 (teacher-forced logits within 1e-3, sample indices bit-exact wherever the oracle's CDF margin
 exceeds 1e-4), with the fp32 oracle (2e-2) and with the per-stream kernel on the same inputs.
-Cases cover one stream, full and partial groups of 16, the fewest layers the kernel takes
+Cases cover one stream, full and partial groups, the fewest layers the kernel takes
 (2, dilation 1), s = 128 and 256, dilations longer than the call, and calls split at odd steps.
+A workgroup serves 8 streams (16 beyond 2048 streams); both group sizes give identical results.
 """
 import zlib
 
@@ -96,11 +97,48 @@ def test_group_kernel_parity(case, monkeypatch):
     net.close()
 
 
+@pytest.mark.parametrize("B", [5, 13, 16, 17])
+def test_group_sizes_agree(B, monkeypatch):
+    """8 and 16 streams per workgroup: every column of a product depends only on its own stream,
+    so the samples and logits agree bit for bit, also across a call split at an odd step."""
+    import paper_1702_07825_amd as wn
+    L, dil, T = 6, (1, 2, 4, 8, 1, 3), 90
+    _log("group sizes, B=%d" % B)
+    w = synth.make_weights(L, 64, 256, seed=B, bias_scale=0.2)
+    cond = synth.make_cond(L, 64, B, T, seed=B, device="cuda")
+    u = torch.tensor(synth.make_uniforms(B, T, seed=B), device="cuda")
+    out = {}
+    for gs in (8, 16):
+        monkeypatch.setenv("WN_GROUP_STREAMS", str(gs))
+        net = wn.WaveNet(w, dil, weight_dtype="bf16")
+        assert net.kernel_variant(B) == "mfma_group"
+        assert net.launch_info(B) == (-(-B // gs), -(-B // gs))
+        y = net.generate(cond, u)
+        lg = net.teacher_force(cond, y)
+        ws = net.new_workspace(B)
+        ya = net.generate(cond[:, :41].contiguous(), u[:, :41].contiguous(), workspace=ws, reset=True)
+        yb = net.generate(cond[:, 41:].contiguous(), u[:, 41:].contiguous(), workspace=ws, reset=False)
+        torch.cuda.synchronize()
+        assert net.status(ws) == 0
+        assert torch.equal(torch.cat([ya, yb], 1), y)
+        out[gs] = (y.cpu(), lg.cpu())
+        net.close()
+    assert torch.equal(out[8][0], out[16][0])
+    assert torch.equal(out[8][1], out[16][1])
+    model = oracle.Model(w, dil, bf16_weights=True)
+    ys, lo, mg = oracle.run_streams(model, cond.cpu().numpy(), u=u.cpu().numpy(), y_in=out[8][0].numpy(), threads=8)
+    ok = mg > MARGIN
+    assert float(np.abs(out[8][1].numpy() - lo).max()) <= 1e-3
+    assert int(np.sum(ys[ok] != out[8][0].numpy()[ok])) == 0
+
+
 def test_group_kernel_variant_selection():
     import paper_1702_07825_amd as wn
     w = synth.make_weights(20, 64, 256, seed=2)
     net = wn.WaveNet(w, synth.dilation_cycle(20), weight_dtype="bf16")
     assert [net.kernel_variant(b) for b in (1, 16, 256)] == ["mfma_group"] * 3
+    # 8 streams per workgroup up to 2048 streams (one workgroup per CU), then 16
+    assert [net.launch_info(b) for b in (1, 9, 256, 2048, 2049)] == [(1, 1), (2, 2), (32, 32), (256, 256), (129, 129)]
     net.close()
     # one layer, or r other than 64, stays on the per-stream kernel
     w1 = synth.make_weights(1, 64, 256, seed=2)
