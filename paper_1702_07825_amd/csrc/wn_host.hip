@@ -22,6 +22,7 @@ struct wn_handle {
   WnDims dims{};
   WnDevWeights w{};
   bool chain_ok = false;  // the multi-CU kernel can serve this model (fp32, supported shape)
+  bool xcd_map = false;   // blocks of the multi-CU kernel's grid run on XCD (block mod 8)
   bool group_ok = false;  // the batched MFMA kernel serves every B
   void* dpack = nullptr;  // its packed bf16 weight tiles
 };
@@ -195,6 +196,10 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
     g.G = plan.G;
     g.ub = plan.ub;
     g.tail_on_chain = plan.tail_on_chain;
+    // posts to same-XCD readers stop at the XCD's L2 when the block -> XCD map is the expected
+    // one; WN_LOCAL_POSTS=0 writes every post through
+    const char* lp = std::getenv("WN_LOCAL_POSTS");
+    g.local_posts = h->xcd_map && !(lp && lp[0] == '0');
     std::memcpy(g.role_of_block, plan.role_of_block, sizeof(g.role_of_block));
     if (reset) {
       const size_t words = (l.mb_off - l.hist_off) / 8 + l.mb_words;
@@ -367,6 +372,7 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
   (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device);
   (void)hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, h->device);
   if (want_chain && !bf && wn_chain_supported(R, S, L) && cus >= WN_CHAIN_GRID && coop) h->chain_ok = true;
+  if (h->chain_ok) h->xcd_map = wn_chain_xcd_map_ok();
   // The batched MFMA kernel needs bf16 weights, r = 64 and its LDS footprint on one CU.
   int lds_max = 0;
   (void)hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device);

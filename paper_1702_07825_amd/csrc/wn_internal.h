@@ -97,6 +97,7 @@ struct WnChainArgs {
   int nrep, G;                   // replicas, streams per replica
   int ub;                        // steps of uniforms / samples staged in LDS per stream
   int tail_on_chain;             // 1: the last chain CU computes the last layer's skip projection
+  int local_posts;               // 1: posts to a reader on the same XCD stop at its L2
   uint16_t role_of_block[WN_CHAIN_GRID];  // replica * per_replica + role; 0xffff = idle block
 };
 
@@ -118,6 +119,9 @@ bool wn_chain_supported(int R, int S, int L);
 // or a layout that does not fit).
 bool wn_chain_plan(int L, int R, int S, int B, bool two_taps, WnChainPlan* p);
 hipError_t wn_chain_reset(unsigned long long* words, size_t n, int* status, hipStream_t stream);
+// True when block b of a cooperative launch of the kernel's grid runs on XCD b mod 8 on the
+// current device (checked with a probe launch), the layout the placement assumes.
+bool wn_chain_xcd_map_ok();
 hipError_t wn_chain_launch(const WnChainArgs& g, bool teacher, hipStream_t stream);
 
 // Batched kernel for bf16 weights: one workgroup per group of 16 streams, MFMA for every
