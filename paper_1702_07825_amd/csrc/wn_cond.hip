@@ -54,7 +54,7 @@ struct GateArgs {
 // both operands, so one b128 LDS read feeds four MFMA steps.  VX: the input rows are float4
 // aligned (cin % 4 == 0), else they are read one float at a time.
 constexpr int NTG = 256;
-constexpr int VM = 128, VN = 128, VK = 32, VLD = VK + 4;  // tile, K chunk, LDS row (floats)
+constexpr int VM = 128, VN = 128, VK = 32, VLD = VK + 8;  // tile, K chunk, LDS row (floats)
 
 template <bool VX>
 __global__ __launch_bounds__(NTG, 2) void qrnn_gate_gemm(const GateArgs a) {

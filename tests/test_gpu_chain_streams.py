@@ -150,3 +150,32 @@ def test_timeout_path_drains_and_recovers(monkeypatch):
     ok = mg > MARGIN
     assert np.array_equal(ys[ok], y.cpu().numpy()[ok])
     net.close()
+
+
+@pytest.mark.parametrize("L,r,B", [(20, 64, 1), (20, 128, 11), (40, 64, 2)])
+def test_same_xcd_posts_change_nothing(L, r, B, monkeypatch):
+    """Posts to a reader on the same XCD stop at its L2; written through instead (WN_LOCAL_POSTS=0)
+    every sample and logit is the same.  l = 20, r = 64 places a replica on one XCD (all posts
+    local); r = 128 and l = 40 spill aux CUs to other XCDs (local and written-through posts mix)."""
+    import paper_1702_07825_amd as wn
+    print("same-XCD posts: L=%d r=%d B=%d" % (L, r, B), flush=True)
+    dil = tuple(synth.dilation_cycle(L))
+    w = synth.make_weights(L, r, 256, seed=L + r + B, bias_scale=0.1)
+    T = 200
+    cond = synth.make_cond(L, r, B, T, seed=L + r + B, device="cuda")
+    u = torch.tensor(synth.make_uniforms(B, T, seed=L + r + B), device="cuda")
+    out = {}
+    for lp in ("0", "1"):
+        monkeypatch.setenv("WN_LOCAL_POSTS", lp)
+        net = wn.WaveNet(w, dil)
+        assert net.kernel_variant(B) == "multi_cu_chain"
+        ws = net.new_workspace(B)
+        y = net.generate(cond, u, workspace=ws)
+        lg = net.teacher_force(cond, y)
+        torch.cuda.synchronize()
+        assert net.status(ws) == 0
+        out[lp] = (y.cpu(), lg.cpu())
+        net.close()
+    assert torch.equal(out["0"][0], out["1"][0])
+    assert torch.equal(out["0"][1], out["1"][1])
+
