@@ -274,7 +274,8 @@ def run_cond_workload(name, args):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic (seeded 227-dim phoneme/stress/F0 features, N(0,1/fan_in) weights)",
         "config": {"workload": wl.description, "B": wl.B, "n_frames": wl.n_frames, "T": wl.T, "h1": wl.h1,
-                   "h2": wl.n_layers * wl.r},
+                   "h2": wl.n_layers * wl.r, "kernel": "conditioning",
+                   "source_digest": kernel_source_digest("conditioning")},
         "real_time_factor_16khz": round(wl.T / avg_s / RATE_HZ, 1),
         "roofline": {
             "bound": "mfma",
