@@ -95,6 +95,28 @@ __device__ __forceinline__ f32x4 mfma_row(u32x4 w, const u16* row, int k0, f32x4
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, lo, acc, 0, 0, 0);
 }
 
+// With 8 streams per workgroup the 16 MFMA columns are paired: column n < 8 takes the hi part of
+// stream n's split row and column n + 8 its lo part, so one MFMA does what two do with 16
+// streams; fold8 then adds the two halves (lanes n and n + 8 of each 16-lane row, row_ror:8).
+template <int K, bool PAIR>
+__device__ __forceinline__ f32x4 mfma_split(u32x4 w, const u16* row, int k0, int part, f32x4 acc) {
+  if constexpr (PAIR) {
+    const bf16x8 a = __builtin_bit_cast(bf16x8, w);
+    const bf16x8 v = *reinterpret_cast<const bf16x8*>(row + part * K + k0);
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, v, acc, 0, 0, 0);
+  } else {
+    return mfma_row<K>(w, row, k0, acc);
+  }
+}
+template <bool PAIR>
+__device__ __forceinline__ f32x4 fold8(f32x4 a) {
+  if constexpr (PAIR) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) a[e] += wnk::dpp<0x128>(a[e]);
+  }
+  return a;
+}
+
 // Tile order of the packed weights, in 1 KB blocks (64 lanes x 16 bytes).
 template <int S>
 struct Pack {
@@ -128,7 +150,11 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
   constexpr int gs = GS;  // streams of this workgroup: columns 0 .. GS - 1; the others are padding
   const int b0 = blockIdx.x * gs;
   const int T = g.io.T, B = g.io.B;
-  const int n = lane & 15, quad = lane >> 4;  // MFMA column (stream) and row quad of this lane
+  const int n = lane & 15, quad = lane >> 4;  // MFMA column and row quad of this lane
+  constexpr bool PAIR = GS == 8;              // paired hi / lo columns (see mfma_split)
+  const int sn = PAIR ? (n & 7) : n;          // the stream of this lane's column
+  const int part = n >> 3;                    // with PAIR: 0 hi, 1 lo
+  const bool wl = !PAIR || n < 8;             // the lane that stores its stream's results
 
   extern __shared__ __align__(16) float sm[];
   float* CD = sm;                // [2][G][PC] conditioning rows (layer parity)
@@ -259,12 +285,14 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
     u32x4 w2[2 * P::KTO];
     {
       f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-      const u16* row = ZS + n * SS;
+      const u16* row = ZS + sn * SS;
 #pragma unroll
       for (int kt = 0; kt < P::KTH; ++kt) {
-        acc[0] = mfma_row<S>(w1[kt], row, kt * 32 + quad * 8, acc[0]);
-        acc[1] = mfma_row<S>(w1[P::KTH + kt], row, kt * 32 + quad * 8, acc[1]);
+        acc[0] = mfma_split<S, PAIR>(w1[kt], row, kt * 32 + quad * 8, part, acc[0]);
+        acc[1] = mfma_split<S, PAIR>(w1[P::KTH + kt], row, kt * 32 + quad * 8, part, acc[1]);
       }
+      acc[0] = fold8<PAIR>(acc[0]);
+      acc[1] = fold8<PAIR>(acc[1]);
       // W_out tiles: issued once the W_relu tiles are consumed (the empty asm keeps the loads
       // behind the products), so the two sets never hold registers at the same time
       asm volatile("" : "+v"(acc[0]), "+v"(acc[1])::"memory");
@@ -276,32 +304,37 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
       for (int k = 0; k < 2; ++k) {
         const int m0 = (2 * wave + k) * 16 + quad * 4;
         const float4 b = *reinterpret_cast<const float4*>(BRL + m0);
-        store_split4<A>(ZA + n * SA, m0,
-                        make_float4(fmaxf(acc[k][0] + b.x, 0.f), fmaxf(acc[k][1] + b.y, 0.f),
-                                    fmaxf(acc[k][2] + b.z, 0.f), fmaxf(acc[k][3] + b.w, 0.f)));
+        if (wl)
+          store_split4<A>(ZA + sn * SA, m0,
+                          make_float4(fmaxf(acc[k][0] + b.x, 0.f), fmaxf(acc[k][1] + b.y, 0.f),
+                                      fmaxf(acc[k][2] + b.z, 0.f), fmaxf(acc[k][3] + b.w, 0.f)));
       }
     }
     lds_barrier();
     {
       f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-      const u16* row = ZA + n * SA;
+      const u16* row = ZA + sn * SA;
 #pragma unroll
       for (int kt = 0; kt < P::KTO; ++kt) {
-        acc[0] = mfma_row<A>(w2[kt], row, kt * 32 + quad * 8, acc[0]);
-        acc[1] = mfma_row<A>(w2[P::KTO + kt], row, kt * 32 + quad * 8, acc[1]);
+        acc[0] = mfma_split<A, PAIR>(w2[kt], row, kt * 32 + quad * 8, part, acc[0]);
+        acc[1] = mfma_split<A, PAIR>(w2[P::KTO + kt], row, kt * 32 + quad * 8, part, acc[1]);
       }
+      acc[0] = fold8<PAIR>(acc[0]);
+      acc[1] = fold8<PAIR>(acc[1]);
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
         const int m0 = (2 * wave + k) * 16 + quad * 4;
         const float4 b = *reinterpret_cast<const float4*>(BO + m0);
-        *reinterpret_cast<float4*>(LG + n * PA + m0) =
-            make_float4(acc[k][0] + b.x, acc[k][1] + b.y, acc[k][2] + b.z, acc[k][3] + b.w);
+        if (wl)
+          *reinterpret_cast<float4*>(LG + sn * PA + m0) =
+              make_float4(acc[k][0] + b.x, acc[k][1] + b.y, acc[k][2] + b.z, acc[k][3] + b.w);
       }
     }
     lds_barrier();
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
       const int nn = 2 * wave + k;
+      if (PAIR && nn >= GS) break;  // padding columns: no logits
       int y;
       if constexpr (TF) {
         y = s_yin[nn];
@@ -347,25 +380,27 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
       u32x4(&cur)[NB] = buf[k];
       const int slot = (int)(q & 1);
       if (j == 0) {  // x0 = E[y_{t-1}] + B_embed (+ E_prev[y_{t-2}])
-        const u16* e = EMB + s_y[n] * R + m0;
-        const u16* ep = EPB + n * R + m0;
+        const u16* e = EMB + s_y[sn] * R + m0;
+        const u16* ep = EPB + sn * R + m0;
         xr = make_float4(bf16_val(e[0]) + BE[m0] + bf16_val(ep[0]), bf16_val(e[1]) + BE[m0 + 1] + bf16_val(ep[1]),
                          bf16_val(e[2]) + BE[m0 + 2] + bf16_val(ep[2]), bf16_val(e[3]) + BE[m0 + 3] + bf16_val(ep[3]));
       }
       f32x4 at = {0.f, 0.f, 0.f, 0.f}, as = {0.f, 0.f, 0.f, 0.f};
-      const u16* xp = XP + (slot * G + n) * SR;
-      const u16* xc = XS + ((j & 1) * G + n) * SR;
+      const u16* xp = XP + (slot * G + sn) * SR;
+      const u16* xc = XS + ((j & 1) * G + sn) * SR;
 #pragma unroll
       for (int kt = 0; kt < P::KTG; ++kt) {
         // inputs 0..R-1: the history row x_{j-1}[t - d_j]; R..2R-1: the current x_{j-1}[t]
         const u16* row = kt < R / 32 ? xp : xc;
         const int k0 = (kt % (R / 32)) * 32 + quad * 8;
-        at = mfma_row<R>(cur[kt], row, k0, at);
-        as = mfma_row<R>(cur[P::KTG + kt], row, k0, as);
+        at = mfma_split<R, PAIR>(cur[kt], row, k0, part, at);
+        as = mfma_split<R, PAIR>(cur[P::KTG + kt], row, k0, part, as);
       }
+      at = fold8<PAIR>(at);
+      as = fold8<PAIR>(as);
       // the next tiles, issued once this layer's products are under way
       issue(buf[(k + WB - 1) % WB], (j + WB - 1) % L);
-      const float* cd = CD + (slot * G + n) * PC;
+      const float* cd = CD + (slot * G + sn) * PC;
       const float4 ch = *reinterpret_cast<const float4*>(cd + m0);
       const float4 cg = *reinterpret_cast<const float4*>(cd + R + m0);
       const float4 bh = *reinterpret_cast<const float4*>(BG + j * 2 * R + m0);
@@ -375,18 +410,20 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
       hv.y = tanh_nl<AX>(at[1] + bh.y + ch.y) * sigmoid_nl<AX>(as[1] + bg.y + cg.y);
       hv.z = tanh_nl<AX>(at[2] + bh.z + ch.z) * sigmoid_nl<AX>(as[2] + bg.z + cg.z);
       hv.w = tanh_nl<AX>(at[3] + bh.w + ch.w) * sigmoid_nl<AX>(as[3] + bg.w + cg.w);
-      store_split4<R>(HS + n * SR, m0, hv);
+      if (wl) store_split4<R>(HS + sn * SR, m0, hv);
       lds_barrier();
       if (j < L - 1) {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kt = 0; kt < P::KTR; ++kt) acc = mfma_row<R>(cur[2 * P::KTG + kt], HS + n * SR, kt * 32 + quad * 8, acc);
+        for (int kt = 0; kt < P::KTR; ++kt)
+          acc = mfma_split<R, PAIR>(cur[2 * P::KTG + kt], HS + sn * SR, kt * 32 + quad * 8, part, acc);
+        acc = fold8<PAIR>(acc);
         const float4 br = *reinterpret_cast<const float4*>(BR + j * R + m0);
         xr.x += acc[0] + br.x;
         xr.y += acc[1] + br.y;
         xr.z += acc[2] + br.z;
         xr.w += acc[3] + br.w;
-        store_split4<R>(XS + (((j + 1) & 1) * G + n) * SR, m0, xr);
+        if (wl) store_split4<R>(XS + (((j + 1) & 1) * G + sn) * SR, m0, xr);
         lds_barrier();
       } else {
         u32x4 w1[2 * P::KTH];
@@ -428,7 +465,7 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
             f32x4 acc = first ? f32x4{0.f, 0.f, 0.f, 0.f} : qacc[k];
 #pragma unroll
             for (int kt = 0; kt < P::KTR; ++kt)
-              acc = mfma_row<R>(cur[k * P::KTR + kt], HS + n * SR, kt * 32 + quad * 8, acc);
+              acc = mfma_split<R, PAIR>(cur[k * P::KTR + kt], HS + sn * SR, kt * 32 + quad * 8, part, acc);
             qacc[k] = acc;
           }
         }
@@ -443,9 +480,11 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
           if (k < nsk) {
             const int m0 = (sk0 + k) * 16 + quad * 4;
             const float4 bs = *reinterpret_cast<const float4*>(BS + m0);
-            store_split4<S>(ZS + n * SS, m0,
-                            make_float4(fmaxf(qacc[k][0] + bs.x, 0.f), fmaxf(qacc[k][1] + bs.y, 0.f),
-                                        fmaxf(qacc[k][2] + bs.z, 0.f), fmaxf(qacc[k][3] + bs.w, 0.f)));
+            const f32x4 q = fold8<PAIR>(qacc[k]);
+            if (wl)
+              store_split4<S>(ZS + sn * SS, m0,
+                              make_float4(fmaxf(q[0] + bs.x, 0.f), fmaxf(q[1] + bs.y, 0.f),
+                                          fmaxf(q[2] + bs.z, 0.f), fmaxf(q[3] + bs.w, 0.f)));
           }
         }
         u32x4 w1[2 * P::KTH];  // after the skip products, whose tiles no longer hold registers

@@ -5,7 +5,7 @@ Each case runs through the C ABI and is compared with the CPU oracle in its bf16
 exceeds 1e-4), with the fp32 oracle (2e-2) and with the per-stream kernel on the same inputs.
 Cases cover one stream, full and partial groups, the fewest layers the kernel takes
 (2, dilation 1), s = 128 and 256, dilations longer than the call, and calls split at odd steps.
-A workgroup serves 8 streams (16 beyond 2048 streams); both group sizes give identical results.
+A workgroup serves 8 streams (16 beyond 2048 streams); the two group sizes agree to rounding.
 """
 import zlib
 
@@ -99,14 +99,17 @@ def test_group_kernel_parity(case, monkeypatch):
 
 @pytest.mark.parametrize("B", [5, 13, 16, 17])
 def test_group_sizes_agree(B, monkeypatch):
-    """8 and 16 streams per workgroup: every column of a product depends only on its own stream,
-    so the samples and logits agree bit for bit, also across a call split at an odd step."""
+    """8 and 16 streams per workgroup.  With 8, each MFMA pairs a stream's hi and lo parts in two
+    columns (the sums meet in another order), so the two agree to rounding: logits within 1e-4 of
+    each other, and each meets the oracle bars, also across a call split at an odd step."""
     import paper_1702_07825_amd as wn
     L, dil, T = 6, (1, 2, 4, 8, 1, 3), 90
     _log("group sizes, B=%d" % B)
     w = synth.make_weights(L, 64, 256, seed=B, bias_scale=0.2)
     cond = synth.make_cond(L, 64, B, T, seed=B, device="cuda")
     u = torch.tensor(synth.make_uniforms(B, T, seed=B), device="cuda")
+    model = oracle.Model(w, dil, bf16_weights=True)
+    cond_np, u_np = cond.cpu().numpy(), u.cpu().numpy()
     out = {}
     for gs in (8, 16):
         monkeypatch.setenv("WN_GROUP_STREAMS", str(gs))
@@ -121,15 +124,22 @@ def test_group_sizes_agree(B, monkeypatch):
         torch.cuda.synchronize()
         assert net.status(ws) == 0
         assert torch.equal(torch.cat([ya, yb], 1), y)
-        out[gs] = (y.cpu(), lg.cpu())
+        y_np, lg_np = y.cpu().numpy(), lg.cpu().numpy()
+        ys, lo, mg = oracle.run_streams(model, cond_np, u=u_np, y_in=y_np, threads=8)
+        ok = mg > MARGIN
+        assert float(np.abs(lg_np - lo).max()) <= 1e-3
+        assert int(np.sum(ys[ok] != y_np[ok])) == 0
+        out[gs] = (y_np, lg_np)
         net.close()
-    assert torch.equal(out[8][0], out[16][0])
-    assert torch.equal(out[8][1], out[16][1])
-    model = oracle.Model(w, dil, bf16_weights=True)
-    ys, lo, mg = oracle.run_streams(model, cond.cpu().numpy(), u=u.cpu().numpy(), y_in=out[8][0].numpy(), threads=8)
-    ok = mg > MARGIN
-    assert float(np.abs(out[8][1].numpy() - lo).max()) <= 1e-3
-    assert int(np.sum(ys[ok] != out[8][0].numpy()[ok])) == 0
+    # the same teacher-forced inputs through both group sizes
+    monkeypatch.setenv("WN_GROUP_STREAMS", "16")
+    net16 = wn.WaveNet(w, dil, weight_dtype="bf16")
+    lg16 = net16.teacher_force(cond, torch.tensor(out[8][0], device="cuda"))
+    torch.cuda.synchronize()
+    d = float(np.abs(lg16.cpu().numpy() - out[8][1]).max())
+    _log("  max|dlogit| between 8 and 16 streams per workgroup: %.3g" % d)
+    assert d <= 1e-4
+    net16.close()
 
 
 def test_group_kernel_variant_selection():
