@@ -2,8 +2,10 @@
 //
 // With many streams a step's layer becomes a real contraction: a = [W_prev | W_cur] [x_prev; x]
 // is [2r x 2r] . [2r x B], and likewise W_res, W_skip and the two head layers (Deep Voice,
-// arXiv 1702.07825, Appendix A.1).  One 512-thread workgroup owns a group of 16 streams (one
-// MFMA N-tile) for the whole call and runs every layer of every step for them.  Per layer:
+// arXiv 1702.07825, Appendix A.1).  One 512-thread workgroup owns a group of 8 streams (16 when
+// a call has more than 2048) for the whole call and runs every layer of every step for them; the
+// group fills the 16 columns of an MFMA N-tile (with 8 streams, each stream's hi and lo parts
+// side by side, see mfma_split).  Per layer:
 //
 //   phase A  waves 0-3: gate.  Wave g computes the tanh rows 16g..16g+15 of a and the matching
 //            sigmoid rows r+16g.., so h = tanh * sigmoid needs no exchange between waves.
@@ -530,7 +532,7 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
       for (int k = 0; k < NC; ++k)
         if (lq + LPS * k < 32) cd[LPS * k] = buf[NH + k];
     };
-    // Samples (generation) or logits (teacher forcing) of step tl, from s_y / LG, for the 16 streams.
+    // Samples (generation) or logits (teacher forcing) of step tl, from s_y / LG, for the group.
     auto write_outputs = [&](int64_t tl) __attribute__((always_inline)) {
       if constexpr (TF) {
 #pragma unroll
@@ -675,10 +677,11 @@ bool wn_group_supported(int R_, int S_, int L) {
   return R_ == R && (S_ == 256 || S_ == 128) && L >= 2 && L <= WN_GROUP_MAX_LAYERS;
 }
 
-// Measured at l = 20, r = 64 (us per step): 16 streams per workgroup 29.0, 8 streams 27.8-29.0,
-// 4 streams 28.2-29.3, one stream 28.5-31.2 (B = 1 .. 1024); eight keep the MFMA columns half
-// busy while the loader wave moves half the rows, and up to 2048 streams still fit one workgroup
-// per CU.
+// Eight streams per workgroup fill the MFMA columns with their hi and lo parts (one MFMA per
+// product instead of two) while the loader wave moves half the rows, and up to 2048 streams still
+// fit one workgroup per CU.  Measured at l = 20, r = 64, B = 256: 25.4 us per step against 29.0
+// with 16 streams per workgroup (with one stream per column, 4, 2 and 1 streams per workgroup
+// took 28.3, 27.9 and 31.2 us).
 int wn_group_streams(int B) {
   if (const char* e = std::getenv("WN_GROUP_STREAMS")) {
     const int v = std::atoi(e);

@@ -124,7 +124,7 @@ hipError_t wn_chain_reset(unsigned long long* words, size_t n, int* status, hipS
 bool wn_chain_xcd_map_ok();
 hipError_t wn_chain_launch(const WnChainArgs& g, bool teacher, hipStream_t stream);
 
-// Batched kernel for bf16 weights: one workgroup per group of 16 streams, MFMA for every
+// Batched kernel for bf16 weights: one workgroup per group of 8 or 16 streams, MFMA for every
 // product, weights pre-packed into MFMA operand tiles (wn_group_pack) and streamed from L2.
 struct WnGroupArgs {
   WnDims d;
