@@ -37,6 +37,13 @@
  *    is launched when an argument check fails.  wn_last_error() gives a detail
  *    string for the calling thread's last failure.
  *  - Two calls that share one workspace must not overlap in time.
+ *  - Environment variables (tuning and tests; read at wn_create or at each call):
+ *      WN_KERNEL=stream      wn_create: serve every call with the per-stream kernel
+ *      WN_SPIN_LIMIT=n       each call: polls before a multi-CU wait gives up (wn_status)
+ *      WN_LOCAL_POSTS=0      each call: the multi-CU kernel writes every message through to
+ *                            memory instead of stopping same-XCD messages at the XCD's L2
+ *      WN_GROUP_STREAMS=8|16 each call: streams per workgroup of the batched bf16 kernel
+ *    None of them changes a result beyond rounding.
  */
 #ifndef WN_H_
 #define WN_H_
