@@ -159,3 +159,30 @@ def test_group_kernel_variant_selection():
     net2 = wn.WaveNet(w2, (1, 2, 4, 8), weight_dtype="bf16")
     assert net2.kernel_variant(16) == "stream_l2"
     net2.close()
+
+
+def test_more_streams_than_eight_per_cu():
+    """2049 streams: the default choice moves to 16 streams per workgroup (129 workgroups, the last
+    holding one stream); sampled streams across the batch meet the oracle bars."""
+    import paper_1702_07825_amd as wn
+    L, dil, T, B = 2, (1, 2), 6, 2049
+    _log("group: B=%d T=%d" % (B, T))
+    w = synth.make_weights(L, 64, 128, seed=7, bias_scale=0.3)
+    net = wn.WaveNet(w, dil, weight_dtype="bf16")
+    assert net.kernel_variant(B) == "mfma_group"
+    assert net.launch_info(B) == (129, 129)
+    cond = synth.make_cond(L, 64, B, T, seed=7, device="cuda")
+    u = torch.tensor(synth.make_uniforms(B, T, seed=7), device="cuda")
+    ws = net.new_workspace(B)
+    y = net.generate(cond, u, workspace=ws)
+    lg = net.teacher_force(cond, y)
+    torch.cuda.synchronize()
+    assert net.status(ws) == 0
+    pick = np.array([0, 1, 15, 16, 17, 1000, 2031, 2032, 2047, 2048])
+    y_np, lg_np = y.cpu().numpy()[pick], lg.cpu().numpy()[pick]
+    model = oracle.Model(w, dil, bf16_weights=True)
+    ys, lo, mg = oracle.run_streams(model, cond.cpu().numpy()[pick], u=u.cpu().numpy()[pick], y_in=y_np, threads=8)
+    ok = mg > MARGIN
+    assert float(np.abs(lg_np - lo).max()) <= 1e-3
+    assert int(np.sum(ys[ok] != y_np[ok])) == 0
+    net.close()
