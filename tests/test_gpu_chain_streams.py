@@ -171,9 +171,13 @@ def test_same_xcd_posts_change_nothing(L, r, B, monkeypatch):
         assert net.kernel_variant(B) == "multi_cu_chain"
         ws = net.new_workspace(B)
         y = net.generate(cond, u, workspace=ws)
+        # the same workspace from zero again: every tag repeats, and words left in an XCD's L2 by
+        # the previous call must not be taken for this call's
+        y_again = net.generate(cond, u, workspace=ws, reset=True)
         lg = net.teacher_force(cond, y)
         torch.cuda.synchronize()
         assert net.status(ws) == 0
+        assert torch.equal(y, y_again)
         out[lp] = (y.cpu(), lg.cpu())
         net.close()
     assert torch.equal(out["0"][0], out["1"][0])
