@@ -110,6 +110,16 @@ __device__ __forceinline__ f32x4 mfma_split(u32x4 w, const u16* row, int k0, int
     return mfma_row<K>(w, row, k0, acc);
   }
 }
+// tanh(ah) sigmoid(ag) with paired columns: lane n < 8 (part 0) evaluates the tanh and lane
+// n + 8 the sigmoid of the same values (after fold8 both hold the same sums), then they swap
+// results (row_ror:8), so a wave issues half the transcendental instructions
+__device__ __forceinline__ float gate_pair8(float ah, float ag, int part) {
+  const bool th = part == 0;
+  const float r = __builtin_amdgcn_rcpf(1.0f + wnk::expf_fast(th ? 2.0f * ah : -ag));
+  const float v = th ? 1.0f - 2.0f * r : r;
+  const float o = wnk::dpp<0x128>(v);
+  return th ? v * o : o * v;
+}
 template <bool PAIR>
 __device__ __forceinline__ f32x4 fold8(f32x4 a) {
   if constexpr (PAIR) {
@@ -408,10 +418,17 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
       const float4 bh = *reinterpret_cast<const float4*>(BG + j * 2 * R + m0);
       const float4 bg = *reinterpret_cast<const float4*>(BG + j * 2 * R + R + m0);
       float4 hv;
-      hv.x = tanh_nl<AX>(at[0] + bh.x + ch.x) * sigmoid_nl<AX>(as[0] + bg.x + cg.x);
-      hv.y = tanh_nl<AX>(at[1] + bh.y + ch.y) * sigmoid_nl<AX>(as[1] + bg.y + cg.y);
-      hv.z = tanh_nl<AX>(at[2] + bh.z + ch.z) * sigmoid_nl<AX>(as[2] + bg.z + cg.z);
-      hv.w = tanh_nl<AX>(at[3] + bh.w + ch.w) * sigmoid_nl<AX>(as[3] + bg.w + cg.w);
+      if constexpr (PAIR && !AX) {
+        hv.x = gate_pair8(at[0] + bh.x + ch.x, as[0] + bg.x + cg.x, part);
+        hv.y = gate_pair8(at[1] + bh.y + ch.y, as[1] + bg.y + cg.y, part);
+        hv.z = gate_pair8(at[2] + bh.z + ch.z, as[2] + bg.z + cg.z, part);
+        hv.w = gate_pair8(at[3] + bh.w + ch.w, as[3] + bg.w + cg.w, part);
+      } else {
+        hv.x = tanh_nl<AX>(at[0] + bh.x + ch.x) * sigmoid_nl<AX>(as[0] + bg.x + cg.x);
+        hv.y = tanh_nl<AX>(at[1] + bh.y + ch.y) * sigmoid_nl<AX>(as[1] + bg.y + cg.y);
+        hv.z = tanh_nl<AX>(at[2] + bh.z + ch.z) * sigmoid_nl<AX>(as[2] + bg.z + cg.z);
+        hv.w = tanh_nl<AX>(at[3] + bh.w + ch.w) * sigmoid_nl<AX>(as[3] + bg.w + cg.w);
+      }
       if (wl) store_split4<R>(HS + sn * SR, m0, hv);
       lds_barrier();
       if (j < L - 1) {
