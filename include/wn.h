@@ -63,7 +63,7 @@ typedef enum {
   WN_ENOMEM = -3,        /* device or host allocation failed */
   WN_EHIP = -4,          /* a HIP runtime call failed; wn_last_error() has its message */
   WN_ETIMEOUT = -5,      /* a kernel's bounded wait expired (reported by wn_status) */
-  WN_EABORTED = -6       /* a kernel stopped early on request (reported by wn_status) */
+  WN_EABORTED = -6       /* a call stopped early on a wn_abort request (reported by wn_status) */
 } wn_status_t;
 
 typedef enum { WN_F32 = 0, WN_BF16 = 1 } wn_dtype_t;
@@ -198,10 +198,23 @@ int wn_teacher_force(wn_handle* h, int32_t B, int32_t T, const float* cond, cons
  * the stream reports an error.  Blocks the calling thread.  The multi-CU kernel's
  * waits for other CUs give up after a bounded number of polls (a few seconds);
  * the environment variable WN_SPIN_LIMIT, read at each call, sets that number
- * (tests force the timeout path with it).  After WN_ETIMEOUT the workspace state
- * is stale: the next call must pass reset = 1.
+ * (tests force the timeout path with it).  After WN_ETIMEOUT or WN_EABORTED the
+ * workspace state is stale: the next call must pass reset = 1.
  */
 int wn_status(wn_handle* h, const void* workspace, void* stream);
+
+/*
+ * Request (on = 1) or withdraw (on = 0) an early stop of this handle's calls, from any host
+ * thread, also while a call runs.  The request is a word in pinned host memory that the handle
+ * owns; every kernel of a wn_generate, wn_generate_sampled or wn_teacher_force call of this
+ * handle reads it at the call's first step and every 64 steps after, and once it reads 1 the
+ * whole grid leaves at a step boundary (its outputs from that step on are not written) and the
+ * call's status word becomes WN_EABORTED (wn_status).  While the request stands, calls still
+ * launch and stop at their first step; withdraw it before the next call, which must pass
+ * reset = 1.  A call that has passed its last check finishes normally (status WN_OK).
+ * Errors: WN_EINVAL (null handle, on not 0 or 1).  Nothing is launched.
+ */
+int wn_abort(wn_handle* h, int32_t on);
 
 /* Name of the kernel family that calls with B streams use (for reports). */
 const char* wn_kernel_variant(const wn_handle* h, int32_t B);

@@ -23,7 +23,7 @@ WN_F32, WN_BF16 = 0, 1
 WN_NONLIN_EXACT, WN_NONLIN_PAPER = 0, 1
 A_CLASSES = 256
 EXPORTED = ("wn_create", "wn_workspace_bytes", "wn_generate", "wn_generate_sampled", "wn_teacher_force", "wn_status",
-            "wn_kernel_variant", "wn_launch_info", "wn_destroy", "wn_error_string", "wn_last_error",
+            "wn_abort", "wn_kernel_variant", "wn_launch_info", "wn_destroy", "wn_error_string", "wn_last_error",
             "wn_cond_create", "wn_cond_workspace_bytes", "wn_condition", "wn_cond_destroy")
 # wn_sample_mode_t: how a step's distribution becomes its sample
 SAMPLE_DIRECT, SAMPLE_TEMPERATURE, SAMPLE_TOPK, SAMPLE_MODE, SAMPLE_MEAN = 0, 1, 2, 3, 4
@@ -95,6 +95,8 @@ def load_library(path: str = LIB_PATH):
         L.wn_teacher_force.argtypes = [vp, i32, i32, vp, vp, vp, vp, sz, i32, vp]
         L.wn_status.restype = ctypes.c_int
         L.wn_status.argtypes = [vp, vp, vp]
+        L.wn_abort.restype = ctypes.c_int
+        L.wn_abort.argtypes = [vp, i32]
         L.wn_kernel_variant.restype = ctypes.c_char_p
         L.wn_kernel_variant.argtypes = [vp, i32]
         L.wn_launch_info.restype = ctypes.c_int
@@ -236,6 +238,10 @@ class WaveNet:
         _check(self._lib.wn_teacher_force(self._h, B, T, cp, yp, lp, workspace.data_ptr(), workspace.numel(),
                                           1 if reset else 0, _stream_handle(stream)), "wn_teacher_force")
         return logits
+
+    def abort(self, on: bool = True):
+        """wn_abort: ask this model's running and later calls to stop early (on=False withdraws it)."""
+        _check(self._lib.wn_abort(self._h, 1 if on else 0), "wn_abort")
 
     def status(self, workspace, stream=None) -> int:
         """Synchronise the stream and return the kernel status word (0 = ok)."""

@@ -778,7 +778,15 @@ __device__ void aux_role(const WnChainArgs& g, const int j, const int b0, const 
   const bool skip_here = (j < L - 1) || !g.tail_on_chain;
   for (int64_t t = tg0; t < tg0 + T; ++t) {
     const bool more = (t + 1 < tg0 + T);
+    // A host abort request, read every WN_ABORT_CHECK steps by the first layer's aux CU, which
+    // works a step ahead of the chain, so the read's PCIe round trip stays off the critical path.
+    // It stops here; every other role sees the status word in its next wait and leaves too.
+    if (j == 0 && threadIdx.x == 0 && ((t - tg0) & (WN_ABORT_CHECK - 1)) == 0 && abort_requested(g.io.abort_flag)) {
+      atomicCAS(g.status, 0, (int)WN_EABORTED);
+      *sy.flag = 1;
+    }
     lds_barrier();
+    if (sy.failed()) return;
     if (more) stage(t + 1, d >= 2);
     if (sy.failed()) return;
     for (int i = 0; i < ns; ++i) {
@@ -1092,6 +1100,13 @@ bool wn_chain_xcd_map_ok() {
   for (int b = 0; ok && b < WN_CHAIN_GRID; ++b) ok = h[b] == b % 8;
   (void)hipFree(d);
   return ok;
+}
+
+__global__ void wn_status_clear_kernel(int* status) { *status = 0; }
+
+hipError_t wn_status_clear(int* status, hipStream_t stream) {
+  hipLaunchKernelGGL(wn_status_clear_kernel, dim3(1), dim3(1), 0, stream, status);
+  return hipGetLastError();
 }
 
 hipError_t wn_chain_reset(unsigned long long* words, size_t n, int* status, hipStream_t stream) {

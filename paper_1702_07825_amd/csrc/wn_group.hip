@@ -33,6 +33,8 @@
 #include "wn_internal.h"
 #include "wn_wave.h"
 
+#include "wn.h"
+
 #include <cstdlib>
 #include <cstring>
 #include <type_traits>
@@ -192,6 +194,9 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
   // layer j's history offset and dilation: read from LDS in the loop (a dynamically indexed
   // kernel argument would be a scalar memory load each time)
   __shared__ int s_hoff[WN_GROUP_MAX_LAYERS], s_dil[WN_GROUP_MAX_LAYERS];
+  // 1 once the loader has seen a host abort request (written before a barrier of a step's first
+  // position, read by every wave after that position's last barrier)
+  __shared__ int s_abort;
 
   const u32x4* pk = static_cast<const u32x4*>(g.packed);
   const unsigned loff = (unsigned)lane * 16u;  // this lane's bytes within a 1 KB tile
@@ -219,6 +224,7 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
       s_y2[tid] = y2 < 0 ? -1 : (y2 > A - 1 ? A - 1 : y2);
     }
   }
+  if (tid == 0) s_abort = 0;
   if (tid < L) {
     s_slot[tid] = (int)(tg0 % D.dil[tid]);
     s_hoff[tid] = D.hoff[tid];
@@ -239,7 +245,6 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
       float4* hist = reinterpret_cast<float4*>(g.ws.hist + (size_t)(b0 + nn) * D.hist_len);
       for (int i = tid; i < D.hist_len / 4; i += NT) hist[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     }
-    if (blockIdx.x == 0 && tid == 0) *g.ws.status = 0;
   }
   // padding columns never receive rows: zero them once (their products then stay finite)
   for (int i = tid; i < 2 * G * SR; i += NT) XP[i] = 0;
@@ -259,7 +264,9 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
 
   // Runs every position (step, layer) of the call.  Positions rotate through NBUF prefetch
   // buffers; the body gets the buffer index as a compile-time constant.  The loop leaves right
-  // after the position that used a buffer or goes on to the one that refills it.
+  // after the position that used a buffer or goes on to the one that refills it, or after the
+  // first position of a step once the loader has seen an abort request (every wave reads s_abort
+  // at the same position, after its barriers, so all leave together).
   auto run = [&](auto nbuf, auto&& body) __attribute__((always_inline)) {
     constexpr int NBUF = decltype(nbuf)::value;
     static_assert(NBUF == 2 || NBUF == 3, "two or three prefetch buffers");
@@ -268,8 +275,9 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
     int64_t q = 0;
     auto step = [&](auto kc) __attribute__((always_inline)) {
       body(kc, q, tl, j);
+      const bool stop = j == 0 && s_abort != 0;
       if (++j == L) j = 0, ++tl;
-      return ++q == nq;
+      return ++q == nq || stop;
     };
     for (;;) {
       if (step(std::integral_constant<int, 0>{})) break;
@@ -630,6 +638,11 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
         pre_e[0] = e[0];
         pre_e[1] = e[1];
       }
+      // a host abort request, read every WN_ABORT_CHECK steps
+      if (j == 0 && lane == 0 && (tl & (WN_ABORT_CHECK - 1)) == 0 && abort_requested(g.io.abort_flag)) {
+        atomicCAS(g.ws.status, 0, (int)WN_EABORTED);
+        s_abort = 1;
+      }
       issue(nxt, tl2, j2);
       if (++j2 == L) j2 = 0, ++tl2;
       lds_barrier();
@@ -642,10 +655,11 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
         head_and_draw(tl, w1);
       }
     });
-    write_outputs(T - 1);  // the last step's, after its draw
+    if (!s_abort) write_outputs(T - 1);  // the last step's, after its draw
   }
   __syncthreads();
-  if (tid < gs && b0 + tid < B) {
+  // after an abort the state stays as it was (the next call must start from zero)
+  if (tid < gs && b0 + tid < B && !s_abort) {
     int64_t* st = g.ws.state + WN_STATE_WORDS * (size_t)(b0 + tid);
     st[0] = tg0 + T;
     st[1] = s_y[tid];

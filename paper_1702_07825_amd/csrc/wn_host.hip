@@ -25,6 +25,9 @@ struct wn_handle {
   bool xcd_map = false;   // blocks of the multi-CU kernel's grid run on XCD (block mod 8)
   bool group_ok = false;  // the batched MFMA kernel serves every B
   void* dpack = nullptr;  // its packed bf16 weight tiles
+  // wn_abort's request word: coherent pinned host memory the kernels read at system scope
+  int* abort_host = nullptr;
+  int* abort_dev = nullptr;
 };
 
 namespace {
@@ -172,6 +175,7 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
     g.io.T = T;
     g.io.reset = reset;
     g.io.init_sample = h->init_sample;
+    g.io.abort_flag = h->abort_dev;
     set_sampler(g.io, sp);
     g.status = reinterpret_cast<int32_t*>(base + l.status_off);
     g.state = reinterpret_cast<int64_t*>(base + l.state_off);
@@ -224,11 +228,16 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
     g.io.T = T;
     g.io.reset = reset;
     g.io.init_sample = h->init_sample;
+    g.io.abort_flag = h->abort_dev;
     set_sampler(g.io, sp);
     g.ws.status = reinterpret_cast<int32_t*>(base + l.status_off);
     g.ws.state = reinterpret_cast<int64_t*>(base + l.state_off);
     g.ws.hist = reinterpret_cast<float*>(base + l.hist_off);
     g.gs = wn_group_streams(B);
+    if (reset) {
+      const hipError_t e = wn_status_clear(g.ws.status, st);
+      if (e != hipSuccess) return hip_fail(e, "status clear launch");
+    }
     const hipError_t e = wn_group_launch(g, teacher, st);
     if (e != hipSuccess) return hip_fail(e, "batched kernel launch");
     return WN_OK;
@@ -245,10 +254,15 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
   args.io.T = T;
   args.io.reset = reset;
   args.io.init_sample = h->init_sample;
+  args.io.abort_flag = h->abort_dev;
   set_sampler(args.io, sp);
   args.ws.status = reinterpret_cast<int32_t*>(base + l.status_off);
   args.ws.state = reinterpret_cast<int64_t*>(base + l.state_off);
   args.ws.hist = reinterpret_cast<float*>(base + l.hist_off);
+  if (reset) {
+    const hipError_t se = wn_status_clear(args.ws.status, st);
+    if (se != hipSuccess) return hip_fail(se, "status clear launch");
+  }
   const hipError_t e = wn_stream_launch(args, teacher, st);
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return WN_OK;
@@ -346,6 +360,19 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
     delete h;
     return hip_fail(e, "hipMemcpy of weights");
   }
+  // the abort request word (wn_abort), in host memory the kernels can read while they run
+  e = hipHostMalloc(reinterpret_cast<void**>(&h->abort_host), 256, hipHostMallocCoherent | hipHostMallocMapped);
+  if (e == hipSuccess) {
+    *h->abort_host = 0;
+    e = hipHostGetDevicePointer(reinterpret_cast<void**>(&h->abort_dev), h->abort_host, 0);
+  }
+  if (e != hipSuccess) {
+    if (h->abort_host) (void)hipHostFree(h->abort_host);
+    (void)hipFree(h->dmem);
+    delete h;
+    return e == hipErrorOutOfMemory ? fail(WN_ENOMEM, "pinned host allocation of the abort word")
+                                    : hip_fail(e, "abort word");
+  }
   char* d = static_cast<char*>(h->dmem);
   // [taps][A][R]: the last table embeds y_{t-1}, the first of two y_{t-2}
   h->w.embed = d + arrs[0].off + (size_t)(c->embed_taps - 1) * A * R * we;
@@ -384,6 +411,7 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
     if (e != hipSuccess) {
       if (h->dpack) (void)hipFree(h->dpack);
       (void)hipFree(h->dmem);
+      (void)hipHostFree(h->abort_host);
       delete h;
       return e == hipErrorOutOfMemory ? fail(WN_ENOMEM, "hipMalloc of packed weights")
                                       : hip_fail(e, "packed weights upload");
@@ -439,6 +467,14 @@ int wn_status(wn_handle* h, const void* workspace, void* stream) {
   return st;
 }
 
+int wn_abort(wn_handle* h, int32_t on) {
+  g_err.clear();
+  if (!h) return fail(WN_EINVAL, "null handle");
+  if (on != 0 && on != 1) return fail(WN_EINVAL, "on must be 0 or 1");
+  __atomic_store_n(h->abort_host, on, __ATOMIC_SEQ_CST);
+  return WN_OK;
+}
+
 const char* wn_kernel_variant(const wn_handle* h, int32_t B) {
   if (!h || B < 1) return "";
   switch (variant_for(h, B)) {
@@ -473,6 +509,7 @@ void wn_destroy(wn_handle* h) {
     DeviceScope scope(h->device);
     if (h->dmem) (void)hipFree(h->dmem);
     if (h->dpack) (void)hipFree(h->dpack);
+    if (h->abort_host) (void)hipHostFree(h->abort_host);
   }
   delete h;
 }

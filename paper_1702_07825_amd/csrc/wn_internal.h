@@ -54,7 +54,12 @@ struct WnIO {
   int smode;
   float inv_t;
   int top_k;
+  // host-requested abort (wn_abort): a word in coherent pinned host memory, read with system-scope
+  // loads every WN_ABORT_CHECK steps of a call; nonzero = stop
+  const int* abort_flag;
 };
+// Steps between two reads of the abort word (a read crosses PCIe: ~1-2 us)
+#define WN_ABORT_CHECK 64
 
 // Caller-owned workspace, carved by the host code.
 struct WnWorkspace {
@@ -119,6 +124,9 @@ bool wn_chain_supported(int R, int S, int L);
 // or a layout that does not fit).
 bool wn_chain_plan(int L, int R, int S, int B, bool two_taps, WnChainPlan* p);
 hipError_t wn_chain_reset(unsigned long long* words, size_t n, int* status, hipStream_t stream);
+// Zeroes the status word before a run from zero of the per-stream or batched kernel (a kernel, not
+// a memset: a caller may capture the call in a graph).
+hipError_t wn_status_clear(int* status, hipStream_t stream);
 // True when block b of a cooperative launch of the kernel's grid runs on XCD b mod 8 on the
 // current device (checked with a probe launch), the layout the placement assumes.
 bool wn_chain_xcd_map_ok();

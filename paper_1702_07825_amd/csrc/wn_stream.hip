@@ -22,6 +22,8 @@
 #include "wn_internal.h"
 #include "wn_wave.h"
 
+#include "wn.h"
+
 namespace {
 
 constexpr int NT = 1024;
@@ -90,6 +92,7 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
   __shared__ __align__(16) float lgs[A];
   __shared__ int yprev_s;   // y_{t-1}
   __shared__ int yprev2_s;  // y_{t-2}, -1 before the first input
+  __shared__ int abort_s;   // 1 once this block has seen an abort request
 
   const WT* embed = static_cast<const WT*>(args.w.embed);
   const WT* embed_prev = static_cast<const WT*>(args.w.embed_prev);  // null with one tap
@@ -111,7 +114,6 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
       yprev_s = args.io.init_sample;
       yprev2_s = -1;
     }
-    if (b == 0 && tid == 0) *args.ws.status = 0;
   } else {
     tg0 = state[0];
     if (tid == 0) {
@@ -119,11 +121,18 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
       yprev2_s = (int)state[2];
     }
   }
+  if (tid == 0) abort_s = 0;
   __syncthreads();
 
   for (int t = 0; t < T; ++t) {
     const int64_t tg = tg0 + t;
     const size_t bt = (size_t)b * T + t;
+    // a host abort request, read every WN_ABORT_CHECK steps; the decision is taken block-wide after
+    // the barrier below
+    if (tid == 0 && (t & (WN_ABORT_CHECK - 1)) == 0 && wnk::abort_requested(args.io.abort_flag)) {
+      atomicCAS(args.ws.status, 0, (int)WN_EABORTED);
+      abort_s = 1;
+    }
     // ---- step inputs: history slots, conditioning, embedding, q = B_skip ----
     {
       const float* cond_t = args.io.cond + bt * (size_t)(L * 2 * R);
@@ -147,6 +156,7 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
       for (int m = tid; m < S; m += NT) qs[m] = args.w.b_skip[m];
     }
     __syncthreads();
+    if (abort_s) break;
 
     for (int j = 0; j < L; ++j) {
       // ---- a = W_prev x[t-d] + W_cur x[t] + B + L ; h = tanh(a[:R]) * sigmoid(a[R:]) ----
@@ -269,7 +279,8 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
     }
     __syncthreads();
   }
-  if (tid == 0) {
+  // after an abort the state stays as it was (the next call must start from zero)
+  if (tid == 0 && !abort_s) {
     state[0] = tg0 + T;
     state[1] = yprev_s;
     state[2] = yprev2_s;

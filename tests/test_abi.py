@@ -87,6 +87,7 @@ def test_null_arguments(lib):
     assert lib.wn_generate(None, 1, 1, None, None, None, None, 0, 1, None) == -1
     assert lib.wn_teacher_force(None, 1, 1, None, None, None, None, 0, 1, None) == -1
     assert lib.wn_status(None, None, None) == -1
+    assert lib.wn_abort(None, 1) == -1
     assert lib.wn_kernel_variant(None, 1) == b""
     wg, rep = ctypes.c_int32(7), ctypes.c_int32(7)
     assert lib.wn_launch_info(None, 1, ctypes.byref(wg), ctypes.byref(rep)) == -1
@@ -124,3 +125,4 @@ def test_conditioning_network_rejects_before_any_device_call(lib):
     assert lib.wn_cond_workspace_bytes(None, 1, 1) == 0
     assert lib.wn_condition(None, 1, 1, None, 1, None, None, 0, None) == wn.WN_EINVAL
     lib.wn_cond_destroy(None)
+
