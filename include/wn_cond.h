@@ -67,6 +67,30 @@ size_t wn_cond_workspace_bytes(const wn_cond* c, int32_t B, int32_t n_frames);
 int wn_condition(wn_cond* c, int32_t B, int32_t n_frames, const float* features, int32_t T, float* cond,
                  void* workspace, size_t ws_bytes, void* stream);
 
+/*
+ * Bytes of the static scratch array wn_condition_static uses on each device: a call with B streams
+ * of n_frames frames is accepted while wn_cond_workspace_bytes(c, B, n_frames) is at most this
+ * (64 MiB: about 5.8 s of audio at 256 frames per second for l = 20, r = 64, h1 = 256).
+ */
+#define WN_COND_SCRATCH_BYTES ((size_t)64 << 20)
+
+/*
+ * wn_condition without a workspace argument, for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).  The scratch the
+ * three kernels use (gate pre-activations, the first layer's output, the frame-rate output) lives
+ * in one static device array per device, WN_COND_SCRATCH_BYTES long, which the library holds
+ * from its first use on a device until the process ends; wn_cond_create looks up that device's
+ * address of it.  This call allocates nothing and calls no allocating routine.
+ * Every call on one device shares that device's array: two calls that overlap in time on one
+ * device (on different streams, or from different threads or handles) race and give undefined
+ * results; calls ordered on one stream do not.  The array keeps the last call's contents; no
+ * result depends on them (every word a call reads it has written first).
+ * Arguments, results and errors as wn_condition, plus WN_EINVAL when
+ * wn_cond_workspace_bytes(c, B, n_frames) > WN_COND_SCRATCH_BYTES (nothing is launched).
+ */
+int wn_condition_static(wn_cond* c, int32_t B, int32_t n_frames, const float* features, int32_t T, float* cond,
+                        void* stream);
+
 /* Free the device weights.  Null is allowed.  No call may be in flight. */
 void wn_cond_destroy(wn_cond* c);
 

@@ -24,7 +24,9 @@ WN_NONLIN_EXACT, WN_NONLIN_PAPER = 0, 1
 A_CLASSES = 256
 EXPORTED = ("wn_create", "wn_workspace_bytes", "wn_generate", "wn_generate_sampled", "wn_teacher_force", "wn_status",
             "wn_abort", "wn_kernel_variant", "wn_launch_info", "wn_destroy", "wn_error_string", "wn_last_error",
-            "wn_cond_create", "wn_cond_workspace_bytes", "wn_condition", "wn_cond_destroy")
+            "wn_cond_create", "wn_cond_workspace_bytes", "wn_condition", "wn_condition_static", "wn_cond_destroy")
+# WN_COND_SCRATCH_BYTES of include/wn_cond.h: the largest scratch wn_condition_static takes
+COND_SCRATCH_BYTES = 64 << 20
 # wn_sample_mode_t: how a step's distribution becomes its sample
 SAMPLE_DIRECT, SAMPLE_TEMPERATURE, SAMPLE_TOPK, SAMPLE_MODE, SAMPLE_MEAN = 0, 1, 2, 3, 4
 
@@ -89,6 +91,8 @@ def load_library(path: str = LIB_PATH):
         L.wn_cond_workspace_bytes.argtypes = [vp, i32, i32]
         L.wn_condition.restype = ctypes.c_int
         L.wn_condition.argtypes = [vp, i32, i32, vp, i32, vp, vp, sz, vp]
+        L.wn_condition_static.restype = ctypes.c_int
+        L.wn_condition_static.argtypes = [vp, i32, i32, vp, i32, vp, vp]
         L.wn_cond_destroy.restype = None
         L.wn_cond_destroy.argtypes = [vp]
         L.wn_teacher_force.restype = ctypes.c_int
@@ -294,4 +298,15 @@ class Conditioner:
             workspace = torch.empty(max(self.workspace_bytes(B, Tf), 1), dtype=torch.uint8, device=features.device)
         _check(self._lib.wn_condition(self._h, B, Tf, fp, int(T), cp, workspace.data_ptr(), workspace.numel(),
                                       _stream_handle(stream)), "wn_condition")
+        return cond
+
+    def condition_static(self, features, T: int, cond, stream=None):
+        """wn_condition_static: as __call__, with the library's static scratch instead of a workspace.
+        ``cond`` (fp32 [B, T, n_layers, 2r], device) is required: this path allocates nothing."""
+        import torch
+        B, Tf = int(features.shape[0]), int(features.shape[1])
+        fp = _dev_ptr(features, torch.float32, (B, Tf, self.n_features), "features")
+        cp = _dev_ptr(cond, torch.float32, (B, T, self.n_layers, 2 * self.r), "cond")
+        _check(self._lib.wn_condition_static(self._h, B, Tf, fp, int(T), cp, _stream_handle(stream)),
+               "wn_condition_static")
         return cond

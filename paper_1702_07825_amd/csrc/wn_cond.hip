@@ -19,6 +19,7 @@
 
 #include <algorithm>
 #include <cstring>
+#include <mutex>
 #include <vector>
 
 struct wn_cond {
@@ -27,7 +28,13 @@ struct wn_cond {
   int cinp1 = 0, cinp2 = 0;  // per-tap input widths of the two layers rounded up to 32
   void* dmem = nullptr;
   const float *w1 = nullptr, *b1 = nullptr, *w2 = nullptr, *b2 = nullptr;
+  void* scratch = nullptr;  // device address of this device's copy of `scratch` (wn_condition_static)
 };
+
+// Scratch of wn_condition_static: one copy per device, held until the process ends.  Host code
+// never uses the array's name as an address (on the host it is only a stand-in for the symbol);
+// wn_cond_create looks up each device's address of it once, with that device current.
+static __device__ __align__(256) unsigned char scratch[WN_COND_SCRATCH_BYTES];
 
 namespace {
 
@@ -292,6 +299,60 @@ std::vector<float> pad_taps(const float* w, int n, int cin, int cinp) {
   return out;
 }
 
+// Device address of `scratch` on device dev (the current device), looked up once per device.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices] = {};
+
+int scratch_address(int dev, void** out) {
+  if (dev < 0 || dev >= kMaxDevices) return wn_set_last_error(WN_EUNSUPPORTED, "device index beyond 63");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return wn_set_last_error(WN_EHIP, "hipGetSymbolAddress of the scratch array failed");
+    g_scratch_addr[dev] = p;
+  }
+  *out = g_scratch_addr[dev];
+  return WN_OK;
+}
+
+// The three kernels of one call, with the scratch at ws (cond_layout(c, B, n_frames) bytes).
+int run_condition(wn_cond* c, int B, int n_frames, const float* features, int T, float* cond, char* ws,
+                  hipStream_t st) {
+  const CondLayout l = cond_layout(c, B, n_frames);
+  float* p = reinterpret_cast<float*>(ws + l.p_off);
+  float* z1 = reinterpret_cast<float*>(ws + l.z1_off);
+  float* cf = reinterpret_cast<float*>(ws + l.c_off);
+  hipError_t e = run_layer(features, B, n_frames, c->F, c->cinp1, c->h1, c->w1, c->b1, p, z1, 0, st);
+  if (e == hipSuccess) e = run_layer(z1, B, n_frames, 2 * c->h1, c->cinp2, c->h2, c->w2, c->b2, p, cf, 1, st);
+  if (e == hipSuccess) {
+    const int C = 2 * c->h2;
+    const unsigned blocks = (unsigned)((long long)B * n_frames);
+    if (C % 4 == 0 && reinterpret_cast<uintptr_t>(cond) % 16 == 0)
+      hipLaunchKernelGGL(cond_repeat4, dim3(blocks), dim3(256), 0, st, reinterpret_cast<const f32x4*>(cf),
+                         reinterpret_cast<f32x4*>(cond), n_frames, (long long)T, C / 4, c->fr, c->ar);
+    else
+      hipLaunchKernelGGL(cond_repeat1, dim3(blocks), dim3(256), 0, st, cf, cond, n_frames, (long long)T, C, c->fr,
+                         c->ar);
+    e = hipGetLastError();
+  }
+  if (e != hipSuccess) return wn_set_last_error(WN_EHIP, hipGetErrorString(e));
+  return WN_OK;
+}
+
+// Checks shared by wn_condition and wn_condition_static (all but the workspace).
+int check_condition(const wn_cond* c, int B, int n_frames, const float* features, int T, const float* cond) {
+  if (!c) return wn_set_last_error(WN_EINVAL, "null handle");
+  if (B < 1 || n_frames < 1 || T < 0) return wn_set_last_error(WN_EINVAL, "B and n_frames must be >= 1, T >= 0");
+  if (T == 0) return WN_OK;
+  if (!features || !cond) return wn_set_last_error(WN_EINVAL, "null pointer");
+  if ((long long)B * n_frames > (1LL << 31) - 1) return wn_set_last_error(WN_EINVAL, "B * n_frames too large");
+  if ((long long)(T - 1) * c->fr / c->ar >= n_frames)
+    return wn_set_last_error(WN_EINVAL, "audio steps beyond the last frame");
+  return WN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -314,6 +375,13 @@ int wn_cond_create(const wn_cond_config* cfg, const wn_cond_weights* w, wn_cond*
   if (hipGetDevice(&c->device) != hipSuccess) {
     delete c;
     return wn_set_last_error(WN_EHIP, "hipGetDevice failed");
+  }
+  {
+    const int rc = scratch_address(c->device, &c->scratch);
+    if (rc != WN_OK) {
+      delete c;
+      return rc;
+    }
   }
   c->cinp1 = (c->F + 31) / 32 * 32;
   c->cinp2 = (2 * c->h1 + 31) / 32 * 32;
@@ -361,39 +429,30 @@ size_t wn_cond_workspace_bytes(const wn_cond* c, int32_t B, int32_t n_frames) {
 int wn_condition(wn_cond* c, int32_t B, int32_t n_frames, const float* features, int32_t T, float* cond,
                  void* workspace, size_t ws_bytes, void* stream) {
   wn_clear_last_error();
-  if (!c) return wn_set_last_error(WN_EINVAL, "null handle");
-  if (B < 1 || n_frames < 1 || T < 0) return wn_set_last_error(WN_EINVAL, "B and n_frames must be >= 1, T >= 0");
-  if (T == 0) return WN_OK;
-  if (!features || !cond || !workspace) return wn_set_last_error(WN_EINVAL, "null pointer");
+  int rc = check_condition(c, B, n_frames, features, T, cond);
+  if (rc != WN_OK || T == 0) return rc;
+  if (!workspace) return wn_set_last_error(WN_EINVAL, "null pointer");
   if (reinterpret_cast<uintptr_t>(workspace) % 256 != 0)
     return wn_set_last_error(WN_EINVAL, "workspace must be 256-byte aligned");
-  if ((long long)B * n_frames > (1LL << 31) - 1) return wn_set_last_error(WN_EINVAL, "B * n_frames too large");
-  if ((long long)(T - 1) * c->fr / c->ar >= n_frames)
-    return wn_set_last_error(WN_EINVAL, "audio steps beyond the last frame");
-  const CondLayout l = cond_layout(c, B, n_frames);
-  if (ws_bytes < l.total) return wn_set_last_error(WN_EINVAL, "workspace too small");
+  if (ws_bytes < cond_layout(c, B, n_frames).total) return wn_set_last_error(WN_EINVAL, "workspace too small");
   DeviceScope scope(c->device);
   if (!scope.ok()) return wn_set_last_error(WN_EHIP, "cannot select the handle's device");
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  char* ws = static_cast<char*>(workspace);
-  float* p = reinterpret_cast<float*>(ws + l.p_off);
-  float* z1 = reinterpret_cast<float*>(ws + l.z1_off);
-  float* cf = reinterpret_cast<float*>(ws + l.c_off);
-  hipError_t e = run_layer(features, B, n_frames, c->F, c->cinp1, c->h1, c->w1, c->b1, p, z1, 0, st);
-  if (e == hipSuccess) e = run_layer(z1, B, n_frames, 2 * c->h1, c->cinp2, c->h2, c->w2, c->b2, p, cf, 1, st);
-  if (e == hipSuccess) {
-    const int C = 2 * c->h2;
-    const unsigned blocks = (unsigned)((long long)B * n_frames);
-    if (C % 4 == 0 && reinterpret_cast<uintptr_t>(cond) % 16 == 0)
-      hipLaunchKernelGGL(cond_repeat4, dim3(blocks), dim3(256), 0, st, reinterpret_cast<const f32x4*>(cf),
-                         reinterpret_cast<f32x4*>(cond), n_frames, (long long)T, C / 4, c->fr, c->ar);
-    else
-      hipLaunchKernelGGL(cond_repeat1, dim3(blocks), dim3(256), 0, st, cf, cond, n_frames, (long long)T, C, c->fr,
-                         c->ar);
-    e = hipGetLastError();
-  }
-  if (e != hipSuccess) return wn_set_last_error(WN_EHIP, hipGetErrorString(e));
-  return WN_OK;
+  return run_condition(c, B, n_frames, features, T, cond, static_cast<char*>(workspace),
+                       static_cast<hipStream_t>(stream));
+}
+
+int wn_condition_static(wn_cond* c, int32_t B, int32_t n_frames, const float* features, int32_t T, float* cond,
+                        void* stream) {
+  wn_clear_last_error();
+  int rc = check_condition(c, B, n_frames, features, T, cond);
+  if (rc != WN_OK || T == 0) return rc;
+  if (cond_layout(c, B, n_frames).total > WN_COND_SCRATCH_BYTES)
+    return wn_set_last_error(WN_EINVAL, "B * n_frames needs more scratch than the static array holds "
+                                        "(wn_cond_workspace_bytes > WN_COND_SCRATCH_BYTES)");
+  DeviceScope scope(c->device);
+  if (!scope.ok()) return wn_set_last_error(WN_EHIP, "cannot select the handle's device");
+  return run_condition(c, B, n_frames, features, T, cond, static_cast<char*>(c->scratch),
+                       static_cast<hipStream_t>(stream));
 }
 
 void wn_cond_destroy(wn_cond* c) {

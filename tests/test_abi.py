@@ -124,5 +124,14 @@ def test_conditioning_network_rejects_before_any_device_call(lib):
     assert lib.wn_cond_create(None, None, None) == wn.WN_EINVAL
     assert lib.wn_cond_workspace_bytes(None, 1, 1) == 0
     assert lib.wn_condition(None, 1, 1, None, 1, None, None, 0, None) == wn.WN_EINVAL
+    assert lib.wn_condition_static(None, 1, 1, None, 1, None, None) == wn.WN_EINVAL
     lib.wn_cond_destroy(None)
 
+
+def test_static_scratch_size_matches_the_header():
+    """The binding's COND_SCRATCH_BYTES is the header's WN_COND_SCRATCH_BYTES."""
+    import paper_1702_07825_amd as wn
+    src = open(os.path.join(ROOT, "include", "wn_cond.h")).read()
+    m = re.search(r"#define\s+WN_COND_SCRATCH_BYTES\s+\(\(size_t\)(\d+)\s*<<\s*(\d+)\)", src)
+    assert m
+    assert wn.COND_SCRATCH_BYTES == int(m.group(1)) << int(m.group(2))
