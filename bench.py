@@ -8,6 +8,8 @@ HBM.  Prints ONE JSON line on stdout:
              per sample of the model) over its average launch duration, from HIP
              events on the stream the kernel runs on, against the chip's peak
   cpu_baseline  the CPU oracle timed on this host on a bounded sample
+  batched    (default workload only) a few launches of each batched workload, timed after the
+             headline's timed region, with their own roofline records
 Default workload: l=20, r=64, s=256, B=1, T=16000 (1 s of 16 kHz audio), fp32.
 """
 import argparse
@@ -74,6 +76,20 @@ def traffic_from_profiles(workload, variant):
     return rec.get("hbm_bytes_per_launch")
 
 
+# The oracle computes in double precision (plain sequential C, gcc -O2) and takes each draw in fp32,
+# the precision of the paper's inference kernels: as slow as or slower than an fp32 oracle would be.
+ORACLE_PRECISION = "fp64 arithmetic, draws compared in fp32"
+
+
+def host_cores():
+    """CPUs this process may run on (the host's nproc) and the machine's total."""
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = os.cpu_count()
+    return {"nproc": avail, "machine": os.cpu_count()}
+
+
 def cpu_baseline(wl, w, cond_dev, u_np, min_seconds):
     """The CPU oracle on whole streams of the workload (stream 0, 1, ...; stream 0 again when the
     workload has one), one thread, until at least `min_seconds` of oracle time have passed."""
@@ -91,6 +107,8 @@ def cpu_baseline(wl, w, cond_dev, u_np, min_seconds):
     which = ("stream 0, %d runs" % len(runs)) if wl.B == 1 else \
             ("streams 0..%d" % (len(runs) - 1) if len(runs) <= wl.B else "streams 0..%d, %d runs" % (wl.B - 1, len(runs)))
     return {"value": steps / secs, "unit": "samples/s", "cores": 1, "kind": "oracle",
+            "host_cores": host_cores(),
+            "precision": ORACLE_PRECISION,
             "sample": "whole streams of %d steps (%s), generation, one thread, fp64 C oracle" % (wl.T, which),
             "seconds": round(secs, 2)}
 
@@ -101,36 +119,18 @@ def algorithmic_hbm_bytes_per_sample(wl):
     return wl.n_layers * 2 * wl.r * 4 + 4 + 4 + 2 * wl.n_layers * wl.r * 4
 
 
-def run_workload(name, args):
-    import numpy as np
+def _timed_launches(net, cond, u, samples, ws, steps, warmup):
+    """`warmup` untimed then `steps` timed wn_generate calls from a reset state; returns the wall
+    time of the timed calls and the average launch duration from HIP events on the stream."""
     import torch
-
-    import synth
-    import paper_1702_07825_amd as wn
-
-    wl = synth.WORKLOADS[name]
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    w = synth.make_weights(wl.n_layers, wl.r, wl.s, seed=args.seed, embed_taps=wl.embed_taps)
-    net = wn.WaveNet(w, wl.dilations, weight_dtype=wl.weight_dtype)
-    cond = synth.make_cond(wl.n_layers, wl.r, wl.B, wl.T, seed=args.seed, device="cuda:0")
-    u_np = synth.make_uniforms(wl.B, wl.T, seed=args.seed)
-    u = torch.tensor(u_np, device=dev)
-    samples = torch.empty((wl.B, wl.T), dtype=torch.int32, device=dev)
-    ws = net.new_workspace(wl.B, dev)
-    variant = net.kernel_variant(wl.B)
-    wgs, reps = net.launch_info(wl.B)
-    print("bench: %s, kernel %s, %d warmup + %d timed steps" % (wl.description, variant, args.warmup, args.steps),
-          file=sys.stderr, flush=True)
-
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         net.generate(cond, u, samples=samples, workspace=ws, reset=True)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.steps):
+    for i in range(steps):
         ev[i][0].record(stream)
         net.generate(cond, u, samples=samples, workspace=ws, reset=True)
         ev[i][1].record(stream)
@@ -138,15 +138,16 @@ def run_workload(name, args):
     elapsed = time.perf_counter() - t0
     assert net.status(ws) == 0
     launch_ms = [a.elapsed_time(b) for a, b in ev]
-    avg_launch_s = sum(launch_ms) / len(launch_ms) / 1e3
+    return elapsed, sum(launch_ms) / len(launch_ms) / 1e3
 
+
+def _roofline(name, wl, variant, avg_launch_s, wgs, reps):
+    """The dominant kernel's roofline record for one launch of the whole workload."""
     n = wl.B * wl.T
-    value = n * args.steps / elapsed
     flop_per_launch = 2.0 * macs_per_sample(wl.n_layers, wl.r, wl.s) * n
     # The batched kernel computes its products on bf16 MFMA; the others on the fp32 vector ALUs.
     bound, peak = ("mfma", PEAKS["bf16_mfma_tflops"]) if variant == "mfma_group" else ("alu", PEAKS["f32_vector_tflops"])
     achieved = flop_per_launch / avg_launch_s / 1e12
-    per_stream_rate = wl.T / avg_launch_s
     hbm_alg = algorithmic_hbm_bytes_per_sample(wl) * n
     onchip = None
     if variant == "multi_cu_chain":
@@ -158,6 +159,83 @@ def run_workload(name, args):
                   "achieved_gbs": round(wbytes / avg_launch_s / 1e9, 2), "peak_gbs": round(lds_gbs, 1),
                   "peak_basis": "%d B/clk/CU x %.1f GHz x workgroups" % (LDS_BYTES_PER_CLK_PER_CU, SHADER_CLOCK_GHZ),
                   "frac": round(wbytes / avg_launch_s / 1e9 / lds_gbs, 6)}
+    return {
+        "bound": bound,
+        "achieved": round(achieved, 4),
+        "peak": peak,
+        "unit": "TFLOP/s",
+        "frac": round(achieved / peak, 6),
+        "traffic": traffic_from_profiles(name, variant),
+        "algorithmic_flop_per_launch": flop_per_launch,
+        "hbm": {"algorithmic_bytes_per_launch": hbm_alg,
+                "achieved_gbs": round(hbm_alg / avg_launch_s / 1e9, 2),
+                "peak_gbs": PEAKS["hbm_gbs"],
+                "frac": round(hbm_alg / avg_launch_s / 1e9 / PEAKS["hbm_gbs"], 6)},
+        "onchip": onchip,
+        "avg_launch_ms": round(avg_launch_s * 1e3, 4),
+    }
+
+
+def _setup_workload(name, seed):
+    import torch
+    import synth
+    import paper_1702_07825_amd as wn
+    wl = synth.WORKLOADS[name]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = synth.make_weights(wl.n_layers, wl.r, wl.s, seed=seed, embed_taps=wl.embed_taps)
+    net = wn.WaveNet(w, wl.dilations, weight_dtype=wl.weight_dtype)
+    cond = synth.make_cond(wl.n_layers, wl.r, wl.B, wl.T, seed=seed, device="cuda:0")
+    u_np = synth.make_uniforms(wl.B, wl.T, seed=seed)
+    u = torch.tensor(u_np, device=dev)
+    samples = torch.empty((wl.B, wl.T), dtype=torch.int32, device=dev)
+    ws = net.new_workspace(wl.B, dev)
+    return wl, w, net, cond, u_np, u, samples, ws
+
+
+# Batched workloads timed beside the headline (outside its timed region), so that their roofline
+# fractions appear in the benchmark's own record.
+BATCHED = ["l20_r128_b32", "l20_r64_b256_bf16"]
+
+
+def batched_record(args):
+    """A few launches of each batched workload: per-step time, throughput and roofline fractions."""
+    import torch
+    rec = {}
+    for name in BATCHED:
+        wl, w, net, cond, u_np, u, samples, ws = _setup_workload(name, args.seed)
+        variant = net.kernel_variant(wl.B)
+        wgs, reps = net.launch_info(wl.B)
+        print("bench: batched record %s, kernel %s, 1 warmup + %d timed steps" % (wl.description, variant,
+              args.batched_steps), file=sys.stderr, flush=True)
+        _, avg_s = _timed_launches(net, cond, u, samples, ws, args.batched_steps, 1)
+        rf = _roofline(name, wl, variant, avg_s, wgs, reps)
+        rec[name] = {"workload": wl.description, "kernel": variant, "workgroups": wgs, "replicas": reps,
+                     "source_digest": kernel_source_digest(variant), "launches": args.batched_steps,
+                     "samples_per_s": round(wl.B * wl.T / avg_s, 1),
+                     "us_per_sample_step": round(avg_s / wl.T * 1e6, 3),
+                     "real_time_factor_16khz": round(wl.T / avg_s / RATE_HZ, 3),
+                     "roofline": rf}
+        net.close()
+        del cond, u, samples, ws
+        torch.cuda.empty_cache()
+    return rec
+
+
+def run_workload(name, args, batched=False):
+    import numpy as np
+    import torch
+
+    wl, w, net, cond, u_np, u, samples, ws = _setup_workload(name, args.seed)
+    variant = net.kernel_variant(wl.B)
+    wgs, reps = net.launch_info(wl.B)
+    print("bench: %s, kernel %s, %d warmup + %d timed steps" % (wl.description, variant, args.warmup, args.steps),
+          file=sys.stderr, flush=True)
+    elapsed, avg_launch_s = _timed_launches(net, cond, u, samples, ws, args.steps, args.warmup)
+
+    n = wl.B * wl.T
+    value = n * args.steps / elapsed
+    per_stream_rate = wl.T / avg_launch_s
     y = samples.cpu().numpy()
     out = {
         "metric": "generated samples/s (16 kHz mu-law audio, all streams)",
@@ -180,21 +258,7 @@ def run_workload(name, args):
         "real_time_factor_48khz": round(per_stream_rate / HI_RATE_HZ, 3),
         "real_time_factor_at_workload_rate": round(per_stream_rate / wl.sample_rate, 3),
         "us_per_sample_step": round(avg_launch_s / wl.T * 1e6, 3),
-        "roofline": {
-            "bound": bound,
-            "achieved": round(achieved, 4),
-            "peak": peak,
-            "unit": "TFLOP/s",
-            "frac": round(achieved / peak, 6),
-            "traffic": traffic_from_profiles(name, variant),
-            "algorithmic_flop_per_launch": flop_per_launch,
-            "hbm": {"algorithmic_bytes_per_launch": hbm_alg,
-                    "achieved_gbs": round(hbm_alg / avg_launch_s / 1e9, 2),
-                    "peak_gbs": PEAKS["hbm_gbs"],
-                    "frac": round(hbm_alg / avg_launch_s / 1e9 / PEAKS["hbm_gbs"], 6)},
-            "onchip": onchip,
-            "avg_launch_ms": round(avg_launch_s * 1e3, 4),
-        },
+        "roofline": _roofline(name, wl, variant, avg_launch_s, wgs, reps),
         "sample_histogram_entropy_bits": round(float(-(lambda p: (p[p > 0] * np.log2(p[p > 0])).sum())(
             np.bincount(y.ravel(), minlength=256) / y.size)), 3),
     }
@@ -202,10 +266,12 @@ def run_workload(name, args):
         out["cpu_baseline"] = cpu_baseline(wl, w, cond, u_np, args.cpu_seconds)
     else:
         out["cpu_baseline"] = None
-    print(json.dumps(out), flush=True)
     net.close()
     del cond, u, samples, ws
     torch.cuda.empty_cache()
+    if batched and args.batched_steps > 0:
+        out["batched"] = batched_record(args)
+    print(json.dumps(out), flush=True)
 
 
 def cond_flops(wl):
@@ -229,6 +295,7 @@ def cond_cpu_baseline(wl, w, x_dev, min_seconds):
         steps += wl.T
         runs += 1
     return {"value": steps / secs, "unit": "samples/s", "cores": 1, "kind": "oracle",
+            "host_cores": host_cores(), "precision": ORACLE_PRECISION,
             "sample": "%d whole utterance(s) of %d frames -> %d audio steps, one thread, fp64 C oracle" %
                       (runs, wl.n_frames, wl.T), "seconds": round(secs, 2)}
 
@@ -311,6 +378,9 @@ def main():
                     help="least oracle time for the CPU baseline, in whole streams (0 = skip)")
     ap.add_argument("--cpu-steps", type=int, default=None, choices=[0], help="0: skip the CPU baseline")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--batched-steps", type=int, default=2,
+                    help="timed launches of each batched workload recorded beside the default headline "
+                         "(after its timed region; 0 = skip)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run one device-to-device copy of BYTES (calibrates HBM byte counters) and exit")
     args = ap.parse_args()
@@ -335,7 +405,7 @@ def main():
         if name in synth.COND_WORKLOADS:
             run_cond_workload(name, args)
         else:
-            run_workload(name, args)
+            run_workload(name, args, batched=(args.workload == "l20_r64_b1"))
 
 
 if __name__ == "__main__":

@@ -176,8 +176,18 @@ def _window(w, dil, dtype, cond_b, u_b, y_b, t):
 FULL = ["l20_r64_b1", "l40_r64_b1", "tiny", "l20_r128_b32", "l20_r64_b256_bf16", "l20_r64_b1_2tap_48k"]
 
 
+def _whole_stream(w, dil, dtype, cb, ub, yb):
+    """The oracle teacher-forced over a whole stream: logits, draws and margins of every step."""
+    m = oracle.Model(w, dil, bf16_weights=(dtype == "bf16"))
+    return oracle.run(m, cb, u=ub, y_in=yb)
+
+
 @pytest.mark.parametrize("name", FULL)
 def test_full_size_sampled(name):
+    """At the benchmark's full sizes, in the launch the benchmark times: every step of stream 0
+    (the oracle replays the GPU's whole sample sequence, teacher-forced, past every wrap of the
+    d = 512 histories), plus sampled steps of the last and the middle stream of a batch (each
+    checked on a window of sum(d) + 1 steps, the receptive field)."""
     wl = synth.WORKLOADS[name]
     _log("full-size %s: %s" % (name, wl.description))
     w = synth.make_weights(wl.n_layers, wl.r, wl.s, seed=0, embed_taps=wl.embed_taps)
@@ -192,23 +202,76 @@ def test_full_size_sampled(name):
     assert y_np.min() >= 0 and y_np.max() <= 255
     rng = np.random.default_rng(0)
     jobs = []
-    for b in sorted(set([0, wl.B - 1, wl.B // 2])):
-        steps = sorted(set([wl.T - 1] + [int(x) for x in rng.integers(0, wl.T, 2 if b == 0 else 1)]))
+    for b in sorted(set([wl.B - 1, wl.B // 2]) - {0}):
+        steps = sorted(set([wl.T - 1] + [int(x) for x in rng.integers(0, wl.T, 1)]))
         cb, ub = cond[b].cpu().numpy(), u[b].cpu().numpy()
         for t in steps:
             jobs.append((b, t, cb, ub, lg[b, t].cpu().numpy()))
+    c0, u0, lg0 = cond[0].cpu().numpy(), u[0].cpu().numpy(), lg[0].cpu().numpy()
     with ThreadPoolExecutor(max_workers=8) as ex:
+        whole = ex.submit(_whole_stream, w, wl.dilations, wl.weight_dtype, c0, u0, y_np[0])
         res = list(ex.map(lambda j: _window(w, wl.dilations, wl.weight_dtype, j[2], j[3], y_np[j[0]], j[1]), jobs))
+        ys0, lo0, mg0 = whole.result()
+    worst0 = float(np.abs(lo0 - lg0).max())
+    ok0 = mg0 > MARGIN
+    mism0 = int(np.sum(ys0[ok0] != y_np[0][ok0]))
+    _log("  stream 0, all %d steps: max|dlogit|=%.3g confident=%d mismatches=%d" %
+         (wl.T, worst0, int(ok0.sum()), mism0))
     worst, checked, mism = 0.0, 0, 0
     for (b, t, _, _, lg_bt), (lo, yo, mg) in zip(jobs, res):
         worst = max(worst, float(np.abs(lo - lg_bt).max()))
         if mg > MARGIN:
             checked += 1
             mism += int(yo != y_np[b, t])
-    _log("  %d sampled (stream, step) pairs: max|dlogit|=%.3g confident=%d mismatches=%d" %
+    _log("  %d sampled (stream, step) pairs of other streams: max|dlogit|=%.3g confident=%d mismatches=%d" %
          (len(jobs), worst, checked, mism))
+    assert worst0 <= LOGIT_TOL[wl.weight_dtype] and mism0 == 0
     assert worst <= LOGIT_TOL[wl.weight_dtype]
     assert mism == 0
+    net.close()
+
+
+WRAP = [
+    # name, r, s, B, dtype, expected kernel
+    ("chain_b1", 64, 256, 1, "f32", "multi_cu_chain"),
+    ("chain_b3", 64, 256, 3, "f32", "multi_cu_chain"),
+    ("chain_r128_b2", 128, 256, 2, "f32", "multi_cu_chain"),
+    ("group_b9", 64, 256, 9, "bf16", "mfma_group"),
+]
+
+
+@pytest.mark.parametrize("case", WRAP, ids=[c[0] for c in WRAP])
+def test_chunks_across_history_wraps(case):
+    """l = 20 with dilations up to 512 over 1100 steps, in chunks whose boundaries straddle steps
+    512 and 1024 (where the d = 512 histories wrap): chunked generation and teacher forcing equal
+    the one-shot call bit for bit, and the one-shot call matches the oracle on every step."""
+    name, r, s, B, dtype, kern = case
+    L, T = 20, 1100
+    dil = tuple(synth.dilation_cycle(L))
+    _log("wrap case %s: L=%d r=%d B=%d T=%d" % (name, L, r, B, T))
+    w, net, cond, u, model = _setup(L, r, s, dil, B, T, seed=zlib.crc32(name.encode()) % 1000, dtype=dtype, bias=0.2)
+    assert net.kernel_variant(B) == kern
+    y = net.generate(cond, u)
+    lg = net.teacher_force(cond, y)
+    ws = net.new_workspace(B)
+    ws2 = net.new_workspace(B)
+    parts, lparts, a = [], [], 0
+    for b_ in (1, 511, 513, 1023, 1025, T):
+        parts.append(net.generate(cond[:, a:b_].contiguous(), u[:, a:b_].contiguous(), workspace=ws, reset=(a == 0)))
+        lparts.append(net.teacher_force(cond[:, a:b_].contiguous(), y[:, a:b_].contiguous(), workspace=ws2,
+                                        reset=(a == 0)))
+        a = b_
+    torch.cuda.synchronize()
+    assert net.status(ws) == 0 and net.status(ws2) == 0
+    assert torch.equal(torch.cat(parts, 1), y)
+    assert torch.equal(torch.cat(lparts, 1), lg)
+    y_np = y.cpu().numpy()
+    ys, lo, mg = oracle.run_streams(model, cond.cpu().numpy(), u=u.cpu().numpy(), y_in=y_np, threads=8)
+    err = float(np.abs(lg.cpu().numpy() - lo).max())
+    ok = mg > MARGIN
+    mism = int(np.sum(ys[ok] != y_np[ok]))
+    _log("  max|dlogit|=%.3g confident=%d/%d mismatches=%d" % (err, int(ok.sum()), ok.size, mism))
+    assert err <= LOGIT_TOL[dtype] and mism == 0
     net.close()
 
 
