@@ -43,6 +43,8 @@
  *      WN_LOCAL_POSTS=0      each call: the multi-CU kernel writes every message through to
  *                            memory instead of stopping same-XCD messages at the XCD's L2
  *      WN_GROUP_STREAMS=8|16 each call: streams per workgroup of the batched bf16 kernel
+ *      WN_AUX_LAYERS=1       each call: the multi-CU kernel gives each aux CU one layer instead of
+ *                            two (r <= 64); it changes the launch layout and the workspace size
  *    Apart from a small WN_SPIN_LIMIT, which can make a wait time out, none of them changes a
  *    result beyond rounding.
  */

@@ -50,6 +50,7 @@
 #include "wn.h"
 
 #include <algorithm>
+#include <cstdlib>
 #include <type_traits>
 
 namespace {
@@ -705,112 +706,158 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
 }
 
 // ------------------------------------------------------------------------------------------
-// aux CU (one per layer): pre-activations of the next step and the skip partial
+// aux CU (nla consecutive layers): pre-activations of the next step and the skip partial
 // ------------------------------------------------------------------------------------------
+// Layers one aux CU can hold: W_prev and W_skip of a layer take 48 floats per lane at r = 64,
+// s = 256 (two layers fit the register file), 128 at r = 128 (one).
+template <int R>
+constexpr int aux_max_layers() { return R <= 64 ? 2 : 1; }
+
 template <int R, int S, bool TF, bool MS>
-__device__ void aux_role(const WnChainArgs& g, const int j, const int b0, const int ns, float* dyn, Sync sy,
+__device__ void aux_role(const WnChainArgs& g, const int ai, const int b0, const int ns, float* dyn, Sync sy,
                          const int64_t tg0, const unsigned lm) {
   using M = ChainMap<R>;
+  constexpr int NLA = aux_max_layers<R>();
   constexpr int LPRS = NT / S, KCS = R / LPRS;
-  constexpr int CQ = (WN_CHAIN_MAX_G * 2 * R / 4 + NT - 1) / NT;  // conditioning float4s per thread
+  constexpr int CQ = (WN_CHAIN_MAX_G * 2 * R / 4 + NT - 1) / NT;  // conditioning float4s per thread and layer
   const int tid = threadIdx.x;
-  const int L = g.d.L, d = g.d.dil[j];
+  const int L = g.d.L;
   const int T = g.io.T;
   const int G = MS ? g.G : 1;
-  float* hs = dyn;            // R     h_j of the current stream
-  float* xpg = hs + R;        // G*R   history reads x_{j-1}[ts - d] of every stream
-  float* clg = xpg + G * R;   // G*2R  conditioning rows L[b, ts, j] of every stream
+  const int ja = ai * g.nla, nl = min(g.nla, L - ja);  // my layers: ja .. ja + nl - 1
+  // layers whose skip projection this CU computes (the last layer's runs on the last chain CU when
+  // it has room for that W_skip); their sum goes to the head CUs as one partial per step
+  const int nsk = (g.tail_on_chain && ja + nl == L) ? nl - 1 : nl;
+  float* hs = dyn;                 // NLA*R     h_j of the current stream, one row per layer
+  float* xpg = hs + NLA * R;       // NLA*G*R   history reads x_{j-1}[ts - d] of every (layer, stream)
+  float* clg = xpg + NLA * G * R;  // NLA*G*2R  conditioning rows L[b, ts, j] of every (layer, stream)
 
   const int rowp = tid / M::LPR1, kq = tid % M::LPR1;
   const int rows = tid / LPRS, ks = tid % LPRS;
-  float wp[M::KC1], wk[KCS];
+  float wp[NLA][M::KC1], wk[NLA][KCS], bg[NLA];
+  int dl[NLA], ho[NLA];  // dilation and history offset of each layer (uniform, kept in registers)
   const float* Wp = static_cast<const float*>(g.w.w_prev);
   const float* Wk = static_cast<const float*>(g.w.w_skip);
 #pragma unroll
-  for (int i = 0; i < M::KC1; ++i) wp[i] = Wp[((size_t)j * 2 * R + rowp) * R + kq * M::KC1 + i];
+  for (int l = 0; l < NLA; ++l) {
+    const int j = ja + (l < nl ? l : 0);
 #pragma unroll
-  for (int i = 0; i < KCS; ++i) wk[i] = Wk[((size_t)j * S + rows) * R + ks * KCS + i];
-  const float bg = g.w.b_gate[j * 2 * R + rowp];
+    for (int i = 0; i < M::KC1; ++i) wp[l][i] = Wp[((size_t)j * 2 * R + rowp) * R + kq * M::KC1 + i];
+#pragma unroll
+    for (int i = 0; i < KCS; ++i) wk[l][i] = Wk[((size_t)j * S + rows) * R + ks * KCS + i];
+    bg[l] = g.w.b_gate[j * 2 * R + rowp];
+    dl[l] = g.d.dil[j];
+    ho[l] = g.d.hoff[j];
+  }
 
-  // The history slot that pre_j[ts] reads, for every stream of the replica (consecutive streams'
-  // histories are hist_len words apart).
-  auto hist_items = [&](int64_t ts) {
+  // The history slot that pre_j[ts] reads for every stream of the replica (consecutive streams'
+  // histories are hist_len words apart), j = ja + l.
+  auto hist_items = [&](int l, int64_t ts) {
+    const int d = dl[l];
     const int slot = (d == 1) ? 0 : (int)(ts % d);
     const unsigned etag = (ts - d >= 0) ? (unsigned)(ts - d + 1) : 0u;
-    return Items{g.ring + (size_t)b0 * g.d.hist_len + g.d.hoff[j] + (size_t)slot * R, R, g.d.hist_len, ns * R, xpg,
-                 etag};
+    return Items{g.ring + (size_t)b0 * g.d.hist_len + ho[l] + (size_t)slot * R, R, g.d.hist_len, ns * R,
+                 xpg + l * G * R, etag};
   };
-  // Stage the inputs of pre_j[ts] for every stream at once: the conditioning rows (one HBM round
-  // trip for all streams) and, when `hist`, the history reads.  The history of ts - d is final
-  // once step ts - d is over, so it is staged here when d >= 2 or at the call's first step; with
-  // d = 1 it is read per stream, together with h_j (both come from the same chain CU).
-  auto stage = [&](int64_t ts, bool hist) {
-    float4 cq[CQ];
-    const float* crow = g.io.cond + ((size_t)b0 * T + (size_t)(ts - tg0)) * L * 2 * R + (size_t)j * 2 * R;
+  // Stage the inputs of pre_j[ts] for every layer and stream at once: the conditioning rows (one HBM
+  // round trip for all of them) and, when `all_hist`, every history read; otherwise the history reads
+  // of the layers with d >= 2, which are final once step ts - d is over (with d = 1 the read waits for
+  // the chain CU's step and is made per stream, together with h_j).
+  auto stage = [&](int64_t ts, bool all_hist) {
+    float4 cq[NLA][CQ];
 #pragma unroll
-    for (int k = 0; k < CQ; ++k) {
-      const int q = tid + k * NT;
-      if (q < ns * (2 * R / 4)) {
-        const int i = q / (2 * R / 4), e = q % (2 * R / 4);
-        cq[k] = *reinterpret_cast<const float4*>(crow + (size_t)i * T * L * 2 * R + 4 * e);
+    for (int l = 0; l < NLA; ++l) {
+      if (l < nl) {
+        const float* crow = g.io.cond + ((size_t)b0 * T + (size_t)(ts - tg0)) * L * 2 * R + (size_t)(ja + l) * 2 * R;
+#pragma unroll
+        for (int k = 0; k < CQ; ++k) {
+          const int q = tid + k * NT;
+          if (q < ns * (2 * R / 4)) {
+            const int i = q / (2 * R / 4), e = q % (2 * R / 4);
+            cq[l][k] = *reinterpret_cast<const float4*>(crow + (size_t)i * T * L * 2 * R + 4 * e);
+          }
+        }
       }
     }
-    if (hist) poll2(g, hist_items(ts), no_items(), dyn, sy);
+    const bool h0 = nl > 0 && (all_hist || dl[0] >= 2);
+    const bool h1 = NLA > 1 && nl > 1 && (all_hist || dl[NLA > 1 ? 1 : 0] >= 2);
+    if (h0 || h1)
+      poll2(g, h0 ? hist_items(0, ts) : no_items(), h1 ? hist_items(NLA > 1 ? 1 : 0, ts) : no_items(), dyn, sy);
 #pragma unroll
-    for (int k = 0; k < CQ; ++k) {
-      const int q = tid + k * NT;
-      if (q < ns * (2 * R / 4)) reinterpret_cast<float4*>(clg)[q] = cq[k];
+    for (int l = 0; l < NLA; ++l) {
+      if (l < nl) {
+#pragma unroll
+        for (int k = 0; k < CQ; ++k) {
+          const int q = tid + k * NT;
+          if (q < ns * (2 * R / 4)) reinterpret_cast<float4*>(clg + l * G * 2 * R)[q] = cq[l][k];
+        }
+      }
     }
     lds_barrier();
   };
-  // pre_j[ts] of local stream i = W_prev x_{j-1}[ts - d] + B + L[b, ts], posted with tag ts + 1
-  auto post_pre = [&](int64_t ts, int i) {
-    const float a = gsum<M::LPR1>(dot_lds<M::KC1>(wp, xpg + i * R + kq * M::KC1));
+  // pre_j[ts] of local stream i = W_prev x_{j-1}[ts - d] + B + L[b, ts], j = ja + l, tag ts + 1
+  auto post_pre = [&](int l, int64_t ts, int i) {
+    const float a = gsum<M::LPR1>(dot_lds<M::KC1>(wp[l], xpg + (l * G + i) * R + kq * M::KC1));
     if (kq == 0)
-      stw(g.mb + (size_t)(b0 + i) * g.mb_words + ((size_t)j * 2 + (ts & 1)) * 2 * R + rowp,
-          pack(a + bg + clg[i * 2 * R + rowp], (unsigned)(ts + 1)), lm & 1u);
+      stw(g.mb + (size_t)(b0 + i) * g.mb_words + ((size_t)(ja + l) * 2 + (ts & 1)) * 2 * R + rowp,
+          pack(a + bg[l] + clg[(l * G + i) * 2 * R + rowp], (unsigned)(ts + 1)), (lm >> l) & 1u);
   };
 
   stage(tg0, true);
   if (sy.failed()) return;
-  for (int i = 0; i < ns; ++i) post_pre(tg0, i);
-  // the last layer's skip projection runs on the last chain CU when it has room for W_skip
-  const bool skip_here = (j < L - 1) || !g.tail_on_chain;
+  for (int i = 0; i < ns; ++i)
+#pragma unroll
+    for (int l = 0; l < NLA; ++l)
+      if (l < nl) post_pre(l, tg0, i);
   for (int64_t t = tg0; t < tg0 + T; ++t) {
     const bool more = (t + 1 < tg0 + T);
-    // A host abort request, read every WN_ABORT_CHECK steps by the first layer's aux CU, which
+    // A host abort request, read every WN_ABORT_CHECK steps by the replica's first aux CU, which
     // works a step ahead of the chain, so the read's PCIe round trip stays off the critical path.
     // It stops here; every other role sees the status word in its next wait and leaves too.
-    if (j == 0 && threadIdx.x == 0 && ((t - tg0) & (WN_ABORT_CHECK - 1)) == 0 && abort_requested(g.io.abort_flag)) {
+    if (ai == 0 && threadIdx.x == 0 && ((t - tg0) & (WN_ABORT_CHECK - 1)) == 0 && abort_requested(g.io.abort_flag)) {
       atomicCAS(g.status, 0, (int)WN_EABORTED);
       *sy.flag = 1;
     }
     lds_barrier();
     if (sy.failed()) return;
-    if (more) stage(t + 1, d >= 2);
+    if (more) stage(t + 1, false);
     if (sy.failed()) return;
     for (int i = 0; i < ns; ++i) {
       const int b = b0 + i;
       u64* const mbs = g.mb + (size_t)b * g.mb_words;
-      // Waiting for h_j[t] also paces this CU: once it has arrived the chain has consumed
-      // pre_j[t], so posting pre_j[t + 1] below cannot overwrite a slot the chain has yet to read.
-      const Items hi{mbs + g.off_h + ((size_t)j * 2 + (t & 1)) * R, R, R, R, hs, (unsigned)(t + 1)};
-      if (more && d == 1) {
-        Items xi = hist_items(t + 1);
-        xi.base += (size_t)i * g.d.hist_len;
-        xi.n = R;
-        xi.dst = xpg + i * R;
-        poll2(g, hi, xi, dyn, sy);
-      } else {
-        poll2(g, hi, no_items(), dyn, sy);
+      float q = 0.f;  // this thread's row of the skip partial, summed over my layers
+#pragma unroll
+      for (int l = 0; l < NLA; ++l) {
+        if (l < nl) {
+          const int j = ja + l;
+          // Waiting for h_j[t] also paces this CU: once it has arrived the chain has consumed
+          // pre_j[t], so posting pre_j[t + 1] below cannot overwrite a slot the chain has yet to read.
+          const Items hi{mbs + g.off_h + ((size_t)j * 2 + (t & 1)) * R, R, R, R, hs + l * R, (unsigned)(t + 1)};
+          if (more && dl[l] == 1) {
+            Items xi = hist_items(l, t + 1);
+            xi.base += (size_t)i * g.d.hist_len;
+            xi.n = R;
+            xi.dst = xpg + (l * G + i) * R;
+            poll2(g, hi, xi, dyn, sy);
+          } else {
+            poll2(g, hi, no_items(), dyn, sy);
+          }
+          lds_barrier();
+          if (sy.failed()) return;
+          if (l < nsk) {
+            q += gsum<LPRS>(dot_lds<KCS>(wk[l], hs + l * R + ks * KCS));
+            // the partial goes out as soon as its last layer is in: a later layer of this CU (the
+            // network's last, whose skip is on the chain) only paces the pre-activations
+            if (l == nsk - 1 && ks == 0)
+              stw(mbs + g.off_q + ((size_t)ai * 2 + (t & 1)) * S + rows, pack(q, (unsigned)(t + 1)), (lm >> 16) & 1u);
+          }
+        }
       }
-      lds_barrier();
-      if (sy.failed()) return;
-      if (skip_here) {
-        const float q = gsum<LPRS>(dot_lds<KCS>(wk, hs + ks * KCS));
-        if (ks == 0) stw(mbs + g.off_q + ((size_t)j * 2 + (t & 1)) * S + rows, pack(q, (unsigned)(t + 1)), (lm >> 1) & 1u);
+      if (more) {
+#pragma unroll
+        for (int l = 0; l < NLA; ++l)
+          if (l < nl) post_pre(l, t + 1, i);
       }
-      if (more) post_pre(t + 1, i);
       lds_barrier();
     }
   }
@@ -827,8 +874,8 @@ __device__ void head_role(const WnChainArgs& g, const int hh, const int b0, cons
   const int tid = threadIdx.x;
   const int L = g.d.L;
   const int T = g.io.T;
-  const int nq = g.tail_on_chain ? L - 1 : L;  // skip partials that come from aux CUs
-  float* qall = dyn;           // L*S skip partials of one step: layers 0..nq-1, then the tail
+  const int nq = g.naux_q;      // skip partials that come from aux CUs (one per aux CU with a skip layer)
+  float* qall = dyn;           // (nq + 1)*S skip partials of one step: the aux CUs', then the tail
   float* zs = qall + L * S;    // S
   float* za = zs + S;          // HR
   float* qpart = za + HR;      // NT per-thread partial sums
@@ -851,14 +898,14 @@ __device__ void head_role(const WnChainArgs& g, const int hh, const int b0, cons
     const int par = (int)(t & 1);
     for (int i = 0; i < ns; ++i) {
       u64* const mbs = g.mb + (size_t)(b0 + i) * g.mb_words;
-      // all skip partials of this step: W_skip_j h_j from the aux CUs and (when the last chain
-      // CU computes it) the last layer's.  Item i is channel i mod S of layer i / S and the
-      // thread of item i is i mod NT, so thread tid polls channel tid mod S of every (NT / S)-th
-      // layer and sums those as they arrive; the NT / S partial sums of a channel then meet in
+      // all skip partials of this step: sum_j W_skip_j h_j over each aux CU's layers and (when the
+      // last chain CU computes it) the last layer's.  Item i is channel i mod S of partial i / S and
+      // the thread of item i is i mod NT, so thread tid polls channel tid mod S of every (NT / S)-th
+      // partial and sums those as they arrive; the NT / S partial sums of a channel then meet in
       // LDS, in a fixed order.
       float part = 0.f;
       poll2<12>(g, Items{mbs + g.off_q + (size_t)par * S, S, 2 * S, nq * S, qall, tag},
-                nq < L ? Items{mbs + g.off_qtail + (size_t)par * S, S, S, S, qall + (L - 1) * S, tag} : no_items(),
+                g.tail_on_chain ? Items{mbs + g.off_qtail + (size_t)par * S, S, S, S, qall + nq * S, tag} : no_items(),
                 dyn, sy, &part);
       qpart[tid] = part;
       lds_barrier();
@@ -891,7 +938,7 @@ __global__ __launch_bounds__(NT) void wn_chain_kernel(const WnChainArgs g) {
   __shared__ int s_abort;
   const int rb = g.role_of_block[blockIdx.x];
   if (rb == 0xffff) return;
-  const int per = g.nch + NHEAD + g.d.L;
+  const int per = g.nch + NHEAD + g.naux;
   const int k = MS ? rb / per : 0, role = rb - k * per;
   const int b0 = MS ? k * g.G : 0;
   const int ns = MS ? min(g.G, g.io.B - b0) : 1;  // streams of this replica
@@ -899,31 +946,66 @@ __global__ __launch_bounds__(NT) void wn_chain_kernel(const WnChainArgs g) {
   if (threadIdx.x == 0) s_abort = 0;
   // Which of this block's posts go to a reader on its own XCD (block b runs on XCD b mod 8, which
   // the host has checked on this device): bit l of a chain CU for the aux CU of its layer l (h
-  // and the history rows), bit 16 for the next chain CU, bit 17 for the head CUs; bit 0 of an aux
-  // CU for its layer's chain CU, bit 1 for the head CUs; bit 0 of a head CU for chain CU 0.
+  // and the history rows), bit 16 for the next chain CU, bit 17 for the head CUs; bit l of an aux
+  // CU for the chain CU of its layer l, bit 16 for the head CUs; bit 0 of a head CU for chain CU 0.
   __shared__ unsigned char s_xcd[WN_MAX_CHAIN + NHEAD + WN_MAX_LAYERS];
+  __shared__ int s_me;
   unsigned lm = 0;
   if (g.local_posts) {
-    for (int b = threadIdx.x; b < WN_CHAIN_GRID; b += NT) {
-      const int r = g.role_of_block[b];
-      if (r != 0xffff && (MS ? r / per : 0) == k) s_xcd[r - k * per] = (unsigned char)(b & 7);
+    // The XCD of every block is read at each launch, not assumed: each block stores its XCC_ID, the
+    // grid meets once (a cooperative launch keeps every block resident), and each block builds its
+    // masks from the map it then reads, so a post is stored at workgroup scope only when its reader
+    // runs on the writer's XCD in this launch.  (The host's placement assumes block b on XCD b mod 8;
+    // a different map only costs hop latency.)
+    if (threadIdx.x == 0) {
+      unsigned v;
+      asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
+      s_me = (int)(v & 0xf);
+      __hip_atomic_store(g.xmap + blockIdx.x, (u64)(v & 0xf), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      // grid barrier: arrival count and generation after the map
+      u64* cnt = g.xmap + WN_CHAIN_GRID;
+      u64* gen = cnt + 1;
+      const u64 g0 = __hip_atomic_load(gen, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+      if (__hip_atomic_fetch_add(cnt, 1ull, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) == (u64)(g.n_active - 1)) {
+        __hip_atomic_store(cnt, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_fetch_add(gen, 1ull, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      } else {
+        int spins = 0;
+        while (__hip_atomic_load(gen, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) == g0) {
+          if (++spins > g.spin_limit) {
+            atomicCAS(g.status, 0, (int)WN_ETIMEOUT);
+            s_me = -1;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
+        }
+      }
     }
     __syncthreads();
-    const int me = blockIdx.x & 7;
+    if (s_me < 0) return;  // the grid never met: WN_ETIMEOUT is in the status word
+    for (int b = threadIdx.x; b < WN_CHAIN_GRID; b += NT) {
+      const int r = g.role_of_block[b];
+      if (r != 0xffff && (MS ? r / per : 0) == k) s_xcd[r - k * per] = (unsigned char)ldw(g.xmap + b);
+    }
+    __syncthreads();
+    const int me = s_me;
     auto same = [&](int r) { return s_xcd[r] == me; };
     const bool heads = same(g.nch) && same(g.nch + 1) && same(g.nch + 2) && same(g.nch + 3);
     if (role < g.nch) {
       const int j0 = g.layer_begin[role], nl = g.layer_begin[role + 1] - j0;
-      for (int l = 0; l < nl; ++l) lm |= (unsigned)same(g.nch + NHEAD + j0 + l) << l;
+      for (int l = 0; l < nl; ++l) lm |= (unsigned)same(g.nch + NHEAD + (j0 + l) / g.nla) << l;
       if (role + 1 < g.nch) lm |= (unsigned)same(role + 1) << 16;
       lm |= (unsigned)heads << 17;
     } else if (role < g.nch + NHEAD) {
       lm = same(0);
     } else {
-      const int j = role - g.nch - NHEAD;
-      int c = 0;
-      while (g.layer_begin[c + 1] <= j) ++c;
-      lm = (unsigned)same(c) | (unsigned)heads << 1;
+      const int ja = (role - g.nch - NHEAD) * g.nla;
+      for (int l = 0; l < g.nla && ja + l < g.d.L; ++l) {
+        int c = 0;
+        while (g.layer_begin[c + 1] <= ja + l) ++c;
+        lm |= (unsigned)same(c) << l;
+      }
+      lm |= (unsigned)heads << 16;
     }
   }
   // where this call starts: from zero, or where the previous call on this workspace stopped (the
@@ -988,7 +1070,10 @@ size_t chain_lds_floats(int R, int S, int nlc, int G, int ub, int nch, int tail,
   return common + var;
 }
 size_t head_lds_floats(int L, int S) { return (size_t)L * S + S + HR + NT; }
-size_t aux_lds_floats(int R, int G) { return (size_t)R + (size_t)3 * R * G; }
+size_t aux_lds_floats(int R, int G) {
+  const size_t nla = R <= 64 ? aux_max_layers<64>() : aux_max_layers<128>();
+  return nla * ((size_t)R + (size_t)3 * R * G);
+}
 constexpr size_t kMaxLds = 160 * 1024;
 
 template <int R, int S>
@@ -1027,7 +1112,8 @@ bool wn_chain_supported(int R, int S, int L) {
   if (L < 1 || L > WN_MAX_LAYERS) return false;
   int lb[WN_MAX_LAYERS + 2];
   const int nch = chain_split(L, R, lb);
-  return L >= 1 && L <= WN_MAX_LAYERS && nch <= WN_MAX_CHAIN && nch + NHEAD + L <= WN_CHAIN_GRID &&
+  const int nla = R <= 64 ? aux_max_layers<64>() : aux_max_layers<128>();
+  return L >= 1 && L <= WN_MAX_LAYERS && nch <= WN_MAX_CHAIN && nch + NHEAD + (L + nla - 1) / nla <= WN_CHAIN_GRID &&
          head_lds_floats(L, S) * sizeof(float) <= kMaxLds;
 }
 
@@ -1036,8 +1122,15 @@ bool wn_chain_plan(int L, int R, int S, int B, bool two_taps, WnChainPlan* p) {
   WnChainPlan q{};
   const int nlc = nlc_for(R);
   q.nch = chain_split(L, R, q.layer_begin);
+  // layers per aux CU: as many as fit its registers (WN_AUX_LAYERS=1 keeps one layer each)
+  q.nla = R <= 64 ? aux_max_layers<64>() : aux_max_layers<128>();
+  if (const char* e = std::getenv("WN_AUX_LAYERS")) {
+    const int v = std::atoi(e);
+    if (v >= 1 && v <= q.nla) q.nla = v;
+  }
+  q.naux = (L + q.nla - 1) / q.nla;
   // as many replicas as the grid holds, the streams spread evenly over them
-  const int per = q.nch + NHEAD + L;
+  const int per = q.nch + NHEAD + q.naux;
   const int max_rep = WN_CHAIN_GRID / per;
   q.G = (B + std::min(B, max_rep) - 1) / std::min(B, max_rep);
   q.nrep = (B + q.G - 1) / q.G;
@@ -1049,16 +1142,20 @@ bool wn_chain_plan(int L, int R, int S, int B, bool two_taps, WnChainPlan* p) {
   if (chain_lds_floats(R, S, nlc, q.G, q.ub, q.nch, 1, two_taps) * sizeof(float) > kMaxLds) q.tail_on_chain = 0;
   if (chain_lds_floats(R, S, nlc, q.G, q.ub, q.nch, q.tail_on_chain, two_taps) * sizeof(float) > kMaxLds)
     return false;
+  // aux CUs that post a skip partial: all but one holding only the last layer when the last chain
+  // CU computes that layer's skip projection
+  q.naux_q = (q.tail_on_chain && (L - 1) % q.nla == 0) ? q.naux - 1 : q.naux;
   // mailboxes of one stream: pre, h, q, x, logits, tail (see WnChainArgs)
   const long long pre_w = (long long)L * 2 * 2 * R;
   q.off_h = (int)pre_w;
   q.off_q = q.off_h + L * 2 * R;
-  q.off_x = q.off_q + L * 2 * S;
+  q.off_x = q.off_q + q.naux * 2 * S;
   q.off_logit = q.off_x + q.nch * 2 * R;
   q.off_qtail = q.off_logit + NHEAD * 2 * A;
   q.mb_words = ((long long)q.off_qtail + 2 * S + 31) / 32 * 32;
   // Placement: slot i of XCD x is block 8 i + x.  Each replica's chain and head CUs go to its home
-  // XCD first, then its aux CUs, last layers first, overflowing to the XCD with the most room.
+  // XCD first, then its aux CUs, last layers first (their skip partials are the last ones the head
+  // waits for), overflowing to the XCD with the most room.
   int used[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   constexpr int per_xcd = WN_CHAIN_GRID / 8;
   for (int b = 0; b < WN_CHAIN_GRID; ++b) q.role_of_block[b] = 0xffff;
@@ -1074,7 +1171,7 @@ bool wn_chain_plan(int L, int R, int S, int B, bool two_taps, WnChainPlan* p) {
   for (int k = 0; k < q.nrep; ++k)
     for (int r = 0; r < q.nch + NHEAD; ++r) place(k * per + r, k % 8);
   for (int k = 0; k < q.nrep; ++k)
-    for (int j = L - 1; j >= 0; --j) place(k * per + q.nch + NHEAD + j, k % 8);
+    for (int a = q.naux - 1; a >= 0; --a) place(k * per + q.nch + NHEAD + a, k % 8);
   *p = q;
   return true;
 }

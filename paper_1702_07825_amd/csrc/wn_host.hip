@@ -98,9 +98,10 @@ int variant_for(const wn_handle* h, int B) {
 }
 
 // Workspace: status word, per-stream state, then either fp32 histories (per-stream and batched
-// kernels) or tagged 64-bit histories followed by the inter-CU mailboxes (multi-CU kernel).
+// kernels) or tagged 64-bit histories followed by the inter-CU mailboxes and the launch-time
+// block -> XCD map with its grid-barrier words (multi-CU kernel).
 struct WsLayout {
-  size_t status_off, state_off, hist_off, mb_off, mb_words, total;
+  size_t status_off, state_off, hist_off, mb_off, mb_words, map_off, total;
 };
 
 WsLayout ws_layout(const wn_handle* h, int B) {
@@ -112,10 +113,12 @@ WsLayout ws_layout(const wn_handle* h, int B) {
   if (chain_plan_for(h, B, &p)) {
     l.mb_off = align_up(l.hist_off + (size_t)B * h->dims.hist_len * 8, 256);
     l.mb_words = (size_t)B * p.mb_words;
-    l.total = align_up(l.mb_off + l.mb_words * 8, 256);
+    l.map_off = l.mb_off + l.mb_words * 8;
+    l.total = align_up(l.map_off + (size_t)WN_CHAIN_MAP_WORDS * 8, 256);
   } else {
     l.mb_off = 0;
     l.mb_words = 0;
+    l.map_off = 0;
     l.total = align_up(l.hist_off + (size_t)B * h->dims.hist_len * sizeof(float), 256);
   }
   return l;
@@ -181,6 +184,9 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
     g.state = reinterpret_cast<int64_t*>(base + l.state_off);
     g.ring = reinterpret_cast<unsigned long long*>(base + l.hist_off);
     g.mb = reinterpret_cast<unsigned long long*>(base + l.mb_off);
+    g.xmap = reinterpret_cast<unsigned long long*>(base + l.map_off);
+    g.n_active = 0;
+    for (int b = 0; b < WN_CHAIN_GRID; ++b) g.n_active += plan.role_of_block[b] != 0xffff;
     g.mb_words = plan.mb_words;
     g.off_h = plan.off_h;
     g.off_q = plan.off_q;
@@ -200,13 +206,16 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
     g.G = plan.G;
     g.ub = plan.ub;
     g.tail_on_chain = plan.tail_on_chain;
+    g.nla = plan.nla;
+    g.naux = plan.naux;
+    g.naux_q = plan.naux_q;
     // posts to same-XCD readers stop at the XCD's L2 when the block -> XCD map is the expected
     // one; WN_LOCAL_POSTS=0 writes every post through
     const char* lp = std::getenv("WN_LOCAL_POSTS");
     g.local_posts = h->xcd_map && !(lp && lp[0] == '0');
     std::memcpy(g.role_of_block, plan.role_of_block, sizeof(g.role_of_block));
     if (reset) {
-      const size_t words = (l.mb_off - l.hist_off) / 8 + l.mb_words;
+      const size_t words = (l.mb_off - l.hist_off) / 8 + l.mb_words + WN_CHAIN_MAP_WORDS;
       const hipError_t e = wn_chain_reset(g.ring, words, g.status, st);
       if (e != hipSuccess) return hip_fail(e, "reset kernel launch");
     }

@@ -78,6 +78,7 @@ struct WnStreamArgs {
 #define WN_MAX_CHAIN 32   // chain CUs of one replica of the multi-CU kernel
 #define WN_CHAIN_GRID 256 // blocks of the multi-CU kernel (one per CU)
 #define WN_CHAIN_MAX_G 16 // streams one replica interleaves
+#define WN_CHAIN_MAP_WORDS (WN_CHAIN_GRID + 2)  // launch-time block -> XCD map and grid-barrier words
 
 // Multi-CU kernel: tagged 64-bit words (value | step + 1 << 32).  The roles (chain, head and aux
 // CUs) form a replica; nrep replicas run side by side, replica k serving streams
@@ -91,8 +92,12 @@ struct WnChainArgs {
   unsigned long long* ring;      // [B][hist_len] tagged dilation histories
   unsigned long long* mb;        // [B][mb_words] mailboxes, placed after the histories
   long long mb_words;            // words of one stream's mailbox block
+  // after the mailboxes: the XCD each block of this launch runs on ([WN_CHAIN_GRID] words), then a
+  // grid barrier's arrival count and generation (2 words); cleared with the histories on a reset
+  unsigned long long* xmap;
+  int n_active;                  // blocks with a role (they meet at the grid barrier)
   // word offsets inside a stream's block: pre-activations [L][2][2R] (aux -> chain) at 0,
-  // hidden states [L][2][R] (chain -> aux), skip partials [L][2][S] (aux -> head),
+  // hidden states [L][2][R] (chain -> aux), skip partials [naux][2][S] (aux -> head),
   // layer-run outputs [nch][2][R] (chain -> next chain), partial logits [4][2][A]
   // (head -> chain CU 0), last layer's skip projection [2][S] (last chain CU -> head)
   int off_h, off_q, off_x, off_logit, off_qtail;
@@ -102,6 +107,7 @@ struct WnChainArgs {
   int nrep, G;                   // replicas, streams per replica
   int ub;                        // steps of uniforms / samples staged in LDS per stream
   int tail_on_chain;             // 1: the last chain CU computes the last layer's skip projection
+  int nla, naux, naux_q;         // layers per aux CU, aux CUs per replica, aux CUs posting a skip partial
   int local_posts;               // 1: posts to a reader on the same XCD stop at its L2
   uint16_t role_of_block[WN_CHAIN_GRID];  // replica * per_replica + role; 0xffff = idle block
 };
@@ -109,6 +115,7 @@ struct WnChainArgs {
 // How the multi-CU kernel lays out a model and a batch over the chip.
 struct WnChainPlan {
   int nch, nrep, G, ub, tail_on_chain;
+  int nla, naux, naux_q;
   int layer_begin[WN_MAX_CHAIN + 1];
   uint16_t role_of_block[WN_CHAIN_GRID];
   long long mb_words;

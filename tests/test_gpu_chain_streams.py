@@ -33,23 +33,28 @@ def _setup(L, r, s, dil, B, T, seed, bias=0.0):
 
 CASES = [
     # name, L, r, s, dilations, B, T, bias
-    # (replicas x streams per replica; a replica is nch chain + 4 head + L aux CUs)
+    # (replicas x streams per replica; a replica is nch chain + 4 head + ceil(L / nla) aux CUs, with
+    # nla = 2 layers per aux CU at r <= 64 and 1 at r = 128)
     ("l20_r128_b11", 20, 128, 256, tuple(synth.dilation_cycle(20)), 11, 300, 0.2),  # 6 x 2 (last 1), 35 CUs each
-    ("l20_r64_b12", 20, 64, 256, tuple(synth.dilation_cycle(20)), 12, 300, 0.0),    # 6 x 2, 27 CUs each
+    ("l20_r64_b12", 20, 64, 256, tuple(synth.dilation_cycle(20)), 12, 300, 0.0),    # 12 x 1, 17 CUs each
     ("l3_r128_b5", 3, 128, 256, (1, 3, 2), 5, 200, 0.3),                             # 5 x 1, 10 CUs each
     ("l1_r128_b2", 1, 128, 256, (1,), 2, 150, 0.4),                                  # one chain CU, skip on aux
     ("l5_r128_b3", 5, 128, 256, (2, 1, 4, 1, 3), 3, 200, 0.3),                      # chain CUs of 1, 2, 1, 1 layers
-    ("l9_r32_b40", 9, 32, 128, (1, 2, 4, 8, 16, 32, 64, 128, 256), 40, 200, 0.2),    # 14 x 3 (last 1), 14 CUs each
-    # the largest batch one launch serves at l = 20, r = 64: 9 replicas of 27 CUs, 16 streams each
-    ("l20_r64_b144", 20, 64, 256, tuple(synth.dilation_cycle(20)), 144, 40, 0.1),
-    # the most layers the library takes: 10 chain CUs of up to 7 layers
+    ("l9_r32_b40", 9, 32, 128, (1, 2, 4, 8, 16, 32, 64, 128, 256), 40, 200, 0.2),    # 20 x 2, 10 CUs each
+    # the largest batch one launch serves at l = 20, r = 64: 15 replicas of 17 CUs, 16 streams each
+    ("l20_r64_b240", 20, 64, 256, tuple(synth.dilation_cycle(20)), 240, 40, 0.1),
+    # the most layers the library takes: 10 chain CUs of up to 7 layers, 32 aux CUs
     ("l64_r64_b1", 64, 64, 256, tuple(synth.dilation_cycle(64)), 1, 120, 0.1),
+    # two d = 1 layers on one aux CU (both history reads wait for the chain CU's step), an odd layer
+    # count whose last aux CU holds only the last layer (its skip projection is on the chain)
+    ("l7_r64_d1s_b2", 7, 64, 256, (1, 1, 2, 1, 1, 4, 1), 2, 200, 0.3),               # 2 x 1, 10 CUs each
 ]
 
 
 # (workgroups, replicas) wn_launch_info reports for the layouts stated above
-LAUNCH = {"l20_r128_b11": (210, 6), "l20_r64_b12": (162, 6), "l3_r128_b5": (50, 5), "l1_r128_b2": (12, 2),
-          "l5_r128_b3": (39, 3), "l9_r32_b40": (196, 14), "l20_r64_b144": (243, 9), "l64_r64_b1": (78, 1)}
+LAUNCH = {"l20_r128_b11": (210, 6), "l20_r64_b12": (204, 12), "l3_r128_b5": (50, 5), "l1_r128_b2": (12, 2),
+          "l5_r128_b3": (39, 3), "l9_r32_b40": (200, 20), "l20_r64_b240": (255, 15), "l64_r64_b1": (46, 1),
+          "l7_r64_d1s_b2": (18, 2)}
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
@@ -152,11 +157,12 @@ def test_timeout_path_drains_and_recovers(monkeypatch):
     net.close()
 
 
-@pytest.mark.parametrize("L,r,B", [(20, 64, 1), (20, 128, 11), (40, 64, 2)])
+@pytest.mark.parametrize("L,r,B", [(20, 64, 1), (20, 128, 11), (40, 64, 2), (64, 64, 1)])
 def test_same_xcd_posts_change_nothing(L, r, B, monkeypatch):
     """Posts to a reader on the same XCD stop at its L2; written through instead (WN_LOCAL_POSTS=0)
-    every sample and logit is the same.  l = 20, r = 64 places a replica on one XCD (all posts
-    local); r = 128 and l = 40 spill aux CUs to other XCDs (local and written-through posts mix)."""
+    every sample and logit is the same.  l = 20 and l = 40 at r = 64 place a replica on one XCD
+    (17 and 30 CUs: all posts local); r = 128 and l = 64 spill aux CUs to other XCDs (local and
+    written-through posts mix)."""
     import paper_1702_07825_amd as wn
     print("same-XCD posts: L=%d r=%d B=%d" % (L, r, B), flush=True)
     dil = tuple(synth.dilation_cycle(L))
@@ -183,3 +189,29 @@ def test_same_xcd_posts_change_nothing(L, r, B, monkeypatch):
     assert torch.equal(out["0"][0], out["1"][0])
     assert torch.equal(out["0"][1], out["1"][1])
 
+
+@pytest.mark.parametrize("L,B,dil", [(20, 1, None), (40, 2, None), (9, 3, (1, 1, 2, 1, 8, 1, 3, 1, 2))])
+def test_one_and_two_layers_per_aux_cu_agree(L, B, dil, monkeypatch):
+    """Aux CUs holding two layers each (the default at r = 64) or one (WN_AUX_LAYERS=1): the same
+    model gives the same logits up to the order of the skip sums, and each layout's samples match the
+    oracle at every confident step."""
+    r, s, T = 64, 256, 300
+    dil = tuple(synth.dilation_cycle(L)) if dil is None else dil
+    print("aux layouts L=%d B=%d" % (L, B), flush=True)
+    w, net, cond, u, model = _setup(L, r, s, dil, B, T, seed=31 + L, bias=0.2)
+    ys, lgs = [], []
+    for nla in ("2", "1"):
+        monkeypatch.setenv("WN_AUX_LAYERS", nla)
+        y = net.generate(cond, u)
+        ys.append(y)
+        lgs.append(net.teacher_force(cond, ys[0]))
+    torch.cuda.synchronize()
+    d = float((lgs[0] - lgs[1]).abs().max())
+    print("  max|dlogit| between the layouts %.3g" % d, flush=True)
+    assert d <= 1e-4
+    for y in ys:
+        y_np = y.cpu().numpy()
+        yo, lo, mg = oracle.run_streams(model, cond.cpu().numpy(), u=u.cpu().numpy(), y_in=y_np, threads=8)
+        ok = mg > MARGIN
+        assert np.array_equal(yo[ok], y_np[ok])
+    net.close()

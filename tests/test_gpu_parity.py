@@ -287,9 +287,10 @@ def test_multi_cu_kernel_is_used_for_one_stream():
     wn = _wn()
     w = synth.make_weights(20, 64, 256, seed=1)
     net = wn.WaveNet(w, synth.dilation_cycle(20))
-    # up to 9 replicas of 27 CUs, at most 16 streams each; beyond that the per-stream kernel
-    assert [net.kernel_variant(b) for b in (1, 2, 144)] == ["multi_cu_chain"] * 3
-    assert net.kernel_variant(145) == "stream_l2"
+    # up to 15 replicas of 17 CUs (two layers per aux CU), at most 16 streams each; beyond that the
+    # per-stream kernel
+    assert [net.kernel_variant(b) for b in (1, 2, 240)] == ["multi_cu_chain"] * 3
+    assert net.kernel_variant(241) == "stream_l2"
     net.close()
 
 
