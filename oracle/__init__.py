@@ -48,7 +48,7 @@ def build(force: bool = True) -> str:
 class _Model(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int), ("r", ctypes.c_int), ("s", ctypes.c_int), ("a", ctypes.c_int),
                 ("dilations", ctypes.POINTER(ctypes.c_int)), ("initial_sample", ctypes.c_int),
-                ("bf16_weights", ctypes.c_int), ("embed_taps", ctypes.c_int), ("approx_nonlin", ctypes.c_int)] + [
+                ("weight_format", ctypes.c_int), ("embed_taps", ctypes.c_int), ("approx_nonlin", ctypes.c_int)] + [
         (n, ctypes.POINTER(ctypes.c_float)) for n in
         ("embed", "b_embed", "w_prev", "w_cur", "b_gate", "w_res", "b_res", "w_skip", "b_skip",
          "w_relu", "b_relu", "w_out", "b_out")]
@@ -96,6 +96,9 @@ def lib():
             L.oracle_param_count.argtypes = [ctypes.c_int] * 4
             L.oracle_flops_per_sample.restype = ctypes.c_double
             L.oracle_flops_per_sample.argtypes = [ctypes.c_int] * 4 + [ctypes.c_double] * 2
+            L.oracle_quantize_rows_i8.restype = None
+            L.oracle_quantize_rows_i8.argtypes = [ctypes.c_void_p, ctypes.c_longlong, ctypes.c_longlong,
+                                                  ctypes.c_void_p, ctypes.c_void_p]
             L.oracle_round_bf16_array.restype = None
             L.oracle_round_bf16_array.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_longlong]
             _lib = L
@@ -119,7 +122,7 @@ class Model:
     embeds y_{t-2}, tap 1 y_{t-1})."""
 
     def __init__(self, weights: Dict[str, np.ndarray], dilations: Sequence[int], initial_sample: int = 128,
-                 bf16_weights: bool = False, approx_nonlin: bool = False):
+                 bf16_weights: bool = False, approx_nonlin: bool = False, int8_weights: bool = False):
         self.w = {k: np.ascontiguousarray(v, dtype=np.float32) for k, v in weights.items()}
         L, two_r, r = self.w["w_prev"].shape
         s = self.w["w_skip"].shape[1]
@@ -128,7 +131,9 @@ class Model:
         self.n_layers, self.r, self.s, self.a = L, r, s, a
         self.dilations = np.ascontiguousarray(dilations, dtype=np.int32)
         self.initial_sample = int(initial_sample)
+        assert not (bf16_weights and int8_weights)
         self.bf16 = bool(bf16_weights)
+        self.int8 = bool(int8_weights)
         e = self.w["embed"]
         assert e.shape[-2:] == (a, r) and (e.ndim == 2 or (e.ndim == 3 and e.shape[0] == 2)), e.shape
         self.embed_taps = 1 if e.ndim == 2 else 2
@@ -136,7 +141,7 @@ class Model:
         m.n_layers, m.r, m.s, m.a = L, r, s, a
         m.dilations = self.dilations.ctypes.data_as(ctypes.POINTER(ctypes.c_int))
         m.initial_sample = self.initial_sample
-        m.bf16_weights = int(self.bf16)
+        m.weight_format = 2 if self.int8 else (1 if self.bf16 else 0)
         m.embed_taps = self.embed_taps
         self.approx_nonlin = bool(approx_nonlin)
         m.approx_nonlin = int(self.approx_nonlin)
@@ -301,3 +306,15 @@ def param_count(n_layers: int, r: int, s: int, a: int = 256) -> int:
 
 def flops_per_sample(n_layers: int, r: int, s: int, a: int = 256, f_div: float = 10.0, f_exp: float = 10.0) -> float:
     return float(lib().oracle_flops_per_sample(n_layers, r, s, a, f_div, f_exp))
+
+
+def quantize_rows_i8(w: np.ndarray):
+    """int8 weight storage of a matrix (the oracle's rule): returns (codes int8 [rows, cols],
+    scales float32 [rows]) for the rows of w reshaped to [-1, w.shape[-1]]."""
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    cols = w.shape[-1]
+    flat = w.reshape(-1, cols)
+    codes = np.zeros(flat.shape, np.float32)
+    scale = np.zeros(flat.shape[0], np.float32)
+    lib().oracle_quantize_rows_i8(_ptr(flat), flat.shape[0], cols, _ptr(codes), _ptr(scale))
+    return codes.astype(np.int8), scale

@@ -45,6 +45,13 @@
  *  - bf16 weight storage: every matrix (W_prev, W_cur, W_res, W_skip, W_relu,
  *    W_out and the embedding table) is rounded to bfloat16 with round-to-
  *    nearest-even and used as the exact value of that bfloat16; biases stay fp32.
+ *  - int8 weight storage (the paper stores int16 weights for its CPU kernels,
+ *    Section 5.1, and names lower-precision weights as further work; it gives no
+ *    scaling scheme): every matrix and the embedding table are stored per row
+ *    as int8 codes with one fp32 scale, s = max|w| / 127 rounded to fp32 and
+ *    code = round-half-even(w / s) (the quotient taken in double) in
+ *    [-127, 127]; a zero row has s = 0 and zero codes.  The weight used is the
+ *    exact product code * s; biases stay fp32.
  *
  * Layouts: every matrix is row-major [out][in]; conditioning is [T][l][2r].
  */
@@ -57,7 +64,8 @@ typedef struct {
     int n_layers, r, s, a;
     const int *dilations;     /* [n_layers], each >= 1 */
     int initial_sample;       /* y_{-1} */
-    int bf16_weights;         /* 0: use the fp32 weights; 1: round matrices to bf16 first */
+    int weight_format;        /* 0: the fp32 weights; 1: matrices rounded to bf16; 2: int8 codes
+                                 with a per-row scale (see above) */
     int embed_taps;           /* 1 or 2 */
     int approx_nonlin;        /* 0: exact tanh, sigmoid, exp; 1: the approximations of Appendix C */
     const float *embed;       /* [taps][a][r]: the last tap embeds y_{t-1}, tap 0 of two y_{t-2} */
@@ -101,10 +109,66 @@ static float round_bf16(float f) {
 
 float oracle_round_bf16(float f) { return round_bf16(f); }
 
-static double wv(const oracle_model *m, const float *p, long idx) {
+/* int8 codes (as floats) and per-row scales of every matrix of a model, made at the start of a run
+ * in weight format 2; NULL pointers in the other formats. */
+typedef struct {
+    float *embed, *w_prev, *w_cur, *w_res, *w_skip, *w_relu, *w_out;
+    float *s_embed, *s_prev, *s_cur, *s_res, *s_skip, *s_relu, *s_out;
+} oracle_i8;
+
+/* Weight idx of a matrix whose rows hold `cols` inputs, as the model uses it: the fp32 value p[idx],
+ * its bf16 rounding, or the product of its int8 code and its row's scale. */
+static double wv(const oracle_model *m, const float *p, const float *codes, const float *scale, long cols, long idx) {
+    if (m->weight_format == 2) return (double)codes[idx] * (double)scale[idx / cols];
     float f = p[idx];
-    if (m->bf16_weights) f = round_bf16(f);
+    if (m->weight_format == 1) f = round_bf16(f);
     return (double)f;
+}
+
+/*
+ * int8 codes of a row-major [rows][cols] matrix with one scale per row: s = max|w| / 127 rounded to
+ * fp32, code = round-half-even(w / s) with the quotient in double, clamped to [-127, 127]; a row
+ * of zeros gets s = 0 and codes 0.  The weight it stands for is code * s, exactly.
+ */
+void oracle_quantize_rows_i8(const float *w, long long rows, long long cols, float *codes, float *scale) {
+    for (long long i = 0; i < rows; ++i) {
+        const float *row = w + i * cols;
+        double mx = 0.0;
+        for (long long k = 0; k < cols; ++k)
+            if (fabs((double)row[k]) > mx) mx = fabs((double)row[k]);
+        const float sc = (float)(mx / 127.0);
+        scale[i] = sc;
+        for (long long k = 0; k < cols; ++k) {
+            double c = sc > 0.0f ? nearbyint((double)row[k] / (double)sc) : 0.0;
+            if (c > 127.0) c = 127.0;
+            if (c < -127.0) c = -127.0;
+            codes[i * cols + k] = (float)c;
+        }
+    }
+}
+
+static void free_i8(oracle_i8 *q) {
+    free(q->embed); free(q->w_prev); free(q->w_cur); free(q->w_res); free(q->w_skip); free(q->w_relu); free(q->w_out);
+    free(q->s_embed); free(q->s_prev); free(q->s_cur); free(q->s_res); free(q->s_skip); free(q->s_relu); free(q->s_out);
+}
+
+/* The int8 codes and scales of every matrix of m.  Returns 0, or -2 on allocation failure. */
+static int make_i8(const oracle_model *m, oracle_i8 *q) {
+    const long long L = m->n_layers, r = m->r, s = m->s, a = m->a, taps = m->embed_taps;
+    struct { const float *w; long long rows, cols; float **codes, **scale; } mats[] = {
+        {m->embed, taps * a, r, &q->embed, &q->s_embed},   {m->w_prev, L * 2 * r, r, &q->w_prev, &q->s_prev},
+        {m->w_cur, L * 2 * r, r, &q->w_cur, &q->s_cur},    {m->w_res, L * r, r, &q->w_res, &q->s_res},
+        {m->w_skip, L * s, r, &q->w_skip, &q->s_skip},     {m->w_relu, a, s, &q->w_relu, &q->s_relu},
+        {m->w_out, a, a, &q->w_out, &q->s_out},
+    };
+    memset(q, 0, sizeof(*q));
+    for (size_t i = 0; i < sizeof(mats) / sizeof(mats[0]); ++i) {
+        *mats[i].codes = malloc(sizeof(float) * (size_t)(mats[i].rows * mats[i].cols));
+        *mats[i].scale = malloc(sizeof(float) * (size_t)mats[i].rows);
+        if (!*mats[i].codes || !*mats[i].scale) { free_i8(q); return -2; }
+        oracle_quantize_rows_i8(mats[i].w, mats[i].rows, mats[i].cols, *mats[i].codes, *mats[i].scale);
+    }
+    return 0;
 }
 
 static double sigmoid(double v) { return 1.0 / (1.0 + exp(-v)); }
@@ -165,7 +229,8 @@ void oracle_reset(const oracle_model *m, oracle_state *st) {
  * ([l][2r]), writes the a = 256 logits of step t and advances the histories.
  * Returns 0 or -1 on allocation failure.
  */
-static int oracle_step(const oracle_model *m, oracle_state *st, const float *cond_t, double *logits) {
+static int oracle_step(const oracle_model *m, const oracle_i8 *q8, oracle_state *st, const float *cond_t,
+                       double *logits) {
     const int L = m->n_layers, r = m->r, s = m->s, a = m->a;
     double *x = malloc(sizeof(double) * r), *xn = malloc(sizeof(double) * r);
     double *act = malloc(sizeof(double) * 2 * r), *h = malloc(sizeof(double) * r);
@@ -177,8 +242,8 @@ static int oracle_step(const oracle_model *m, oracle_state *st, const float *con
     /* Sample embedding: x^(0) = E_cur[y_{t-1}] (+ E_prev[y_{t-2}]) + B_embed. */
     const long cur = (long)(m->embed_taps - 1) * a;  /* first row of the current tap's table */
     for (int c = 0; c < r; ++c) {
-        x[c] = wv(m, m->embed, (cur + st->last_sample) * r + c) + (double)m->b_embed[c];
-        if (m->embed_taps == 2 && st->prev_sample >= 0) x[c] += wv(m, m->embed, (long)st->prev_sample * r + c);
+        x[c] = wv(m, m->embed, q8->embed, q8->s_embed, r, (cur + st->last_sample) * r + c) + (double)m->b_embed[c];
+        if (m->embed_taps == 2 && st->prev_sample >= 0) x[c] += wv(m, m->embed, q8->embed, q8->s_embed, r, (long)st->prev_sample * r + c);
     }
     /* q^(0) = B_skip. */
     for (int k = 0; k < s; ++k) q[k] = (double)m->b_skip[k];
@@ -191,8 +256,8 @@ static int oracle_step(const oracle_model *m, oracle_state *st, const float *con
         for (int o = 0; o < 2 * r; ++o) {
             double ap = 0.0, ac = 0.0;
             for (int c = 0; c < r; ++c) {
-                ap += wv(m, m->w_prev, ((long)j * 2 * r + o) * r + c) * slot[c];
-                ac += wv(m, m->w_cur, ((long)j * 2 * r + o) * r + c) * x[c];
+                ap += wv(m, m->w_prev, q8->w_prev, q8->s_prev, r, ((long)j * 2 * r + o) * r + c) * slot[c];
+                ac += wv(m, m->w_cur, q8->w_cur, q8->s_cur, r, ((long)j * 2 * r + o) * r + c) * x[c];
             }
             act[o] = ap + ac + (double)m->b_gate[(long)j * 2 * r + o] + (double)cond_t[(long)j * 2 * r + o];
         }
@@ -203,13 +268,13 @@ static int oracle_step(const oracle_model *m, oracle_state *st, const float *con
         /* skip contribution: q += W_skip^(j) h */
         for (int k = 0; k < s; ++k) {
             double acc = 0.0;
-            for (int c = 0; c < r; ++c) acc += wv(m, m->w_skip, ((long)j * s + k) * r + c) * h[c];
+            for (int c = 0; c < r; ++c) acc += wv(m, m->w_skip, q8->w_skip, q8->s_skip, r, ((long)j * s + k) * r + c) * h[c];
             q[k] += acc;
         }
         /* residual: x^(j) = x^(j-1) + W_res h + B_res */
         for (int o = 0; o < r; ++o) {
             double acc = 0.0;
-            for (int c = 0; c < r; ++c) acc += wv(m, m->w_res, ((long)j * r + o) * r + c) * h[c];
+            for (int c = 0; c < r; ++c) acc += wv(m, m->w_res, q8->w_res, q8->s_res, r, ((long)j * r + o) * r + c) * h[c];
             xn[o] = x[o] + acc + (double)m->b_res[(long)j * r + o];
         }
         memcpy(x, xn, sizeof(double) * r);
@@ -219,13 +284,13 @@ static int oracle_step(const oracle_model *m, oracle_state *st, const float *con
     for (int k = 0; k < s; ++k) q[k] = q[k] > 0.0 ? q[k] : 0.0;
     for (int i = 0; i < a; ++i) {
         double acc = 0.0;
-        for (int k = 0; k < s; ++k) acc += wv(m, m->w_relu, (long)i * s + k) * q[k];
+        for (int k = 0; k < s; ++k) acc += wv(m, m->w_relu, q8->w_relu, q8->s_relu, s, (long)i * s + k) * q[k];
         acc += (double)m->b_relu[i];
         za[i] = acc > 0.0 ? acc : 0.0;
     }
     for (int i = 0; i < a; ++i) {
         double acc = 0.0;
-        for (int k = 0; k < a; ++k) acc += wv(m, m->w_out, (long)i * a + k) * za[k];
+        for (int k = 0; k < a; ++k) acc += wv(m, m->w_out, q8->w_out, q8->s_out, a, (long)i * a + k) * za[k];
         logits[i] = acc + (double)m->b_out[i];
     }
     free(x); free(xn); free(act); free(h); free(q); free(za);
@@ -383,7 +448,7 @@ int oracle_run_sampled(const oracle_model *m, oracle_state *st, int mode, long l
                        int *samples_out, double *logits_out, double *margin_out,
                        int sample_mode, double temperature, int top_k) {
     if (!m || T < 0 || (mode != 0 && mode != 1) || m->embed_taps < 1 || m->embed_taps > 2 ||
-        (m->approx_nonlin != 0 && m->approx_nonlin != 1))
+        (m->approx_nonlin != 0 && m->approx_nonlin != 1) || m->weight_format < 0 || m->weight_format > 2)
         return -1;
     if (mode == 0 && !u) return -1;
     if (mode == 1 && !y_in) return -1;
@@ -398,14 +463,17 @@ int oracle_run_sampled(const oracle_model *m, oracle_state *st, int mode, long l
     }
     double *lg = malloc(sizeof(double) * m->a);
     if (!lg) { free(own); return -2; }
+    oracle_i8 q8;
+    memset(&q8, 0, sizeof(q8));
+    if (m->weight_format == 2 && make_i8(m, &q8) != 0) { free(lg); free(own); return -2; }
     const long long per_step = (long long)m->n_layers * 2 * m->r;
     for (long long t = 0; t < T; ++t) {
-        if (oracle_step(m, st, cond + t * per_step, lg) != 0) { free(lg); free(own); return -2; }
+        if (oracle_step(m, &q8, st, cond + t * per_step, lg) != 0) { free(lg); free(own); free_i8(&q8); return -2; }
         if (logits_out) memcpy(logits_out + t * m->a, lg, sizeof(double) * m->a);
         int y = 0;
         double mg = 0.0;
         if (u) y = sample_nl(m->approx_nonlin, m->a, lg, u[t], sample_mode, temperature, top_k, &mg);
-        if (y < 0) { free(lg); free(own); return -1; }
+        if (y < 0) { free(lg); free(own); free_i8(&q8); return -1; }
         if (margin_out) margin_out[t] = u ? mg : 0.0;
         if (samples_out) samples_out[t] = y;
         st->prev_sample = st->last_sample;
@@ -413,6 +481,7 @@ int oracle_run_sampled(const oracle_model *m, oracle_state *st, int mode, long l
     }
     free(lg);
     free(own);
+    free_i8(&q8);
     return 0;
 }
 

@@ -2,7 +2,7 @@
  * Driver for a sanitized build of the CPU oracle (AddressSanitizer and UndefinedBehaviorSanitizer,
  * built and run by tests/test_oracle_sanitize.py).  It includes the oracle's single source file and
  * calls every exported function on small models with odd sizes (a 5-class head, non-power-of-two
- * dilations, one and two embedding taps, the bf16 and approximate-nonlinearity modes, chunked
+ * dilations, one and two embedding taps, the bf16, int8 and approximate-nonlinearity modes, chunked
  * runs that resume a state, every sampling rule, the conditioning network), so that an
  * out-of-bounds access, a leak or undefined arithmetic anywhere on those paths ends the run with
  * a sanitizer report and a nonzero exit.
@@ -22,11 +22,11 @@ static float *fill(size_t n, float scale) {
     return p;
 }
 
-static int run_model(int L, int r, int s, int a, const int *dil, int taps, int bf16, int ax) {
+static int run_model(int L, int r, int s, int a, const int *dil, int taps, int fmt, int ax) {
     oracle_model m;
     memset(&m, 0, sizeof(m));
     m.n_layers = L; m.r = r; m.s = s; m.a = a; m.dilations = dil; m.initial_sample = a / 2;
-    m.bf16_weights = bf16; m.embed_taps = taps; m.approx_nonlin = ax;
+    m.weight_format = fmt; m.embed_taps = taps; m.approx_nonlin = ax;
     float *e = fill((size_t)taps * a * r, 0.5f), *be = fill(r, 0.1f), *wp = fill((size_t)L * 2 * r * r, 0.3f);
     float *wc = fill((size_t)L * 2 * r * r, 0.3f), *bg = fill((size_t)L * 2 * r, 0.1f);
     float *wr = fill((size_t)L * r * r, 0.3f), *br = fill((size_t)L * r, 0.1f), *wk = fill((size_t)L * s * r, 0.3f);
@@ -81,12 +81,16 @@ int main(void) {
     if (!rc) rc = run_model(3, 5, 7, 5, d3, 2, 0, 0);
     if (!rc) rc = run_model(3, 6, 4, 7, d3, 1, 1, 1);
     if (!rc) rc = run_model(1, 3, 2, 2, d1, 2, 1, 0);
+    if (!rc) rc = run_model(3, 5, 7, 5, d3, 2, 2, 0);
+    if (!rc) rc = run_model(4, 16, 32, 256, d4, 1, 2, 1);
     if (!rc) rc = run_conditioning();
     double xs[64], ys[64];
     for (int i = 0; i < 64; ++i) xs[i] = (i - 32) * 0.37;
     for (int which = 0; which < 3; ++which) oracle_approx_nonlin(which, xs, ys, 64);
     float f[5] = {1.0f, -0.0f, 3.4e38f, 1e-40f, 0.333f}, g[5];
     oracle_round_bf16_array(f, g, 5);
+    float zrow[6] = {0, 0, 0, 1e-30f, -2.5f, 7.0f}, codes[6], sc[2];
+    oracle_quantize_rows_i8(zrow, 2, 3, codes, sc);
     if (oracle_param_count(40, 64, 256, 256) != 1630528) rc = -5;
     printf("oracle sanitize driver: rc=%d\n", rc);
     return rc == 0 ? 0 : 1;

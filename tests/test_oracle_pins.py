@@ -286,6 +286,77 @@ def test_bf16_weights_round_to_nearest_even():
     assert 1e-5 < np.abs(lg_b - lg_f).max() < 5e-2
 
 
+def _numpy_quantize_rows_i8(w):
+    """int8 per-row quantizer written with numpy: scale = max|w| / 127 in fp32, codes = nearest
+    integer of w / scale (ties to even) clipped to +-127, zero rows all zero."""
+    w = np.asarray(w, np.float32).reshape(-1, np.asarray(w).shape[-1])
+    scale = (np.abs(w).max(axis=1).astype(np.float64) / 127.0).astype(np.float32)
+    safe = np.where(scale > 0, scale, 1).astype(np.float64)
+    codes = np.clip(np.rint(w.astype(np.float64) / safe[:, None]), -127, 127)
+    codes[scale == 0] = 0
+    return codes.astype(np.int8), scale
+
+
+def test_int8_quantizer_matches_numpy():
+    """The oracle's int8 storage rule == a numpy quantizer, on random rows, a zero row, a row with one
+    non-zero entry and rows whose quotients are exact halves (ties go to the even code)."""
+    rng = np.random.default_rng(61)
+    w = rng.normal(0, 0.2, (40, 64)).astype(np.float32)
+    w[3] = 0.0
+    w[5] = 0.0
+    w[5, 17] = -0.37
+    step = np.float32(2.0 ** -7)  # rows with max 127 * 2^-7 have scale 2^-7 exactly
+    for i, row in enumerate((8, 9, 10)):
+        w[row] = (np.arange(64) % 9 - 4 + 0.5).astype(np.float32) * step
+        w[row, 0] = 127 * step * (-1) ** i
+    codes, scale = oracle.quantize_rows_i8(w)
+    codes_np, scale_np = _numpy_quantize_rows_i8(w)
+    np.testing.assert_array_equal(scale, scale_np)
+    np.testing.assert_array_equal(codes, codes_np)
+    assert scale[3] == 0 and not codes[3].any()
+    assert codes[5, 17] == -127 and np.count_nonzero(codes[5]) == 1
+    assert scale[8] == step
+    # ties: k + 1/2 goes to the even one of k, k + 1
+    half = (np.arange(64) % 9 - 4 + 0.5)[1:]
+    np.testing.assert_array_equal(codes[8, 1:], (2 * np.round(half / 2)).astype(np.int8))
+    assert np.abs(codes).max() <= 127
+    # every weight is within half a step of its stored value
+    err = np.abs(codes.astype(np.float64) * scale[:, None] - w)
+    assert np.all(err <= 0.5 * scale[:, None].astype(np.float64) * (1 + 1e-6))
+
+
+def test_int8_weights_model():
+    """The int8 storage mode uses code * scale exactly: with weights already on an int8 grid whose rows
+    reach +-127 steps (scale a power of two) it equals the fp32 oracle bit for bit; in general it
+    matches the fp32 oracle run on the dequantized weights (rounded to fp32) within rounding, and it
+    differs from the unquantized model."""
+    L, r, s, dil, T = 3, 16, 32, (1, 2, 4), 40
+    mats = ("embed", "w_prev", "w_cur", "w_res", "w_skip", "w_relu", "w_out")
+    w = synth.make_weights(L, r, s, seed=62, bias_scale=0.3)
+    cond = _cond(L, r, T, seed=63)
+    y = synth.make_samples(1, T, seed=64)[0]
+    rng = np.random.default_rng(65)
+    grid = dict(w)
+    for k in mats:
+        cols = w[k].shape[-1]
+        c = rng.integers(-126, 127, w[k].shape).reshape(-1, cols)
+        c[:, 0] = 127
+        e = rng.integers(-9, -4, c.shape[0])
+        grid[k] = (c * np.ldexp(1.0, e)[:, None]).reshape(w[k].shape).astype(np.float32)
+    _, lg_q, _ = oracle.run(oracle.Model(grid, dil, int8_weights=True), cond, y_in=y)
+    _, lg_g, _ = oracle.run(oracle.Model(grid, dil), cond, y_in=y)
+    np.testing.assert_array_equal(lg_q, lg_g)
+    deq = dict(w)
+    for k in mats:
+        codes, scale = _numpy_quantize_rows_i8(w[k])
+        deq[k] = (codes.astype(np.float64) * scale[:, None].astype(np.float64)).astype(np.float32).reshape(w[k].shape)
+    _, lg_8, _ = oracle.run(oracle.Model(w, dil, int8_weights=True), cond, y_in=y)
+    _, lg_d, _ = oracle.run(oracle.Model(deq, dil), cond, y_in=y)
+    assert np.abs(lg_8 - lg_d).max() < 1e-5
+    _, lg_f, _ = oracle.run(oracle.Model(w, dil), cond, y_in=y)
+    assert 1e-4 < np.abs(lg_8 - lg_f).max() < 5e-2
+
+
 def test_model_size_and_flops_match_the_paper():
     g = json.load(open(os.path.join(GOLDEN, "paper_figures.json")))
     n = oracle.param_count(40, 64, 256)
