@@ -94,7 +94,8 @@ def cpu_baseline(wl, w, cond_dev, u_np, min_seconds):
     """The CPU oracle on whole streams of the workload (stream 0, 1, ...; stream 0 again when the
     workload has one), one thread, until at least `min_seconds` of oracle time have passed."""
     import oracle
-    m = oracle.Model(w, wl.dilations, bf16_weights=(wl.weight_dtype == "bf16"))
+    m = oracle.Model(w, wl.dilations, bf16_weights=(wl.weight_dtype == "bf16"),
+                     int8_weights=(wl.weight_dtype == "i8"))
     steps, secs, runs = 0, 0.0, []
     while secs < min_seconds:
         b = len(runs) % wl.B
@@ -248,7 +249,7 @@ def run_workload(name, args, batched=False):
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32" if wl.weight_dtype == "f32" else "bf16-weights/f32",
+        "dtype": {"f32": "f32", "bf16": "bf16-weights/f32", "i8": "i8-weights/f32"}[wl.weight_dtype],
         "data": "synthetic (seeded N(0,1/fan_in) weights, N(0,1) conditioning, U[0,1) uniforms)",
         "config": {"workload": wl.description, "B": wl.B, "T": wl.T, "n_layers": wl.n_layers, "r": wl.r,
                    "s": wl.s, "a": wl.a, "kernel": variant, "workgroups": wgs,

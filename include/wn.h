@@ -24,8 +24,8 @@
  *
  * Conventions:
  *  - Every matrix is row-major [out][in], fp32 on the host.  wn_create copies
- *    (and for WN_BF16 rounds, to nearest even) them into device memory owned by
- *    the handle; the caller's host arrays may be freed afterwards.
+ *    (and for WN_BF16 / WN_I8 converts, see wn_dtype_t) them into device memory owned
+ *    by the handle; the caller's host arrays may be freed afterwards.
  *  - cond, uniforms, samples, y, logits and workspace are DEVICE pointers owned
  *    by the caller.  Calls are asynchronous and ordered on `stream` (a
  *    hipStream_t, NULL = the default stream); the caller keeps every buffer alive
@@ -68,7 +68,18 @@ typedef enum {
   WN_EABORTED = -6       /* a call stopped early on a wn_abort request (reported by wn_status) */
 } wn_status_t;
 
-typedef enum { WN_F32 = 0, WN_BF16 = 1 } wn_dtype_t;
+/*
+ * Storage of the matrices and the embedding table (biases, activations and accumulation are always
+ * fp32):
+ *   WN_F32   as given
+ *   WN_BF16  rounded to bfloat16, nearest even
+ *   WN_I8    int8 codes with one fp32 scale per row (the paper runs int16 weights in its CPU
+ *            kernels, Section 5.1, and names lower precision as further work): per row
+ *            s = max|w| / 127 rounded to fp32, code = w / s (the quotient in double) rounded to
+ *            nearest, ties to even, clamped to [-127, 127]; a zero row has s = 0.  The weight used
+ *            is code * s.
+ */
+typedef enum { WN_F32 = 0, WN_BF16 = 1, WN_I8 = 2 } wn_dtype_t;
 
 /*
  * How a step's output distribution P = softmax(logits) becomes its sample: the ways the paper

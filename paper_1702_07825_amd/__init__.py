@@ -19,7 +19,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libwn.so")
 
 WN_OK, WN_EINVAL, WN_EUNSUPPORTED, WN_ENOMEM, WN_EHIP, WN_ETIMEOUT, WN_EABORTED = 0, -1, -2, -3, -4, -5, -6
-WN_F32, WN_BF16 = 0, 1
+WN_F32, WN_BF16, WN_I8 = 0, 1, 2
 WN_NONLIN_EXACT, WN_NONLIN_PAPER = 0, 1
 A_CLASSES = 256
 EXPORTED = ("wn_create", "wn_workspace_bytes", "wn_generate", "wn_generate_sampled", "wn_teacher_force", "wn_status",
@@ -169,7 +169,7 @@ class WaveNet:
         self.weight_dtype = weight_dtype
         cfg = Config(self.n_layers, self.r, self.s, self.a,
                      self.dilations.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), int(embed_taps),
-                     self.initial_sample, {"f32": WN_F32, "bf16": WN_BF16}[weight_dtype],
+                     self.initial_sample, {"f32": WN_F32, "bf16": WN_BF16, "i8": WN_I8}[weight_dtype],
                      WN_NONLIN_PAPER if approx_nonlin else WN_NONLIN_EXACT)
         self.approx_nonlin = bool(approx_nonlin)
         ws = Weights(*[w[k].ctypes.data_as(ctypes.POINTER(ctypes.c_float)) for k in WEIGHT_FIELDS])

@@ -3,6 +3,7 @@
 #include "wn.h"
 #include "wn_internal.h"
 
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -65,6 +66,23 @@ int hip_fail(hipError_t e, const char* what) {
 }
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// int8 storage of a row-major [rows][cols] matrix: per row s = max|w| / 127 rounded to fp32, codes
+// w / s (in double) rounded to nearest, ties to even, clamped to [-127, 127]; a zero row has s = 0
+// and zero codes.
+void quantize_rows_i8(const float* w, size_t rows, size_t cols, int8_t* codes, float* scale) {
+  for (size_t i = 0; i < rows; ++i) {
+    const float* row = w + i * cols;
+    double mx = 0.0;
+    for (size_t k = 0; k < cols; ++k) mx = std::max(mx, std::fabs((double)row[k]));
+    const float s = (float)(mx / 127.0);
+    scale[i] = s;
+    for (size_t k = 0; k < cols; ++k) {
+      const double q = s > 0.0f ? std::nearbyint((double)row[k] / (double)s) : 0.0;
+      codes[i * cols + k] = (int8_t)std::min(127.0, std::max(-127.0, q));
+    }
+  }
+}
 
 class DeviceScope {
  public:
@@ -287,7 +305,8 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
   if (c->n_layers < 1 || c->n_layers > WN_MAX_LAYERS) return fail(WN_EINVAL, "n_layers must be 1..64");
   if (!c->dilations) return fail(WN_EINVAL, "null dilations");
   if (c->r < 1 || c->s < 1 || c->a < 1) return fail(WN_EINVAL, "r, s, a must be >= 1");
-  if (c->weight_dtype != WN_F32 && c->weight_dtype != WN_BF16) return fail(WN_EINVAL, "unknown weight_dtype");
+  if (c->weight_dtype != WN_F32 && c->weight_dtype != WN_BF16 && c->weight_dtype != WN_I8)
+    return fail(WN_EINVAL, "unknown weight_dtype");
   if (c->initial_sample < 0 || c->initial_sample >= c->a) return fail(WN_EINVAL, "initial_sample out of range");
   if (c->embed_taps < 1 || c->embed_taps > 2) return fail(WN_EINVAL, "embed_taps must be 1 or 2");
   if (c->nonlinearity != WN_NONLIN_EXACT && c->nonlinearity != WN_NONLIN_PAPER)
@@ -331,29 +350,43 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
     }
   }
 
-  // Pack every array into one device allocation, each 256-byte aligned.
-  const bool bf = (h->dtype == WN_BF16);
-  const size_t we = bf ? 2 : 4;
-  struct Arr { const float* src; size_t n; bool matrix; size_t off; };
+  // Pack every array into one device allocation, each 256-byte aligned.  int8 storage adds one fp32
+  // scale per matrix row (`cols` inputs per row).
+  const bool bf = (h->dtype == WN_BF16), i8 = (h->dtype == WN_I8);
+  const size_t we = bf ? 2 : (i8 ? 1 : 4);
+  struct Arr { const float* src; size_t n; bool matrix; size_t cols; size_t off, soff; };
   Arr arrs[] = {
-      {w->embed, (size_t)c->embed_taps * A * R, true, 0}, {w->w_prev, (size_t)L * 2 * R * R, true, 0},
-      {w->w_cur, (size_t)L * 2 * R * R, true, 0},  {w->w_res, (size_t)L * R * R, true, 0},
-      {w->w_skip, (size_t)L * S * R, true, 0},     {w->w_relu, (size_t)A * S, true, 0},
-      {w->w_out, (size_t)A * A, true, 0},          {w->b_embed, (size_t)R, false, 0},
-      {w->b_gate, (size_t)L * 2 * R, false, 0},    {w->b_res, (size_t)L * R, false, 0},
-      {w->b_skip, (size_t)S, false, 0},            {w->b_relu, (size_t)A, false, 0},
-      {w->b_out, (size_t)A, false, 0},
+      {w->embed, (size_t)c->embed_taps * A * R, true, (size_t)R, 0, 0},
+      {w->w_prev, (size_t)L * 2 * R * R, true, (size_t)R, 0, 0},
+      {w->w_cur, (size_t)L * 2 * R * R, true, (size_t)R, 0, 0},
+      {w->w_res, (size_t)L * R * R, true, (size_t)R, 0, 0},
+      {w->w_skip, (size_t)L * S * R, true, (size_t)R, 0, 0},
+      {w->w_relu, (size_t)A * S, true, (size_t)S, 0, 0},
+      {w->w_out, (size_t)A * A, true, (size_t)A, 0, 0},
+      {w->b_embed, (size_t)R, false, 0, 0, 0},
+      {w->b_gate, (size_t)L * 2 * R, false, 0, 0, 0},
+      {w->b_res, (size_t)L * R, false, 0, 0, 0},
+      {w->b_skip, (size_t)S, false, 0, 0, 0},
+      {w->b_relu, (size_t)A, false, 0, 0, 0},
+      {w->b_out, (size_t)A, false, 0, 0, 0},
   };
   size_t total = 0;
   for (Arr& a : arrs) {
     a.off = total;
     total = align_up(total + a.n * (a.matrix ? we : 4), 256);
+    if (a.matrix && i8) {
+      a.soff = total;
+      total = align_up(total + a.n / a.cols * 4, 256);
+    }
   }
   std::vector<unsigned char> host(total, 0);
   for (const Arr& a : arrs) {
     if (a.matrix && bf) {
       uint16_t* d = reinterpret_cast<uint16_t*>(host.data() + a.off);
       for (size_t i = 0; i < a.n; ++i) d[i] = wn_to_bf16(a.src[i]);
+    } else if (a.matrix && i8) {
+      quantize_rows_i8(a.src, a.n / a.cols, a.cols, reinterpret_cast<int8_t*>(host.data() + a.off),
+                       reinterpret_cast<float*>(host.data() + a.soff));
     } else {
       std::memcpy(host.data() + a.off, a.src, a.n * 4);
     }
@@ -399,6 +432,18 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
   h->w.b_relu = reinterpret_cast<const float*>(d + arrs[11].off);
   h->w.b_out = reinterpret_cast<const float*>(d + arrs[12].off);
   h->w.bf16 = bf ? 1 : 0;
+  h->w.i8 = i8 ? 1 : 0;
+  if (i8) {
+    auto sc = [&](int k) { return reinterpret_cast<const float*>(d + arrs[k].soff); };
+    h->w.s_embed = sc(0) + (size_t)(c->embed_taps - 1) * A;
+    h->w.s_embed_prev = c->embed_taps == 2 ? sc(0) : nullptr;
+    h->w.s_prev = sc(1);
+    h->w.s_cur = sc(2);
+    h->w.s_res = sc(3);
+    h->w.s_skip = sc(4);
+    h->w.s_relu = sc(5);
+    h->w.s_out = sc(6);
+  }
   h->w.approx_nl = c->nonlinearity == WN_NONLIN_PAPER ? 1 : 0;
 
   // The multi-CU kernel needs fp32 weights, a supported shape and one CU per block of its grid.
@@ -407,7 +452,7 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
   int cus = 0, coop = 0;
   (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device);
   (void)hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, h->device);
-  if (want_chain && !bf && wn_chain_supported(R, S, L) && cus >= WN_CHAIN_GRID && coop) h->chain_ok = true;
+  if (want_chain && !bf && !i8 && wn_chain_supported(R, S, L) && cus >= WN_CHAIN_GRID && coop) h->chain_ok = true;
   if (h->chain_ok) h->xcd_map = wn_chain_xcd_map_ok();
   // The batched MFMA kernel needs bf16 weights, r = 64 and its LDS footprint on one CU.
   int lds_max = 0;

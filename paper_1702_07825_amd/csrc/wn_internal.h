@@ -21,7 +21,7 @@ struct WnDims {
 };
 
 // Device copies of the weights.  Matrices are row-major [out][in] and either
-// fp32 or bf16 (uint16 bit patterns); biases are fp32.
+// fp32, bf16 (uint16 bit patterns) or int8 codes with one fp32 scale per row; biases are fp32.
 struct WnDevWeights {
   const void* embed;       // [A][R] embedding of y_{t-1}
   const void* embed_prev;  // [A][R] embedding of y_{t-2} (two-tap input convolution), or null
@@ -38,6 +38,15 @@ struct WnDevWeights {
   const float* b_relu;
   const float* b_out;
   int bf16;
+  int i8;  // 1: int8 codes; the weight of row i is code * s_<matrix>[i]
+  const float* s_embed;       // [A] scales of the y_{t-1} table
+  const float* s_embed_prev;  // [A] scales of the y_{t-2} table (two taps)
+  const float* s_prev;        // [L][2R]
+  const float* s_cur;         // [L][2R]
+  const float* s_res;         // [L][R]
+  const float* s_skip;        // [L][S]
+  const float* s_relu;        // [A]
+  const float* s_out;         // [A]
   int approx_nl;  // 1: the approximate tanh, sigmoid and softmax exp of the paper's Appendix C
 };
 

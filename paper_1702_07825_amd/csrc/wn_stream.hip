@@ -10,8 +10,9 @@
 //
 // Data placement:
 //  - weights stay in HBM and are re-read every step through the L2 (each row is
-//    read by LPR adjacent lanes with 16-byte loads, so a wave instruction covers
-//    contiguous row segments);
+//    read by LPR adjacent lanes, 4 weights per load, so a wave instruction covers
+//    contiguous row segments); fp32, bf16 or int8 codes with a per-row scale that
+//    multiplies the row's dot product;
 //  - activations (x, h, q, z_a, logits) and the step's conditioning and history
 //    reads live in LDS;
 //  - each layer's dilation history is a ring of d_j slots of r floats in the
@@ -41,6 +42,17 @@ __device__ __forceinline__ float4 ld4(const uint16_t* p) {
   const uint2 v = *reinterpret_cast<const uint2*>(p);
   return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
                      __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u));
+}
+// four int8 codes (the row's scale is applied to the row's dot product)
+__device__ __forceinline__ float4 ld4(const int8_t* p) {
+  const int v = *reinterpret_cast<const int*>(p);
+  return make_float4((float)((v << 24) >> 24), (float)((v << 16) >> 24), (float)((v << 8) >> 24), (float)(v >> 24));
+}
+// Scale of row `row` of a matrix stored as WT: the int8 codes' per-row scale, else 1.
+template <typename WT>
+__device__ __forceinline__ float row_scale(const float* s, size_t row) {
+  if constexpr (sizeof(WT) == 1) return s[row];
+  else return 1.0f;
 }
 __device__ __forceinline__ float dot4(float4 w, float4 x, float acc) {
   acc = fmaf(w.x, x.x, acc);
@@ -149,8 +161,8 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
           if constexpr (sizeof(WT) == 2) return __uint_as_float((uint32_t)e[tid] << 16);
           else return (float)e[tid];
         };
-        float ev = ld(embed + (size_t)yp * R) + args.w.b_embed[tid];
-        if (embed_prev && yp2 >= 0) ev += ld(embed_prev + (size_t)yp2 * R);
+        float ev = ld(embed + (size_t)yp * R) * row_scale<WT>(args.w.s_embed, yp) + args.w.b_embed[tid];
+        if (embed_prev && yp2 >= 0) ev += ld(embed_prev + (size_t)yp2 * R) * row_scale<WT>(args.w.s_embed_prev, yp2);
         xs[tid] = ev;
       }
       for (int m = tid; m < S; m += NT) qs[m] = args.w.b_skip[m];
@@ -173,8 +185,11 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
         for (int p = 0; p < P; ++p) {
           const int c = p * RD::G + grp;
           if (c < R) {
-            float s0 = RD::partial(wp + (size_t)c * R, xp4, li) + RD::partial(wc + (size_t)c * R, xc4, li);
-            float s1 = RD::partial(wp + (size_t)(c + R) * R, xp4, li) + RD::partial(wc + (size_t)(c + R) * R, xc4, li);
+            const size_t r0 = (size_t)j * 2 * R + c, r1 = r0 + R;  // rows c (tanh) and c + R (sigmoid)
+            float s0 = RD::partial(wp + (size_t)c * R, xp4, li) * row_scale<WT>(args.w.s_prev, r0) +
+                       RD::partial(wc + (size_t)c * R, xc4, li) * row_scale<WT>(args.w.s_cur, r0);
+            float s1 = RD::partial(wp + (size_t)(c + R) * R, xp4, li) * row_scale<WT>(args.w.s_prev, r1) +
+                       RD::partial(wc + (size_t)(c + R) * R, xc4, li) * row_scale<WT>(args.w.s_cur, r1);
             s0 = RD::reduce(s0);
             s1 = RD::reduce(s1);
             if (li == 0) {
@@ -204,12 +219,14 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
           const int row = p * RD::G + grp;
           if (row < R) {
             if (!last) {
-              const float v = RD::reduce(RD::partial(wr + (size_t)row * R, h4, li));
+              const float v = RD::reduce(RD::partial(wr + (size_t)row * R, h4, li)) *
+                              row_scale<WT>(args.w.s_res, (size_t)j * R + row);
               if (li == 0) xs[row] += v + args.w.b_res[j * R + row];
             }
           } else if (row < R + S) {
             const int m = row - R;
-            const float v = RD::reduce(RD::partial(wk + (size_t)m * R, h4, li));
+            const float v = RD::reduce(RD::partial(wk + (size_t)m * R, h4, li)) *
+                            row_scale<WT>(args.w.s_skip, (size_t)j * S + m);
             if (li == 0) qs[m] += v;
           }
         }
@@ -232,7 +249,7 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
 #pragma unroll
       for (int p = 0; p < P; ++p) {
         const int i = p * RD::G + grp;
-        const float v = RD::reduce(RD::partial(w_relu + (size_t)i * S, z4, li));
+        const float v = RD::reduce(RD::partial(w_relu + (size_t)i * S, z4, li)) * row_scale<WT>(args.w.s_relu, i);
         if (li == 0) zas[i] = fmaxf(v + args.w.b_relu[i], 0.f);
       }
     }
@@ -247,7 +264,7 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
 #pragma unroll
       for (int p = 0; p < P; ++p) {
         const int i = p * RD::G + grp;
-        const float v = RD::reduce(RD::partial(w_out + (size_t)i * A, z4, li));
+        const float v = RD::reduce(RD::partial(w_out + (size_t)i * A, z4, li)) * row_scale<WT>(args.w.s_out, i);
         if (li == 0) {
           const float lg = v + args.w.b_out[i];
           if constexpr (TF) args.io.logits[bt * A + i] = lg;
@@ -301,6 +318,8 @@ hipError_t launch_rs(const WnStreamArgs& args, bool teacher, hipStream_t stream)
   } while (0)
   if (args.w.bf16) {
     if (teacher) WN_LAUNCH(uint16_t, true); else WN_LAUNCH(uint16_t, false);
+  } else if (args.w.i8) {
+    if (teacher) WN_LAUNCH(int8_t, true); else WN_LAUNCH(int8_t, false);
   } else {
     if (teacher) WN_LAUNCH(float, true); else WN_LAUNCH(float, false);
   }

@@ -51,7 +51,7 @@ class Workload:
     dilations: tuple
     B: int
     T: int
-    weight_dtype: str  # "f32" or "bf16" (storage); arithmetic is fp32 on the GPU
+    weight_dtype: str  # "f32", "bf16" or "i8" (storage); arithmetic is fp32 on the GPU
     description: str
     embed_taps: int = 1          # 2: the width-2 input convolution of Section 5.1
     sample_rate: int = 16000     # Hz of the audio the workload stands for
@@ -74,6 +74,13 @@ WORKLOADS: Dict[str, Workload] = {
                                   "bf16",
                                   "l=20 (d=2^(i mod 10)), r=64, s=256, a=256, B=256, T=32000, "
                                   "bf16 weights, fp32 accumulate and activations"),
+    "l20_r64_b1_i8": Workload("l20_r64_b1_i8", 20, 64, 256, A_CLASSES, tuple(dilation_cycle(20)), 1, 16000, "i8",
+                              "l=20 (d=2^(i mod 10)), r=64, s=256, a=256, B=1, T=16000, "
+                              "int8 weights (per-row scale), fp32 accumulate and activations"),
+    "l20_r64_b256_i8": Workload("l20_r64_b256_i8", 20, 64, 256, A_CLASSES, tuple(dilation_cycle(20)), 256, 32000,
+                                "i8",
+                                "l=20 (d=2^(i mod 10)), r=64, s=256, a=256, B=256, T=32000, "
+                                "int8 weights (per-row scale), fp32 accumulate and activations"),
     "l20_r64_b1_2tap_48k": Workload("l20_r64_b1_2tap_48k", 20, 64, 256, A_CLASSES, tuple(dilation_cycle(20)), 1,
                                     48000, "f32",
                                     "l=20 (d=2^(i mod 10)), r=64, s=256, a=256, two-tap input embedding, B=1, "

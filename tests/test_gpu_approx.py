@@ -20,6 +20,7 @@ pytestmark = pytest.mark.gpu
 
 LOGIT_TOL = 1e-3
 MARGIN = 1e-4
+I8_KERNEL = "stream_l2"  # the kernel int8 models with r = 64 run on
 
 CASES = [
     # name, kernel forced, expected variant, L, r, s, dil, B, T, dtype, bias, taps
@@ -28,6 +29,7 @@ CASES = [
     ("chain_l20_r128_b3_2tap", "", "multi_cu_chain", 20, 128, 256, tuple(synth.dilation_cycle(20)), 3, 100, "f32",
      0.1, 2),
     ("group_l20_b5", "", "mfma_group", 20, 64, 256, tuple(synth.dilation_cycle(20)), 5, 140, "bf16", 0.2, 1),
+    ("i8_l20_r64_b2", "", I8_KERNEL, 20, 64, 256, tuple(synth.dilation_cycle(20)), 2, 150, "i8", 0.2, 1),
 ]
 
 
@@ -56,7 +58,7 @@ def test_approximate_nonlinearities_parity(case, monkeypatch):
     lg_exact = exact.teacher_force(cond, y)
     torch.cuda.synchronize()
     y_np, lg_np = y.cpu().numpy(), lg.cpu().numpy()
-    model = oracle.Model(w, dil, bf16_weights=(dtype == "bf16"), approx_nonlin=True)
+    model = oracle.Model(w, dil, bf16_weights=(dtype == "bf16"), int8_weights=(dtype == "i8"), approx_nonlin=True)
     ys, lo, mg = oracle.run_streams(model, cond.cpu().numpy(), u=u.cpu().numpy(), y_in=y_np, threads=8)
     err = float(np.abs(lg_np - lo).max())
     ok = mg > MARGIN

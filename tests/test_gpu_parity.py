@@ -17,7 +17,7 @@ import synth
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
-LOGIT_TOL = {"f32": 1e-3, "bf16": 1e-3}
+LOGIT_TOL = {"f32": 1e-3, "bf16": 1e-3, "i8": 1e-3}
 BF16_VS_F32_TOL = 2e-2
 MARGIN = 1e-4
 
@@ -33,7 +33,7 @@ def _setup(L, r, s, dil, B, T, seed, dtype="f32", bias=0.0, init=128):
     net = wn.WaveNet(w, dil, initial_sample=init, weight_dtype=dtype)
     cond = synth.make_cond(L, r, B, T, seed=seed, device="cuda")
     u = torch.tensor(synth.make_uniforms(B, T, seed=seed), device="cuda")
-    model = oracle.Model(w, dil, initial_sample=init, bf16_weights=(dtype == "bf16"))
+    model = oracle.Model(w, dil, initial_sample=init, bf16_weights=(dtype == "bf16"), int8_weights=(dtype == "i8"))
     return w, net, cond, u, model
 
 
@@ -168,17 +168,18 @@ def _window(w, dil, dtype, cond_b, u_b, y_b, t):
     taps = 1 if np.asarray(w["embed"]).ndim == 2 else 2
     t0 = max(0, t - (taps - 1) - int(sum(dil)))
     init = 128 if t0 == 0 else int(y_b[t0 - 1])
-    m = oracle.Model(w, dil, initial_sample=init, bf16_weights=(dtype == "bf16"))
+    m = oracle.Model(w, dil, initial_sample=init, bf16_weights=(dtype == "bf16"), int8_weights=(dtype == "i8"))
     ys, lo, mg = oracle.run(m, cond_b[t0:t + 1], u=u_b[t0:t + 1], y_in=y_b[t0:t + 1])
     return lo[-1], int(ys[-1]), float(mg[-1])
 
 
-FULL = ["l20_r64_b1", "l40_r64_b1", "tiny", "l20_r128_b32", "l20_r64_b256_bf16", "l20_r64_b1_2tap_48k"]
+FULL = ["l20_r64_b1", "l40_r64_b1", "tiny", "l20_r128_b32", "l20_r64_b256_bf16", "l20_r64_b1_2tap_48k",
+        "l20_r64_b1_i8", "l20_r64_b256_i8"]
 
 
 def _whole_stream(w, dil, dtype, cb, ub, yb):
     """The oracle teacher-forced over a whole stream: logits, draws and margins of every step."""
-    m = oracle.Model(w, dil, bf16_weights=(dtype == "bf16"))
+    m = oracle.Model(w, dil, bf16_weights=(dtype == "bf16"), int8_weights=(dtype == "i8"))
     return oracle.run(m, cb, u=ub, y_in=yb)
 
 

@@ -38,7 +38,7 @@ def _setup(name, L, r, s, dil, B, T, dtype):
     net = wn.WaveNet(w, dil, weight_dtype=dtype)
     cond = synth.make_cond(L, r, B, T, seed=seed, device="cuda")
     u = torch.tensor(synth.make_uniforms(B, T, seed=seed), device="cuda")
-    return w, net, cond, u, oracle.Model(w, dil, bf16_weights=(dtype == "bf16"))
+    return w, net, cond, u, oracle.Model(w, dil, bf16_weights=(dtype == "bf16"), int8_weights=(dtype == "i8"))
 
 
 @pytest.mark.parametrize("model", MODELS, ids=[m[0] for m in MODELS])

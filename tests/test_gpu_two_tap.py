@@ -20,6 +20,7 @@ pytestmark = pytest.mark.gpu
 
 LOGIT_TOL = 1e-3
 MARGIN = 1e-4
+I8_KERNEL = "stream_l2"  # the kernel int8 models with r = 64 run on
 
 CASES = [
     # name, kernel forced ("" = the library's choice), expected variant, L, r, s, dil, B, T, dtype, bias
@@ -30,6 +31,8 @@ CASES = [
     ("chain_r32_b2", "", "multi_cu_chain", 6, 32, 128, (1, 2, 4, 8, 16, 32), 2, 200, "f32", 0.2),
     ("group_l20_b5", "", "mfma_group", 20, 64, 256, tuple(synth.dilation_cycle(20)), 5, 140, "bf16", 0.1),
     ("group_l40_b17", "", "mfma_group", 40, 64, 256, tuple(synth.dilation_cycle(40)), 17, 60, "bf16", 0.0),
+    ("i8_l20_r64", "", I8_KERNEL, 20, 64, 256, tuple(synth.dilation_cycle(20)), 1, 200, "i8", 0.1),
+    ("i8_stream_r16", "stream", "stream_l2", 3, 16, 32, (1, 2, 4), 2, 200, "i8", 0.3),
 ]
 
 
@@ -60,7 +63,7 @@ def test_two_tap_parity(case, monkeypatch):
     lg = net.teacher_force(cond, y)
     torch.cuda.synchronize()
     y_np, lg_np = y.cpu().numpy(), lg.cpu().numpy()
-    model = oracle.Model(w, dil, bf16_weights=(dtype == "bf16"))
+    model = oracle.Model(w, dil, bf16_weights=(dtype == "bf16"), int8_weights=(dtype == "i8"))
     assert model.receptive_field == 2 + sum(dil)
     ys, lo, mg = oracle.run_streams(model, cond.cpu().numpy(), u=u.cpu().numpy(), y_in=y_np, threads=8)
     err = float(np.abs(lg_np - lo).max())
