@@ -26,6 +26,10 @@ struct wn_handle {
   bool xcd_map = false;   // blocks of the multi-CU kernel's grid run on XCD (block mod 8)
   bool group_ok = false;  // the batched MFMA kernel serves every B
   void* dpack = nullptr;  // its packed bf16 weight tiles
+  // int8 models on the multi-CU kernel: the matrices as fp32 values code * scale (that kernel holds
+  // its weights in registers and LDS for a whole call, so it takes them in fp32 and reads them once)
+  void* dmem_f32 = nullptr;
+  WnDevWeights w_chain{};
   // wn_abort's request word: coherent pinned host memory the kernels read at system scope
   int* abort_host = nullptr;
   int* abort_dev = nullptr;
@@ -186,7 +190,7 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
   if (chain_plan_for(h, B, &plan)) {
     WnChainArgs g{};
     g.d = h->dims;
-    g.w = h->w;
+    g.w = h->dmem_f32 ? h->w_chain : h->w;
     g.io.cond = cond;
     g.io.u = u;
     g.io.y_in = y_in;
@@ -446,14 +450,50 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
   }
   h->w.approx_nl = c->nonlinearity == WN_NONLIN_PAPER ? 1 : 0;
 
-  // The multi-CU kernel needs fp32 weights, a supported shape and one CU per block of its grid.
+  // The multi-CU kernel needs fp32 or int8 weights, a supported shape and one CU per block of its grid.
   const char* force = std::getenv("WN_KERNEL");
   const bool want_chain = !(force && std::strcmp(force, "stream") == 0);
   int cus = 0, coop = 0;
   (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device);
   (void)hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, h->device);
-  if (want_chain && !bf && !i8 && wn_chain_supported(R, S, L) && cus >= WN_CHAIN_GRID && coop) h->chain_ok = true;
+  if (want_chain && !bf && wn_chain_supported(R, S, L) && cus >= WN_CHAIN_GRID && coop) h->chain_ok = true;
   if (h->chain_ok) h->xcd_map = wn_chain_xcd_map_ok();
+  if (h->chain_ok && i8) {
+    // fp32 copies of the int8 matrices for the multi-CU kernel: each weight code * scale, rounded to
+    // fp32 once here (the per-stream kernel multiplies its row sums by the scale instead)
+    size_t ftotal = 0;
+    std::vector<size_t> foff(7);
+    for (int k = 0; k < 7; ++k) {
+      foff[k] = ftotal;
+      ftotal = align_up(ftotal + arrs[k].n * 4, 256);
+    }
+    std::vector<float> fh(ftotal / 4, 0.f);
+    for (int k = 0; k < 7; ++k) {
+      const int8_t* codes = reinterpret_cast<const int8_t*>(host.data() + arrs[k].off);
+      const float* scale = reinterpret_cast<const float*>(host.data() + arrs[k].soff);
+      for (size_t i = 0; i < arrs[k].n; ++i) fh[foff[k] / 4 + i] = (float)codes[i] * scale[i / arrs[k].cols];
+    }
+    e = hipMalloc(&h->dmem_f32, ftotal);
+    if (e == hipSuccess) e = hipMemcpy(h->dmem_f32, fh.data(), ftotal, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      if (h->dmem_f32) (void)hipFree(h->dmem_f32);
+      (void)hipFree(h->dmem);
+      (void)hipHostFree(h->abort_host);
+      delete h;
+      return e == hipErrorOutOfMemory ? fail(WN_ENOMEM, "hipMalloc of fp32 weights") : hip_fail(e, "fp32 weights upload");
+    }
+    char* f = static_cast<char*>(h->dmem_f32);
+    h->w_chain = h->w;
+    h->w_chain.embed = f + foff[0] + (size_t)(c->embed_taps - 1) * A * R * 4;
+    h->w_chain.embed_prev = c->embed_taps == 2 ? f + foff[0] : nullptr;
+    h->w_chain.w_prev = f + foff[1];
+    h->w_chain.w_cur = f + foff[2];
+    h->w_chain.w_res = f + foff[3];
+    h->w_chain.w_skip = f + foff[4];
+    h->w_chain.w_relu = f + foff[5];
+    h->w_chain.w_out = f + foff[6];
+    h->w_chain.i8 = 0;
+  }
   // The batched MFMA kernel needs bf16 weights, r = 64 and its LDS footprint on one CU.
   int lds_max = 0;
   (void)hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device);
@@ -563,6 +603,7 @@ void wn_destroy(wn_handle* h) {
     DeviceScope scope(h->device);
     if (h->dmem) (void)hipFree(h->dmem);
     if (h->dpack) (void)hipFree(h->dpack);
+    if (h->dmem_f32) (void)hipFree(h->dmem_f32);
     if (h->abort_host) (void)hipHostFree(h->abort_host);
   }
   delete h;

@@ -10,9 +10,9 @@
 //
 // Data placement:
 //  - weights stay in HBM and are re-read every step through the L2 (each row is
-//    read by LPR adjacent lanes, 4 weights per load, so a wave instruction covers
-//    contiguous row segments); fp32, bf16 or int8 codes with a per-row scale that
-//    multiplies the row's dot product;
+//    read by LPR adjacent lanes, 4 weights per load (16 int8 codes), so a wave
+//    instruction covers contiguous row segments); fp32, bf16 or int8 codes with a
+//    per-row scale that multiplies the row's dot product;
 //  - activations (x, h, q, z_a, logits) and the step's conditioning and history
 //    reads live in LDS;
 //  - each layer's dilation history is a ring of d_j slots of r floats in the
@@ -61,23 +61,47 @@ __device__ __forceinline__ float dot4(float4 w, float4 x, float acc) {
   return fmaf(w.w, x.w, acc);
 }
 
-// Dot products of K-long rows: LPR adjacent lanes share a row, each handling NV
-// float4 chunks (chunk index lane + i*LPR), then reduce across the LPR lanes.
-template <int K>
+// Unpacks 16 int8 codes (one 16-byte load) and adds their dot product with 16 inputs to acc.
+__device__ __forceinline__ float dot16_i8(const int8_t* p, const float4* x, float acc) {
+  const int4 v = *reinterpret_cast<const int4*>(p);
+  const int w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    acc = fmaf((float)((w[q] << 24) >> 24), x[q].x, acc);
+    acc = fmaf((float)((w[q] << 16) >> 24), x[q].y, acc);
+    acc = fmaf((float)((w[q] << 8) >> 24), x[q].z, acc);
+    acc = fmaf((float)(w[q] >> 24), x[q].w, acc);
+  }
+  return acc;
+}
+
+// Inputs one lane takes from a row per load: 4 fp32 or bf16 weights, or 16 int8 codes.
+template <typename WT>
+constexpr int kChunk = sizeof(WT) == 1 ? 16 : 4;
+
+// Dot products of K-long rows stored as WT: LPR adjacent lanes share a row, each handling NV
+// chunks of CH inputs (chunk index lane + i*LPR), then reduce across the LPR lanes.
+template <int K, typename WT>
 struct RowDot {
-  static constexpr int LPR = (K / 4 < 16) ? K / 4 : 16;
-  static constexpr int NV = K / 4 / LPR;
-  static constexpr int G = NT / LPR;  // rows per pass over the workgroup
-  template <typename WT>
-  __device__ static float partial(const WT* row, const float4 (&x4)[NV], int li) {
+  static constexpr int CH = kChunk<WT>;
+  static constexpr int LPR = (K / CH < 16) ? K / CH : 16;
+  static constexpr int NV = K / CH / LPR;
+  static constexpr int NX = NV * CH / 4;  // float4s of the input a lane holds
+  static constexpr int G = NT / LPR;      // rows per pass over the workgroup
+  __device__ static float partial(const WT* row, const float4 (&x4)[NX], int li) {
     float s = 0.f;
 #pragma unroll
-    for (int i = 0; i < NV; ++i) s = dot4(ld4(row + 4 * (li + i * LPR)), x4[i], s);
+    for (int i = 0; i < NV; ++i) {
+      if constexpr (CH == 16) s = dot16_i8(row + CH * (li + i * LPR), x4 + 4 * i, s);
+      else s = dot4(ld4(row + CH * (li + i * LPR)), x4[i], s);
+    }
     return s;
   }
-  __device__ static void load_x(const float* x, float4 (&x4)[NV], int li) {
+  __device__ static void load_x(const float* x, float4 (&x4)[NX], int li) {
 #pragma unroll
-    for (int i = 0; i < NV; ++i) x4[i] = reinterpret_cast<const float4*>(x)[li + i * LPR];
+    for (int i = 0; i < NV; ++i)
+#pragma unroll
+      for (int q = 0; q < CH / 4; ++q) x4[i * (CH / 4) + q] = reinterpret_cast<const float4*>(x)[(li + i * LPR) * (CH / 4) + q];
   }
   __device__ static float reduce(float v) {
 #pragma unroll
@@ -173,9 +197,9 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
     for (int j = 0; j < L; ++j) {
       // ---- a = W_prev x[t-d] + W_cur x[t] + B + L ; h = tanh(a[:R]) * sigmoid(a[R:]) ----
       {
-        using RD = RowDot<R>;
+        using RD = RowDot<R, WT>;
         const int li = tid % RD::LPR, grp = tid / RD::LPR;
-        float4 xp4[RD::NV], xc4[RD::NV];
+        float4 xp4[RD::NX], xc4[RD::NX];
         RD::load_x(xr + j * R, xp4, li);
         RD::load_x(xs, xc4, li);
         const WT* wp = w_prev + (size_t)j * 2 * R * R;
@@ -206,9 +230,9 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
       __syncthreads();
       // ---- x += W_res h + B_res (rows 0..R-1) ; q += W_skip h (rows R..R+S-1) ----
       {
-        using RD = RowDot<R>;
+        using RD = RowDot<R, WT>;
         const int li = tid % RD::LPR, grp = tid / RD::LPR;
-        float4 h4[RD::NV];
+        float4 h4[RD::NX];
         RD::load_x(hs, h4, li);
         const bool last = (j == L - 1);  // x_L feeds nothing
         const WT* wr = w_res + (size_t)j * R * R;
@@ -236,19 +260,20 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
 
     // ---- z_a = relu(W_relu relu(q) + B_relu) ----
     {
-      using RD = RowDot<S>;
+      using RD = RowDot<S, WT>;
       const int li = tid % RD::LPR, grp = tid / RD::LPR;
-      float4 z4[RD::NV];
+      float4 z4[RD::NX];
       RD::load_x(qs, z4, li);
 #pragma unroll
-      for (int i = 0; i < RD::NV; ++i) {
+      for (int i = 0; i < RD::NX; ++i) {
         z4[i].x = fmaxf(z4[i].x, 0.f); z4[i].y = fmaxf(z4[i].y, 0.f);
         z4[i].z = fmaxf(z4[i].z, 0.f); z4[i].w = fmaxf(z4[i].w, 0.f);
       }
-      constexpr int P = A / RD::G;
+      constexpr int P = (A + RD::G - 1) / RD::G;  // int8 rows of s = 32 take 2 lanes: one pass covers 512 rows
 #pragma unroll
       for (int p = 0; p < P; ++p) {
         const int i = p * RD::G + grp;
+        if (i >= A) break;  // uniform over the lanes of a row
         const float v = RD::reduce(RD::partial(w_relu + (size_t)i * S, z4, li)) * row_scale<WT>(args.w.s_relu, i);
         if (li == 0) zas[i] = fmaxf(v + args.w.b_relu[i], 0.f);
       }
@@ -256,9 +281,9 @@ __global__ __launch_bounds__(NT) void wn_stream_kernel(const WnStreamArgs args) 
     __syncthreads();
     // ---- logits = W_out z_a + B_out ----
     {
-      using RD = RowDot<A>;
+      using RD = RowDot<A, WT>;
       const int li = tid % RD::LPR, grp = tid / RD::LPR;
-      float4 z4[RD::NV];
+      float4 z4[RD::NX];
       RD::load_x(zas, z4, li);
       constexpr int P = A / RD::G;
 #pragma unroll

@@ -17,7 +17,9 @@ torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
 MARGIN = 1e-4
-I8_KERNEL = {16: "stream_l2", 32: "stream_l2", 64: "stream_l2", 128: "stream_l2"}
+# the kernel the library picks for int8 models: the multi-CU kernel (which converts the codes to
+# fp32 once, as it loads its resident weights) wherever it serves the shape, else the per-stream one
+I8_KERNEL = {16: "stream_l2", 32: "multi_cu_chain", 64: "multi_cu_chain", 128: "multi_cu_chain"}
 
 CASES = [
     # name, L, r, s, dilations, B, T, bias
@@ -31,16 +33,33 @@ CASES = [
 ]
 
 
+STREAM_CASES = [c for c in CASES if c[0] in ("r32_s128", "l9_r64_s128_b3", "l20_r128_b3")]
+
+
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
-def test_int8_parity(case):
+def test_int8_parity(case, monkeypatch):
+    _int8_case(case, monkeypatch, force_stream=False)
+
+
+@pytest.mark.parametrize("case", STREAM_CASES, ids=[c[0] for c in STREAM_CASES])
+def test_int8_parity_per_stream_kernel(case, monkeypatch):
+    """The per-stream kernel's int8 rows (16 codes per lane and load) for r = 32, 64, 128 and
+    s = 128, 256, which the multi-CU kernel serves by default."""
+    _int8_case(case, monkeypatch, force_stream=True)
+
+
+def _int8_case(case, monkeypatch, force_stream):
     import paper_1702_07825_amd as wn
     name, L, r, s, dil, B, T, bias = case
+    if force_stream:
+        monkeypatch.setenv("WN_KERNEL", "stream")
     seed = zlib.crc32(name.encode()) % 1000
-    print("int8 case %s: L=%d r=%d s=%d B=%d T=%d" % (name, L, r, s, B, T), flush=True)
+    print("int8 case %s%s: L=%d r=%d s=%d B=%d T=%d" % (name, " (per-stream kernel)" if force_stream else "", L, r,
+                                                      s, B, T), flush=True)
     w = synth.make_weights(L, r, s, seed=seed, bias_scale=bias)
     w["w_res"][0, 3] = 0.0  # a row of zeros: scale 0
     net = wn.WaveNet(w, dil, weight_dtype="i8")
-    assert net.kernel_variant(B) == I8_KERNEL[r]
+    assert net.kernel_variant(B) == ("stream_l2" if force_stream else I8_KERNEL[r])
     cond = synth.make_cond(L, r, B, T, seed=seed, device="cuda")
     u = torch.tensor(synth.make_uniforms(B, T, seed=seed), device="cuda")
     y = net.generate(cond, u)

@@ -20,7 +20,7 @@ pytestmark = pytest.mark.gpu
 
 LOGIT_TOL = 1e-3
 MARGIN = 1e-4
-I8_KERNEL = "stream_l2"  # the kernel int8 models with r = 64 run on
+I8_KERNEL = "multi_cu_chain"  # the kernel int8 models with r = 64 run on
 
 CASES = [
     # name, kernel forced ("" = the library's choice), expected variant, L, r, s, dil, B, T, dtype, bias
