@@ -203,11 +203,15 @@ __global__ __launch_bounds__(NT) void wn_group_kernel(const WnGroupArgs g) {
   // Opaque copies of the tile base and the lane offset keep the compiler from hoisting the
   // addresses of loop-invariant tiles (head, first layer) out of the loops, where they would
   // hold registers for the whole call; the load takes the base in SGPRs and the lane offset.
+  // The opaque pointer is generic, so it is cast back to the global address space: a generic
+  // (flat) load also counts against the LDS counter, and every wait for an LDS access or an LDS
+  // barrier would then wait for the weight tiles in flight from L2 as well.
+  typedef const u32x4 __attribute__((address_space(1)))* gtile_ptr;
   auto tile = [&](size_t blk) __attribute__((always_inline)) {
     const char* b = reinterpret_cast<const char*>(pk + blk * 64);
     unsigned o = loff;
     asm volatile("" : "+s"(b), "+v"(o));
-    return *reinterpret_cast<const u32x4*>(b + o);
+    return *(gtile_ptr)(b + o);
   };
   int64_t tg0 = 0;
   {
