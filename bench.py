@@ -49,8 +49,9 @@ def macs_per_sample(L, r, s, a=256, last_res=False):
 
 # Source files each kernel family is built from (the digest of a committed counter run must match).
 KERNEL_SOURCES = {
-    "multi_cu_chain": ["wn_chain.hip", "wn_wave.h", "wn_internal.h"],
-    "mfma_group": ["wn_group.hip", "wn_wave.h", "wn_internal.h"],
+    "multi_cu_chain": ["wn_chain.hip", "wn_msg.h", "wn_wave.h", "wn_internal.h"],
+    "multi_cu_mfma": ["wn_mchain.hip", "wn_mfma.h", "wn_msg.h", "wn_wave.h", "wn_internal.h"],
+    "mfma_group": ["wn_group.hip", "wn_mfma.h", "wn_wave.h", "wn_internal.h"],
     "stream_l2": ["wn_stream.hip", "wn_wave.h", "wn_internal.h"],
     "conditioning": ["wn_cond.hip", "wn_wave.h", "wn_internal.h"],
 }
@@ -146,8 +147,9 @@ def _roofline(name, wl, variant, avg_launch_s, wgs, reps):
     """The dominant kernel's roofline record for one launch of the whole workload."""
     n = wl.B * wl.T
     flop_per_launch = 2.0 * macs_per_sample(wl.n_layers, wl.r, wl.s) * n
-    # The batched kernel computes its products on bf16 MFMA; the others on the fp32 vector ALUs.
-    bound, peak = ("mfma", PEAKS["bf16_mfma_tflops"]) if variant == "mfma_group" else ("alu", PEAKS["f32_vector_tflops"])
+    # The MFMA kernels compute their products on bf16 MFMA; the others on the fp32 vector ALUs.
+    mfma = variant in ("mfma_group", "multi_cu_mfma")
+    bound, peak = ("mfma", PEAKS["bf16_mfma_tflops"]) if mfma else ("alu", PEAKS["f32_vector_tflops"])
     achieved = flop_per_launch / avg_launch_s / 1e12
     hbm_alg = algorithmic_hbm_bytes_per_sample(wl) * n
     onchip = None

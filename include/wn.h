@@ -38,7 +38,8 @@
  *    string for the calling thread's last failure.
  *  - Two calls that share one workspace must not overlap in time.
  *  - Environment variables (tuning and tests; read at wn_create or at each call):
- *      WN_KERNEL=stream      wn_create: serve every call with the per-stream kernel
+ *      WN_KERNEL=name        wn_create: serve every call with one kernel family (a name that
+ *                            wn_kernel_variant returns; calls it cannot serve use stream_l2)
  *      WN_SPIN_LIMIT=n       each call: polls before a multi-CU wait gives up (wn_status)
  *      WN_LOCAL_POSTS=0      each call: the multi-CU kernel writes every message through to
  *                            memory instead of stopping same-XCD messages at the XCD's L2
@@ -229,7 +230,12 @@ int wn_status(wn_handle* h, const void* workspace, void* stream);
  */
 int wn_abort(wn_handle* h, int32_t on);
 
-/* Name of the kernel family that calls with B streams use (for reports). */
+/* Name of the kernel family that calls with B streams use (for reports):
+ *   multi_cu_chain  fp32 (and int8) weights, resident across many CUs, VALU products
+ *   multi_cu_mfma   bf16 and int8 weights (r = 64, s = 256), resident across many CUs, up to 16
+ *                   streams per replica as the columns of MFMA tiles
+ *   mfma_group      bf16 weights (r = 64), every layer of a group of streams on one CU
+ *   stream_l2       any model, one workgroup per stream */
 const char* wn_kernel_variant(const wn_handle* h, int32_t B);
 
 /* For reports: the workgroups (one per CU) a call with B streams launches, and how many

@@ -7,7 +7,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libwn.so")
-SOURCES = ["wn_host.hip", "wn_stream.hip", "wn_chain.hip", "wn_group.hip", "wn_cond.hip"]
+SOURCES = ["wn_host.hip", "wn_stream.hip", "wn_chain.hip", "wn_mchain.hip", "wn_group.hip", "wn_cond.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          # gfx950 code is built without packed-fp32 instructions
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

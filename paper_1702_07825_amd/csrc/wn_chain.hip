@@ -45,6 +45,7 @@
 // head CUs and as many of its aux CUs as fit (the last layers first) share one XCD.
 // The protocol does not depend on that placement, only the hop latency does.
 #include "wn_internal.h"
+#include "wn_msg.h"
 #include "wn_wave.h"
 
 #include "wn.h"
@@ -61,36 +62,6 @@ constexpr int NT = 512;
 constexpr int A = WN_A;
 constexpr int NHEAD = 4;
 constexpr int HR = A / NHEAD;  // z_a rows per head CU
-
-typedef unsigned long long u64;
-
-__device__ __forceinline__ u64 pack(float v, unsigned tag) {
-  return ((u64)tag << 32) | (u64)__float_as_uint(v);
-}
-__device__ __forceinline__ float wval(u64 w) { return __uint_as_float((unsigned)w); }
-__device__ __forceinline__ unsigned wtag(u64 w) { return (unsigned)(w >> 32); }
-__device__ __forceinline__ u64 ldw(const u64* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void stw(u64* p, u64 w) {
-  __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// A post whose reader runs on the same XCD: the store only has to reach that XCD's L2, which the
-// reader's agent-scope loads read through, so it is issued at workgroup scope (it is not written
-// through to memory; measured: 0.64 against 0.86 us per round trip between two CUs of one XCD).
-__device__ __forceinline__ void stw(u64* p, u64 w, bool local) {
-  if (local) __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-  else __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ int ld_status(const int* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Block-uniform abort flag kept in LDS.
-struct Sync {
-  int* flag;
-  __device__ bool failed() const { return *flag != 0; }
-};
 
 // A set of tagged words to wait for: item i lives at base + (i / len) * stride + i % len and
 // its value goes to dst[i].
@@ -957,32 +928,7 @@ __global__ __launch_bounds__(NT) void wn_chain_kernel(const WnChainArgs g) {
     // masks from the map it then reads, so a post is stored at workgroup scope only when its reader
     // runs on the writer's XCD in this launch.  (The host's placement assumes block b on XCD b mod 8;
     // a different map only costs hop latency.)
-    if (threadIdx.x == 0) {
-      unsigned v;
-      asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
-      s_me = (int)(v & 0xf);
-      __hip_atomic_store(g.xmap + blockIdx.x, (u64)(v & 0xf), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      // grid barrier: arrival count and generation after the map
-      u64* cnt = g.xmap + WN_CHAIN_GRID;
-      u64* gen = cnt + 1;
-      const u64 g0 = __hip_atomic_load(gen, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
-      if (__hip_atomic_fetch_add(cnt, 1ull, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) == (u64)(g.n_active - 1)) {
-        __hip_atomic_store(cnt, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_fetch_add(gen, 1ull, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-      } else {
-        int spins = 0;
-        while (__hip_atomic_load(gen, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) == g0) {
-          if (++spins > g.spin_limit) {
-            atomicCAS(g.status, 0, (int)WN_ETIMEOUT);
-            s_me = -1;
-            break;
-          }
-          __builtin_amdgcn_s_sleep(1);
-        }
-      }
-    }
-    __syncthreads();
-    if (s_me < 0) return;  // the grid never met: WN_ETIMEOUT is in the status word
+    if (grid_meet(g.xmap, g.n_active, g.spin_limit, g.status, &s_me) < 0) return;  // WN_ETIMEOUT is in the status word
     for (int b = threadIdx.x; b < WN_CHAIN_GRID; b += NT) {
       const int r = g.role_of_block[b];
       if (r != 0xffff && (MS ? r / per : 0) == k) s_xcd[r - k * per] = (unsigned char)ldw(g.xmap + b);

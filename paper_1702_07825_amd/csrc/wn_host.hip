@@ -11,7 +11,7 @@
 #include <string>
 #include <vector>
 
-enum WnVariant { WN_VARIANT_STREAM = 0, WN_VARIANT_CHAIN = 1, WN_VARIANT_GROUP = 2 };
+enum WnVariant { WN_VARIANT_STREAM = 0, WN_VARIANT_CHAIN = 1, WN_VARIANT_GROUP = 2, WN_VARIANT_MCHAIN = 3 };
 
 struct wn_handle {
   int device = 0;
@@ -25,6 +25,10 @@ struct wn_handle {
   bool chain_ok = false;  // the multi-CU kernel can serve this model (fp32, supported shape)
   bool xcd_map = false;   // blocks of the multi-CU kernel's grid run on XCD (block mod 8)
   bool group_ok = false;  // the batched MFMA kernel serves every B
+  bool mchain_ok = false; // the multi-CU MFMA kernel can serve this model (bf16 or int8, supported shape)
+  // WN_KERNEL at wn_create: the one kernel family calls may use ("" = the default choice); a call the
+  // family cannot serve runs on the per-stream kernel
+  std::string force;
   void* dpack = nullptr;  // its packed bf16 weight tiles
   // int8 models on the multi-CU kernel: the matrices as fp32 values code * scale (that kernel holds
   // its weights in registers and LDS for a whole call, so it takes them in fp32 and reads them once)
@@ -113,9 +117,22 @@ bool chain_plan_for(const wn_handle* h, int B, WnChainPlan* p) {
          (1ull << 32);
 }
 
+// The multi-CU MFMA kernel's layout of B streams, if it serves them.
+bool mchain_plan_for(const wn_handle* h, int B, WnChainPlan* p) {
+  return h->mchain_ok && wn_mchain_plan(h->L, h->R, h->S, B, p);
+}
+
 int variant_for(const wn_handle* h, int B) {
   WnChainPlan p;
+  const std::string& f = h->force;
+  if (f == "stream") return WN_VARIANT_STREAM;
+  if (f == "multi_cu_mfma") return mchain_plan_for(h, B, &p) ? WN_VARIANT_MCHAIN : WN_VARIANT_STREAM;
+  if (f == "multi_cu_chain") return chain_plan_for(h, B, &p) ? WN_VARIANT_CHAIN : WN_VARIANT_STREAM;
+  if (f == "mfma_group") return h->group_ok ? WN_VARIANT_GROUP : WN_VARIANT_STREAM;
   if (chain_plan_for(h, B, &p)) return WN_VARIANT_CHAIN;
+  // int8 batches beyond the fp32 multi-CU kernel's replicas: the MFMA one (2.5x the per-stream kernel
+  // at l = 20, B = 256)
+  if (h->dtype == WN_I8 && mchain_plan_for(h, B, &p)) return WN_VARIANT_MCHAIN;
   return h->group_ok ? WN_VARIANT_GROUP : WN_VARIANT_STREAM;
 }
 
@@ -132,7 +149,14 @@ WsLayout ws_layout(const wn_handle* h, int B) {
   l.state_off = 256;
   l.hist_off = align_up(l.state_off + (size_t)B * WN_STATE_WORDS * sizeof(int64_t), 256);
   WnChainPlan p;
-  if (chain_plan_for(h, B, &p)) {
+  const int v = variant_for(h, B);
+  if (v == WN_VARIANT_MCHAIN && mchain_plan_for(h, B, &p)) {
+    // tagged histories of 16-column tiles per replica, then the replicas' mailboxes and the map
+    l.mb_off = align_up(l.hist_off + (size_t)p.nrep * h->dims.hist_len * 16 * 8, 256);
+    l.mb_words = (size_t)p.nrep * p.mb_words;
+    l.map_off = l.mb_off + l.mb_words * 8;
+    l.total = align_up(l.map_off + (size_t)WN_CHAIN_MAP_WORDS * 8, 256);
+  } else if (v == WN_VARIANT_CHAIN && chain_plan_for(h, B, &p)) {
     l.mb_off = align_up(l.hist_off + (size_t)B * h->dims.hist_len * 8, 256);
     l.mb_words = (size_t)B * p.mb_words;
     l.map_off = l.mb_off + l.mb_words * 8;
@@ -187,10 +211,13 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
   char* base = static_cast<char*>(ws);
   hipStream_t st = static_cast<hipStream_t>(stream);
   WnChainPlan plan;
-  if (chain_plan_for(h, B, &plan)) {
+  const int variant = variant_for(h, B);
+  const bool mchain = variant == WN_VARIANT_MCHAIN && mchain_plan_for(h, B, &plan);
+  if (mchain || (variant == WN_VARIANT_CHAIN && chain_plan_for(h, B, &plan))) {
     WnChainArgs g{};
     g.d = h->dims;
-    g.w = h->dmem_f32 ? h->w_chain : h->w;
+    // the fp32 multi-CU kernel takes an int8 model's fp32 copy; the MFMA one the int8 codes
+    g.w = (h->dmem_f32 && !mchain) ? h->w_chain : h->w;
     g.io.cond = cond;
     g.io.u = u;
     g.io.y_in = y_in;
@@ -241,11 +268,11 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
       const hipError_t e = wn_chain_reset(g.ring, words, g.status, st);
       if (e != hipSuccess) return hip_fail(e, "reset kernel launch");
     }
-    const hipError_t e = wn_chain_launch(g, teacher, st);
+    const hipError_t e = mchain ? wn_mchain_launch(g, teacher, st) : wn_chain_launch(g, teacher, st);
     if (e != hipSuccess) return hip_fail(e, "multi-CU kernel launch");
     return WN_OK;
   }
-  if (variant_for(h, B) == WN_VARIANT_GROUP) {
+  if (variant == WN_VARIANT_GROUP) {
     WnGroupArgs g{};
     g.d = h->dims;
     g.w = h->w;
@@ -450,14 +477,16 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
   }
   h->w.approx_nl = c->nonlinearity == WN_NONLIN_PAPER ? 1 : 0;
 
-  // The multi-CU kernel needs fp32 or int8 weights, a supported shape and one CU per block of its grid.
-  const char* force = std::getenv("WN_KERNEL");
-  const bool want_chain = !(force && std::strcmp(force, "stream") == 0);
+  // The multi-CU kernels need one CU per block of their grid: the fp32 one fp32 or int8 weights, the
+  // MFMA one bf16 or int8 weights, each a supported shape.
+  if (const char* force = std::getenv("WN_KERNEL")) h->force = force;
+  const bool want_chain = h->force != "stream";
   int cus = 0, coop = 0;
   (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device);
   (void)hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, h->device);
   if (want_chain && !bf && wn_chain_supported(R, S, L) && cus >= WN_CHAIN_GRID && coop) h->chain_ok = true;
-  if (h->chain_ok) h->xcd_map = wn_chain_xcd_map_ok();
+  if (want_chain && (bf || i8) && wn_mchain_supported(R, S, L) && cus >= WN_CHAIN_GRID && coop) h->mchain_ok = true;
+  if (h->chain_ok || h->mchain_ok) h->xcd_map = wn_chain_xcd_map_ok();
   if (h->chain_ok && i8) {
     // fp32 copies of the int8 matrices for the multi-CU kernel: each weight code * scale, rounded to
     // fp32 once here (the per-stream kernel multiplies its row sums by the scale instead)
@@ -573,6 +602,7 @@ const char* wn_kernel_variant(const wn_handle* h, int32_t B) {
   if (!h || B < 1) return "";
   switch (variant_for(h, B)) {
     case WN_VARIANT_CHAIN: return "multi_cu_chain";
+    case WN_VARIANT_MCHAIN: return "multi_cu_mfma";
     case WN_VARIANT_GROUP: return "mfma_group";
     default: return "stream_l2";
   }
@@ -581,12 +611,13 @@ const char* wn_kernel_variant(const wn_handle* h, int32_t B) {
 int wn_launch_info(const wn_handle* h, int32_t B, int32_t* workgroups, int32_t* replicas) {
   if (!h || B < 1 || !workgroups || !replicas) return WN_EINVAL;
   WnChainPlan p;
-  if (chain_plan_for(h, B, &p)) {
+  const int v = variant_for(h, B);
+  if ((v == WN_VARIANT_MCHAIN && mchain_plan_for(h, B, &p)) || (v == WN_VARIANT_CHAIN && chain_plan_for(h, B, &p))) {
     int used = 0;
     for (int b = 0; b < WN_CHAIN_GRID; ++b) used += p.role_of_block[b] != 0xffff;
     *workgroups = used;
     *replicas = p.nrep;
-  } else if (h->group_ok) {
+  } else if (v == WN_VARIANT_GROUP) {
     const int gs = wn_group_streams(B);
     *workgroups = (B + gs - 1) / gs;
     *replicas = *workgroups;

@@ -148,6 +148,14 @@ hipError_t wn_status_clear(int* status, hipStream_t stream);
 bool wn_chain_xcd_map_ok();
 hipError_t wn_chain_launch(const WnChainArgs& g, bool teacher, hipStream_t stream);
 
+// Multi-CU kernel for bf16 and int8 models (r = 64): the chain kernel's roles on MFMA, up to 16
+// streams per replica carried together as the columns of 16 x 16 tiles.  Same argument block and
+// workspace words as the chain kernel (mailbox offsets from wn_mchain_plan; the histories hold
+// 16-column tiles per replica, hist_len * 16 words each).
+bool wn_mchain_supported(int R, int S, int L);
+bool wn_mchain_plan(int L, int R, int S, int B, WnChainPlan* p);
+hipError_t wn_mchain_launch(const WnChainArgs& g, bool teacher, hipStream_t stream);
+
 // Batched kernel for bf16 weights: one workgroup per group of 8 or 16 streams, MFMA for every
 // product, weights pre-packed into MFMA operand tiles (wn_group_pack) and streamed from L2.
 struct WnGroupArgs {

@@ -1,0 +1,1101 @@
+// Multi-CU persistent generation kernel for bf16 and int8 models (r = 64) on gfx950 MFMA: up to 16
+// streams per replica go through the layer chain together.
+//
+// The roles and the messages are those of the fp32 multi-CU kernel: the weights stay resident for
+// the whole call, as in the paper's persistent GPU kernel (Deep Voice, arXiv 1702.07825, Appendix
+// D), and the work that does not depend on the current step's chain is done off the chain, a step
+// ahead, as its CPU design does with auxiliary threads (Section 5.1); the arithmetic is Appendix
+// A.1's.  What differs is the batch: a replica carries up to 16 streams at once, one per column of a
+// 16 x 16 MFMA tile, so every product of a layer is a [rows x 64] . [64 x 16] contraction on
+// v_mfma_f32_16x16x32_bf16, and every message is a block of 16-column tiles.
+//
+//   chain CU  (up to NLC layers) wave w keeps row tile w of the tanh half and of the sigmoid half
+//             of W_cur and row tile w of W_res in registers, as MFMA A operands.  Per layer:
+//               phase A  a = pre + W_cur x; h = tanh(a_tanh) sigmoid(a_sigmoid) (a wave holds both
+//                        halves of its rows, so the gate needs no exchange); h goes to the layer's
+//                        aux CU (skip projection), and the layer's input x_{j-1}[t] to its dilation
+//                        history, as tagged tiles;
+//               phase B  x += W_res h + B_res (each lane keeps its four rows of x in fp32).
+//             The last chain CU also computes the last layer's skip projection (its W_skip in LDS)
+//             and posts it to the head.
+//   aux CU    (up to NLA layers) wave v keeps row tiles 2v, 2v + 1 of W_prev and four of W_skip.
+//             For the next step it computes pre = W_prev x_{j-1}[t + 1 - d] + B + L[t + 1] of each
+//             layer (the dilated half, the bias and the HBM read of the conditioning all happen a
+//             step early), and for the current step the sum of W_skip h over its layers.
+//   head CU   wave v keeps four row tiles of W_relu and of W_out.  It sums the skip partials,
+//             z_s = relu(.. + B_skip), z_a = relu(W_relu z_s + B_relu), logits = W_out z_a + B_out,
+//             draws four streams per wave and posts the next step's x0 = E[y] + B_embed
+//             (+ E_prev[y_{t-1}], the two-tap input of Section 5.1) to chain CU 0.
+//
+// A CU runs four waves, one per SIMD, so that each wave can hold 512 registers (the resident weights
+// take up to 240 of them); the layer's critical path is the gate waves' either way.
+//
+// An activation enters a product as a pair of bf16 values, hi = bf16(v) and lo = bf16(v - hi),
+// and both are multiplied, so a product sees about 16 bits of the activation; the weights are
+// exactly bf16 (int8 codes are exact in bf16, and each row's scale multiplies its fp32 result).
+// Accumulation, the gate, the residual and skip sums and the softmax are fp32.
+//
+// Messages are tagged 64-bit words (fp32 value, step + 1; see wn_msg.h) laid out in the MFMA
+// accumulator order: word (tile 64 + lane) 4 + e holds row 16 tile + 4 (lane / 16) + e of column
+// lane mod 16, so the lanes that computed a tile post it as it lies in their registers.  Mailboxes
+// have two slots (step parity); every producer stays at most one step ahead of its consumer.  The
+// dilation histories are rings of such tiles: slot t mod d_j of layer j holds x_{j-1}[t].  Every
+// wait is bounded: a block that times out stores WN_ETIMEOUT in the status word, and every other
+// block sees it in its next wait and leaves, so the grid always drains.
+#include "wn_internal.h"
+#include "wn_mfma.h"
+#include "wn_msg.h"
+#include "wn_wave.h"
+
+#include "wn.h"
+
+#include <algorithm>
+#include <cstdlib>
+#include <type_traits>
+
+namespace {
+
+using namespace wnk;
+
+constexpr int NT = 256;          // four waves: one per SIMD, so each can hold 512 registers
+constexpr int R = 64;
+constexpr int A = WN_A;
+constexpr int GC = 16;         // MFMA columns: the streams of a replica (the others are padding)
+constexpr int NLC = 10;        // layers per chain CU
+constexpr int NLA = 5;         // layers per aux CU
+constexpr int SR = 2 * R + 8;  // split-row pitch (16-bit units) of an r-vector in LDS
+constexpr int XW = R * GC;     // words of an r-vector block (x, h)
+constexpr int PW = 2 * R * GC; // words of a pre-activation block
+
+// Place of (row m, column n) in a block of 16-column tiles: tile m / 16, lane n + 16 ((m mod 16) / 4),
+// element m mod 4 (the MFMA accumulator order); trow / tcol invert it.
+__device__ __forceinline__ int tpos(int m, int n) { return ((((m >> 4) << 6) + n + ((m & 12) << 2)) << 2) + (m & 3); }
+__device__ __forceinline__ int trow(int i) { return ((i >> 8) << 4) + (((i >> 6) & 3) << 2) + (i & 3); }
+__device__ __forceinline__ int tcol(int i) { return (i >> 2) & 15; }
+
+// MFMA A operand from a row-major [rows][K] matrix: row `row`, inputs col .. col + 7 as bf16 (int8
+// codes are exact in bf16).
+template <bool I8>
+__device__ __forceinline__ u32x4 wfrag(const void* W, size_t row, int K, int col) {
+  if constexpr (I8) {
+    const uint2 q = *reinterpret_cast<const uint2*>(static_cast<const signed char*>(W) + row * K + col);
+    auto cv = [](unsigned w, int b) { return (float)(signed char)(w >> (8 * b)); };
+    u32x4 r;
+    r[0] = pack_bf16(cv(q.x, 0), cv(q.x, 1));
+    r[1] = pack_bf16(cv(q.x, 2), cv(q.x, 3));
+    r[2] = pack_bf16(cv(q.y, 0), cv(q.y, 1));
+    r[3] = pack_bf16(cv(q.y, 2), cv(q.y, 3));
+    return r;
+  } else {
+    return *reinterpret_cast<const u32x4*>(static_cast<const u16*>(W) + row * K + col);
+  }
+}
+
+__device__ __forceinline__ f32x4 f4(float4 v) { return f32x4{v.x, v.y, v.z, v.w}; }
+__device__ __forceinline__ float4 v4(f32x4 v) { return make_float4(v[0], v[1], v[2], v[3]); }
+__device__ __forceinline__ u32x4 ld16(const u16* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+// Products whose A operand (resident weights) stays in AGPRs.  The gfx950 MFMA reads its A operand
+// from AGPRs directly; the compiler's builtin takes it from VGPRs and would copy four AGPRs before
+// every product.  A block issues its MFMAs back to back (accumulating into the same registers needs
+// no wait), starts with 2 wait states (an operand a VALU instruction has just written) and ends with
+// 16 (a VALU read of an 8-pass MFMA result needs 11-12), so no instruction around it can see a result
+// in flight.  Two tiles that share their B operands are interleaved.
+#define WN_MFMA "v_mfma_f32_16x16x32_bf16 "
+// a += Wa [hi; lo], b += Wb [hi; lo] over 64 inputs: w*0 / w*1 hold inputs 0-31 / 32-63 of the rows;
+// h0, l0 / h1, l1 the hi and lo parts of this lane's B operand for each half
+__device__ __forceinline__ void mfma_k64_2(f32x4& a, f32x4& b, const u32x4& wa0, const u32x4& wa1, const u32x4& wb0,
+                                           const u32x4& wb1, u32x4 h0, u32x4 l0, u32x4 h1, u32x4 l1) {
+  asm volatile("s_nop 1\n\t"
+               WN_MFMA "%0, %2, %6, %0\n\t" WN_MFMA "%1, %4, %6, %1\n\t"
+               WN_MFMA "%0, %2, %7, %0\n\t" WN_MFMA "%1, %4, %7, %1\n\t"
+               WN_MFMA "%0, %3, %8, %0\n\t" WN_MFMA "%1, %5, %8, %1\n\t"
+               WN_MFMA "%0, %3, %9, %0\n\t" WN_MFMA "%1, %5, %9, %1\n\t"
+               "s_nop 7\n\ts_nop 7"
+               : "+v"(a), "+v"(b)
+               : "a"(wa0), "a"(wa1), "a"(wb0), "a"(wb1), "v"(h0), "v"(l0), "v"(h1), "v"(l1));
+}
+__device__ __forceinline__ f32x4 mfma_k64(f32x4 a, const u32x4& w0, const u32x4& w1, u32x4 h0, u32x4 l0, u32x4 h1,
+                                          u32x4 l1) {
+  asm volatile("s_nop 1\n\t"
+               WN_MFMA "%0, %1, %3, %0\n\t" WN_MFMA "%0, %1, %4, %0\n\t"
+               WN_MFMA "%0, %2, %5, %0\n\t" WN_MFMA "%0, %2, %6, %0\n\t"
+               "s_nop 7\n\ts_nop 7"
+               : "+v"(a)
+               : "a"(w0), "a"(w1), "v"(h0), "v"(l0), "v"(h1), "v"(l1));
+  return a;
+}
+// a += Wa [hi; lo], b += Wb [hi; lo] over 128 inputs (four 32-input chunks k: wa[k], h[k], l[k])
+__device__ __forceinline__ void mfma_k128_2(f32x4& a, f32x4& b, const u32x4 (&wa)[4], const u32x4 (&wb)[4],
+                                            const u32x4 (&h)[4], const u32x4 (&l)[4]) {
+  asm volatile("s_nop 1\n\t"
+               WN_MFMA "%0, %2, %10, %0\n\t" WN_MFMA "%1, %6, %10, %1\n\t"
+               WN_MFMA "%0, %2, %14, %0\n\t" WN_MFMA "%1, %6, %14, %1\n\t"
+               WN_MFMA "%0, %3, %11, %0\n\t" WN_MFMA "%1, %7, %11, %1\n\t"
+               WN_MFMA "%0, %3, %15, %0\n\t" WN_MFMA "%1, %7, %15, %1\n\t"
+               WN_MFMA "%0, %4, %12, %0\n\t" WN_MFMA "%1, %8, %12, %1\n\t"
+               WN_MFMA "%0, %4, %16, %0\n\t" WN_MFMA "%1, %8, %16, %1\n\t"
+               WN_MFMA "%0, %5, %13, %0\n\t" WN_MFMA "%1, %9, %13, %1\n\t"
+               WN_MFMA "%0, %5, %17, %0\n\t" WN_MFMA "%1, %9, %17, %1\n\t"
+               "s_nop 7\n\ts_nop 7"
+               : "+v"(a), "+v"(b)
+               : "a"(wa[0]), "a"(wa[1]), "a"(wa[2]), "a"(wa[3]), "a"(wb[0]), "a"(wb[1]), "a"(wb[2]), "a"(wb[3]),
+                 "v"(h[0]), "v"(h[1]), "v"(h[2]), "v"(h[3]), "v"(l[0]), "v"(l[1]), "v"(l[2]), "v"(l[3]));
+}
+// Four tagged words (one lane's element run of a tile) with one scope decision.
+__device__ __forceinline__ void stw4(u64* p, float4 v, unsigned tag, bool local) {
+  const u64 a = pack(v.x, tag), b = pack(v.y, tag), c = pack(v.z, tag), d = pack(v.w, tag);
+  if (local) {
+    __hip_atomic_store(p + 0, a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    __hip_atomic_store(p + 1, b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    __hip_atomic_store(p + 2, c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    __hip_atomic_store(p + 3, d, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  } else {
+    __hip_atomic_store(p + 0, a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(p + 1, b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(p + 2, c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(p + 3, d, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Polls of pairs of tagged words (16 bytes) through a buffer resource over the workspace's tagged region
+// (histories and mailboxes): 128-bit loads at agent scope (cache policy sc1: past the CU's L1, from
+// the L2), about three times the rate of 64-bit atomic loads per CU (measured: 123 against 38 GB/s),
+// and bounds-checked by the hardware (a read past the region returns zeros).  Each 64-bit word is
+// written whole by one store, so a word read in a pair is never torn; the two words of a pair carry
+// their own tags.  Pair p holds words 2p and 2p + 1 of a block; word(p) is the word offset of word 2p
+// in the region.
+typedef __amdgpu_buffer_rsrc_t wrsrc;
+__device__ __forceinline__ wrsrc tagged_region(const WnChainArgs& g) {
+  const size_t bytes = (size_t)((const char*)(g.mb + (size_t)g.nrep * g.mb_words) - (const char*)g.ring);
+  return __builtin_amdgcn_make_buffer_rsrc((void*)g.ring, (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ u32x4 ld_pair(wrsrc rs, unsigned word) {
+  return __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(word * 8u), 0, 16 /* sc1 */);
+}
+template <int K, int NP = NT, class Word>
+__device__ __forceinline__ void pairs_start(u32x4 (&w)[K], wrsrc rs, int ti, int np, Word word) {
+#pragma unroll
+  for (int k = 0; k < K; ++k)
+    if (ti + k * NP < np) w[k] = ld_pair(rs, word(ti + k * NP));
+}
+// Waits until both words of each of this thread's pairs carry their tags, then sink(i, q, value) for
+// words i = 2p, 2p + 1 in order (q = 2k or 2k + 1: the word's place in the batch).
+// ZZ: s_sleep units (64 clocks each) between two reloads of words that are not there yet: long for
+// waits off the critical path (they would otherwise keep the L2 busy for microseconds), short for the
+// rest.
+template <int K, int NP = NT, int ZZ = 1, class Word, class Tag, class Sink>
+__device__ __forceinline__ void pairs_finish(const WnChainArgs& g, u32x4 (&w)[K], wrsrc rs, int ti, int np, Word word,
+                                             Tag tag, Sink sink, Sync s) {
+  static_assert(K <= 32, "pending bits");
+  unsigned pend = 0;
+#pragma unroll
+  for (int k = 0; k < K; ++k)
+    if (ti + k * NP < np) pend |= 1u << k;
+  int spins = 0;
+  for (;;) {
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      const int p = ti + k * NP;
+      if (((pend >> k) & 1u) && w[k][1] == tag(2 * p) && w[k][3] == tag(2 * p + 1)) pend &= ~(1u << k);
+    }
+    if (!pend) break;
+    if (++spins > g.spin_limit || ((spins & 63) == 0 && ld_status(g.status) != 0)) {
+      if (ld_status(g.status) == 0) atomicCAS(g.status, 0, (int)WN_ETIMEOUT);
+      *s.flag = 1;
+      return;
+    }
+    if constexpr (ZZ > 0) __builtin_amdgcn_s_sleep(ZZ);
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+      if ((pend >> k) & 1u) w[k] = ld_pair(rs, word(ti + k * NP));
+  }
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const int p = ti + k * NP;
+    if (p < np) {
+      sink(2 * p, 2 * k, __uint_as_float(w[k][0]));
+      sink(2 * p + 1, 2 * k + 1, __uint_as_float(w[k][2]));
+    }
+  }
+}
+// Both halves at once, in batches of K pairs per thread.
+template <int K, int NP = NT, int ZZ = 1, class Word, class Tag, class Sink>
+__device__ __forceinline__ void poll_pairs(const WnChainArgs& g, wrsrc rs, int ti, int np, Word word, Tag tag, Sink sink,
+                                           Sync s) {
+  for (int base = 0; base < np; base += K * NP) {
+    u32x4 w[K];
+    const int rem = np - base;
+    auto wd = [&](int p) { return word(base + p); };
+    auto tg = [&](int i) { return tag(2 * base + i); };
+    auto sk = [&](int i, int q, float v) { sink(2 * base + i, q, v); };
+    pairs_start<K, NP>(w, rs, ti, rem, wd);
+    pairs_finish<K, NP, ZZ>(g, w, rs, ti, rem, wd, tg, sk, s);
+    if (s.failed()) return;
+  }
+}
+
+// tanh(a) sigmoid(g) with two exponentials and one reciprocal: (e^{2a} - 1) / ((e^{2a} + 1)(1 + e^{-g})).
+// a is clamped to +-15, where tanh is +-1 to fp32 already; a large -g makes e^{-g} infinite and the
+// product 0, as sigmoid's limit.
+__device__ __forceinline__ float gate_tanh_sigmoid(float a, float g) {
+  const float e2a = expf_fast(2.0f * fminf(fmaxf(a, -15.0f), 15.0f));
+  const float eg = expf_fast(-g);
+  return (e2a - 1.0f) * __builtin_amdgcn_rcpf((e2a + 1.0f) * (1.0f + eg));
+}
+template <bool AX>
+__device__ __forceinline__ float gate_h(float a, float g) {
+  if constexpr (AX) return tanh_paper(a) * sigmoid_paper(g);
+  else return gate_tanh_sigmoid(a, g);
+}
+
+// A polled word of an r-vector block into a split row set [GC][SR] (hi and lo parts).
+__device__ __forceinline__ void split_into(u16* rows, int i, float v) {
+  const int m = trow(i), c = tcol(i);
+  split1(v, rows[c * SR + m], rows[c * SR + R + m]);
+}
+
+// Dynamic LDS of each role, in bytes (the launch takes the largest); mirrors the carving below.
+constexpr size_t chain_lds(int S) {
+  return 4 * ((size_t)NLC * PW + (size_t)XW + (size_t)NLC * R + (size_t)NLC * 3 * R + S) + 2 * (size_t)3 * GC * SR +
+         (size_t)(S / 16) * 2 * 64 * 16;
+}
+constexpr size_t aux_lds(int S) {
+  return 4 * ((size_t)NLA * PW + (size_t)NLA * 4 * R + (size_t)NLA * S) + 2 * (size_t)2 * NLA * GC * SR;
+}
+constexpr size_t head_lds(int S) {
+  return 2 * ((size_t)GC * (2 * S + 8) + (size_t)GC * (2 * A + 8)) + 4 * ((size_t)GC * (A + 4) + S + 6 * A + R) +
+         2 * (size_t)2 * A * R;
+}
+
+// ------------------------------------------------------------------------------------------
+// chain CU: layers j0 .. j0 + nl - 1
+// ------------------------------------------------------------------------------------------
+template <int S, bool AX, bool I8>
+__device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, const int rep, float* dyn, Sync sy, const int64_t tg0,
+                         const unsigned lm) {
+  constexpr int KS = S / 64;  // row tiles per wave of the last layer's W_skip (tail)
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = lane & 15, quad = lane >> 4;
+  const int L = g.d.L, T = g.io.T;
+  const int j0 = g.layer_begin[c], nl = g.layer_begin[c + 1] - j0;
+  const bool tail = c + 1 == g.nch && g.tail_on_chain;
+  u64* const mb = g.mb + (size_t)rep * g.mb_words;
+  u64* const ring = g.ring + (size_t)rep * g.d.hist_len * GC;
+  const wrsrc rs = tagged_region(g);
+  const unsigned mbw = (unsigned)(mb - g.ring);  // word offset of my replica's mailboxes in the region
+  float* PRE = dyn;                  // [NLC][PW] this step's pre-activations of my layers
+  float* XF = PRE + NLC * PW;        // [XW]      the step's input x, fp32
+  float* BRS = XF + XW;              // [NLC][R]  B_res
+  float* SCL = BRS + NLC * R;        // [NLC][3R] int8: row scales of W_cur (2R rows) and W_res (R)
+  float* SSK = SCL + NLC * 3 * R;    // [S]       int8: row scales of the last layer's W_skip
+  u16* XS = reinterpret_cast<u16*>(SSK + S);             // [2][GC][SR] x, split, by layer parity
+  u16* HS = XS + 2 * GC * SR;                            // [GC][SR]    h, split
+  u32x4* WSK = reinterpret_cast<u32x4*>(HS + GC * SR);   // [S/16][2][64] the last layer's W_skip tiles
+
+  // wave w: row tile w of the tanh half and of the sigmoid half of W_cur, row tile w of W_res
+  const int m0 = 16 * wave + 4 * quad;  // this lane's rows of x, h and the tanh half of a
+  u32x4 wt[NLC][2], wg[NLC][2], wr[NLC][2];
+#pragma unroll
+  for (int l = 0; l < NLC; ++l) {
+    const size_t j = (size_t)j0 + (l < nl ? l : 0);
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      const int col = 32 * kt + 8 * quad;
+      wt[l][kt] = wfrag<I8>(g.w.w_cur, j * 2 * R + 16 * wave + n, R, col);
+      wg[l][kt] = wfrag<I8>(g.w.w_cur, j * 2 * R + R + 16 * wave + n, R, col);
+      wr[l][kt] = wfrag<I8>(g.w.w_res, j * R + 16 * wave + n, R, col);
+    }
+  }
+  for (int i = tid; i < nl * R; i += NT) BRS[i] = g.w.b_res[(size_t)j0 * R + i];
+  if constexpr (I8) {
+    for (int i = tid; i < nl * 3 * R; i += NT) {
+      const int l = i / (3 * R), m = i % (3 * R);
+      SCL[i] = m < 2 * R ? g.w.s_cur[(size_t)(j0 + l) * 2 * R + m] : g.w.s_res[(size_t)(j0 + l) * R + (m - 2 * R)];
+    }
+  }
+  if (tail) {
+    for (int i = tid; i < (S / 16) * 2 * 64; i += NT) {
+      const int ln = i & 63, kt = (i >> 6) & 1, rt = i >> 7;
+      WSK[i] = wfrag<I8>(g.w.w_skip, (size_t)(L - 1) * S + 16 * rt + (ln & 15), R, 32 * kt + 8 * (ln >> 4));
+    }
+    if constexpr (I8)
+      for (int i = tid; i < S; i += NT) SSK[i] = g.w.s_skip[(size_t)(L - 1) * S + i];
+  }
+  // history slot (t mod d_j), dilation and offset of each of my layers
+  int slot[NLC], dil[NLC], hoff[NLC];
+#pragma unroll
+  for (int l = 0; l < NLC; ++l) {
+    const int j = j0 + (l < nl ? l : 0);
+    dil[l] = g.d.dil[j];
+    hoff[l] = g.d.hoff[j];
+    slot[l] = (int)(tg0 % dil[l]);
+  }
+  __syncthreads();
+
+  float4 xr = make_float4(0.f, 0.f, 0.f, 0.f);  // x_{j-1}[t], rows m0 .. m0 + 3 of column n, fp32
+  for (int64_t t = tg0; t < tg0 + T; ++t) {
+    const unsigned tag = (unsigned)(t + 1);
+    const int par = (int)(t & 1);
+    // the pre-activations of my layers (posted by their aux CUs during the previous step), then the
+    // input x: from the previous chain CU, or for chain CU 0 the head's x0
+    const unsigned pre_w = mbw + ((unsigned)j0 * 2 + par) * PW;
+    poll_pairs<16, NT, 16>(
+        g, rs, tid, nl * PW / 2, [&](int p) { return pre_w + (unsigned)((2 * p) / PW) * 2 * PW + (2 * p) % PW; },
+        [&](int) { return tag; }, [&](int i, int, float v) { PRE[i] = v; }, sy);
+    const unsigned x_w = mbw + g.off_x + ((unsigned)c * 2 + par) * XW;
+    poll_pairs<2>(
+        g, rs, tid, XW / 2, [&](int p) { return x_w + 2 * p; }, [&](int) { return tag; },
+        [&](int i, int, float v) {
+          XF[i] = v;
+          split_into(XS, i, v);
+        },
+        sy);
+    lds_barrier();
+    if (sy.failed()) return;
+    xr = *reinterpret_cast<const float4*>(XF + (wave * 64 + lane) * 4);
+#pragma unroll
+    for (int l = 0; l < NLC; ++l) {
+      if (l < nl) {
+        const int j = j0 + l;
+        const int ot = (wave * 64 + lane) * 4;  // this lane's words of a tile block
+        {
+          // a = pre + W_cur x_{j-1}; h = tanh(a[rows]) sigmoid(a[R + rows])
+          const u16* xs = XS + (l & 1) * GC * SR + n * SR;
+          const float4 pt = *reinterpret_cast<const float4*>(PRE + l * PW + ot);
+          const float4 pg = *reinterpret_cast<const float4*>(PRE + l * PW + 4 * 64 * 4 + ot);
+          f32x4 at = {0.f, 0.f, 0.f, 0.f}, ag = {0.f, 0.f, 0.f, 0.f};
+          if constexpr (!I8) {
+            at = f4(pt);
+            ag = f4(pg);
+          }
+          mfma_k64_2(at, ag, wt[l][0], wt[l][1], wg[l][0], wg[l][1], ld16(xs + 8 * quad), ld16(xs + R + 8 * quad),
+                     ld16(xs + 32 + 8 * quad), ld16(xs + R + 32 + 8 * quad));
+          // x_{j-1}[t] into slot t mod d_j of layer j's history, which its aux CU reads at t + d_j
+          stw4(ring + ((size_t)hoff[l] + (size_t)slot[l] * R) * GC + ot, xr, tag, (lm >> l) & 1u);
+          slot[l] = slot[l] + 1 == dil[l] ? 0 : slot[l] + 1;
+          if constexpr (I8) {
+            const float4 st = *reinterpret_cast<const float4*>(SCL + l * 3 * R + m0);
+            const float4 sg = *reinterpret_cast<const float4*>(SCL + l * 3 * R + R + m0);
+            at = f32x4{pt.x + st.x * at[0], pt.y + st.y * at[1], pt.z + st.z * at[2], pt.w + st.w * at[3]};
+            ag = f32x4{pg.x + sg.x * ag[0], pg.y + sg.y * ag[1], pg.z + sg.z * ag[2], pg.w + sg.w * ag[3]};
+          }
+          float4 h;
+          h.x = gate_h<AX>(at[0], ag[0]);
+          h.y = gate_h<AX>(at[1], ag[1]);
+          h.z = gate_h<AX>(at[2], ag[2]);
+          h.w = gate_h<AX>(at[3], ag[3]);
+          store_split4<R>(HS + n * SR, m0, h);
+          // h_j[t] -> the layer's aux CU
+          stw4(mb + g.off_h + ((size_t)j * 2 + par) * XW + ot, h, tag, (lm >> l) & 1u);
+        }
+        lds_barrier();
+        if (j < L - 1) {  // x_l feeds nothing
+          // x_j = x_{j-1} + W_res h + B_res
+          const float4 br = *reinterpret_cast<const float4*>(BRS + l * R + m0);
+          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+          if constexpr (!I8) acc = f32x4{xr.x + br.x, xr.y + br.y, xr.z + br.z, xr.w + br.w};
+          {
+            const u16* hs = HS + n * SR;
+            acc = mfma_k64(acc, wr[l][0], wr[l][1], ld16(hs + 8 * quad), ld16(hs + R + 8 * quad), ld16(hs + 32 + 8 * quad),
+                           ld16(hs + R + 32 + 8 * quad));
+          }
+          if constexpr (I8) {
+            const float4 sr = *reinterpret_cast<const float4*>(SCL + l * 3 * R + 2 * R + m0);
+            xr = make_float4(xr.x + br.x + sr.x * acc[0], xr.y + br.y + sr.y * acc[1], xr.z + br.z + sr.z * acc[2],
+                             xr.w + br.w + sr.w * acc[3]);
+          } else {
+            xr = v4(acc);
+          }
+          store_split4<R>(XS + ((l + 1) & 1) * GC * SR + n * SR, m0, xr);
+          if (l == nl - 1 && c + 1 < g.nch) {
+            // x of my last layer -> the next chain CU
+            stw4(mb + g.off_x + ((size_t)(c + 1) * 2 + par) * XW + ot, xr, tag, (lm >> 16) & 1u);
+          }
+          lds_barrier();
+        }
+      }
+    }
+    if (tail) {
+      // the last layer's skip projection W_skip h_{l-1} (h is in HS): row tiles KS wave .. + KS - 1
+#pragma unroll
+      for (int k = 0; k < KS; ++k) {
+        const int rt = KS * wave + k;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) acc = mfma_row<R>(WSK[(rt * 2 + kt) * 64 + lane], HS + n * SR, 32 * kt + 8 * quad, acc);
+        if constexpr (I8) {
+          const float4 s4 = *reinterpret_cast<const float4*>(SSK + rt * 16 + 4 * quad);
+          acc = f32x4{s4.x * acc[0], s4.y * acc[1], s4.z * acc[2], s4.w * acc[3]};
+        }
+        stw4(mb + g.off_qtail + (size_t)par * S * GC + (rt * 64 + lane) * 4, v4(acc), tag, (lm >> 17) & 1u);
+      }
+      lds_barrier();  // HS is rewritten in the next step's first layer
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// aux CU: layers ja .. ja + nl - 1
+// ------------------------------------------------------------------------------------------
+template <int S, bool AX, bool I8>
+__device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const int rep, float* dyn, Sync sy, const int64_t tg0,
+                       const unsigned lm) {
+  constexpr int KS = S / 64;  // row tiles of W_skip per wave
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = lane & 15, quad = lane >> 4;
+  const int L = g.d.L, T = g.io.T;
+  const int ja = ai * g.nla, nl = min(g.nla, L - ja);
+  // layers whose skip projection this CU computes (the last layer's runs on the last chain CU)
+  const int nsk = (g.tail_on_chain && ja + nl == L) ? nl - 1 : nl;
+  const int b0 = rep * g.G, ns = min(g.G, g.io.B - b0);
+  u64* const mb = g.mb + (size_t)rep * g.mb_words;
+  const u64* const ring = g.ring + (size_t)rep * g.d.hist_len * GC;
+  const wrsrc rs = tagged_region(g);
+  const unsigned mbw = (unsigned)(mb - g.ring), rgw = (unsigned)(ring - g.ring);
+  float* CD = dyn;                 // [NLA][PW]  conditioning rows L[b, t + 1, j], tile order
+  float* BG = CD + NLA * PW;       // [NLA][2R]  B (gate bias)
+  float* SP = BG + NLA * 2 * R;    // [NLA][2R]  int8: row scales of W_prev
+  float* SK = SP + NLA * 2 * R;    // [NLA][S]   int8: row scales of W_skip
+  u16* HX = reinterpret_cast<u16*>(SK + NLA * S);  // [NLA][GC][SR] history rows x_{j-1}[t + 1 - d], split
+  u16* HH = HX + NLA * GC * SR;                    // [NLA][GC][SR] h_j[t], split
+  __shared__ unsigned long long s_hb[NLA];         // stage(): history block (word offset) of each polled layer
+  __shared__ unsigned s_ht[NLA];                   //          and the tag it must carry
+  __shared__ int s_hl[NLA], s_nh;                  //          and its layer index; how many
+
+  // wave v: row tiles 2v, 2v + 1 of W_prev and KS v .. KS v + KS - 1 of W_skip
+  u32x4 wp[NLA][2][2], wk[NLA][KS][2];
+  int dl[NLA], ho[NLA];
+#pragma unroll
+  for (int l = 0; l < NLA; ++l) {
+    const size_t j = (size_t)ja + (l < nl ? l : 0);
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      const int col = 32 * kt + 8 * quad;
+#pragma unroll
+      for (int k = 0; k < 2; ++k) wp[l][k][kt] = wfrag<I8>(g.w.w_prev, j * 2 * R + 16 * (2 * wave + k) + n, R, col);
+#pragma unroll
+      for (int k = 0; k < KS; ++k) wk[l][k][kt] = wfrag<I8>(g.w.w_skip, j * S + 16 * (KS * wave + k) + n, R, col);
+    }
+    dl[l] = g.d.dil[ja + (l < nl ? l : 0)];
+    ho[l] = g.d.hoff[ja + (l < nl ? l : 0)];
+  }
+  for (int i = tid; i < nl * 2 * R; i += NT) BG[i] = g.w.b_gate[(size_t)ja * 2 * R + i];
+  if constexpr (I8) {
+    for (int i = tid; i < nl * 2 * R; i += NT) SP[i] = g.w.s_prev[(size_t)ja * 2 * R + i];
+    for (int i = tid; i < nl * S; i += NT) SK[i] = g.w.s_skip[(size_t)ja * S + i];
+  }
+  for (int i = tid; i < NLA * PW; i += NT) CD[i] = 0.f;  // padding columns stay zero
+  __syncthreads();
+
+  // Conditioning rows of step ts, two float4s per thread and layer: piece q (0 .. 511) holds rows
+  // 4 (q mod 32) .. + 3 of column q / 32, i.e. tile (q mod 32) / 4, lane q / 32 + 16 (q mod 4).
+  // Columns past the replica's streams read the last stream's row and never store it.
+  constexpr int CQ = 2 * R * GC / 4 / NT;
+  size_t cq_src[CQ];
+  int cq_dst[CQ];
+  bool cq_on[CQ];
+#pragma unroll
+  for (int k = 0; k < CQ; ++k) {
+    const int q = tid + NT * k, cn = q >> 5, e4 = q & 31;
+    cq_on[k] = cn < ns;
+    cq_src[k] = (size_t)min(cn, ns - 1) * T * L * 2 * R + 4 * e4;  // + (step L + layer) 2R
+    cq_dst[k] = ((e4 >> 2) * 64 + cn + 16 * (e4 & 3)) * 4;
+  }
+  const float* const cbase = g.io.cond + (size_t)b0 * T * L * 2 * R;
+  // Stage the inputs of pre_j[ts]: the conditioning rows of every layer and the history rows
+  // x_{j-1}[ts - d] of the layers with d >= 2 (final once step ts - d is over), or of every layer
+  // (all_hist, the call's first step).  With d = 1 the row is written during step ts - 1 and is
+  // waited for together with h_j.
+  auto stage = [&](int64_t ts, bool all_hist) __attribute__((always_inline)) {
+    float4 cq[NLA][CQ];
+    const float* crow = cbase + ((size_t)(ts - tg0) * L + ja) * 2 * R;
+#pragma unroll
+    for (int l = 0; l < NLA; ++l)
+#pragma unroll
+      for (int k = 0; k < CQ; ++k)
+        cq[l][k] = l < nl ? *reinterpret_cast<const float4*>(crow + cq_src[k] + l * 2 * R) : make_float4(0.f, 0.f, 0.f, 0.f);
+    if (tid == 0) {
+      int nh = 0;
+#pragma unroll
+      for (int l = 0; l < NLA; ++l) {
+        if (l < nl && (all_hist || dl[l] >= 2)) {
+          const int d = dl[l];
+          const int64_t sl = ts % d;
+          s_hb[nh] = ((unsigned long long)ho[l] + (unsigned long long)sl * R) * GC;
+          s_ht[nh] = ts - d >= 0 ? (unsigned)(ts - d + 1) : 0u;
+          s_hl[nh] = l;
+          ++nh;
+        }
+      }
+      s_nh = nh;
+    }
+    __syncthreads();
+    poll_pairs<4, NT, 16>(
+        g, rs, tid, s_nh * XW / 2, [&](int p) { return rgw + (unsigned)s_hb[(2 * p) / XW] + (2 * p) % XW; },
+        [&](int i) { return s_ht[i / XW]; },
+        [&](int i, int, float v) { split_into(HX + s_hl[i / XW] * GC * SR, i % XW, v); }, sy);
+#pragma unroll
+    for (int l = 0; l < NLA; ++l)
+#pragma unroll
+      for (int k = 0; k < CQ; ++k)
+        if (l < nl && cq_on[k]) *reinterpret_cast<float4*>(CD + l * PW + cq_dst[k]) = cq[l][k];
+    lds_barrier();
+  };
+  // pre_j[ts] = W_prev x_{j-1}[ts - d] + B + L[b, ts, j] of row tiles 2 wave, 2 wave + 1, j = ja + l,
+  // posted with tag ts + 1
+  auto post_pre = [&](int l, int64_t ts) __attribute__((always_inline)) {
+    const unsigned tg = (unsigned)(ts + 1);
+    const bool loc = (lm >> l) & 1u;
+    f32x4 pa[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+    {
+      const u16* hx = HX + l * GC * SR + n * SR;
+      mfma_k64_2(pa[0], pa[1], wp[l][0][0], wp[l][0][1], wp[l][1][0], wp[l][1][1], ld16(hx + 8 * quad),
+                 ld16(hx + R + 8 * quad), ld16(hx + 32 + 8 * quad), ld16(hx + R + 32 + 8 * quad));
+    }
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int rt = 2 * wave + k;
+      const f32x4 acc = pa[k];
+      const int mr = 16 * rt + 4 * quad;
+      const float4 b = *reinterpret_cast<const float4*>(BG + l * 2 * R + mr);
+      const float4 cd = *reinterpret_cast<const float4*>(CD + l * PW + (rt * 64 + lane) * 4);
+      float4 v;
+      if constexpr (I8) {
+        const float4 s4 = *reinterpret_cast<const float4*>(SP + l * 2 * R + mr);
+        v = make_float4(s4.x * acc[0] + b.x + cd.x, s4.y * acc[1] + b.y + cd.y, s4.z * acc[2] + b.z + cd.z,
+                        s4.w * acc[3] + b.w + cd.w);
+      } else {
+        v = make_float4(acc[0] + b.x + cd.x, acc[1] + b.y + cd.y, acc[2] + b.z + cd.z, acc[3] + b.w + cd.w);
+      }
+      stw4(mb + ((size_t)(ja + l) * 2 + (ts & 1)) * PW + (rt * 64 + lane) * 4, v, tg, loc);
+    }
+  };
+
+  stage(tg0, true);
+  if (sy.failed()) return;
+#pragma unroll
+  for (int l = 0; l < NLA; ++l)
+    if (l < nl) post_pre(l, tg0);
+  for (int64_t t = tg0; t < tg0 + T; ++t) {
+    const bool more = t + 1 < tg0 + T;
+    const int par = (int)(t & 1);
+    const unsigned tag = (unsigned)(t + 1);
+    // A host abort request, read every WN_ABORT_CHECK steps by the replica's first aux CU, which works
+    // a step ahead of the chain (the read's PCIe round trip stays off the critical path); every other
+    // role sees the status word in its next wait and leaves too.
+    if (ai == 0 && tid == 0 && ((t - tg0) & (WN_ABORT_CHECK - 1)) == 0 && abort_requested(g.io.abort_flag)) {
+      atomicCAS(g.status, 0, (int)WN_EABORTED);
+      *sy.flag = 1;
+    }
+    lds_barrier();
+    if (sy.failed()) return;
+    if (more) {
+      stage(t + 1, false);
+      if (sy.failed()) return;
+    }
+    f32x4 qs[KS];
+#pragma unroll
+    for (int k = 0; k < KS; ++k) qs[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // The words each layer waits for: h_j[t] and, with d = 1, the history row x_{j-1}[t] that
+    // pre_j[t + 1] reads.  Once h_j[t] is in, the chain has consumed pre_j[t], so posting pre_j[t + 1]
+    // cannot overwrite a slot it has yet to read.  The next layer's loads are issued before this
+    // layer's products, so their round trip overlaps them.
+    auto lw_n = [&](int l) { return (more && dl[l] == 1) ? XW : XW / 2; };  // pairs
+    auto lw_word = [&](int l) {
+      const unsigned hw = mbw + g.off_h + ((unsigned)(ja + l) * 2 + par) * XW;
+      const unsigned xw = rgw + (unsigned)ho[l] * GC;
+      return [=](int p) { return 2 * p < XW ? hw + 2 * p : xw + (2 * p - XW); };
+    };
+    u32x4 pw[XW / NT];
+    pairs_start(pw, rs, tid, lw_n(0), lw_word(0));
+#pragma unroll
+    for (int l = 0; l < NLA; ++l) {
+      if (l < nl) {
+        pairs_finish(
+            g, pw, rs, tid, lw_n(l), lw_word(l), [&](int) { return tag; },
+            [&](int i, int, float v) {
+              if (i < XW) split_into(HH + l * GC * SR, i, v);
+              else split_into(HX + l * GC * SR, i - XW, v);
+            },
+            sy);
+        lds_barrier();
+        if (sy.failed()) return;
+        if (l + 1 < NLA && l + 1 < nl) pairs_start(pw, rs, tid, lw_n(l + 1), lw_word(l + 1));
+        if (l < nsk) {
+          // q += W_skip h_j, row tiles KS wave ..
+          const u16* hh = HH + l * GC * SR + n * SR;
+          const u32x4 h0 = ld16(hh + 8 * quad), l0 = ld16(hh + R + 8 * quad), h1 = ld16(hh + 32 + 8 * quad),
+                      l1 = ld16(hh + R + 32 + 8 * quad);
+          f32x4 sa[KS];
+#pragma unroll
+          for (int k = 0; k < KS; ++k) sa[k] = I8 ? f32x4{0.f, 0.f, 0.f, 0.f} : qs[k];
+#pragma unroll
+          for (int k = 0; k < KS; k += 2)
+            mfma_k64_2(sa[k], sa[k + 1], wk[l][k][0], wk[l][k][1], wk[l][k + 1][0], wk[l][k + 1][1], h0, l0, h1, l1);
+#pragma unroll
+          for (int k = 0; k < KS; ++k) {
+            const f32x4 acc = sa[k];
+            if constexpr (I8) {
+              const float4 s4 = *reinterpret_cast<const float4*>(SK + l * S + (KS * wave + k) * 16 + 4 * quad);
+              qs[k] = f32x4{qs[k][0] + s4.x * acc[0], qs[k][1] + s4.y * acc[1], qs[k][2] + s4.z * acc[2],
+                            qs[k][3] + s4.w * acc[3]};
+            } else {
+              qs[k] = acc;
+            }
+          }
+          // The partial goes out as soon as its last layer is in, with the previous aux CU's added: the
+          // partials of all but the last posting aux CU form a running sum, so the head waits for two
+          // of them (the last one is posted alone, to keep this wait off the end of the step).  A lane
+          // reads the previous partial's words it holds itself (same tiles and elements).
+          if (l == nsk - 1) {
+            if (ai > 0 && ai < g.naux_q - 1) {
+              const unsigned pq = mbw + g.off_q + ((unsigned)(ai - 1) * 2 + par) * S * GC;
+              poll_pairs<2 * KS, 1>(
+                  g, rs, 0, 2 * KS, [&](int p) { return pq + ((KS * wave + (p >> 1)) * 64 + lane) * 4 + 2 * (p & 1); },
+                  [&](int) { return tag; }, [&](int, int q, float v) { qs[q >> 2][q & 3] += v; }, sy);
+            }
+            const bool loc = (lm >> 16) & 1u;
+#pragma unroll
+            for (int k = 0; k < KS; ++k)
+              stw4(mb + g.off_q + ((size_t)ai * 2 + par) * S * GC + ((KS * wave + k) * 64 + lane) * 4, v4(qs[k]), tag, loc);
+          }
+        }
+      }
+    }
+    // the next step's pre-activations, once the skip partial is out (each layer's h_j[t] is in)
+    if (more) {
+#pragma unroll
+      for (int l = 0; l < NLA; ++l)
+        if (l < nl) post_pre(l, t + 1);
+    }
+    lds_barrier();
+  }
+}
+
+// The head's products for the four row tiles of a wave: acc[k] = W[k] [hi; lo] over K inputs (a split
+// row of this lane's column at `row`), two tiles and 128 inputs per MFMA block.
+template <int K, int KT>
+__device__ __forceinline__ void head_products(f32x4 (&acc)[4], const u32x4 (&w)[4][KT], const u16* row, int quad) {
+  static_assert(KT % 4 == 0, "128-input blocks");
+#pragma unroll
+  for (int k = 0; k < 4; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // every B operand first (one LDS round trip), then the MFMA blocks back to back
+  u32x4 hb[KT], lb[KT];
+#pragma unroll
+  for (int q = 0; q < KT; ++q) {
+    hb[q] = ld16(row + 32 * q + 8 * quad);
+    lb[q] = ld16(row + K + 32 * q + 8 * quad);
+  }
+#pragma unroll
+  for (int kb = 0; kb < KT; kb += 4) {
+    const u32x4 h[4] = {hb[kb], hb[kb + 1], hb[kb + 2], hb[kb + 3]};
+    const u32x4 l[4] = {lb[kb], lb[kb + 1], lb[kb + 2], lb[kb + 3]};
+#pragma unroll
+    for (int k = 0; k < 4; k += 2) {
+      const u32x4 wa[4] = {w[k][kb], w[k][kb + 1], w[k][kb + 2], w[k][kb + 3]};
+      const u32x4 wb[4] = {w[k + 1][kb], w[k + 1][kb + 1], w[k + 1][kb + 2], w[k + 1][kb + 3]};
+      mfma_k128_2(acc[k], acc[k + 1], wa, wb, h, l);
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// head CU: the skip sum, the two head layers, the draw and the next step's x0
+// ------------------------------------------------------------------------------------------
+template <int S, bool TF, bool AX, bool I8>
+__device__ __forceinline__ void mc_head(const WnChainArgs& g, const int rep, float* dyn, Sync sy, const int64_t tg0,
+                        const unsigned lm) {
+  constexpr int KTH = S / 32, KTO = A / 32;
+  constexpr int SS = 2 * S + 8, SA = 2 * A + 8, PA = A + 4;
+  constexpr int QW = S * GC;     // words of a skip partial
+  constexpr int NQ = QW / NT;    // skip-sum entries per thread
+  constexpr int HT = A / 16 / 4; // row tiles of W_relu and of W_out per wave
+  static_assert(16 % NQ == 0, "a poll batch covers whole partials");
+  static_assert(HT == 4, "four row tiles per wave");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = lane & 15, quad = lane >> 4;
+  const int T = g.io.T;
+  const int b0 = rep * g.G, ns = min(g.G, g.io.B - b0);
+  const bool e2 = g.w.embed_prev != nullptr;
+  u64* const mb = g.mb + (size_t)rep * g.mb_words;
+  const wrsrc rs = tagged_region(g);
+  const unsigned mbw = (unsigned)(mb - g.ring);
+  u16* ZS = reinterpret_cast<u16*>(dyn);               // [GC][SS] z_s, split
+  u16* ZA = ZS + GC * SS;                              // [GC][SA] z_a, split
+  float* LG = reinterpret_cast<float*>(ZA + GC * SA);  // [GC][PA] logits
+  float* BSK = LG + GC * PA;  // [S] B_skip
+  float* BRL = BSK + S;       // [A] B_relu
+  float* BO = BRL + A;        // [A] B_out
+  float* BE = BO + A;         // [R] B_embed
+  float* SRL = BE + R;        // [A] int8: row scales of W_relu, W_out and the two embedding tables
+  float* SO = SRL + A;
+  float* SE = SO + A;
+  float* SEP = SE + A;
+  u16* EMB = reinterpret_cast<u16*>(SEP + A);  // [A][R] the table of y_{t-1}: bf16, or int8 codes
+  u16* EMBP = EMB + A * R;                     // [A][R] the table of y_{t-2} (two taps)
+  __shared__ int s_y[GC], s_y2[GC];            // y_{t-1}, y_{t-2} (-1 before the first input)
+  __shared__ float s_u[GC];
+  __shared__ int s_yin[GC];
+
+  // wave v: row tiles HT v .. HT v + HT - 1 of W_relu and of W_out
+  u32x4 w1[HT][KTH], w2[HT][KTO];
+#pragma unroll
+  for (int k = 0; k < HT; ++k) {
+    const size_t row = 16 * (HT * wave + k) + n;
+#pragma unroll
+    for (int kt = 0; kt < KTH; ++kt) w1[k][kt] = wfrag<I8>(g.w.w_relu, row, S, 32 * kt + 8 * quad);
+#pragma unroll
+    for (int kt = 0; kt < KTO; ++kt) w2[k][kt] = wfrag<I8>(g.w.w_out, row, A, 32 * kt + 8 * quad);
+  }
+  for (int i = tid; i < S; i += NT) BSK[i] = g.w.b_skip[i];
+  for (int i = tid; i < A; i += NT) {
+    BRL[i] = g.w.b_relu[i];
+    BO[i] = g.w.b_out[i];
+    if constexpr (I8) {
+      SRL[i] = g.w.s_relu[i];
+      SO[i] = g.w.s_out[i];
+      SE[i] = g.w.s_embed[i];
+      SEP[i] = e2 ? g.w.s_embed_prev[i] : 0.f;
+    }
+  }
+  for (int i = tid; i < R; i += NT) BE[i] = g.w.b_embed[i];
+  {
+    // the tables as 32-bit words (bf16 pairs, or int8 quadruples)
+    constexpr int TW = I8 ? A * R / 4 : A * R / 2;
+    const unsigned* e = static_cast<const unsigned*>(g.w.embed);
+    for (int i = tid; i < TW; i += NT) reinterpret_cast<unsigned*>(EMB)[i] = e[i];
+    if (e2) {
+      const unsigned* ep = static_cast<const unsigned*>(g.w.embed_prev);
+      for (int i = tid; i < TW; i += NT) reinterpret_cast<unsigned*>(EMBP)[i] = ep[i];
+    }
+  }
+  if (tid < GC) {
+    int y = 0, y2 = -1;
+    if (tid < ns) {
+      const int64_t* st = g.state + WN_STATE_WORDS * (size_t)(b0 + tid);
+      y = g.io.reset ? g.io.init_sample : (int)st[1];
+      y2 = g.io.reset ? -1 : (int)st[2];
+    }
+    s_y[tid] = y < 0 ? 0 : (y > A - 1 ? A - 1 : y);
+    s_y2[tid] = y2 < 0 ? -1 : (y2 > A - 1 ? A - 1 : y2);
+  }
+  __syncthreads();
+  // row k of a table's entry y
+  auto emb = [&](const u16* tab, const float* sc, int y, int k) __attribute__((always_inline)) -> float {
+    if constexpr (I8) return (float)reinterpret_cast<const signed char*>(tab)[y * R + k] * sc[y];
+    else return bf16_val(tab[y * R + k]);
+  };
+  // x0 of the call's first step (padding columns get zeros)
+  for (int i = tid; i < XW; i += NT) {
+    const int m = trow(i), cn = tcol(i);
+    float v = 0.f;
+    if (cn < ns) {
+      v = emb(EMB, SE, s_y[cn], m) + BE[m];
+      if (e2 && s_y2[cn] >= 0) v += emb(EMBP, SEP, s_y2[cn], m);
+    }
+    stw(mb + g.off_x + (size_t)(tg0 & 1) * XW + i, pack(v, (unsigned)(tg0 + 1)), lm & 1u);
+  }
+
+  // skip partials per step: the running sum of all aux CUs' but the last (posted by the one before
+  // the last), the last aux CU's own, and the last layer's from the last chain CU
+  const int nqa = g.naux_q >= 2 ? 2 : g.naux_q;  // aux partials polled
+  const int np = nqa + (g.tail_on_chain ? 1 : 0);
+  auto part_word = [&](int p, int par) -> unsigned {
+    if (p < nqa) return mbw + g.off_q + ((unsigned)(g.naux_q - nqa + p) * 2 + par) * QW;
+    return mbw + g.off_qtail + (unsigned)par * QW;
+  };
+  for (int64_t t = tg0; t < tg0 + T; ++t) {
+    const unsigned tag = (unsigned)(t + 1);
+    const int par = (int)(t & 1);
+    const bool more = t + 1 < tg0 + T;
+    // this step's uniform (or teacher-forced sample) of each stream, staged after the wait below
+    float uv = 0.f;
+    int yv = 0;
+    if (tid < ns) {
+      const size_t at = (size_t)(b0 + tid) * T + (size_t)(t - tg0);
+      if constexpr (TF) yv = g.io.y_in[at];
+      else uv = g.io.u[at];
+    }
+    // the skip partials of the step: the aux CUs' sum, then the last layer's from the last chain CU.
+    // Entry e of this thread is word tid + NT e of each partial, summed in partial order.
+    float qa[NQ];
+#pragma unroll
+    for (int e = 0; e < NQ; ++e) qa[e] = 0.f;
+    // pair p = tid + NT k holds words 2 tid + 2 NT k (+ 1) of partial (2 p) / QW: entry 2 (k mod (NQ / 2))
+    // (+ 1) of this thread, the same position in every partial
+    // (two partials per batch)
+    {
+      constexpr int KP = NQ;
+      poll_pairs<KP>(
+          g, rs, tid, np * QW / 2, [&](int p) { return part_word((2 * p) / QW, par) + (2 * p) % QW; },
+          [&](int) { return tag; }, [&](int, int q, float v) { qa[q % NQ] += v; }, sy);
+    }
+    if (tid < GC) {
+      if constexpr (TF) s_yin[tid] = yv < 0 ? 0 : (yv > A - 1 ? A - 1 : yv);
+      else s_u[tid] = uv;
+    }
+    // z_s = relu(B_skip + sum of the partials); entries 2e' and 2e' + 1 are rows m, m + 1 (m even) of
+    // one column, stored as one 32-bit word of hi parts and one of lo parts
+#pragma unroll
+    for (int e = 0; e < NQ; e += 2) {
+      const int wi = 2 * tid + NT * e, m = trow(wi), cn = tcol(wi);
+      const float z0 = fmaxf(qa[e] + BSK[m], 0.f), z1 = fmaxf(qa[e + 1] + BSK[m + 1], 0.f);
+      const unsigned hi = pack_bf16(z0, z1);
+      const unsigned lo = pack_bf16(z0 - low_bf16(hi), z1 - high_bf16(hi));
+      *reinterpret_cast<unsigned*>(ZS + cn * SS + m) = hi;
+      *reinterpret_cast<unsigned*>(ZS + cn * SS + S + m) = lo;
+    }
+    lds_barrier();
+    if (sy.failed()) return;
+    // z_a = relu(W_relu z_s + B_relu)
+    f32x4 za[HT];
+    head_products<S, KTH>(za, w1, ZS + n * SS, quad);
+#pragma unroll
+    for (int k = 0; k < HT; ++k) {
+      f32x4 acc = za[k];
+      const int mr = 16 * (HT * wave + k) + 4 * quad;
+      const float4 b = *reinterpret_cast<const float4*>(BRL + mr);
+      if constexpr (I8) {
+        const float4 s4 = *reinterpret_cast<const float4*>(SRL + mr);
+        acc = f32x4{s4.x * acc[0], s4.y * acc[1], s4.z * acc[2], s4.w * acc[3]};
+      }
+      store_split4<A>(ZA + n * SA, mr,
+                      make_float4(fmaxf(acc[0] + b.x, 0.f), fmaxf(acc[1] + b.y, 0.f), fmaxf(acc[2] + b.z, 0.f),
+                                  fmaxf(acc[3] + b.w, 0.f)));
+    }
+    lds_barrier();
+    // logits = W_out z_a + B_out
+    f32x4 lo[HT];
+    head_products<A, KTO>(lo, w2, ZA + n * SA, quad);
+#pragma unroll
+    for (int k = 0; k < HT; ++k) {
+      f32x4 acc = lo[k];
+      const int mr = 16 * (HT * wave + k) + 4 * quad;
+      const float4 b = *reinterpret_cast<const float4*>(BO + mr);
+      if constexpr (I8) {
+        const float4 s4 = *reinterpret_cast<const float4*>(SO + mr);
+        acc = f32x4{s4.x * acc[0], s4.y * acc[1], s4.z * acc[2], s4.w * acc[3]};
+      }
+      *reinterpret_cast<float4*>(LG + n * PA + mr) = make_float4(acc[0] + b.x, acc[1] + b.y, acc[2] + b.z, acc[3] + b.w);
+    }
+    lds_barrier();
+    // the draws of streams GC / 4 wave .. (all four at once, so that their steps interleave; a padding
+    // column's draw is made and dropped), then their x0 of the next step (row = lane)
+    int ys[GC / 4];
+#pragma unroll
+    for (int k = 0; k < GC / 4; ++k) {
+      const int nn = (GC / 4) * wave + k;
+      if constexpr (TF) {
+        ys[k] = s_yin[nn];
+      } else {
+        const float4 lv = *reinterpret_cast<const float4*>(LG + nn * PA + 4 * lane);
+        ys[k] = wave_draw<AX>(lv, s_u[nn], g.io.smode, g.io.inv_t, g.io.top_k, lane);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < GC / 4; ++k) {
+      const int nn = (GC / 4) * wave + k;
+      const int y = nn < ns ? ys[k] : 0;
+      if (nn < ns) {
+        const size_t at = (size_t)(b0 + nn) * T + (size_t)(t - tg0);
+        if constexpr (TF) reinterpret_cast<float4*>(g.io.logits + at * A)[lane] = *reinterpret_cast<const float4*>(LG + nn * PA + 4 * lane);
+        else if (lane == 0) g.io.y_out[at] = y;
+      }
+      const int yp = s_y[nn];
+      if (more) {
+        float v = 0.f;
+        if (nn < ns) {
+          v = emb(EMB, SE, y, lane) + BE[lane];
+          if (e2) v += emb(EMBP, SEP, yp, lane);
+        }
+        stw(mb + g.off_x + (size_t)((t + 1) & 1) * XW + tpos(lane, nn), pack(v, tag + 1), lm & 1u);
+      }
+      if (lane == 0 && nn < ns) {
+        s_y2[nn] = yp;
+        s_y[nn] = y;
+      }
+    }
+    lds_barrier();
+  }
+  // after a timeout or an abort the state stays as it was (the next call must start from zero)
+  if (!sy.failed() && tid < ns) {
+    int64_t* st = g.state + WN_STATE_WORDS * (size_t)(b0 + tid);
+    st[0] = tg0 + T;
+    st[1] = s_y[tid];
+    st[2] = s_y2[tid];
+  }
+}
+
+template <int S, bool TF, bool AX, bool I8>
+__global__ __launch_bounds__(NT, 1) void wn_mchain_kernel(const WnChainArgs ga) {
+  // The argument block is read in place, through the kernel-argument segment: used as the by-value
+  // parameter, the compiler copies all of it to scratch memory once the roles index it at run time.
+#if __HIP_DEVICE_COMPILE__
+  const WnChainArgs& g = *(const WnChainArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+#else
+  const WnChainArgs& g = ga;  // the host pass only checks the body
+#endif
+  (void)ga;
+  extern __shared__ __align__(16) float dyn[];
+  __shared__ int s_abort;
+  __shared__ unsigned char s_xcd[WN_MAX_CHAIN + 1 + WN_MAX_LAYERS];
+  __shared__ unsigned char s_cof[WN_MAX_LAYERS];
+  __shared__ int s_me;
+  const int rb = g.role_of_block[blockIdx.x];
+  if (rb == 0xffff) return;
+  const int per = g.nch + 1 + g.naux;  // roles of a replica: chain CUs, the head, aux CUs
+  const int k = rb / per, role = rb - k * per;
+  const int head = g.nch;
+  if (threadIdx.x == 0) s_abort = 0;
+  // Which of this block's posts go to a reader on its own XCD in this launch: bit l of a chain CU for
+  // the aux CU of its layer l (h and the history rows), bit 16 for the next chain CU, bit 17 for the
+  // head; bit l of an aux CU for the chain CU of its layer l, bit 16 for the head; bit 0 of the head
+  // for chain CU 0.  The map is read at the launch (grid_meet).
+  unsigned lm = 0;
+  if (g.local_posts) {
+    if (grid_meet(g.xmap, g.n_active, g.spin_limit, g.status, &s_me) < 0) return;  // WN_ETIMEOUT is in the status word
+    for (int b = threadIdx.x; b < WN_CHAIN_GRID; b += NT) {
+      const int r = g.role_of_block[b];
+      if (r != 0xffff && r / per == k) s_xcd[r - k * per] = (unsigned char)ldw(g.xmap + b);
+    }
+    // the chain CU of every layer (a loop over the layer split in the argument block here would make
+    // the compiler copy the whole block to scratch memory)
+    for (int c = threadIdx.x; c < g.nch; c += NT)
+      for (int j = g.layer_begin[c]; j < g.layer_begin[c + 1]; ++j) s_cof[j] = (unsigned char)c;
+    __syncthreads();
+    const int me = s_me;
+    auto same = [&](int r) { return s_xcd[r] == me; };
+    if (role < head) {
+      const int j0 = g.layer_begin[role], nl = g.layer_begin[role + 1] - j0;
+      for (int l = 0; l < nl; ++l) lm |= (unsigned)same(head + 1 + (j0 + l) / g.nla) << l;
+      if (role + 1 < g.nch) lm |= (unsigned)same(role + 1) << 16;
+      lm |= (unsigned)same(head) << 17;
+    } else if (role == head) {
+      lm = same(0);
+    } else {
+      const int ja = (role - head - 1) * g.nla;
+      for (int l = 0; l < g.nla && ja + l < g.d.L; ++l) lm |= (unsigned)same(s_cof[ja + l]) << l;
+      lm |= (unsigned)same(head) << 16;
+    }
+  }
+  // where this call starts: from zero, or where the previous call on this workspace stopped (the
+  // head rewrites the state only after the whole call, when every role has started)
+  const int64_t tg0 = g.io.reset ? 0 : g.state[WN_STATE_WORDS * (size_t)(k * g.G)];
+  __syncthreads();
+  Sync sy{&s_abort};
+  if (role < head) mc_chain<S, AX, I8>(g, role, k, dyn, sy, tg0, lm);
+  else if (role == head) mc_head<S, TF, AX, I8>(g, k, dyn, sy, tg0, lm);
+  else mc_aux<S, AX, I8>(g, role - head - 1, k, dyn, sy, tg0, lm);
+}
+
+// Layers of each chain CU: runs of at most NLC, as even as possible.
+int mchain_split(int L, int* layer_begin) {
+  const int nch = (L + NLC - 1) / NLC;
+  if (nch > WN_MAX_CHAIN) return nch;
+  const int base = L / nch, extra = L % nch;
+  layer_begin[0] = 0;
+  for (int c = 0; c < nch; ++c) layer_begin[c + 1] = layer_begin[c] + base + (c < extra ? 1 : 0);
+  return nch;
+}
+
+constexpr size_t kMaxLds = 160 * 1024;
+
+template <int S>
+size_t mchain_lds() { return std::max(chain_lds(S), std::max(aux_lds(S), head_lds(S))); }
+
+template <int S>
+hipError_t launch_mchain_s(const WnChainArgs& g, bool teacher, hipStream_t stream) {
+  const size_t dyn = mchain_lds<S>();
+  const bool ax = g.w.approx_nl != 0, i8 = g.w.i8 != 0;
+  const void* k;
+  if (teacher) {
+    if (i8) k = ax ? reinterpret_cast<const void*>(wn_mchain_kernel<S, true, true, true>)
+                   : reinterpret_cast<const void*>(wn_mchain_kernel<S, true, false, true>);
+    else k = ax ? reinterpret_cast<const void*>(wn_mchain_kernel<S, true, true, false>)
+                : reinterpret_cast<const void*>(wn_mchain_kernel<S, true, false, false>);
+  } else {
+    if (i8) k = ax ? reinterpret_cast<const void*>(wn_mchain_kernel<S, false, true, true>)
+                   : reinterpret_cast<const void*>(wn_mchain_kernel<S, false, false, true>);
+    else k = ax ? reinterpret_cast<const void*>(wn_mchain_kernel<S, false, true, false>)
+                : reinterpret_cast<const void*>(wn_mchain_kernel<S, false, false, false>);
+  }
+  hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
+  if (e != hipSuccess) return e;
+  void* args[] = {const_cast<WnChainArgs*>(&g)};
+  return hipLaunchCooperativeKernel(k, dim3(WN_CHAIN_GRID), dim3(NT), args, (unsigned)dyn, stream);
+}
+
+}  // namespace
+
+bool wn_mchain_supported(int R_, int S_, int L) {
+  if (R_ != R || S_ != 256 || L < 1 || L > WN_MAX_LAYERS) return false;
+  int lb[WN_MAX_LAYERS + 2];
+  const int nch = mchain_split(L, lb);
+  const int naux = (L + NLA - 1) / NLA;
+  return nch <= WN_MAX_CHAIN && nch + 1 + naux <= WN_CHAIN_GRID && mchain_lds<256>() <= kMaxLds;
+}
+
+int wn_mchain_streams_max() { return GC; }
+
+bool wn_mchain_plan(int L, int R_, int S_, int B, WnChainPlan* p) {
+  if (!p || B < 1 || !wn_mchain_supported(R_, S_, L)) return false;
+  WnChainPlan q{};
+  q.nch = mchain_split(L, q.layer_begin);
+  // layers per aux CU (an aux CU runs only the skip products in step with the chain, which keeps pace
+  // with it; fewer aux CUs mean fewer skip partials); WN_AUX_LAYERS=n forces n
+  q.nla = NLA;
+  if (const char* e = std::getenv("WN_AUX_LAYERS")) {
+    const int v = std::atoi(e);
+    if (v >= 1 && v <= NLA) q.nla = v;
+  }
+  q.naux = (L + q.nla - 1) / q.nla;
+  q.tail_on_chain = 1;
+  // aux CUs that post a skip partial: all but one holding only the last layer
+  q.naux_q = (L - 1) % q.nla == 0 ? q.naux - 1 : q.naux;
+  // as few replicas as carry B streams (up to 16 each), the streams spread evenly
+  const int per = q.nch + 1 + q.naux;
+  const int max_rep = WN_CHAIN_GRID / per;
+  const int nrep = (B + GC - 1) / GC;
+  if (nrep > max_rep) return false;
+  q.G = (B + nrep - 1) / nrep;
+  q.nrep = (B + q.G - 1) / q.G;
+  q.ub = 0;
+  // mailboxes of one replica, in words: pre [L][2][PW] at 0, h [L][2][XW], skip partials
+  // [naux][2][S GC], the tail's [2][S GC], x [nch][2][XW]
+  const long long qw = (long long)S_ * GC;
+  q.off_h = L * 2 * PW;
+  q.off_q = q.off_h + L * 2 * XW;
+  q.off_qtail = (int)(q.off_q + q.naux * 2 * qw);
+  q.off_x = (int)(q.off_qtail + 2 * qw);
+  q.off_logit = 0;
+  q.mb_words = ((long long)q.off_x + q.nch * 2 * XW + 31) / 32 * 32;
+  // Placement: slot i of XCD x is block 8 i + x.  Each replica's chain CUs and head go to its home
+  // XCD first, then its aux CUs, last layers first, overflowing to the XCD with the most room.
+  int used[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  constexpr int per_xcd = WN_CHAIN_GRID / 8;
+  for (int b = 0; b < WN_CHAIN_GRID; ++b) q.role_of_block[b] = 0xffff;
+  auto place = [&](int role, int home) {
+    int x = home;
+    if (used[x] >= per_xcd) {
+      for (int y = 0; y < 8; ++y)
+        if (used[y] < used[x]) x = y;
+    }
+    q.role_of_block[8 * used[x] + x] = (uint16_t)role;
+    ++used[x];
+  };
+  for (int k = 0; k < q.nrep; ++k)
+    for (int r = 0; r <= q.nch; ++r) place(k * per + r, k % 8);
+  for (int k = 0; k < q.nrep; ++k)
+    for (int a = q.naux - 1; a >= 0; --a) place(k * per + q.nch + 1 + a, k % 8);
+  *p = q;
+  return true;
+}
+
+hipError_t wn_mchain_launch(const WnChainArgs& g, bool teacher, hipStream_t stream) {
+  if (g.d.R == R && g.d.S == 256) return launch_mchain_s<256>(g, teacher, stream);
+  return hipErrorInvalidValue;
+}

@@ -234,12 +234,12 @@ __device__ __forceinline__ int wave_draw(float4 lv, float u, int mode, float inv
   return y > last ? last : y;
 }
 
-// LDS-only barrier: waits for this wave's LDS traffic, not for its global stores.
 // True when the host has requested an abort (wn_abort): the word lives in pinned host memory, so
 // the load is at system scope (it crosses PCIe and takes ~1-2 us).
 __device__ __forceinline__ bool abort_requested(const int* flag) {
   return flag && __hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != 0;
 }
+// LDS-only barrier: waits for this wave's LDS traffic, not for its global stores.
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 }  // namespace wnk

@@ -1,0 +1,166 @@
+"""GPU parity of the multi-CU MFMA kernel (bf16 and int8 weights, r = 64): up to 16 streams per
+replica carried together through chain CUs with resident weights.
+
+Each case runs through the C ABI and is compared with the CPU oracle in the matching weight mode
+(bf16, or int8 with its quantization rule): teacher-forced logits within 1e-3, sample indices
+bit-exact wherever the oracle's CDF margin exceeds 1e-4; with the fp32 oracle within 2e-2 for bf16
+models.  Cases cover one stream, a full replica of 16, several replicas with a partial one, the
+fewest layers, every dilation 1 (histories read in the step they are written), dilations longer
+than the call, 40 layers (four chain CUs), int8 weights with a zero row, two taps, and calls split
+at odd steps (one-shot and chunked runs agree bit for bit).  The batched MFMA kernel (one CU per
+group of streams) agrees with it to rounding on the same inputs.
+"""
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+MARGIN = 1e-4
+KERNEL = "multi_cu_mfma"
+
+
+def _log(msg):
+    print(msg, flush=True)
+
+
+CASES = [
+    # name, L, dilations, B, T, dtype, bias, taps
+    ("l20_b1", 20, tuple(synth.dilation_cycle(20)), 1, 300, "bf16", 0.1, 1),
+    ("l20_b16", 20, tuple(synth.dilation_cycle(20)), 16, 200, "bf16", 0.2, 1),
+    ("l20_b37", 20, tuple(synth.dilation_cycle(20)), 37, 120, "bf16", 0.0, 1),
+    ("l2_d1_b1", 2, (1, 1), 1, 300, "bf16", 0.3, 1),
+    ("l3_d1_b3", 3, (1, 1, 1), 3, 200, "bf16", 0.2, 1),
+    ("l5_b5", 5, (1, 3, 9, 2, 4), 5, 150, "bf16", 0.4, 1),
+    ("long_dilations_b2", 4, (700, 1, 300, 2), 2, 800, "bf16", 0.2, 1),
+    ("l40_b20", 40, tuple(synth.dilation_cycle(40)), 20, 60, "bf16", 0.0, 1),
+    ("l20_2tap_b3", 20, tuple(synth.dilation_cycle(20)), 3, 150, "bf16", 0.1, 2),
+    ("i8_l20_b3", 20, tuple(synth.dilation_cycle(20)), 3, 200, "i8", 0.2, 1),
+    ("i8_l9_b17", 9, (1, 1, 2, 1, 8, 1, 3, 1, 2), 17, 120, "i8", 0.3, 1),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_mfma_chain_parity(case, monkeypatch):
+    import paper_1702_07825_amd as wn
+    name, L, dil, B, T, dtype, bias, taps = case
+    seed = zlib.crc32(name.encode()) % 1000
+    _log("multi-CU MFMA case %s: L=%d B=%d T=%d %s taps=%d" % (name, L, B, T, dtype, taps))
+    monkeypatch.setenv("WN_KERNEL", KERNEL)
+    w = synth.make_weights(L, 64, 256, seed=seed, bias_scale=bias, embed_taps=taps)
+    if dtype == "i8":
+        w["w_res"][0, 3] = 0.0  # a row of zeros: scale 0
+    net = wn.WaveNet(w, dil, weight_dtype=dtype)
+    assert net.kernel_variant(B) == KERNEL
+    cond = synth.make_cond(L, 64, B, T, seed=seed, device="cuda")
+    u = torch.tensor(synth.make_uniforms(B, T, seed=seed), device="cuda")
+    y = net.generate(cond, u)
+    y2 = net.generate(cond, u)
+    lg = net.teacher_force(cond, y)
+    torch.cuda.synchronize()
+    assert net.status(net.new_workspace(B)) == 0
+    assert torch.equal(y, y2)
+    y_np, lg_np = y.cpu().numpy(), lg.cpu().numpy()
+    cond_np, u_np = cond.cpu().numpy(), u.cpu().numpy()
+    assert y_np.min() >= 0 and y_np.max() <= 255
+
+    mode = {"bf16_weights": True} if dtype == "bf16" else {"int8_weights": True}
+    model = oracle.Model(w, dil, **mode)
+    ys, lo, mg = oracle.run_streams(model, cond_np, u=u_np, y_in=y_np, threads=8)
+    err = float(np.abs(lg_np - lo).max())
+    ok = mg > MARGIN
+    mism = int(np.sum(ys[ok] != y_np[ok]))
+    _log("  max|dlogit| oracle (%s) %.3g; confident %d/%d, mismatches %d" % (dtype, err, int(ok.sum()), ok.size, mism))
+    assert err <= 1e-3
+    assert mism == 0
+    if dtype == "bf16":
+        _, lo32, _ = oracle.run_streams(oracle.Model(w, dil), cond_np, y_in=y_np, threads=8)
+        err32 = float(np.abs(lg_np - lo32).max())
+        _log("  max|dlogit| fp32 oracle %.3g" % err32)
+        assert err32 <= 2e-2
+
+    # calls split at odd steps continue exactly where the previous one stopped
+    ws = net.new_workspace(B)
+    parts, a = [], 0
+    for b_ in (1, 2, 37, 38, T):
+        parts.append(net.generate(cond[:, a:b_].contiguous(), u[:, a:b_].contiguous(), workspace=ws, reset=(a == 0)))
+        a = b_
+    ws2 = net.new_workspace(B)
+    lgp = [net.teacher_force(cond[:, :29].contiguous(), y[:, :29].contiguous(), workspace=ws2, reset=True),
+           net.teacher_force(cond[:, 29:].contiguous(), y[:, 29:].contiguous(), workspace=ws2, reset=False)]
+    torch.cuda.synchronize()
+    assert net.status(ws) == 0 and net.status(ws2) == 0
+    assert torch.equal(torch.cat(parts, 1), y)
+    assert torch.equal(torch.cat(lgp, 1), lg)
+    net.close()
+
+    if dtype == "bf16" and taps == 1:
+        # the batched MFMA kernel (every layer of a group on one CU) agrees on the same inputs
+        monkeypatch.setenv("WN_KERNEL", "mfma_group")
+        ref = wn.WaveNet(w, dil, weight_dtype=dtype)
+        assert ref.kernel_variant(B) == "mfma_group"
+        lg_ref = ref.teacher_force(cond, y)
+        torch.cuda.synchronize()
+        d_ref = float((lg_ref - lg).abs().max())
+        _log("  max|dlogit| vs the batched kernel %.3g" % d_ref)
+        assert d_ref <= 1e-3
+        ref.close()
+
+
+def test_mfma_chain_launch_layout(monkeypatch):
+    """Replicas of up to 16 streams: l = 20 takes 2 chain CUs, 1 head and 4 aux CUs per replica."""
+    import paper_1702_07825_amd as wn
+    monkeypatch.setenv("WN_KERNEL", KERNEL)
+    L = 20
+    w = synth.make_weights(L, 64, 256, seed=3)
+    net = wn.WaveNet(w, synth.dilation_cycle(L), weight_dtype="bf16")
+    for B, reps in ((1, 1), (16, 1), (17, 2), (256, 16)):
+        assert net.kernel_variant(B) == KERNEL
+        assert net.launch_info(B) == (7 * reps, reps)
+    net.close()
+
+
+def test_mfma_chain_timeout_then_reset(monkeypatch):
+    """A wait that gives up (forced from the host with a spin limit of 1) ends the call with
+    WN_ETIMEOUT and every block leaves; a run from zero on the same workspace is then correct."""
+    import paper_1702_07825_amd as wn
+    monkeypatch.setenv("WN_KERNEL", KERNEL)
+    L, B, T = 20, 3, 64
+    w = synth.make_weights(L, 64, 256, seed=5, bias_scale=0.1)
+    dil = synth.dilation_cycle(L)
+    cond = synth.make_cond(L, 64, B, T, seed=5, device="cuda")
+    u = torch.tensor(synth.make_uniforms(B, T, seed=5), device="cuda")
+    good = wn.WaveNet(w, dil, weight_dtype="bf16")
+    y_ref = good.generate(cond, u)
+    torch.cuda.synchronize()
+    monkeypatch.setenv("WN_SPIN_LIMIT", "1")
+    bad = wn.WaveNet(w, dil, weight_dtype="bf16")
+    ws = bad.new_workspace(B)
+    bad.generate(cond, u, workspace=ws, reset=True)
+    torch.cuda.synchronize()
+    assert bad.status(ws) == wn.WN_ETIMEOUT
+    monkeypatch.delenv("WN_SPIN_LIMIT")
+    y = good.generate(cond, u, workspace=ws, reset=True)
+    torch.cuda.synchronize()
+    assert good.status(ws) == 0
+    assert torch.equal(y, y_ref)
+    bad.close()
+    good.close()
+
+
+def test_int8_batches_beyond_the_fp32_chain_use_it(monkeypatch):
+    """int8 models: the fp32 multi-CU kernel (on the fp32 copy) while its replicas carry the batch,
+    this kernel beyond that (instead of the per-stream kernel)."""
+    import paper_1702_07825_amd as wn
+    monkeypatch.delenv("WN_KERNEL", raising=False)
+    L = 20
+    w = synth.make_weights(L, 64, 256, seed=4)
+    net = wn.WaveNet(w, synth.dilation_cycle(L), weight_dtype="i8")
+    assert [net.kernel_variant(b) for b in (1, 240)] == ["multi_cu_chain"] * 2
+    assert [net.kernel_variant(b) for b in (241, 256)] == [KERNEL] * 2
+    net.close()
