@@ -151,8 +151,8 @@ WsLayout ws_layout(const wn_handle* h, int B) {
   WnChainPlan p;
   const int v = variant_for(h, B);
   if (v == WN_VARIANT_MCHAIN && mchain_plan_for(h, B, &p)) {
-    // tagged histories of 16-column tiles per replica, then the replicas' mailboxes and the map
-    l.mb_off = align_up(l.hist_off + (size_t)p.nrep * h->dims.hist_len * 16 * 8, 256);
+    // tagged histories of each replica's column blocks, then the replicas' mailboxes and the map
+    l.mb_off = align_up(l.hist_off + (size_t)p.nrep * h->dims.hist_len * wn_mchain_columns(p) * 8, 256);
     l.mb_words = (size_t)p.nrep * p.mb_words;
     l.map_off = l.mb_off + l.mb_words * 8;
     l.total = align_up(l.map_off + (size_t)WN_CHAIN_MAP_WORDS * 8, 256);
@@ -258,6 +258,7 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
     g.nla = plan.nla;
     g.naux = plan.naux;
     g.naux_q = plan.naux_q;
+    g.pair = plan.pair;
     // posts to same-XCD readers stop at the XCD's L2 when the block -> XCD map is the expected
     // one; WN_LOCAL_POSTS=0 writes every post through
     const char* lp = std::getenv("WN_LOCAL_POSTS");

@@ -118,12 +118,13 @@ struct WnChainArgs {
   int tail_on_chain;             // 1: the last chain CU computes the last layer's skip projection
   int nla, naux, naux_q;         // layers per aux CU, aux CUs per replica, aux CUs posting a skip partial
   int local_posts;               // 1: posts to a reader on the same XCD stop at its L2
+  int pair;                      // MFMA kernel: 1 = paired columns (8 streams per replica), 0 = 16 streams
   uint16_t role_of_block[WN_CHAIN_GRID];  // replica * per_replica + role; 0xffff = idle block
 };
 
 // How the multi-CU kernel lays out a model and a batch over the chip.
 struct WnChainPlan {
-  int nch, nrep, G, ub, tail_on_chain;
+  int nch, nrep, G, ub, tail_on_chain, pair;
   int nla, naux, naux_q;
   int layer_begin[WN_MAX_CHAIN + 1];
   uint16_t role_of_block[WN_CHAIN_GRID];
@@ -148,12 +149,14 @@ hipError_t wn_status_clear(int* status, hipStream_t stream);
 bool wn_chain_xcd_map_ok();
 hipError_t wn_chain_launch(const WnChainArgs& g, bool teacher, hipStream_t stream);
 
-// Multi-CU kernel for bf16 and int8 models (r = 64): the chain kernel's roles on MFMA, up to 16
-// streams per replica carried together as the columns of 16 x 16 tiles.  Same argument block and
-// workspace words as the chain kernel (mailbox offsets from wn_mchain_plan; the histories hold
-// 16-column tiles per replica, hist_len * 16 words each).
+// Multi-CU kernel for bf16 and int8 models (r = 64): the chain kernel's roles on MFMA, 8 streams
+// per replica in paired columns (hi and lo parts of a stream in two columns of a 16 x 16 tile) or 16
+// streams, one per column.  Same argument block and workspace words as the chain kernel (mailbox
+// offsets from wn_mchain_plan; the histories hold hist_len * wn_mchain_columns(plan) words per
+// replica).
 bool wn_mchain_supported(int R, int S, int L);
 bool wn_mchain_plan(int L, int R, int S, int B, WnChainPlan* p);
+int wn_mchain_columns(const WnChainPlan& p);
 hipError_t wn_mchain_launch(const WnChainArgs& g, bool teacher, hipStream_t stream);
 
 // Batched kernel for bf16 weights: one workgroup per group of 8 or 16 streams, MFMA for every

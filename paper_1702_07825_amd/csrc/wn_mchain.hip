@@ -1,13 +1,24 @@
-// Multi-CU persistent generation kernel for bf16 and int8 models (r = 64) on gfx950 MFMA: up to 16
-// streams per replica go through the layer chain together.
+// Multi-CU persistent generation kernel for bf16 and int8 models (r = 64) on gfx950 MFMA: the
+// streams of a replica go through the layer chain together.
 //
 // The roles and the messages are those of the fp32 multi-CU kernel: the weights stay resident for
 // the whole call, as in the paper's persistent GPU kernel (Deep Voice, arXiv 1702.07825, Appendix
 // D), and the work that does not depend on the current step's chain is done off the chain, a step
 // ahead, as its CPU design does with auxiliary threads (Section 5.1); the arithmetic is Appendix
-// A.1's.  What differs is the batch: a replica carries up to 16 streams at once, one per column of a
-// 16 x 16 MFMA tile, so every product of a layer is a [rows x 64] . [64 x 16] contraction on
-// v_mfma_f32_16x16x32_bf16, and every message is a block of 16-column tiles.
+// A.1's.  What differs is the batch: every product of a layer is a [rows x 64] . [64 x 16]
+// contraction on v_mfma_f32_16x16x32_bf16, and every message is a block of tiles.
+//
+// An activation enters a product as a pair of bf16 values, hi = bf16(v) and lo = bf16(v - hi),
+// and both are multiplied, so a product sees about 16 bits of the activation; the weights are
+// exactly bf16 (int8 codes are exact in bf16, and each row's scale multiplies its fp32 result).
+// Accumulation, the gate, the residual and skip sums and the softmax are fp32.  The 16 columns of a
+// tile take the streams in one of two ways:
+//   paired   8 streams per replica: column n < 8 holds the hi part of stream n and column n + 8 its
+//            lo part, so one MFMA per 32 inputs does the work of two, and fold8 (row_ror:8) adds the
+//            halves, leaving lanes n and n + 8 with the same sums.  The two lanes then share the
+//            gate (one takes the tanh, the other the sigmoid) and the posts.  One head CU.
+//   16-wide  16 streams per replica, one per column, two MFMAs per 32 inputs (hi, lo); two head
+//            CUs of 8 streams each.  Used when the paired replicas cannot carry the batch.
 //
 //   chain CU  (up to NLC layers) wave w keeps row tile w of the tanh half and of the sigmoid half
 //             of W_cur and row tile w of W_res in registers, as MFMA A operands.  Per layer:
@@ -22,26 +33,22 @@
 //             For the next step it computes pre = W_prev x_{j-1}[t + 1 - d] + B + L[t + 1] of each
 //             layer (the dilated half, the bias and the HBM read of the conditioning all happen a
 //             step early), and for the current step the sum of W_skip h over its layers.
-//   head CU   wave v keeps four row tiles of W_relu and of W_out.  It sums the skip partials,
-//             z_s = relu(.. + B_skip), z_a = relu(W_relu z_s + B_relu), logits = W_out z_a + B_out,
-//             draws four streams per wave and posts the next step's x0 = E[y] + B_embed
-//             (+ E_prev[y_{t-1}], the two-tap input of Section 5.1) to chain CU 0.
+//   head CU   8 streams; wave v keeps four row tiles of W_relu and of W_out.  It sums the skip
+//             partials, z_s = relu(.. + B_skip), z_a = relu(W_relu z_s + B_relu), logits = W_out
+//             z_a + B_out (paired columns), draws two streams per wave and posts the next step's
+//             x0 = E[y] + B_embed (+ E_prev[y_{t-1}], the two-tap input of Section 5.1) to chain
+//             CU 0.
 //
 // A CU runs four waves, one per SIMD, so that each wave can hold 512 registers (the resident weights
 // take up to 240 of them); the layer's critical path is the gate waves' either way.
 //
-// An activation enters a product as a pair of bf16 values, hi = bf16(v) and lo = bf16(v - hi),
-// and both are multiplied, so a product sees about 16 bits of the activation; the weights are
-// exactly bf16 (int8 codes are exact in bf16, and each row's scale multiplies its fp32 result).
-// Accumulation, the gate, the residual and skip sums and the softmax are fp32.
-//
 // Messages are tagged 64-bit words (fp32 value, step + 1; see wn_msg.h) laid out in the MFMA
-// accumulator order: word (tile 64 + lane) 4 + e holds row 16 tile + 4 (lane / 16) + e of column
-// lane mod 16, so the lanes that computed a tile post it as it lies in their registers.  Mailboxes
-// have two slots (step parity); every producer stays at most one step ahead of its consumer.  The
-// dilation histories are rings of such tiles: slot t mod d_j of layer j holds x_{j-1}[t].  Every
-// wait is bounded: a block that times out stores WN_ETIMEOUT in the status word, and every other
-// block sees it in its next wait and leaves, so the grid always drains.
+// accumulator order: in a block of NS-column tiles (NS streams), word 16 NS tile + 4 (NS quad + c) +
+// e holds row 16 tile + 4 quad + e of column c, so the lanes that computed a tile post it as it lies
+// in their registers.  Mailboxes have two slots (step parity); every producer stays at most one step
+// ahead of its consumer.  The dilation histories are rings of such blocks: slot t mod d_j of layer
+// j holds x_{j-1}[t].  Every wait is bounded: a block that times out stores WN_ETIMEOUT in the
+// status word, and every other block sees it in its next wait and leaves, so the grid always drains.
 #include "wn_internal.h"
 #include "wn_mfma.h"
 #include "wn_msg.h"
@@ -57,21 +64,32 @@ namespace {
 
 using namespace wnk;
 
-constexpr int NT = 256;          // four waves: one per SIMD, so each can hold 512 registers
+constexpr int NT = 256;        // four waves: one per SIMD, so each can hold 512 registers
 constexpr int R = 64;
 constexpr int A = WN_A;
-constexpr int GC = 16;         // MFMA columns: the streams of a replica (the others are padding)
 constexpr int NLC = 10;        // layers per chain CU
 constexpr int NLA = 5;         // layers per aux CU
 constexpr int SR = 2 * R + 8;  // split-row pitch (16-bit units) of an r-vector in LDS
-constexpr int XW = R * GC;     // words of an r-vector block (x, h)
-constexpr int PW = 2 * R * GC; // words of a pre-activation block
+constexpr int HG = 8;          // streams per head CU
 
-// Place of (row m, column n) in a block of 16-column tiles: tile m / 16, lane n + 16 ((m mod 16) / 4),
-// element m mod 4 (the MFMA accumulator order); trow / tcol invert it.
-__device__ __forceinline__ int tpos(int m, int n) { return ((((m >> 4) << 6) + n + ((m & 12) << 2)) << 2) + (m & 3); }
-__device__ __forceinline__ int trow(int i) { return ((i >> 8) << 4) + (((i >> 6) & 3) << 2) + (i & 3); }
-__device__ __forceinline__ int tcol(int i) { return (i >> 2) & 15; }
+// Column layout of a replica's tiles.
+template <bool PAIR>
+struct Cols {
+  static constexpr int NS = PAIR ? 8 : 16;  // streams of a replica
+  static constexpr int NH = PAIR ? 1 : 2;   // head CUs of a replica
+  static constexpr int XW = R * NS;         // words of an r-vector block (x, h)
+  static constexpr int PW = 2 * R * NS;     // words of a pre-activation block
+  static constexpr int TW = 16 * NS;        // words of one 16-row tile of a block
+};
+// Place of (row m, column c) in a block of NS-column tiles; trow / tcol invert it.
+template <int NS>
+__device__ __forceinline__ int tpos(int m, int c) {
+  return (m >> 4) * 16 * NS + (((m >> 2) & 3) * NS + c) * 4 + (m & 3);
+}
+template <int NS>
+__device__ __forceinline__ int trow(int i) { return (i / (16 * NS)) * 16 + ((i / (4 * NS)) & 3) * 4 + (i & 3); }
+template <int NS>
+__device__ __forceinline__ int tcol(int i) { return (i >> 2) & (NS - 1); }
 
 // MFMA A operand from a row-major [rows][K] matrix: row `row`, inputs col .. col + 7 as bf16 (int8
 // codes are exact in bf16).
@@ -85,6 +103,9 @@ __device__ __forceinline__ u32x4 wfrag(const void* W, size_t row, int K, int col
     r[1] = pack_bf16(cv(q.x, 2), cv(q.x, 3));
     r[2] = pack_bf16(cv(q.y, 0), cv(q.y, 1));
     r[3] = pack_bf16(cv(q.y, 2), cv(q.y, 3));
+    // the fragment moves to AGPRs once, here: a value a VALU instruction produced otherwise stays in
+    // VGPRs and is copied to AGPRs before every product that reads it
+    asm volatile("" : "+a"(r));
     return r;
   } else {
     return *reinterpret_cast<const u32x4*>(static_cast<const u16*>(W) + row * K + col);
@@ -125,23 +146,67 @@ __device__ __forceinline__ f32x4 mfma_k64(f32x4 a, const u32x4& w0, const u32x4&
                : "a"(w0), "a"(w1), "v"(h0), "v"(l0), "v"(h1), "v"(l1));
   return a;
 }
-// a += Wa [hi; lo], b += Wb [hi; lo] over 128 inputs (four 32-input chunks k: wa[k], h[k], l[k])
-__device__ __forceinline__ void mfma_k128_2(f32x4& a, f32x4& b, const u32x4 (&wa)[4], const u32x4 (&wb)[4],
-                                            const u32x4 (&h)[4], const u32x4 (&l)[4]) {
+// The same products with paired columns: one B operand per 32 inputs (this lane's part of its stream).
+__device__ __forceinline__ void mfma_k64_2p(f32x4& a, f32x4& b, const u32x4& wa0, const u32x4& wa1, const u32x4& wb0,
+                                            const u32x4& wb1, u32x4 x0, u32x4 x1) {
+  asm volatile("s_nop 1\n\t"
+               WN_MFMA "%0, %2, %6, %0\n\t" WN_MFMA "%1, %4, %6, %1\n\t"
+               WN_MFMA "%0, %3, %7, %0\n\t" WN_MFMA "%1, %5, %7, %1\n\t"
+               "s_nop 7\n\ts_nop 7"
+               : "+v"(a), "+v"(b)
+               : "a"(wa0), "a"(wa1), "a"(wb0), "a"(wb1), "v"(x0), "v"(x1));
+}
+__device__ __forceinline__ f32x4 mfma_k64p(f32x4 a, const u32x4& w0, const u32x4& w1, u32x4 x0, u32x4 x1) {
+  asm volatile("s_nop 1\n\t"
+               WN_MFMA "%0, %1, %3, %0\n\t" WN_MFMA "%0, %2, %4, %0\n\t"
+               "s_nop 7\n\ts_nop 7"
+               : "+v"(a)
+               : "a"(w0), "a"(w1), "v"(x0), "v"(x1));
+  return a;
+}
+// a += Wa x, b += Wb x over 128 inputs in paired columns (four 32-input chunks k: wa[k], x[k])
+__device__ __forceinline__ void mfma_k128_2p(f32x4& a, f32x4& b, const u32x4 (&wa)[4], const u32x4 (&wb)[4],
+                                             const u32x4 (&x)[4]) {
   asm volatile("s_nop 1\n\t"
                WN_MFMA "%0, %2, %10, %0\n\t" WN_MFMA "%1, %6, %10, %1\n\t"
-               WN_MFMA "%0, %2, %14, %0\n\t" WN_MFMA "%1, %6, %14, %1\n\t"
                WN_MFMA "%0, %3, %11, %0\n\t" WN_MFMA "%1, %7, %11, %1\n\t"
-               WN_MFMA "%0, %3, %15, %0\n\t" WN_MFMA "%1, %7, %15, %1\n\t"
                WN_MFMA "%0, %4, %12, %0\n\t" WN_MFMA "%1, %8, %12, %1\n\t"
-               WN_MFMA "%0, %4, %16, %0\n\t" WN_MFMA "%1, %8, %16, %1\n\t"
                WN_MFMA "%0, %5, %13, %0\n\t" WN_MFMA "%1, %9, %13, %1\n\t"
-               WN_MFMA "%0, %5, %17, %0\n\t" WN_MFMA "%1, %9, %17, %1\n\t"
                "s_nop 7\n\ts_nop 7"
                : "+v"(a), "+v"(b)
                : "a"(wa[0]), "a"(wa[1]), "a"(wa[2]), "a"(wa[3]), "a"(wb[0]), "a"(wb[1]), "a"(wb[2]), "a"(wb[3]),
-                 "v"(h[0]), "v"(h[1]), "v"(h[2]), "v"(h[3]), "v"(l[0]), "v"(l[1]), "v"(l[2]), "v"(l[3]));
+                 "v"(x[0]), "v"(x[1]), "v"(x[2]), "v"(x[3]));
 }
+// Products over 64 inputs taken from a split row (the lane's stream): a += Wa x, b += Wb x.  With
+// paired columns the lane reads its part (hi or lo) only and the caller folds.
+template <bool PAIR>
+__device__ __forceinline__ void prod2(f32x4& a, f32x4& b, const u32x4& wa0, const u32x4& wa1, const u32x4& wb0,
+                                      const u32x4& wb1, const u16* row, int quad, int part) {
+  if constexpr (PAIR) {
+    const u16* r = row + part * R + 8 * quad;
+    mfma_k64_2p(a, b, wa0, wa1, wb0, wb1, ld16(r), ld16(r + 32));
+  } else {
+    mfma_k64_2(a, b, wa0, wa1, wb0, wb1, ld16(row + 8 * quad), ld16(row + R + 8 * quad), ld16(row + 32 + 8 * quad),
+               ld16(row + R + 32 + 8 * quad));
+  }
+}
+template <bool PAIR>
+__device__ __forceinline__ f32x4 prod1(f32x4 a, const u32x4& w0, const u32x4& w1, const u16* row, int quad, int part) {
+  if constexpr (PAIR) {
+    const u16* r = row + part * R + 8 * quad;
+    return mfma_k64p(a, w0, w1, ld16(r), ld16(r + 32));
+  } else {
+    return mfma_k64(a, w0, w1, ld16(row + 8 * quad), ld16(row + R + 8 * quad), ld16(row + 32 + 8 * quad),
+                    ld16(row + R + 32 + 8 * quad));
+  }
+}
+// Paired columns: lanes n and n + 8 of each 16-lane row add their sums (row_ror:8).
+__device__ __forceinline__ f32x4 fold8(f32x4 a) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) a[e] += dpp<0x128>(a[e]);
+  return a;
+}
+
 // Four tagged words (one lane's element run of a tile) with one scope decision.
 __device__ __forceinline__ void stw4(u64* p, float4 v, unsigned tag, bool local) {
   const u64 a = pack(v.x, tag), b = pack(v.y, tag), c = pack(v.z, tag), d = pack(v.w, tag);
@@ -155,6 +220,29 @@ __device__ __forceinline__ void stw4(u64* p, float4 v, unsigned tag, bool local)
     __hip_atomic_store(p + 1, b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(p + 2, c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __hip_atomic_store(p + 3, d, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Two tagged words.
+__device__ __forceinline__ void stw2(u64* p, float a, float b, unsigned tag, bool local) {
+  const u64 x = pack(a, tag), y = pack(b, tag);
+  if (local) {
+    __hip_atomic_store(p + 0, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    __hip_atomic_store(p + 1, y, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  } else {
+    __hip_atomic_store(p + 0, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(p + 1, y, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+// A lane's four rows of a tile, posted at p (its run of four words): with paired columns the two
+// lanes of a stream post two words each (part 0 elements 0 and 1, part 1 elements 2 and 3).
+template <bool PAIR>
+__device__ __forceinline__ void post4(u64* p, float4 v, unsigned tag, bool local, int part) {
+  if constexpr (PAIR) {
+    if (part) stw2(p + 2, v.z, v.w, tag, local);
+    else stw2(p, v.x, v.y, tag, local);
+  } else {
+    stw4(p, v, tag, local);
   }
 }
 
@@ -249,40 +337,90 @@ __device__ __forceinline__ float gate_h(float a, float g) {
   else return gate_tanh_sigmoid(a, g);
 }
 
-// A polled word of an r-vector block into a split row set [GC][SR] (hi and lo parts).
+// tanh(ah) sigmoid(ag) with paired columns: after fold8 lanes n and n + 8 hold the same ah and ag;
+// lane n (part 0) evaluates the tanh and lane n + 8 the sigmoid, and they swap results (row_ror:8),
+// so a wave issues half the transcendental instructions.  AX: Appendix C's forms with the same
+// operations as tanh_paper and sigmoid_paper.
+template <bool AX>
+__device__ __forceinline__ float gate_pair8(float ah, float ag, int part) {
+  const bool th = part == 0;
+  float v;
+  if constexpr (AX) {
+    const float x = th ? ah : ag;
+    const float e = e_tilde(x);
+    const float r = __builtin_amdgcn_rcpf(th ? e : 1.0f + e);
+    v = th ? copysignf((e - r) * __builtin_amdgcn_rcpf(e + r), x) : (x >= 0.0f ? e * r : r);
+  } else {
+    const float r = __builtin_amdgcn_rcpf(1.0f + expf_fast(th ? 2.0f * ah : -ag));
+    v = th ? 1.0f - 2.0f * r : r;
+  }
+  const float o = dpp<0x128>(v);
+  return th ? v * o : o * v;
+}
+template <bool AX, bool PAIR>
+__device__ __forceinline__ float4 gate4(f32x4 at, f32x4 ag, int part) {
+  if constexpr (PAIR)
+    return make_float4(gate_pair8<AX>(at[0], ag[0], part), gate_pair8<AX>(at[1], ag[1], part),
+                       gate_pair8<AX>(at[2], ag[2], part), gate_pair8<AX>(at[3], ag[3], part));
+  else
+    return make_float4(gate_h<AX>(at[0], ag[0]), gate_h<AX>(at[1], ag[1]), gate_h<AX>(at[2], ag[2]),
+                       gate_h<AX>(at[3], ag[3]));
+}
+// Rows m0 .. m0 + 3 of an r-vector into a split row: with paired columns lane part 0 writes the hi
+// parts and part 1 the lo parts.
+template <bool PAIR>
+__device__ __forceinline__ void put_split4(u16* row, int m0, float4 v, int part) {
+  if constexpr (PAIR) {
+    uint2 hi, lo;
+    split4(v, hi, lo);
+    *reinterpret_cast<uint2*>(row + part * R + m0) = part ? lo : hi;
+  } else {
+    store_split4<R>(row, m0, v);
+  }
+}
+
+// A polled word of an r-vector block into a split row set [NS][SR] (hi and lo parts).
+template <int NS>
 __device__ __forceinline__ void split_into(u16* rows, int i, float v) {
-  const int m = trow(i), c = tcol(i);
+  const int m = trow<NS>(i), c = tcol<NS>(i);
   split1(v, rows[c * SR + m], rows[c * SR + R + m]);
 }
 
 // Dynamic LDS of each role, in bytes (the launch takes the largest); mirrors the carving below.
+template <bool PAIR>
 constexpr size_t chain_lds(int S) {
-  return 4 * ((size_t)NLC * PW + (size_t)XW + (size_t)NLC * R + (size_t)NLC * 3 * R + S) + 2 * (size_t)3 * GC * SR +
-         (size_t)(S / 16) * 2 * 64 * 16;
+  using C = Cols<PAIR>;
+  return 4 * ((size_t)NLC * C::PW + (size_t)C::XW + (size_t)NLC * R + (size_t)NLC * 3 * R + S) +
+         2 * (size_t)3 * C::NS * SR + (size_t)(S / 16) * 2 * 64 * 16;
 }
+template <bool PAIR>
 constexpr size_t aux_lds(int S) {
-  return 4 * ((size_t)NLA * PW + (size_t)NLA * 4 * R + (size_t)NLA * S) + 2 * (size_t)2 * NLA * GC * SR;
+  using C = Cols<PAIR>;
+  return 4 * ((size_t)NLA * C::PW + (size_t)NLA * 4 * R + (size_t)NLA * S) + 2 * (size_t)2 * NLA * C::NS * SR;
 }
 constexpr size_t head_lds(int S) {
-  return 2 * ((size_t)GC * (2 * S + 8) + (size_t)GC * (2 * A + 8)) + 4 * ((size_t)GC * (A + 4) + S + 6 * A + R) +
+  return 2 * ((size_t)HG * (2 * S + 8) + (size_t)HG * (2 * A + 8)) + 4 * ((size_t)HG * (A + 4) + S + 6 * A + R) +
          2 * (size_t)2 * A * R;
 }
 
 // ------------------------------------------------------------------------------------------
 // chain CU: layers j0 .. j0 + nl - 1
 // ------------------------------------------------------------------------------------------
-template <int S, bool AX, bool I8>
-__device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, const int rep, float* dyn, Sync sy, const int64_t tg0,
-                         const unsigned lm) {
+template <int S, bool AX, bool I8, bool PAIR>
+__device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, const int rep, float* dyn, Sync sy,
+                                         const int64_t tg0, const unsigned lm) {
+  using C = Cols<PAIR>;
+  constexpr int NS = C::NS, XW = C::XW, PW = C::PW, TW = C::TW;
   constexpr int KS = S / 64;  // row tiles per wave of the last layer's W_skip (tail)
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 15, quad = lane >> 4;
+  const int sn = PAIR ? (n & 7) : n, part = PAIR ? (n >> 3) : 0;  // this lane's stream and part
   const int L = g.d.L, T = g.io.T;
   const int j0 = g.layer_begin[c], nl = g.layer_begin[c + 1] - j0;
   const bool tail = c + 1 == g.nch && g.tail_on_chain;
   u64* const mb = g.mb + (size_t)rep * g.mb_words;
-  u64* const ring = g.ring + (size_t)rep * g.d.hist_len * GC;
+  u64* const ring = g.ring + (size_t)rep * g.d.hist_len * NS;
   const wrsrc rs = tagged_region(g);
   const unsigned mbw = (unsigned)(mb - g.ring);  // word offset of my replica's mailboxes in the region
   float* PRE = dyn;                  // [NLC][PW] this step's pre-activations of my layers
@@ -290,9 +428,9 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
   float* BRS = XF + XW;              // [NLC][R]  B_res
   float* SCL = BRS + NLC * R;        // [NLC][3R] int8: row scales of W_cur (2R rows) and W_res (R)
   float* SSK = SCL + NLC * 3 * R;    // [S]       int8: row scales of the last layer's W_skip
-  u16* XS = reinterpret_cast<u16*>(SSK + S);             // [2][GC][SR] x, split, by layer parity
-  u16* HS = XS + 2 * GC * SR;                            // [GC][SR]    h, split
-  u32x4* WSK = reinterpret_cast<u32x4*>(HS + GC * SR);   // [S/16][2][64] the last layer's W_skip tiles
+  u16* XS = reinterpret_cast<u16*>(SSK + S);             // [2][NS][SR] x, split, by layer parity
+  u16* HS = XS + 2 * NS * SR;                            // [NS][SR]    h, split
+  u32x4* WSK = reinterpret_cast<u32x4*>(HS + NS * SR);   // [S/16][2][64] the last layer's W_skip tiles
 
   // wave w: row tile w of the tanh half and of the sigmoid half of W_cur, row tile w of W_res
   const int m0 = 16 * wave + 4 * quad;  // this lane's rows of x, h and the tanh half of a
@@ -334,7 +472,9 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
   }
   __syncthreads();
 
-  float4 xr = make_float4(0.f, 0.f, 0.f, 0.f);  // x_{j-1}[t], rows m0 .. m0 + 3 of column n, fp32
+  const int ot = wave * TW + (quad * NS + sn) * 4;  // this lane's words of tile `wave` of a block
+  const bool p0 = part == 0;                        // the lane that adds the fp32 terms before a fold
+  float4 xr = make_float4(0.f, 0.f, 0.f, 0.f);      // x_{j-1}[t], rows m0 .. m0 + 3 of stream sn, fp32
   for (int64_t t = tg0; t < tg0 + T; ++t) {
     const unsigned tag = (unsigned)(t + 1);
     const int par = (int)(t & 1);
@@ -345,62 +485,59 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
         g, rs, tid, nl * PW / 2, [&](int p) { return pre_w + (unsigned)((2 * p) / PW) * 2 * PW + (2 * p) % PW; },
         [&](int) { return tag; }, [&](int i, int, float v) { PRE[i] = v; }, sy);
     const unsigned x_w = mbw + g.off_x + ((unsigned)c * 2 + par) * XW;
-    poll_pairs<2>(
+    poll_pairs<XW / 2 / NT>(
         g, rs, tid, XW / 2, [&](int p) { return x_w + 2 * p; }, [&](int) { return tag; },
         [&](int i, int, float v) {
           XF[i] = v;
-          split_into(XS, i, v);
+          split_into<NS>(XS, i, v);
         },
         sy);
     lds_barrier();
     if (sy.failed()) return;
-    xr = *reinterpret_cast<const float4*>(XF + (wave * 64 + lane) * 4);
+    xr = *reinterpret_cast<const float4*>(XF + ot);
 #pragma unroll
     for (int l = 0; l < NLC; ++l) {
       if (l < nl) {
         const int j = j0 + l;
-        const int ot = (wave * 64 + lane) * 4;  // this lane's words of a tile block
         {
           // a = pre + W_cur x_{j-1}; h = tanh(a[rows]) sigmoid(a[R + rows])
-          const u16* xs = XS + (l & 1) * GC * SR + n * SR;
           const float4 pt = *reinterpret_cast<const float4*>(PRE + l * PW + ot);
-          const float4 pg = *reinterpret_cast<const float4*>(PRE + l * PW + 4 * 64 * 4 + ot);
+          const float4 pg = *reinterpret_cast<const float4*>(PRE + l * PW + 4 * TW + ot);
           f32x4 at = {0.f, 0.f, 0.f, 0.f}, ag = {0.f, 0.f, 0.f, 0.f};
-          if constexpr (!I8) {
+          if (!I8 && p0) {
             at = f4(pt);
             ag = f4(pg);
           }
-          mfma_k64_2(at, ag, wt[l][0], wt[l][1], wg[l][0], wg[l][1], ld16(xs + 8 * quad), ld16(xs + R + 8 * quad),
-                     ld16(xs + 32 + 8 * quad), ld16(xs + R + 32 + 8 * quad));
-          // x_{j-1}[t] into slot t mod d_j of layer j's history, which its aux CU reads at t + d_j
-          stw4(ring + ((size_t)hoff[l] + (size_t)slot[l] * R) * GC + ot, xr, tag, (lm >> l) & 1u);
+          prod2<PAIR>(at, ag, wt[l][0], wt[l][1], wg[l][0], wg[l][1], XS + (l & 1) * NS * SR + sn * SR, quad, part);
+          if constexpr (PAIR) {
+            at = fold8(at);
+            ag = fold8(ag);
+          }
+          // x_{j-1}[t] goes into slot t mod d_j of layer j's history, which its aux CU reads at t + d_j
+          u64* const hist = ring + ((size_t)hoff[l] + (size_t)slot[l] * R) * NS + ot;
           slot[l] = slot[l] + 1 == dil[l] ? 0 : slot[l] + 1;
+          if constexpr (!PAIR) stw4(hist, xr, tag, (lm >> l) & 1u);
           if constexpr (I8) {
             const float4 st = *reinterpret_cast<const float4*>(SCL + l * 3 * R + m0);
             const float4 sg = *reinterpret_cast<const float4*>(SCL + l * 3 * R + R + m0);
             at = f32x4{pt.x + st.x * at[0], pt.y + st.y * at[1], pt.z + st.z * at[2], pt.w + st.w * at[3]};
             ag = f32x4{pg.x + sg.x * ag[0], pg.y + sg.y * ag[1], pg.z + sg.z * ag[2], pg.w + sg.w * ag[3]};
           }
-          float4 h;
-          h.x = gate_h<AX>(at[0], ag[0]);
-          h.y = gate_h<AX>(at[1], ag[1]);
-          h.z = gate_h<AX>(at[2], ag[2]);
-          h.w = gate_h<AX>(at[3], ag[3]);
-          store_split4<R>(HS + n * SR, m0, h);
-          // h_j[t] -> the layer's aux CU
-          stw4(mb + g.off_h + ((size_t)j * 2 + par) * XW + ot, h, tag, (lm >> l) & 1u);
+          const float4 h = gate4<AX, PAIR>(at, ag, part);
+          put_split4<PAIR>(HS + sn * SR, m0, h, part);
+          // h_j[t] -> the layer's aux CU (with paired columns lane n posts h, lane n + 8 the history row)
+          u64* const hpost = mb + g.off_h + ((size_t)j * 2 + par) * XW + ot;
+          if constexpr (PAIR) stw4(p0 ? hpost : hist, p0 ? h : xr, tag, (lm >> l) & 1u);
+          else stw4(hpost, h, tag, (lm >> l) & 1u);
         }
         lds_barrier();
         if (j < L - 1) {  // x_l feeds nothing
           // x_j = x_{j-1} + W_res h + B_res
           const float4 br = *reinterpret_cast<const float4*>(BRS + l * R + m0);
           f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-          if constexpr (!I8) acc = f32x4{xr.x + br.x, xr.y + br.y, xr.z + br.z, xr.w + br.w};
-          {
-            const u16* hs = HS + n * SR;
-            acc = mfma_k64(acc, wr[l][0], wr[l][1], ld16(hs + 8 * quad), ld16(hs + R + 8 * quad), ld16(hs + 32 + 8 * quad),
-                           ld16(hs + R + 32 + 8 * quad));
-          }
+          if (!I8 && p0) acc = f32x4{xr.x + br.x, xr.y + br.y, xr.z + br.z, xr.w + br.w};
+          acc = prod1<PAIR>(acc, wr[l][0], wr[l][1], HS + sn * SR, quad, part);
+          if constexpr (PAIR) acc = fold8(acc);
           if constexpr (I8) {
             const float4 sr = *reinterpret_cast<const float4*>(SCL + l * 3 * R + 2 * R + m0);
             xr = make_float4(xr.x + br.x + sr.x * acc[0], xr.y + br.y + sr.y * acc[1], xr.z + br.z + sr.z * acc[2],
@@ -408,10 +545,10 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
           } else {
             xr = v4(acc);
           }
-          store_split4<R>(XS + ((l + 1) & 1) * GC * SR + n * SR, m0, xr);
+          put_split4<PAIR>(XS + ((l + 1) & 1) * NS * SR + sn * SR, m0, xr, part);
           if (l == nl - 1 && c + 1 < g.nch) {
             // x of my last layer -> the next chain CU
-            stw4(mb + g.off_x + ((size_t)(c + 1) * 2 + par) * XW + ot, xr, tag, (lm >> 16) & 1u);
+            post4<PAIR>(mb + g.off_x + ((size_t)(c + 1) * 2 + par) * XW + ot, xr, tag, (lm >> 16) & 1u, part);
           }
           lds_barrier();
         }
@@ -423,13 +560,25 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
       for (int k = 0; k < KS; ++k) {
         const int rt = KS * wave + k;
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        const u16* hs = HS + sn * SR;
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt) acc = mfma_row<R>(WSK[(rt * 2 + kt) * 64 + lane], HS + n * SR, 32 * kt + 8 * quad, acc);
+        for (int kt = 0; kt < 2; ++kt) {
+          const u32x4 w = WSK[(rt * 2 + kt) * 64 + lane];
+          if constexpr (PAIR) {
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w),
+                                                         *reinterpret_cast<const bf16x8*>(hs + part * R + 32 * kt + 8 * quad),
+                                                         acc, 0, 0, 0);
+          } else {
+            acc = mfma_row<R>(w, hs, 32 * kt + 8 * quad, acc);
+          }
+        }
+        if constexpr (PAIR) acc = fold8(acc);
         if constexpr (I8) {
           const float4 s4 = *reinterpret_cast<const float4*>(SSK + rt * 16 + 4 * quad);
           acc = f32x4{s4.x * acc[0], s4.y * acc[1], s4.z * acc[2], s4.w * acc[3]};
         }
-        stw4(mb + g.off_qtail + (size_t)par * S * GC + (rt * 64 + lane) * 4, v4(acc), tag, (lm >> 17) & 1u);
+        post4<PAIR>(mb + g.off_qtail + (size_t)par * S * NS + rt * TW + (quad * NS + sn) * 4, v4(acc), tag,
+                    (lm >> 17) & 1u, part);
       }
       lds_barrier();  // HS is rewritten in the next step's first layer
     }
@@ -439,28 +588,31 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
 // ------------------------------------------------------------------------------------------
 // aux CU: layers ja .. ja + nl - 1
 // ------------------------------------------------------------------------------------------
-template <int S, bool AX, bool I8>
-__device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const int rep, float* dyn, Sync sy, const int64_t tg0,
-                       const unsigned lm) {
+template <int S, bool AX, bool I8, bool PAIR>
+__device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const int rep, float* dyn, Sync sy,
+                                       const int64_t tg0, const unsigned lm) {
+  using C = Cols<PAIR>;
+  constexpr int NS = C::NS, XW = C::XW, PW = C::PW, TW = C::TW;
   constexpr int KS = S / 64;  // row tiles of W_skip per wave
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 15, quad = lane >> 4;
+  const int sn = PAIR ? (n & 7) : n, part = PAIR ? (n >> 3) : 0;
   const int L = g.d.L, T = g.io.T;
   const int ja = ai * g.nla, nl = min(g.nla, L - ja);
   // layers whose skip projection this CU computes (the last layer's runs on the last chain CU)
   const int nsk = (g.tail_on_chain && ja + nl == L) ? nl - 1 : nl;
   const int b0 = rep * g.G, ns = min(g.G, g.io.B - b0);
   u64* const mb = g.mb + (size_t)rep * g.mb_words;
-  const u64* const ring = g.ring + (size_t)rep * g.d.hist_len * GC;
+  const u64* const ring = g.ring + (size_t)rep * g.d.hist_len * NS;
   const wrsrc rs = tagged_region(g);
   const unsigned mbw = (unsigned)(mb - g.ring), rgw = (unsigned)(ring - g.ring);
   float* CD = dyn;                 // [NLA][PW]  conditioning rows L[b, t + 1, j], tile order
   float* BG = CD + NLA * PW;       // [NLA][2R]  B (gate bias)
   float* SP = BG + NLA * 2 * R;    // [NLA][2R]  int8: row scales of W_prev
   float* SK = SP + NLA * 2 * R;    // [NLA][S]   int8: row scales of W_skip
-  u16* HX = reinterpret_cast<u16*>(SK + NLA * S);  // [NLA][GC][SR] history rows x_{j-1}[t + 1 - d], split
-  u16* HH = HX + NLA * GC * SR;                    // [NLA][GC][SR] h_j[t], split
+  u16* HX = reinterpret_cast<u16*>(SK + NLA * S);  // [NLA][NS][SR] history rows x_{j-1}[t + 1 - d], split
+  u16* HH = HX + NLA * NS * SR;                    // [NLA][NS][SR] h_j[t], split
   __shared__ unsigned long long s_hb[NLA];         // stage(): history block (word offset) of each polled layer
   __shared__ unsigned s_ht[NLA];                   //          and the tag it must carry
   __shared__ int s_hl[NLA], s_nh;                  //          and its layer index; how many
@@ -490,10 +642,12 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
   for (int i = tid; i < NLA * PW; i += NT) CD[i] = 0.f;  // padding columns stay zero
   __syncthreads();
 
-  // Conditioning rows of step ts, two float4s per thread and layer: piece q (0 .. 511) holds rows
-  // 4 (q mod 32) .. + 3 of column q / 32, i.e. tile (q mod 32) / 4, lane q / 32 + 16 (q mod 4).
-  // Columns past the replica's streams read the last stream's row and never store it.
-  constexpr int CQ = 2 * R * GC / 4 / NT;
+  // this lane's words of row tile rt of a block
+  auto lot = [&](int rt) { return rt * TW + (quad * NS + sn) * 4; };
+  // Conditioning rows of step ts, CQ float4s per thread and layer: piece q holds rows 4 (q mod 32) ..
+  // + 3 of column q / 32, i.e. tile (q mod 32) / 4, run (q mod 4, q / 32).  Columns past the
+  // replica's streams read the last stream's row and never store it.
+  constexpr int CQ = 2 * R * NS / 4 / NT;
   size_t cq_src[CQ];
   int cq_dst[CQ];
   bool cq_on[CQ];
@@ -502,7 +656,7 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
     const int q = tid + NT * k, cn = q >> 5, e4 = q & 31;
     cq_on[k] = cn < ns;
     cq_src[k] = (size_t)min(cn, ns - 1) * T * L * 2 * R + 4 * e4;  // + (step L + layer) 2R
-    cq_dst[k] = ((e4 >> 2) * 64 + cn + 16 * (e4 & 3)) * 4;
+    cq_dst[k] = (e4 >> 2) * TW + ((e4 & 3) * NS + cn) * 4;
   }
   const float* const cbase = g.io.cond + (size_t)b0 * T * L * 2 * R;
   // Stage the inputs of pre_j[ts]: the conditioning rows of every layer and the history rows
@@ -524,7 +678,7 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
         if (l < nl && (all_hist || dl[l] >= 2)) {
           const int d = dl[l];
           const int64_t sl = ts % d;
-          s_hb[nh] = ((unsigned long long)ho[l] + (unsigned long long)sl * R) * GC;
+          s_hb[nh] = ((unsigned long long)ho[l] + (unsigned long long)sl * R) * NS;
           s_ht[nh] = ts - d >= 0 ? (unsigned)(ts - d + 1) : 0u;
           s_hl[nh] = l;
           ++nh;
@@ -536,7 +690,7 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
     poll_pairs<4, NT, 16>(
         g, rs, tid, s_nh * XW / 2, [&](int p) { return rgw + (unsigned)s_hb[(2 * p) / XW] + (2 * p) % XW; },
         [&](int i) { return s_ht[i / XW]; },
-        [&](int i, int, float v) { split_into(HX + s_hl[i / XW] * GC * SR, i % XW, v); }, sy);
+        [&](int i, int, float v) { split_into<NS>(HX + s_hl[i / XW] * NS * SR, i % XW, v); }, sy);
 #pragma unroll
     for (int l = 0; l < NLA; ++l)
 #pragma unroll
@@ -550,18 +704,15 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
     const unsigned tg = (unsigned)(ts + 1);
     const bool loc = (lm >> l) & 1u;
     f32x4 pa[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-    {
-      const u16* hx = HX + l * GC * SR + n * SR;
-      mfma_k64_2(pa[0], pa[1], wp[l][0][0], wp[l][0][1], wp[l][1][0], wp[l][1][1], ld16(hx + 8 * quad),
-                 ld16(hx + R + 8 * quad), ld16(hx + 32 + 8 * quad), ld16(hx + R + 32 + 8 * quad));
-    }
+    prod2<PAIR>(pa[0], pa[1], wp[l][0][0], wp[l][0][1], wp[l][1][0], wp[l][1][1], HX + l * NS * SR + sn * SR, quad,
+                part);
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
       const int rt = 2 * wave + k;
-      const f32x4 acc = pa[k];
+      const f32x4 acc = PAIR ? fold8(pa[k]) : pa[k];
       const int mr = 16 * rt + 4 * quad;
       const float4 b = *reinterpret_cast<const float4*>(BG + l * 2 * R + mr);
-      const float4 cd = *reinterpret_cast<const float4*>(CD + l * PW + (rt * 64 + lane) * 4);
+      const float4 cd = *reinterpret_cast<const float4*>(CD + l * PW + lot(rt));
       float4 v;
       if constexpr (I8) {
         const float4 s4 = *reinterpret_cast<const float4*>(SP + l * 2 * R + mr);
@@ -570,7 +721,7 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
       } else {
         v = make_float4(acc[0] + b.x + cd.x, acc[1] + b.y + cd.y, acc[2] + b.z + cd.z, acc[3] + b.w + cd.w);
       }
-      stw4(mb + ((size_t)(ja + l) * 2 + (ts & 1)) * PW + (rt * 64 + lane) * 4, v, tg, loc);
+      post4<PAIR>(mb + ((size_t)(ja + l) * 2 + (ts & 1)) * PW + lot(rt), v, tg, loc, part);
     }
   };
 
@@ -596,6 +747,7 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
       stage(t + 1, false);
       if (sy.failed()) return;
     }
+    // the skip sum of my layers (with paired columns unfolded until it is posted: the fold is linear)
     f32x4 qs[KS];
 #pragma unroll
     for (int k = 0; k < KS; ++k) qs[k] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -606,7 +758,7 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
     auto lw_n = [&](int l) { return (more && dl[l] == 1) ? XW : XW / 2; };  // pairs
     auto lw_word = [&](int l) {
       const unsigned hw = mbw + g.off_h + ((unsigned)(ja + l) * 2 + par) * XW;
-      const unsigned xw = rgw + (unsigned)ho[l] * GC;
+      const unsigned xw = rgw + (unsigned)ho[l] * NS;
       return [=](int p) { return 2 * p < XW ? hw + 2 * p : xw + (2 * p - XW); };
     };
     u32x4 pw[XW / NT];
@@ -617,8 +769,8 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
         pairs_finish(
             g, pw, rs, tid, lw_n(l), lw_word(l), [&](int) { return tag; },
             [&](int i, int, float v) {
-              if (i < XW) split_into(HH + l * GC * SR, i, v);
-              else split_into(HX + l * GC * SR, i - XW, v);
+              if (i < XW) split_into<NS>(HH + l * NS * SR, i, v);
+              else split_into<NS>(HX + l * NS * SR, i - XW, v);
             },
             sy);
         lds_barrier();
@@ -626,15 +778,13 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
         if (l + 1 < NLA && l + 1 < nl) pairs_start(pw, rs, tid, lw_n(l + 1), lw_word(l + 1));
         if (l < nsk) {
           // q += W_skip h_j, row tiles KS wave ..
-          const u16* hh = HH + l * GC * SR + n * SR;
-          const u32x4 h0 = ld16(hh + 8 * quad), l0 = ld16(hh + R + 8 * quad), h1 = ld16(hh + 32 + 8 * quad),
-                      l1 = ld16(hh + R + 32 + 8 * quad);
+          const u16* hh = HH + l * NS * SR + sn * SR;
           f32x4 sa[KS];
 #pragma unroll
           for (int k = 0; k < KS; ++k) sa[k] = I8 ? f32x4{0.f, 0.f, 0.f, 0.f} : qs[k];
 #pragma unroll
           for (int k = 0; k < KS; k += 2)
-            mfma_k64_2(sa[k], sa[k + 1], wk[l][k][0], wk[l][k][1], wk[l][k + 1][0], wk[l][k + 1][1], h0, l0, h1, l1);
+            prod2<PAIR>(sa[k], sa[k + 1], wk[l][k][0], wk[l][k][1], wk[l][k + 1][0], wk[l][k + 1][1], hh, quad, part);
 #pragma unroll
           for (int k = 0; k < KS; ++k) {
             const f32x4 acc = sa[k];
@@ -649,18 +799,29 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
           // The partial goes out as soon as its last layer is in, with the previous aux CU's added: the
           // partials of all but the last posting aux CU form a running sum, so the head waits for two
           // of them (the last one is posted alone, to keep this wait off the end of the step).  A lane
-          // reads the previous partial's words it holds itself (same tiles and elements).
+          // reads the previous partial's words it posts itself (same tiles and elements).
           if (l == nsk - 1) {
+            if constexpr (PAIR) {
+#pragma unroll
+              for (int k = 0; k < KS; ++k) qs[k] = fold8(qs[k]);
+            }
             if (ai > 0 && ai < g.naux_q - 1) {
-              const unsigned pq = mbw + g.off_q + ((unsigned)(ai - 1) * 2 + par) * S * GC;
-              poll_pairs<2 * KS, 1>(
-                  g, rs, 0, 2 * KS, [&](int p) { return pq + ((KS * wave + (p >> 1)) * 64 + lane) * 4 + 2 * (p & 1); },
-                  [&](int) { return tag; }, [&](int, int q, float v) { qs[q >> 2][q & 3] += v; }, sy);
+              const unsigned pq = mbw + g.off_q + ((unsigned)(ai - 1) * 2 + par) * S * NS;
+              if constexpr (PAIR) {
+                poll_pairs<KS, 1>(
+                    g, rs, 0, KS, [&](int p) { return pq + lot(KS * wave + p) + 2 * part; }, [&](int) { return tag; },
+                    [&](int, int q, float v) { qs[q >> 1][2 * part + (q & 1)] += v; }, sy);
+              } else {
+                poll_pairs<2 * KS, 1>(
+                    g, rs, 0, 2 * KS, [&](int p) { return pq + lot(KS * wave + (p >> 1)) + 2 * (p & 1); },
+                    [&](int) { return tag; }, [&](int, int q, float v) { qs[q >> 2][q & 3] += v; }, sy);
+              }
             }
             const bool loc = (lm >> 16) & 1u;
 #pragma unroll
             for (int k = 0; k < KS; ++k)
-              stw4(mb + g.off_q + ((size_t)ai * 2 + par) * S * GC + ((KS * wave + k) * 64 + lane) * 4, v4(qs[k]), tag, loc);
+              post4<PAIR>(mb + g.off_q + ((size_t)ai * 2 + par) * S * NS + lot(KS * wave + k), v4(qs[k]), tag, loc,
+                          part);
           }
         }
       }
@@ -675,59 +836,64 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
   }
 }
 
-// The head's products for the four row tiles of a wave: acc[k] = W[k] [hi; lo] over K inputs (a split
-// row of this lane's column at `row`), two tiles and 128 inputs per MFMA block.
-template <int K, int KT>
+// The head's products for the four row tiles of a wave: acc[k] = W[k] z over K inputs, row = this
+// lane's part (hi or lo) of its stream's split row; folded.
+template <int KT>
 __device__ __forceinline__ void head_products(f32x4 (&acc)[4], const u32x4 (&w)[4][KT], const u16* row, int quad) {
   static_assert(KT % 4 == 0, "128-input blocks");
 #pragma unroll
   for (int k = 0; k < 4; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // every B operand first (one LDS round trip), then the MFMA blocks back to back
-  u32x4 hb[KT], lb[KT];
+  u32x4 xb[KT];  // every B operand first (one LDS round trip), then the MFMA blocks back to back
 #pragma unroll
-  for (int q = 0; q < KT; ++q) {
-    hb[q] = ld16(row + 32 * q + 8 * quad);
-    lb[q] = ld16(row + K + 32 * q + 8 * quad);
-  }
+  for (int q = 0; q < KT; ++q) xb[q] = ld16(row + 32 * q + 8 * quad);
 #pragma unroll
   for (int kb = 0; kb < KT; kb += 4) {
-    const u32x4 h[4] = {hb[kb], hb[kb + 1], hb[kb + 2], hb[kb + 3]};
-    const u32x4 l[4] = {lb[kb], lb[kb + 1], lb[kb + 2], lb[kb + 3]};
+    const u32x4 x[4] = {xb[kb], xb[kb + 1], xb[kb + 2], xb[kb + 3]};
 #pragma unroll
     for (int k = 0; k < 4; k += 2) {
       const u32x4 wa[4] = {w[k][kb], w[k][kb + 1], w[k][kb + 2], w[k][kb + 3]};
       const u32x4 wb[4] = {w[k + 1][kb], w[k + 1][kb + 1], w[k + 1][kb + 2], w[k + 1][kb + 3]};
-      mfma_k128_2(acc[k], acc[k + 1], wa, wb, h, l);
+      mfma_k128_2p(acc[k], acc[k + 1], wa, wb, x);
     }
   }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) acc[k] = fold8(acc[k]);
 }
 
 // ------------------------------------------------------------------------------------------
-// head CU: the skip sum, the two head layers, the draw and the next step's x0
+// head CU hh: columns 8 hh .. 8 hh + 7 of the replica's tiles (8 streams): the skip sum, the two head
+// layers, the draw and the next step's x0
 // ------------------------------------------------------------------------------------------
-template <int S, bool TF, bool AX, bool I8>
-__device__ __forceinline__ void mc_head(const WnChainArgs& g, const int rep, float* dyn, Sync sy, const int64_t tg0,
-                        const unsigned lm) {
+template <int S, bool TF, bool AX, bool I8, bool PAIR>
+__device__ __forceinline__ void mc_head(const WnChainArgs& g, const int hh, const int rep, float* dyn, Sync sy,
+                                        const int64_t tg0, const unsigned lm) {
+  using C = Cols<PAIR>;
+  constexpr int NS = C::NS, XW = C::XW;
   constexpr int KTH = S / 32, KTO = A / 32;
   constexpr int SS = 2 * S + 8, SA = 2 * A + 8, PA = A + 4;
-  constexpr int QW = S * GC;     // words of a skip partial
-  constexpr int NQ = QW / NT;    // skip-sum entries per thread
-  constexpr int HT = A / 16 / 4; // row tiles of W_relu and of W_out per wave
-  static_assert(16 % NQ == 0, "a poll batch covers whole partials");
-  static_assert(HT == 4, "four row tiles per wave");
+  constexpr int QW = S * NS;           // words of a skip partial
+  constexpr int QP = S * HG / 2;       // pairs of a partial in my 8 columns
+  constexpr int NQP = QP / NT;         // of them per thread
+  constexpr int NQ = 2 * NQP;          // skip-sum entries per thread
+  constexpr int HT = A / 16 / 4;       // row tiles of W_relu and of W_out per wave
+  static_assert(HT == 4 && NQP == 4, "four row tiles per wave, four pairs per partial and thread");
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int n = lane & 15, quad = lane >> 4;
+  const int n = lane & 15, quad = lane >> 4, sn = n & 7, part = n >> 3;
+  const bool wl = part == 0;  // the lane that stores its stream's results (lanes n, n + 8 hold the same)
   const int T = g.io.T;
-  const int b0 = rep * g.G, ns = min(g.G, g.io.B - b0);
+  const int c0 = HG * hh;                              // my first column of the replica's tiles
+  const int nrs = min(g.G, g.io.B - rep * g.G);        // streams of the replica
+  const int ns = max(0, min(HG, nrs - c0));            // mine
+  const int b0 = rep * g.G + c0;
   const bool e2 = g.w.embed_prev != nullptr;
   u64* const mb = g.mb + (size_t)rep * g.mb_words;
   const wrsrc rs = tagged_region(g);
   const unsigned mbw = (unsigned)(mb - g.ring);
-  u16* ZS = reinterpret_cast<u16*>(dyn);               // [GC][SS] z_s, split
-  u16* ZA = ZS + GC * SS;                              // [GC][SA] z_a, split
-  float* LG = reinterpret_cast<float*>(ZA + GC * SA);  // [GC][PA] logits
-  float* BSK = LG + GC * PA;  // [S] B_skip
+  u16* ZS = reinterpret_cast<u16*>(dyn);               // [HG][SS] z_s, split
+  u16* ZA = ZS + HG * SS;                              // [HG][SA] z_a, split
+  float* LG = reinterpret_cast<float*>(ZA + HG * SA);  // [HG][PA] logits
+  float* BSK = LG + HG * PA;  // [S] B_skip
   float* BRL = BSK + S;       // [A] B_relu
   float* BO = BRL + A;        // [A] B_out
   float* BE = BO + A;         // [R] B_embed
@@ -737,9 +903,9 @@ __device__ __forceinline__ void mc_head(const WnChainArgs& g, const int rep, flo
   float* SEP = SE + A;
   u16* EMB = reinterpret_cast<u16*>(SEP + A);  // [A][R] the table of y_{t-1}: bf16, or int8 codes
   u16* EMBP = EMB + A * R;                     // [A][R] the table of y_{t-2} (two taps)
-  __shared__ int s_y[GC], s_y2[GC];            // y_{t-1}, y_{t-2} (-1 before the first input)
-  __shared__ float s_u[GC];
-  __shared__ int s_yin[GC];
+  __shared__ int s_y[HG], s_y2[HG];            // y_{t-1}, y_{t-2} (-1 before the first input)
+  __shared__ float s_u[HG];
+  __shared__ int s_yin[HG];
 
   // wave v: row tiles HT v .. HT v + HT - 1 of W_relu and of W_out
   u32x4 w1[HT][KTH], w2[HT][KTO];
@@ -773,7 +939,8 @@ __device__ __forceinline__ void mc_head(const WnChainArgs& g, const int rep, flo
       for (int i = tid; i < TW; i += NT) reinterpret_cast<unsigned*>(EMBP)[i] = ep[i];
     }
   }
-  if (tid < GC) {
+  for (int i = tid; i < HG * SS; i += NT) ZS[i] = 0;  // padding streams' rows stay finite
+  if (tid < HG) {
     int y = 0, y2 = -1;
     if (tid < ns) {
       const int64_t* st = g.state + WN_STATE_WORDS * (size_t)(b0 + tid);
@@ -789,24 +956,31 @@ __device__ __forceinline__ void mc_head(const WnChainArgs& g, const int rep, flo
     if constexpr (I8) return (float)reinterpret_cast<const signed char*>(tab)[y * R + k] * sc[y];
     else return bf16_val(tab[y * R + k]);
   };
-  // x0 of the call's first step (padding columns get zeros)
-  for (int i = tid; i < XW; i += NT) {
-    const int m = trow(i), cn = tcol(i);
+  // x0 of the call's first step in my columns (padding columns get zeros)
+  for (int i = tid; i < R * HG; i += NT) {
+    const int m = i >> 3, q = i & 7;
     float v = 0.f;
-    if (cn < ns) {
-      v = emb(EMB, SE, s_y[cn], m) + BE[m];
-      if (e2 && s_y2[cn] >= 0) v += emb(EMBP, SEP, s_y2[cn], m);
+    if (q < ns) {
+      v = emb(EMB, SE, s_y[q], m) + BE[m];
+      if (e2 && s_y2[q] >= 0) v += emb(EMBP, SEP, s_y2[q], m);
     }
-    stw(mb + g.off_x + (size_t)(tg0 & 1) * XW + i, pack(v, (unsigned)(tg0 + 1)), lm & 1u);
+    stw(mb + g.off_x + (size_t)(tg0 & 1) * XW + tpos<NS>(m, c0 + q), pack(v, (unsigned)(tg0 + 1)), lm & 1u);
   }
 
   // skip partials per step: the running sum of all aux CUs' but the last (posted by the one before
   // the last), the last aux CU's own, and the last layer's from the last chain CU
-  const int nqa = g.naux_q >= 2 ? 2 : g.naux_q;  // aux partials polled
+  const int nqa = g.naux_q >= 2 ? 2 : g.naux_q;
   const int np = nqa + (g.tail_on_chain ? 1 : 0);
   auto part_word = [&](int p, int par) -> unsigned {
     if (p < nqa) return mbw + g.off_q + ((unsigned)(g.naux_q - nqa + p) * 2 + par) * QW;
     return mbw + g.off_qtail + (unsigned)par * QW;
+  };
+  // pair r (0 .. QP - 1) of a partial in my columns: with paired columns the whole partial; else tile
+  // r / 64, run (i / 8, c0 + i mod 8) with i = (r / 2) mod 32, words 2 (r mod 2), + 1 of that run
+  auto pair_off = [&](int r) {
+    if constexpr (PAIR) return (unsigned)(2 * r);
+    const int i = (r >> 1) & 31;
+    return (unsigned)((((r >> 6) << 6) + (i & 7) + c0 + ((i >> 3) << 4)) * 4 + 2 * (r & 1));
   };
   for (int64_t t = tg0; t < tg0 + T; ++t) {
     const unsigned tag = (unsigned)(t + 1);
@@ -820,103 +994,110 @@ __device__ __forceinline__ void mc_head(const WnChainArgs& g, const int rep, flo
       if constexpr (TF) yv = g.io.y_in[at];
       else uv = g.io.u[at];
     }
-    // the skip partials of the step: the aux CUs' sum, then the last layer's from the last chain CU.
-    // Entry e of this thread is word tid + NT e of each partial, summed in partial order.
+    // the skip partials of the step, my columns, all in one batch: pair p = tid + NT k is pair
+    // tid + NT (k mod NQP) of partial k / NQP, entries 2 (k mod NQP) (+ 1) of this thread, the same
+    // position in every partial, summed in partial order
     float qa[NQ];
 #pragma unroll
     for (int e = 0; e < NQ; ++e) qa[e] = 0.f;
-    // pair p = tid + NT k holds words 2 tid + 2 NT k (+ 1) of partial (2 p) / QW: entry 2 (k mod (NQ / 2))
-    // (+ 1) of this thread, the same position in every partial
-    // (two partials per batch)
     {
-      constexpr int KP = NQ;
-      poll_pairs<KP>(
-          g, rs, tid, np * QW / 2, [&](int p) { return part_word((2 * p) / QW, par) + (2 * p) % QW; },
-          [&](int) { return tag; }, [&](int, int q, float v) { qa[q % NQ] += v; }, sy);
+      constexpr int KP = 3 * NQP;
+      u32x4 w[KP];
+      auto word = [&](int p) { return part_word(p / QP, par) + pair_off(p % QP); };
+      pairs_start<KP>(w, rs, tid, np * QP, word);
+      pairs_finish<KP>(
+          g, w, rs, tid, np * QP, word, [&](int) { return tag; }, [&](int, int q, float v) { qa[q % NQ] += v; }, sy);
     }
-    if (tid < GC) {
+    if (tid < HG) {
       if constexpr (TF) s_yin[tid] = yv < 0 ? 0 : (yv > A - 1 ? A - 1 : yv);
       else s_u[tid] = uv;
     }
-    // z_s = relu(B_skip + sum of the partials); entries 2e' and 2e' + 1 are rows m, m + 1 (m even) of
+    // z_s = relu(B_skip + sum of the partials); the two words of a pair are rows m, m + 1 (m even) of
     // one column, stored as one 32-bit word of hi parts and one of lo parts
 #pragma unroll
     for (int e = 0; e < NQ; e += 2) {
-      const int wi = 2 * tid + NT * e, m = trow(wi), cn = tcol(wi);
+      const unsigned wo = pair_off(tid + NT * (e >> 1));
+      const int m = trow<NS>((int)wo), q = tcol<NS>((int)wo) - c0;
       const float z0 = fmaxf(qa[e] + BSK[m], 0.f), z1 = fmaxf(qa[e + 1] + BSK[m + 1], 0.f);
       const unsigned hi = pack_bf16(z0, z1);
       const unsigned lo = pack_bf16(z0 - low_bf16(hi), z1 - high_bf16(hi));
-      *reinterpret_cast<unsigned*>(ZS + cn * SS + m) = hi;
-      *reinterpret_cast<unsigned*>(ZS + cn * SS + S + m) = lo;
+      *reinterpret_cast<unsigned*>(ZS + q * SS + m) = hi;
+      *reinterpret_cast<unsigned*>(ZS + q * SS + S + m) = lo;
     }
     lds_barrier();
     if (sy.failed()) return;
     // z_a = relu(W_relu z_s + B_relu)
-    f32x4 za[HT];
-    head_products<S, KTH>(za, w1, ZS + n * SS, quad);
+    {
+      f32x4 za[HT];
+      head_products<KTH>(za, w1, ZS + sn * SS + part * S, quad);
 #pragma unroll
-    for (int k = 0; k < HT; ++k) {
-      f32x4 acc = za[k];
-      const int mr = 16 * (HT * wave + k) + 4 * quad;
-      const float4 b = *reinterpret_cast<const float4*>(BRL + mr);
-      if constexpr (I8) {
-        const float4 s4 = *reinterpret_cast<const float4*>(SRL + mr);
-        acc = f32x4{s4.x * acc[0], s4.y * acc[1], s4.z * acc[2], s4.w * acc[3]};
+      for (int k = 0; k < HT; ++k) {
+        f32x4 acc = za[k];
+        const int mr = 16 * (HT * wave + k) + 4 * quad;
+        const float4 b = *reinterpret_cast<const float4*>(BRL + mr);
+        if constexpr (I8) {
+          const float4 s4 = *reinterpret_cast<const float4*>(SRL + mr);
+          acc = f32x4{s4.x * acc[0], s4.y * acc[1], s4.z * acc[2], s4.w * acc[3]};
+        }
+        if (wl)
+          store_split4<A>(ZA + sn * SA, mr,
+                          make_float4(fmaxf(acc[0] + b.x, 0.f), fmaxf(acc[1] + b.y, 0.f), fmaxf(acc[2] + b.z, 0.f),
+                                      fmaxf(acc[3] + b.w, 0.f)));
       }
-      store_split4<A>(ZA + n * SA, mr,
-                      make_float4(fmaxf(acc[0] + b.x, 0.f), fmaxf(acc[1] + b.y, 0.f), fmaxf(acc[2] + b.z, 0.f),
-                                  fmaxf(acc[3] + b.w, 0.f)));
     }
     lds_barrier();
     // logits = W_out z_a + B_out
-    f32x4 lo[HT];
-    head_products<A, KTO>(lo, w2, ZA + n * SA, quad);
+    {
+      f32x4 lo[HT];
+      head_products<KTO>(lo, w2, ZA + sn * SA + part * A, quad);
 #pragma unroll
-    for (int k = 0; k < HT; ++k) {
-      f32x4 acc = lo[k];
-      const int mr = 16 * (HT * wave + k) + 4 * quad;
-      const float4 b = *reinterpret_cast<const float4*>(BO + mr);
-      if constexpr (I8) {
-        const float4 s4 = *reinterpret_cast<const float4*>(SO + mr);
-        acc = f32x4{s4.x * acc[0], s4.y * acc[1], s4.z * acc[2], s4.w * acc[3]};
+      for (int k = 0; k < HT; ++k) {
+        f32x4 acc = lo[k];
+        const int mr = 16 * (HT * wave + k) + 4 * quad;
+        const float4 b = *reinterpret_cast<const float4*>(BO + mr);
+        if constexpr (I8) {
+          const float4 s4 = *reinterpret_cast<const float4*>(SO + mr);
+          acc = f32x4{s4.x * acc[0], s4.y * acc[1], s4.z * acc[2], s4.w * acc[3]};
+        }
+        if (wl)
+          *reinterpret_cast<float4*>(LG + sn * PA + mr) = make_float4(acc[0] + b.x, acc[1] + b.y, acc[2] + b.z, acc[3] + b.w);
       }
-      *reinterpret_cast<float4*>(LG + n * PA + mr) = make_float4(acc[0] + b.x, acc[1] + b.y, acc[2] + b.z, acc[3] + b.w);
     }
     lds_barrier();
-    // the draws of streams GC / 4 wave .. (all four at once, so that their steps interleave; a padding
-    // column's draw is made and dropped), then their x0 of the next step (row = lane)
-    int ys[GC / 4];
+    // the draws of my streams HG / 4 wave .. (both at once, so that their steps interleave; a padding
+    // stream's draw is made and dropped), then their x0 of the next step (row = lane)
+    int ys[HG / 4];
 #pragma unroll
-    for (int k = 0; k < GC / 4; ++k) {
-      const int nn = (GC / 4) * wave + k;
+    for (int k = 0; k < HG / 4; ++k) {
+      const int q = (HG / 4) * wave + k;
       if constexpr (TF) {
-        ys[k] = s_yin[nn];
+        ys[k] = s_yin[q];
       } else {
-        const float4 lv = *reinterpret_cast<const float4*>(LG + nn * PA + 4 * lane);
-        ys[k] = wave_draw<AX>(lv, s_u[nn], g.io.smode, g.io.inv_t, g.io.top_k, lane);
+        const float4 lv = *reinterpret_cast<const float4*>(LG + q * PA + 4 * lane);
+        ys[k] = wave_draw<AX>(lv, s_u[q], g.io.smode, g.io.inv_t, g.io.top_k, lane);
       }
     }
 #pragma unroll
-    for (int k = 0; k < GC / 4; ++k) {
-      const int nn = (GC / 4) * wave + k;
-      const int y = nn < ns ? ys[k] : 0;
-      if (nn < ns) {
-        const size_t at = (size_t)(b0 + nn) * T + (size_t)(t - tg0);
-        if constexpr (TF) reinterpret_cast<float4*>(g.io.logits + at * A)[lane] = *reinterpret_cast<const float4*>(LG + nn * PA + 4 * lane);
+    for (int k = 0; k < HG / 4; ++k) {
+      const int q = (HG / 4) * wave + k;
+      const int y = q < ns ? ys[k] : 0;
+      if (q < ns) {
+        const size_t at = (size_t)(b0 + q) * T + (size_t)(t - tg0);
+        if constexpr (TF) reinterpret_cast<float4*>(g.io.logits + at * A)[lane] = *reinterpret_cast<const float4*>(LG + q * PA + 4 * lane);
         else if (lane == 0) g.io.y_out[at] = y;
       }
-      const int yp = s_y[nn];
+      const int yp = s_y[q];
       if (more) {
         float v = 0.f;
-        if (nn < ns) {
+        if (q < ns) {
           v = emb(EMB, SE, y, lane) + BE[lane];
           if (e2) v += emb(EMBP, SEP, yp, lane);
         }
-        stw(mb + g.off_x + (size_t)((t + 1) & 1) * XW + tpos(lane, nn), pack(v, tag + 1), lm & 1u);
+        stw(mb + g.off_x + (size_t)((t + 1) & 1) * XW + tpos<NS>(lane, c0 + q), pack(v, tag + 1), lm & 1u);
       }
-      if (lane == 0 && nn < ns) {
-        s_y2[nn] = yp;
-        s_y[nn] = y;
+      if (lane == 0 && q < ns) {
+        s_y2[q] = yp;
+        s_y[q] = y;
       }
     }
     lds_barrier();
@@ -930,8 +1111,10 @@ __device__ __forceinline__ void mc_head(const WnChainArgs& g, const int rep, flo
   }
 }
 
-template <int S, bool TF, bool AX, bool I8>
+
+template <int S, bool TF, bool AX, bool I8, bool PAIR>
 __global__ __launch_bounds__(NT, 1) void wn_mchain_kernel(const WnChainArgs ga) {
+  using C = Cols<PAIR>;
   // The argument block is read in place, through the kernel-argument segment: used as the by-value
   // parameter, the compiler copies all of it to scratch memory once the roles index it at run time.
 #if __HIP_DEVICE_COMPILE__
@@ -942,19 +1125,19 @@ __global__ __launch_bounds__(NT, 1) void wn_mchain_kernel(const WnChainArgs ga) 
   (void)ga;
   extern __shared__ __align__(16) float dyn[];
   __shared__ int s_abort;
-  __shared__ unsigned char s_xcd[WN_MAX_CHAIN + 1 + WN_MAX_LAYERS];
+  __shared__ unsigned char s_xcd[WN_MAX_CHAIN + 2 + WN_MAX_LAYERS];
   __shared__ unsigned char s_cof[WN_MAX_LAYERS];
   __shared__ int s_me;
   const int rb = g.role_of_block[blockIdx.x];
   if (rb == 0xffff) return;
-  const int per = g.nch + 1 + g.naux;  // roles of a replica: chain CUs, the head, aux CUs
+  const int per = g.nch + C::NH + g.naux;  // roles of a replica: chain CUs, head CUs, aux CUs
   const int k = rb / per, role = rb - k * per;
-  const int head = g.nch;
+  const int head = g.nch, aux0 = g.nch + C::NH;
   if (threadIdx.x == 0) s_abort = 0;
   // Which of this block's posts go to a reader on its own XCD in this launch: bit l of a chain CU for
   // the aux CU of its layer l (h and the history rows), bit 16 for the next chain CU, bit 17 for the
-  // head; bit l of an aux CU for the chain CU of its layer l, bit 16 for the head; bit 0 of the head
-  // for chain CU 0.  The map is read at the launch (grid_meet).
+  // head CUs; bit l of an aux CU for the chain CU of its layer l, bit 16 for the head CUs; bit 0 of a
+  // head CU for chain CU 0.  The map is read at the launch (grid_meet).
   unsigned lm = 0;
   if (g.local_posts) {
     if (grid_meet(g.xmap, g.n_active, g.spin_limit, g.status, &s_me) < 0) return;  // WN_ETIMEOUT is in the status word
@@ -969,17 +1152,18 @@ __global__ __launch_bounds__(NT, 1) void wn_mchain_kernel(const WnChainArgs ga) 
     __syncthreads();
     const int me = s_me;
     auto same = [&](int r) { return s_xcd[r] == me; };
+    const bool heads_same = same(head) && (C::NH == 1 || same(head + 1));
     if (role < head) {
       const int j0 = g.layer_begin[role], nl = g.layer_begin[role + 1] - j0;
-      for (int l = 0; l < nl; ++l) lm |= (unsigned)same(head + 1 + (j0 + l) / g.nla) << l;
+      for (int l = 0; l < nl; ++l) lm |= (unsigned)same(aux0 + (j0 + l) / g.nla) << l;
       if (role + 1 < g.nch) lm |= (unsigned)same(role + 1) << 16;
-      lm |= (unsigned)same(head) << 17;
-    } else if (role == head) {
+      lm |= (unsigned)heads_same << 17;
+    } else if (role < aux0) {
       lm = same(0);
     } else {
-      const int ja = (role - head - 1) * g.nla;
+      const int ja = (role - aux0) * g.nla;
       for (int l = 0; l < g.nla && ja + l < g.d.L; ++l) lm |= (unsigned)same(s_cof[ja + l]) << l;
-      lm |= (unsigned)same(head) << 16;
+      lm |= (unsigned)heads_same << 16;
     }
   }
   // where this call starts: from zero, or where the previous call on this workspace stopped (the
@@ -987,9 +1171,9 @@ __global__ __launch_bounds__(NT, 1) void wn_mchain_kernel(const WnChainArgs ga) 
   const int64_t tg0 = g.io.reset ? 0 : g.state[WN_STATE_WORDS * (size_t)(k * g.G)];
   __syncthreads();
   Sync sy{&s_abort};
-  if (role < head) mc_chain<S, AX, I8>(g, role, k, dyn, sy, tg0, lm);
-  else if (role == head) mc_head<S, TF, AX, I8>(g, k, dyn, sy, tg0, lm);
-  else mc_aux<S, AX, I8>(g, role - head - 1, k, dyn, sy, tg0, lm);
+  if (role < head) mc_chain<S, AX, I8, PAIR>(g, role, k, dyn, sy, tg0, lm);
+  else if (role < aux0) mc_head<S, TF, AX, I8, PAIR>(g, role - head, k, dyn, sy, tg0, lm);
+  else mc_aux<S, AX, I8, PAIR>(g, role - aux0, k, dyn, sy, tg0, lm);
 }
 
 // Layers of each chain CU: runs of at most NLC, as even as possible.
@@ -1005,24 +1189,29 @@ int mchain_split(int L, int* layer_begin) {
 constexpr size_t kMaxLds = 160 * 1024;
 
 template <int S>
-size_t mchain_lds() { return std::max(chain_lds(S), std::max(aux_lds(S), head_lds(S))); }
+size_t mchain_lds() {
+  return std::max({chain_lds<false>(S), chain_lds<true>(S), aux_lds<false>(S), aux_lds<true>(S), head_lds(S)});
+}
+
+template <int S, bool PAIR>
+const void* mchain_kernel(bool teacher, bool ax, bool i8) {
+  if (teacher) {
+    if (i8) return ax ? reinterpret_cast<const void*>(wn_mchain_kernel<S, true, true, true, PAIR>)
+                      : reinterpret_cast<const void*>(wn_mchain_kernel<S, true, false, true, PAIR>);
+    return ax ? reinterpret_cast<const void*>(wn_mchain_kernel<S, true, true, false, PAIR>)
+              : reinterpret_cast<const void*>(wn_mchain_kernel<S, true, false, false, PAIR>);
+  }
+  if (i8) return ax ? reinterpret_cast<const void*>(wn_mchain_kernel<S, false, true, true, PAIR>)
+                    : reinterpret_cast<const void*>(wn_mchain_kernel<S, false, false, true, PAIR>);
+  return ax ? reinterpret_cast<const void*>(wn_mchain_kernel<S, false, true, false, PAIR>)
+            : reinterpret_cast<const void*>(wn_mchain_kernel<S, false, false, false, PAIR>);
+}
 
 template <int S>
 hipError_t launch_mchain_s(const WnChainArgs& g, bool teacher, hipStream_t stream) {
   const size_t dyn = mchain_lds<S>();
   const bool ax = g.w.approx_nl != 0, i8 = g.w.i8 != 0;
-  const void* k;
-  if (teacher) {
-    if (i8) k = ax ? reinterpret_cast<const void*>(wn_mchain_kernel<S, true, true, true>)
-                   : reinterpret_cast<const void*>(wn_mchain_kernel<S, true, false, true>);
-    else k = ax ? reinterpret_cast<const void*>(wn_mchain_kernel<S, true, true, false>)
-                : reinterpret_cast<const void*>(wn_mchain_kernel<S, true, false, false>);
-  } else {
-    if (i8) k = ax ? reinterpret_cast<const void*>(wn_mchain_kernel<S, false, true, true>)
-                   : reinterpret_cast<const void*>(wn_mchain_kernel<S, false, false, true>);
-    else k = ax ? reinterpret_cast<const void*>(wn_mchain_kernel<S, false, true, false>)
-                : reinterpret_cast<const void*>(wn_mchain_kernel<S, false, false, false>);
-  }
+  const void* k = g.pair ? mchain_kernel<S, true>(teacher, ax, i8) : mchain_kernel<S, false>(teacher, ax, i8);
   hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
   if (e != hipSuccess) return e;
   void* args[] = {const_cast<WnChainArgs*>(&g)};
@@ -1039,8 +1228,6 @@ bool wn_mchain_supported(int R_, int S_, int L) {
   return nch <= WN_MAX_CHAIN && nch + 1 + naux <= WN_CHAIN_GRID && mchain_lds<256>() <= kMaxLds;
 }
 
-int wn_mchain_streams_max() { return GC; }
-
 bool wn_mchain_plan(int L, int R_, int S_, int B, WnChainPlan* p) {
   if (!p || B < 1 || !wn_mchain_supported(R_, S_, L)) return false;
   WnChainPlan q{};
@@ -1056,24 +1243,38 @@ bool wn_mchain_plan(int L, int R_, int S_, int B, WnChainPlan* p) {
   q.tail_on_chain = 1;
   // aux CUs that post a skip partial: all but one holding only the last layer
   q.naux_q = (L - 1) % q.nla == 0 ? q.naux - 1 : q.naux;
-  // as few replicas as carry B streams (up to 16 each), the streams spread evenly
-  const int per = q.nch + 1 + q.naux;
-  const int max_rep = WN_CHAIN_GRID / per;
-  const int nrep = (B + GC - 1) / GC;
-  if (nrep > max_rep) return false;
+  // Paired columns (8 streams per replica, one head CU) while their replicas carry the batch, else
+  // 16 streams per replica (two head CUs); WN_MFMA_COLUMNS=16 forces the latter.  As few replicas as
+  // carry B streams, the streams spread evenly.
+  const char* ce = std::getenv("WN_MFMA_COLUMNS");
+  const bool force16 = ce && std::atoi(ce) == 16;
+  int per = 0, nrep = 0;
+  q.pair = 0;
+  for (int pair = force16 ? 0 : 1; pair >= 0; --pair) {
+    const int ns = pair ? 8 : 16;
+    per = q.nch + (pair ? 1 : 2) + q.naux;
+    nrep = (B + ns - 1) / ns;
+    if (nrep <= WN_CHAIN_GRID / per) {
+      q.pair = pair;
+      break;
+    }
+    nrep = 0;
+  }
+  if (nrep == 0) return false;
+  const int NS = q.pair ? 8 : 16, NH = q.pair ? 1 : 2;
   q.G = (B + nrep - 1) / nrep;
   q.nrep = (B + q.G - 1) / q.G;
   q.ub = 0;
-  // mailboxes of one replica, in words: pre [L][2][PW] at 0, h [L][2][XW], skip partials
-  // [naux][2][S GC], the tail's [2][S GC], x [nch][2][XW]
-  const long long qw = (long long)S_ * GC;
-  q.off_h = L * 2 * PW;
-  q.off_q = q.off_h + L * 2 * XW;
+  // mailboxes of one replica, in words: pre [L][2][2R NS] at 0, h [L][2][R NS], skip partials
+  // [naux][2][S NS], the tail's [2][S NS], x [nch][2][R NS]
+  const long long xw = (long long)R * NS, pw = 2 * xw, qw = (long long)S_ * NS;
+  q.off_h = (int)(L * 2 * pw);
+  q.off_q = (int)(q.off_h + L * 2 * xw);
   q.off_qtail = (int)(q.off_q + q.naux * 2 * qw);
   q.off_x = (int)(q.off_qtail + 2 * qw);
   q.off_logit = 0;
-  q.mb_words = ((long long)q.off_x + q.nch * 2 * XW + 31) / 32 * 32;
-  // Placement: slot i of XCD x is block 8 i + x.  Each replica's chain CUs and head go to its home
+  q.mb_words = ((long long)q.off_x + q.nch * 2 * xw + 31) / 32 * 32;
+  // Placement: slot i of XCD x is block 8 i + x.  Each replica's chain CUs and head CUs go to its home
   // XCD first, then its aux CUs, last layers first, overflowing to the XCD with the most room.
   int used[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   constexpr int per_xcd = WN_CHAIN_GRID / 8;
@@ -1088,12 +1289,14 @@ bool wn_mchain_plan(int L, int R_, int S_, int B, WnChainPlan* p) {
     ++used[x];
   };
   for (int k = 0; k < q.nrep; ++k)
-    for (int r = 0; r <= q.nch; ++r) place(k * per + r, k % 8);
+    for (int r = 0; r < q.nch + NH; ++r) place(k * per + r, k % 8);
   for (int k = 0; k < q.nrep; ++k)
-    for (int a = q.naux - 1; a >= 0; --a) place(k * per + q.nch + 1 + a, k % 8);
+    for (int a = q.naux - 1; a >= 0; --a) place(k * per + q.nch + NH + a, k % 8);
   *p = q;
   return true;
 }
+
+int wn_mchain_columns(const WnChainPlan& p) { return p.pair ? 8 : 16; }
 
 hipError_t wn_mchain_launch(const WnChainArgs& g, bool teacher, hipStream_t stream) {
   if (g.d.R == R && g.d.S == 256) return launch_mchain_s<256>(g, teacher, stream);

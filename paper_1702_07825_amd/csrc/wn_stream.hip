@@ -43,11 +43,6 @@ __device__ __forceinline__ float4 ld4(const uint16_t* p) {
   return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
                      __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u));
 }
-// four int8 codes (the row's scale is applied to the row's dot product)
-__device__ __forceinline__ float4 ld4(const int8_t* p) {
-  const int v = *reinterpret_cast<const int*>(p);
-  return make_float4((float)((v << 24) >> 24), (float)((v << 16) >> 24), (float)((v << 8) >> 24), (float)(v >> 24));
-}
 // Scale of row `row` of a matrix stored as WT: the int8 codes' per-row scale, else 1.
 template <typename WT>
 __device__ __forceinline__ float row_scale(const float* s, size_t row) {

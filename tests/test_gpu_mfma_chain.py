@@ -1,5 +1,6 @@
-"""GPU parity of the multi-CU MFMA kernel (bf16 and int8 weights, r = 64): up to 16 streams per
-replica carried together through chain CUs with resident weights.
+"""GPU parity of the multi-CU MFMA kernel (bf16 and int8 weights, r = 64): the streams of a replica
+carried together through chain CUs with resident weights, 8 per replica in paired columns (the
+default) or 16, one per column (WN_MFMA_COLUMNS=16, the layout of the largest batches).
 
 Each case runs through the C ABI and is compared with the CPU oracle in the matching weight mode
 (bf16, or int8 with its quantization rule): teacher-forced logits within 1e-3, sample indices
@@ -7,8 +8,8 @@ bit-exact wherever the oracle's CDF margin exceeds 1e-4; with the fp32 oracle wi
 models.  Cases cover one stream, a full replica of 16, several replicas with a partial one, the
 fewest layers, every dilation 1 (histories read in the step they are written), dilations longer
 than the call, 40 layers (four chain CUs), int8 weights with a zero row, two taps, and calls split
-at odd steps (one-shot and chunked runs agree bit for bit).  The batched MFMA kernel (one CU per
-group of streams) agrees with it to rounding on the same inputs.
+at odd steps (one-shot and chunked runs agree bit for bit), in both column layouts.  The batched
+MFMA kernel (one CU per group of streams) agrees with it to rounding on the same inputs.
 """
 import zlib
 
@@ -30,28 +31,38 @@ def _log(msg):
 
 
 CASES = [
-    # name, L, dilations, B, T, dtype, bias, taps
-    ("l20_b1", 20, tuple(synth.dilation_cycle(20)), 1, 300, "bf16", 0.1, 1),
-    ("l20_b16", 20, tuple(synth.dilation_cycle(20)), 16, 200, "bf16", 0.2, 1),
-    ("l20_b37", 20, tuple(synth.dilation_cycle(20)), 37, 120, "bf16", 0.0, 1),
-    ("l2_d1_b1", 2, (1, 1), 1, 300, "bf16", 0.3, 1),
-    ("l3_d1_b3", 3, (1, 1, 1), 3, 200, "bf16", 0.2, 1),
-    ("l5_b5", 5, (1, 3, 9, 2, 4), 5, 150, "bf16", 0.4, 1),
-    ("long_dilations_b2", 4, (700, 1, 300, 2), 2, 800, "bf16", 0.2, 1),
-    ("l40_b20", 40, tuple(synth.dilation_cycle(40)), 20, 60, "bf16", 0.0, 1),
-    ("l20_2tap_b3", 20, tuple(synth.dilation_cycle(20)), 3, 150, "bf16", 0.1, 2),
-    ("i8_l20_b3", 20, tuple(synth.dilation_cycle(20)), 3, 200, "i8", 0.2, 1),
-    ("i8_l9_b17", 9, (1, 1, 2, 1, 8, 1, 3, 1, 2), 17, 120, "i8", 0.3, 1),
+    # name, L, dilations, B, T, dtype, bias, taps, columns (8: paired, 16: one stream per column)
+    ("l20_b1", 20, tuple(synth.dilation_cycle(20)), 1, 300, "bf16", 0.1, 1, 8),
+    ("l20_b16", 20, tuple(synth.dilation_cycle(20)), 16, 200, "bf16", 0.2, 1, 8),
+    ("l20_b37", 20, tuple(synth.dilation_cycle(20)), 37, 120, "bf16", 0.0, 1, 8),
+    ("l2_d1_b1", 2, (1, 1), 1, 300, "bf16", 0.3, 1, 8),
+    ("l3_d1_b3", 3, (1, 1, 1), 3, 200, "bf16", 0.2, 1, 8),
+    ("l5_b5", 5, (1, 3, 9, 2, 4), 5, 150, "bf16", 0.4, 1, 8),
+    ("long_dilations_b2", 4, (700, 1, 300, 2), 2, 800, "bf16", 0.2, 1, 8),
+    ("l40_b20", 40, tuple(synth.dilation_cycle(40)), 20, 60, "bf16", 0.0, 1, 8),
+    ("l20_2tap_b3", 20, tuple(synth.dilation_cycle(20)), 3, 150, "bf16", 0.1, 2, 8),
+    ("i8_l20_b3", 20, tuple(synth.dilation_cycle(20)), 3, 200, "i8", 0.2, 1, 8),
+    ("i8_l9_b17", 9, (1, 1, 2, 1, 8, 1, 3, 1, 2), 17, 120, "i8", 0.3, 1, 8),
+    ("c16_l20_b16", 20, tuple(synth.dilation_cycle(20)), 16, 200, "bf16", 0.2, 1, 16),
+    ("c16_l20_b37", 20, tuple(synth.dilation_cycle(20)), 37, 120, "bf16", 0.0, 1, 16),
+    ("c16_l3_d1_b3", 3, (1, 1, 1), 3, 200, "bf16", 0.2, 1, 16),
+    ("c16_l40_b20", 40, tuple(synth.dilation_cycle(40)), 20, 60, "bf16", 0.0, 1, 16),
+    ("c16_l20_2tap_b3", 20, tuple(synth.dilation_cycle(20)), 3, 150, "bf16", 0.1, 2, 16),
+    ("c16_i8_l9_b17", 9, (1, 1, 2, 1, 8, 1, 3, 1, 2), 17, 120, "i8", 0.3, 1, 16),
 ]
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_mfma_chain_parity(case, monkeypatch):
     import paper_1702_07825_amd as wn
-    name, L, dil, B, T, dtype, bias, taps = case
+    name, L, dil, B, T, dtype, bias, taps, cols = case
     seed = zlib.crc32(name.encode()) % 1000
-    _log("multi-CU MFMA case %s: L=%d B=%d T=%d %s taps=%d" % (name, L, B, T, dtype, taps))
+    _log("multi-CU MFMA case %s: L=%d B=%d T=%d %s taps=%d columns=%d" % (name, L, B, T, dtype, taps, cols))
     monkeypatch.setenv("WN_KERNEL", KERNEL)
+    if cols == 16:
+        monkeypatch.setenv("WN_MFMA_COLUMNS", "16")
+    else:
+        monkeypatch.delenv("WN_MFMA_COLUMNS", raising=False)
     w = synth.make_weights(L, 64, 256, seed=seed, bias_scale=bias, embed_taps=taps)
     if dtype == "i8":
         w["w_res"][0, 3] = 0.0  # a row of zeros: scale 0
@@ -113,15 +124,22 @@ def test_mfma_chain_parity(case, monkeypatch):
 
 
 def test_mfma_chain_launch_layout(monkeypatch):
-    """Replicas of up to 16 streams: l = 20 takes 2 chain CUs, 1 head and 4 aux CUs per replica."""
+    """l = 20: replicas of up to 8 streams in paired columns take 2 chain CUs, 1 head CU and 4 aux
+    CUs (up to 36 replicas); larger batches take replicas of up to 16 streams, 2 chain, 2 head and 4
+    aux CUs each (up to 32)."""
     import paper_1702_07825_amd as wn
     monkeypatch.setenv("WN_KERNEL", KERNEL)
+    monkeypatch.delenv("WN_MFMA_COLUMNS", raising=False)
     L = 20
     w = synth.make_weights(L, 64, 256, seed=3)
     net = wn.WaveNet(w, synth.dilation_cycle(L), weight_dtype="bf16")
-    for B, reps in ((1, 1), (16, 1), (17, 2), (256, 16)):
+    for B, cus in ((1, 7), (8, 7), (9, 14), (16, 14), (17, 21), (256, 224), (288, 252), (289, 152), (512, 256)):
         assert net.kernel_variant(B) == KERNEL
-        assert net.launch_info(B) == (7 * reps, reps)
+        assert net.launch_info(B)[0] == cus, B
+    assert net.kernel_variant(513) != KERNEL
+    monkeypatch.setenv("WN_MFMA_COLUMNS", "16")
+    for B, cus in ((1, 8), (17, 16), (256, 128)):
+        assert net.launch_info(B)[0] == cus, B
     net.close()
 
 
