@@ -129,11 +129,17 @@ int variant_for(const wn_handle* h, int B) {
   if (f == "multi_cu_mfma") return mchain_plan_for(h, B, &p) ? WN_VARIANT_MCHAIN : WN_VARIANT_STREAM;
   if (f == "multi_cu_chain") return chain_plan_for(h, B, &p) ? WN_VARIANT_CHAIN : WN_VARIANT_STREAM;
   if (f == "mfma_group") return h->group_ok ? WN_VARIANT_GROUP : WN_VARIANT_STREAM;
-  if (chain_plan_for(h, B, &p)) return WN_VARIANT_CHAIN;
-  // int8 batches beyond the fp32 multi-CU kernel's replicas: the MFMA one (2.5x the per-stream kernel
-  // at l = 20, B = 256)
-  if (h->dtype == WN_I8 && mchain_plan_for(h, B, &p)) return WN_VARIANT_MCHAIN;
-  return h->group_ok ? WN_VARIANT_GROUP : WN_VARIANT_STREAM;
+  // fp32 models: the fp32 multi-CU kernel while its replicas carry the batch.  bf16 and int8 models run
+  // it on their exact fp32 copy while a replica carries at most 3 streams, and the MFMA one beyond
+  // (measured at l = 20, r = 64: 15.4 / 16.3 / 18.6 us/step at 1 / 2 / 3 streams per replica and 30.8
+  // at 5, against a flat 20.8 (bf16) or 22.7 (int8) on the MFMA kernel and 24.9 on the batched one),
+  // then the batched kernel (bf16); the fp32 one again for the shapes that neither MFMA kernel serves.
+  const bool chain = chain_plan_for(h, B, &p);
+  if (chain && (h->dtype == WN_F32 || p.G <= 3)) return WN_VARIANT_CHAIN;
+  WnChainPlan q;
+  if (mchain_plan_for(h, B, &q)) return WN_VARIANT_MCHAIN;
+  if (h->group_ok) return WN_VARIANT_GROUP;
+  return chain ? WN_VARIANT_CHAIN : WN_VARIANT_STREAM;
 }
 
 // Workspace: status word, per-stream state, then either fp32 histories (per-stream and batched
@@ -478,19 +484,21 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
   }
   h->w.approx_nl = c->nonlinearity == WN_NONLIN_PAPER ? 1 : 0;
 
-  // The multi-CU kernels need one CU per block of their grid: the fp32 one fp32 or int8 weights, the
-  // MFMA one bf16 or int8 weights, each a supported shape.
+  // The multi-CU kernels need one CU per block of their grid and a supported shape: the fp32 one runs
+  // on fp32 weights (for bf16 and int8 models on an exact fp32 copy), the MFMA one on bf16 or int8
+  // weights.
   if (const char* force = std::getenv("WN_KERNEL")) h->force = force;
   const bool want_chain = h->force != "stream";
   int cus = 0, coop = 0;
   (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device);
   (void)hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, h->device);
-  if (want_chain && !bf && wn_chain_supported(R, S, L) && cus >= WN_CHAIN_GRID && coop) h->chain_ok = true;
+  if (want_chain && wn_chain_supported(R, S, L) && cus >= WN_CHAIN_GRID && coop) h->chain_ok = true;
   if (want_chain && (bf || i8) && wn_mchain_supported(R, S, L) && cus >= WN_CHAIN_GRID && coop) h->mchain_ok = true;
   if (h->chain_ok || h->mchain_ok) h->xcd_map = wn_chain_xcd_map_ok();
-  if (h->chain_ok && i8) {
-    // fp32 copies of the int8 matrices for the multi-CU kernel: each weight code * scale, rounded to
-    // fp32 once here (the per-stream kernel multiplies its row sums by the scale instead)
+  if (h->chain_ok && (i8 || bf)) {
+    // fp32 copies of the matrices for the multi-CU kernel: each bf16 weight (exact in fp32), or each
+    // int8 code * scale, rounded to fp32 once here (the per-stream kernel multiplies its row sums by
+    // the scale instead)
     size_t ftotal = 0;
     std::vector<size_t> foff(7);
     for (int k = 0; k < 7; ++k) {
@@ -499,9 +507,17 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
     }
     std::vector<float> fh(ftotal / 4, 0.f);
     for (int k = 0; k < 7; ++k) {
-      const int8_t* codes = reinterpret_cast<const int8_t*>(host.data() + arrs[k].off);
-      const float* scale = reinterpret_cast<const float*>(host.data() + arrs[k].soff);
-      for (size_t i = 0; i < arrs[k].n; ++i) fh[foff[k] / 4 + i] = (float)codes[i] * scale[i / arrs[k].cols];
+      if (bf) {
+        const uint16_t* bits = reinterpret_cast<const uint16_t*>(host.data() + arrs[k].off);
+        for (size_t i = 0; i < arrs[k].n; ++i) {
+          const uint32_t u = (uint32_t)bits[i] << 16;
+          std::memcpy(&fh[foff[k] / 4 + i], &u, 4);
+        }
+      } else {
+        const int8_t* codes = reinterpret_cast<const int8_t*>(host.data() + arrs[k].off);
+        const float* scale = reinterpret_cast<const float*>(host.data() + arrs[k].soff);
+        for (size_t i = 0; i < arrs[k].n; ++i) fh[foff[k] / 4 + i] = (float)codes[i] * scale[i / arrs[k].cols];
+      }
     }
     e = hipMalloc(&h->dmem_f32, ftotal);
     if (e == hipSuccess) e = hipMemcpy(h->dmem_f32, fh.data(), ftotal, hipMemcpyHostToDevice);
@@ -523,6 +539,7 @@ int wn_create(const wn_config* c, const wn_weights* w, wn_handle** out) {
     h->w_chain.w_relu = f + foff[5];
     h->w_chain.w_out = f + foff[6];
     h->w_chain.i8 = 0;
+    h->w_chain.bf16 = 0;
   }
   // The batched MFMA kernel needs bf16 weights, r = 64 and its LDS footprint on one CU.
   int lds_max = 0;

@@ -817,11 +817,15 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
                     [&](int) { return tag; }, [&](int, int q, float v) { qs[q >> 2][q & 3] += v; }, sy);
               }
             }
-            const bool loc = (lm >> 16) & 1u;
+            // a wait that gave up (a timeout or an abort) posts nothing: a partial without the previous
+            // one's share must not complete the head's sum (the block leaves at its next barrier)
+            if (!sy.failed()) {
+              const bool loc = (lm >> 16) & 1u;
 #pragma unroll
-            for (int k = 0; k < KS; ++k)
-              post4<PAIR>(mb + g.off_q + ((size_t)ai * 2 + par) * S * NS + lot(KS * wave + k), v4(qs[k]), tag, loc,
-                          part);
+              for (int k = 0; k < KS; ++k)
+                post4<PAIR>(mb + g.off_q + ((size_t)ai * 2 + par) * S * NS + lot(KS * wave + k), v4(qs[k]), tag, loc,
+                            part);
+            }
           }
         }
       }

@@ -22,6 +22,7 @@ CASES = [
     ("chain_l20_r64_b1", 20, 64, 256, 1, "f32", "multi_cu_chain", 200, 16000),
     ("chain_l20_r64_b3", 20, 64, 256, 3, "f32", "multi_cu_chain", 200, 16000),
     ("group_l20_bf16_b24", 20, 64, 256, 24, "bf16", "mfma_group", 200, 16000),
+    ("mfma_chain_l20_bf16_b9", 20, 64, 256, 9, "bf16", "multi_cu_mfma", 200, 16000),
 ]
 
 
@@ -36,9 +37,10 @@ def _setup(L, r, s, B, T, dtype, seed):
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
-def test_standing_request_stops_at_first_step(case):
+def test_standing_request_stops_at_first_step(case, monkeypatch):
     import paper_1702_07825_amd as wn
     name, L, r, s, B, dt, kern, T, _ = case
+    monkeypatch.setenv("WN_KERNEL", kern)
     print("abort case %s (standing request): L=%d r=%d B=%d T=%d" % (name, L, r, B, T), flush=True)
     net, cond, u = _setup(L, r, s, B, T, dt, seed=5)
     assert net.kernel_variant(B) == kern
@@ -60,9 +62,10 @@ def test_standing_request_stops_at_first_step(case):
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
-def test_request_during_a_call_stops_it(case):
+def test_request_during_a_call_stops_it(case, monkeypatch):
     import paper_1702_07825_amd as wn
     name, L, r, s, B, dt, kern, T, TL = case
+    monkeypatch.setenv("WN_KERNEL", kern)
     print("abort case %s (request while running): L=%d r=%d B=%d T=%d" % (name, L, r, B, TL), flush=True)
     net, cond, u = _setup(L, r, s, B, TL, dt, seed=6)
     ws = net.new_workspace(B)

@@ -28,7 +28,11 @@ CASES = [
     ("chain_l20_r64", "", "multi_cu_chain", 20, 64, 256, tuple(synth.dilation_cycle(20)), 1, 300, "f32", 0.2, 1),
     ("chain_l20_r128_b3_2tap", "", "multi_cu_chain", 20, 128, 256, tuple(synth.dilation_cycle(20)), 3, 100, "f32",
      0.1, 2),
-    ("group_l20_b5", "", "mfma_group", 20, 64, 256, tuple(synth.dilation_cycle(20)), 5, 140, "bf16", 0.2, 1),
+    ("group_l20_b5", "mfma_group", "mfma_group", 20, 64, 256, tuple(synth.dilation_cycle(20)), 5, 140, "bf16", 0.2, 1),
+    ("mfma_chain_l20_b9", "multi_cu_mfma", "multi_cu_mfma", 20, 64, 256, tuple(synth.dilation_cycle(20)), 9, 140,
+     "bf16", 0.2, 1),
+    ("mfma_chain_i8_l20_b17", "multi_cu_mfma", "multi_cu_mfma", 20, 64, 256, tuple(synth.dilation_cycle(20)), 17,
+     100, "i8", 0.2, 1),
     ("i8_l20_r64_b2", "", I8_KERNEL, 20, 64, 256, tuple(synth.dilation_cycle(20)), 2, 150, "i8", 0.2, 1),
 ]
 

@@ -21,6 +21,13 @@ pytestmark = pytest.mark.gpu
 MARGIN = 1e-4
 
 
+@pytest.fixture(autouse=True)
+def _group_kernel(monkeypatch):
+    # the batched kernel serves a bf16 model when selected by name (the default choice prefers the
+    # multi-CU kernels where their replicas carry the batch)
+    monkeypatch.setenv("WN_KERNEL", "mfma_group")
+
+
 def _log(msg):
     print(msg, flush=True)
 
@@ -142,15 +149,24 @@ def test_group_sizes_agree(B, monkeypatch):
     net16.close()
 
 
-def test_group_kernel_variant_selection():
+def test_group_kernel_variant_selection(monkeypatch):
     import paper_1702_07825_amd as wn
     w = synth.make_weights(20, 64, 256, seed=2)
+    monkeypatch.delenv("WN_KERNEL")
+    dflt = wn.WaveNet(w, synth.dilation_cycle(20), weight_dtype="bf16")
+    # the default: the fp32 multi-CU kernel (exact fp32 copy) up to 3 streams per replica, the MFMA
+    # multi-CU kernel while its replicas carry the batch, then this one
+    assert [dflt.kernel_variant(b) for b in (1, 16, 45)] == ["multi_cu_chain"] * 3
+    assert [dflt.kernel_variant(b) for b in (46, 256, 512)] == ["multi_cu_mfma"] * 3
+    assert [dflt.kernel_variant(b) for b in (513, 2048)] == ["mfma_group"] * 2
+    dflt.close()
+    monkeypatch.setenv("WN_KERNEL", "mfma_group")
     net = wn.WaveNet(w, synth.dilation_cycle(20), weight_dtype="bf16")
     assert [net.kernel_variant(b) for b in (1, 16, 256)] == ["mfma_group"] * 3
     # 8 streams per workgroup up to 2048 streams (one workgroup per CU), then 16
     assert [net.launch_info(b) for b in (1, 9, 256, 2048, 2049)] == [(1, 1), (2, 2), (32, 32), (256, 256), (129, 129)]
     net.close()
-    # one layer, or r other than 64, stays on the per-stream kernel
+    # one layer, or r other than 64, stays on the per-stream kernel when this one is asked for
     w1 = synth.make_weights(1, 64, 256, seed=2)
     net1 = wn.WaveNet(w1, (1,), weight_dtype="bf16")
     assert net1.kernel_variant(16) == "stream_l2"

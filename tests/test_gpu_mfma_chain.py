@@ -171,14 +171,18 @@ def test_mfma_chain_timeout_then_reset(monkeypatch):
     good.close()
 
 
-def test_int8_batches_beyond_the_fp32_chain_use_it(monkeypatch):
-    """int8 models: the fp32 multi-CU kernel (on the fp32 copy) while its replicas carry the batch,
-    this kernel beyond that (instead of the per-stream kernel)."""
+@pytest.mark.parametrize("dtype", ["bf16", "i8"])
+def test_default_choice(dtype, monkeypatch):
+    """bf16 and int8 models: the fp32 multi-CU kernel (on the exact fp32 copy) while its replicas
+    carry at most 3 streams each (l = 20: B <= 45), this kernel beyond that while its replicas carry
+    the batch (B <= 512), then the batched kernel (bf16) or the per-stream one (int8)."""
     import paper_1702_07825_amd as wn
     monkeypatch.delenv("WN_KERNEL", raising=False)
+    monkeypatch.delenv("WN_MFMA_COLUMNS", raising=False)
     L = 20
     w = synth.make_weights(L, 64, 256, seed=4)
-    net = wn.WaveNet(w, synth.dilation_cycle(L), weight_dtype="i8")
-    assert [net.kernel_variant(b) for b in (1, 240)] == ["multi_cu_chain"] * 2
-    assert [net.kernel_variant(b) for b in (241, 256)] == [KERNEL] * 2
+    net = wn.WaveNet(w, synth.dilation_cycle(L), weight_dtype=dtype)
+    assert [net.kernel_variant(b) for b in (1, 16, 45)] == ["multi_cu_chain"] * 3
+    assert [net.kernel_variant(b) for b in (46, 256, 512)] == [KERNEL] * 3
+    assert net.kernel_variant(513) == ("mfma_group" if dtype == "bf16" else "stream_l2")
     net.close()

@@ -238,15 +238,18 @@ WRAP = [
     ("chain_b3", 64, 256, 3, "f32", "multi_cu_chain"),
     ("chain_r128_b2", 128, 256, 2, "f32", "multi_cu_chain"),
     ("group_b9", 64, 256, 9, "bf16", "mfma_group"),
+    ("mfma_chain_b9", 64, 256, 9, "bf16", "multi_cu_mfma"),
+    ("mfma_chain_i8_b64", 64, 256, 64, "i8", "multi_cu_mfma"),
 ]
 
 
 @pytest.mark.parametrize("case", WRAP, ids=[c[0] for c in WRAP])
-def test_chunks_across_history_wraps(case):
+def test_chunks_across_history_wraps(case, monkeypatch):
     """l = 20 with dilations up to 512 over 1100 steps, in chunks whose boundaries straddle steps
     512 and 1024 (where the d = 512 histories wrap): chunked generation and teacher forcing equal
     the one-shot call bit for bit, and the one-shot call matches the oracle on every step."""
     name, r, s, B, dtype, kern = case
+    monkeypatch.setenv("WN_KERNEL", kern)
     L, T = 20, 1100
     dil = tuple(synth.dilation_cycle(L))
     _log("wrap case %s: L=%d r=%d B=%d T=%d" % (name, L, r, B, T))

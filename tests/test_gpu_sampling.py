@@ -27,6 +27,7 @@ MODELS = [
     ("l20_r64_chain_b1", 20, 64, 256, tuple(synth.dilation_cycle(20)), 1, 200, "f32", "multi_cu_chain"),
     ("l20_r128_chain_b11", 20, 128, 256, tuple(synth.dilation_cycle(20)), 11, 120, "f32", "multi_cu_chain"),
     ("l5_bf16_group_b17", 5, 64, 256, (1, 3, 9, 2, 4), 17, 150, "bf16", "mfma_group"),
+    ("l20_bf16_mfma_chain_b9", 20, 64, 256, tuple(synth.dilation_cycle(20)), 9, 150, "bf16", "multi_cu_mfma"),
 ]
 
 
@@ -42,8 +43,9 @@ def _setup(name, L, r, s, dil, B, T, dtype):
 
 
 @pytest.mark.parametrize("model", MODELS, ids=[m[0] for m in MODELS])
-def test_sampling_rules_match_the_oracle(model):
+def test_sampling_rules_match_the_oracle(model, monkeypatch):
     name, L, r, s, dil, B, T, dtype, kernel = model
+    monkeypatch.setenv("WN_KERNEL", kernel)
     w, net, cond, u, om = _setup(name, L, r, s, dil, B, T, dtype)
     assert net.kernel_variant(B) == kernel
     cond_np, u_np = cond.cpu().numpy(), u.cpu().numpy()

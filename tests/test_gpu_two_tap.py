@@ -29,8 +29,8 @@ CASES = [
     ("chain_l20_r64", "", "multi_cu_chain", 20, 64, 256, tuple(synth.dilation_cycle(20)), 1, 300, "f32", 0.1),
     ("chain_l20_r128_b3", "", "multi_cu_chain", 20, 128, 256, tuple(synth.dilation_cycle(20)), 3, 120, "f32", 0.0),
     ("chain_r32_b2", "", "multi_cu_chain", 6, 32, 128, (1, 2, 4, 8, 16, 32), 2, 200, "f32", 0.2),
-    ("group_l20_b5", "", "mfma_group", 20, 64, 256, tuple(synth.dilation_cycle(20)), 5, 140, "bf16", 0.1),
-    ("group_l40_b17", "", "mfma_group", 40, 64, 256, tuple(synth.dilation_cycle(40)), 17, 60, "bf16", 0.0),
+    ("group_l20_b5", "mfma_group", "mfma_group", 20, 64, 256, tuple(synth.dilation_cycle(20)), 5, 140, "bf16", 0.1),
+    ("group_l40_b17", "mfma_group", "mfma_group", 40, 64, 256, tuple(synth.dilation_cycle(40)), 17, 60, "bf16", 0.0),
     ("i8_l20_r64", "", I8_KERNEL, 20, 64, 256, tuple(synth.dilation_cycle(20)), 1, 200, "i8", 0.1),
     ("i8_stream_r16", "stream", "stream_l2", 3, 16, 32, (1, 2, 4), 2, 200, "i8", 0.3),
 ]
