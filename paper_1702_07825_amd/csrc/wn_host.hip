@@ -265,6 +265,7 @@ int launch(wn_handle* h, int B, int T, const float* cond, const float* u, const 
     g.naux = plan.naux;
     g.naux_q = plan.naux_q;
     g.pair = plan.pair;
+    for (int a = 0; a <= plan.naux; ++a) g.aux_begin[a] = plan.aux_begin[a];
     // posts to same-XCD readers stop at the XCD's L2 when the block -> XCD map is the expected
     // one; WN_LOCAL_POSTS=0 writes every post through
     const char* lp = std::getenv("WN_LOCAL_POSTS");

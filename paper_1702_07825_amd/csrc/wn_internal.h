@@ -119,6 +119,7 @@ struct WnChainArgs {
   int nla, naux, naux_q;         // layers per aux CU, aux CUs per replica, aux CUs posting a skip partial
   int local_posts;               // 1: posts to a reader on the same XCD stop at its L2
   int pair;                      // MFMA kernel: 1 = paired columns (8 streams per replica), 0 = 16 streams
+  int aux_begin[WN_MAX_LAYERS + 1];  // MFMA kernel: first layer of each aux CU (then L)
   uint16_t role_of_block[WN_CHAIN_GRID];  // replica * per_replica + role; 0xffff = idle block
 };
 
@@ -127,6 +128,7 @@ struct WnChainPlan {
   int nch, nrep, G, ub, tail_on_chain, pair;
   int nla, naux, naux_q;
   int layer_begin[WN_MAX_CHAIN + 1];
+  int aux_begin[WN_MAX_LAYERS + 1];
   uint16_t role_of_block[WN_CHAIN_GRID];
   long long mb_words;
   int off_h, off_q, off_x, off_logit, off_qtail;

@@ -599,7 +599,7 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
   const int n = lane & 15, quad = lane >> 4;
   const int sn = PAIR ? (n & 7) : n, part = PAIR ? (n >> 3) : 0;
   const int L = g.d.L, T = g.io.T;
-  const int ja = ai * g.nla, nl = min(g.nla, L - ja);
+  const int ja = g.aux_begin[ai], nl = g.aux_begin[ai + 1] - ja;  // nl <= NLA
   // layers whose skip projection this CU computes (the last layer's runs on the last chain CU)
   const int nsk = (g.tail_on_chain && ja + nl == L) ? nl - 1 : nl;
   const int b0 = rep * g.G, ns = min(g.G, g.io.B - b0);
@@ -775,7 +775,8 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
             sy);
         lds_barrier();
         if (sy.failed()) return;
-        if (l + 1 < NLA && l + 1 < nl) pairs_start(pw, rs, tid, lw_n(l + 1), lw_word(l + 1));
+        const bool posts = l == nsk - 1, more_l = l + 1 < NLA && l + 1 < nl;
+        if (more_l) pairs_start(pw, rs, tid, lw_n(l + 1), lw_word(l + 1));
         if (l < nsk) {
           // q += W_skip h_j, row tiles KS wave ..
           const u16* hh = HH + l * NS * SR + sn * SR;
@@ -796,36 +797,17 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
               qs[k] = acc;
             }
           }
-          // The partial goes out as soon as its last layer is in, with the previous aux CU's added: the
-          // partials of all but the last posting aux CU form a running sum, so the head waits for two
-          // of them (the last one is posted alone, to keep this wait off the end of the step).  A lane
-          // reads the previous partial's words it posts itself (same tiles and elements).
-          if (l == nsk - 1) {
+          // the partial goes out as soon as its last layer is in (the head sums the partials)
+          if (posts) {
             if constexpr (PAIR) {
 #pragma unroll
               for (int k = 0; k < KS; ++k) qs[k] = fold8(qs[k]);
             }
-            if (ai > 0 && ai < g.naux_q - 1) {
-              const unsigned pq = mbw + g.off_q + ((unsigned)(ai - 1) * 2 + par) * S * NS;
-              if constexpr (PAIR) {
-                poll_pairs<KS, 1>(
-                    g, rs, 0, KS, [&](int p) { return pq + lot(KS * wave + p) + 2 * part; }, [&](int) { return tag; },
-                    [&](int, int q, float v) { qs[q >> 1][2 * part + (q & 1)] += v; }, sy);
-              } else {
-                poll_pairs<2 * KS, 1>(
-                    g, rs, 0, 2 * KS, [&](int p) { return pq + lot(KS * wave + (p >> 1)) + 2 * (p & 1); },
-                    [&](int) { return tag; }, [&](int, int q, float v) { qs[q >> 2][q & 3] += v; }, sy);
-              }
-            }
-            // a wait that gave up (a timeout or an abort) posts nothing: a partial without the previous
-            // one's share must not complete the head's sum (the block leaves at its next barrier)
-            if (!sy.failed()) {
-              const bool loc = (lm >> 16) & 1u;
+            const bool loc = (lm >> 16) & 1u;
 #pragma unroll
-              for (int k = 0; k < KS; ++k)
-                post4<PAIR>(mb + g.off_q + ((size_t)ai * 2 + par) * S * NS + lot(KS * wave + k), v4(qs[k]), tag, loc,
-                            part);
-            }
+            for (int k = 0; k < KS; ++k)
+              post4<PAIR>(mb + g.off_q + ((size_t)ai * 2 + par) * S * NS + lot(KS * wave + k), v4(qs[k]), tag, loc,
+                          part);
           }
         }
       }
@@ -971,12 +953,11 @@ __device__ __forceinline__ void mc_head(const WnChainArgs& g, const int hh, cons
     stw(mb + g.off_x + (size_t)(tg0 & 1) * XW + tpos<NS>(m, c0 + q), pack(v, (unsigned)(tg0 + 1)), lm & 1u);
   }
 
-  // skip partials per step: the running sum of all aux CUs' but the last (posted by the one before
-  // the last), the last aux CU's own, and the last layer's from the last chain CU
-  const int nqa = g.naux_q >= 2 ? 2 : g.naux_q;
-  const int np = nqa + (g.tail_on_chain ? 1 : 0);
+  // skip partials per step: one from each aux CU that posts one, then the last layer's from the last
+  // chain CU, summed in that order
+  const int np = g.naux_q + (g.tail_on_chain ? 1 : 0);
   auto part_word = [&](int p, int par) -> unsigned {
-    if (p < nqa) return mbw + g.off_q + ((unsigned)(g.naux_q - nqa + p) * 2 + par) * QW;
+    if (p < g.naux_q) return mbw + g.off_q + ((unsigned)p * 2 + par) * QW;
     return mbw + g.off_qtail + (unsigned)par * QW;
   };
   // pair r (0 .. QP - 1) of a partial in my columns: with paired columns the whole partial; else tile
@@ -998,19 +979,24 @@ __device__ __forceinline__ void mc_head(const WnChainArgs& g, const int hh, cons
       if constexpr (TF) yv = g.io.y_in[at];
       else uv = g.io.u[at];
     }
-    // the skip partials of the step, my columns, all in one batch: pair p = tid + NT k is pair
-    // tid + NT (k mod NQP) of partial k / NQP, entries 2 (k mod NQP) (+ 1) of this thread, the same
-    // position in every partial, summed in partial order
+    // the skip partials of the step, my columns, in batches of up to three partials: the early ones
+    // while the chain still runs, then the last three (the aux CUs of the last layers and the chain's
+    // tail).  In a batch, pair p = tid + NT k is pair tid + NT (k mod NQP) of partial k / NQP, entries
+    // 2 (k mod NQP) (+ 1) of this thread, the same position in every partial.
     float qa[NQ];
 #pragma unroll
     for (int e = 0; e < NQ; ++e) qa[e] = 0.f;
-    {
+    for (int p0 = 0; p0 < np;) {
+      const int p1 = np - p0 <= 3 ? np : min(p0 + 3, np - 3);
       constexpr int KP = 3 * NQP;
       u32x4 w[KP];
-      auto word = [&](int p) { return part_word(p / QP, par) + pair_off(p % QP); };
-      pairs_start<KP>(w, rs, tid, np * QP, word);
+      auto word = [&](int p) { return part_word(p0 + p / QP, par) + pair_off(p % QP); };
+      pairs_start<KP>(w, rs, tid, (p1 - p0) * QP, word);
       pairs_finish<KP>(
-          g, w, rs, tid, np * QP, word, [&](int) { return tag; }, [&](int, int q, float v) { qa[q % NQ] += v; }, sy);
+          g, w, rs, tid, (p1 - p0) * QP, word, [&](int) { return tag; }, [&](int, int q, float v) { qa[q % NQ] += v; },
+          sy);
+      if (sy.failed()) break;
+      p0 = p1;
     }
     if (tid < HG) {
       if constexpr (TF) s_yin[tid] = yv < 0 ? 0 : (yv > A - 1 ? A - 1 : yv);
@@ -1130,7 +1116,7 @@ __global__ __launch_bounds__(NT, 1) void wn_mchain_kernel(const WnChainArgs ga) 
   extern __shared__ __align__(16) float dyn[];
   __shared__ int s_abort;
   __shared__ unsigned char s_xcd[WN_MAX_CHAIN + 2 + WN_MAX_LAYERS];
-  __shared__ unsigned char s_cof[WN_MAX_LAYERS];
+  __shared__ unsigned char s_cof[WN_MAX_LAYERS], s_aof[WN_MAX_LAYERS];
   __shared__ int s_me;
   const int rb = g.role_of_block[blockIdx.x];
   if (rb == 0xffff) return;
@@ -1149,24 +1135,25 @@ __global__ __launch_bounds__(NT, 1) void wn_mchain_kernel(const WnChainArgs ga) 
       const int r = g.role_of_block[b];
       if (r != 0xffff && r / per == k) s_xcd[r - k * per] = (unsigned char)ldw(g.xmap + b);
     }
-    // the chain CU of every layer (a loop over the layer split in the argument block here would make
-    // the compiler copy the whole block to scratch memory)
+    // the chain CU and the aux CU of every layer
     for (int c = threadIdx.x; c < g.nch; c += NT)
       for (int j = g.layer_begin[c]; j < g.layer_begin[c + 1]; ++j) s_cof[j] = (unsigned char)c;
+    for (int a = threadIdx.x; a < g.naux; a += NT)
+      for (int j = g.aux_begin[a]; j < g.aux_begin[a + 1]; ++j) s_aof[j] = (unsigned char)a;
     __syncthreads();
     const int me = s_me;
     auto same = [&](int r) { return s_xcd[r] == me; };
     const bool heads_same = same(head) && (C::NH == 1 || same(head + 1));
     if (role < head) {
       const int j0 = g.layer_begin[role], nl = g.layer_begin[role + 1] - j0;
-      for (int l = 0; l < nl; ++l) lm |= (unsigned)same(aux0 + (j0 + l) / g.nla) << l;
+      for (int l = 0; l < nl; ++l) lm |= (unsigned)same(aux0 + s_aof[j0 + l]) << l;
       if (role + 1 < g.nch) lm |= (unsigned)same(role + 1) << 16;
       lm |= (unsigned)heads_same << 17;
     } else if (role < aux0) {
       lm = same(0);
     } else {
-      const int ja = (role - aux0) * g.nla;
-      for (int l = 0; l < g.nla && ja + l < g.d.L; ++l) lm |= (unsigned)same(s_cof[ja + l]) << l;
+      const int ai = role - aux0, ja = g.aux_begin[ai];
+      for (int j = ja; j < g.aux_begin[ai + 1]; ++j) lm |= (unsigned)same(s_cof[j]) << (j - ja);
       lm |= (unsigned)heads_same << 16;
     }
   }
@@ -1188,6 +1175,26 @@ int mchain_split(int L, int* layer_begin) {
   layer_begin[0] = 0;
   for (int c = 0; c < nch; ++c) layer_begin[c + 1] = layer_begin[c] + base + (c < extra ? 1 : 0);
   return nch;
+}
+
+// Layers of each aux CU: uniform runs of nla, or front-loaded runs (the last two hold 2 and 3 layers,
+// the others NLA, the first the remainder), so that the aux CUs of the last layers, which trail the
+// chain by the most, have the fewest layers to catch up on.  Returns the number of aux CUs.
+int aux_split(int L, int nla, bool front, int* begin) {
+  int sizes[WN_MAX_LAYERS];
+  int n = 0;
+  if (front) {
+    for (int rem = L; rem > 0; ++n) {
+      sizes[n] = std::min(n == 0 ? 2 : (n == 1 ? 3 : NLA), rem);
+      rem -= sizes[n];
+    }
+    std::reverse(sizes, sizes + n);
+  } else {
+    for (int j = 0; j < L; j += nla) sizes[n++] = std::min(nla, L - j);
+  }
+  begin[0] = 0;
+  for (int a = 0; a < n; ++a) begin[a + 1] = begin[a] + sizes[a];
+  return n;
 }
 
 constexpr size_t kMaxLds = 160 * 1024;
@@ -1236,35 +1243,37 @@ bool wn_mchain_plan(int L, int R_, int S_, int B, WnChainPlan* p) {
   if (!p || B < 1 || !wn_mchain_supported(R_, S_, L)) return false;
   WnChainPlan q{};
   q.nch = mchain_split(L, q.layer_begin);
-  // layers per aux CU (an aux CU runs only the skip products in step with the chain, which keeps pace
-  // with it; fewer aux CUs mean fewer skip partials); WN_AUX_LAYERS=n forces n
-  q.nla = NLA;
-  if (const char* e = std::getenv("WN_AUX_LAYERS")) {
-    const int v = std::atoi(e);
-    if (v >= 1 && v <= NLA) q.nla = v;
-  }
-  q.naux = (L + q.nla - 1) / q.nla;
   q.tail_on_chain = 1;
-  // aux CUs that post a skip partial: all but one holding only the last layer
-  q.naux_q = (L - 1) % q.nla == 0 ? q.naux - 1 : q.naux;
-  // Paired columns (8 streams per replica, one head CU) while their replicas carry the batch, else
-  // 16 streams per replica (two head CUs); WN_MFMA_COLUMNS=16 forces the latter.  As few replicas as
-  // carry B streams, the streams spread evenly.
+  // Layouts in order of preference: paired columns (8 streams per replica, one head CU), then 16
+  // streams per replica (two head CUs; WN_MFMA_COLUMNS=16 forces it); each with front-loaded aux
+  // ranges, then uniform ones (WN_AUX_LAYERS=n forces uniform runs of n).  The first whose replicas
+  // carry B streams (as few replicas as do, the streams spread evenly) is taken.
   const char* ce = std::getenv("WN_MFMA_COLUMNS");
   const bool force16 = ce && std::atoi(ce) == 16;
+  int nla_forced = 0;
+  if (const char* e = std::getenv("WN_AUX_LAYERS")) {
+    const int v = std::atoi(e);
+    if (v >= 1 && v <= NLA) nla_forced = v;
+  }
   int per = 0, nrep = 0;
-  q.pair = 0;
-  for (int pair = force16 ? 0 : 1; pair >= 0; --pair) {
-    const int ns = pair ? 8 : 16;
-    per = q.nch + (pair ? 1 : 2) + q.naux;
-    nrep = (B + ns - 1) / ns;
-    if (nrep <= WN_CHAIN_GRID / per) {
-      q.pair = pair;
-      break;
+  for (int pair = force16 ? 0 : 1; pair >= 0 && nrep == 0; --pair) {
+    for (int front = nla_forced ? 0 : 1; front >= 0; --front) {
+      const int ns = pair ? 8 : 16;
+      q.naux = aux_split(L, nla_forced ? nla_forced : NLA, front != 0, q.aux_begin);
+      per = q.nch + (pair ? 1 : 2) + q.naux;
+      const int nr = (B + ns - 1) / ns;
+      if (nr <= WN_CHAIN_GRID / per) {
+        q.pair = pair;
+        nrep = nr;
+        break;
+      }
     }
-    nrep = 0;
   }
   if (nrep == 0) return false;
+  q.nla = 0;
+  for (int a = 0; a < q.naux; ++a) q.nla = std::max(q.nla, q.aux_begin[a + 1] - q.aux_begin[a]);
+  // aux CUs that post a skip partial: all but one holding only the last layer
+  q.naux_q = q.aux_begin[q.naux - 1] == L - 1 ? q.naux - 1 : q.naux;
   const int NS = q.pair ? 8 : 16, NH = q.pair ? 1 : 2;
   q.G = (B + nrep - 1) / nrep;
   q.nrep = (B + q.G - 1) / q.G;

@@ -1,6 +1,7 @@
 """GPU parity of the multi-CU MFMA kernel (bf16 and int8 weights, r = 64): the streams of a replica
 carried together through chain CUs with resident weights, 8 per replica in paired columns (the
-default) or 16, one per column (WN_MFMA_COLUMNS=16, the layout of the largest batches).
+default) or 16, one per column (WN_MFMA_COLUMNS=16, the layout of the largest batches), with
+front-loaded aux layer runs (the default) or uniform ones (WN_AUX_LAYERS=5).
 
 Each case runs through the C ABI and is compared with the CPU oracle in the matching weight mode
 (bf16, or int8 with its quantization rule): teacher-forced logits within 1e-3, sample indices
@@ -49,6 +50,10 @@ CASES = [
     ("c16_l40_b20", 40, tuple(synth.dilation_cycle(40)), 20, 60, "bf16", 0.0, 1, 16),
     ("c16_l20_2tap_b3", 20, tuple(synth.dilation_cycle(20)), 3, 150, "bf16", 0.1, 2, 16),
     ("c16_i8_l9_b17", 9, (1, 1, 2, 1, 8, 1, 3, 1, 2), 17, 120, "i8", 0.3, 1, 16),
+    # uniform aux runs of 5 layers (the layout of batches whose front-loaded replicas do not fit)
+    ("u5_l20_b16", 20, tuple(synth.dilation_cycle(20)), 16, 200, "bf16", 0.2, 1, 8),
+    ("u5_i8_l20_b37", 20, tuple(synth.dilation_cycle(20)), 37, 120, "i8", 0.1, 1, 8),
+    ("u5_c16_l20_b17", 20, tuple(synth.dilation_cycle(20)), 17, 120, "bf16", 0.1, 1, 16),
 ]
 
 
@@ -63,6 +68,10 @@ def test_mfma_chain_parity(case, monkeypatch):
         monkeypatch.setenv("WN_MFMA_COLUMNS", "16")
     else:
         monkeypatch.delenv("WN_MFMA_COLUMNS", raising=False)
+    if name.startswith("u5_"):
+        monkeypatch.setenv("WN_AUX_LAYERS", "5")
+    else:
+        monkeypatch.delenv("WN_AUX_LAYERS", raising=False)
     w = synth.make_weights(L, 64, 256, seed=seed, bias_scale=bias, embed_taps=taps)
     if dtype == "i8":
         w["w_res"][0, 3] = 0.0  # a row of zeros: scale 0
@@ -124,21 +133,28 @@ def test_mfma_chain_parity(case, monkeypatch):
 
 
 def test_mfma_chain_launch_layout(monkeypatch):
-    """l = 20: replicas of up to 8 streams in paired columns take 2 chain CUs, 1 head CU and 4 aux
-    CUs (up to 36 replicas); larger batches take replicas of up to 16 streams, 2 chain, 2 head and 4
-    aux CUs each (up to 32)."""
+    """l = 20: replicas of up to 8 streams in paired columns take 2 chain CUs, 1 head CU and 5 aux CUs
+    (front-loaded layer runs 5, 5, 5, 3, 2) while 8 CUs per replica fit the chip (32 replicas), else
+    4 aux CUs of 5 layers (up to 36 replicas); larger batches take replicas of up to 16 streams with
+    2 chain, 2 head and 5 or 4 aux CUs (up to 32 replicas)."""
     import paper_1702_07825_amd as wn
     monkeypatch.setenv("WN_KERNEL", KERNEL)
     monkeypatch.delenv("WN_MFMA_COLUMNS", raising=False)
+    monkeypatch.delenv("WN_AUX_LAYERS", raising=False)
     L = 20
     w = synth.make_weights(L, 64, 256, seed=3)
     net = wn.WaveNet(w, synth.dilation_cycle(L), weight_dtype="bf16")
-    for B, cus in ((1, 7), (8, 7), (9, 14), (16, 14), (17, 21), (256, 224), (288, 252), (289, 152), (512, 256)):
+    for B, cus in ((1, 8), (8, 8), (9, 16), (16, 16), (17, 24), (256, 256), (257, 231), (288, 252), (289, 171),
+                   (512, 256)):
         assert net.kernel_variant(B) == KERNEL
         assert net.launch_info(B)[0] == cus, B
     assert net.kernel_variant(513) != KERNEL
     monkeypatch.setenv("WN_MFMA_COLUMNS", "16")
-    for B, cus in ((1, 8), (17, 16), (256, 128)):
+    for B, cus in ((1, 9), (17, 18), (256, 144)):
+        assert net.launch_info(B)[0] == cus, B
+    monkeypatch.delenv("WN_MFMA_COLUMNS")
+    monkeypatch.setenv("WN_AUX_LAYERS", "5")
+    for B, cus in ((1, 7), (256, 224)):
         assert net.launch_info(B)[0] == cus, B
     net.close()
 
