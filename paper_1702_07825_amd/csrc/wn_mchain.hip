@@ -45,9 +45,12 @@
 // Messages are tagged 64-bit words (fp32 value, step + 1; see wn_msg.h) laid out in the MFMA
 // accumulator order: in a block of NS-column tiles (NS streams), word 16 NS tile + 4 (NS quad + c) +
 // e holds row 16 tile + 4 quad + e of column c, so the lanes that computed a tile post it as it lies
-// in their registers.  Mailboxes have two slots (step parity); every producer stays at most one step
-// ahead of its consumer.  The dilation histories are rings of such blocks: slot t mod d_j of layer
-// j holds x_{j-1}[t].  Every wait is bounded: a block that times out stores WN_ETIMEOUT in the
+// in their registers.  A mailbox has one slot: a producer writes step t + 1 only after something
+// that depends on its consumer's read of step t (the aux CU posts pre_j[t + 1] once h_j[t] is in,
+// which the chain posts after reading pre_j[t]; every role's step t + 1 needs x0[t + 1], which the
+// head posts after reading the skip partials of step t, the last of the step's messages), and the
+// tags keep the steps apart.  The dilation histories are rings of such blocks: slot t mod d_j of
+// layer j holds x_{j-1}[t].  Every wait is bounded: a block that times out stores WN_ETIMEOUT in the
 // status word, and every other block sees it in its next wait and leaves, so the grid always drains.
 #include "wn_internal.h"
 #include "wn_mfma.h"
@@ -477,14 +480,13 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
   float4 xr = make_float4(0.f, 0.f, 0.f, 0.f);      // x_{j-1}[t], rows m0 .. m0 + 3 of stream sn, fp32
   for (int64_t t = tg0; t < tg0 + T; ++t) {
     const unsigned tag = (unsigned)(t + 1);
-    const int par = (int)(t & 1);
     // the pre-activations of my layers (posted by their aux CUs during the previous step), then the
     // input x: from the previous chain CU, or for chain CU 0 the head's x0
-    const unsigned pre_w = mbw + ((unsigned)j0 * 2 + par) * PW;
+    const unsigned pre_w = mbw + (unsigned)j0 * PW;
     poll_pairs<16, NT, 16>(
-        g, rs, tid, nl * PW / 2, [&](int p) { return pre_w + (unsigned)((2 * p) / PW) * 2 * PW + (2 * p) % PW; },
+        g, rs, tid, nl * PW / 2, [&](int p) { return pre_w + 2 * p; },
         [&](int) { return tag; }, [&](int i, int, float v) { PRE[i] = v; }, sy);
-    const unsigned x_w = mbw + g.off_x + ((unsigned)c * 2 + par) * XW;
+    const unsigned x_w = mbw + g.off_x + (unsigned)c * XW;
     poll_pairs<XW / 2 / NT>(
         g, rs, tid, XW / 2, [&](int p) { return x_w + 2 * p; }, [&](int) { return tag; },
         [&](int i, int, float v) {
@@ -526,7 +528,7 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
           const float4 h = gate4<AX, PAIR>(at, ag, part);
           put_split4<PAIR>(HS + sn * SR, m0, h, part);
           // h_j[t] -> the layer's aux CU (with paired columns lane n posts h, lane n + 8 the history row)
-          u64* const hpost = mb + g.off_h + ((size_t)j * 2 + par) * XW + ot;
+          u64* const hpost = mb + g.off_h + (size_t)j * XW + ot;
           if constexpr (PAIR) stw4(p0 ? hpost : hist, p0 ? h : xr, tag, (lm >> l) & 1u);
           else stw4(hpost, h, tag, (lm >> l) & 1u);
         }
@@ -548,7 +550,7 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
           put_split4<PAIR>(XS + ((l + 1) & 1) * NS * SR + sn * SR, m0, xr, part);
           if (l == nl - 1 && c + 1 < g.nch) {
             // x of my last layer -> the next chain CU
-            post4<PAIR>(mb + g.off_x + ((size_t)(c + 1) * 2 + par) * XW + ot, xr, tag, (lm >> 16) & 1u, part);
+            post4<PAIR>(mb + g.off_x + (size_t)(c + 1) * XW + ot, xr, tag, (lm >> 16) & 1u, part);
           }
           lds_barrier();
         }
@@ -577,7 +579,7 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
           const float4 s4 = *reinterpret_cast<const float4*>(SSK + rt * 16 + 4 * quad);
           acc = f32x4{s4.x * acc[0], s4.y * acc[1], s4.z * acc[2], s4.w * acc[3]};
         }
-        post4<PAIR>(mb + g.off_qtail + (size_t)par * S * NS + rt * TW + (quad * NS + sn) * 4, v4(acc), tag,
+        post4<PAIR>(mb + g.off_qtail + rt * TW + (quad * NS + sn) * 4, v4(acc), tag,
                     (lm >> 17) & 1u, part);
       }
       lds_barrier();  // HS is rewritten in the next step's first layer
@@ -664,13 +666,15 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
   // (all_hist, the call's first step).  With d = 1 the row is written during step ts - 1 and is
   // waited for together with h_j.
   auto stage = [&](int64_t ts, bool all_hist) __attribute__((always_inline)) {
-    float4 cq[NLA][CQ];
+    // each row is read once: non-temporal loads, so that the stream does not evict the mailboxes
+    f32x4 cq[NLA][CQ];
     const float* crow = cbase + ((size_t)(ts - tg0) * L + ja) * 2 * R;
 #pragma unroll
     for (int l = 0; l < NLA; ++l)
 #pragma unroll
       for (int k = 0; k < CQ; ++k)
-        cq[l][k] = l < nl ? *reinterpret_cast<const float4*>(crow + cq_src[k] + l * 2 * R) : make_float4(0.f, 0.f, 0.f, 0.f);
+        cq[l][k] = l < nl ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(crow + cq_src[k] + l * 2 * R))
+                          : f32x4{0.f, 0.f, 0.f, 0.f};
     if (tid == 0) {
       int nh = 0;
 #pragma unroll
@@ -695,7 +699,7 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
     for (int l = 0; l < NLA; ++l)
 #pragma unroll
       for (int k = 0; k < CQ; ++k)
-        if (l < nl && cq_on[k]) *reinterpret_cast<float4*>(CD + l * PW + cq_dst[k]) = cq[l][k];
+        if (l < nl && cq_on[k]) *reinterpret_cast<f32x4*>(CD + l * PW + cq_dst[k]) = cq[l][k];
     lds_barrier();
   };
   // pre_j[ts] = W_prev x_{j-1}[ts - d] + B + L[b, ts, j] of row tiles 2 wave, 2 wave + 1, j = ja + l,
@@ -721,7 +725,7 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
       } else {
         v = make_float4(acc[0] + b.x + cd.x, acc[1] + b.y + cd.y, acc[2] + b.z + cd.z, acc[3] + b.w + cd.w);
       }
-      post4<PAIR>(mb + ((size_t)(ja + l) * 2 + (ts & 1)) * PW + lot(rt), v, tg, loc, part);
+      post4<PAIR>(mb + (size_t)(ja + l) * PW + lot(rt), v, tg, loc, part);
     }
   };
 
@@ -732,7 +736,6 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
     if (l < nl) post_pre(l, tg0);
   for (int64_t t = tg0; t < tg0 + T; ++t) {
     const bool more = t + 1 < tg0 + T;
-    const int par = (int)(t & 1);
     const unsigned tag = (unsigned)(t + 1);
     // A host abort request, read every WN_ABORT_CHECK steps by the replica's first aux CU, which works
     // a step ahead of the chain (the read's PCIe round trip stays off the critical path); every other
@@ -757,7 +760,7 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
     // layer's products, so their round trip overlaps them.
     auto lw_n = [&](int l) { return (more && dl[l] == 1) ? XW : XW / 2; };  // pairs
     auto lw_word = [&](int l) {
-      const unsigned hw = mbw + g.off_h + ((unsigned)(ja + l) * 2 + par) * XW;
+      const unsigned hw = mbw + g.off_h + (unsigned)(ja + l) * XW;
       const unsigned xw = rgw + (unsigned)ho[l] * NS;
       return [=](int p) { return 2 * p < XW ? hw + 2 * p : xw + (2 * p - XW); };
     };
@@ -806,7 +809,7 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
             const bool loc = (lm >> 16) & 1u;
 #pragma unroll
             for (int k = 0; k < KS; ++k)
-              post4<PAIR>(mb + g.off_q + ((size_t)ai * 2 + par) * S * NS + lot(KS * wave + k), v4(qs[k]), tag, loc,
+              post4<PAIR>(mb + g.off_q + (size_t)ai * S * NS + lot(KS * wave + k), v4(qs[k]), tag, loc,
                           part);
           }
         }
@@ -854,7 +857,7 @@ template <int S, bool TF, bool AX, bool I8, bool PAIR>
 __device__ __forceinline__ void mc_head(const WnChainArgs& g, const int hh, const int rep, float* dyn, Sync sy,
                                         const int64_t tg0, const unsigned lm) {
   using C = Cols<PAIR>;
-  constexpr int NS = C::NS, XW = C::XW;
+  constexpr int NS = C::NS;
   constexpr int KTH = S / 32, KTO = A / 32;
   constexpr int SS = 2 * S + 8, SA = 2 * A + 8, PA = A + 4;
   constexpr int QW = S * NS;           // words of a skip partial
@@ -950,15 +953,15 @@ __device__ __forceinline__ void mc_head(const WnChainArgs& g, const int hh, cons
       v = emb(EMB, SE, s_y[q], m) + BE[m];
       if (e2 && s_y2[q] >= 0) v += emb(EMBP, SEP, s_y2[q], m);
     }
-    stw(mb + g.off_x + (size_t)(tg0 & 1) * XW + tpos<NS>(m, c0 + q), pack(v, (unsigned)(tg0 + 1)), lm & 1u);
+    stw(mb + g.off_x + tpos<NS>(m, c0 + q), pack(v, (unsigned)(tg0 + 1)), lm & 1u);
   }
 
   // skip partials per step: one from each aux CU that posts one, then the last layer's from the last
   // chain CU, summed in that order
   const int np = g.naux_q + (g.tail_on_chain ? 1 : 0);
-  auto part_word = [&](int p, int par) -> unsigned {
-    if (p < g.naux_q) return mbw + g.off_q + ((unsigned)p * 2 + par) * QW;
-    return mbw + g.off_qtail + (unsigned)par * QW;
+  auto part_word = [&](int p) -> unsigned {
+    if (p < g.naux_q) return mbw + g.off_q + (unsigned)p * QW;
+    return mbw + g.off_qtail;
   };
   // pair r (0 .. QP - 1) of a partial in my columns: with paired columns the whole partial; else tile
   // r / 64, run (i / 8, c0 + i mod 8) with i = (r / 2) mod 32, words 2 (r mod 2), + 1 of that run
@@ -969,7 +972,6 @@ __device__ __forceinline__ void mc_head(const WnChainArgs& g, const int hh, cons
   };
   for (int64_t t = tg0; t < tg0 + T; ++t) {
     const unsigned tag = (unsigned)(t + 1);
-    const int par = (int)(t & 1);
     const bool more = t + 1 < tg0 + T;
     // this step's uniform (or teacher-forced sample) of each stream, staged after the wait below
     float uv = 0.f;
@@ -990,7 +992,7 @@ __device__ __forceinline__ void mc_head(const WnChainArgs& g, const int hh, cons
       const int p1 = np - p0 <= 3 ? np : min(p0 + 3, np - 3);
       constexpr int KP = 3 * NQP;
       u32x4 w[KP];
-      auto word = [&](int p) { return part_word(p0 + p / QP, par) + pair_off(p % QP); };
+      auto word = [&](int p) { return part_word(p0 + p / QP) + pair_off(p % QP); };
       pairs_start<KP>(w, rs, tid, (p1 - p0) * QP, word);
       pairs_finish<KP>(
           g, w, rs, tid, (p1 - p0) * QP, word, [&](int) { return tag; }, [&](int, int q, float v) { qa[q % NQ] += v; },
@@ -1083,7 +1085,7 @@ __device__ __forceinline__ void mc_head(const WnChainArgs& g, const int hh, cons
           v = emb(EMB, SE, y, lane) + BE[lane];
           if (e2) v += emb(EMBP, SEP, yp, lane);
         }
-        stw(mb + g.off_x + (size_t)((t + 1) & 1) * XW + tpos<NS>(lane, c0 + q), pack(v, tag + 1), lm & 1u);
+        stw(mb + g.off_x + tpos<NS>(lane, c0 + q), pack(v, tag + 1), lm & 1u);
       }
       if (lane == 0 && q < ns) {
         s_y2[q] = yp;
@@ -1278,15 +1280,15 @@ bool wn_mchain_plan(int L, int R_, int S_, int B, WnChainPlan* p) {
   q.G = (B + nrep - 1) / nrep;
   q.nrep = (B + q.G - 1) / q.G;
   q.ub = 0;
-  // mailboxes of one replica, in words: pre [L][2][2R NS] at 0, h [L][2][R NS], skip partials
-  // [naux][2][S NS], the tail's [2][S NS], x [nch][2][R NS]
+  // mailboxes of one replica (one slot each), in words: pre [L][2R NS] at 0, h [L][R NS], skip
+  // partials [naux][S NS], the tail's [S NS], x [nch][R NS]
   const long long xw = (long long)R * NS, pw = 2 * xw, qw = (long long)S_ * NS;
-  q.off_h = (int)(L * 2 * pw);
-  q.off_q = (int)(q.off_h + L * 2 * xw);
-  q.off_qtail = (int)(q.off_q + q.naux * 2 * qw);
-  q.off_x = (int)(q.off_qtail + 2 * qw);
+  q.off_h = (int)(L * pw);
+  q.off_q = (int)(q.off_h + L * xw);
+  q.off_qtail = (int)(q.off_q + q.naux * qw);
+  q.off_x = (int)(q.off_qtail + qw);
   q.off_logit = 0;
-  q.mb_words = ((long long)q.off_x + q.nch * 2 * xw + 31) / 32 * 32;
+  q.mb_words = ((long long)q.off_x + q.nch * xw + 31) / 32 * 32;
   // Placement: slot i of XCD x is block 8 i + x.  Each replica's chain CUs and head CUs go to its home
   // XCD first, then its aux CUs, last layers first, overflowing to the XCD with the most room.
   int used[8] = {0, 0, 0, 0, 0, 0, 0, 0};
