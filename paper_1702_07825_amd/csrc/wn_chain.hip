@@ -25,10 +25,13 @@
 // Messages between CUs are vectors of 64-bit words (fp32 value in the low half,
 // step + 1 in the high half) written and read with relaxed agent-scope atomics.
 // Every word carries its own step tag, so a reader needs no fence: it re-reads a
-// word until the tag it expects appears.  Each mailbox has two slots (step
-// parity); the dependency chain keeps every producer at most one step ahead of
-// its consumer.  The dilation histories are rings of tagged words in the
-// workspace: slot (t mod d) of layer j holds x_{j-1}[t] tagged t + 1.
+// word until the tag it expects appears.  Each mailbox has one slot: per stream, a
+// producer writes step t + 1 only after something that depends on its consumer's
+// read of step t (an aux CU posts pre_j[t + 1] once h_j[t] is in, which the chain
+// posts after reading pre_j[t]; every role's step t + 1 needs chain CU 0's draw of
+// step t, which reads the head's logits, which need every skip partial of step t),
+// and the tags keep the steps apart.  The dilation histories are rings of tagged
+// words in the workspace: slot (t mod d) of layer j holds x_{j-1}[t] tagged t + 1.
 //
 // Several streams: the roles above form one replica.  Up to 256 / (roles per replica) replicas
 // run side by side, each serving G streams, and every role of a replica takes its streams in
@@ -58,6 +61,7 @@ namespace {
 
 using namespace wnk;
 
+typedef float f4v __attribute__((ext_vector_type(4)));
 constexpr int NT = 512;
 constexpr int A = WN_A;
 constexpr int NHEAD = 4;
@@ -390,8 +394,7 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
   };
   // The head's partial logits of step ts of stream b (tag ts + 1).
   auto logit_items = [&](int64_t ts, int b) {
-    return Items{g.mb + (size_t)b * g.mb_words + g.off_logit + (size_t)(ts & 1) * A, A, 2 * A, NHEAD * A, lgp,
-                 (unsigned)(ts + 1)};
+    return Items{g.mb + (size_t)b * g.mb_words + g.off_logit, A, A, NHEAD * A, lgp, (unsigned)(ts + 1)};
   };
   // Move staged samples (steps before next0) to the output and stage the next block of inputs.
   auto roll_buffers = [&](int64_t next0) {
@@ -417,7 +420,7 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
       u64* const rings = g.ring + (size_t)b * g.d.hist_len;
       // ---- inputs of this step, all waited for together: the pre-activations of my layers, and
       //      either x from the previous chain CU or (chain CU 0) the previous step's partial logits ----
-      const Items pre_items{mbs + ((size_t)j0 * 2 + par) * 2 * R, 2 * R, 2 * 2 * R, nl * 2 * R, pre, tag};
+      const Items pre_items{mbs + (size_t)j0 * 2 * R, 2 * R, 2 * R, nl * 2 * R, pre, tag};
       if (first) {
         // two-tap embedding: the row of y_{t-2}, known since the previous step, from LDS; at
         // r = 128 from global memory before the wait for the previous step's logits (the empty
@@ -453,7 +456,7 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
           }
         }
       } else {
-        poll2(g, pre_items, Items{mbs + g.off_x + ((size_t)c * 2 + par) * R, R, R, R, xs, tag}, dyn, sy);
+        poll2(g, pre_items, Items{mbs + g.off_x + (size_t)c * R, R, R, R, xs, tag}, dyn, sy);
       }
       lds_barrier();
       if (sy.failed()) return;
@@ -477,12 +480,12 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
         // of the step loop (they would not fit in registers)
         asm volatile("" : "+v"(row));
         hpost[l % HPOST] = pack(h, tag);
-        stw(mbs + g.off_h + ((size_t)j * 2 + par) * R + row, hpost[l % HPOST], (lm >> l) & 1u);
+        stw(mbs + g.off_h + (size_t)j * R + row, hpost[l % HPOST], (lm >> l) & 1u);
       };
       // x of this CU's last layer -> the next chain CU, posted by the lanes that computed it
       const bool handoff = c + 1 < g.nch;
       auto post_x = [&](int row, float v) __attribute__((always_inline)) {
-        if (handoff) stw(mbs + g.off_x + ((size_t)(c + 1) * 2 + par) * R + row, pack(v, tag), (lm >> 16) & 1u);
+        if (handoff) stw(mbs + g.off_x + (size_t)(c + 1) * R + row, pack(v, tag), (lm >> 16) & 1u);
       };
 #pragma unroll
       for (int l = 0; l < NLC; ++l) {
@@ -639,7 +642,7 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
         const float q = xreduce8<RPG>(p, li);
         const int m = RPG * gq + (upper ? RPG / 2 : 0) + (RPG == 4 && (li & 2) ? 1 : 0);
         const int ks = (RPG == 4) ? (li & 1) : (li & 3);  // lanes holding the same row: post once
-        if (ks == 0) stw(mbs + g.off_qtail + (size_t)par * S + m, pack(q, tag), (lm >> 17) & 1u);
+        if (ks == 0) stw(mbs + g.off_qtail + m, pack(q, tag), (lm >> 17) & 1u);
       }
       // Then x_{j-1} of each layer into the history slot (t mod d_j) that layer j's aux CU reads
       // again at t + d_j (the next chain CU's x went out in the last layer).
@@ -735,7 +738,7 @@ __device__ void aux_role(const WnChainArgs& g, const int ai, const int b0, const
   // of the layers with d >= 2, which are final once step ts - d is over (with d = 1 the read waits for
   // the chain CU's step and is made per stream, together with h_j).
   auto stage = [&](int64_t ts, bool all_hist) {
-    float4 cq[NLA][CQ];
+    f4v cq[NLA][CQ];
 #pragma unroll
     for (int l = 0; l < NLA; ++l) {
       if (l < nl) {
@@ -745,7 +748,8 @@ __device__ void aux_role(const WnChainArgs& g, const int ai, const int b0, const
           const int q = tid + k * NT;
           if (q < ns * (2 * R / 4)) {
             const int i = q / (2 * R / 4), e = q % (2 * R / 4);
-            cq[l][k] = *reinterpret_cast<const float4*>(crow + (size_t)i * T * L * 2 * R + 4 * e);
+            // each row is read once: a non-temporal load, so that the stream does not evict the mailboxes
+            cq[l][k] = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(crow + (size_t)i * T * L * 2 * R + 4 * e));
           }
         }
       }
@@ -760,7 +764,7 @@ __device__ void aux_role(const WnChainArgs& g, const int ai, const int b0, const
 #pragma unroll
         for (int k = 0; k < CQ; ++k) {
           const int q = tid + k * NT;
-          if (q < ns * (2 * R / 4)) reinterpret_cast<float4*>(clg + l * G * 2 * R)[q] = cq[l][k];
+          if (q < ns * (2 * R / 4)) reinterpret_cast<f4v*>(clg + l * G * 2 * R)[q] = cq[l][k];
         }
       }
     }
@@ -770,7 +774,7 @@ __device__ void aux_role(const WnChainArgs& g, const int ai, const int b0, const
   auto post_pre = [&](int l, int64_t ts, int i) {
     const float a = gsum<M::LPR1>(dot_lds<M::KC1>(wp[l], xpg + (l * G + i) * R + kq * M::KC1));
     if (kq == 0)
-      stw(g.mb + (size_t)(b0 + i) * g.mb_words + ((size_t)(ja + l) * 2 + (ts & 1)) * 2 * R + rowp,
+      stw(g.mb + (size_t)(b0 + i) * g.mb_words + (size_t)(ja + l) * 2 * R + rowp,
           pack(a + bg[l] + clg[(l * G + i) * 2 * R + rowp], (unsigned)(ts + 1)), (lm >> l) & 1u);
   };
 
@@ -803,7 +807,7 @@ __device__ void aux_role(const WnChainArgs& g, const int ai, const int b0, const
           const int j = ja + l;
           // Waiting for h_j[t] also paces this CU: once it has arrived the chain has consumed
           // pre_j[t], so posting pre_j[t + 1] below cannot overwrite a slot the chain has yet to read.
-          const Items hi{mbs + g.off_h + ((size_t)j * 2 + (t & 1)) * R, R, R, R, hs + l * R, (unsigned)(t + 1)};
+          const Items hi{mbs + g.off_h + (size_t)j * R, R, R, R, hs + l * R, (unsigned)(t + 1)};
           if (more && dl[l] == 1) {
             Items xi = hist_items(l, t + 1);
             xi.base += (size_t)i * g.d.hist_len;
@@ -820,7 +824,7 @@ __device__ void aux_role(const WnChainArgs& g, const int ai, const int b0, const
             // the partial goes out as soon as its last layer is in: a later layer of this CU (the
             // network's last, whose skip is on the chain) only paces the pre-activations
             if (l == nsk - 1 && ks == 0)
-              stw(mbs + g.off_q + ((size_t)ai * 2 + (t & 1)) * S + rows, pack(q, (unsigned)(t + 1)), (lm >> 16) & 1u);
+              stw(mbs + g.off_q + (size_t)ai * S + rows, pack(q, (unsigned)(t + 1)), (lm >> 16) & 1u);
           }
         }
       }
@@ -866,7 +870,6 @@ __device__ void head_role(const WnChainArgs& g, const int hh, const int b0, cons
 
   for (int64_t t = tg0; t < tg0 + T; ++t) {
     const unsigned tag = (unsigned)(t + 1);
-    const int par = (int)(t & 1);
     for (int i = 0; i < ns; ++i) {
       u64* const mbs = g.mb + (size_t)(b0 + i) * g.mb_words;
       // all skip partials of this step: sum_j W_skip_j h_j over each aux CU's layers and (when the
@@ -875,8 +878,8 @@ __device__ void head_role(const WnChainArgs& g, const int hh, const int b0, cons
       // partial and sums those as they arrive; the NT / S partial sums of a channel then meet in
       // LDS, in a fixed order.
       float part = 0.f;
-      poll2<12>(g, Items{mbs + g.off_q + (size_t)par * S, S, 2 * S, nq * S, qall, tag},
-                g.tail_on_chain ? Items{mbs + g.off_qtail + (size_t)par * S, S, S, S, qall + nq * S, tag} : no_items(),
+      poll2<12>(g, Items{mbs + g.off_q, S, S, nq * S, qall, tag},
+                g.tail_on_chain ? Items{mbs + g.off_qtail, S, S, S, qall + nq * S, tag} : no_items(),
                 dyn, sy, &part);
       qpart[tid] = part;
       lds_barrier();
@@ -896,7 +899,7 @@ __device__ void head_role(const WnChainArgs& g, const int hh, const int b0, cons
       lds_barrier();
       {
         const float v = gsum<LPRO>(dot_lds<KCO>(wo, za + ko * KCO));
-        if (ko == 0) stw(mbs + g.off_logit + ((size_t)hh * 2 + par) * A + oo, pack(v, tag), lm & 1u);
+        if (ko == 0) stw(mbs + g.off_logit + (size_t)hh * A + oo, pack(v, tag), lm & 1u);
       }
       lds_barrier();
     }
@@ -1092,13 +1095,13 @@ bool wn_chain_plan(int L, int R, int S, int B, bool two_taps, WnChainPlan* p) {
   // CU computes that layer's skip projection
   q.naux_q = (q.tail_on_chain && (L - 1) % q.nla == 0) ? q.naux - 1 : q.naux;
   // mailboxes of one stream: pre, h, q, x, logits, tail (see WnChainArgs)
-  const long long pre_w = (long long)L * 2 * 2 * R;
+  const long long pre_w = (long long)L * 2 * R;
   q.off_h = (int)pre_w;
-  q.off_q = q.off_h + L * 2 * R;
-  q.off_x = q.off_q + q.naux * 2 * S;
-  q.off_logit = q.off_x + q.nch * 2 * R;
-  q.off_qtail = q.off_logit + NHEAD * 2 * A;
-  q.mb_words = ((long long)q.off_qtail + 2 * S + 31) / 32 * 32;
+  q.off_q = q.off_h + L * R;
+  q.off_x = q.off_q + q.naux * S;
+  q.off_logit = q.off_x + q.nch * R;
+  q.off_qtail = q.off_logit + NHEAD * A;
+  q.mb_words = ((long long)q.off_qtail + S + 31) / 32 * 32;
   // Placement: slot i of XCD x is block 8 i + x.  Each replica's chain and head CUs go to its home
   // XCD first, then its aux CUs, last layers first (their skip partials are the last ones the head
   // waits for), overflowing to the XCD with the most room.
