@@ -198,7 +198,7 @@ def _setup_workload(name, seed):
 
 # Batched workloads timed beside the headline (outside its timed region), so that their roofline
 # fractions appear in the benchmark's own record.
-BATCHED = ["l20_r128_b32", "l20_r64_b256_bf16"]
+BATCHED = ["l20_r128_b32", "l20_r64_b256_bf16", "l20_r64_b256_i8"]
 
 
 def batched_record(args):
