@@ -202,3 +202,39 @@ def test_default_choice(dtype, monkeypatch):
     assert [net.kernel_variant(b) for b in (46, 256, 512)] == [KERNEL] * 3
     assert net.kernel_variant(513) == ("mfma_group" if dtype == "bf16" else "stream_l2")
     net.close()
+
+
+@pytest.mark.parametrize("B,cols", [(9, 8), (256, 8), (40, 16)])
+def test_same_xcd_posts_change_nothing(B, cols, monkeypatch):
+    """Posts to a reader on the same XCD stop at its L2; written through instead (WN_LOCAL_POSTS=0)
+    every sample and logit is the same, also when every CU of the chip is in the launch (B = 256: 32
+    replicas, 4 per XCD) and when the same workspace runs again from zero (every tag repeats, and a
+    word a previous call left in an L2 must not be taken for this call's)."""
+    import paper_1702_07825_amd as wn
+    _log("multi-CU MFMA same-XCD posts: B=%d columns=%d" % (B, cols))
+    monkeypatch.setenv("WN_KERNEL", KERNEL)
+    monkeypatch.delenv("WN_AUX_LAYERS", raising=False)
+    if cols == 16:
+        monkeypatch.setenv("WN_MFMA_COLUMNS", "16")
+    else:
+        monkeypatch.delenv("WN_MFMA_COLUMNS", raising=False)
+    L, T = 20, 120
+    w = synth.make_weights(L, 64, 256, seed=B + cols, bias_scale=0.1)
+    cond = synth.make_cond(L, 64, B, T, seed=B + cols, device="cuda")
+    u = torch.tensor(synth.make_uniforms(B, T, seed=B + cols), device="cuda")
+    out = {}
+    for lp in ("0", "1"):
+        monkeypatch.setenv("WN_LOCAL_POSTS", lp)
+        net = wn.WaveNet(w, synth.dilation_cycle(L), weight_dtype="bf16")
+        assert net.kernel_variant(B) == KERNEL
+        ws = net.new_workspace(B)
+        y = net.generate(cond, u, workspace=ws)
+        y_again = net.generate(cond, u, workspace=ws, reset=True)
+        lg = net.teacher_force(cond, y)
+        torch.cuda.synchronize()
+        assert net.status(ws) == 0
+        assert torch.equal(y, y_again)
+        out[lp] = (y.cpu(), lg.cpu())
+        net.close()
+    assert torch.equal(out["0"][0], out["1"][0])
+    assert torch.equal(out["0"][1], out["1"][1])
