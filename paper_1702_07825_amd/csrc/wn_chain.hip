@@ -77,26 +77,29 @@ struct Items {
 };
 __device__ __forceinline__ Items no_items() { return Items{nullptr, 1, 0, 0, nullptr, 0u}; }
 
-// Wait until every item of `a` and `b` owned by this thread (item i belongs to thread i mod NT)
-// carries its descriptor's tag, writing the values to LDS (dst pointers lie in `lds`).  Up to K
-// owned loads are in flight together.  A thread that times out, or sees a nonzero status word, sets the
-// block's abort flag and stops waiting.  Every polled word lies in the workspace's tagged region,
-// which starts at g.ring; items are tracked as 32-bit word offsets from there.
-// With acc != nullptr the thread also adds the values of its items to *acc, in item order.
-template <int K = 4>
+// Wait until every item of `a` and `b` owned by this thread carries its descriptor's tag, writing
+// the values to LDS (dst pointers lie in `lds`).  Items go in pairs (2p, 2p + 1), one 128-bit load
+// each (wn_msg.h); pair p belongs to thread p mod NT, and up to K owned pairs are in flight together.
+// Every descriptor's item count and segment length are even, so a pair never straddles two
+// segments.  A thread that times out, or sees a nonzero status word, sets the block's abort flag and
+// stops waiting.  Every polled word lies in the workspace's tagged region, which starts at g.ring;
+// items are tracked as 32-bit word offsets from there.  With acc != nullptr the thread also adds the
+// values of its pairs' first items to acc[0] and of their second items to acc[1], in pair order.
+template <int K = 2>
 __device__ void poll2(const WnChainArgs& g, const Items a, const Items b, float* lds, Sync s,
                       float* acc = nullptr) {
-  const int n = a.n + b.n;
+  const int np = (a.n + b.n) / 2;
   const u64* wbase = g.ring;
-  for (int base = threadIdx.x; base < n; base += K * NT) {
-    u64 w[K];
+  const wrsrc rs = region_rsrc(g.ring, (size_t)(g.mb + (size_t)g.io.B * g.mb_words - g.ring));
+  for (int base = threadIdx.x; base < np; base += K * NT) {
+    u32x4 w[K];
     unsigned so[K], dofs[K];
-    unsigned pend = 0, useb = 0;  // bit k: item base + k * NT pending / belongs to descriptor b
+    unsigned pend = 0, useb = 0;  // bit k: pair base + k * NT pending / belongs to descriptor b
     static_assert(K <= 32, "pending bits");
 #pragma unroll
     for (int k = 0; k < K; ++k) {
-      const int i = base + k * NT;
-      if (i < n) {
+      const int i = 2 * (base + k * NT);
+      if (i < 2 * np) {
         const bool inb = (i >= a.n);
         const Items& it = inb ? b : a;
         const int ii = inb ? i - a.n : i;
@@ -104,7 +107,7 @@ __device__ void poll2(const WnChainArgs& g, const Items a, const Items b, float*
         dofs[k] = (unsigned)((it.dst - lds) + ii);
         pend |= 1u << k;
         useb |= (inb ? 1u : 0u) << k;
-        w[k] = ldw(wbase + so[k]);
+        w[k] = ld_pair(rs, so[k]);
       }
     }
     int spins = 0;
@@ -112,17 +115,23 @@ __device__ void poll2(const WnChainArgs& g, const Items a, const Items b, float*
 #pragma unroll
       for (int k = 0; k < K; ++k) {
         if (pend & (1u << k)) {
-          if (wtag(w[k]) == ((useb & (1u << k)) ? b.tag : a.tag)) {
+          const unsigned tg = (useb & (1u << k)) ? b.tag : a.tag;
+          if (w[k][1] == tg && w[k][3] == tg) {
             pend &= ~(1u << k);
-            lds[dofs[k]] = wval(w[k]);
+            lds[dofs[k]] = __uint_as_float(w[k][0]);
+            lds[dofs[k] + 1] = __uint_as_float(w[k][2]);
           }
         }
       }
       if (!pend) {
         if (acc) {
 #pragma unroll
-          for (int k = 0; k < K; ++k)
-            if (base + k * NT < n) *acc += wval(w[k]);
+          for (int k = 0; k < K; ++k) {
+            if (base + k * NT < np) {
+              acc[0] += __uint_as_float(w[k][0]);
+              acc[1] += __uint_as_float(w[k][2]);
+            }
+          }
         }
         break;
       }
@@ -131,9 +140,11 @@ __device__ void poll2(const WnChainArgs& g, const Items a, const Items b, float*
         *s.flag = 1;
         return;
       }
+      // a side effect between reloads: without one the compiler may hoist the loads out of the loop
+      __builtin_amdgcn_s_sleep(1);
 #pragma unroll
       for (int k = 0; k < K; ++k)
-        if (pend & (1u << k)) w[k] = ldw(wbase + so[k]);
+        if (pend & (1u << k)) w[k] = ld_pair(rs, so[k]);
     }
   }
 }
@@ -853,8 +864,8 @@ __device__ void head_role(const WnChainArgs& g, const int hh, const int b0, cons
   float* qall = dyn;           // (nq + 1)*S skip partials of one step: the aux CUs', then the tail
   float* zs = qall + L * S;    // S
   float* za = zs + S;          // HR
-  float* qpart = za + HR;      // NT per-thread partial sums
-  static_assert(NT % S == 0, "a thread's skip items share one channel");
+  float* qpart = za + HR;      // 2 NT per-thread partial sums (two channels per thread)
+  static_assert((2 * NT) % S == 0 && S % 2 == 0, "a thread's skip pairs share two channels");
 
   const int rl = tid / LPRH, kr = tid % LPRH;
   const int oo = tid / LPRO, ko = tid % LPRO;
@@ -874,21 +885,23 @@ __device__ void head_role(const WnChainArgs& g, const int hh, const int b0, cons
       u64* const mbs = g.mb + (size_t)(b0 + i) * g.mb_words;
       // all skip partials of this step: sum_j W_skip_j h_j over each aux CU's layers and (when the
       // last chain CU computes it) the last layer's.  Item i is channel i mod S of partial i / S and
-      // the thread of item i is i mod NT, so thread tid polls channel tid mod S of every (NT / S)-th
-      // partial and sums those as they arrive; the NT / S partial sums of a channel then meet in
+      // pair p (items 2p, 2p + 1) belongs to thread p mod NT, so thread tid polls channels
+      // 2 tid mod S and 2 tid mod S + 1 of every (2 NT / S)-th partial, from partial 2 tid / S on,
+      // and sums each channel's as they arrive; the 2 NT / S partial sums of a channel then meet in
       // LDS, in a fixed order.
-      float part = 0.f;
-      poll2<12>(g, Items{mbs + g.off_q, S, S, nq * S, qall, tag},
-                g.tail_on_chain ? Items{mbs + g.off_qtail, S, S, S, qall + nq * S, tag} : no_items(),
-                dyn, sy, &part);
-      qpart[tid] = part;
+      float part[2] = {0.f, 0.f};
+      poll2<3>(g, Items{mbs + g.off_q, S, S, nq * S, qall, tag},
+               g.tail_on_chain ? Items{mbs + g.off_qtail, S, S, S, qall + nq * S, tag} : no_items(),
+               dyn, sy, part);
+      qpart[(2 * tid / S) * S + (2 * tid) % S] = part[0];
+      qpart[(2 * tid / S) * S + (2 * tid) % S + 1] = part[1];
       lds_barrier();
       if (sy.failed()) return;
       // z_s = relu(B_skip + sum_j q_j)
       if (tid < S) {
         float q = bsk;
 #pragma unroll
-        for (int p = 0; p < NT / S; ++p) q += qpart[p * S + tid];
+        for (int p = 0; p < 2 * NT / S; ++p) q += qpart[p * S + tid];
         zs[tid] = fmaxf(q, 0.f);
       }
       lds_barrier();
@@ -1018,7 +1031,7 @@ size_t chain_lds_floats(int R, int S, int nlc, int G, int ub, int nch, int tail,
   if (R == 128) var = std::max(var, (size_t)2 * R * lds_row_stride(R, 2));
   return common + var;
 }
-size_t head_lds_floats(int L, int S) { return (size_t)L * S + S + HR + NT; }
+size_t head_lds_floats(int L, int S) { return (size_t)L * S + S + HR + 2 * NT; }
 size_t aux_lds_floats(int R, int G) {
   const size_t nla = R <= 64 ? aux_max_layers<64>() : aux_max_layers<128>();
   return nla * ((size_t)R + (size_t)3 * R * G);

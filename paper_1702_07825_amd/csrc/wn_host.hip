@@ -109,17 +109,21 @@ class DeviceScope {
   bool ok_ = false;
 };
 
-// The multi-CU kernel's layout of B streams, if it serves them: every tagged word it polls
-// (histories, then mailboxes) must lie within 2^32 words of the first.
+// The multi-CU kernels poll their tagged words (histories, then mailboxes) through a buffer
+// resource, whose byte offsets are 32-bit: the region must stay under 2 GiB.
+bool tagged_region_fits(unsigned long long words) { return words * 8 + 4096 < (1ull << 31); }
+
+// The multi-CU kernel's layout of B streams, if it serves them.
 bool chain_plan_for(const wn_handle* h, int B, WnChainPlan* p) {
   if (!h->chain_ok || !wn_chain_plan(h->L, h->R, h->S, B, h->w.embed_prev != nullptr, p)) return false;
-  return (unsigned long long)B * ((unsigned long long)h->dims.hist_len + (unsigned long long)p->mb_words) + 64 <
-         (1ull << 32);
+  return tagged_region_fits((unsigned long long)B * ((unsigned long long)h->dims.hist_len + (unsigned long long)p->mb_words));
 }
 
 // The multi-CU MFMA kernel's layout of B streams, if it serves them.
 bool mchain_plan_for(const wn_handle* h, int B, WnChainPlan* p) {
-  return h->mchain_ok && wn_mchain_plan(h->L, h->R, h->S, B, p);
+  if (!h->mchain_ok || !wn_mchain_plan(h->L, h->R, h->S, B, p)) return false;
+  return tagged_region_fits((unsigned long long)p->nrep *
+                            ((unsigned long long)h->dims.hist_len * wn_mchain_columns(*p) + (unsigned long long)p->mb_words));
 }
 
 int variant_for(const wn_handle* h, int B) {

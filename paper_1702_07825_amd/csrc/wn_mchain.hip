@@ -249,20 +249,10 @@ __device__ __forceinline__ void post4(u64* p, float4 v, unsigned tag, bool local
   }
 }
 
-// Polls of pairs of tagged words (16 bytes) through a buffer resource over the workspace's tagged region
-// (histories and mailboxes): 128-bit loads at agent scope (cache policy sc1: past the CU's L1, from
-// the L2), about three times the rate of 64-bit atomic loads per CU (measured: 123 against 38 GB/s),
-// and bounds-checked by the hardware (a read past the region returns zeros).  Each 64-bit word is
-// written whole by one store, so a word read in a pair is never torn; the two words of a pair carry
-// their own tags.  Pair p holds words 2p and 2p + 1 of a block; word(p) is the word offset of word 2p
-// in the region.
-typedef __amdgpu_buffer_rsrc_t wrsrc;
+// Pair polls (wn_msg.h) over the replicas' histories and mailboxes.  Pair p holds words 2p and 2p + 1
+// of a block; word(p) is the word offset of word 2p in the region.
 __device__ __forceinline__ wrsrc tagged_region(const WnChainArgs& g) {
-  const size_t bytes = (size_t)((const char*)(g.mb + (size_t)g.nrep * g.mb_words) - (const char*)g.ring);
-  return __builtin_amdgcn_make_buffer_rsrc((void*)g.ring, (short)0, (int)bytes, 0x00020000);
-}
-__device__ __forceinline__ u32x4 ld_pair(wrsrc rs, unsigned word) {
-  return __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(word * 8u), 0, 16 /* sc1 */);
+  return region_rsrc(g.ring, (size_t)(g.mb + (size_t)g.nrep * g.mb_words - g.ring));
 }
 template <int K, int NP = NT, class Word>
 __device__ __forceinline__ void pairs_start(u32x4 (&w)[K], wrsrc rs, int ti, int np, Word word) {

@@ -35,6 +35,22 @@ __device__ __forceinline__ int ld_status(const int* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Polls of pairs of tagged words (16 bytes) through a buffer resource over the workspace's tagged
+// region (histories and mailboxes): 128-bit loads at agent scope (cache policy sc1: past the CU's
+// L1, from the L2), about three times the rate of 64-bit atomic loads per CU (measured: 123 against
+// 38 GB/s), and bounds-checked by the hardware (a read past the region returns zeros; the host keeps
+// the region under 2 GiB, the buffer's 32-bit byte offsets).  Each 64-bit word is written whole by
+// one store, so a word read in a pair is never torn; the two words of a pair carry their own tags.
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef __amdgpu_buffer_rsrc_t wrsrc;
+__device__ __forceinline__ wrsrc region_rsrc(const u64* base, size_t words) {
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, (int)(words * 8), 0x00020000);
+}
+// words `word`, `word` + 1 of the region (word even)
+__device__ __forceinline__ u32x4 ld_pair(wrsrc rs, unsigned word) {
+  return __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(word * 8u), 0, 16 /* sc1 */);
+}
+
 // Block-uniform abort flag kept in LDS.
 struct Sync {
   int* flag;
