@@ -263,9 +263,10 @@ __device__ __forceinline__ void pairs_start(u32x4 (&w)[K], wrsrc rs, int ti, int
 // Waits until both words of each of this thread's pairs carry their tags, then sink(i, q, value) for
 // words i = 2p, 2p + 1 in order (q = 2k or 2k + 1: the word's place in the batch).
 // ZZ: s_sleep units (64 clocks each) between two reloads of words that are not there yet: long for
-// waits off the critical path (they would otherwise keep the L2 busy for microseconds), short for the
-// rest.
-template <int K, int NP = NT, int ZZ = 1, class Word, class Tag, class Sink>
+// waits off the critical path (they would otherwise keep the L2 busy for microseconds), none for the
+// rest (a one-unit sleep there measured 0.7 us/step slower at l = 20, B = 256), with a compiler barrier
+// in its place so that the loads stay in the loop.
+template <int K, int NP = NT, int ZZ = 0, class Word, class Tag, class Sink>
 __device__ __forceinline__ void pairs_finish(const WnChainArgs& g, u32x4 (&w)[K], wrsrc rs, int ti, int np, Word word,
                                              Tag tag, Sink sink, Sync s) {
   static_assert(K <= 32, "pending bits");
@@ -287,6 +288,7 @@ __device__ __forceinline__ void pairs_finish(const WnChainArgs& g, u32x4 (&w)[K]
       return;
     }
     if constexpr (ZZ > 0) __builtin_amdgcn_s_sleep(ZZ);
+    else asm volatile("" ::: "memory");  // keeps the reloads in the loop
 #pragma unroll
     for (int k = 0; k < K; ++k)
       if ((pend >> k) & 1u) w[k] = ld_pair(rs, word(ti + k * NP));
@@ -301,7 +303,7 @@ __device__ __forceinline__ void pairs_finish(const WnChainArgs& g, u32x4 (&w)[K]
   }
 }
 // Both halves at once, in batches of K pairs per thread.
-template <int K, int NP = NT, int ZZ = 1, class Word, class Tag, class Sink>
+template <int K, int NP = NT, int ZZ = 0, class Word, class Tag, class Sink>
 __device__ __forceinline__ void poll_pairs(const WnChainArgs& g, wrsrc rs, int ti, int np, Word word, Tag tag, Sink sink,
                                            Sync s) {
   for (int base = 0; base < np; base += K * NP) {
