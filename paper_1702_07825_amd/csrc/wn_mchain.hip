@@ -332,31 +332,31 @@ __device__ __forceinline__ float gate_h(float a, float g) {
   else return gate_tanh_sigmoid(a, g);
 }
 
-// tanh(ah) sigmoid(ag) with paired columns: after fold8 lanes n and n + 8 hold the same ah and ag;
-// lane n (part 0) evaluates the tanh and lane n + 8 the sigmoid, and they swap results (row_ror:8),
-// so a wave issues half the transcendental instructions.  AX: Appendix C's forms with the same
-// operations as tanh_paper and sigmoid_paper.
-template <bool AX>
-__device__ __forceinline__ float gate_pair8(float ah, float ag, int part) {
+// Appendix C's tanh(ah) sigmoid(ag) with paired columns: after fold8 lanes n and n + 8 hold the
+// same ah and ag; lane n (part 0) evaluates the tanh and lane n + 8 the sigmoid, with the same
+// operations as tanh_paper and sigmoid_paper, and they swap results (row_ror:8).
+__device__ __forceinline__ float gate_pair8_paper(float ah, float ag, int part) {
   const bool th = part == 0;
-  float v;
-  if constexpr (AX) {
-    const float x = th ? ah : ag;
-    const float e = e_tilde(x);
-    const float r = __builtin_amdgcn_rcpf(th ? e : 1.0f + e);
-    v = th ? copysignf((e - r) * __builtin_amdgcn_rcpf(e + r), x) : (x >= 0.0f ? e * r : r);
-  } else {
-    const float r = __builtin_amdgcn_rcpf(1.0f + expf_fast(th ? 2.0f * ah : -ag));
-    v = th ? 1.0f - 2.0f * r : r;
-  }
+  const float x = th ? ah : ag;
+  const float e = e_tilde(x);
+  const float r = __builtin_amdgcn_rcpf(th ? e : 1.0f + e);
+  const float v = th ? copysignf((e - r) * __builtin_amdgcn_rcpf(e + r), x) : (x >= 0.0f ? e * r : r);
   const float o = dpp<0x128>(v);
   return th ? v * o : o * v;
 }
+// Four gates of paired columns.  Exact forms (AX false): lane part 0 evaluates elements 0 and 1 and part 1
+// elements 2 and 3 in the unpaired form (three transcendental instructions each), and the two lanes
+// swap results, fewer instructions than splitting every element into tanh and sigmoid halves.
 template <bool AX, bool PAIR>
 __device__ __forceinline__ float4 gate4(f32x4 at, f32x4 ag, int part) {
-  if constexpr (PAIR)
-    return make_float4(gate_pair8<AX>(at[0], ag[0], part), gate_pair8<AX>(at[1], ag[1], part),
-                       gate_pair8<AX>(at[2], ag[2], part), gate_pair8<AX>(at[3], ag[3], part));
+  if constexpr (PAIR && !AX) {
+    const float h0 = gate_tanh_sigmoid(part ? at[2] : at[0], part ? ag[2] : ag[0]);
+    const float h1 = gate_tanh_sigmoid(part ? at[3] : at[1], part ? ag[3] : ag[1]);
+    const float o0 = dpp<0x128>(h0), o1 = dpp<0x128>(h1);
+    return part ? make_float4(o0, o1, h0, h1) : make_float4(h0, h1, o0, o1);
+  } else if constexpr (PAIR)
+    return make_float4(gate_pair8_paper(at[0], ag[0], part), gate_pair8_paper(at[1], ag[1], part),
+                       gate_pair8_paper(at[2], ag[2], part), gate_pair8_paper(at[3], ag[3], part));
   else
     return make_float4(gate_h<AX>(at[0], ag[0]), gate_h<AX>(at[1], ag[1]), gate_h<AX>(at[2], ag[2]),
                        gate_h<AX>(at[3], ag[3]));
