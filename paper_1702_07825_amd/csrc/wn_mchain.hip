@@ -1051,12 +1051,23 @@ __device__ __forceinline__ void mc_head(const WnChainArgs& g, const int hh, cons
     // the draws of my streams HG / 4 wave .. (both at once, so that their steps interleave; a padding
     // stream's draw is made and dropped), then their x0 of the next step (row = lane)
     int ys[HG / 4];
+    if constexpr (TF) {
 #pragma unroll
-    for (int k = 0; k < HG / 4; ++k) {
-      const int q = (HG / 4) * wave + k;
-      if constexpr (TF) {
-        ys[k] = s_yin[q];
-      } else {
+      for (int k = 0; k < HG / 4; ++k) ys[k] = s_yin[(HG / 4) * wave + k];
+    } else if (g.io.smode == WN_DRAW_DIRECT || g.io.smode == WN_DRAW_TEMPERATURE) {
+      float4 lv[HG / 4];
+      float uq[HG / 4];
+#pragma unroll
+      for (int k = 0; k < HG / 4; ++k) {
+        const int q = (HG / 4) * wave + k;
+        lv[k] = *reinterpret_cast<const float4*>(LG + q * PA + 4 * lane);
+        uq[k] = s_u[q];
+      }
+      wave_draw_cdf<AX>(lv, uq, g.io.smode == WN_DRAW_TEMPERATURE ? g.io.inv_t : 1.0f, ys);
+    } else {
+#pragma unroll
+      for (int k = 0; k < HG / 4; ++k) {
+        const int q = (HG / 4) * wave + k;
         const float4 lv = *reinterpret_cast<const float4*>(LG + q * PA + 4 * lane);
         ys[k] = wave_draw<AX>(lv, s_u[q], g.io.smode, g.io.inv_t, g.io.top_k, lane);
       }

@@ -79,16 +79,6 @@ __device__ __forceinline__ float wave_max(float v) {
   const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
   return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
 }
-__device__ __forceinline__ int wave_sum_int(int v) {
-  float f = (float)v;  // counts are at most 255: exact in fp32
-  f = gsum16(f);
-  const int r0 = __builtin_amdgcn_readlane(__builtin_bit_cast(int, f), 0);
-  const int r1 = __builtin_amdgcn_readlane(__builtin_bit_cast(int, f), 16);
-  const int r2 = __builtin_amdgcn_readlane(__builtin_bit_cast(int, f), 32);
-  const int r3 = __builtin_amdgcn_readlane(__builtin_bit_cast(int, f), 48);
-  return (int)(__builtin_bit_cast(float, r0) + __builtin_bit_cast(float, r1) + __builtin_bit_cast(float, r2) +
-               __builtin_bit_cast(float, r3));
-}
 
 __device__ __forceinline__ float expf_fast(float v) { return __builtin_amdgcn_exp2f(v * 1.4426950408889634f); }
 __device__ __forceinline__ float tanh_f(float v) { return 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + expf_fast(2.0f * v)); }
@@ -163,6 +153,14 @@ __device__ __forceinline__ unsigned float_key(float f) {
 // "Sampling from Output Distribution"); the values are those of wn_sample_mode_t.
 enum { WN_DRAW_DIRECT = 0, WN_DRAW_TEMPERATURE = 1, WN_DRAW_TOPK = 2, WN_DRAW_MODE = 3, WN_DRAW_MEAN = 4 };
 
+// #{k <= 254 : excl + s_i <= uz} over a wave, k = 4 lane + i: the inverse CDF at u with unnormalised
+// prefix sums (excl the lane's exclusive prefix, s_i its own running sums) and uz = u Z, Z the total;
+// counted by ballots.
+__device__ __forceinline__ int cdf_count(float excl, const float (&s)[4], float uz) {
+  return __popcll(__ballot(excl + s[0] <= uz)) + __popcll(__ballot(excl + s[1] <= uz)) +
+         __popcll(__ballot(excl + s[2] <= uz)) + __popcll(__ballot(excl + s[3] <= uz) & 0x7fffffffffffffffull);
+}
+
 // One step's sample from the a = 256 logits held by one wave, lane l holding logits 4l .. 4l+3;
 // every lane returns it.  P = softmax(logits).  Rules (mode is wave-uniform):
 //   direct       y = #{k <= 254 : C_k <= u}, C_k = (p_0 + .. + p_k), the inverse CDF at u
@@ -172,7 +170,8 @@ enum { WN_DRAW_DIRECT = 0, WN_DRAW_TEMPERATURE = 1, WN_DRAW_TOPK = 2, WN_DRAW_MO
 //                rounding) becomes that class
 //   mode         the smallest index of the largest logit
 //   mean         floor(sum_k k p_k + 1/2)
-// AX: e^x of the softmax by the approximation of Appendix C.
+// The CDF rules compare the unnormalised prefix sums with u Z.  AX: e^x of the softmax by the
+// approximation of Appendix C.
 template <bool AX = false>
 __device__ __forceinline__ int wave_draw(float4 lv, float u, int mode, float inv_t, int top_k, int lane) {
   float l[4] = {lv.x, lv.y, lv.z, lv.w};
@@ -217,21 +216,54 @@ __device__ __forceinline__ int wave_draw(float4 lv, float u, int mode, float inv
       if (mk) last = max(last, 4 * (63 - __clzll((long long)mk)) + i);
     }
   }
-  const float s0 = e[0], s1 = s0 + e[1], s2 = s1 + e[2], s3 = s2 + e[3];
-  const float incl = wave_incl_scan(s3);
+  const float s[4] = {e[0], e[0] + e[1], e[0] + e[1] + e[2], e[0] + e[1] + e[2] + e[3]};
+  const float incl = wave_incl_scan(s[3]);
   const float excl = wave_shr1(incl);
   const float Z = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, incl), 63));
-  const float iz = 1.0f / Z;
   if (mode == WN_DRAW_MEAN) {
     const float k0 = (float)(4 * lane);
     const float part = k0 * e[0] + (k0 + 1.f) * e[1] + (k0 + 2.f) * e[2] + (k0 + 3.f) * e[3];
-    const int y = (int)floorf(wave_sum(part) * iz + 0.5f);
+    const int y = (int)floorf(wave_sum(part) * (1.0f / Z) + 0.5f);
     return y < 0 ? 0 : (y > 255 ? 255 : y);
   }
-  int cnt = ((excl + s0) * iz <= u) + ((excl + s1) * iz <= u) + ((excl + s2) * iz <= u);
-  if (lane != 63) cnt += ((excl + s3) * iz <= u);  // k = 255 is never counted
-  const int y = wave_sum_int(cnt);
+  const int y = cdf_count(excl, s, u * Z);
   return y > last ? last : y;
+}
+
+// The direct rule (sc = 1) or the temperature rule (sc = 1 / t) for N streams of one wave at once,
+// the same arithmetic as wave_draw's; straight-line code, so that the streams' cross-lane steps
+// interleave.
+template <bool AX, int N>
+__device__ __forceinline__ void wave_draw_cdf(const float4 (&lv)[N], const float (&u)[N], float sc, int (&y)[N]) {
+  float l[N][4], m[N], s[N][4], incl[N];
+#pragma unroll
+  for (int n = 0; n < N; ++n) {
+    l[n][0] = lv[n].x * sc;
+    l[n][1] = lv[n].y * sc;
+    l[n][2] = lv[n].z * sc;
+    l[n][3] = lv[n].w * sc;
+    m[n] = fmaxf(fmaxf(l[n][0], l[n][1]), fmaxf(l[n][2], l[n][3]));
+  }
+#pragma unroll
+  for (int n = 0; n < N; ++n) m[n] = wave_max(m[n]);
+#pragma unroll
+  for (int n = 0; n < N; ++n) {
+    float e[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) e[i] = exp_nl<AX>(l[n][i] - m[n]);
+    s[n][0] = e[0];
+    s[n][1] = e[0] + e[1];
+    s[n][2] = e[0] + e[1] + e[2];
+    s[n][3] = e[0] + e[1] + e[2] + e[3];
+  }
+#pragma unroll
+  for (int n = 0; n < N; ++n) incl[n] = wave_incl_scan(s[n][3]);
+#pragma unroll
+  for (int n = 0; n < N; ++n) {
+    const float excl = wave_shr1(incl[n]);
+    const float Z = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, incl[n]), 63));
+    y[n] = cdf_count(excl, s[n], u[n] * Z);
+  }
 }
 
 // True when the host has requested an abort (wn_abort): the word lives in pinned host memory, so
