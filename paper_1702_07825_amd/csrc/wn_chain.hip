@@ -217,9 +217,9 @@ __device__ __forceinline__ float dot_lds(const float (&w)[K], const float* x, fl
 // Two embedding tables fit chain CU 0's LDS beside its other buffers up to r = 64.
 constexpr bool e2_in_lds(int R) { return R <= 64; }
 
-template <int R, int S, int NLC, bool TF, bool MS, bool E2, bool AX>
-__device__ void chain_role(const WnChainArgs& g, const int c, const int b0, const int ns, float* dyn, Sync sy,
-                           const int64_t tg0, const unsigned lm) {
+template <int R, int S, int NLC, bool TF, bool MS, bool E2, bool AX, class LM>
+__device__ __forceinline__ void chain_role(const WnChainArgs& g, const int c, const int b0, const int ns, float* dyn, Sync sy,
+                           const int64_t tg0, const LM lm) {
   constexpr bool E2L = E2 && e2_in_lds(R);
   using M = ChainMap<R>;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -492,12 +492,12 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
         // of the step loop (they would not fit in registers)
         asm volatile("" : "+v"(row));
         hpost[l % HPOST] = pack(h, tag);
-        stw(mbs + g.off_h + (size_t)j * R + row, hpost[l % HPOST], (lm >> l) & 1u);
+        stw(mbs + g.off_h + (size_t)j * R + row, hpost[l % HPOST], lm(l));
       };
       // x of this CU's last layer -> the next chain CU, posted by the lanes that computed it
       const bool handoff = c + 1 < g.nch;
       auto post_x = [&](int row, float v) __attribute__((always_inline)) {
-        if (handoff) stw(mbs + g.off_x + (size_t)(c + 1) * R + row, pack(v, tag), (lm >> 16) & 1u);
+        if (handoff) stw(mbs + g.off_x + (size_t)(c + 1) * R + row, pack(v, tag), lm(16));
       };
 #pragma unroll
       for (int l = 0; l < NLC; ++l) {
@@ -654,14 +654,14 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
         const float q = xreduce8<RPG>(p, li);
         const int m = RPG * gq + (upper ? RPG / 2 : 0) + (RPG == 4 && (li & 2) ? 1 : 0);
         const int ks = (RPG == 4) ? (li & 1) : (li & 3);  // lanes holding the same row: post once
-        if (ks == 0) stw(mbs + g.off_qtail + m, pack(q, tag), (lm >> 17) & 1u);
+        if (ks == 0) stw(mbs + g.off_qtail + m, pack(q, tag), lm(17));
       }
       // Then x_{j-1} of each layer into the history slot (t mod d_j) that layer j's aux CU reads
       // again at t + d_j (the next chain CU's x went out in the last layer).
       for (int k = tid; k < nl * R; k += NT) {
         const int l = k / R, e = k % R;
         const int slot = slotv[par * NLCP + l];
-        stw(rings + lhoff[l] + (size_t)slot * R + e, pack(xbuf[l * R + e], tag), (lm >> l) & 1u);
+        stw(rings + lhoff[l] + (size_t)slot * R + e, pack(xbuf[l * R + e], tag), lm(l));
       }
 #pragma unroll
       for (int l = 0; l < HPOST; ++l) asm volatile("" ::"v"(hpost[l]));
@@ -699,9 +699,9 @@ __device__ void chain_role(const WnChainArgs& g, const int c, const int b0, cons
 template <int R>
 constexpr int aux_max_layers() { return R <= 64 ? 2 : 1; }
 
-template <int R, int S, bool TF, bool MS>
-__device__ void aux_role(const WnChainArgs& g, const int ai, const int b0, const int ns, float* dyn, Sync sy,
-                         const int64_t tg0, const unsigned lm) {
+template <int R, int S, bool TF, bool MS, class LM>
+__device__ __forceinline__ void aux_role(const WnChainArgs& g, const int ai, const int b0, const int ns, float* dyn, Sync sy,
+                         const int64_t tg0, const LM lm) {
   using M = ChainMap<R>;
   constexpr int NLA = aux_max_layers<R>();
   constexpr int LPRS = NT / S, KCS = R / LPRS;
@@ -787,7 +787,7 @@ __device__ void aux_role(const WnChainArgs& g, const int ai, const int b0, const
     const float a = gsum<M::LPR1>(dot_lds<M::KC1>(wp[l], xpg + (l * G + i) * R + kq * M::KC1));
     if (kq == 0)
       stw(g.mb + (size_t)(b0 + i) * g.mb_words + (size_t)(ja + l) * 2 * R + rowp,
-          pack(a + bg[l] + clg[(l * G + i) * 2 * R + rowp], (unsigned)(ts + 1)), (lm >> l) & 1u);
+          pack(a + bg[l] + clg[(l * G + i) * 2 * R + rowp], (unsigned)(ts + 1)), lm(l));
   };
 
   stage(tg0, true);
@@ -836,7 +836,7 @@ __device__ void aux_role(const WnChainArgs& g, const int ai, const int b0, const
             // the partial goes out as soon as its last layer is in: a later layer of this CU (the
             // network's last, whose skip is on the chain) only paces the pre-activations
             if (l == nsk - 1 && ks == 0)
-              stw(mbs + g.off_q + (size_t)ai * S + rows, pack(q, (unsigned)(t + 1)), (lm >> 16) & 1u);
+              stw(mbs + g.off_q + (size_t)ai * S + rows, pack(q, (unsigned)(t + 1)), lm(16));
           }
         }
       }
@@ -853,9 +853,9 @@ __device__ void aux_role(const WnChainArgs& g, const int ai, const int b0, const
 // ------------------------------------------------------------------------------------------
 // head CU: rows [64 h, 64 h + 64) of z_a and their share of the logits
 // ------------------------------------------------------------------------------------------
-template <int R, int S, bool TF, bool MS>
-__device__ void head_role(const WnChainArgs& g, const int hh, const int b0, const int ns, float* dyn, Sync sy,
-                          const int64_t tg0, const unsigned lm) {
+template <int R, int S, bool TF, bool MS, class LM>
+__device__ __forceinline__ void head_role(const WnChainArgs& g, const int hh, const int b0, const int ns, float* dyn, Sync sy,
+                          const int64_t tg0, const LM lm) {
   constexpr int LPRH = NT / HR, KCH = S / LPRH;   // W_relu: 8 lanes per row
   constexpr int LPRO = NT / A, KCO = HR / LPRO;   // W_out: 2 lanes per output
   const int tid = threadIdx.x;
@@ -913,7 +913,7 @@ __device__ void head_role(const WnChainArgs& g, const int hh, const int b0, cons
       lds_barrier();
       {
         const float v = gsum<LPRO>(dot_lds<KCO>(wo, za + ko * KCO));
-        if (ko == 0) stw(mbs + g.off_logit + (size_t)hh * A + oo, pack(v, tag), lm & 1u);
+        if (ko == 0) stw(mbs + g.off_logit + (size_t)hh * A + oo, pack(v, tag), lm(0));
       }
       lds_barrier();
     }
@@ -936,9 +936,11 @@ __global__ __launch_bounds__(NT) void wn_chain_kernel(const WnChainArgs g) {
   // the host has checked on this device): bit l of a chain CU for the aux CU of its layer l (h
   // and the history rows), bit 16 for the next chain CU, bit 17 for the head CUs; bit l of an aux
   // CU for the chain CU of its layer l, bit 16 for the head CUs; bit 0 of a head CU for chain CU 0.
+  // When every role of the replica runs on the block's XCD, the roles run their all-local build.
   __shared__ unsigned char s_xcd[WN_MAX_CHAIN + NHEAD + WN_MAX_LAYERS];
   __shared__ int s_me;
   unsigned lm = 0;
+  bool all_local = false;  // every role of the replica on this block's XCD
   if (g.local_posts) {
     // The XCD of every block is read at each launch, not assumed: each block stores its XCC_ID, the
     // grid meets once (a cooperative launch keeps every block resident), and each block builds its
@@ -954,6 +956,8 @@ __global__ __launch_bounds__(NT) void wn_chain_kernel(const WnChainArgs g) {
     const int me = s_me;
     auto same = [&](int r) { return s_xcd[r] == me; };
     const bool heads = same(g.nch) && same(g.nch + 1) && same(g.nch + 2) && same(g.nch + 3);
+    all_local = true;
+    for (int r = 0; r < per; ++r) all_local = all_local && same(r);
     if (role < g.nch) {
       const int j0 = g.layer_begin[role], nl = g.layer_begin[role + 1] - j0;
       for (int l = 0; l < nl; ++l) lm |= (unsigned)same(g.nch + NHEAD + (j0 + l) / g.nla) << l;
@@ -976,9 +980,13 @@ __global__ __launch_bounds__(NT) void wn_chain_kernel(const WnChainArgs g) {
   const int64_t tg0 = g.io.reset ? 0 : g.state[WN_STATE_WORDS * (size_t)b0];
   __syncthreads();
   Sync sy{&s_abort};
-  if (role < g.nch) chain_role<R, S, NLC, TF, MS, E2, AX>(g, role, b0, ns, dyn, sy, tg0, lm);
-  else if (role < g.nch + NHEAD) head_role<R, S, TF, MS>(g, role - g.nch, b0, ns, dyn, sy, tg0, lm);
-  else aux_role<R, S, TF, MS>(g, role - g.nch - NHEAD, b0, ns, dyn, sy, tg0, lm);
+  auto run = [&](auto loc) {
+    if (role < g.nch) chain_role<R, S, NLC, TF, MS, E2, AX>(g, role, b0, ns, dyn, sy, tg0, loc);
+    else if (role < g.nch + NHEAD) head_role<R, S, TF, MS>(g, role - g.nch, b0, ns, dyn, sy, tg0, loc);
+    else aux_role<R, S, TF, MS>(g, role - g.nch - NHEAD, b0, ns, dyn, sy, tg0, loc);
+  };
+  if (all_local) run(Local<true>{lm});
+  else run(Local<false>{lm});
 }
 
 // Clears the tagged histories and mailboxes and the status word before a run from zero.

@@ -401,9 +401,9 @@ constexpr size_t head_lds(int S) {
 // ------------------------------------------------------------------------------------------
 // chain CU: layers j0 .. j0 + nl - 1
 // ------------------------------------------------------------------------------------------
-template <int S, bool AX, bool I8, bool PAIR>
+template <int S, bool AX, bool I8, bool PAIR, class LM>
 __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, const int rep, float* dyn, Sync sy,
-                                         const int64_t tg0, const unsigned lm) {
+                                         const int64_t tg0, const LM lm) {
   using C = Cols<PAIR>;
   constexpr int NS = C::NS, XW = C::XW, PW = C::PW, TW = C::TW;
   constexpr int KS = S / 64;  // row tiles per wave of the last layer's W_skip (tail)
@@ -510,7 +510,7 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
           // x_{j-1}[t] goes into slot t mod d_j of layer j's history, which its aux CU reads at t + d_j
           u64* const hist = ring + ((size_t)hoff[l] + (size_t)slot[l] * R) * NS + ot;
           slot[l] = slot[l] + 1 == dil[l] ? 0 : slot[l] + 1;
-          if constexpr (!PAIR) stw4(hist, xr, tag, (lm >> l) & 1u);
+          if constexpr (!PAIR) stw4(hist, xr, tag, lm(l));
           if constexpr (I8) {
             const float4 st = *reinterpret_cast<const float4*>(SCL + l * 3 * R + m0);
             const float4 sg = *reinterpret_cast<const float4*>(SCL + l * 3 * R + R + m0);
@@ -521,8 +521,8 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
           put_split4<PAIR>(HS + sn * SR, m0, h, part);
           // h_j[t] -> the layer's aux CU (with paired columns lane n posts h, lane n + 8 the history row)
           u64* const hpost = mb + g.off_h + (size_t)j * XW + ot;
-          if constexpr (PAIR) stw4(p0 ? hpost : hist, p0 ? h : xr, tag, (lm >> l) & 1u);
-          else stw4(hpost, h, tag, (lm >> l) & 1u);
+          if constexpr (PAIR) stw4(p0 ? hpost : hist, p0 ? h : xr, tag, lm(l));
+          else stw4(hpost, h, tag, lm(l));
         }
         lds_barrier();
         if (j < L - 1) {  // x_l feeds nothing
@@ -542,7 +542,7 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
           put_split4<PAIR>(XS + ((l + 1) & 1) * NS * SR + sn * SR, m0, xr, part);
           if (l == nl - 1 && c + 1 < g.nch) {
             // x of my last layer -> the next chain CU
-            post4<PAIR>(mb + g.off_x + (size_t)(c + 1) * XW + ot, xr, tag, (lm >> 16) & 1u, part);
+            post4<PAIR>(mb + g.off_x + (size_t)(c + 1) * XW + ot, xr, tag, lm(16), part);
           }
           lds_barrier();
         }
@@ -572,7 +572,7 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
           acc = f32x4{s4.x * acc[0], s4.y * acc[1], s4.z * acc[2], s4.w * acc[3]};
         }
         post4<PAIR>(mb + g.off_qtail + rt * TW + (quad * NS + sn) * 4, v4(acc), tag,
-                    (lm >> 17) & 1u, part);
+                    lm(17), part);
       }
       lds_barrier();  // HS is rewritten in the next step's first layer
     }
@@ -582,9 +582,9 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
 // ------------------------------------------------------------------------------------------
 // aux CU: layers ja .. ja + nl - 1
 // ------------------------------------------------------------------------------------------
-template <int S, bool AX, bool I8, bool PAIR>
+template <int S, bool AX, bool I8, bool PAIR, class LM>
 __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const int rep, float* dyn, Sync sy,
-                                       const int64_t tg0, const unsigned lm) {
+                                       const int64_t tg0, const LM lm) {
   using C = Cols<PAIR>;
   constexpr int NS = C::NS, XW = C::XW, PW = C::PW, TW = C::TW;
   constexpr int KS = S / 64;  // row tiles of W_skip per wave
@@ -698,7 +698,7 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
   // posted with tag ts + 1
   auto post_pre = [&](int l, int64_t ts) __attribute__((always_inline)) {
     const unsigned tg = (unsigned)(ts + 1);
-    const bool loc = (lm >> l) & 1u;
+    const bool loc = lm(l);
     f32x4 pa[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
     prod2<PAIR>(pa[0], pa[1], wp[l][0][0], wp[l][0][1], wp[l][1][0], wp[l][1][1], HX + l * NS * SR + sn * SR, quad,
                 part);
@@ -798,7 +798,7 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
 #pragma unroll
               for (int k = 0; k < KS; ++k) qs[k] = fold8(qs[k]);
             }
-            const bool loc = (lm >> 16) & 1u;
+            const bool loc = lm(16);
 #pragma unroll
             for (int k = 0; k < KS; ++k)
               post4<PAIR>(mb + g.off_q + (size_t)ai * S * NS + lot(KS * wave + k), v4(qs[k]), tag, loc,
@@ -845,9 +845,9 @@ __device__ __forceinline__ void head_products(f32x4 (&acc)[4], const u32x4 (&w)[
 // head CU hh: columns 8 hh .. 8 hh + 7 of the replica's tiles (8 streams): the skip sum, the two head
 // layers, the draw and the next step's x0
 // ------------------------------------------------------------------------------------------
-template <int S, bool TF, bool AX, bool I8, bool PAIR>
+template <int S, bool TF, bool AX, bool I8, bool PAIR, class LM>
 __device__ __forceinline__ void mc_head(const WnChainArgs& g, const int hh, const int rep, float* dyn, Sync sy,
-                                        const int64_t tg0, const unsigned lm) {
+                                        const int64_t tg0, const LM lm) {
   using C = Cols<PAIR>;
   constexpr int NS = C::NS;
   constexpr int KTH = S / 32, KTO = A / 32;
@@ -945,7 +945,7 @@ __device__ __forceinline__ void mc_head(const WnChainArgs& g, const int hh, cons
       v = emb(EMB, SE, s_y[q], m) + BE[m];
       if (e2 && s_y2[q] >= 0) v += emb(EMBP, SEP, s_y2[q], m);
     }
-    stw(mb + g.off_x + tpos<NS>(m, c0 + q), pack(v, (unsigned)(tg0 + 1)), lm & 1u);
+    stw(mb + g.off_x + tpos<NS>(m, c0 + q), pack(v, (unsigned)(tg0 + 1)), lm(0));
   }
 
   // skip partials per step: one from each aux CU that posts one, then the last layer's from the last
@@ -1088,7 +1088,7 @@ __device__ __forceinline__ void mc_head(const WnChainArgs& g, const int hh, cons
           v = emb(EMB, SE, y, lane) + BE[lane];
           if (e2) v += emb(EMBP, SEP, yp, lane);
         }
-        stw(mb + g.off_x + tpos<NS>(lane, c0 + q), pack(v, tag + 1), lm & 1u);
+        stw(mb + g.off_x + tpos<NS>(lane, c0 + q), pack(v, tag + 1), lm(0));
       }
       if (lane == 0 && q < ns) {
         s_y2[q] = yp;
@@ -1132,8 +1132,10 @@ __global__ __launch_bounds__(NT, 1) void wn_mchain_kernel(const WnChainArgs ga) 
   // Which of this block's posts go to a reader on its own XCD in this launch: bit l of a chain CU for
   // the aux CU of its layer l (h and the history rows), bit 16 for the next chain CU, bit 17 for the
   // head CUs; bit l of an aux CU for the chain CU of its layer l, bit 16 for the head CUs; bit 0 of a
-  // head CU for chain CU 0.  The map is read at the launch (grid_meet).
+  // head CU for chain CU 0.  The map is read at the launch (grid_meet).  When every role of the
+  // replica runs on the block's XCD, the roles run their all-local build.
   unsigned lm = 0;
+  bool all_local = false;
   if (g.local_posts) {
     if (grid_meet(g.xmap, g.n_active, g.spin_limit, g.status, &s_me) < 0) return;  // WN_ETIMEOUT is in the status word
     for (int b = threadIdx.x; b < WN_CHAIN_GRID; b += NT) {
@@ -1149,6 +1151,8 @@ __global__ __launch_bounds__(NT, 1) void wn_mchain_kernel(const WnChainArgs ga) 
     const int me = s_me;
     auto same = [&](int r) { return s_xcd[r] == me; };
     const bool heads_same = same(head) && (C::NH == 1 || same(head + 1));
+    all_local = true;
+    for (int r = 0; r < per; ++r) all_local = all_local && same(r);
     if (role < head) {
       const int j0 = g.layer_begin[role], nl = g.layer_begin[role + 1] - j0;
       for (int l = 0; l < nl; ++l) lm |= (unsigned)same(aux0 + s_aof[j0 + l]) << l;
@@ -1167,9 +1171,13 @@ __global__ __launch_bounds__(NT, 1) void wn_mchain_kernel(const WnChainArgs ga) 
   const int64_t tg0 = g.io.reset ? 0 : g.state[WN_STATE_WORDS * (size_t)(k * g.G)];
   __syncthreads();
   Sync sy{&s_abort};
-  if (role < head) mc_chain<S, AX, I8, PAIR>(g, role, k, dyn, sy, tg0, lm);
-  else if (role < aux0) mc_head<S, TF, AX, I8, PAIR>(g, role - head, k, dyn, sy, tg0, lm);
-  else mc_aux<S, AX, I8, PAIR>(g, role - aux0, k, dyn, sy, tg0, lm);
+  auto run = [&](auto loc) {
+    if (role < head) mc_chain<S, AX, I8, PAIR>(g, role, k, dyn, sy, tg0, loc);
+    else if (role < aux0) mc_head<S, TF, AX, I8, PAIR>(g, role - head, k, dyn, sy, tg0, loc);
+    else mc_aux<S, AX, I8, PAIR>(g, role - aux0, k, dyn, sy, tg0, loc);
+  };
+  if (all_local) run(Local<true>{lm});
+  else run(Local<false>{lm});
 }
 
 // Layers of each chain CU: runs of at most NLC, as even as possible.
