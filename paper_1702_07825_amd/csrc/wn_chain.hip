@@ -694,10 +694,16 @@ __device__ __forceinline__ void chain_role(const WnChainArgs& g, const int c, co
 // ------------------------------------------------------------------------------------------
 // aux CU (nla consecutive layers): pre-activations of the next step and the skip partial
 // ------------------------------------------------------------------------------------------
-// Layers one aux CU can hold: W_prev and W_skip of a layer take 48 floats per lane at r = 64,
-// s = 256 (two layers fit the register file), 128 at r = 128 (one).
+// Layers one aux CU holds: W_prev and W_skip of a layer take 48 floats per lane at r = 64,
+// s = 256 (two layers fit the register file).  At r = 128 they take 128: the CU keeps both layers'
+// W_prev (64 floats per lane each) and the second layer's W_skip in VGPRs and the first layer's
+// W_skip in LDS (256 rows of 128 floats), so that an l = 20 replica (11 chain, 4 head, 10 aux CUs)
+// fits one XCD's 32 CUs.
 template <int R>
-constexpr int aux_max_layers() { return R <= 64 ? 2 : 1; }
+constexpr int aux_max_layers() { return 2; }
+// r = 128: the aux CU's first layer's W_skip is read from LDS
+template <int R>
+constexpr bool aux_skip_in_lds() { return R == 128; }
 
 template <int R, int S, bool TF, bool MS, class LM>
 __device__ __forceinline__ void aux_role(const WnChainArgs& g, const int ai, const int b0, const int ns, float* dyn, Sync sy,
@@ -705,6 +711,10 @@ __device__ __forceinline__ void aux_role(const WnChainArgs& g, const int ai, con
   using M = ChainMap<R>;
   constexpr int NLA = aux_max_layers<R>();
   constexpr int LPRS = NT / S, KCS = R / LPRS;
+  constexpr bool SKL = aux_skip_in_lds<R>();      // layer 0's W_skip in LDS
+  constexpr int NWK = SKL ? NLA - 1 : NLA;        // W_skip blocks in VGPRs (layers SKL ..)
+  constexpr int RPG = S / 64;                     // LDS skip product: rows per 8-lane group
+  constexpr int WSKA = lds_row_stride(R, RPG);    // and its row stride
   constexpr int CQ = (WN_CHAIN_MAX_G * 2 * R / 4 + NT - 1) / NT;  // conditioning float4s per thread and layer
   const int tid = threadIdx.x;
   const int L = g.d.L;
@@ -717,10 +727,13 @@ __device__ __forceinline__ void aux_role(const WnChainArgs& g, const int ai, con
   float* hs = dyn;                 // NLA*R     h_j of the current stream, one row per layer
   float* xpg = hs + NLA * R;       // NLA*G*R   history reads x_{j-1}[ts - d] of every (layer, stream)
   float* clg = xpg + NLA * G * R;  // NLA*G*2R  conditioning rows L[b, ts, j] of every (layer, stream)
+  float* wska = clg + NLA * G * 2 * R;  // SKL: S rows of stride WSKA, W_skip of layer ja
+  float* qsk = wska + S * WSKA;         // SKL: layer ja's skip projection of the current stream
+  const int gq = tid >> 3, li = tid & 7;  // 8-lane groups of the LDS product
 
   const int rowp = tid / M::LPR1, kq = tid % M::LPR1;
   const int rows = tid / LPRS, ks = tid % LPRS;
-  float wp[NLA][M::KC1], wk[NLA][KCS], bg[NLA];
+  float wp[NLA][M::KC1], wk[NWK][KCS], bg[NLA];
   int dl[NLA], ho[NLA];  // dilation and history offset of each layer (uniform, kept in registers)
   const float* Wp = static_cast<const float*>(g.w.w_prev);
   const float* Wk = static_cast<const float*>(g.w.w_skip);
@@ -729,12 +742,17 @@ __device__ __forceinline__ void aux_role(const WnChainArgs& g, const int ai, con
     const int j = ja + (l < nl ? l : 0);
 #pragma unroll
     for (int i = 0; i < M::KC1; ++i) wp[l][i] = Wp[((size_t)j * 2 * R + rowp) * R + kq * M::KC1 + i];
+    if (l >= (SKL ? 1 : 0)) {
 #pragma unroll
-    for (int i = 0; i < KCS; ++i) wk[l][i] = Wk[((size_t)j * S + rows) * R + ks * KCS + i];
+      for (int i = 0; i < KCS; ++i) wk[l - (SKL ? 1 : 0)][i] = Wk[((size_t)j * S + rows) * R + ks * KCS + i];
+    }
     bg[l] = g.w.b_gate[j * 2 * R + rowp];
     dl[l] = g.d.dil[j];
     ho[l] = g.d.hoff[j];
   }
+
+  if (SKL && nsk > 0)
+    for (int i = tid; i < S * R; i += NT) wska[(i / R) * WSKA + i % R] = Wk[(size_t)ja * S * R + i];
 
   // The history slot that pre_j[ts] reads for every stream of the replica (consecutive streams'
   // histories are hist_len words apart), j = ja + l.
@@ -831,10 +849,34 @@ __device__ __forceinline__ void aux_role(const WnChainArgs& g, const int ai, con
           }
           lds_barrier();
           if (sy.failed()) return;
-          if (l < nsk) {
-            q += gsum<LPRS>(dot_lds<KCS>(wk[l], hs + l * R + ks * KCS));
-            // the partial goes out as soon as its last layer is in: a later layer of this CU (the
-            // network's last, whose skip is on the chain) only paces the pre-activations
+          // the partial goes out as soon as its last layer is in: a later layer of this CU (the
+          // network's last, whose skip is on the chain) only paces the pre-activations
+          if (SKL && l == 0 && l < nsk) {
+            // W_skip from LDS: 8-lane group q takes rows RPG q .. RPG q + RPG - 1, lane i the
+            // chunks i, i + 8, ... of each row; a full sum ends on a lane pair of every row
+            float p[RPG];
+#pragma unroll
+            for (int rr = 0; rr < RPG; ++rr) p[rr] = 0.f;
+#pragma unroll
+            for (int m = 0; m < R / 32; ++m) {
+              const int k = 4 * (li + 8 * m);
+              const float4 v = *reinterpret_cast<const float4*>(hs + l * R + k);
+#pragma unroll
+              for (int rr = 0; rr < RPG; ++rr) {
+                const float4 a = *reinterpret_cast<const float4*>(wska + (RPG * gq + rr) * WSKA + k);
+                p[rr] = fmaf(a.x, v.x, fmaf(a.y, v.y, fmaf(a.z, v.z, fmaf(a.w, v.w, p[rr]))));
+              }
+            }
+            const float qv = xreduce8<RPG>(p, li);
+            const int m = RPG * gq + ((li & 4) ? RPG / 2 : 0) + (RPG == 4 && (li & 2) ? 1 : 0);
+            if ((RPG == 4 ? (li & 1) : (li & 3)) == 0) {
+              if (nsk == 1) stw(mbs + g.off_q + (size_t)ai * S + m, pack(qv, (unsigned)(t + 1)), lm(16));
+              else qsk[m] = qv;  // read by the next layer's lanes of row m, after its barrier
+            }
+          } else if (l < nsk) {
+            float qq = gsum<LPRS>(dot_lds<KCS>(wk[l - (SKL ? 1 : 0)], hs + l * R + ks * KCS));
+            if (SKL && l == 1) qq += qsk[rows];
+            q += qq;
             if (l == nsk - 1 && ks == 0)
               stw(mbs + g.off_q + (size_t)ai * S + rows, pack(q, (unsigned)(t + 1)), lm(16));
           }
@@ -1041,9 +1083,10 @@ size_t chain_lds_floats(int R, int S, int nlc, int G, int ub, int nch, int tail,
   return common + var;
 }
 size_t head_lds_floats(int L, int S) { return (size_t)L * S + S + HR + 2 * NT; }
-size_t aux_lds_floats(int R, int G) {
+size_t aux_lds_floats(int R, int S, int G) {
   const size_t nla = R <= 64 ? aux_max_layers<64>() : aux_max_layers<128>();
-  return nla * ((size_t)R + (size_t)3 * R * G);
+  const bool skl = R <= 64 ? aux_skip_in_lds<64>() : aux_skip_in_lds<128>();
+  return nla * ((size_t)R + (size_t)3 * R * G) + (skl ? (size_t)S * lds_row_stride(R, S / 64) + S : 0);
 }
 constexpr size_t kMaxLds = 160 * 1024;
 
@@ -1052,7 +1095,7 @@ hipError_t launch_chain_rs(const WnChainArgs& g, bool teacher, hipStream_t strea
   constexpr int NLC = chain_nlc<R>();
   const size_t dyn = sizeof(float) * std::max(chain_lds_floats(R, S, NLC, g.G, g.ub, g.nch, g.tail_on_chain,
                                                                 g.w.embed_prev != nullptr),
-                                              std::max(head_lds_floats(g.d.L, S), aux_lds_floats(R, g.G)));
+                                              std::max(head_lds_floats(g.d.L, S), aux_lds_floats(R, S, g.G)));
   void* args[] = {const_cast<WnChainArgs*>(&g)};
   // one stream (no replicas) gets a build with the stream loops folded away, a one-table
   // embedding one without the second table's load; the approximate nonlinearities are built
@@ -1106,6 +1149,7 @@ bool wn_chain_plan(int L, int R, int S, int B, bool two_taps, WnChainPlan* p) {
   q.G = (B + std::min(B, max_rep) - 1) / std::min(B, max_rep);
   q.nrep = (B + q.G - 1) / q.G;
   if (q.G > WN_CHAIN_MAX_G) return false;
+  if (aux_lds_floats(R, S, q.G) * sizeof(float) > kMaxLds) return false;
   int gp = 1;
   while (gp < q.G) gp *= 2;
   q.ub = std::max(16, 512 / gp);

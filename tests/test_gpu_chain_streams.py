@@ -33,11 +33,11 @@ def _setup(L, r, s, dil, B, T, seed, bias=0.0):
 
 CASES = [
     # name, L, r, s, dilations, B, T, bias
-    # (replicas x streams per replica; a replica is nch chain + 4 head + ceil(L / nla) aux CUs, with
-    # nla = 2 layers per aux CU at r <= 64 and 1 at r = 128)
-    ("l20_r128_b11", 20, 128, 256, tuple(synth.dilation_cycle(20)), 11, 300, 0.2),  # 6 x 2 (last 1), 35 CUs each
+    # (replicas x streams per replica; a replica is nch chain + 4 head + ceil(L / 2) aux CUs: two
+    # layers per aux CU, at r = 128 with the first layer's W_skip in LDS)
+    ("l20_r128_b11", 20, 128, 256, tuple(synth.dilation_cycle(20)), 11, 300, 0.2),  # 6 x 2 (last 1), 25 CUs each
     ("l20_r64_b12", 20, 64, 256, tuple(synth.dilation_cycle(20)), 12, 300, 0.0),    # 12 x 1, 17 CUs each
-    ("l3_r128_b5", 3, 128, 256, (1, 3, 2), 5, 200, 0.3),                             # 5 x 1, 10 CUs each
+    ("l3_r128_b5", 3, 128, 256, (1, 3, 2), 5, 200, 0.3),                             # 5 x 1, 9 CUs each
     ("l1_r128_b2", 1, 128, 256, (1,), 2, 150, 0.4),                                  # one chain CU, skip on aux
     ("l5_r128_b3", 5, 128, 256, (2, 1, 4, 1, 3), 3, 200, 0.3),                      # chain CUs of 1, 2, 1, 1 layers
     ("l9_r32_b40", 9, 32, 128, (1, 2, 4, 8, 16, 32, 64, 128, 256), 40, 200, 0.2),    # 20 x 2, 10 CUs each
@@ -52,8 +52,8 @@ CASES = [
 
 
 # (workgroups, replicas) wn_launch_info reports for the layouts stated above
-LAUNCH = {"l20_r128_b11": (210, 6), "l20_r64_b12": (204, 12), "l3_r128_b5": (50, 5), "l1_r128_b2": (12, 2),
-          "l5_r128_b3": (39, 3), "l9_r32_b40": (200, 20), "l20_r64_b240": (255, 15), "l64_r64_b1": (46, 1),
+LAUNCH = {"l20_r128_b11": (150, 6), "l20_r64_b12": (204, 12), "l3_r128_b5": (45, 5), "l1_r128_b2": (12, 2),
+          "l5_r128_b3": (33, 3), "l9_r32_b40": (200, 20), "l20_r64_b240": (255, 15), "l64_r64_b1": (46, 1),
           "l7_r64_d1s_b2": (18, 2)}
 
 
@@ -190,14 +190,15 @@ def test_same_xcd_posts_change_nothing(L, r, B, monkeypatch):
     assert torch.equal(out["0"][1], out["1"][1])
 
 
-@pytest.mark.parametrize("L,B,dil", [(20, 1, None), (40, 2, None), (9, 3, (1, 1, 2, 1, 8, 1, 3, 1, 2))])
-def test_one_and_two_layers_per_aux_cu_agree(L, B, dil, monkeypatch):
-    """Aux CUs holding two layers each (the default at r = 64) or one (WN_AUX_LAYERS=1): the same
-    model gives the same logits up to the order of the skip sums, and each layout's samples match the
-    oracle at every confident step."""
-    r, s, T = 64, 256, 300
+@pytest.mark.parametrize("L,r,B,dil", [(20, 64, 1, None), (40, 64, 2, None), (9, 64, 3, (1, 1, 2, 1, 8, 1, 3, 1, 2)),
+                                        (20, 128, 3, None), (5, 128, 2, (1, 2, 1, 4, 1))])
+def test_one_and_two_layers_per_aux_cu_agree(L, r, B, dil, monkeypatch):
+    """Aux CUs holding two layers each (the default) or one (WN_AUX_LAYERS=1; at r = 128 every aux
+    CU then reads its layer's W_skip from LDS): the same model gives the same logits up to the order
+    of the skip sums, and each layout's samples match the oracle at every confident step."""
+    s, T = 256, 300
     dil = tuple(synth.dilation_cycle(L)) if dil is None else dil
-    print("aux layouts L=%d B=%d" % (L, B), flush=True)
+    print("aux layouts L=%d r=%d B=%d" % (L, r, B), flush=True)
     w, net, cond, u, model = _setup(L, r, s, dil, B, T, seed=31 + L, bias=0.2)
     ys, lgs = [], []
     for nla in ("2", "1"):
