@@ -217,14 +217,17 @@ __device__ __forceinline__ float dot_lds(const float (&w)[K], const float* x, fl
 // Two embedding tables fit chain CU 0's LDS beside its other buffers up to r = 64.
 constexpr bool e2_in_lds(int R) { return R <= 64; }
 
-template <int R, int S, int NLC, bool TF, bool MS, bool E2, bool AX, class LM>
+// NLK > 0: this CU holds NLK layers, a compile-time count, so that no layer of the unrolled loop
+// tests a run-time count (measured ~0.06 us per layer, in reloads of spilled masks and branches);
+// NLK = 0: the count is read at run time.
+template <int R, int S, int NLC, bool TF, bool MS, bool E2, bool AX, int NLK, class LM>
 __device__ __forceinline__ void chain_role(const WnChainArgs& g, const int c, const int b0, const int ns, float* dyn, Sync sy,
                            const int64_t tg0, const LM lm) {
   constexpr bool E2L = E2 && e2_in_lds(R);
   using M = ChainMap<R>;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int L = g.d.L;
-  const int j0 = g.layer_begin[c], nl = g.layer_begin[c + 1] - j0;
+  const int j0 = g.layer_begin[c], nl = NLK > 0 ? NLK : g.layer_begin[c + 1] - j0;
   const bool first = (c == 0);
   const bool lastc = (c + 1 == g.nch);
   const bool tail = lastc && g.tail_on_chain;
@@ -503,7 +506,8 @@ __device__ __forceinline__ void chain_role(const WnChainArgs& g, const int c, co
       for (int l = 0; l < NLC; ++l) {
         if (l < nl) {
           const int j = j0 + l;
-          if (j == L - 1 && tid < R) xbuf[l * R + tid] = xs[tid];
+          const bool last_layer = lastc && l == nl - 1;  // j == L - 1
+          if (last_layer && tid < R) xbuf[l * R + tid] = xs[tid];
           // a = W_cur x + pre ; h = tanh(a[0:R]) * sigmoid(a[R:2R]).  Each lane ends with both rows
           // of a pair; the first lane of a group starts its partial sums from pre, so pre joins
           // the reduction.
@@ -579,7 +583,7 @@ __device__ __forceinline__ void chain_role(const WnChainArgs& g, const int c, co
           }
           lds_barrier();
           // x_j = x_{j-1} + W_res h + B_res (x_l feeds nothing); x_{j-1} is kept for the history
-          if (j < L - 1) {
+          if (!last_layer) {
             if constexpr (M::G8) {
               // lower four lanes: row 2q, upper four: row 2q + 1.  x_{j-1} + B_res of the row joins
               // the reduction through lane 0 (row 2q) and lane 4 (row 2q + 1); every lane reads
@@ -1023,7 +1027,16 @@ __global__ __launch_bounds__(NT) void wn_chain_kernel(const WnChainArgs g) {
   __syncthreads();
   Sync sy{&s_abort};
   auto run = [&](auto loc) {
-    if (role < g.nch) chain_role<R, S, NLC, TF, MS, E2, AX>(g, role, b0, ns, dyn, sy, tg0, loc);
+    if (role < g.nch) {
+      // the all-local one-stream build also fixes the layer count of the common chain CUs at compile
+      // time (with the stream loop, those builds spill)
+      const int nl = g.layer_begin[role + 1] - g.layer_begin[role];
+      constexpr bool FIX = std::is_same<decltype(loc), Local<true>>::value && !MS;
+      constexpr int K1 = FIX ? NLC : 0, K2 = (FIX && NLC > 1) ? NLC - 1 : 0;
+      if (K1 > 0 && nl == K1) chain_role<R, S, NLC, TF, MS, E2, AX, K1>(g, role, b0, ns, dyn, sy, tg0, loc);
+      else if (K2 > 0 && nl == K2) chain_role<R, S, NLC, TF, MS, E2, AX, K2>(g, role, b0, ns, dyn, sy, tg0, loc);
+      else chain_role<R, S, NLC, TF, MS, E2, AX, 0>(g, role, b0, ns, dyn, sy, tg0, loc);
+    }
     else if (role < g.nch + NHEAD) head_role<R, S, TF, MS>(g, role - g.nch, b0, ns, dyn, sy, tg0, loc);
     else aux_role<R, S, TF, MS>(g, role - g.nch - NHEAD, b0, ns, dyn, sy, tg0, loc);
   };
