@@ -401,7 +401,9 @@ constexpr size_t head_lds(int S) {
 // ------------------------------------------------------------------------------------------
 // chain CU: layers j0 .. j0 + nl - 1
 // ------------------------------------------------------------------------------------------
-template <int S, bool AX, bool I8, bool PAIR, class LM>
+// NLK > 0: this CU holds NLK layers, a compile-time count, so that no layer of the unrolled loop
+// tests a run-time count; NLK = 0: the count is read at run time.
+template <int S, bool AX, bool I8, bool PAIR, int NLK, class LM>
 __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, const int rep, float* dyn, Sync sy,
                                          const int64_t tg0, const LM lm) {
   using C = Cols<PAIR>;
@@ -412,8 +414,9 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
   const int n = lane & 15, quad = lane >> 4;
   const int sn = PAIR ? (n & 7) : n, part = PAIR ? (n >> 3) : 0;  // this lane's stream and part
   const int L = g.d.L, T = g.io.T;
-  const int j0 = g.layer_begin[c], nl = g.layer_begin[c + 1] - j0;
-  const bool tail = c + 1 == g.nch && g.tail_on_chain;
+  const int j0 = g.layer_begin[c], nl = NLK > 0 ? NLK : g.layer_begin[c + 1] - j0;
+  const bool lastc = c + 1 == g.nch;
+  const bool tail = lastc && g.tail_on_chain;
   u64* const mb = g.mb + (size_t)rep * g.mb_words;
   u64* const ring = g.ring + (size_t)rep * g.d.hist_len * NS;
   const wrsrc rs = tagged_region(g);
@@ -525,7 +528,7 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
           else stw4(hpost, h, tag, lm(l));
         }
         lds_barrier();
-        if (j < L - 1) {  // x_l feeds nothing
+        if (!(lastc && l == nl - 1)) {  // j < L - 1: x_l feeds nothing
           // x_j = x_{j-1} + W_res h + B_res
           const float4 br = *reinterpret_cast<const float4*>(BRS + l * R + m0);
           f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -540,7 +543,7 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
             xr = v4(acc);
           }
           put_split4<PAIR>(XS + ((l + 1) & 1) * NS * SR + sn * SR, m0, xr, part);
-          if (l == nl - 1 && c + 1 < g.nch) {
+          if (l == nl - 1 && !lastc) {
             // x of my last layer -> the next chain CU
             post4<PAIR>(mb + g.off_x + (size_t)(c + 1) * XW + ot, xr, tag, lm(16), part);
           }
@@ -1172,7 +1175,15 @@ __global__ __launch_bounds__(NT, 1) void wn_mchain_kernel(const WnChainArgs ga) 
   __syncthreads();
   Sync sy{&s_abort};
   auto run = [&](auto loc) {
-    if (role < head) mc_chain<S, AX, I8, PAIR>(g, role, k, dyn, sy, tg0, loc);
+    if (role < head) {
+      // the all-local build also fixes the layer count of the common chain CUs at compile time
+      const int nl = g.layer_begin[role + 1] - g.layer_begin[role];
+      constexpr bool FIX = std::is_same<decltype(loc), Local<true>>::value;
+      constexpr int K1 = FIX ? NLC : 0, K2 = (FIX && NLC > 1) ? NLC - 1 : 0;
+      if (K1 > 0 && nl == K1) mc_chain<S, AX, I8, PAIR, K1>(g, role, k, dyn, sy, tg0, loc);
+      else if (K2 > 0 && nl == K2) mc_chain<S, AX, I8, PAIR, K2>(g, role, k, dyn, sy, tg0, loc);
+      else mc_chain<S, AX, I8, PAIR, 0>(g, role, k, dyn, sy, tg0, loc);
+    }
     else if (role < aux0) mc_head<S, TF, AX, I8, PAIR>(g, role - head, k, dyn, sy, tg0, loc);
     else mc_aux<S, AX, I8, PAIR>(g, role - aux0, k, dyn, sy, tg0, loc);
   };
