@@ -211,6 +211,25 @@ __device__ __forceinline__ float dot_lds(const float (&w)[K], const float* x, fl
   return s0 + s1;
 }
 
+// The same over a group of G lanes that share a row, in 16-byte chunks: this lane takes chunks
+// c, c + G, c + 2 G, ... of the input vector (x points at its first chunk) and w holds its weights
+// in that order.  Consecutive lanes read consecutive chunks, so the group's reads fall on distinct
+// LDS banks (a lane-contiguous split with K >= 32 puts every other lane on the same banks).
+template <int K, int G>
+__device__ __forceinline__ float dot_lds_il(const float (&w)[K], const float* x) {
+  static_assert(K % 4 == 0, "whole chunks");
+  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+#pragma unroll
+  for (int m = 0; m < K / 4; ++m) {
+    const float4 v = *reinterpret_cast<const float4*>(x + 4 * G * m);
+    s0 = fmaf(w[4 * m], v.x, s0);
+    s1 = fmaf(w[4 * m + 1], v.y, s1);
+    s2 = fmaf(w[4 * m + 2], v.z, s2);
+    s3 = fmaf(w[4 * m + 3], v.w, s3);
+  }
+  return (s0 + s1) + (s2 + s3);
+}
+
 // ------------------------------------------------------------------------------------------
 // chain CU
 // ------------------------------------------------------------------------------------------
@@ -391,6 +410,12 @@ __device__ __forceinline__ void chain_role(const WnChainArgs& g, const int c, co
         *reinterpret_cast<float4*>(g.io.logits + ((size_t)(b0 + i) * T + (size_t)(ts - tg0)) * A + 4 * lane) = lv;
         y = reinterpret_cast<const int*>(ubuf)[at];
         y = y < 0 ? 0 : (y > A - 1 ? A - 1 : y);
+      } else if (g.io.smode == WN_DRAW_DIRECT || g.io.smode == WN_DRAW_TEMPERATURE) {
+        const float4 lv1[1] = {lv};
+        const float u1[1] = {ubuf[at]};
+        int y1[1];
+        wave_draw_cdf<AX>(lv1, u1, g.io.smode == WN_DRAW_TEMPERATURE ? g.io.inv_t : 1.0f, y1);
+        y = y1[0];
       } else {
         y = wave_draw<AX>(lv, ubuf[at], g.io.smode, g.io.inv_t, g.io.top_k, lane);
       }
@@ -920,7 +945,7 @@ __device__ __forceinline__ void head_role(const WnChainArgs& g, const int hh, co
   const float* Wl = static_cast<const float*>(g.w.w_relu);
   const float* Wo = static_cast<const float*>(g.w.w_out);
 #pragma unroll
-  for (int i = 0; i < KCH; ++i) wl[i] = Wl[(size_t)(hh * HR + rl) * S + kr * KCH + i];
+  for (int i = 0; i < KCH; ++i) wl[i] = Wl[(size_t)(hh * HR + rl) * S + 4 * (kr + LPRH * (i / 4)) + i % 4];
 #pragma unroll
   for (int i = 0; i < KCO; ++i) wo[i] = Wo[(size_t)oo * A + hh * HR + ko * KCO + i];
   const float bl = g.w.b_relu[hh * HR + rl];
@@ -953,7 +978,7 @@ __device__ __forceinline__ void head_role(const WnChainArgs& g, const int hh, co
       }
       lds_barrier();
       {
-        const float v = gsum<LPRH>(dot_lds<KCH>(wl, zs + kr * KCH));
+        const float v = gsum<LPRH>(dot_lds_il<KCH, LPRH>(wl, zs + 4 * kr));
         if (kr == 0) za[rl] = fmaxf(v + bl, 0.f);
       }
       lds_barrier();
