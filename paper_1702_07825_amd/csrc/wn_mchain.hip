@@ -585,7 +585,8 @@ __device__ __forceinline__ void mc_chain(const WnChainArgs& g, const int c, cons
 // ------------------------------------------------------------------------------------------
 // aux CU: layers ja .. ja + nl - 1
 // ------------------------------------------------------------------------------------------
-template <int S, bool AX, bool I8, bool PAIR, class LM>
+// NLK > 0: this CU holds NLK layers, a compile-time count; NLK = 0: read at run time.
+template <int S, bool AX, bool I8, bool PAIR, int NLK, class LM>
 __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const int rep, float* dyn, Sync sy,
                                        const int64_t tg0, const LM lm) {
   using C = Cols<PAIR>;
@@ -596,7 +597,7 @@ __device__ __forceinline__ void mc_aux(const WnChainArgs& g, const int ai, const
   const int n = lane & 15, quad = lane >> 4;
   const int sn = PAIR ? (n & 7) : n, part = PAIR ? (n >> 3) : 0;
   const int L = g.d.L, T = g.io.T;
-  const int ja = g.aux_begin[ai], nl = g.aux_begin[ai + 1] - ja;  // nl <= NLA
+  const int ja = g.aux_begin[ai], nl = NLK > 0 ? NLK : g.aux_begin[ai + 1] - ja;  // nl <= NLA
   // layers whose skip projection this CU computes (the last layer's runs on the last chain CU)
   const int nsk = (g.tail_on_chain && ja + nl == L) ? nl - 1 : nl;
   const int b0 = rep * g.G, ns = min(g.G, g.io.B - b0);
@@ -1185,7 +1186,16 @@ __global__ __launch_bounds__(NT, 1) void wn_mchain_kernel(const WnChainArgs ga) 
       else mc_chain<S, AX, I8, PAIR, 0>(g, role, k, dyn, sy, tg0, loc);
     }
     else if (role < aux0) mc_head<S, TF, AX, I8, PAIR>(g, role - head, k, dyn, sy, tg0, loc);
-    else mc_aux<S, AX, I8, PAIR>(g, role - aux0, k, dyn, sy, tg0, loc);
+    else {
+      // and the aux CUs' runs of the default l = 20 plan (5, 5, 5, 3, 2 layers)
+      const int ai = role - aux0, na = g.aux_begin[ai + 1] - g.aux_begin[ai];
+      constexpr bool FIX = std::is_same<decltype(loc), Local<true>>::value;
+      constexpr int A1 = FIX ? NLA : 0, A2 = FIX ? 3 : 0, A3 = FIX ? 2 : 0;
+      if (A1 > 0 && na == A1) mc_aux<S, AX, I8, PAIR, A1>(g, ai, k, dyn, sy, tg0, loc);
+      else if (A2 > 0 && na == A2) mc_aux<S, AX, I8, PAIR, A2>(g, ai, k, dyn, sy, tg0, loc);
+      else if (A3 > 0 && na == A3) mc_aux<S, AX, I8, PAIR, A3>(g, ai, k, dyn, sy, tg0, loc);
+      else mc_aux<S, AX, I8, PAIR, 0>(g, ai, k, dyn, sy, tg0, loc);
+    }
   };
   if (all_local) run(Local<true>{lm});
   else run(Local<false>{lm});
