@@ -45,8 +45,8 @@
  *                            memory instead of stopping same-XCD messages at the XCD's L2
  *      WN_GROUP_STREAMS=8|16 each call: streams per workgroup of the batched bf16 kernel
  *      WN_AUX_LAYERS=n       each call: layers per aux CU of the multi-CU kernels (fp32: 1 instead
- *                            of two at r <= 64; MFMA: 1..5 instead of 5); it changes the launch
- *                            layout and the workspace size
+ *                            of two; MFMA: 1..5 instead of the default runs); it changes the
+ *                            launch layout and the workspace size
  *      WN_MFMA_COLUMNS=16    each call: the multi-CU MFMA kernel carries 16 streams per replica
  *                            (one per tile column) also where 8 in paired columns would do
  *    Apart from a small WN_SPIN_LIMIT, which can make a wait time out, none of them changes a
