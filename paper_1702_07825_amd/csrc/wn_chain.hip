@@ -14,16 +14,19 @@
 //              compute, per layer, a = W_cur x + pre, h = tanh(a_h) sigmoid(a_g),
 //              x += W_res h + B_res.  Chain CU 0 also holds the embedding table in
 //              LDS, sums the head's partial logits and draws the sample.
-//   aux CUs    (one per layer) hold W_prev and W_skip in VGPRs.  For the NEXT step
-//              they compute pre = W_prev x[t+1-d] + B + L[t+1] (so the dilated half,
-//              the bias and the HBM read of the conditioning all happen a step
-//              early), and for the current step the skip partial W_skip h.
+//   aux CUs    (two consecutive layers each) hold W_prev and W_skip in VGPRs (at
+//              r = 128 the first layer's W_skip in LDS).  For the NEXT step they
+//              compute pre = W_prev x[t+1-d] + B + L[t+1] (so the dilated half, the
+//              bias and the HBM read of the conditioning all happen a step early), and
+//              for the current step the skip partial W_skip h summed over their layers.
 //   head CUs   (four) hold 64 rows of W_relu and the matching 64 columns of W_out:
 //              z_a = relu(W_relu relu(q) + B_relu) for their rows and the partial
 //              logits W_out[:, rows] z_a[rows].
 //
 // Messages between CUs are vectors of 64-bit words (fp32 value in the low half,
-// step + 1 in the high half) written and read with relaxed agent-scope atomics.
+// step + 1 in the high half), written with relaxed atomic stores (workgroup scope when
+// the reader runs on the writer's XCD, else agent scope) and read in pairs with
+// 128-bit agent-scope loads.
 // Every word carries its own step tag, so a reader needs no fence: it re-reads a
 // word until the tag it expects appears.  Each mailbox has one slot: per stream, a
 // producer writes step t + 1 only after something that depends on its consumer's

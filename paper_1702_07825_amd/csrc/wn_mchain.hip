@@ -16,7 +16,9 @@
 //   paired   8 streams per replica: column n < 8 holds the hi part of stream n and column n + 8 its
 //            lo part, so one MFMA per 32 inputs does the work of two, and fold8 (row_ror:8) adds the
 //            halves, leaving lanes n and n + 8 with the same sums.  The two lanes then share the
-//            gate (one takes the tanh, the other the sigmoid) and the posts.  One head CU.
+//            gates (each evaluates two of its four whole and they swap results; the Appendix C
+//            forms split each gate into the tanh and the sigmoid instead) and the posts.  One
+//            head CU.
 //   16-wide  16 streams per replica, one per column, two MFMAs per 32 inputs (hi, lo); two head
 //            CUs of 8 streams each.  Used when the paired replicas cannot carry the batch.
 //
