@@ -45,6 +45,9 @@ CASES = [
     ("l20_r64_b240", 20, 64, 256, tuple(synth.dilation_cycle(20)), 240, 40, 0.1),
     # the most layers the library takes: 10 chain CUs of up to 7 layers, 32 aux CUs
     ("l64_r64_b1", 64, 64, 256, tuple(synth.dilation_cycle(64)), 1, 120, 0.1),
+    # one stream with chain CUs of 5 and 4 layers: the one-stream build whose layer counts are read at
+    # run time (7- and 6-layer chain CUs get builds with the count fixed)
+    ("l9_r64_b1", 9, 64, 256, (1, 2, 4, 8, 16, 32, 64, 128, 256), 1, 300, 0.2),       # 1 x 1, 11 CUs
     # two d = 1 layers on one aux CU (both history reads wait for the chain CU's step), an odd layer
     # count whose last aux CU holds only the last layer (its skip projection is on the chain)
     ("l7_r64_d1s_b2", 7, 64, 256, (1, 1, 2, 1, 1, 4, 1), 2, 200, 0.3),               # 2 x 1, 10 CUs each
@@ -53,7 +56,7 @@ CASES = [
 
 # (workgroups, replicas) wn_launch_info reports for the layouts stated above
 LAUNCH = {"l20_r128_b11": (150, 6), "l20_r64_b12": (204, 12), "l3_r128_b5": (45, 5), "l1_r128_b2": (12, 2),
-          "l5_r128_b3": (33, 3), "l9_r32_b40": (200, 20), "l20_r64_b240": (255, 15), "l64_r64_b1": (46, 1),
+          "l5_r128_b3": (33, 3), "l9_r32_b40": (200, 20), "l20_r64_b240": (255, 15), "l64_r64_b1": (46, 1), "l9_r64_b1": (11, 1),
           "l7_r64_d1s_b2": (18, 2)}
 
 
