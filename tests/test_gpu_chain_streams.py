@@ -135,17 +135,19 @@ def test_multi_stream_chain_matches_per_stream_kernel(monkeypatch):
     net.close()
 
 
-def test_timeout_path_drains_and_recovers(monkeypatch):
+@pytest.mark.parametrize("B", [1, 2])
+def test_timeout_path_drains_and_recovers(B, monkeypatch):
     """Every wait of the multi-CU kernel is bounded.  With the host's spin limit forced to one
     poll, a launch must end with WN_ETIMEOUT in the status word (every block leaves, so the call
-    returns), and the next call that starts from zero on the same workspace must run cleanly."""
+    returns), and the next call that starts from zero on the same workspace must run cleanly.
+    B = 1 runs the one-stream build (fixed layer counts), B = 2 the multi-stream one."""
     import paper_1702_07825_amd as wn
-    L, r, s, dil, B, T = 20, 64, 256, tuple(synth.dilation_cycle(20)), 2, 50
+    L, r, s, dil, T = 20, 64, 256, tuple(synth.dilation_cycle(20)), 50
     w, net, cond, u, model = _setup(L, r, s, dil, B, T, seed=77, bias=0.1)
     assert net.kernel_variant(B) == "multi_cu_chain"
     ws = net.new_workspace(B)
     monkeypatch.setenv("WN_SPIN_LIMIT", "1")
-    print("forced timeout run", flush=True)
+    print("forced timeout run, B=%d" % B, flush=True)
     net.generate(cond, u, workspace=ws)
     assert net.status(ws) == wn.WN_ETIMEOUT
     monkeypatch.delenv("WN_SPIN_LIMIT")
