@@ -756,10 +756,11 @@ __device__ __forceinline__ void aux_role(const WnChainArgs& g, const int ai, con
   // layers whose skip projection this CU computes (the last layer's runs on the last chain CU when
   // it has room for that W_skip); their sum goes to the head CUs as one partial per step
   const int nsk = (g.tail_on_chain && ja + nl == L) ? nl - 1 : nl;
-  float* hs = dyn;                 // NLA*R     h_j of the current stream, one row per layer
-  float* xpg = hs + NLA * R;       // NLA*G*R   history reads x_{j-1}[ts - d] of every (layer, stream)
-  float* clg = xpg + NLA * G * R;  // NLA*G*2R  conditioning rows L[b, ts, j] of every (layer, stream)
-  float* wska = clg + NLA * G * 2 * R;  // SKL: S rows of stride WSKA, W_skip of layer ja
+  // LDS, carved for the plan's layers per aux CU (g.nla <= NLA)
+  float* hs = dyn;                     // nla*R     h_j of the current stream, one row per layer
+  float* xpg = hs + g.nla * R;         // nla*G*R   history reads x_{j-1}[ts - d] of every (layer, stream)
+  float* clg = xpg + g.nla * G * R;    // nla*G*2R  conditioning rows L[b, ts, j] of every (layer, stream)
+  float* wska = clg + g.nla * G * 2 * R;  // SKL: S rows of stride WSKA, W_skip of layer ja
   float* qsk = wska + S * WSKA;         // SKL: layer ja's skip projection of the current stream
   const int gq = tid >> 3, li = tid & 7;  // 8-lane groups of the LDS product
 
@@ -1124,10 +1125,9 @@ size_t chain_lds_floats(int R, int S, int nlc, int G, int ub, int nch, int tail,
   return common + var;
 }
 size_t head_lds_floats(int L, int S) { return (size_t)L * S + S + HR + 2 * NT; }
-size_t aux_lds_floats(int R, int S, int G) {
-  const size_t nla = R <= 64 ? aux_max_layers<64>() : aux_max_layers<128>();
+size_t aux_lds_floats(int R, int S, int G, int nla) {
   const bool skl = R <= 64 ? aux_skip_in_lds<64>() : aux_skip_in_lds<128>();
-  return nla * ((size_t)R + (size_t)3 * R * G) + (skl ? (size_t)S * lds_row_stride(R, S / 64) + S : 0);
+  return (size_t)nla * ((size_t)R + (size_t)3 * R * G) + (skl ? (size_t)S * lds_row_stride(R, S / 64) + S : 0);
 }
 constexpr size_t kMaxLds = 160 * 1024;
 
@@ -1136,7 +1136,7 @@ hipError_t launch_chain_rs(const WnChainArgs& g, bool teacher, hipStream_t strea
   constexpr int NLC = chain_nlc<R>();
   const size_t dyn = sizeof(float) * std::max(chain_lds_floats(R, S, NLC, g.G, g.ub, g.nch, g.tail_on_chain,
                                                                 g.w.embed_prev != nullptr),
-                                              std::max(head_lds_floats(g.d.L, S), aux_lds_floats(R, S, g.G)));
+                                              std::max(head_lds_floats(g.d.L, S), aux_lds_floats(R, S, g.G, g.nla)));
   void* args[] = {const_cast<WnChainArgs*>(&g)};
   // one stream (no replicas) gets a build with the stream loops folded away, a one-table
   // embedding one without the second table's load; the approximate nonlinearities are built
@@ -1177,20 +1177,25 @@ bool wn_chain_plan(int L, int R, int S, int B, bool two_taps, WnChainPlan* p) {
   WnChainPlan q{};
   const int nlc = nlc_for(R);
   q.nch = chain_split(L, R, q.layer_begin);
-  // layers per aux CU: as many as fit its registers (WN_AUX_LAYERS=1 keeps one layer each)
-  q.nla = R <= 64 ? aux_max_layers<64>() : aux_max_layers<128>();
+  // layers per aux CU: as many as fit its registers (WN_AUX_LAYERS=1 keeps one layer each), fewer
+  // where the aux CUs' staging of more streams per replica would not fit their LDS (r = 128)
+  int nla_max = R <= 64 ? aux_max_layers<64>() : aux_max_layers<128>();
   if (const char* e = std::getenv("WN_AUX_LAYERS")) {
     const int v = std::atoi(e);
-    if (v >= 1 && v <= q.nla) q.nla = v;
+    if (v >= 1 && v <= nla_max) nla_max = v;
   }
-  q.naux = (L + q.nla - 1) / q.nla;
-  // as many replicas as the grid holds, the streams spread evenly over them
-  const int per = q.nch + NHEAD + q.naux;
-  const int max_rep = WN_CHAIN_GRID / per;
-  q.G = (B + std::min(B, max_rep) - 1) / std::min(B, max_rep);
-  q.nrep = (B + q.G - 1) / q.G;
-  if (q.G > WN_CHAIN_MAX_G) return false;
-  if (aux_lds_floats(R, S, q.G) * sizeof(float) > kMaxLds) return false;
+  int per = 0;
+  for (q.nla = nla_max; q.nla >= 1; --q.nla) {
+    q.naux = (L + q.nla - 1) / q.nla;
+    // as many replicas as the grid holds, the streams spread evenly over them
+    per = q.nch + NHEAD + q.naux;
+    const int max_rep = WN_CHAIN_GRID / per;
+    if (max_rep < 1) continue;
+    q.G = (B + std::min(B, max_rep) - 1) / std::min(B, max_rep);
+    q.nrep = (B + q.G - 1) / q.G;
+    if (q.G <= WN_CHAIN_MAX_G && aux_lds_floats(R, S, q.G, q.nla) * sizeof(float) <= kMaxLds) break;
+  }
+  if (q.nla < 1) return false;
   int gp = 1;
   while (gp < q.G) gp *= 2;
   q.ub = std::max(16, 512 / gp);

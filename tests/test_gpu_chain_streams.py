@@ -37,6 +37,8 @@ CASES = [
     # layers per aux CU, at r = 128 with the first layer's W_skip in LDS)
     ("l20_r128_b11", 20, 128, 256, tuple(synth.dilation_cycle(20)), 11, 300, 0.2),  # 6 x 2 (last 1), 25 CUs each
     ("l20_r64_b12", 20, 64, 256, tuple(synth.dilation_cycle(20)), 12, 300, 0.0),    # 12 x 1, 17 CUs each
+    # more streams per replica than two-layer aux CUs can stage at r = 128: one layer per aux CU
+    ("l20_r128_b80", 20, 128, 256, tuple(synth.dilation_cycle(20)), 80, 60, 0.1),   # 7 x 12 (last 8), 35 CUs each
     ("l3_r128_b5", 3, 128, 256, (1, 3, 2), 5, 200, 0.3),                             # 5 x 1, 9 CUs each
     ("l1_r128_b2", 1, 128, 256, (1,), 2, 150, 0.4),                                  # one chain CU, skip on aux
     ("l5_r128_b3", 5, 128, 256, (2, 1, 4, 1, 3), 3, 200, 0.3),                      # chain CUs of 1, 2, 1, 1 layers
@@ -55,7 +57,7 @@ CASES = [
 
 
 # (workgroups, replicas) wn_launch_info reports for the layouts stated above
-LAUNCH = {"l20_r128_b11": (150, 6), "l20_r64_b12": (204, 12), "l3_r128_b5": (45, 5), "l1_r128_b2": (12, 2),
+LAUNCH = {"l20_r128_b11": (150, 6), "l20_r128_b80": (245, 7), "l20_r64_b12": (204, 12), "l3_r128_b5": (45, 5), "l1_r128_b2": (12, 2),
           "l5_r128_b3": (33, 3), "l9_r32_b40": (200, 20), "l20_r64_b240": (255, 15), "l64_r64_b1": (46, 1), "l9_r64_b1": (11, 1),
           "l7_r64_d1s_b2": (18, 2)}
 
