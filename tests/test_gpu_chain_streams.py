@@ -63,8 +63,11 @@ LAUNCH = {"l20_r128_b11": (150, 6), "l20_r128_b80": (245, 7), "l20_r64_b12": (20
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
-def test_multi_stream_chain_parity(case):
+def test_multi_stream_chain_parity(case, monkeypatch):
     name, L, r, s, dil, B, T, bias = case
+    # the multi-CU kernel by name: by default fp32 batches of more than 13 streams per replica at
+    # r <= 64 go to the per-stream kernel
+    monkeypatch.setenv("WN_KERNEL", "multi_cu_chain")
     print("case %s: L=%d r=%d s=%d B=%d T=%d" % (name, L, r, s, B, T), flush=True)
     w, net, cond, u, model = _setup(L, r, s, dil, B, T, seed=zlib.crc32(name.encode()) % 1000, bias=bias)
     assert net.kernel_variant(B) == "multi_cu_chain"

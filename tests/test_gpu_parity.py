@@ -5,6 +5,7 @@ compared with the oracle's bf16 mode at 1e-3 and with the fp32 oracle at 2e-2);
 sample indices bit-exact at every step whose oracle CDF margin exceeds 1e-4,
 judged on the GPU's own sample sequence (the oracle replays it teacher-forced).
 """
+import os
 import zlib
 from concurrent.futures import ThreadPoolExecutor
 
@@ -291,11 +292,18 @@ def test_multi_cu_kernel_is_used_for_one_stream():
     wn = _wn()
     w = synth.make_weights(20, 64, 256, seed=1)
     net = wn.WaveNet(w, synth.dilation_cycle(20))
-    # up to 15 replicas of 17 CUs (two layers per aux CU), at most 16 streams each; beyond that the
-    # per-stream kernel
-    assert [net.kernel_variant(b) for b in (1, 2, 240)] == ["multi_cu_chain"] * 3
-    assert net.kernel_variant(241) == "stream_l2"
+    # up to 15 replicas of 17 CUs (two layers per aux CU); by default at most 13 streams each (the
+    # per-stream kernel is faster beyond), up to 16 when forced
+    assert [net.kernel_variant(b) for b in (1, 2, 195)] == ["multi_cu_chain"] * 3
+    assert [net.kernel_variant(b) for b in (196, 240, 241)] == ["stream_l2"] * 3
     net.close()
+    os.environ["WN_KERNEL"] = "multi_cu_chain"
+    try:
+        forced = wn.WaveNet(w, synth.dilation_cycle(20))
+        assert forced.kernel_variant(240) == "multi_cu_chain" and forced.kernel_variant(241) == "stream_l2"
+        forced.close()
+    finally:
+        del os.environ["WN_KERNEL"]
 
 
 @pytest.mark.parametrize("L,S", [(20, 256), (9, 128), (40, 256), (3, 256), (7, 128)])
