@@ -134,17 +134,17 @@ int variant_for(const wn_handle* h, int B) {
   if (f == "multi_cu_chain") return chain_plan_for(h, B, &p) ? WN_VARIANT_CHAIN : WN_VARIANT_STREAM;
   if (f == "mfma_group") return h->group_ok ? WN_VARIANT_GROUP : WN_VARIANT_STREAM;
   // fp32 models: the fp32 multi-CU kernel while its replicas carry the batch.  bf16 and int8 models run
-  // it on their exact fp32 copy while a replica carries at most 3 streams, and the MFMA one beyond
-  // (measured at l = 20, r = 64: 15.4 / 16.3 / 18.6 us/step at 1 / 2 / 3 streams per replica and 30.8
-  // at 5, against a flat 20.8 (bf16) or 22.7 (int8) on the MFMA kernel and 24.9 on the batched one),
-  // then the batched kernel (bf16); the fp32 one again for the shapes that neither MFMA kernel serves.
+  // it on their exact fp32 copy while a replica carries at most 2 streams, and the MFMA one beyond
+  // (measured at l = 20, r = 64, bf16: 11.7 / 14.7 / 18.6 / 24.8 us/step at 1 / 2 / 3 / 4 streams per
+  // replica, against a flat 18.1 on the MFMA kernel; int8 the same within 0.2 us), then the batched
+  // kernel (bf16); the fp32 one again for the shapes that neither MFMA kernel serves.
   // fp32 at r <= 64 goes to the per-stream kernel from 14 streams per replica on (measured at l = 20,
   // r = 64: 74.3 against 80.0 us/step at 12 streams per replica, 86.5 against ~83.6 at 14, 99.0
   // against 87.2 at 16); at r = 128 the per-stream kernel reads its weights from the MALL and
   // stays far behind (197 against 28 us/step at B = 32).
   const bool chain = chain_plan_for(h, B, &p);
   if (h->dtype == WN_F32) return chain && (h->R > 64 || p.G <= 13) ? WN_VARIANT_CHAIN : WN_VARIANT_STREAM;
-  if (chain && p.G <= 3) return WN_VARIANT_CHAIN;
+  if (chain && p.G <= 2) return WN_VARIANT_CHAIN;
   WnChainPlan q;
   if (mchain_plan_for(h, B, &q)) return WN_VARIANT_MCHAIN;
   if (h->group_ok) return WN_VARIANT_GROUP;

@@ -154,10 +154,10 @@ def test_group_kernel_variant_selection(monkeypatch):
     w = synth.make_weights(20, 64, 256, seed=2)
     monkeypatch.delenv("WN_KERNEL")
     dflt = wn.WaveNet(w, synth.dilation_cycle(20), weight_dtype="bf16")
-    # the default: the fp32 multi-CU kernel (exact fp32 copy) up to 3 streams per replica, the MFMA
+    # the default: the fp32 multi-CU kernel (exact fp32 copy) up to 2 streams per replica, the MFMA
     # multi-CU kernel while its replicas carry the batch, then this one
-    assert [dflt.kernel_variant(b) for b in (1, 16, 45)] == ["multi_cu_chain"] * 3
-    assert [dflt.kernel_variant(b) for b in (46, 256, 512)] == ["multi_cu_mfma"] * 3
+    assert [dflt.kernel_variant(b) for b in (1, 16, 30)] == ["multi_cu_chain"] * 3
+    assert [dflt.kernel_variant(b) for b in (31, 45, 256, 512)] == ["multi_cu_mfma"] * 4
     assert [dflt.kernel_variant(b) for b in (513, 2048)] == ["mfma_group"] * 2
     dflt.close()
     monkeypatch.setenv("WN_KERNEL", "mfma_group")

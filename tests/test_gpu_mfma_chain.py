@@ -190,7 +190,7 @@ def test_mfma_chain_timeout_then_reset(monkeypatch):
 @pytest.mark.parametrize("dtype", ["bf16", "i8"])
 def test_default_choice(dtype, monkeypatch):
     """bf16 and int8 models: the fp32 multi-CU kernel (on the exact fp32 copy) while its replicas
-    carry at most 3 streams each (l = 20: B <= 45), this kernel beyond that while its replicas carry
+    carry at most 2 streams each (l = 20: B <= 30), this kernel beyond that while its replicas carry
     the batch (B <= 512), then the batched kernel (bf16) or the per-stream one (int8)."""
     import paper_1702_07825_amd as wn
     monkeypatch.delenv("WN_KERNEL", raising=False)
@@ -198,8 +198,8 @@ def test_default_choice(dtype, monkeypatch):
     L = 20
     w = synth.make_weights(L, 64, 256, seed=4)
     net = wn.WaveNet(w, synth.dilation_cycle(L), weight_dtype=dtype)
-    assert [net.kernel_variant(b) for b in (1, 16, 45)] == ["multi_cu_chain"] * 3
-    assert [net.kernel_variant(b) for b in (46, 256, 512)] == [KERNEL] * 3
+    assert [net.kernel_variant(b) for b in (1, 16, 30)] == ["multi_cu_chain"] * 3
+    assert [net.kernel_variant(b) for b in (31, 45, 256, 512)] == [KERNEL] * 4
     assert net.kernel_variant(513) == ("mfma_group" if dtype == "bf16" else "stream_l2")
     net.close()
 
